@@ -1,0 +1,239 @@
+"""ctypes front end of the CPU oracle (ra_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's CPU
+baseline leg call this module; the product library never imports it.  It
+compiles ``ra_oracle.c`` with gcc into ``libra_oracle.so`` beside it.
+
+Every function returns plain numpy arrays / Python ints.  Field elements are
+canonical integers in [0, p), p = 2^61 - 1.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+P61 = (1 << 61) - 1
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ra_oracle.c")
+_LIB = os.path.join(_HERE, "libra_oracle.so")
+_lib = None
+
+ERRORS = {-1: "invalid argument", -3: "field too small", -4: "range",
+          -5: "challenge stream", -10: "out of memory"}
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code):
+        super().__init__(f"oracle error {code}: {ERRORS.get(code, '?')}")
+        self.code = code
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain C11, -O2, no OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC",
+                        _SRC, "-o", tmp], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class LayerInfo(ctypes.Structure):
+    _fields_ = [("t", ctypes.c_int32), ("P", ctypes.c_int32), ("log_p", ctypes.c_int32),
+                ("n_mm_rounds", ctypes.c_int32), ("n_rs_rounds", ctypes.c_int32),
+                ("n_zc_rounds", ctypes.c_int32), ("challenges_used", ctypes.c_int64),
+                ("c0", ctypes.c_uint64), ("a_star", ctypes.c_uint64), ("b_star", ctypes.c_uint64),
+                ("r_claim", ctypes.c_uint64), ("rm_claim", ctypes.c_uint64),
+                ("y_claim", ctypes.c_uint64), ("z_claim", ctypes.c_uint64),
+                ("range_sum", ctypes.c_uint64), ("bits_claim", ctypes.c_uint64),
+                ("r_at", ctypes.c_uint64), ("y_at", ctypes.c_uint64)]
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB)
+        u64p = ctypes.POINTER(ctypes.c_uint64)
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        u8p = ctypes.POINTER(ctypes.c_uint8)
+        L.orc_fmul.restype = L.orc_fadd.restype = L.orc_fsub.restype = ctypes.c_uint64
+        L.orc_fmul.argtypes = L.orc_fadd.argtypes = L.orc_fsub.argtypes = [ctypes.c_uint64] * 2
+        L.orc_fint.restype = ctypes.c_uint64
+        L.orc_fint.argtypes = [ctypes.c_int64]
+        L.orc_chi_at.restype = ctypes.c_uint64
+        L.orc_chi_at.argtypes = [u64p, ctypes.c_int, ctypes.c_uint64]
+        L.orc_chi_vector.argtypes = [u64p, ctypes.c_int, u64p]
+        L.orc_mle_int.argtypes = [i64p, ctypes.c_int, u64p, u64p]
+        L.orc_mle_field.argtypes = [u64p, ctypes.c_int, u64p, u64p]
+        L.orc_interp.restype = ctypes.c_uint64
+        L.orc_interp.argtypes = [u64p, ctypes.c_int, ctypes.c_uint64]
+        L.orc_plane_count.argtypes = [ctypes.c_int] * 3
+        L.orc_prove_layer.argtypes = [ctypes.c_int64] * 3 + [i64p, i64p] + [ctypes.c_int] * 4 + \
+            [u64p, ctypes.c_int64, i64p] + [i64p] * 5 + [u8p, u64p, u64p, u64p,
+                                                        ctypes.POINTER(LayerInfo)]
+        L.orc_verify_layer.argtypes = [ctypes.c_int64] * 3 + [i64p] * 3 + [ctypes.c_int] * 3 + \
+            [i64p] * 4 + [u64p] * 3 + [ctypes.POINTER(LayerInfo), u64p, ctypes.c_int64, i64p]
+        _lib = L
+    return _lib
+
+
+def _u64(a):
+    return np.ascontiguousarray(a, dtype=np.uint64)
+
+
+def _i64(a):
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _ptr(a, ct):
+    return a.ctypes.data_as(ctypes.POINTER(ct))
+
+
+# --- small helpers exported for pins -------------------------------------
+def fmul(a, b): return int(lib().orc_fmul(a, b))
+def fadd(a, b): return int(lib().orc_fadd(a, b))
+def fsub(a, b): return int(lib().orc_fsub(a, b))
+def fint(z): return int(lib().orc_fint(int(z)))
+
+
+def chi_at(z, y):
+    z = _u64(z)
+    return int(lib().orc_chi_at(_ptr(z, ctypes.c_uint64), len(z), y))
+
+
+def chi_vector(z):
+    z = _u64(z)
+    out = np.zeros(1 << len(z), dtype=np.uint64)
+    lib().orc_chi_vector(_ptr(z, ctypes.c_uint64), len(z), _ptr(out, ctypes.c_uint64))
+    return out
+
+
+def mle_int(table, z):
+    t = _i64(np.asarray(table).reshape(-1))
+    z = _u64(z)
+    assert t.size == 1 << len(z)
+    out = np.zeros(1, dtype=np.uint64)
+    lib().orc_mle_int(_ptr(t, ctypes.c_int64), len(z), _ptr(z, ctypes.c_uint64), _ptr(out, ctypes.c_uint64))
+    return int(out[0])
+
+
+def mle_field(table, z):
+    t = _u64(np.asarray(table).reshape(-1))
+    z = _u64(z)
+    assert t.size == 1 << len(z)
+    out = np.zeros(1, dtype=np.uint64)
+    lib().orc_mle_field(_ptr(t, ctypes.c_uint64), len(z), _ptr(z, ctypes.c_uint64), _ptr(out, ctypes.c_uint64))
+    return int(out[0])
+
+
+def interp(evals, x):
+    e = _u64(evals)
+    return int(lib().orc_interp(_ptr(e, ctypes.c_uint64), len(e) - 1, x))
+
+
+def plane_count(s, t, relu):
+    return int(lib().orc_plane_count(s, t, int(bool(relu))))
+
+
+# --- layer protocol -------------------------------------------------------
+def prove_layer(A, B, s, relu, mode, chal, cursor=0, t_in=-1):
+    """Prove one layer; returns a dict with the witness tables, the bit table
+    (uint8, planes x N), the transcript and the new challenge cursor."""
+    A = _i64(A)
+    B = _i64(B)
+    n, m = A.shape
+    m2, k = B.shape
+    assert m == m2
+    N = n * k
+    chal = _u64(chal)
+    cur = np.array([cursor], dtype=np.int64)
+    C, R, Rm, Y, Z = (np.zeros(N, dtype=np.int64) for _ in range(5))
+    bits = np.zeros(128 * N, dtype=np.uint8)
+    lm = m.bit_length() - 1
+    lN = N.bit_length() - 1
+    mm = np.zeros(3 * max(lm, 1), dtype=np.uint64)
+    rs = np.zeros(4 * (lN + 7), dtype=np.uint64)
+    zc = np.zeros(4 * max(lN, 1), dtype=np.uint64)
+    info = LayerInfo()
+    i64 = ctypes.c_int64
+    rc = lib().orc_prove_layer(n, m, k, _ptr(A, i64), _ptr(B, i64), s, int(bool(relu)), mode, t_in,
+                               _ptr(chal, ctypes.c_uint64), len(chal), _ptr(cur, i64),
+                               _ptr(C, i64), _ptr(R, i64), _ptr(Rm, i64), _ptr(Y, i64), _ptr(Z, i64),
+                               _ptr(bits, ctypes.c_uint8), _ptr(mm, ctypes.c_uint64),
+                               _ptr(rs, ctypes.c_uint64), _ptr(zc, ctypes.c_uint64), ctypes.byref(info))
+    if rc != 0:
+        raise OracleError(rc)
+    P = info.P
+    out = dict(n=n, m=m, k=k, s=s, relu=int(bool(relu)), mode=mode,
+               C=C.reshape(n, k), R=R.reshape(n, k), Rm=Rm.reshape(n, k), Y=Y.reshape(n, k),
+               Z=Z.reshape(n, k), bits=bits[:P * N].reshape(P, N).copy(),
+               t=info.t, P=P, cursor=int(cur[0]), challenges_used=int(info.challenges_used),
+               c0=int(info.c0), mm_evals=[int(v) for v in mm[:3 * info.n_mm_rounds]],
+               a_star=int(info.a_star), b_star=int(info.b_star),
+               r_claim=int(info.r_claim), rm_claim=int(info.rm_claim),
+               y_claim=int(info.y_claim), z_claim=int(info.z_claim),
+               range_sum=int(info.range_sum),
+               rs_evals=[int(v) for v in rs[:4 * info.n_rs_rounds]], bits_claim=int(info.bits_claim),
+               zc_evals=[int(v) for v in zc[:4 * info.n_zc_rounds]],
+               r_at=int(info.r_at), y_at=int(info.y_at))
+    return out
+
+
+def verify_layer(A, B, Z, s, relu, mode, R, Rm, Y, bits, tr, chal, cursor=0):
+    """Run the oracle's verifier; returns (verdict, new_cursor).  verdict 0 =
+    accept, else the number of the first failing check (see ra_oracle.c)."""
+    A = _i64(A)
+    B = _i64(B)
+    n, m = A.shape
+    k = B.shape[1]
+    N = n * k
+    lm = m.bit_length() - 1
+    lN = N.bit_length() - 1
+    info = LayerInfo()
+    info.t = tr["t"]
+    info.P = tr["P"]
+    for key in ("c0", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_claim",
+                "bits_claim", "r_at", "y_at"):
+        setattr(info, key, int(tr[key]) & 0xFFFFFFFFFFFFFFFF)
+    mm = _u64(np.array(list(tr["mm_evals"]) + [0] * 3, dtype=object).astype(np.uint64))
+    rs = _u64(np.array(list(tr["rs_evals"]) + [0] * 4, dtype=object).astype(np.uint64))
+    zc = _u64(np.array(list(tr["zc_evals"]) + [0] * 4, dtype=object).astype(np.uint64))
+    want_rs = 4 * (int(tr["P"]).bit_length() - 1 + lN)
+    if len(tr["mm_evals"]) != 3 * lm or len(tr["rs_evals"]) != want_rs or \
+            len(tr["zc_evals"]) != (4 * lN if relu else 0):
+        return 13, cursor
+    bits = _i64(np.asarray(bits).reshape(-1))
+    if bits.size != int(tr["P"]) * N:
+        return 12, cursor
+    chal = _u64(chal)
+    cur = np.array([cursor], dtype=np.int64)
+    i64 = ctypes.c_int64
+    arrs = [_i64(np.asarray(x).reshape(-1)) for x in (Z, R, Rm, Y)]
+    v = lib().orc_verify_layer(n, m, k, _ptr(A, i64), _ptr(B, i64), _ptr(arrs[0], i64), s,
+                               int(bool(relu)), mode, _ptr(arrs[1], i64), _ptr(arrs[2], i64),
+                               _ptr(arrs[3], i64), _ptr(bits, i64), _ptr(mm, ctypes.c_uint64),
+                               _ptr(rs, ctypes.c_uint64), _ptr(zc, ctypes.c_uint64), ctypes.byref(info),
+                               _ptr(chal, ctypes.c_uint64), len(chal), _ptr(cur, i64))
+    return int(v), int(cur[0])
+
+
+def prove_network(workload, layers_out=None):
+    """Prove every layer of a workload (see paper_2505_17623_amd.inputs) in
+    order; a layer's A is the workload's input or the previous output passed
+    through the workload's link.  Returns the list of per-layer results."""
+    results = []
+    cursor = 0
+    Z = None
+    for li, layer in enumerate(workload.layers):
+        A = workload.layer_input(li, Z)
+        res = prove_layer(A, layer.B, layer.s, layer.relu, workload.mode, workload.challenges, cursor)
+        cursor = res["cursor"]
+        res["A"] = A
+        Z = res["Z"]
+        results.append(res)
+    return results

@@ -1,0 +1,223 @@
+/*
+ * ra.h -- C ABI of the MI355X (gfx950) Range-Arithmetic prover.
+ *
+ * One layer of a fixed-point network is C = A B followed by the rounding
+ * operator of Sec. II-A and an optional ReLU (Sec. III-B).  The prover
+ * convinces a verifier of it with
+ *   - a sum-check over the inner index of gamma(l) = a~(r1, l) b~(l, r2)
+ *     (Sec. III-A-1, Eq. (4); Alg. 1 step 6),
+ *   - one concatenated range sum-check over a bit table holding the shifted
+ *     remainder (s bits), R + 2^(t+1) (t + 2 bits) and, with ReLU, Y = |R|
+ *     (t + 2 bits) (Sec. III-A-2; Alg. 1 steps 11-12; Sec. III-B),
+ *   - the ReLU square-equality zero-check of Eq. (6).
+ * All arithmetic is in F_p with p = 2^61 - 1; field elements cross the ABI
+ * as uint64_t in [0, p).
+ *
+ * Calling convention
+ *   - Per layer: ra_sumcheck_matmul_prove, then ra_rescale_relu_witness,
+ *     then ra_range_prove; layers in order.  Out of order -> RA_E_STATE.
+ *   - Pointers named d_* are device pointers (caller-owned, on the device
+ *     that was current when the context was created); h_* and the arrays
+ *     inside the proof structs are host pointers (caller-owned).
+ *   - All device work is enqueued on the context's HIP stream; every call
+ *     synchronises that stream before it returns, so outputs are ready.
+ *   - A context is not thread-safe.  Contexts on one device may run
+ *     concurrently on different streams.
+ *   - Dimensions n, m, k are powers of two >= 1 (Sec. III-A-1 assumes
+ *     powers of two; callers zero-pad, which leaves the proof sound and
+ *     complete because zero rows/columns give C = 0).
+ *   - Matrices are row-major.  A table of 2^v entries is a function on
+ *     {0,1}^v whose first variable is the most significant index bit; a
+ *     matrix entry (i, j) sits at index i * cols + j, so row bits come
+ *     before column bits (worked example of Sec. III-A-1).
+ *   - Every function returns RA_OK (0) or a negative ra_status; none throws
+ *     or aborts.  After an error the context is left in its previous state
+ *     unless the error is RA_E_HIP.
+ */
+#ifndef RA_H
+#define RA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ra_status;
+#define RA_OK 0
+#define RA_E_INVAL (-1)             /* bad argument: null pointer, dimension not a power of two, ... */
+#define RA_E_UNSUPPORTED_PRIME (-2) /* p != 2^61 - 1 */
+#define RA_E_FIELD_TOO_SMALL (-3)   /* s + t + 3 > 61 bits of p (Theorem A.1, condition 1) */
+#define RA_E_RANGE (-4)             /* R outside [-2^(t+1), 2^(t+1)) for a given t, or too many bit planes */
+#define RA_E_CHALLENGES (-5)        /* challenge stream exhausted, or a challenge >= p */
+#define RA_E_HIP (-6)               /* a HIP runtime call failed */
+#define RA_E_STATE (-7)             /* call out of the per-layer order */
+#define RA_E_BUFSIZE (-8)           /* a caller buffer is too small */
+#define RA_E_NOMEM (-9)             /* device or host allocation failed */
+
+typedef enum { RA_I16 = 1, RA_I32 = 2, RA_I64 = 3, RA_FIELD = 4 } ra_dtype;
+
+/* Rounding operator.  RA_ROUND_NEAREST is R(x) = (x + 2^(s-1) - ((x + 2^(s-1))
+ * mod 2^s)) / 2^s of Sec. II-A with the floor modulo; the shifted remainder
+ * Rm = (x + 2^(s-1)) mod 2^s = E + 2^(s-1) lies in [0, 2^s).  RA_ROUND_FLOOR
+ * is R(x) = floor(x / 2^s), Rm = x mod 2^s. */
+typedef enum { RA_ROUND_NEAREST = 0, RA_ROUND_FLOOR = 1 } ra_round;
+
+typedef struct ra_ctx ra_ctx;
+
+/* Create a prover context.
+ *   p             must be 2^61 - 1, else RA_E_UNSUPPORTED_PRIME.
+ *   h_challenges  the verifier's random challenges (Alg. 1 step 4 and every
+ *                 sum-check round of Sec. II-D), n_challenges field elements
+ *                 in [0, p); copied to the device once.  They are consumed in
+ *                 this order per layer: r1 (log n), r2 (log k), rho (log m),
+ *                 lambda1, lambda2, lambda3, mu, tau_p (log P),
+ *                 sigma (log P + log N), and with ReLU rho' (log N),
+ *                 where N = n k and P is the layer's bit-plane count.
+ *   hip_stream    hipStream_t to enqueue on (NULL = the null stream).
+ *   out           receives the context. */
+ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, void *hip_stream,
+                        ra_ctx **out);
+ra_status ra_ctx_destroy(ra_ctx *ctx);
+/* Number of challenges consumed so far. */
+ra_status ra_ctx_cursor(const ra_ctx *ctx, uint64_t *consumed);
+const char *ra_status_str(ra_status st);
+
+/* Multilinear-extension binding of one side of a matrix (the chi-vector inner
+ * product of Sec. II-C applied to every row or column):
+ *   bind_rows = 1:  d_out[c] = sum_r eq(point, r) T[r, c],  point_len = log2(rows),
+ *                   d_out has cols entries;
+ *   bind_rows = 0:  d_out[r] = sum_c T[r, c] eq(point, c),  point_len = log2(cols),
+ *                   d_out has rows entries;
+ * with eq(z, y) = prod_i (z_i y_i + (1 - z_i)(1 - y_i)) (Eq. (1)).
+ *   d_T     rows x cols, row-major, of dtype RA_I16 / RA_I32 / RA_I64
+ *           (signed integers embedded in F_p) or RA_FIELD (uint64 in [0, p)).
+ *   h_point point_len field elements in [0, p) (host).
+ *   d_out   device, uint64 field elements.
+ * Consumes no challenges.  RA_E_INVAL on a bad dimension, dtype or point. */
+ra_status ra_mle_bind(ra_ctx *ctx, const void *d_T, ra_dtype dtype, uint32_t rows, uint32_t cols, int bind_rows,
+                      const uint64_t *h_point, uint32_t point_len, uint64_t *d_out);
+
+/* Transcript of the matrix-multiplication sum-check. */
+typedef struct {
+    uint32_t log_m;  /* out: number of rounds */
+    uint64_t c0;     /* out: claimed sum  sum_l a~(r1, l) b~(l, r2) = C~(r1, r2) */
+    uint64_t *evals; /* in: host buffer of 3 * log m words; out: g_j(0), g_j(1), g_j(2) per round */
+    uint64_t a_star; /* out: a~(r1, rho) */
+    uint64_t b_star; /* out: b~(rho, r2) */
+} ra_matmul_proof;
+
+/* Alg. 1 steps 2 and 4-6 for one layer: computes the witness C = A B exactly
+ * (int64), draws r1, r2, binds A's rows at r1 and B's columns at r2 (Eq. (4))
+ * and runs the degree-2 sum-check over l in {0,1}^(log m), drawing rho.
+ *   d_A     n x m, RA_I16 or RA_I32 (layer input; later layers use the
+ *           previous int32 output).  With RA_I32, m * 2^46 must not exceed
+ *           2^62 (exactness of the int64 product), i.e. m <= 65536.
+ *   d_B     m x k int16 weights.
+ *   d_C     out, n x k int64, the exact product.
+ *   out     transcript; out->evals must hold 3 * log2(m) words.
+ * The context keeps r1, r2 for the next two calls of this layer. */
+ra_status ra_sumcheck_matmul_prove(ra_ctx *ctx, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
+                                   uint32_t m, uint32_t k, int64_t *d_C, ra_matmul_proof *out);
+
+/* Parameters and claims of the rescale / ReLU witness. */
+typedef struct {
+    uint32_t s;          /* in: fractional bits removed, 1..16 */
+    uint32_t relu;       /* in: 1 = ReLU after the rescale */
+    uint32_t round_mode; /* in: ra_round */
+    int32_t t;           /* in: -1 = least t with R in [-2^(t+1), 2^(t+1)); >= 0 = given.  out: t used */
+    uint32_t P;          /* out: bit planes, next power of two >= s + (t+2) (1 + relu), at most 64 */
+    uint64_t r_claim;    /* out: R~(r1, r2) */
+    uint64_t rm_claim;   /* out: Rm~(r1, r2) */
+    uint64_t y_claim;    /* out: Y~(r1, r2) */
+    uint64_t z_claim;    /* out: Z~(r1, r2) */
+} ra_witness_info;
+
+/* Alg. 1 step 9 and the witness side of Sec. III-B: from C computes
+ *   R  = rounded output (int32),  Rm = shifted remainder in [0, 2^s) (uint16),
+ *   Y  = |R| (int32),  Z = ReLU(R) = (R + Y) / 2 with ReLU, else Z = R (int32,
+ *        the layer's inference output),
+ *   bits: one uint64 word per output x (index i * k + j); bit q of word x is
+ *        plane q of x:  q in [0, s): bit q of Rm;  q in [s, s + t + 2):
+ *        bit q - s of R + 2^(t+1);  with ReLU q in [s + t + 2, s + 2t + 4):
+ *        bit q - s - t - 2 of Y;  higher planes are zero,
+ * picks t (or checks the given one), and returns the claims at (r1, r2).
+ *   bits_words  capacity of d_bits in words, at least n * k.
+ * Errors: RA_E_RANGE if a given t does not hold R, if t > 29 (R must fit
+ * int32) or if more than 64 planes would be needed; RA_E_FIELD_TOO_SMALL if
+ * s + t + 3 > 61. */
+ra_status ra_rescale_relu_witness(ra_ctx *ctx, const int64_t *d_C, uint32_t n, uint32_t k, int32_t *d_R,
+                                  uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits,
+                                  uint64_t bits_words, ra_witness_info *io);
+
+/* Transcript of the range sum-check and the ReLU zero-check. */
+typedef struct {
+    uint32_t rounds;       /* out: log P + log N */
+    uint64_t *evals;       /* in: host buffer of 4 * (log P + log N) words; out: g_j(0..3) */
+    uint64_t range_sum;    /* out: claimed sum mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~) at (r1, r2) */
+    uint64_t bits_claim;   /* out: b~(sigma), the bit table's extension at the final point */
+    uint32_t relu_rounds;  /* out: log N with ReLU, else 0 */
+    uint64_t *relu_evals;  /* in: host buffer of 4 * log N words (unused without ReLU); out */
+    uint64_t r_at;         /* out: R~(rho') */
+    uint64_t y_at;         /* out: Y~(rho') */
+} ra_range_proof;
+
+/* Alg. 1 steps 11-12 and Sec. III-B in sum-check form.  Over the table
+ * b(q, x) (index q N + x, plane bits first) proves
+ *   sum_{q,x} eq(tau, (q, x)) b (b - 1) + mu W(q) eq((r1, r2), x) b
+ *     = mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~)(r1, r2)
+ * with tau = (tau_p, r1, r2) and W(q) = lambda_group(q) 2^(bit of q), i.e.
+ * booleanity of every bit and recomposition of every range-checked value;
+ * then with ReLU the zero-check sum_x eq((r1, r2), x) (R(x)^2 - Y(x)^2) = 0
+ * of Eq. (6).  Inputs are the buffers the witness call filled and its info. */
+ra_status ra_range_prove(ra_ctx *ctx, const uint64_t *d_bits, const int32_t *d_R, const int32_t *d_Y, uint32_t n,
+                         uint32_t k, const ra_witness_info *info, ra_range_proof *out);
+
+/* Public data of one layer for the verifier (host pointers). */
+typedef struct {
+    uint32_t n, m, k;
+    uint32_t s, relu, round_mode;
+    ra_dtype a_dtype;  /* RA_I16 or RA_I32 */
+    const void *A;     /* n x m */
+    const int16_t *B;  /* m x k */
+    const int32_t *Z;  /* n x k, the claimed layer output */
+    uint32_t chained;  /* 1: A must equal the previous layer's Z (int32) */
+} ra_layer_public;
+
+/* Opened tables standing in for the paper's commitments (host pointers). */
+typedef struct {
+    const int32_t *R;
+    const uint16_t *Rm;
+    const int32_t *Y;
+    const uint64_t *bits; /* n * k words, layout of ra_rescale_relu_witness */
+} ra_layer_tables;
+
+typedef struct {
+    ra_matmul_proof mm;
+    ra_witness_info wit;
+    ra_range_proof rng;
+} ra_layer_transcript;
+
+/* Host-only verifier (Sec. IV).  Replays the challenge stream, checks every
+ * sum-check chain (g_j(0) + g_j(1) against the previous round's value at its
+ * challenge, by Lagrange interpolation), every final identity, the rounding
+ * link C~ = 2^s R~ + Rm~ - 2^(s-1) (floor mode: no offset), the output link
+ * 2 Z~ = R~ + Y~ (or Z~ = R~), the field guard s + t + 3 <= 61, and opens the
+ * tables by evaluating their multilinear extensions.
+ *   *verdict      0 accept, else the first failing check:
+ *                 1 matmul chain, 2 matmul final, 3 a-star / b-star opening, 4 rounding
+ *                 link, 5 range chain, 6 range final identity, 7 bit-table
+ *                 opening, 8 R/Rm/Y openings, 9 ReLU chain or final identity,
+ *                 10 ReLU openings, 11 output link or Z opening, 12 parameters,
+ *                 13 malformed layer, 14 chaining.
+ *   *failed_layer index of the failing layer (0 when accepted). */
+ra_status ra_verify(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, uint32_t n_layers,
+                    const ra_layer_public *pub, const ra_layer_tables *tables, const ra_layer_transcript *tr,
+                    int32_t *verdict, uint32_t *failed_layer);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RA_H */

@@ -1,0 +1,419 @@
+// abi.hip -- host driver behind the C ABI of include/ra.h: context, device
+// workspace, per-layer protocol state, and the orchestration of the kernels
+// of witness.hip and sumcheck.hip for each entry point.
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "common.hpp"
+#include "ra.h"
+
+using namespace ra;
+
+namespace {
+constexpr uint64_t kP = 0x1FFFFFFFFFFFFFFFull;
+
+bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
+int log2u(uint64_t x)
+{
+    int l = 0;
+    while ((1ull << l) < x) l++;
+    return l;
+}
+}  // namespace
+
+struct ra_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    uint64_t *d_chal = nullptr;
+    uint64_t n_chal = 0;
+    uint64_t cursor = 0;
+    // per-layer state between the three prover calls
+    int phase = 0;  // 0: expects matmul, 1: expects witness, 2: expects range
+    uint32_t n = 0, m = 0, k = 0;
+    uint64_t *d_eq = nullptr;  // E1 (n words) then E2 (k words)
+    size_t eq_cap = 0;
+    WitParams *d_params = nullptr;
+    uint64_t *d_claims = nullptr;  // R~, Rm~, Y~, Z~ at (r1, r2)
+    int s = 0, relu = 0, mode = 0, t = 0, P = 0;
+    // scratch
+    char *ws = nullptr;
+    size_t ws_cap = 0;
+    uint64_t *h_stage = nullptr;  // pinned host staging
+    size_t stage_cap = 0;
+};
+
+#define RA_HIP(call)                                      \
+    do {                                                  \
+        if ((call) != hipSuccess) return RA_E_HIP;        \
+    } while (0)
+
+namespace {
+
+// Bump allocator over the context workspace (256-byte aligned pieces).
+struct Carve {
+    size_t off = 0;
+    template <typename T> size_t take(size_t count)
+    {
+        const size_t o = off;
+        off += (count * sizeof(T) + 255) & ~(size_t)255;
+        return o;
+    }
+};
+
+ra_status ensure_ws(ra_ctx *c, size_t bytes)
+{
+    if (bytes <= c->ws_cap) return RA_OK;
+    RA_HIP(hipStreamSynchronize(c->stream));
+    if (c->ws) RA_HIP(hipFree(c->ws));
+    c->ws = nullptr;
+    c->ws_cap = 0;
+    const size_t want = std::max(bytes + bytes / 4, (size_t)1 << 20);
+    if (hipMalloc((void **)&c->ws, want) != hipSuccess) return RA_E_NOMEM;
+    c->ws_cap = want;
+    return RA_OK;
+}
+
+ra_status ensure_stage(ra_ctx *c, size_t words)
+{
+    if (words <= c->stage_cap) return RA_OK;
+    RA_HIP(hipStreamSynchronize(c->stream));
+    if (c->h_stage) RA_HIP(hipHostFree(c->h_stage));
+    c->h_stage = nullptr;
+    c->stage_cap = 0;
+    const size_t want = std::max(words, (size_t)4096);
+    if (hipHostMalloc((void **)&c->h_stage, want * 8, hipHostMallocDefault) != hipSuccess) return RA_E_NOMEM;
+    c->stage_cap = want;
+    return RA_OK;
+}
+
+ra_status ensure_eq(ra_ctx *c, size_t words)
+{
+    if (words <= c->eq_cap) return RA_OK;
+    RA_HIP(hipStreamSynchronize(c->stream));
+    if (c->d_eq) RA_HIP(hipFree(c->d_eq));
+    c->d_eq = nullptr;
+    c->eq_cap = 0;
+    if (hipMalloc((void **)&c->d_eq, words * 8) != hipSuccess) return RA_E_NOMEM;
+    c->eq_cap = words;
+    return RA_OK;
+}
+
+ra_status finish(ra_ctx *c, const uint64_t *d_src, size_t words)
+{
+    RA_HIP(hipGetLastError());
+    RA_HIP(hipMemcpyAsync(c->h_stage, d_src, words * 8, hipMemcpyDeviceToHost, c->stream));
+    RA_HIP(hipStreamSynchronize(c->stream));
+    return RA_OK;
+}
+
+constexpr int kPartStride = kMaxBlocks * 6;  // words per partial-sum slot
+
+}  // namespace
+
+extern "C" {
+
+const char *ra_status_str(ra_status st)
+{
+    switch (st) {
+    case RA_OK: return "ok";
+    case RA_E_INVAL: return "invalid argument";
+    case RA_E_UNSUPPORTED_PRIME: return "unsupported prime (only 2^61 - 1)";
+    case RA_E_FIELD_TOO_SMALL: return "field too small: s + t + 3 > 61";
+    case RA_E_RANGE: return "value range: given t does not hold R, or too many bit planes";
+    case RA_E_CHALLENGES: return "challenge stream exhausted or not canonical";
+    case RA_E_HIP: return "HIP runtime error";
+    case RA_E_STATE: return "call out of the per-layer order";
+    case RA_E_BUFSIZE: return "buffer too small";
+    case RA_E_NOMEM: return "allocation failed";
+    default: return "unknown status";
+    }
+}
+
+ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, void *hip_stream,
+                        ra_ctx **out)
+{
+    if (!out) return RA_E_INVAL;
+    *out = nullptr;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    if (n_challenges && !h_challenges) return RA_E_INVAL;
+    for (uint64_t i = 0; i < n_challenges; i++)
+        if (h_challenges[i] >= kP) return RA_E_CHALLENGES;
+    ra_ctx *c = new (std::nothrow) ra_ctx();
+    if (!c) return RA_E_NOMEM;
+    c->stream = (hipStream_t)hip_stream;
+    ra_status st = RA_OK;
+    if (hipGetDevice(&c->device) != hipSuccess) st = RA_E_HIP;
+    if (st == RA_OK && hipMalloc((void **)&c->d_chal, std::max<uint64_t>(n_challenges, 1) * 8) != hipSuccess)
+        st = RA_E_NOMEM;
+    if (st == RA_OK && n_challenges &&
+        hipMemcpy(c->d_chal, h_challenges, n_challenges * 8, hipMemcpyHostToDevice) != hipSuccess)
+        st = RA_E_HIP;
+    if (st == RA_OK && hipMalloc((void **)&c->d_params, sizeof(WitParams)) != hipSuccess) st = RA_E_NOMEM;
+    if (st == RA_OK && hipMalloc((void **)&c->d_claims, 8 * 8) != hipSuccess) st = RA_E_NOMEM;
+    if (st == RA_OK) st = ensure_stage(c, 4096);
+    if (st != RA_OK) {
+        ra_ctx_destroy(c);
+        return st;
+    }
+    c->n_chal = n_challenges;
+    init_kernel_attributes();
+    *out = c;
+    return RA_OK;
+}
+
+ra_status ra_ctx_destroy(ra_ctx *c)
+{
+    if (!c) return RA_E_INVAL;
+    if (c->stream || c->ws || c->d_chal) (void)hipStreamSynchronize(c->stream);
+    if (c->d_chal) (void)hipFree(c->d_chal);
+    if (c->d_eq) (void)hipFree(c->d_eq);
+    if (c->d_params) (void)hipFree(c->d_params);
+    if (c->d_claims) (void)hipFree(c->d_claims);
+    if (c->ws) (void)hipFree(c->ws);
+    if (c->h_stage) (void)hipHostFree(c->h_stage);
+    delete c;
+    return RA_OK;
+}
+
+ra_status ra_ctx_cursor(const ra_ctx *c, uint64_t *consumed)
+{
+    if (!c || !consumed) return RA_E_INVAL;
+    *consumed = c->cursor;
+    return RA_OK;
+}
+
+ra_status ra_mle_bind(ra_ctx *c, const void *d_T, ra_dtype dtype, uint32_t rows, uint32_t cols, int bind_rows,
+                      const uint64_t *h_point, uint32_t point_len, uint64_t *d_out)
+{
+    if (!c || !d_T || !d_out || !is_pow2(rows) || !is_pow2(cols)) return RA_E_INVAL;
+    if (dtype != RA_I16 && dtype != RA_I32 && dtype != RA_I64 && dtype != RA_FIELD) return RA_E_INVAL;
+    const int v = log2u(bind_rows ? rows : cols);
+    if ((int)point_len != v || (v && !h_point)) return RA_E_INVAL;
+    for (int i = 0; i < v; i++)
+        if (h_point[i] >= kP) return RA_E_INVAL;
+    Carve cv;
+    const size_t o_pt = cv.take<uint64_t>(std::max(v, 1));
+    const size_t o_eq = cv.take<uint64_t>(1ull << v);
+    const size_t o_scr = cv.take<uint64_t>(bind_rows ? (size_t)bind_rows_chunks(rows) * cols : 1);
+    ra_status st = ensure_ws(c, cv.off);
+    if (st != RA_OK) return st;
+    st = ensure_stage(c, std::max(v, 1));
+    if (st != RA_OK) return st;
+    uint64_t *pt = (uint64_t *)(c->ws + o_pt), *eq = (uint64_t *)(c->ws + o_eq), *scr = (uint64_t *)(c->ws + o_scr);
+    RA_HIP(hipStreamSynchronize(c->stream));  // staging buffer is free
+    if (v) std::memcpy(c->h_stage, h_point, (size_t)v * 8);
+    RA_HIP(hipMemcpyAsync(pt, c->h_stage, (size_t)std::max(v, 1) * 8, hipMemcpyHostToDevice, c->stream));
+    launch_eq_table(pt, v, eq, c->stream);
+    if (bind_rows)
+        launch_bind_rows(d_T, dtype, rows, cols, eq, scr, d_out, c->stream);
+    else
+        launch_bind_cols(d_T, dtype, rows, cols, eq, d_out, c->stream);
+    RA_HIP(hipGetLastError());
+    RA_HIP(hipStreamSynchronize(c->stream));
+    return RA_OK;
+}
+
+ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
+                                   uint32_t m, uint32_t k, int64_t *d_C, ra_matmul_proof *out)
+{
+    if (!c || !d_A || !d_B || !d_C || !out) return RA_E_INVAL;
+    if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k)) return RA_E_INVAL;
+    if (a_dtype != RA_I16 && a_dtype != RA_I32) return RA_E_INVAL;
+    if (a_dtype == RA_I32 && m > 65536) return RA_E_INVAL;  // exact int64 product
+    if (c->phase != 0) return RA_E_STATE;
+    const int ln = log2u(n), lm = log2u(m), lk = log2u(k);
+    if (lm && !out->evals) return RA_E_INVAL;
+    const uint64_t need = (uint64_t)ln + lk + lm;
+    if (c->cursor + need > c->n_chal) return RA_E_CHALLENGES;
+    const uint64_t *r1 = c->d_chal + c->cursor, *r2 = r1 + ln, *rho = r2 + lk;
+
+    ra_status st = ensure_eq(c, (size_t)n + k);
+    if (st != RA_OK) return st;
+    const size_t cap = tail_capacity(2);
+    int nslots = 1;
+    for (size_t S = m; S > cap; S >>= 1) nslots++;
+    const size_t trw = 3 + 3 * (size_t)lm;
+    Carve cv;
+    const size_t o_a = cv.take<uint64_t>(m), o_b = cv.take<uint64_t>(m);
+    const size_t o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n) * m);
+    const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
+    const size_t o_tr = cv.take<uint64_t>(trw);
+    if ((st = ensure_ws(c, cv.off)) != RA_OK) return st;
+    if ((st = ensure_stage(c, trw)) != RA_OK) return st;
+    uint64_t *a = (uint64_t *)(c->ws + o_a), *b = (uint64_t *)(c->ws + o_b);
+    uint64_t *scr = (uint64_t *)(c->ws + o_scr), *part = (uint64_t *)(c->ws + o_part), *tr = (uint64_t *)(c->ws + o_tr);
+    uint64_t *E1 = c->d_eq, *E2 = c->d_eq + n;
+    hipStream_t s = c->stream;
+
+    launch_eq_table(r1, ln, E1, s);
+    launch_eq_table(r2, lk, E2, s);
+    launch_gemm_i64(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, s);
+    launch_bind_rows(d_A, a_dtype, n, m, E1, scr, a, s);
+    launch_bind_cols(d_B, RA_I16, m, k, E2, b, s);
+
+    // transcript: [c0][evals 3 lm][a*][b*]
+    SlotTable slots;
+    slots.count = 0;
+    if (m > cap) {
+        launch_dot(a, b, m, part, s);
+        slots.s[slots.count++] = Slot{round_blocks(m), 1, 0, 2, 0};
+        int j = 0;
+        for (size_t S = m; S > cap; S >>= 1, j++) {
+            const uint64_t h = S / 2;
+            launch_round(KIND_MATMUL, a, b, nullptr, h, rho + j, nullptr, part + (size_t)slots.count * kPartStride, s);
+            slots.s[slots.count++] = Slot{round_blocks(h), 3, 1 + 3 * j, 0, 0};
+        }
+        launch_tail(KIND_MATMUL, a, b, nullptr, lm - j, rho + j, nullptr, tr + 1 + 3 * j, tr + 1 + 3 * lm, nullptr, s);
+    } else {
+        launch_tail(KIND_MATMUL, a, b, nullptr, lm, rho, nullptr, tr + 1, tr + 1 + 3 * lm, tr, s);
+    }
+    launch_assemble(slots, part, kPartStride, nullptr, 0, tr, s);
+    if ((st = finish(c, tr, trw)) != RA_OK) return st;
+
+    const uint64_t *h = c->h_stage;
+    out->log_m = (uint32_t)lm;
+    out->c0 = h[0];
+    if (lm) std::memcpy(out->evals, h + 1, 3 * (size_t)lm * 8);
+    out->a_star = h[1 + 3 * lm];
+    out->b_star = h[2 + 3 * lm];
+    c->n = n;
+    c->m = m;
+    c->k = k;
+    c->phase = 1;
+    c->cursor += need;
+    return RA_OK;
+}
+
+ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uint32_t k, int32_t *d_R,
+                                  uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words,
+                                  ra_witness_info *io)
+{
+    if (!c || !d_C || !d_R || !d_Rm || !d_Y || !d_Z || !d_bits || !io) return RA_E_INVAL;
+    if (c->phase != 1) return RA_E_STATE;
+    if (n != c->n || k != c->k) return RA_E_INVAL;
+    if (io->s < 1 || io->s > 16 || io->relu > 1 || io->round_mode > 1 || io->t < -1) return RA_E_INVAL;
+    const uint64_t N = (uint64_t)n * k;
+    if (bits_words < N) return RA_E_BUFSIZE;
+    const int nb = witness_blocks(N);
+    Carve cv;
+    const size_t o_mm = cv.take<int64_t>(2 * (size_t)nb), o_cl = cv.take<uint64_t>(4 * (size_t)nb);
+    ra_status st = ensure_ws(c, cv.off);
+    if (st != RA_OK) return st;
+    const int lk = log2u(k);
+    launch_witness(d_C, N, lk, (int)io->s, (int)io->relu, (int)io->round_mode, io->t, c->d_eq, c->d_eq + n, d_R, d_Rm,
+                   d_Y, d_Z, d_bits, (int64_t *)(c->ws + o_mm), (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims,
+                   c->stream);
+    RA_HIP(hipGetLastError());
+    WitParams prm;
+    RA_HIP(hipMemcpyAsync(&prm, c->d_params, sizeof(prm), hipMemcpyDeviceToHost, c->stream));
+    if ((st = finish(c, c->d_claims, 4)) != RA_OK) return st;
+    if (prm.status != 0) return prm.status;
+    io->t = prm.t;
+    io->P = (uint32_t)prm.P;
+    io->r_claim = c->h_stage[0];
+    io->rm_claim = c->h_stage[1];
+    io->y_claim = c->h_stage[2];
+    io->z_claim = c->h_stage[3];
+    c->s = (int)io->s;
+    c->relu = (int)io->relu;
+    c->mode = (int)io->round_mode;
+    c->t = prm.t;
+    c->P = prm.P;
+    c->phase = 2;
+    return RA_OK;
+}
+
+ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, const int32_t *d_Y, uint32_t n,
+                         uint32_t k, const ra_witness_info *info, ra_range_proof *out)
+{
+    if (!c || !d_bits || !info || !out || !out->evals) return RA_E_INVAL;
+    if (c->phase != 2) return RA_E_STATE;
+    if (n != c->n || k != c->k) return RA_E_INVAL;
+    if ((int)info->s != c->s || (int)info->relu != c->relu || (int)info->round_mode != c->mode || info->t != c->t ||
+        (int)info->P != c->P)
+        return RA_E_INVAL;
+    const int relu = c->relu;
+    if (relu && (!d_R || !d_Y || !out->relu_evals)) return RA_E_INVAL;
+    const uint64_t N = (uint64_t)n * k;
+    const int lP = log2u((uint64_t)c->P), lN = log2u(N), lk = log2u(k), R = lP + lN;
+    const uint64_t need = 4 + (uint64_t)lP + R + (relu ? lN : 0);
+    if (c->cursor + need > c->n_chal) return RA_E_CHALLENGES;
+    const uint64_t *lam = c->d_chal + c->cursor, *sigma = lam + 4 + lP, *rho2 = sigma + R;
+
+    const size_t cap2 = tail_capacity(2), cap3 = tail_capacity(3);
+    int nslots = lP;
+    for (size_t S = N; S > cap2; S >>= 1) nslots++;
+    if (relu)
+        for (size_t S = N; S > cap3; S >>= 1) nslots++;
+    if (nslots > kMaxSlots) return RA_E_INVAL;
+    // transcript: [evals 4R][EQ fin][bits_claim][range_sum][relu evals 4 lN][EQ fin][r_at][y_at]
+    const size_t F_R = 4 * (size_t)R, RS = F_R + 2, Z0 = F_R + 3, FZ = Z0 + 4 * (size_t)lN, trw = FZ + 3;
+    Carve cv;
+    const size_t o_cst = cv.take<uint64_t>(C_WORDS);
+    const size_t o_eq = cv.take<uint64_t>(N), o_bx = cv.take<uint64_t>(N);
+    const size_t o_eq2 = cv.take<uint64_t>(relu ? N : 1), o_rf = cv.take<uint64_t>(relu ? N : 1),
+                 o_yf = cv.take<uint64_t>(relu ? N : 1);
+    const size_t o_part = cv.take<uint64_t>((size_t)std::max(nslots, 1) * kPartStride);
+    const size_t o_tr = cv.take<uint64_t>(trw);
+    ra_status st = ensure_ws(c, cv.off);
+    if (st != RA_OK) return st;
+    if ((st = ensure_stage(c, trw)) != RA_OK) return st;
+    uint64_t *cst = (uint64_t *)(c->ws + o_cst), *EQ = (uint64_t *)(c->ws + o_eq), *Bx = (uint64_t *)(c->ws + o_bx);
+    uint64_t *EQ2 = (uint64_t *)(c->ws + o_eq2), *Rf = (uint64_t *)(c->ws + o_rf), *Yf = (uint64_t *)(c->ws + o_yf);
+    uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = (uint64_t *)(c->ws + o_tr);
+    hipStream_t s = c->stream;
+
+    launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, s);
+    SlotTable slots;
+    slots.count = 0;
+    const int pnb = plane_blocks(N);
+    for (int j = 0; j < lP; j++) slots.s[slots.count++] = Slot{pnb, 6, 4 * j, 1, j + 1};
+    launch_plane_rounds(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, cst, sigma, EQ, relu ? EQ2 : nullptr, Bx, part, s);
+    {   // rounds over x of the range instance
+        int j = 0;
+        size_t S = N;
+        for (; S > cap2; S >>= 1, j++) {
+            const uint64_t h = S / 2;
+            launch_round(KIND_RANGE, EQ, Bx, nullptr, h, sigma + lP + j, cst + C_EP,
+                         part + (size_t)slots.count * kPartStride, s);
+            slots.s[slots.count++] = Slot{round_blocks(h), 4, 4 * (lP + j), 0, 0};
+        }
+        launch_tail(KIND_RANGE, EQ, Bx, nullptr, lN - j, sigma + lP + j, cst + C_EP, tr + 4 * (lP + j), tr + F_R,
+                    nullptr, s);
+    }
+    if (relu) {  // zero-check of Eq. (6) at (r1, r2)
+        launch_i32_to_field(d_R, N, Rf, s);
+        launch_i32_to_field(d_Y, N, Yf, s);
+        int j = 0;
+        size_t S = N;
+        for (; S > cap3; S >>= 1, j++) {
+            const uint64_t h = S / 2;
+            launch_round(KIND_RELU, EQ2, Rf, Yf, h, rho2 + j, nullptr, part + (size_t)slots.count * kPartStride, s);
+            slots.s[slots.count++] = Slot{round_blocks(h), 4, (int)Z0 + 4 * j, 0, 0};
+        }
+        launch_tail(KIND_RELU, EQ2, Rf, Yf, lN - j, rho2 + j, nullptr, tr + Z0 + 4 * j, tr + FZ, nullptr, s);
+    }
+    launch_assemble(slots, part, kPartStride, cst, lP, tr, s);
+    if ((st = finish(c, tr, trw)) != RA_OK) return st;
+
+    const uint64_t *h = c->h_stage;
+    out->rounds = (uint32_t)R;
+    std::memcpy(out->evals, h, 4 * (size_t)R * 8);
+    out->bits_claim = h[F_R + 1];
+    out->range_sum = h[RS];
+    out->relu_rounds = relu ? (uint32_t)lN : 0;
+    if (relu) {
+        if (lN) std::memcpy(out->relu_evals, h + Z0, 4 * (size_t)lN * 8);
+        out->r_at = h[FZ + 1];
+        out->y_at = h[FZ + 2];
+    } else {
+        out->r_at = out->y_at = 0;
+    }
+    c->phase = 0;
+    c->cursor += need;
+    return RA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,86 @@
+// common.hpp -- declarations shared by the HIP kernel files and the host
+// driver of the Range-Arithmetic prover.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ra {
+
+constexpr int kThreads = 256;          // block size of streaming kernels
+constexpr int kTailThreads = 1024;     // block size of the LDS tail kernel
+constexpr int kMaxBlocks = 1024;       // blocks of a grid-stride round kernel
+constexpr size_t kTailLdsBytes = 128 * 1024;  // LDS budget of the tail (160 KB per CU on gfx950)
+constexpr int kMaxSlots = 96;          // per-call partial-sum slots (rounds)
+constexpr int kMaxPlaneLog = 6;        // bit planes per output <= 64 (one word)
+
+// Constant block of the concatenated range check (words), see sumcheck.hip.
+constexpr int C_E = 0;      // e_j[p'] = eq(tau_{>j}, p'), j = 1..lP, sizes P/2, P/4, ..., 1
+constexpr int C_W = 64;     // W_j, sizes P, P/2, ..., 2
+constexpr int C_W2 = 192;   // 2 W_j[i + h] - W_j[i], sizes P/2, ..., 1
+constexpr int C_K = 256;    // K_j, j = 1..lP
+constexpr int C_TAU = 264;  // tau_p
+constexpr int C_EP = 272;   // Ep, c (the kind parameters of KIND_RANGE), Wp, mu
+constexpr int C_WORDS = 280;
+
+// Sum-check instance kinds (see sumcheck.hip).
+enum Kind { KIND_MATMUL = 0, KIND_RANGE = 1, KIND_RELU = 2 };
+
+// Parameters of the rescale / ReLU witness, written on the device.
+struct WitParams {
+    int32_t status;  // 0 ok, else an RA_E_* code
+    int32_t t, P, lP;
+    int32_t s, relu, mode, t_in;
+    int64_t cmin, cmax;
+};
+
+// Where the per-block partial sums of one round live and how to combine them.
+struct Slot {
+    int32_t nblk;      // blocks that wrote partials
+    int32_t width;     // words per block (d + 1, or 6 for a plane round)
+    int32_t out;       // offset of the round's evaluations in the transcript buffer
+    int32_t kind;      // 0: plain sums -> evals; 1: plane round (combine with constants); 2: scalar sum
+    int32_t round;     // plane round index for kind 1
+};
+struct SlotTable {
+    int32_t count;
+    Slot s[kMaxSlots];
+};
+
+// ---- launchers (witness.hip) ----
+void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st);
+void launch_gemm_i64(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
+                     hipStream_t st);
+// rows binding: out[c] = sum_r E[r] T[r, c]; needs scratch of nchunks(rows) * cols words
+int bind_rows_chunks(uint32_t rows);
+void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,
+                      uint64_t *out, hipStream_t st);
+void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *out,
+                      hipStream_t st);
+int witness_blocks(uint64_t N);
+void launch_witness(const int64_t *C, uint64_t N, int lk, int s, int relu, int mode, int t_in, const uint64_t *E1,
+                    const uint64_t *E2, int32_t *R, uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits,
+                    int64_t *mm_part, uint64_t *claim_part, WitParams *params, uint64_t *claims_out, hipStream_t st);
+
+// ---- launchers (sumcheck.hip) ----
+int round_blocks(uint64_t h);
+size_t tail_capacity(int ntab);  // largest 2^v table size the LDS tail holds
+void launch_round(int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t h, const uint64_t *rho,
+                  const uint64_t *kp, uint64_t *part, hipStream_t st);
+void launch_tail(int kind, const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
+                 const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out, hipStream_t st);
+void launch_dot(const uint64_t *a, const uint64_t *b, uint64_t len, uint64_t *part, hipStream_t st);
+void launch_i32_to_field(const int32_t *src, uint64_t N, uint64_t *dst, hipStream_t st);
+// range constants: lambda/mu/tau_p/sigma_p at `chal`, claims from the witness
+size_t range_consts_words(int lP);
+void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,
+                        uint64_t *tr_range_sum, hipStream_t st);
+int plane_blocks(uint64_t N);
+void launch_plane_rounds(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
+                         const uint64_t *cst, const uint64_t *sigma, uint64_t *EQ, uint64_t *EQ2, uint64_t *Bx,
+                         uint64_t *part, hipStream_t st);
+void init_kernel_attributes();
+void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, const uint64_t *cst, int lP,
+                     uint64_t *tr, hipStream_t st);
+
+}  // namespace ra

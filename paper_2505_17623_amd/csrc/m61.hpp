@@ -1,0 +1,103 @@
+// m61.hpp -- arithmetic in F_p, p = 2^61 - 1, for gfx950 wave64 kernels.
+//
+// Elements are uint64 in [0, p).  A product of two elements is formed from
+// four 32x32->64 partial products (the high limbs are below 2^29), and the
+// 122-bit result is folded with 2^61 = 1 (mod p): 2^64 = 8 and
+// x 2^32 = (x >> 29) 2^61 + (x mod 2^29) 2^32 = (x >> 29) + (x mod 2^29) 2^32.
+// Every helper returns a canonical value.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace m61 {
+
+constexpr uint64_t P = 0x1FFFFFFFFFFFFFFFull;
+
+__device__ __forceinline__ uint64_t reduce64(uint64_t x)
+{
+    // any x < 2^64 -> [0, p)
+    x = (x & P) + (x >> 61);
+    return x >= P ? x - P : x;
+}
+
+__device__ __forceinline__ uint64_t add(uint64_t a, uint64_t b)
+{
+    uint64_t s = a + b;
+    return s >= P ? s - P : s;
+}
+
+__device__ __forceinline__ uint64_t sub(uint64_t a, uint64_t b) { return a >= b ? a - b : a + P - b; }
+
+__device__ __forceinline__ uint64_t neg(uint64_t a) { return a ? P - a : 0; }
+
+__device__ __forceinline__ uint64_t mul(uint64_t a, uint64_t b)
+{
+    const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32);
+    const uint32_t b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+    const uint64_t lo = (uint64_t)a0 * b0;                          // < 2^64
+    const uint64_t mid = (uint64_t)a0 * b1 + (uint64_t)a1 * b0;     // < 2^62
+    const uint64_t hi = (uint64_t)a1 * b1;                          // < 2^58
+    const uint64_t s = (hi << 3) + (mid >> 29) + ((mid & 0x1FFFFFFFull) << 32) + (lo & P) + (lo >> 61);
+    return reduce64(s);                                             // s < 2^63
+}
+
+__device__ __forceinline__ uint64_t sqr(uint64_t a) { return mul(a, a); }
+
+// Field element of a signed integer with |z| < 2^63.
+__device__ __forceinline__ uint64_t from_i64(int64_t z)
+{
+    if (z >= 0) return reduce64((uint64_t)z);
+    return neg(reduce64((uint64_t)(-z)));
+}
+
+// e * z for a field element e and a signed integer |z| < 2^31.
+__device__ __forceinline__ uint64_t mul_small(uint64_t e, int32_t z)
+{
+    const uint32_t az = z < 0 ? (uint32_t)(-(int64_t)z) : (uint32_t)z;
+    const uint64_t lo = (uint64_t)(uint32_t)e * az;                 // < 2^63
+    const uint64_t hi = (uint64_t)(uint32_t)(e >> 32) * az;         // < 2^60, weight 2^32
+    const uint64_t s = (hi >> 29) + ((hi & 0x1FFFFFFFull) << 32) + (lo & P) + (lo >> 61);
+    const uint64_t r = reduce64(s);
+    return z < 0 ? neg(r) : r;
+}
+
+// eq(z, b) for a single variable: z b + (1 - z)(1 - b) with b in {0, 1}.
+__device__ __forceinline__ uint64_t eq1_bit(uint64_t z, uint32_t b) { return b ? z : sub(1, z); }
+
+// eq(z, X) = (1 - X) + z (2X - 1) for a small integer X.
+__device__ __forceinline__ uint64_t eq1_small(uint64_t z, int X)
+{
+    return add(from_i64(1 - X), mul_small(z, 2 * X - 1));
+}
+
+// Wave64 sum of one field element per lane (every lane gets the total).
+__device__ __forceinline__ uint64_t wave_sum(uint64_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = add(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// Block sum of NV field values per thread; thread 0 of the block ends with
+// the totals in v[].  `lds` must hold NV * (blockDim.x / 64) words.
+template <int NV>
+__device__ __forceinline__ void block_sum(uint64_t (&v)[NV], uint64_t *lds)
+{
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int i = 0; i < NV; i++) v[i] = wave_sum(v[i]);
+    if (lane == 0)
+#pragma unroll
+        for (int i = 0; i < NV; i++) lds[i * nw + wid] = v[i];
+    __syncthreads();
+    if (wid == 0) {
+#pragma unroll
+        for (int i = 0; i < NV; i++) {
+            uint64_t x = lane < nw ? lds[i * nw + lane] : 0;
+            v[i] = wave_sum(x);
+        }
+    }
+    __syncthreads();
+}
+
+}  // namespace m61

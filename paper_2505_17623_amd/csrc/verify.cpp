@@ -1,0 +1,269 @@
+// verify.cpp -- host-only verifier of the C ABI (ra_verify), Sec. IV.
+//
+// The verifier replays the challenge stream and checks, per layer: the three
+// sum-check chains (Sec. II-D: g_j(0) + g_j(1) equals the previous round's
+// polynomial at its challenge), each instance's final identity, the rounding
+// link between the matrix claim and the rounded output (Theorem A.1,
+// condition 1), the ReLU output link 2 Z = R + Y (Sec. IV), the field guard,
+// and opens the tables handed over in place of commitments by evaluating
+// their multilinear extensions (Eq. (1)) at the challenge points.
+#include <cstring>
+#include <vector>
+
+#include "ra.h"
+
+namespace {
+
+constexpr uint64_t kP = 0x1FFFFFFFFFFFFFFFull;
+typedef unsigned __int128 u128;
+
+// host arithmetic modulo 2^61 - 1 by folding at bit 61
+uint64_t fold(u128 x)
+{
+    uint64_t lo = (uint64_t)x & kP;
+    u128 rest = x >> 61;
+    while (rest) {
+        x = (u128)lo + rest;
+        lo = (uint64_t)x & kP;
+        rest = x >> 61;
+    }
+    return lo == kP ? 0 : lo;
+}
+uint64_t fadd(uint64_t a, uint64_t b) { return fold((u128)a + b); }
+uint64_t fsub(uint64_t a, uint64_t b) { return fold((u128)a + kP - b); }
+uint64_t fmul(uint64_t a, uint64_t b) { return fold((u128)a * b); }
+uint64_t fint(int64_t z) { return z >= 0 ? fold((u128)(uint64_t)z) : fsub(0, fold((u128)(uint64_t)(-(z + 1)) + 1)); }
+uint64_t fpow(uint64_t b, uint64_t e)
+{
+    uint64_t r = 1;
+    while (e) {
+        if (e & 1) r = fmul(r, b);
+        b = fmul(b, b);
+        e >>= 1;
+    }
+    return r;
+}
+uint64_t eq1(uint64_t a, uint64_t b) { return fadd(fmul(a, b), fmul(fsub(1, a), fsub(1, b))); }
+
+bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
+int log2u(uint64_t x)
+{
+    int l = 0;
+    while ((1ull << l) < x) l++;
+    return l;
+}
+
+// value at x of the polynomial of degree d through (i, e[i]), i = 0..d
+uint64_t lagrange(const uint64_t *e, int d, uint64_t x)
+{
+    uint64_t acc = 0;
+    for (int i = 0; i <= d; i++) {
+        uint64_t num = 1, den = 1;
+        for (int j = 0; j <= d; j++) {
+            if (j == i) continue;
+            num = fmul(num, fsub(x, (uint64_t)j));
+            den = fmul(den, fint(i - j));
+        }
+        acc = fadd(acc, fmul(e[i], fmul(num, fpow(den, kP - 2))));
+    }
+    return acc;
+}
+
+// Checks one sum-check transcript; returns false on a broken chain.
+bool chain(int rounds, int d, uint64_t claim, const uint64_t *evals, const uint64_t *rho, uint64_t *final_value)
+{
+    uint64_t cur = claim;
+    for (int j = 0; j < rounds; j++) {
+        const uint64_t *g = evals + (size_t)j * (d + 1);
+        if (fadd(g[0], g[1]) != cur) return false;
+        cur = lagrange(g, d, rho[j]);
+    }
+    *final_value = cur;
+    return true;
+}
+
+// Multilinear extension of a table at z by binding its variables one at a
+// time, most significant first: T[i] <- T[i] + z_j (T[i + h] - T[i]).
+uint64_t mle_bind_all(std::vector<uint64_t> T, const uint64_t *z, int v)
+{
+    size_t size = T.size();
+    for (int j = 0; j < v; j++) {
+        const size_t h = size / 2;
+        for (size_t i = 0; i < h; i++) T[i] = fadd(T[i], fmul(z[j], fsub(T[i + h], T[i])));
+        size = h;
+    }
+    return T[0];
+}
+
+template <typename I> uint64_t mle_ints(const I *tab, size_t len, const uint64_t *z, int v)
+{
+    std::vector<uint64_t> T(len);
+    for (size_t i = 0; i < len; i++) T[i] = fint((int64_t)tab[i]);
+    return mle_bind_all(std::move(T), z, v);
+}
+
+uint64_t eq_points(const uint64_t *a, const uint64_t *b, int v)
+{
+    uint64_t acc = 1;
+    for (int i = 0; i < v; i++) acc = fmul(acc, eq1(a[i], b[i]));
+    return acc;
+}
+
+int verify_layer(const ra_layer_public &L, const ra_layer_tables &T, const ra_layer_transcript &tr,
+                 const ra_layer_public *prev, const uint64_t *chal, uint64_t nchal, uint64_t *cursor,
+                 ra_status *err)
+{
+    const uint32_t n = L.n, m = L.m, k = L.k;
+    if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k) || !L.A || !L.B || !L.Z || !T.R || !T.Rm || !T.Y || !T.bits)
+        return 13;
+    if ((L.a_dtype != RA_I16 && L.a_dtype != RA_I32) || L.s < 1 || L.s > 30 || L.relu > 1 || L.round_mode > 1)
+        return 13;
+    const int ln = log2u(n), lm = log2u(m), lk = log2u(k), lN = ln + lk;
+    const uint64_t N = (uint64_t)n * k;
+    const int s = (int)L.s, relu = (int)L.relu, t = tr.wit.t;
+    // 14: chaining
+    if (L.chained) {
+        if (!prev || L.a_dtype != RA_I32 || prev->n != n || prev->k != m) return 14;
+        const int32_t *A = (const int32_t *)L.A;
+        for (uint64_t i = 0; i < (uint64_t)n * m; i++)
+            if (A[i] != prev->Z[i]) return 14;
+    }
+    // 12: parameters
+    if (t < 0 || s + t + 3 > 61 || tr.wit.s != L.s || tr.wit.relu != L.relu || tr.wit.round_mode != L.round_mode)
+        return 12;
+    const int Q = s + (t + 2) * (relu ? 2 : 1);
+    int P = 1, lP = 0;
+    while (P < Q) {
+        P <<= 1;
+        lP++;
+    }
+    if ((int)tr.wit.P != P || lP > 6) return 12;
+    if (tr.mm.log_m != (uint32_t)lm || tr.rng.rounds != (uint32_t)(lP + lN) ||
+        tr.rng.relu_rounds != (uint32_t)(relu ? lN : 0))
+        return 13;
+    if ((lm && !tr.mm.evals) || !tr.rng.evals || (relu && lN && !tr.rng.relu_evals)) return 13;
+    std::vector<uint64_t> words = {tr.mm.c0, tr.mm.a_star, tr.mm.b_star, tr.wit.r_claim, tr.wit.rm_claim,
+                                   tr.wit.y_claim, tr.wit.z_claim, tr.rng.range_sum, tr.rng.bits_claim,
+                                   tr.rng.r_at, tr.rng.y_at};
+    for (int i = 0; i < 3 * lm; i++) words.push_back(tr.mm.evals[i]);
+    for (int i = 0; i < 4 * (lP + lN); i++) words.push_back(tr.rng.evals[i]);
+    if (relu)
+        for (int i = 0; i < 4 * lN; i++) words.push_back(tr.rng.relu_evals[i]);
+    for (uint64_t w : words)
+        if (w >= kP) return 12;
+
+    const uint64_t need = (uint64_t)ln + lk + lm + 4 + lP + (lP + lN) + (relu ? lN : 0);
+    if (*cursor + need > nchal) {
+        *err = RA_E_CHALLENGES;
+        return 13;
+    }
+    const uint64_t *r1 = chal + *cursor, *r2 = r1 + ln, *rho = r2 + lk, *lam = rho + lm;
+    const uint64_t mu = lam[3], *tau_p = lam + 4, *sigma = tau_p + lP, *rho2 = sigma + lP + lN;
+    *cursor += need;
+    std::vector<uint64_t> r12(r1, r1 + ln);
+    r12.insert(r12.end(), r2, r2 + lk);
+
+    // 1-2: matrix-multiplication sum-check (Eq. (4))
+    uint64_t fin;
+    if (!chain(lm, 2, tr.mm.c0, tr.mm.evals, rho, &fin)) return 1;
+    if (fin != fmul(tr.mm.a_star, tr.mm.b_star)) return 2;
+    // 3: a* = A~(r1, rho), b* = B~(rho, r2)
+    {
+        std::vector<uint64_t> pa(r1, r1 + ln), pb(rho, rho + lm);
+        pa.insert(pa.end(), rho, rho + lm);
+        pb.insert(pb.end(), r2, r2 + lk);
+        const uint64_t ea = L.a_dtype == RA_I16 ? mle_ints((const int16_t *)L.A, (size_t)n * m, pa.data(), ln + lm)
+                                                : mle_ints((const int32_t *)L.A, (size_t)n * m, pa.data(), ln + lm);
+        const uint64_t eb = mle_ints(L.B, (size_t)m * k, pb.data(), lm + lk);
+        if (ea != tr.mm.a_star || eb != tr.mm.b_star) return 3;
+    }
+    // 4: C = 2^s R + Rm - 2^(s-1) (floor mode: C = 2^s R + Rm), at (r1, r2)
+    {
+        uint64_t rhs = fadd(fmul(fint((int64_t)1 << s), tr.wit.r_claim), tr.wit.rm_claim);
+        if (L.round_mode == RA_ROUND_NEAREST) rhs = fsub(rhs, fint((int64_t)1 << (s - 1)));
+        if (rhs != tr.mm.c0) return 4;
+    }
+    // 5-7: concatenated range sum-check
+    {
+        uint64_t H = fadd(fmul(lam[0], tr.wit.rm_claim), fmul(lam[1], fadd(tr.wit.r_claim, fint((int64_t)1 << (t + 1)))));
+        if (relu) H = fadd(H, fmul(lam[2], tr.wit.y_claim));
+        H = fmul(mu, H);
+        if (H != tr.rng.range_sum) return 5;
+        if (!chain(lP + lN, 3, H, tr.rng.evals, sigma, &fin)) return 5;
+        std::vector<uint64_t> W(P, 0);
+        int q = 0;
+        for (int b = 0; b < s; b++) W[q++] = fmul(lam[0], 1ull << b);
+        for (int b = 0; b < t + 2; b++) W[q++] = fmul(lam[1], 1ull << b);
+        if (relu)
+            for (int b = 0; b < t + 2; b++) W[q++] = fmul(lam[2], 1ull << b);
+        const uint64_t wsig = mle_bind_all(W, sigma, lP);
+        const uint64_t ep = eq_points(tau_p, sigma, lP), ex = eq_points(r12.data(), sigma + lP, lN);
+        const uint64_t bc = tr.rng.bits_claim;
+        const uint64_t want = fadd(fmul(fmul(ep, ex), fmul(bc, fsub(bc, 1))), fmul(mu, fmul(fmul(wsig, ex), bc)));
+        if (fin != want) return 6;
+        // 7: b~(sigma): bind the plane variables word by word, then the x variables
+        std::vector<uint64_t> eqp(P);
+        for (int qq = 0; qq < P; qq++) {
+            uint64_t acc = 1;
+            for (int i = 0; i < lP; i++) acc = fmul(acc, eq1(sigma[i], (uint64_t)((qq >> (lP - 1 - i)) & 1)));
+            eqp[qq] = acc;
+        }
+        std::vector<uint64_t> bx(N);
+        for (uint64_t x = 0; x < N; x++) {
+            const uint64_t w = T.bits[x];
+            if (P < 64 && (w >> P)) return 7;  // bits beyond the plane count
+            uint64_t acc = 0;
+            for (int qq = 0; qq < P; qq++)
+                if ((w >> qq) & 1) acc = fadd(acc, eqp[qq]);
+            bx[x] = acc;
+        }
+        if (mle_bind_all(std::move(bx), sigma + lP, lN) != bc) return 7;
+    }
+    // 8: openings of R, Rm, Y at (r1, r2)
+    if (mle_ints(T.R, N, r12.data(), lN) != tr.wit.r_claim || mle_ints(T.Rm, N, r12.data(), lN) != tr.wit.rm_claim ||
+        mle_ints(T.Y, N, r12.data(), lN) != tr.wit.y_claim)
+        return 8;
+    // 9-10: ReLU zero-check (Eq. (6)) from 0, its final identity, openings at rho'
+    if (relu) {
+        if (!chain(lN, 3, 0, tr.rng.relu_evals, rho2, &fin)) return 9;
+        const uint64_t ex = eq_points(r12.data(), rho2, lN);
+        if (fin != fmul(ex, fsub(fmul(tr.rng.r_at, tr.rng.r_at), fmul(tr.rng.y_at, tr.rng.y_at)))) return 9;
+        if (mle_ints(T.R, N, rho2, lN) != tr.rng.r_at || mle_ints(T.Y, N, rho2, lN) != tr.rng.y_at) return 10;
+    }
+    // 11: output link and the public output's opening
+    if (relu) {
+        if (fmul(2, tr.wit.z_claim) != fadd(tr.wit.r_claim, tr.wit.y_claim)) return 11;
+    } else if (tr.wit.z_claim != tr.wit.r_claim) {
+        return 11;
+    }
+    if (mle_ints(L.Z, N, r12.data(), lN) != tr.wit.z_claim) return 11;
+    return 0;
+}
+
+}  // namespace
+
+extern "C" ra_status ra_verify(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, uint32_t n_layers,
+                               const ra_layer_public *pub, const ra_layer_tables *tables,
+                               const ra_layer_transcript *tr, int32_t *verdict, uint32_t *failed_layer)
+{
+    if (!verdict || !failed_layer || (n_layers && (!pub || !tables || !tr)) || (n_challenges && !h_challenges))
+        return RA_E_INVAL;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    for (uint64_t i = 0; i < n_challenges; i++)
+        if (h_challenges[i] >= kP) return RA_E_CHALLENGES;
+    *verdict = 0;
+    *failed_layer = 0;
+    uint64_t cursor = 0;
+    for (uint32_t l = 0; l < n_layers; l++) {
+        ra_status err = RA_OK;
+        const int v = verify_layer(pub[l], tables[l], tr[l], l ? &pub[l - 1] : nullptr, h_challenges, n_challenges,
+                                   &cursor, &err);
+        if (err != RA_OK) return err;
+        if (v) {
+            *verdict = v;
+            *failed_layer = l;
+            return RA_OK;
+        }
+    }
+    return RA_OK;
+}

@@ -1,0 +1,334 @@
+// witness.hip -- eq tables, exact integer matrix product, multilinear binding
+// of matrix sides, and the rescale / ReLU / bit-plane witness.
+#include "common.hpp"
+#include "m61.hpp"
+#include "ra.h"
+
+namespace ra {
+
+// ---------------------------------------------------------------------------
+// eq table (Eq. (1) / chi vector of Sec. II-C):
+//   out[i] = prod_j (z_j i_j + (1 - z_j)(1 - i_j)),  i_1 = MSB of i.
+// ---------------------------------------------------------------------------
+__global__ void k_eq_table(const uint64_t *__restrict__ z, int v, uint64_t *__restrict__ out)
+{
+    const uint64_t n = 1ull << v;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x) {
+        uint64_t acc = 1;
+        for (int j = 0; j < v; j++) acc = m61::mul(acc, m61::eq1_bit(z[j], (uint32_t)(i >> (v - 1 - j)) & 1u));
+        out[i] = acc;
+    }
+}
+
+void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st)
+{
+    const uint64_t n = 1ull << v;
+    const int blocks = (int)((n + kThreads - 1) / kThreads < 4096 ? (n + kThreads - 1) / kThreads : 4096);
+    hipLaunchKernelGGL(k_eq_table, dim3(blocks), dim3(kThreads), 0, st, z, v, out);
+}
+
+// ---------------------------------------------------------------------------
+// Exact product C = A B (Alg. 1 step 2) with int64 accumulation.
+// 64x64 output tile per 256-thread block, 32-deep k slices staged in LDS;
+// thread (tx, ty) owns rows ty + 16 a and columns tx + 16 b, a, b < 4.
+// ---------------------------------------------------------------------------
+template <typename TA>
+__global__ __launch_bounds__(256) void k_gemm_i64(const TA *__restrict__ A, const int16_t *__restrict__ B,
+                                                  int64_t *__restrict__ C, uint32_t n, uint32_t m, uint32_t k)
+{
+    __shared__ int32_t As[32][65];
+    __shared__ int32_t Bs[32][65];
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    const uint32_t row0 = blockIdx.y * 64, col0 = blockIdx.x * 64;
+    int64_t acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; a++)
+#pragma unroll
+        for (int b = 0; b < 4; b++) acc[a][b] = 0;
+
+    for (uint32_t k0 = 0; k0 < m; k0 += 32) {
+#pragma unroll
+        for (int q = 0; q < 8; q++) {
+            const int e = threadIdx.x + 256 * q;
+            const int r = e >> 5, c = e & 31;
+            const uint32_t gr = row0 + r, gc = k0 + c;
+            As[c][r] = (gr < n && gc < m) ? (int32_t)A[(size_t)gr * m + gc] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; q++) {
+            const int e = threadIdx.x + 256 * q;
+            const int r = e >> 6, c = e & 63;
+            const uint32_t gr = k0 + r, gc = col0 + c;
+            Bs[r][c] = (gr < m && gc < k) ? (int32_t)B[(size_t)gr * k + gc] : 0;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int kk = 0; kk < 32; kk++) {
+            int32_t av[4], bv[4];
+#pragma unroll
+            for (int a = 0; a < 4; a++) av[a] = As[kk][ty + 16 * a];
+#pragma unroll
+            for (int b = 0; b < 4; b++) bv[b] = Bs[kk][tx + 16 * b];
+#pragma unroll
+            for (int a = 0; a < 4; a++)
+#pragma unroll
+                for (int b = 0; b < 4; b++) acc[a][b] += (int64_t)av[a] * bv[b];
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int a = 0; a < 4; a++)
+#pragma unroll
+        for (int b = 0; b < 4; b++) {
+            const uint32_t r = row0 + ty + 16 * a, c = col0 + tx + 16 * b;
+            if (r < n && c < k) C[(size_t)r * k + c] = acc[a][b];
+        }
+}
+
+void launch_gemm_i64(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
+                     hipStream_t st)
+{
+    dim3 grid((k + 63) / 64, (n + 63) / 64);
+    if (a_is_i32)
+        hipLaunchKernelGGL(k_gemm_i64<int32_t>, grid, dim3(256), 0, st, (const int32_t *)A, B, C, n, m, k);
+    else
+        hipLaunchKernelGGL(k_gemm_i64<int16_t>, grid, dim3(256), 0, st, (const int16_t *)A, B, C, n, m, k);
+}
+
+// ---------------------------------------------------------------------------
+// Binding one side of a matrix with an eq table (Eq. (4): a~(r1, l) is the
+// r1-row combination of A, b~(l, r2) the r2-column combination of B).
+// ---------------------------------------------------------------------------
+template <typename T> __device__ __forceinline__ uint64_t term(uint64_t e, T a);
+template <> __device__ __forceinline__ uint64_t term<int16_t>(uint64_t e, int16_t a) { return m61::mul_small(e, a); }
+template <> __device__ __forceinline__ uint64_t term<int32_t>(uint64_t e, int32_t a) { return m61::mul_small(e, a); }
+template <> __device__ __forceinline__ uint64_t term<int64_t>(uint64_t e, int64_t a)
+{
+    return m61::mul(e, m61::from_i64(a));
+}
+template <> __device__ __forceinline__ uint64_t term<uint64_t>(uint64_t e, uint64_t a) { return m61::mul(e, a); }
+
+constexpr uint32_t kBindRowsPerChunk = 64;
+
+int bind_rows_chunks(uint32_t rows) { return (int)((rows + kBindRowsPerChunk - 1) / kBindRowsPerChunk); }
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_bind_rows(const T *__restrict__ A, uint32_t rows, uint32_t cols,
+                                                   const uint64_t *__restrict__ E, uint64_t *__restrict__ part)
+{
+    const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= cols) return;
+    const uint32_t r0 = blockIdx.y * kBindRowsPerChunk;
+    const uint32_t r1 = r0 + kBindRowsPerChunk < rows ? r0 + kBindRowsPerChunk : rows;
+    uint64_t acc = 0;
+    for (uint32_t r = r0; r < r1; r++) acc = m61::add(acc, term<T>(E[r], A[(size_t)r * cols + c]));
+    part[(size_t)blockIdx.y * cols + c] = acc;
+}
+
+__global__ __launch_bounds__(256) void k_sum_chunks(const uint64_t *__restrict__ part, int nchunks, uint32_t cols,
+                                                    uint64_t *__restrict__ out)
+{
+    const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= cols) return;
+    uint64_t acc = 0;
+    for (int q = 0; q < nchunks; q++) acc = m61::add(acc, part[(size_t)q * cols + c]);
+    out[c] = acc;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_bind_cols(const T *__restrict__ B, uint32_t rows, uint32_t cols,
+                                                   const uint64_t *__restrict__ E, uint64_t *__restrict__ out)
+{
+    const uint32_t row = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;  // one wave per row
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;                                          // wave-uniform
+    uint64_t acc = 0;
+    for (uint32_t c = lane; c < cols; c += 64) acc = m61::add(acc, term<T>(E[c], B[(size_t)row * cols + c]));
+    acc = m61::wave_sum(acc);
+    if (lane == 0) out[row] = acc;
+}
+
+void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,
+                      uint64_t *out, hipStream_t st)
+{
+    const int nch = bind_rows_chunks(rows);
+    dim3 grid((cols + 255) / 256, nch);
+    switch (dtype) {
+    case RA_I16: hipLaunchKernelGGL(k_bind_rows<int16_t>, grid, dim3(256), 0, st, (const int16_t *)T, rows, cols, E, scratch); break;
+    case RA_I32: hipLaunchKernelGGL(k_bind_rows<int32_t>, grid, dim3(256), 0, st, (const int32_t *)T, rows, cols, E, scratch); break;
+    case RA_I64: hipLaunchKernelGGL(k_bind_rows<int64_t>, grid, dim3(256), 0, st, (const int64_t *)T, rows, cols, E, scratch); break;
+    default: hipLaunchKernelGGL(k_bind_rows<uint64_t>, grid, dim3(256), 0, st, (const uint64_t *)T, rows, cols, E, scratch); break;
+    }
+    hipLaunchKernelGGL(k_sum_chunks, dim3((cols + 255) / 256), dim3(256), 0, st, (const uint64_t *)scratch, nch, cols, out);
+}
+
+void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *out,
+                      hipStream_t st)
+{
+    dim3 grid((rows + 3) / 4);  // four waves (rows) per block
+    switch (dtype) {
+    case RA_I16: hipLaunchKernelGGL(k_bind_cols<int16_t>, grid, dim3(256), 0, st, (const int16_t *)T, rows, cols, E, out); break;
+    case RA_I32: hipLaunchKernelGGL(k_bind_cols<int32_t>, grid, dim3(256), 0, st, (const int32_t *)T, rows, cols, E, out); break;
+    case RA_I64: hipLaunchKernelGGL(k_bind_cols<int64_t>, grid, dim3(256), 0, st, (const int64_t *)T, rows, cols, E, out); break;
+    default: hipLaunchKernelGGL(k_bind_cols<uint64_t>, grid, dim3(256), 0, st, (const uint64_t *)T, rows, cols, E, out); break;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Rescale / ReLU witness (Sec. II-A, Sec. III-A-2, Sec. III-B).
+// Pass 1: min and max of C -> t (R is monotone in C, so the extreme R come
+// from the extreme C).  Pass 2: R, Rm, Y, Z, the bit word and the four claims.
+// ---------------------------------------------------------------------------
+int witness_blocks(uint64_t N)
+{
+    const uint64_t b = (N + kThreads - 1) / kThreads;
+    return (int)(b < (uint64_t)kMaxBlocks ? b : (uint64_t)kMaxBlocks);
+}
+
+__global__ __launch_bounds__(256) void k_minmax(const int64_t *__restrict__ C, uint64_t N, int64_t *__restrict__ part)
+{
+    __shared__ int64_t smin[4], smax[4];
+    int64_t mn = INT64_MAX, mx = INT64_MIN;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += (uint64_t)gridDim.x * blockDim.x) {
+        const int64_t c = C[i];
+        mn = c < mn ? c : mn;
+        mx = c > mx ? c : mx;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const int64_t a = __shfl_xor(mn, off, 64), b = __shfl_xor(mx, off, 64);
+        mn = a < mn ? a : mn;
+        mx = b > mx ? b : mx;
+    }
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    if (lane == 0) {
+        smin[wid] = mn;
+        smax[wid] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < (int)(blockDim.x >> 6); w++) {
+            mn = smin[w] < mn ? smin[w] : mn;
+            mx = smax[w] > mx ? smax[w] : mx;
+        }
+        part[2 * blockIdx.x] = mn;
+        part[2 * blockIdx.x + 1] = mx;
+    }
+}
+
+__device__ __forceinline__ int64_t rescale(int64_t c, int s, int mode)
+{
+    const int64_t half = mode == RA_ROUND_NEAREST ? (int64_t)1 << (s - 1) : 0;
+    return (c + half) >> s;  // arithmetic shift = floor division by 2^s
+}
+
+__global__ void k_wit_params(const int64_t *__restrict__ part, int nblk, int s, int relu, int mode, int t_in,
+                             WitParams *__restrict__ prm)
+{
+    if (threadIdx.x != 0) return;
+    int64_t mn = INT64_MAX, mx = INT64_MIN;
+    for (int b = 0; b < nblk; b++) {
+        mn = part[2 * b] < mn ? part[2 * b] : mn;
+        mx = part[2 * b + 1] > mx ? part[2 * b + 1] : mx;
+    }
+    WitParams p;
+    p.status = 0;
+    p.s = s;
+    p.relu = relu;
+    p.mode = mode;
+    p.t_in = t_in;
+    p.cmin = mn;
+    p.cmax = mx;
+    const int64_t rlo = rescale(mn, s, mode), rhi = rescale(mx, s, mode);
+    // u = R for R >= 0, -R - 1 for R < 0; R in [-2^(t+1), 2^(t+1)) iff u < 2^(t+1)
+    const uint64_t ulo = rlo >= 0 ? (uint64_t)rlo : (uint64_t)(-(rlo + 1));
+    const uint64_t uhi = rhi >= 0 ? (uint64_t)rhi : (uint64_t)(-(rhi + 1));
+    const uint64_t umax = ulo > uhi ? ulo : uhi;
+    int bl = 0;
+    while (bl < 64 && (umax >> bl) != 0) bl++;
+    int t = bl > 1 ? bl - 1 : 0;
+    if (t_in >= 0) {
+        if (t_in < 62 && (umax >> (t_in + 1)) != 0) p.status = RA_E_RANGE;
+        t = t_in;
+    }
+    if (p.status == 0 && t > 29) p.status = RA_E_RANGE;  // R, Y must fit int32
+    if (p.status == 0 && s + t + 3 > 61) p.status = RA_E_FIELD_TOO_SMALL;
+    const int Q = s + (t + 2) * (relu ? 2 : 1);
+    int P = 1, lP = 0;
+    while (P < Q) {
+        P <<= 1;
+        lP++;
+    }
+    if (p.status == 0 && lP > kMaxPlaneLog) p.status = RA_E_RANGE;
+    p.t = t;
+    p.P = P;
+    p.lP = lP;
+    *prm = p;
+}
+
+__global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, uint64_t N, int lk,
+                                                 const WitParams *__restrict__ prm, const uint64_t *__restrict__ E1,
+                                                 const uint64_t *__restrict__ E2, int32_t *__restrict__ R,
+                                                 uint16_t *__restrict__ Rm, int32_t *__restrict__ Y,
+                                                 int32_t *__restrict__ Z, uint64_t *__restrict__ bits,
+                                                 uint64_t *__restrict__ claim_part)
+{
+    __shared__ uint64_t red[4 * 4];
+    const WitParams p = *prm;
+    if (p.status != 0) return;  // uniform over the grid
+    const int s = p.s, t = p.t, relu = p.relu;
+    const int64_t half = p.mode == RA_ROUND_NEAREST ? (int64_t)1 << (s - 1) : 0;
+    const int64_t shift_r = (int64_t)1 << (t + 1);
+    const uint64_t kmask = (1ull << lk) - 1;
+    uint64_t acc[4] = {0, 0, 0, 0};
+    for (uint64_t x = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; x < N; x += (uint64_t)gridDim.x * blockDim.x) {
+        const int64_t c = C[x] + half;
+        const int64_t q = c >> s;
+        const int32_t rm = (int32_t)(c - (q << s));
+        const int32_t r = (int32_t)q;
+        const int32_t y = r < 0 ? -r : r;
+        const int32_t z = relu ? (r > 0 ? r : 0) : r;
+        R[x] = r;
+        Rm[x] = (uint16_t)rm;
+        Y[x] = y;
+        Z[x] = z;
+        uint64_t w = (uint64_t)rm | ((uint64_t)(q + shift_r) << s);
+        if (relu) w |= (uint64_t)y << (s + t + 2);
+        bits[x] = w;
+        const uint64_t e = m61::mul(E1[x >> lk], E2[x & kmask]);
+        acc[0] = m61::add(acc[0], m61::mul_small(e, r));
+        acc[1] = m61::add(acc[1], m61::mul_small(e, rm));
+        acc[2] = m61::add(acc[2], m61::mul_small(e, y));
+        acc[3] = m61::add(acc[3], m61::mul_small(e, z));
+    }
+    m61::block_sum<4>(acc, red);
+    if (threadIdx.x == 0)
+        for (int i = 0; i < 4; i++) claim_part[4 * blockIdx.x + i] = acc[i];
+}
+
+__global__ __launch_bounds__(256) void k_claims_final(const uint64_t *__restrict__ part, int nblk,
+                                                      const WitParams *__restrict__ prm, uint64_t *__restrict__ out)
+{
+    __shared__ uint64_t red[4 * 4];
+    uint64_t acc[4] = {0, 0, 0, 0};
+    for (int b = threadIdx.x; b < nblk; b += blockDim.x)
+        for (int i = 0; i < 4; i++) acc[i] = m61::add(acc[i], part[4 * b + i]);
+    m61::block_sum<4>(acc, red);
+    if (threadIdx.x == 0 && prm->status == 0)
+        for (int i = 0; i < 4; i++) out[i] = acc[i];
+}
+
+void launch_witness(const int64_t *C, uint64_t N, int lk, int s, int relu, int mode, int t_in, const uint64_t *E1,
+                    const uint64_t *E2, int32_t *R, uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits,
+                    int64_t *mm_part, uint64_t *claim_part, WitParams *params, uint64_t *claims_out, hipStream_t st)
+{
+    const int nb = witness_blocks(N);
+    hipLaunchKernelGGL(k_minmax, dim3(nb), dim3(kThreads), 0, st, C, N, mm_part);
+    hipLaunchKernelGGL(k_wit_params, dim3(1), dim3(64), 0, st, (const int64_t *)mm_part, nb, s, relu, mode, t_in, params);
+    hipLaunchKernelGGL(k_rescale, dim3(nb), dim3(kThreads), 0, st, C, N, lk, (const WitParams *)params, E1, E2, R, Rm,
+                       Y, Z, bits, claim_part);
+    hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, (const uint64_t *)claim_part, nb,
+                       (const WitParams *)params, claims_out);
+}
+
+}  // namespace ra

@@ -1,0 +1,298 @@
+"""Python binding of the C ABI in include/ra.h (libra_mi355x.so).
+
+Argument marshalling only: every step of the prover runs in the HIP library.
+torch supplies device memory and the HIP stream.  Field elements are held in
+int64 tensors / uint64 numpy arrays (same bits).  The library must be built
+(``python -m paper_2505_17623_amd.build``); importing this module without it
+raises, there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libra_mi355x.so")
+P61 = (1 << 61) - 1
+
+RA_I16, RA_I32, RA_I64, RA_FIELD = 1, 2, 3, 4
+RA_ROUND_NEAREST, RA_ROUND_FLOOR = 0, 1
+STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_FIELD_TOO_SMALL",
+          -4: "RA_E_RANGE", -5: "RA_E_CHALLENGES", -6: "RA_E_HIP", -7: "RA_E_STATE",
+          -8: "RA_E_BUFSIZE", -9: "RA_E_NOMEM"}
+EXPORTS = ["ra_ctx_create", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str", "ra_mle_bind",
+           "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify"]
+
+
+class RAError(RuntimeError):
+    def __init__(self, code, where=""):
+        super().__init__(f"{where}: {STATUS.get(code, code)}")
+        self.code = code
+
+
+u64 = ctypes.c_uint64
+u64p = ctypes.POINTER(ctypes.c_uint64)
+
+
+class MatmulProof(ctypes.Structure):
+    _fields_ = [("log_m", ctypes.c_uint32), ("c0", u64), ("evals", u64p), ("a_star", u64), ("b_star", u64)]
+
+
+class WitnessInfo(ctypes.Structure):
+    _fields_ = [("s", ctypes.c_uint32), ("relu", ctypes.c_uint32), ("round_mode", ctypes.c_uint32),
+                ("t", ctypes.c_int32), ("P", ctypes.c_uint32), ("r_claim", u64), ("rm_claim", u64),
+                ("y_claim", u64), ("z_claim", u64)]
+
+
+class RangeProof(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.c_uint32), ("evals", u64p), ("range_sum", u64), ("bits_claim", u64),
+                ("relu_rounds", ctypes.c_uint32), ("relu_evals", u64p), ("r_at", u64), ("y_at", u64)]
+
+
+class LayerPublic(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_uint32), ("m", ctypes.c_uint32), ("k", ctypes.c_uint32),
+                ("s", ctypes.c_uint32), ("relu", ctypes.c_uint32), ("round_mode", ctypes.c_uint32),
+                ("a_dtype", ctypes.c_int), ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
+                ("Z", ctypes.c_void_p), ("chained", ctypes.c_uint32)]
+
+
+class LayerTables(ctypes.Structure):
+    _fields_ = [("R", ctypes.c_void_p), ("Rm", ctypes.c_void_p), ("Y", ctypes.c_void_p),
+                ("bits", ctypes.c_void_p)]
+
+
+class LayerTranscript(ctypes.Structure):
+    _fields_ = [("mm", MatmulProof), ("wit", WitnessInfo), ("rng", RangeProof)]
+
+
+_lib = None
+
+
+def lib():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} not built; run python -m paper_2505_17623_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        vp = ctypes.c_void_p
+        L.ra_ctx_create.argtypes = [u64, u64p, u64, vp, ctypes.POINTER(vp)]
+        L.ra_ctx_destroy.argtypes = [vp]
+        L.ra_ctx_cursor.argtypes = [vp, u64p]
+        L.ra_status_str.restype = ctypes.c_char_p
+        L.ra_status_str.argtypes = [ctypes.c_int32]
+        L.ra_mle_bind.argtypes = [vp, vp, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int, u64p,
+                                  ctypes.c_uint32, vp]
+        L.ra_sumcheck_matmul_prove.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_uint32, ctypes.c_uint32,
+                                               ctypes.c_uint32, vp, ctypes.POINTER(MatmulProof)]
+        L.ra_rescale_relu_witness.argtypes = [vp, vp, ctypes.c_uint32, ctypes.c_uint32, vp, vp, vp, vp, vp,
+                                              u64, ctypes.POINTER(WitnessInfo)]
+        L.ra_range_prove.argtypes = [vp, vp, vp, vp, ctypes.c_uint32, ctypes.c_uint32,
+                                     ctypes.POINTER(WitnessInfo), ctypes.POINTER(RangeProof)]
+        L.ra_verify.argtypes = [u64, u64p, u64, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
+                                ctypes.POINTER(LayerTables), ctypes.POINTER(LayerTranscript),
+                                ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
+        for f in (L.ra_ctx_create, L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
+                  L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify):
+            f.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def _check(code, where):
+    if code != 0:
+        raise RAError(code, where)
+
+
+def _dptr(t: torch.Tensor):
+    assert t.is_cuda and t.is_contiguous(), "device tensors must be contiguous CUDA tensors"
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _u64_array(vals):
+    a = np.ascontiguousarray(np.asarray(vals, dtype=np.uint64))
+    return a, a.ctypes.data_as(u64p)
+
+
+_DT = {torch.int16: RA_I16, torch.int32: RA_I32, torch.int64: RA_I64}
+
+
+class Context:
+    """A prover context: the challenge stream on the device plus per-layer state."""
+
+    def __init__(self, challenges, stream: torch.cuda.Stream | None = None):
+        self._chal, cp = _u64_array(challenges)
+        self.stream = stream or torch.cuda.current_stream()
+        h = ctypes.c_void_p()
+        _check(lib().ra_ctx_create(P61, cp, len(self._chal), ctypes.c_void_p(self.stream.cuda_stream),
+                                   ctypes.byref(h)), "ra_ctx_create")
+        self.h = h
+
+    def close(self):
+        if self.h:
+            lib().ra_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def cursor(self):
+        v = u64()
+        _check(lib().ra_ctx_cursor(self.h, ctypes.byref(v)), "ra_ctx_cursor")
+        return int(v.value)
+
+
+def ra_mle_bind(ctx: Context, T: torch.Tensor, bind_rows: bool, point, field: bool = False):
+    """d_out[c] = sum_r eq(point, r) T[r, c] (rows) or d_out[r] = sum_c T[r, c] eq(point, c)."""
+    rows, cols = T.shape
+    dt = RA_FIELD if field else _DT[T.dtype]
+    pt, pp = _u64_array(point)
+    out = torch.empty(cols if bind_rows else rows, dtype=torch.int64, device=T.device)
+    _check(lib().ra_mle_bind(ctx.h, _dptr(T), dt, rows, cols, int(bool(bind_rows)), pp, len(pt), _dptr(out)),
+           "ra_mle_bind")
+    return out
+
+
+def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor):
+    n, m = A.shape
+    m2, k = B.shape
+    assert m == m2 and B.dtype == torch.int16
+    C = torch.empty((n, k), dtype=torch.int64, device=A.device)
+    lm = m.bit_length() - 1
+    ev = np.zeros(max(3 * lm, 1), dtype=np.uint64)
+    pr = MatmulProof()
+    pr.evals = ev.ctypes.data_as(u64p)
+    _check(lib().ra_sumcheck_matmul_prove(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C),
+                                          ctypes.byref(pr)), "ra_sumcheck_matmul_prove")
+    return C, dict(c0=int(pr.c0), mm_evals=[int(x) for x in ev[:3 * lm]], a_star=int(pr.a_star),
+                   b_star=int(pr.b_star))
+
+
+def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1):
+    n, k = C.shape
+    dev = C.device
+    R = torch.empty((n, k), dtype=torch.int32, device=dev)
+    Rm = torch.empty((n, k), dtype=torch.int16, device=dev)   # uint16 bits
+    Y = torch.empty((n, k), dtype=torch.int32, device=dev)
+    Z = torch.empty((n, k), dtype=torch.int32, device=dev)
+    bits = torch.empty(n * k, dtype=torch.int64, device=dev)  # uint64 words
+    info = WitnessInfo(s=s, relu=int(bool(relu)), round_mode=mode, t=t)
+    _check(lib().ra_rescale_relu_witness(ctx.h, _dptr(C), n, k, _dptr(R), _dptr(Rm), _dptr(Y), _dptr(Z),
+                                         _dptr(bits), n * k, ctypes.byref(info)), "ra_rescale_relu_witness")
+    return (R, Rm, Y, Z, bits), info
+
+
+def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
+    n, k = R.shape
+    N = n * k
+    lN = N.bit_length() - 1
+    lP = info.P.bit_length() - 1
+    ev = np.zeros(4 * (lP + lN), dtype=np.uint64)
+    zev = np.zeros(max(4 * lN, 1), dtype=np.uint64)
+    pr = RangeProof()
+    pr.evals = ev.ctypes.data_as(u64p)
+    pr.relu_evals = zev.ctypes.data_as(u64p)
+    _check(lib().ra_range_prove(ctx.h, _dptr(bits), _dptr(R), _dptr(Y), n, k, ctypes.byref(info),
+                                ctypes.byref(pr)), "ra_range_prove")
+    return dict(rs_evals=[int(x) for x in ev], range_sum=int(pr.range_sum), bits_claim=int(pr.bits_claim),
+                zc_evals=[int(x) for x in zev[:4 * pr.relu_rounds]], r_at=int(pr.r_at), y_at=int(pr.y_at))
+
+
+def prove_layer(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1):
+    """The three calls of one layer; returns device tensors and the transcript."""
+    C, mm = ra_sumcheck_matmul_prove(ctx, A, B)
+    (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t)
+    rs = ra_range_prove(ctx, bits, R, Y, info)
+    tr = dict(mm)
+    tr.update(rs)
+    tr.update(t=int(info.t), P=int(info.P), r_claim=int(info.r_claim), rm_claim=int(info.rm_claim),
+              y_claim=int(info.y_claim), z_claim=int(info.z_claim), s=s, relu=int(bool(relu)), mode=mode)
+    return dict(C=C, R=R, Rm=Rm, Y=Y, Z=Z, bits=bits, transcript=tr)
+
+
+def to_device(a: np.ndarray, device="cuda"):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None):
+    """Prove every layer of a workload in order.  A layer's input is the
+    previous output on the device (MLP chains) or the workload's link (im2col)
+    applied on the host.  X / Bs may hold device copies of the inputs."""
+    X = to_device(workload.X, device) if X is None else X
+    Bs = [to_device(L.B, device) for L in workload.layers] if Bs is None else Bs
+    outs = []
+    Z = None
+    for li, layer in enumerate(workload.layers):
+        if li == 0:
+            A = X
+        elif workload.links[li] is None:
+            A = Z
+        else:
+            A = to_device(workload.links[li](Z.cpu().numpy()), device)
+        res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode)
+        res["A"] = A
+        Z = res["Z"]
+        outs.append(res)
+    return outs
+
+
+def unpack_bits(words: np.ndarray, P: int) -> np.ndarray:
+    """(N,) uint64 words -> (P, N) uint8 planes (bit q of word x = plane q)."""
+    w = np.asarray(words).view(np.uint64)
+    q = np.arange(P, dtype=np.uint64)[:, None]
+    return ((w[None, :] >> q) & np.uint64(1)).astype(np.uint8)
+
+
+def ra_verify(challenges, layers):
+    """Host verifier.  `layers` is a list of dicts with numpy arrays A, B, Z,
+    R, Rm, Y, bits (uint64 words) and the transcript dict; returns
+    (verdict, failed_layer)."""
+    chal, cp = _u64_array(challenges)
+    nl = len(layers)
+    pubs = (LayerPublic * nl)()
+    tabs = (LayerTables * nl)()
+    trs = (LayerTranscript * nl)()
+    keep = []
+    for i, L in enumerate(layers):
+        tr = L["transcript"]
+        A = np.ascontiguousarray(L["A"])
+        B = np.ascontiguousarray(L["B"], dtype=np.int16)
+        n, m = A.shape
+        k = B.shape[1]
+        arrs = dict(A=A, B=B, Z=np.ascontiguousarray(L["Z"], dtype=np.int32),
+                    R=np.ascontiguousarray(L["R"], dtype=np.int32),
+                    Rm=np.ascontiguousarray(np.asarray(L["Rm"]).view(np.uint16)),
+                    Y=np.ascontiguousarray(L["Y"], dtype=np.int32),
+                    bits=np.ascontiguousarray(np.asarray(L["bits"]).view(np.uint64)))
+        mm = np.array(tr["mm_evals"] + [0], dtype=np.uint64)
+        rs = np.array(tr["rs_evals"] + [0], dtype=np.uint64)
+        zc = np.array(tr["zc_evals"] + [0], dtype=np.uint64)
+        keep += list(arrs.values()) + [mm, rs, zc]
+        pubs[i] = LayerPublic(n, m, k, tr["s"], tr["relu"], tr["mode"],
+                              RA_I16 if A.dtype == np.int16 else RA_I32, arrs["A"].ctypes.data,
+                              arrs["B"].ctypes.data, arrs["Z"].ctypes.data, int(L.get("chained", 0)))
+        tabs[i] = LayerTables(arrs["R"].ctypes.data, arrs["Rm"].ctypes.data, arrs["Y"].ctypes.data,
+                              arrs["bits"].ctypes.data)
+        t = trs[i]
+        t.mm.log_m = m.bit_length() - 1
+        t.mm.c0, t.mm.a_star, t.mm.b_star = tr["c0"], tr["a_star"], tr["b_star"]
+        t.mm.evals = mm.ctypes.data_as(u64p)
+        t.wit = WitnessInfo(tr["s"], tr["relu"], tr["mode"], tr["t"], tr["P"], tr["r_claim"], tr["rm_claim"],
+                            tr["y_claim"], tr["z_claim"])
+        t.rng.rounds = len(tr["rs_evals"]) // 4
+        t.rng.evals = rs.ctypes.data_as(u64p)
+        t.rng.range_sum, t.rng.bits_claim = tr["range_sum"], tr["bits_claim"]
+        t.rng.relu_rounds = len(tr["zc_evals"]) // 4
+        t.rng.relu_evals = zc.ctypes.data_as(u64p)
+        t.rng.r_at, t.rng.y_at = tr["r_at"], tr["y_at"]
+    verdict = ctypes.c_int32()
+    failed = ctypes.c_uint32()
+    _check(lib().ra_verify(P61, cp, len(chal), nl, pubs, tabs, trs, ctypes.byref(verdict), ctypes.byref(failed)),
+           "ra_verify")
+    return int(verdict.value), int(failed.value)

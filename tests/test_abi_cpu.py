@@ -1,0 +1,119 @@
+"""The C-ABI library on the host: it loads, exports every symbol that
+include/ra.h declares, rejects bad arguments before touching a device, and
+its host-only verifier (ra_verify) accepts the oracle's honest transcripts
+and rejects tampered ones.  No GPU compute call is made here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from helpers import oracle_layer_for_abi
+from oracle import oracle as orc
+from paper_2505_17623_amd import inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def ra():
+    from paper_2505_17623_amd import ra as ra_mod
+    if not os.path.exists(ra_mod.LIB_PATH):
+        from paper_2505_17623_amd import build
+        build.build()
+    ra_mod.lib()
+    return ra_mod
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "ra.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ra_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(ra):
+    syms = declared_symbols()
+    assert set(syms) == set(ra.EXPORTS), syms
+    L = ctypes.CDLL(ra.LIB_PATH)
+    for s in syms:
+        assert hasattr(L, s), s
+
+
+def test_host_side_argument_errors(ra):
+    L = ra.lib()
+    h = ctypes.c_void_p()
+    assert L.ra_ctx_create(7, None, 0, None, ctypes.byref(h)) == -2       # unsupported prime
+    assert L.ra_ctx_create(ra.P61, None, 0, None, None) == -1             # null out
+    bad = np.array([ra.P61], dtype=np.uint64)
+    assert L.ra_ctx_create(ra.P61, bad.ctypes.data_as(ra.u64p), 1, None, ctypes.byref(h)) == -5
+    assert L.ra_ctx_destroy(None) == -1
+    for code, name in ra.STATUS.items():
+        assert L.ra_status_str(code)
+    v = ctypes.c_int32()
+    f = ctypes.c_uint32()
+    assert L.ra_verify(ra.P61, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == 0
+    assert L.ra_verify(5, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == -2
+
+
+def oracle_network(wl):
+    outs = orc.prove_network(wl)
+    layers = []
+    for li, res in enumerate(outs):
+        layers.append(oracle_layer_for_abi(res, wl.layers[li].B, chained=li > 0 and wl.links[li] is None))
+    return layers
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 5])
+def test_library_verifier_accepts_oracle_transcripts(ra, cfg):
+    wl = inputs.small(cfg)
+    layers = oracle_network(wl)
+    assert ra.ra_verify(wl.challenges, layers) == (0, 0)
+
+
+def test_library_verifier_rejects_tampering(ra):
+    wl = inputs.small(2)
+    base = oracle_network(wl)
+
+    def check(li, mutate):
+        layers = [dict(L, transcript=dict(L["transcript"])) for L in base]
+        layers[li] = dict(layers[li])
+        mutate(layers[li])
+        v, f = ra.ra_verify(wl.challenges, layers)
+        assert v != 0 and f == li
+        return v
+
+    P = ra.P61
+
+    def bump(key, i=None):
+        def f(L):
+            tr = L["transcript"]
+            if i is None:
+                tr[key] = (tr[key] + 1) % P
+            else:
+                ev = list(tr[key]); ev[i] = (ev[i] + 1) % P; tr[key] = ev
+        return f
+
+    for key in ("c0", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_claim", "bits_claim",
+                "range_sum"):
+        check(0, bump(key))
+    for key in ("mm_evals", "rs_evals", "zc_evals"):
+        check(1, bump(key, 0))
+        check(1, bump(key, -1))
+
+    def flip_bit(L):
+        b = L["bits"].copy(); b[3] ^= np.uint64(1 << 2); L["bits"] = b
+    assert check(0, flip_bit) == 7
+
+    def wrong_output(L):
+        Z = L["Z"].copy(); Z.flat[5] += 1; L["Z"] = Z
+    assert check(2, wrong_output) == 11
+
+    def relu_sign(L):
+        R = L["R"]; idx = int(np.argmax(R.reshape(-1) < 0))
+        Y = L["Y"].copy(); Y.flat[idx] = R.flat[idx]; L["Y"] = Y
+    assert check(0, relu_sign) != 0
+
+    def unchained(L):
+        A = L["A"].copy(); A.flat[0] += 1; L["A"] = A
+    assert check(1, unchained) == 14

@@ -84,6 +84,17 @@ ra_status ra_ctx_destroy(ra_ctx *ctx);
 ra_status ra_ctx_cursor(const ra_ctx *ctx, uint64_t *consumed);
 const char *ra_status_str(ra_status st);
 
+/* Kernel timing for benchmarks.  With profiling on, every group of kernel
+ * launches (matrix product, bindings, witness passes, plane rounds, global
+ * rounds, LDS tails, assembly) is bracketed by HIP events recorded on the
+ * context's stream; the elapsed times are accumulated per group when each
+ * call synchronises.  Turning profiling on or off clears the totals.
+ *   ra_ctx_profile: group `index` (0-based; RA_E_INVAL past the last one)
+ *   -> its name (static string), total milliseconds and launch count. */
+ra_status ra_ctx_set_profiling(ra_ctx *ctx, int on);
+ra_status ra_ctx_profile(const ra_ctx *ctx, uint32_t index, const char **name, double *total_ms,
+                         uint64_t *launches);
+
 /* Multilinear-extension binding of one side of a matrix (the chi-vector inner
  * product of Sec. II-C applied to every row or column):
  *   bind_rows = 1:  d_out[c] = sum_r eq(point, r) T[r, c],  point_len = log2(rows),

@@ -37,6 +37,12 @@ struct ra_ctx {
     WitParams *d_params = nullptr;
     uint64_t *d_claims = nullptr;  // R~, Rm~, Y~, Z~ at (r1, r2)
     int s = 0, relu = 0, mode = 0, t = 0, P = 0;
+    // kernel-group timing (ra_ctx_set_profiling)
+    bool prof_on = false;
+    std::vector<hipEvent_t> ev_pool;                   // free events
+    std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> ev_pending;
+    double prof_ms[32] = {};
+    uint64_t prof_n[32] = {};
     // scratch
     char *ws = nullptr;
     size_t ws_cap = 0;
@@ -100,16 +106,114 @@ ra_status ensure_eq(ra_ctx *c, size_t words)
     return RA_OK;
 }
 
+// Kernel groups timed with events when profiling is on.
+enum Group {
+    G_EQ = 0, G_GEMM, G_BIND_ROWS, G_BIND_COLS, G_MM_ROUNDS, G_MM_TAIL, G_WIT_MINMAX, G_WIT_RESCALE,
+    G_RANGE_SETUP, G_RANGE_PLANE, G_RANGE_ROUNDS, G_RANGE_TAIL, G_RELU_FIELD, G_RELU_ROUNDS, G_RELU_TAIL,
+    G_ASSEMBLE, G_COUNT
+};
+const char *const kGroupName[G_COUNT] = {
+    "eq_table", "gemm_i64", "bind_rows", "bind_cols", "matmul_rounds", "matmul_tail", "witness_minmax",
+    "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail", "relu_to_field",
+    "relu_rounds", "relu_tail", "assemble"};
+
+hipEvent_t take_event(ra_ctx *c)
+{
+    if (c->ev_pool.empty()) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+    hipEvent_t e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return e;
+}
+
+// Record an event pair around a launch group (no-op unless profiling).
+struct Timed {
+    ra_ctx *c;
+    int g;
+    hipEvent_t a = nullptr;
+    Timed(ra_ctx *c_, int g_) : c(c_), g(g_)
+    {
+        if (c->prof_on && (a = take_event(c))) (void)hipEventRecord(a, c->stream);
+    }
+    ~Timed()
+    {
+        if (!a) return;
+        hipEvent_t b = take_event(c);
+        if (!b) {
+            c->ev_pool.push_back(a);
+            return;
+        }
+        (void)hipEventRecord(b, c->stream);
+        c->ev_pending.push_back({g, {a, b}});
+    }
+};
+
+void flush_profile(ra_ctx *c)
+{
+    for (auto &p : c->ev_pending) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, p.second.first, p.second.second) == hipSuccess) {
+            c->prof_ms[p.first] += ms;
+            c->prof_n[p.first] += 1;
+        }
+        c->ev_pool.push_back(p.second.first);
+        c->ev_pool.push_back(p.second.second);
+    }
+    c->ev_pending.clear();
+}
+
 ra_status finish(ra_ctx *c, const uint64_t *d_src, size_t words)
 {
     RA_HIP(hipGetLastError());
     RA_HIP(hipMemcpyAsync(c->h_stage, d_src, words * 8, hipMemcpyDeviceToHost, c->stream));
     RA_HIP(hipStreamSynchronize(c->stream));
+    flush_profile(c);
     return RA_OK;
 }
 
 constexpr int kPartStride = kMaxBlocks * 6;  // words per partial-sum slot
 
+int log2_tail() { return log2u(tail_capacity(0)); }
+// rounds of a v-variable instance that run as global (multi-block) launches
+int global_rounds(int v) { return v > log2_tail() ? v - log2_tail() : 0; }
+
+// One sum-check instance over tables of 2^v entries (in place): fused global
+// launches while the table exceeds the LDS tail, then the tail.  Round j's
+// width = D + 1 evaluations go to tr[ev_base + width j]; the tables' final
+// values to finals[0..NT); with sum_out >= 0 the claimed sum to tr[sum_out].
+void run_instance(ra_ctx *c, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v, const uint64_t *rho,
+                  const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals, int sum_out,
+                  SlotTable &slots, uint64_t *part, int g_rounds, int g_tail);
+
+}  // namespace
+
+namespace {
+void run_instance(ra_ctx *c, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v, const uint64_t *rho,
+                  const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals, int sum_out,
+                  SlotTable &slots, uint64_t *part, int g_rounds, int g_tail)
+{
+    const int cmax = fused_rounds_max(kind), lt = log2_tail();
+    int j = 0, lS = v;
+    while (lS > lt) {
+        const int C = std::min(cmax, lS - lt);
+        {
+            Timed tm(c, g_rounds);
+            launch_rounds(kind, C, t0, t1, t2, 1ull << lS, rho + j, kp, part + (size_t)slots.count * kPartStride,
+                          kPartStride, c->stream);
+        }
+        const int nb = round_blocks(1ull << (lS - C));
+        for (int r = 0; r < C; r++)
+            slots.s[slots.count++] = Slot{nb, width, ev_base + width * (j + r), 0, 0, (j + r == 0) ? sum_out : -1};
+        lS -= C;
+        j += C;
+    }
+    Timed tm(c, g_tail);
+    launch_tail(kind, t0, t1, t2, v - j, rho + j, kp, tr + ev_base + width * j, finals,
+                (j == 0 && sum_out >= 0) ? tr + sum_out : nullptr, c->stream);
+}
 }  // namespace
 
 extern "C" {
@@ -173,6 +277,8 @@ ra_status ra_ctx_destroy(ra_ctx *c)
     if (c->d_claims) (void)hipFree(c->d_claims);
     if (c->ws) (void)hipFree(c->ws);
     if (c->h_stage) (void)hipHostFree(c->h_stage);
+    flush_profile(c);
+    for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
     delete c;
     return RA_OK;
 }
@@ -181,6 +287,28 @@ ra_status ra_ctx_cursor(const ra_ctx *c, uint64_t *consumed)
 {
     if (!c || !consumed) return RA_E_INVAL;
     *consumed = c->cursor;
+    return RA_OK;
+}
+
+ra_status ra_ctx_set_profiling(ra_ctx *c, int on)
+{
+    if (!c) return RA_E_INVAL;
+    RA_HIP(hipStreamSynchronize(c->stream));
+    flush_profile(c);
+    c->prof_on = on != 0;
+    for (int g = 0; g < G_COUNT; g++) {
+        c->prof_ms[g] = 0;
+        c->prof_n[g] = 0;
+    }
+    return RA_OK;
+}
+
+ra_status ra_ctx_profile(const ra_ctx *c, uint32_t index, const char **name, double *total_ms, uint64_t *launches)
+{
+    if (!c || index >= (uint32_t)G_COUNT) return RA_E_INVAL;
+    if (name) *name = kGroupName[index];
+    if (total_ms) *total_ms = c->prof_ms[index];
+    if (launches) *launches = c->prof_n[index];
     return RA_OK;
 }
 
@@ -231,9 +359,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
 
     ra_status st = ensure_eq(c, (size_t)n + k);
     if (st != RA_OK) return st;
-    const size_t cap = tail_capacity(2);
-    int nslots = 1;
-    for (size_t S = m; S > cap; S >>= 1) nslots++;
+    const int nslots = std::max(1, global_rounds(lm));
     const size_t trw = 3 + 3 * (size_t)lm;
     Carve cv;
     const size_t o_a = cv.take<uint64_t>(m), o_b = cv.take<uint64_t>(m);
@@ -247,29 +373,33 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     uint64_t *E1 = c->d_eq, *E2 = c->d_eq + n;
     hipStream_t s = c->stream;
 
-    launch_eq_table(r1, ln, E1, s);
-    launch_eq_table(r2, lk, E2, s);
-    launch_gemm_i64(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, s);
-    launch_bind_rows(d_A, a_dtype, n, m, E1, scr, a, s);
-    launch_bind_cols(d_B, RA_I16, m, k, E2, b, s);
+    {
+        Timed tm(c, G_EQ);
+        launch_eq_table(r1, ln, E1, s);
+        launch_eq_table(r2, lk, E2, s);
+    }
+    {
+        Timed tm(c, G_GEMM);
+        launch_gemm_i64(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, s);
+    }
+    {
+        Timed tm(c, G_BIND_ROWS);
+        launch_bind_rows(d_A, a_dtype, n, m, E1, scr, a, s);
+    }
+    {
+        Timed tm(c, G_BIND_COLS);
+        launch_bind_cols(d_B, RA_I16, m, k, E2, b, s);
+    }
 
     // transcript: [c0][evals 3 lm][a*][b*]
     SlotTable slots;
     slots.count = 0;
-    if (m > cap) {
-        launch_dot(a, b, m, part, s);
-        slots.s[slots.count++] = Slot{round_blocks(m), 1, 0, 2, 0};
-        int j = 0;
-        for (size_t S = m; S > cap; S >>= 1, j++) {
-            const uint64_t h = S / 2;
-            launch_round(KIND_MATMUL, a, b, nullptr, h, rho + j, nullptr, part + (size_t)slots.count * kPartStride, s);
-            slots.s[slots.count++] = Slot{round_blocks(h), 3, 1 + 3 * j, 0, 0};
-        }
-        launch_tail(KIND_MATMUL, a, b, nullptr, lm - j, rho + j, nullptr, tr + 1 + 3 * j, tr + 1 + 3 * lm, nullptr, s);
-    } else {
-        launch_tail(KIND_MATMUL, a, b, nullptr, lm, rho, nullptr, tr + 1, tr + 1 + 3 * lm, tr, s);
+    run_instance(c, KIND_MATMUL, a, b, nullptr, lm, rho, nullptr, tr, 1, 3, tr + 1 + 3 * lm, 0, slots, part,
+                 G_MM_ROUNDS, G_MM_TAIL);
+    {
+        Timed tm(c, G_ASSEMBLE);
+        launch_assemble(slots, part, kPartStride, tr, s);
     }
-    launch_assemble(slots, part, kPartStride, nullptr, 0, tr, s);
     if ((st = finish(c, tr, trw)) != RA_OK) return st;
 
     const uint64_t *h = c->h_stage;
@@ -302,9 +432,16 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
     const int lk = log2u(k);
-    launch_witness(d_C, N, lk, (int)io->s, (int)io->relu, (int)io->round_mode, io->t, c->d_eq, c->d_eq + n, d_R, d_Rm,
-                   d_Y, d_Z, d_bits, (int64_t *)(c->ws + o_mm), (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims,
-                   c->stream);
+    {
+        Timed tm(c, G_WIT_MINMAX);
+        launch_witness_params(d_C, N, (int)io->s, (int)io->relu, (int)io->round_mode, io->t,
+                              (int64_t *)(c->ws + o_mm), c->d_params, c->stream);
+    }
+    {
+        Timed tm(c, G_WIT_RESCALE);
+        launch_witness_rescale(d_C, N, lk, c->d_eq, c->d_eq + n, d_R, d_Rm, d_Y, d_Z, d_bits,
+                               (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims, c->stream);
+    }
     RA_HIP(hipGetLastError());
     WitParams prm;
     RA_HIP(hipMemcpyAsync(&prm, c->d_params, sizeof(prm), hipMemcpyDeviceToHost, c->stream));
@@ -342,12 +479,9 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     if (c->cursor + need > c->n_chal) return RA_E_CHALLENGES;
     const uint64_t *lam = c->d_chal + c->cursor, *sigma = lam + 4 + lP, *rho2 = sigma + R;
 
-    const size_t cap2 = tail_capacity(2), cap3 = tail_capacity(3);
-    int nslots = lP;
-    for (size_t S = N; S > cap2; S >>= 1) nslots++;
-    if (relu)
-        for (size_t S = N; S > cap3; S >>= 1) nslots++;
+    const int nslots = global_rounds(lN) * (relu ? 2 : 1);
     if (nslots > kMaxSlots) return RA_E_INVAL;
+    const int gtiles = plane_gram_tiles(lP), gblocks = plane_gram_blocks(N, lP);
     // transcript: [evals 4R][EQ fin][bits_claim][range_sum][relu evals 4 lN][EQ fin][r_at][y_at]
     const size_t F_R = 4 * (size_t)R, RS = F_R + 2, Z0 = F_R + 3, FZ = Z0 + 4 * (size_t)lN, trw = FZ + 3;
     Carve cv;
@@ -357,45 +491,48 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
                  o_yf = cv.take<uint64_t>(relu ? N : 1);
     const size_t o_part = cv.take<uint64_t>((size_t)std::max(nslots, 1) * kPartStride);
     const size_t o_tr = cv.take<uint64_t>(trw);
+    const size_t o_lut = cv.take<uint64_t>(8 * 256);
+    const size_t o_gp = cv.take<uint64_t>((size_t)gblocks * gtiles * 1024);
+    const size_t o_gs = cv.take<uint64_t>((size_t)kGramSlices * gtiles * 1024);
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
     if ((st = ensure_stage(c, trw)) != RA_OK) return st;
     uint64_t *cst = (uint64_t *)(c->ws + o_cst), *EQ = (uint64_t *)(c->ws + o_eq), *Bx = (uint64_t *)(c->ws + o_bx);
     uint64_t *EQ2 = (uint64_t *)(c->ws + o_eq2), *Rf = (uint64_t *)(c->ws + o_rf), *Yf = (uint64_t *)(c->ws + o_yf);
     uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = (uint64_t *)(c->ws + o_tr);
+    uint64_t *lut = (uint64_t *)(c->ws + o_lut), *gpart = (uint64_t *)(c->ws + o_gp), *gsum = (uint64_t *)(c->ws + o_gs);
     hipStream_t s = c->stream;
 
-    launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, s);
+    {
+        Timed tm(c, G_RANGE_SETUP);
+        launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, lut, s);
+    }
     SlotTable slots;
     slots.count = 0;
-    const int pnb = plane_blocks(N);
-    for (int j = 0; j < lP; j++) slots.s[slots.count++] = Slot{pnb, 6, 4 * j, 1, j + 1};
-    launch_plane_rounds(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, cst, sigma, EQ, relu ? EQ2 : nullptr, Bx, part, s);
-    {   // rounds over x of the range instance
-        int j = 0;
-        size_t S = N;
-        for (; S > cap2; S >>= 1, j++) {
-            const uint64_t h = S / 2;
-            launch_round(KIND_RANGE, EQ, Bx, nullptr, h, sigma + lP + j, cst + C_EP,
-                         part + (size_t)slots.count * kPartStride, s);
-            slots.s[slots.count++] = Slot{round_blocks(h), 4, 4 * (lP + j), 0, 0};
-        }
-        launch_tail(KIND_RANGE, EQ, Bx, nullptr, lN - j, sigma + lP + j, cst + C_EP, tr + 4 * (lP + j), tr + F_R,
-                    nullptr, s);
+    {   // plane rounds: Gram matrix on the matrix cores, EQ and Bx per output
+        Timed tm(c, G_RANGE_PLANE);
+        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, EQ, relu ? EQ2 : nullptr, Bx, gpart, gsum, s);
     }
+    {
+        Timed tm(c, G_ASSEMBLE);
+        launch_plane_assemble(lP, gsum, sigma, cst, tr, s);
+    }
+    // rounds over x of the range instance
+    run_instance(c, KIND_RANGE, EQ, Bx, nullptr, lN, sigma + lP, cst + C_EP, tr, 4 * lP, 4, tr + F_R, -1, slots, part,
+                 G_RANGE_ROUNDS, G_RANGE_TAIL);
     if (relu) {  // zero-check of Eq. (6) at (r1, r2)
-        launch_i32_to_field(d_R, N, Rf, s);
-        launch_i32_to_field(d_Y, N, Yf, s);
-        int j = 0;
-        size_t S = N;
-        for (; S > cap3; S >>= 1, j++) {
-            const uint64_t h = S / 2;
-            launch_round(KIND_RELU, EQ2, Rf, Yf, h, rho2 + j, nullptr, part + (size_t)slots.count * kPartStride, s);
-            slots.s[slots.count++] = Slot{round_blocks(h), 4, (int)Z0 + 4 * j, 0, 0};
+        {
+            Timed tm(c, G_RELU_FIELD);
+            launch_i32_to_field(d_R, N, Rf, s);
+            launch_i32_to_field(d_Y, N, Yf, s);
         }
-        launch_tail(KIND_RELU, EQ2, Rf, Yf, lN - j, rho2 + j, nullptr, tr + Z0 + 4 * j, tr + FZ, nullptr, s);
+        run_instance(c, KIND_RELU, EQ2, Rf, Yf, lN, rho2, nullptr, tr, (int)Z0, 4, tr + FZ, -1, slots, part,
+                     G_RELU_ROUNDS, G_RELU_TAIL);
     }
-    launch_assemble(slots, part, kPartStride, cst, lP, tr, s);
+    {
+        Timed tm(c, G_ASSEMBLE);
+        launch_assemble(slots, part, kPartStride, tr, s);
+    }
     if ((st = finish(c, tr, trw)) != RA_OK) return st;
 
     const uint64_t *h = c->h_stage;

@@ -8,9 +8,9 @@
 namespace ra {
 
 constexpr int kThreads = 256;          // block size of streaming kernels
-constexpr int kTailThreads = 1024;     // block size of the LDS tail kernel
+constexpr int kTailThreads = 256;      // block size of the LDS tail kernel
+constexpr int kTailMax = 1024;         // largest table the single-workgroup tail takes
 constexpr int kMaxBlocks = 1024;       // blocks of a grid-stride round kernel
-constexpr size_t kTailLdsBytes = 128 * 1024;  // LDS budget of the tail (160 KB per CU on gfx950)
 constexpr int kMaxSlots = 96;          // per-call partial-sum slots (rounds)
 constexpr int kMaxPlaneLog = 6;        // bit planes per output <= 64 (one word)
 
@@ -39,8 +39,9 @@ struct Slot {
     int32_t nblk;      // blocks that wrote partials
     int32_t width;     // words per block (d + 1, or 6 for a plane round)
     int32_t out;       // offset of the round's evaluations in the transcript buffer
-    int32_t kind;      // 0: plain sums -> evals; 1: plane round (combine with constants); 2: scalar sum
-    int32_t round;     // plane round index for kind 1
+    int32_t kind;      // reserved (0)
+    int32_t round;     // reserved (0)
+    int32_t sum_out;   // >= 0: also write g(0) + g(1) (the instance's claimed sum) there
 };
 struct SlotTable {
     int32_t count;
@@ -58,29 +59,41 @@ void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, co
 void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *out,
                       hipStream_t st);
 int witness_blocks(uint64_t N);
-void launch_witness(const int64_t *C, uint64_t N, int lk, int s, int relu, int mode, int t_in, const uint64_t *E1,
-                    const uint64_t *E2, int32_t *R, uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits,
-                    int64_t *mm_part, uint64_t *claim_part, WitParams *params, uint64_t *claims_out, hipStream_t st);
+void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mode, int t_in, int64_t *mm_part,
+                           WitParams *params, hipStream_t st);
+void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
+                            uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
+                            const WitParams *params, uint64_t *claims_out, hipStream_t st);
 
 // ---- launchers (sumcheck.hip) ----
 int round_blocks(uint64_t h);
 size_t tail_capacity(int ntab);  // largest 2^v table size the LDS tail holds
-void launch_round(int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t h, const uint64_t *rho,
-                  const uint64_t *kp, uint64_t *part, hipStream_t st);
+int fused_rounds_max(int kind);
+// C fused rounds over tables of size S (C <= fused_rounds_max); partials of
+// round r at part + r * stride
+void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t S, const uint64_t *rho,
+                   const uint64_t *kp, uint64_t *part, int stride, hipStream_t st);
 void launch_tail(int kind, const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
                  const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out, hipStream_t st);
-void launch_dot(const uint64_t *a, const uint64_t *b, uint64_t len, uint64_t *part, hipStream_t st);
 void launch_i32_to_field(const int32_t *src, uint64_t N, uint64_t *dst, hipStream_t st);
 // range constants: lambda/mu/tau_p/sigma_p at `chal`, claims from the witness
 size_t range_consts_words(int lP);
+// also writes the 8 x 256 byte tables of the plane-bound table Bx to lut
 void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,
-                        uint64_t *tr_range_sum, hipStream_t st);
-int plane_blocks(uint64_t N);
-void launch_plane_rounds(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                         const uint64_t *cst, const uint64_t *sigma, uint64_t *EQ, uint64_t *EQ2, uint64_t *Bx,
-                         uint64_t *part, hipStream_t st);
+                        uint64_t *tr_range_sum, uint64_t *lut, hipStream_t st);
 void init_kernel_attributes();
-void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, const uint64_t *cst, int lP,
-                     uint64_t *tr, hipStream_t st);
+void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, hipStream_t st);
+
+// ---- launchers (planes.hip) ----
+constexpr int kGramSlices = 8;
+int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
+int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
+// EQ, EQ2 (optional), Bx per x and the Gram matrix partials; gsum: kGramSlices * tiles * 1024 words
+void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
+                       const uint64_t *lut, uint64_t *EQ, uint64_t *EQ2, uint64_t *Bx, uint64_t *gpart,
+                       uint64_t *gsum, hipStream_t st);
+// round polynomials of the lP plane rounds into tr[0 .. 4 lP)
+void launch_plane_assemble(int lP, const uint64_t *gsum, const uint64_t *sigma, const uint64_t *cst, uint64_t *tr,
+                           hipStream_t st);
 
 }  // namespace ra

@@ -108,7 +108,7 @@ template <> __device__ __forceinline__ uint64_t term<int64_t>(uint64_t e, int64_
 }
 template <> __device__ __forceinline__ uint64_t term<uint64_t>(uint64_t e, uint64_t a) { return m61::mul(e, a); }
 
-constexpr uint32_t kBindRowsPerChunk = 64;
+constexpr uint32_t kBindRowsPerChunk = 8;
 
 int bind_rows_chunks(uint32_t rows) { return (int)((rows + kBindRowsPerChunk - 1) / kBindRowsPerChunk); }
 
@@ -222,14 +222,30 @@ __device__ __forceinline__ int64_t rescale(int64_t c, int s, int mode)
     return (c + half) >> s;  // arithmetic shift = floor division by 2^s
 }
 
-__global__ void k_wit_params(const int64_t *__restrict__ part, int nblk, int s, int relu, int mode, int t_in,
-                             WitParams *__restrict__ prm)
+__global__ __launch_bounds__(256) void k_wit_params(const int64_t *__restrict__ part, int nblk, int s, int relu,
+                                                    int mode, int t_in, WitParams *__restrict__ prm)
 {
-    if (threadIdx.x != 0) return;
+    __shared__ int64_t smin[4], smax[4];
     int64_t mn = INT64_MAX, mx = INT64_MIN;
-    for (int b = 0; b < nblk; b++) {
+    for (int b = threadIdx.x; b < nblk; b += blockDim.x) {
         mn = part[2 * b] < mn ? part[2 * b] : mn;
         mx = part[2 * b + 1] > mx ? part[2 * b + 1] : mx;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const int64_t a = __shfl_xor(mn, off, 64), b = __shfl_xor(mx, off, 64);
+        mn = a < mn ? a : mn;
+        mx = b > mx ? b : mx;
+    }
+    if ((threadIdx.x & 63) == 0) {
+        smin[threadIdx.x >> 6] = mn;
+        smax[threadIdx.x >> 6] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    for (int w = 1; w < (int)(blockDim.x >> 6); w++) {
+        mn = smin[w] < mn ? smin[w] : mn;
+        mx = smax[w] > mx ? smax[w] : mx;
     }
     WitParams p;
     p.status = 0;
@@ -318,17 +334,23 @@ __global__ __launch_bounds__(256) void k_claims_final(const uint64_t *__restrict
         for (int i = 0; i < 4; i++) out[i] = acc[i];
 }
 
-void launch_witness(const int64_t *C, uint64_t N, int lk, int s, int relu, int mode, int t_in, const uint64_t *E1,
-                    const uint64_t *E2, int32_t *R, uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits,
-                    int64_t *mm_part, uint64_t *claim_part, WitParams *params, uint64_t *claims_out, hipStream_t st)
+void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mode, int t_in, int64_t *mm_part,
+                           WitParams *params, hipStream_t st)
 {
     const int nb = witness_blocks(N);
     hipLaunchKernelGGL(k_minmax, dim3(nb), dim3(kThreads), 0, st, C, N, mm_part);
-    hipLaunchKernelGGL(k_wit_params, dim3(1), dim3(64), 0, st, (const int64_t *)mm_part, nb, s, relu, mode, t_in, params);
-    hipLaunchKernelGGL(k_rescale, dim3(nb), dim3(kThreads), 0, st, C, N, lk, (const WitParams *)params, E1, E2, R, Rm,
-                       Y, Z, bits, claim_part);
-    hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, (const uint64_t *)claim_part, nb,
-                       (const WitParams *)params, claims_out);
+    hipLaunchKernelGGL(k_wit_params, dim3(1), dim3(256), 0, st, (const int64_t *)mm_part, nb, s, relu, mode, t_in, params);
+}
+
+void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
+                            uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
+                            const WitParams *params, uint64_t *claims_out, hipStream_t st)
+{
+    const int nb = witness_blocks(N);
+    hipLaunchKernelGGL(k_rescale, dim3(nb), dim3(kThreads), 0, st, C, N, lk, params, E1, E2, R, Rm, Y, Z, bits,
+                       claim_part);
+    hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, (const uint64_t *)claim_part, nb, params,
+                       claims_out);
 }
 
 }  // namespace ra

@@ -23,7 +23,8 @@ RA_ROUND_NEAREST, RA_ROUND_FLOOR = 0, 1
 STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_FIELD_TOO_SMALL",
           -4: "RA_E_RANGE", -5: "RA_E_CHALLENGES", -6: "RA_E_HIP", -7: "RA_E_STATE",
           -8: "RA_E_BUFSIZE", -9: "RA_E_NOMEM"}
-EXPORTS = ["ra_ctx_create", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str", "ra_mle_bind",
+EXPORTS = ["ra_ctx_create", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str", "ra_ctx_set_profiling",
+           "ra_ctx_profile", "ra_mle_bind",
            "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify"]
 
 
@@ -82,6 +83,9 @@ def lib():
         L.ra_ctx_create.argtypes = [u64, u64p, u64, vp, ctypes.POINTER(vp)]
         L.ra_ctx_destroy.argtypes = [vp]
         L.ra_ctx_cursor.argtypes = [vp, u64p]
+        L.ra_ctx_set_profiling.argtypes = [vp, ctypes.c_int]
+        L.ra_ctx_profile.argtypes = [vp, ctypes.c_uint32, ctypes.POINTER(ctypes.c_char_p),
+                                     ctypes.POINTER(ctypes.c_double), u64p]
         L.ra_status_str.restype = ctypes.c_char_p
         L.ra_status_str.argtypes = [ctypes.c_int32]
         L.ra_mle_bind.argtypes = [vp, vp, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int, u64p,
@@ -95,7 +99,8 @@ def lib():
         L.ra_verify.argtypes = [u64, u64p, u64, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
                                 ctypes.POINTER(LayerTables), ctypes.POINTER(LayerTranscript),
                                 ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
-        for f in (L.ra_ctx_create, L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
+        for f in (L.ra_ctx_create, L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
+                  L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
                   L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify):
             f.restype = ctypes.c_int32
         _lib = L
@@ -141,6 +146,22 @@ class Context:
             self.close()
         except Exception:
             pass
+
+    def set_profiling(self, on: bool):
+        _check(lib().ra_ctx_set_profiling(self.h, int(bool(on))), "ra_ctx_set_profiling")
+
+    def profile(self):
+        """{group name: (total ms, launches)} accumulated since profiling was turned on."""
+        out = {}
+        i = 0
+        while True:
+            name = ctypes.c_char_p()
+            ms = ctypes.c_double()
+            cnt = u64()
+            if lib().ra_ctx_profile(self.h, i, ctypes.byref(name), ctypes.byref(ms), ctypes.byref(cnt)) != 0:
+                return out
+            out[name.value.decode()] = (float(ms.value), int(cnt.value))
+            i += 1
 
     def cursor(self):
         v = u64()
@@ -296,3 +317,4 @@ def ra_verify(challenges, layers):
     _check(lib().ra_verify(P61, cp, len(chal), nl, pubs, tabs, trs, ctypes.byref(verdict), ctypes.byref(failed)),
            "ra_verify")
     return int(verdict.value), int(failed.value)
+

@@ -78,7 +78,7 @@ def group_work(shapes, planes):
 
     for (n, m, k, ab, _, relu), P in zip(shapes, planes):
         N = n * k
-        add("gemm_i64", "alu", n * m * k, "Gimul")                    # one 32x32->64 MAC per (i, l, j)
+        add("gemm_mfma", "mfma", 2 * n * m * k, "GOP")                # 2 n m k integer ops (algorithmic)
         add("bind_rows", "hbm", n * m * ab + 8 * m, "GB")
         add("bind_cols", "hbm", m * k * 2 + 8 * m, "GB")
         add("witness_minmax", "hbm", 8 * N, "GB")

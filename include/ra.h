@@ -123,8 +123,9 @@ typedef struct {
  * (int64), draws r1, r2, binds A's rows at r1 and B's columns at r2 (Eq. (4))
  * and runs the degree-2 sum-check over l in {0,1}^(log m), drawing rho.
  *   d_A     n x m, RA_I16 or RA_I32 (layer input; later layers use the
- *           previous int32 output).  With RA_I32, m * 2^46 must not exceed
- *           2^62 (exactness of the int64 product), i.e. m <= 65536.
+ *           previous int32 output).  m <= 32768 (the product is formed
+ *           exactly from 8-bit limbs with int32 partial sums; beyond that
+ *           RA_E_INVAL).
  *   d_B     m x k int16 weights.
  *   d_C     out, n x k int64, the exact product.
  *   out     transcript; out->evals must hold 3 * log2(m) words.

@@ -113,7 +113,7 @@ enum Group {
     G_ASSEMBLE, G_COUNT
 };
 const char *const kGroupName[G_COUNT] = {
-    "eq_table", "gemm_i64", "bind_rows", "bind_cols", "matmul_rounds", "matmul_tail", "witness_minmax",
+    "eq_table", "gemm_mfma", "bind_rows", "bind_cols", "matmul_rounds", "matmul_tail", "witness_minmax",
     "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail", "relu_to_field",
     "relu_rounds", "relu_tail", "assemble"};
 
@@ -349,7 +349,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     if (!c || !d_A || !d_B || !d_C || !out) return RA_E_INVAL;
     if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k)) return RA_E_INVAL;
     if (a_dtype != RA_I16 && a_dtype != RA_I32) return RA_E_INVAL;
-    if (a_dtype == RA_I32 && m > 65536) return RA_E_INVAL;  // exact int64 product
+    if (m > kGemmMaxInner) return RA_E_INVAL;  // exactness of the limb products
     if (c->phase != 0) return RA_E_STATE;
     const int ln = log2u(n), lm = log2u(m), lk = log2u(k);
     if (lm && !out->evals) return RA_E_INVAL;
@@ -366,6 +366,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     const size_t o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n) * m);
     const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
     const size_t o_tr = cv.take<uint64_t>(trw);
+    const size_t o_gemm = cv.take<char>(gemm_workspace_bytes(a_dtype == RA_I32, n, m, k));
     if ((st = ensure_ws(c, cv.off)) != RA_OK) return st;
     if ((st = ensure_stage(c, trw)) != RA_OK) return st;
     uint64_t *a = (uint64_t *)(c->ws + o_a), *b = (uint64_t *)(c->ws + o_b);
@@ -380,7 +381,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     }
     {
         Timed tm(c, G_GEMM);
-        launch_gemm_i64(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, s);
+        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s);
     }
     {
         Timed tm(c, G_BIND_ROWS);

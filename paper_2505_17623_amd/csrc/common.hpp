@@ -50,8 +50,11 @@ struct SlotTable {
 
 // ---- launchers (witness.hip) ----
 void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st);
-void launch_gemm_i64(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
-                     hipStream_t st);
+// ---- launchers (gemm.hip) ----
+constexpr uint32_t kGemmMaxInner = 32768;  // exactness bound of the int32 limb accumulators
+size_t gemm_workspace_bytes(int a_is_i32, uint32_t n, uint32_t m, uint32_t k);
+void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
+                      void *ws, hipStream_t st);
 // rows binding: out[c] = sum_r E[r] T[r, c]; needs scratch of nchunks(rows) * cols words
 int bind_rows_chunks(uint32_t rows);
 void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,

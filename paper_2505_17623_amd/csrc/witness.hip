@@ -28,74 +28,6 @@ void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st)
 }
 
 // ---------------------------------------------------------------------------
-// Exact product C = A B (Alg. 1 step 2) with int64 accumulation.
-// 64x64 output tile per 256-thread block, 32-deep k slices staged in LDS;
-// thread (tx, ty) owns rows ty + 16 a and columns tx + 16 b, a, b < 4.
-// ---------------------------------------------------------------------------
-template <typename TA>
-__global__ __launch_bounds__(256) void k_gemm_i64(const TA *__restrict__ A, const int16_t *__restrict__ B,
-                                                  int64_t *__restrict__ C, uint32_t n, uint32_t m, uint32_t k)
-{
-    __shared__ int32_t As[32][65];
-    __shared__ int32_t Bs[32][65];
-    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    const uint32_t row0 = blockIdx.y * 64, col0 = blockIdx.x * 64;
-    int64_t acc[4][4];
-#pragma unroll
-    for (int a = 0; a < 4; a++)
-#pragma unroll
-        for (int b = 0; b < 4; b++) acc[a][b] = 0;
-
-    for (uint32_t k0 = 0; k0 < m; k0 += 32) {
-#pragma unroll
-        for (int q = 0; q < 8; q++) {
-            const int e = threadIdx.x + 256 * q;
-            const int r = e >> 5, c = e & 31;
-            const uint32_t gr = row0 + r, gc = k0 + c;
-            As[c][r] = (gr < n && gc < m) ? (int32_t)A[(size_t)gr * m + gc] : 0;
-        }
-#pragma unroll
-        for (int q = 0; q < 8; q++) {
-            const int e = threadIdx.x + 256 * q;
-            const int r = e >> 6, c = e & 63;
-            const uint32_t gr = k0 + r, gc = col0 + c;
-            Bs[r][c] = (gr < m && gc < k) ? (int32_t)B[(size_t)gr * k + gc] : 0;
-        }
-        __syncthreads();
-#pragma unroll 8
-        for (int kk = 0; kk < 32; kk++) {
-            int32_t av[4], bv[4];
-#pragma unroll
-            for (int a = 0; a < 4; a++) av[a] = As[kk][ty + 16 * a];
-#pragma unroll
-            for (int b = 0; b < 4; b++) bv[b] = Bs[kk][tx + 16 * b];
-#pragma unroll
-            for (int a = 0; a < 4; a++)
-#pragma unroll
-                for (int b = 0; b < 4; b++) acc[a][b] += (int64_t)av[a] * bv[b];
-        }
-        __syncthreads();
-    }
-#pragma unroll
-    for (int a = 0; a < 4; a++)
-#pragma unroll
-        for (int b = 0; b < 4; b++) {
-            const uint32_t r = row0 + ty + 16 * a, c = col0 + tx + 16 * b;
-            if (r < n && c < k) C[(size_t)r * k + c] = acc[a][b];
-        }
-}
-
-void launch_gemm_i64(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
-                     hipStream_t st)
-{
-    dim3 grid((k + 63) / 64, (n + 63) / 64);
-    if (a_is_i32)
-        hipLaunchKernelGGL(k_gemm_i64<int32_t>, grid, dim3(256), 0, st, (const int32_t *)A, B, C, n, m, k);
-    else
-        hipLaunchKernelGGL(k_gemm_i64<int16_t>, grid, dim3(256), 0, st, (const int16_t *)A, B, C, n, m, k);
-}
-
-// ---------------------------------------------------------------------------
 // Binding one side of a matrix with an eq table (Eq. (4): a~(r1, l) is the
 // r1-row combination of A, b~(l, r2) the r2-column combination of B).
 // ---------------------------------------------------------------------------

@@ -169,3 +169,29 @@ def test_gpu_transcripts_verify_both_ways(ra):
     assert ra.ra_verify(wl.challenges, layers) == (0, 0)
     layers[1]["transcript"] = dict(layers[1]["transcript"], bits_claim=(layers[1]["transcript"]["bits_claim"] + 1) % P61)
     assert ra.ra_verify(wl.challenges, layers)[0] != 0
+
+
+@pytest.mark.parametrize("a_dtype,n,m,k", [(np.int16, 64, 128, 64), (np.int32, 32, 256, 128),
+                                           (np.int32, 1, 64, 1), (np.int16, 128, 32768, 2)])
+def test_matmul_extreme_values(ra, a_dtype, n, m, k):
+    """Exact product and matrix sum-check at the edges of the limb split:
+    int32 inputs near +-2^31, int16 at -32768 / 32767, the largest inner
+    dimension (2^15), and tiles that are not full."""
+    rng = np.random.default_rng(n + m + k)
+    info = np.iinfo(a_dtype)
+    A = rng.integers(info.min, info.max, size=(n, m), dtype=np.int64, endpoint=True).astype(a_dtype)
+    B = rng.integers(-32768, 32767, size=(m, k), dtype=np.int64, endpoint=True).astype(np.int16)
+    A.flat[:4] = [info.min, info.max, -1, 0][:A.size]
+    B.flat[:4] = [-32768, 32767, -1, 0][:B.size]
+    if m == 32768:                      # worst case for the int32 limb accumulators
+        A[:, :] = info.min
+        B[:, 0] = -32768
+    chal = inputs.xorshift64_stream(555 + m, 512)
+    o = orc.prove_layer(A, B, 30, False, 0, chal)  # s = 30 keeps the oracle's t small; only C and the
+    ctx = ra.Context(chal)                          # matrix transcript are compared
+    C, mm = ra.ra_sumcheck_matmul_prove(ctx, torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
+    want = (A.astype(object) @ B.astype(object))
+    assert np.array_equal(C.cpu().numpy().astype(object), want)
+    assert np.array_equal(C.cpu().numpy(), o["C"])
+    for key in ("c0", "mm_evals", "a_star", "b_star"):
+        assert mm[key] == o[key], key

@@ -121,6 +121,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after the timed region, copy a MIB-sized device buffer once (a plain copy kernel "
+                         "of known size, to scale hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this prover runs on one GPU; --gpus {args.gpus} is not supported "
@@ -192,6 +195,14 @@ def main():
                 d["achieved"] = round(a / s_per / 1e9, 2)
                 d["unit"] = "GB/s" if b == "hbm" else "Gimul/s"
                 d["frac"] = round(d["achieved"] / (HBM_PEAK_GBS if b == "hbm" else IMUL_PEAK_G), 4)
+
+    if args.copy_calibration:
+        src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

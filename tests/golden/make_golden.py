@@ -1,0 +1,60 @@
+"""Writes tests/golden/full_cfg<N>.json: the CPU oracle's transcript of every
+layer of workload N at full size, with SHA-256 digests of the inputs and of
+every output table.  Calls only the oracle and the seeded input generator.
+
+    python tests/golden/make_golden.py [cfg ...]      (default: 1 2 3 4 5)
+
+Digest formats: C, R, Rm, Y, Z as little-endian int64 arrays in row-major
+order; the bit table as P x N bytes (0/1), plane-major; A and B as int64.
+"""
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+from oracle import oracle as orc  # noqa: E402
+from paper_2505_17623_amd import inputs  # noqa: E402
+
+TRANSCRIPT = ["t", "P", "c0", "mm_evals", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_claim",
+              "range_sum", "rs_evals", "bits_claim", "zc_evals", "r_at", "y_at", "challenges_used"]
+
+
+def digest(a) -> str:
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def digest_i64(a) -> str:
+    return digest(np.asarray(a).astype("<i8"))
+
+
+def main(cfgs):
+    orc.build(force=False)
+    for cfg in cfgs:
+        wl = inputs.workload(cfg, "full")
+        t0 = time.time()
+        res = orc.prove_network(wl)
+        layers = []
+        for li, r in enumerate(res):
+            layers.append(dict(
+                shape=[r["n"], r["m"], r["k"]], s=r["s"], relu=r["relu"], mode=r["mode"],
+                transcript={k: r[k] for k in TRANSCRIPT},
+                digests=dict(A=digest_i64(r["A"]), B=digest_i64(wl.layers[li].B), C=digest_i64(r["C"]),
+                             R=digest_i64(r["R"]), Rm=digest_i64(r["Rm"]), Y=digest_i64(r["Y"]),
+                             Z=digest_i64(r["Z"]), bits=digest(r["bits"].astype(np.uint8)))))
+        out = dict(workload=wl.name, config=cfg, oracle_seconds=round(time.time() - t0, 1), layers=layers,
+                   source="oracle/ra_oracle.c via tests/golden/make_golden.py")
+        path = os.path.join(HERE, f"full_cfg{cfg}.json")
+        with open(path, "w") as f:
+            json.dump(out, f, indent=1)
+        print(f"config {cfg}: {len(layers)} layers, oracle {out['oracle_seconds']} s -> {path}", flush=True)
+
+
+if __name__ == "__main__":
+    main([int(a) for a in sys.argv[1:]] or [1, 2, 3, 4, 5])

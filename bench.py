@@ -84,11 +84,11 @@ def group_work(shapes, planes):
         add("witness_minmax", "hbm", 8 * N, "GB")
         add("witness_rescale", "hbm", N * (8 + 4 + 2 + 4 + 4 + 8), "GB")  # C in; R, Rm, Y, Z, bits out
         add("range_plane", "hbm", N * (8 + 16 + 8 * relu), "GB")         # bits in; EQ, Bx (+EQ) out
-        add_instance(w, "range_rounds", N.bit_length() - 1, 2, 4)      # x rounds: EQ and Bx
+        add_instance(w, "range_rounds", N.bit_length() - 1, 2, 2)      # x rounds: EQ and Bx
         if relu:
             add("relu_to_field", "hbm", 24 * N, "GB")
-            add_instance(w, "relu_rounds", N.bit_length() - 1, 3, 3)
-        add_instance(w, "matmul_rounds", m.bit_length() - 1, 2, 4)
+            add_instance(w, "range_rounds", N.bit_length() - 1, 3, 2)  # ReLU rounds share the launches
+        add_instance(w, "matmul_rounds", m.bit_length() - 1, 2, 2)
     return w
 
 
@@ -137,7 +137,7 @@ def main():
     torch.cuda.set_device(0)
     wl = inputs.workload(args.config, "full")
     L = len(wl.layers)
-    steps_total = args.warmup + args.steps + 1
+    steps_total = args.warmup + 2 * args.steps + 1
     chal = inputs.xorshift64_stream(inputs.CHALLENGE_SEED_BASE + args.config,
                                     inputs.CHALLENGES_PER_LAYER * L * steps_total)
     dev = torch.device("cuda:0")
@@ -156,18 +156,25 @@ def main():
         print(f"# warmup step {i} done", file=sys.stderr, flush=True)
     planes = [tr["P"] for tr in first] if first else None
 
-    ctx.set_profiling(True)
+    # timed region: K steps, no instrumentation
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         out = ra.prove_network(ctx, wl, dev, X=X, Bs=Bs)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    prof = ctx.profile()
-    ctx.set_profiling(False)
     if planes is None:
         planes = [o["transcript"]["P"] for o in out]
     elapsed = t1 - t0
+    # the same K steps again with HIP events around every kernel group (recording
+    # events adds host work between launches, so this pass is not the one timed)
+    ctx.set_profiling(True)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        ra.prove_network(ctx, wl, dev, X=X, Bs=Bs)
+    torch.cuda.synchronize()
+    prof = ctx.profile()
+    ctx.set_profiling(False)
     ms_step = 1e3 * elapsed / args.steps
     el = elements_folded(shapes, planes)
     value = el * args.steps / elapsed

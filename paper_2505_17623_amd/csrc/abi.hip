@@ -324,7 +324,7 @@ ra_status ra_mle_bind(ra_ctx *c, const void *d_T, ra_dtype dtype, uint32_t rows,
     Carve cv;
     const size_t o_pt = cv.take<uint64_t>(std::max(v, 1));
     const size_t o_eq = cv.take<uint64_t>(1ull << v);
-    const size_t o_scr = cv.take<uint64_t>(bind_rows ? (size_t)bind_rows_chunks(rows) * cols : 1);
+    const size_t o_scr = cv.take<uint64_t>(bind_rows ? (size_t)bind_rows_chunks(rows, cols) * cols : 1);
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
     st = ensure_stage(c, std::max(v, 1));
@@ -363,7 +363,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     const size_t trw = 3 + 3 * (size_t)lm;
     Carve cv;
     const size_t o_a = cv.take<uint64_t>(m), o_b = cv.take<uint64_t>(m);
-    const size_t o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n) * m);
+    const size_t o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n, m) * m);
     const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
     const size_t o_tr = cv.take<uint64_t>(trw);
     const size_t o_gemm = cv.take<char>(gemm_workspace_bytes(a_dtype == RA_I32, n, m, k));
@@ -494,7 +494,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const size_t o_tr = cv.take<uint64_t>(trw);
     const size_t o_lut = cv.take<uint64_t>(8 * 256);
     const size_t o_gp = cv.take<uint64_t>((size_t)gblocks * gtiles * 1024);
-    const size_t o_gs = cv.take<uint64_t>((size_t)kGramSlices * gtiles * 1024);
+    const size_t o_gs = cv.take<uint64_t>(64 * 64);
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
     if ((st = ensure_stage(c, trw)) != RA_OK) return st;
@@ -518,17 +518,36 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
         Timed tm(c, G_ASSEMBLE);
         launch_plane_assemble(lP, gsum, sigma, cst, tr, s);
     }
-    // rounds over x of the range instance
-    run_instance(c, KIND_RANGE, EQ, Bx, nullptr, lN, sigma + lP, cst + C_EP, tr, 4 * lP, 4, tr + F_R, -1, slots, part,
-                 G_RANGE_ROUNDS, G_RANGE_TAIL);
-    if (relu) {  // zero-check of Eq. (6) at (r1, r2)
+    if (!relu) {  // rounds over x of the range instance
+        run_instance(c, KIND_RANGE, EQ, Bx, nullptr, lN, sigma + lP, cst + C_EP, tr, 4 * lP, 4, tr + F_R, -1, slots,
+                     part, G_RANGE_ROUNDS, G_RANGE_TAIL);
+    } else {  // and the ReLU zero-check of Eq. (6) at (r1, r2), same table size: shared launches
         {
             Timed tm(c, G_RELU_FIELD);
             launch_i32_to_field(d_R, N, Rf, s);
             launch_i32_to_field(d_Y, N, Yf, s);
         }
-        run_instance(c, KIND_RELU, EQ2, Rf, Yf, lN, rho2, nullptr, tr, (int)Z0, 4, tr + FZ, -1, slots, part,
-                     G_RELU_ROUNDS, G_RELU_TAIL);
+        const int lt = log2_tail(), cmax = std::min(fused_rounds_max(KIND_RANGE), fused_rounds_max(KIND_RELU));
+        int j = 0, lS = lN;
+        while (lS > lt) {
+            const int C = std::min(cmax, lS - lt);
+            const InstArgs ra_{EQ, Bx, nullptr, sigma + lP + j, cst + C_EP, part + (size_t)slots.count * kPartStride};
+            const InstArgs rz{EQ2, Rf, Yf, rho2 + j, nullptr, part + (size_t)(slots.count + C) * kPartStride};
+            {
+                Timed tm(c, G_RANGE_ROUNDS);
+                launch_rounds_range_relu(C, ra_, rz, 1ull << lS, kPartStride, s);
+            }
+            const int nb = round_blocks(1ull << (lS - C));
+            for (int r = 0; r < C; r++) slots.s[slots.count++] = Slot{nb, 4, 4 * (lP + j + r), 0, 0, -1};
+            for (int r = 0; r < C; r++) slots.s[slots.count++] = Slot{nb, 4, (int)Z0 + 4 * (j + r), 0, 0, -1};
+            lS -= C;
+            j += C;
+        }
+        Timed tm(c, G_RANGE_TAIL);
+        launch_tail_range_relu(make_tail_args(EQ, Bx, nullptr, lN - j, sigma + lP + j, cst + C_EP, tr + 4 * (lP + j),
+                                              tr + F_R, nullptr),
+                               make_tail_args(EQ2, Rf, Yf, lN - j, rho2 + j, nullptr, tr + Z0 + 4 * j, tr + FZ, nullptr),
+                               s);
     }
     {
         Timed tm(c, G_ASSEMBLE);

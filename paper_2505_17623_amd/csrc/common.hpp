@@ -9,7 +9,8 @@ namespace ra {
 
 constexpr int kThreads = 256;          // block size of streaming kernels
 constexpr int kTailThreads = 256;      // block size of the LDS tail kernel
-constexpr int kTailMax = 1024;         // largest table the single-workgroup tail takes
+constexpr int kTailMaxLog = 10;
+constexpr int kTailMax = 1 << kTailMaxLog;  // largest table the single-workgroup tail takes
 constexpr int kMaxBlocks = 1024;       // blocks of a grid-stride round kernel
 constexpr int kMaxSlots = 96;          // per-call partial-sum slots (rounds)
 constexpr int kMaxPlaneLog = 6;        // bit planes per output <= 64 (one word)
@@ -55,8 +56,8 @@ constexpr uint32_t kGemmMaxInner = 32768;  // exactness bound of the int32 limb 
 size_t gemm_workspace_bytes(int a_is_i32, uint32_t n, uint32_t m, uint32_t k);
 void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
                       void *ws, hipStream_t st);
-// rows binding: out[c] = sum_r E[r] T[r, c]; needs scratch of nchunks(rows) * cols words
-int bind_rows_chunks(uint32_t rows);
+// rows binding: out[c] = sum_r E[r] T[r, c]; needs scratch of bind_rows_chunks(rows, cols) * cols words
+int bind_rows_chunks(uint32_t rows, uint32_t cols);
 void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,
                       uint64_t *out, hipStream_t st);
 void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *out,
@@ -71,6 +72,24 @@ void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t
 // ---- launchers (sumcheck.hip) ----
 int round_blocks(uint64_t h);
 size_t tail_capacity(int ntab);  // largest 2^v table size the LDS tail holds
+// Arguments of one sum-check instance's global-round launch and of its tail.
+struct InstArgs {
+    uint64_t *t0, *t1, *t2;
+    const uint64_t *rho, *kp;
+    uint64_t *part;
+};
+struct TailArgs {
+    const uint64_t *t0, *t1, *t2;
+    int v;
+    const uint64_t *rho, *kp;
+    uint64_t *evals, *fin0, *fin1, *fin2, *sum_out;
+};
+TailArgs make_tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
+                        const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out);
+// the range and ReLU instances (same table size) in shared launches
+void launch_rounds_range_relu(int C, const InstArgs &range, const InstArgs &relu, uint64_t S, int stride,
+                              hipStream_t st);
+void launch_tail_range_relu(const TailArgs &range, const TailArgs &relu, hipStream_t st);
 int fused_rounds_max(int kind);
 // C fused rounds over tables of size S (C <= fused_rounds_max); partials of
 // round r at part + r * stride
@@ -88,10 +107,9 @@ void init_kernel_attributes();
 void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, hipStream_t st);
 
 // ---- launchers (planes.hip) ----
-constexpr int kGramSlices = 8;
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
-// EQ, EQ2 (optional), Bx per x and the Gram matrix partials; gsum: kGramSlices * tiles * 1024 words
+// EQ, EQ2 (optional), Bx per x and the Gram matrix G (gsum: 64 x 64 words)
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
                        const uint64_t *lut, uint64_t *EQ, uint64_t *EQ2, uint64_t *Bx, uint64_t *gpart,
                        uint64_t *gsum, hipStream_t st);

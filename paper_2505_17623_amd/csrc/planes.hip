@@ -25,7 +25,6 @@ namespace ra {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 constexpr int kLimbs = 9;    // 7-bit limbs of a field element (63 bits)
-constexpr int kSlices = kGramSlices;  // partial sums per Gram entry after the first reduction
 
 // Output fragment of v_mfma_i32_32x32x32_i8: lane l, register r holds
 // row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
@@ -69,13 +68,32 @@ __global__ __launch_bounds__(64 * TP) void k_plane_gram(const uint64_t *__restri
         for (int r = 0; r < 16; r++) acc[t][r] = 0;
     __syncthreads();
 
+    // the next chunk's word and eq factors are loaded one iteration ahead, so
+    // their latency overlaps the matrix-core work of the current chunk
+    uint64_t nw = 0, ne1 = 0, ne2 = 0;
+    {
+        const uint64_t x = (uint64_t)blockIdx.x * NX + tid;
+        if (x < N) {
+            nw = bits[x];
+            ne1 = E1[x >> lk];
+            ne2 = E2[x & kmask];
+        }
+    }
     for (uint64_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
         const uint64_t x = ch * NX + tid;
         const bool valid = x < N;
-        uint64_t w = 0, eqx = 0;
+        const uint64_t w = nw, e1 = ne1, e2 = ne2;
+        {
+            const uint64_t xn = (ch + gridDim.x) * NX + tid;
+            if (xn < N) {
+                nw = bits[xn];
+                ne1 = E1[xn >> lk];
+                ne2 = E2[xn & kmask];
+            }
+        }
+        uint64_t eqx = 0;
         if (valid) {
-            w = bits[x];
-            eqx = m61::mul(E1[x >> lk], E2[x & kmask]);
+            eqx = m61::mul(e1, e2);
             EQ[x] = eqx;
             if (EQ2) EQ2[x] = eqx;
         }
@@ -134,105 +152,114 @@ __global__ __launch_bounds__(64 * TP) void k_plane_gram(const uint64_t *__restri
     }
 }
 
-// First reduction: gsum[slice][e] = sum of the partial tiles of the blocks in slice.
-__global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict__ gpart, int nblk, int entries,
-                                                     uint64_t *__restrict__ gsum)
+// Sum of the blocks' partial tiles, written as G[q][q'] (64 x 64, both
+// triangles).  Each block covers 64 tile entries; its four waves split the
+// partial blocks and combine through LDS.
+__global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict__ gpart, int nblk, int TP,
+                                                     uint64_t *__restrict__ G)
 {
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= entries) return;
-    const int sl = blockIdx.y, per = (nblk + kSlices - 1) / kSlices;
-    const int b0 = sl * per, b1 = b0 + per < nblk ? b0 + per : nblk;
-    uint64_t acc = 0;
-    for (int b = b0; b < b1; b++) acc = m61::add(acc, gpart[(size_t)b * entries + e]);
-    gsum[(size_t)sl * entries + e] = acc;
+    __shared__ uint64_t red[4][64];
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, entries = TP * 1024;
+    const int e = blockIdx.x * 64 + lane;
+    uint64_t a[4] = {0, 0, 0, 0};
+    int b = wid;
+    for (; b + 12 < nblk; b += 16)
+#pragma unroll
+        for (int u = 0; u < 4; u++) a[u] = m61::add(a[u], gpart[(size_t)(b + 4 * u) * entries + e]);
+    for (; b < nblk; b += 4) a[0] = m61::add(a[0], gpart[(size_t)b * entries + e]);
+    red[wid][lane] = m61::add(m61::add(a[0], a[1]), m61::add(a[2], a[3]));
+    __syncthreads();
+    if (wid != 0) return;
+    const uint64_t v = m61::add(m61::add(red[0][lane], red[1][lane]), m61::add(red[2][lane], red[3][lane]));
+    const int tp = e >> 10, l = (e & 1023) >> 4, r = e & 15;
+    const int q = 32 * tile_row(tp, TP) + frag_row(l, r), q2 = 32 * tile_col(tp, TP) + (l & 31);
+    G[q * 64 + q2] = v;
+    G[q2 * 64 + q] = v;  // symmetric (the same value when the tile is diagonal)
 }
 
-// Round polynomials of the plane rounds from G.  One block of 256 threads.
-// cst: the constant block of the range check (e_j, W_j, w2_j, K_j, tau_j, mu).
-__global__ __launch_bounds__(256) void k_plane_assemble(const uint64_t *__restrict__ gsum, int TP, int lP,
+// Round polynomials of the plane rounds from G.  One block of 256 threads;
+// the rounds are independent given G, so all of them are evaluated at once.
+// For round j (ny = 2^(j-1) bound-variable patterns y, np = P / 2^j suffixes p'):
+//   Q_ab(p') = sum_{y,y'} c_y c_y' G[(y,a,p')][(y',b,p')],  L_a(p') = sum_y c_y G[(y,a,p')][(y,a,p')],
+// giving sum_x EQ b_a b_b and sum_x EQ b_a; b_2 = 2 b_1 - b_0 is extrapolated.
+__global__ __launch_bounds__(256) void k_plane_assemble(const uint64_t *__restrict__ Gg, int lP,
                                                         const uint64_t *__restrict__ sigma,
                                                         const uint64_t *__restrict__ cst, uint64_t *__restrict__ tr)
 {
     __shared__ uint64_t G[64][65];
-    __shared__ uint64_t c[32];
-    __shared__ uint64_t part[3 * 32 * 33];  // [combo][p'][y] quadratic-form partials; p' < 32, y < 32
-    __shared__ uint64_t lin[2][32];
-    __shared__ uint64_t contrib[32][6];
-    const int tid = threadIdx.x, P = 1 << lP;
-    for (int i = tid; i < 64 * 65; i += blockDim.x) (&G[0][0])[i] = 0;
-    __syncthreads();
-    for (int idx = tid; idx < TP * 1024; idx += blockDim.x) {
-        uint64_t v = 0;
-        for (int sl = 0; sl < kSlices; sl++) v = m61::add(v, gsum[(size_t)sl * TP * 1024 + idx]);
-        const int tp = idx >> 10, e = idx & 1023, l = e >> 4, r = e & 15;
-        const int q = 32 * tile_row(tp, TP) + frag_row(l, r), q2 = 32 * tile_col(tp, TP) + (l & 31);
-        G[q][q2] = v;
-        G[q2][q] = v;  // symmetric (same value when the tile is diagonal)
+    __shared__ uint64_t c[64];              // round j's c_y at (1 << (j - 1)) - 1 + y
+    __shared__ uint64_t part[6][96];        // [j][(combo np + p') ny + y]
+    __shared__ uint64_t lin[6][64];         // [j][a np + p']
+    __shared__ uint64_t contrib[6][32][6];  // [j][p'][A0 A1 A2 B0 B1 B2]
+    const int tid = threadIdx.x, P = 1 << lP, nf = 3 * (P / 2);
+    for (int i = tid; i < P * P; i += blockDim.x) G[i / P][i % P] = Gg[(i / P) * 64 + (i % P)];
+    for (int i = tid; i < P - 1; i += blockDim.x) {
+        int j = 1;
+        while (i >= (1 << j) - 1) j++;
+        const int y = i - ((1 << (j - 1)) - 1);
+        uint64_t a = 1;
+        for (int k = 0; k < j - 1; k++) a = m61::mul(a, m61::eq1_bit(sigma[k], (y >> (j - 2 - k)) & 1));
+        c[i] = a;
     }
     __syncthreads();
-    for (int j = 1; j <= lP; j++) {
-        const int ny = 1 << (j - 1), np = P >> j, lo = lP - j;  // y count, p' count, low bits below X
-        if (tid < ny) {  // c_y = eq(sigma_<j, y)
-            uint64_t a = 1;
-            for (int i = 0; i < j - 1; i++) a = m61::mul(a, m61::eq1_bit(sigma[i], (tid >> (j - 2 - i)) & 1));
-            c[tid] = a;
+    for (int t = tid; t < lP * nf; t += blockDim.x) {
+        const int j = t / nf + 1, r = t % nf, ny = 1 << (j - 1), np = P >> j, lo = lP - j;
+        const int combo = r / (np * ny), rem = r % (np * ny), p = rem / ny, y = rem % ny;
+        const int xa = combo == 1 ? 1 : 0, xb = combo == 0 ? 0 : 1;
+        const uint64_t *cj = c + (ny - 1);
+        const int qa = (y << (lo + 1)) | (xa << lo) | p;
+        uint64_t sacc = 0;
+        for (int y2 = 0; y2 < ny; y2++) sacc = m61::add(sacc, m61::mul(cj[y2], G[qa][(y2 << (lo + 1)) | (xb << lo) | p]));
+        part[j - 1][r] = m61::mul(cj[y], sacc);
+    }
+    for (int t = tid; t < lP * P; t += blockDim.x) {
+        const int j = t / P + 1, r = t % P, ny = 1 << (j - 1), np = P >> j, lo = lP - j;
+        if (r >= 2 * np) continue;
+        const int xa = r / np, p = r % np;
+        const uint64_t *cj = c + (ny - 1);
+        uint64_t sacc = 0;
+        for (int y = 0; y < ny; y++) {
+            const int q = (y << (lo + 1)) | (xa << lo) | p;
+            sacc = m61::add(sacc, m61::mul(cj[y], G[q][q]));
         }
-        __syncthreads();
-        // quadratic forms: combos (X, X') = (0,0), (1,1), (0,1)
-        for (int idx = tid; idx < 3 * np * ny; idx += blockDim.x) {
-            const int combo = idx / (np * ny), rem = idx % (np * ny), p = rem / ny, y = rem % ny;
-            const int Xa = combo == 1 ? 1 : 0, Xb = combo == 0 ? 0 : 1;
-            const int qa = (y << (lo + 1)) | (Xa << lo) | p;
-            uint64_t s = 0;
-            for (int y2 = 0; y2 < ny; y2++) s = m61::add(s, m61::mul(c[y2], G[qa][(y2 << (lo + 1)) | (Xb << lo) | p]));
-            part[(combo * 32 + p) * 33 + y] = m61::mul(c[y], s);
-        }
-        for (int idx = tid; idx < 2 * np; idx += blockDim.x) {  // linear terms L_X(p') from the diagonal
-            const int X = idx / np, p = idx % np;
-            uint64_t s = 0;
-            for (int y = 0; y < ny; y++) {
-                const int q = (y << (lo + 1)) | (X << lo) | p;
-                s = m61::add(s, m61::mul(c[y], G[q][q]));
+        lin[j - 1][r] = sacc;
+    }
+    __syncthreads();
+    for (int t = tid; t < lP * 32; t += blockDim.x) {
+        const int j = t / 32 + 1, p = t % 32, ny = 1 << (j - 1), np = P >> j;
+        if (p >= np) continue;
+        uint64_t Q[3] = {0, 0, 0};
+        for (int combo = 0; combo < 3; combo++)
+            for (int y = 0; y < ny; y++) Q[combo] = m61::add(Q[combo], part[j - 1][(combo * np + p) * ny + y]);
+        const uint64_t L0 = lin[j - 1][p], L1 = lin[j - 1][np + p];
+        const uint64_t Q2 = m61::add(m61::sub(m61::mul(4, Q[1]), m61::mul(4, Q[2])), Q[0]);
+        const uint64_t L2 = m61::sub(m61::add(L1, L1), L0);
+        const int oh = P - (P >> (j - 1));
+        const uint64_t e = cst[C_E + oh + p], w2 = cst[C_W2 + oh + p];
+        const uint64_t *Wj = cst + C_W + (2 * P - 2 * (P >> (j - 1)));
+        uint64_t *o = contrib[j - 1][p];
+        o[0] = m61::mul(e, m61::sub(Q[0], L0));
+        o[1] = m61::mul(e, m61::sub(Q[1], L1));
+        o[2] = m61::mul(e, m61::sub(Q2, L2));
+        o[3] = m61::mul(Wj[p], L0);
+        o[4] = m61::mul(Wj[p + np], L1);
+        o[5] = m61::mul(w2, L2);
+    }
+    __syncthreads();
+    if (tid < lP) {
+        const int j = tid + 1, np = P >> j;
+        uint64_t A[4] = {0, 0, 0, 0}, B[4] = {0, 0, 0, 0};
+        for (int p = 0; p < np; p++)
+            for (int X = 0; X < 3; X++) {
+                A[X] = m61::add(A[X], contrib[j - 1][p][X]);
+                B[X] = m61::add(B[X], contrib[j - 1][p][3 + X]);
             }
-            lin[X][p] = s;
-        }
-        __syncthreads();
-        if (tid < np) {
-            const int p = tid;
-            uint64_t Q[3] = {0, 0, 0};
-            for (int combo = 0; combo < 3; combo++)
-                for (int y = 0; y < ny; y++) Q[combo] = m61::add(Q[combo], part[(combo * 32 + p) * 33 + y]);
-            const uint64_t L0 = lin[0][p], L1 = lin[1][p];
-            // b_2 = 2 b_1 - b_0
-            const uint64_t Q2 = m61::add(m61::sub(m61::mul(4, Q[1]), m61::mul(4, Q[2])), Q[0]);
-            const uint64_t L2 = m61::sub(m61::add(L1, L1), L0);
-            const uint64_t e = cst[C_E + (P - (P >> (j - 1))) + p];
-            const uint64_t *Wj = cst + C_W + (2 * P - 2 * (P >> (j - 1)));
-            const uint64_t w2 = cst[C_W2 + (P - (P >> (j - 1))) + p];
-            contrib[p][0] = m61::mul(e, m61::sub(Q[0], L0));
-            contrib[p][1] = m61::mul(e, m61::sub(Q[1], L1));
-            contrib[p][2] = m61::mul(e, m61::sub(Q2, L2));
-            contrib[p][3] = m61::mul(Wj[p], L0);
-            contrib[p][4] = m61::mul(Wj[p + np], L1);
-            contrib[p][5] = m61::mul(w2, L2);
-        }
-        __syncthreads();
-        if (tid == 0) {
-            uint64_t A[4] = {0, 0, 0, 0}, B[4] = {0, 0, 0, 0};
-            for (int p = 0; p < np; p++)
-                for (int X = 0; X < 3; X++) {
-                    A[X] = m61::add(A[X], contrib[p][X]);
-                    B[X] = m61::add(B[X], contrib[p][3 + X]);
-                }
-            // quadratic extension to X = 3: f(3) = f(0) + 3 (f(2) - f(1))
-            A[3] = m61::add(A[0], m61::mul(3, m61::sub(A[2], A[1])));
-            B[3] = m61::add(B[0], m61::mul(3, m61::sub(B[2], B[1])));
-            const uint64_t K = cst[C_K + j - 1], tau = cst[C_TAU + j - 1], mu = cst[C_EP + 3];
-            for (int X = 0; X < 4; X++)
-                tr[4 * (j - 1) + X] =
-                    m61::add(m61::mul(m61::mul(K, m61::eq1_small(tau, X)), A[X]), m61::mul(mu, B[X]));
-        }
-        __syncthreads();
+        // quadratic extension to X = 3: f(3) = f(0) + 3 (f(2) - f(1))
+        A[3] = m61::add(A[0], m61::mul(3, m61::sub(A[2], A[1])));
+        B[3] = m61::add(B[0], m61::mul(3, m61::sub(B[2], B[1])));
+        const uint64_t K = cst[C_K + j - 1], tau = cst[C_TAU + j - 1], mu = cst[C_EP + 3];
+        for (int X = 0; X < 4; X++)
+            tr[4 * (j - 1) + X] = m61::add(m61::mul(m61::mul(K, m61::eq1_small(tau, X)), A[X]), m61::mul(mu, B[X]));
     }
 }
 
@@ -242,7 +269,7 @@ int plane_gram_blocks(uint64_t N, int lP)
 {
     const int TP = plane_gram_tiles(lP);
     const uint64_t chunks = (N + 64 * TP - 1) / (64 * TP);
-    return (int)(chunks < 512 ? chunks : 512);
+    return (int)(chunks < 256 ? chunks : 256);
 }
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
@@ -254,15 +281,13 @@ void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const u
         hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(64), 0, st, bits, N, lk, E1, E2, lut, EQ, EQ2, Bx, gpart);
     else
         hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(192), 0, st, bits, N, lk, E1, E2, lut, EQ, EQ2, Bx, gpart);
-    const int entries = TP * 1024;
-    hipLaunchKernelGGL(k_gram_reduce, dim3(entries / 256, kSlices), dim3(256), 0, st, (const uint64_t *)gpart, nb,
-                       entries, gsum);
+    hipLaunchKernelGGL(k_gram_reduce, dim3(TP * 16), dim3(256), 0, st, (const uint64_t *)gpart, nb, TP, gsum);
 }
 
 void launch_plane_assemble(int lP, const uint64_t *gsum, const uint64_t *sigma, const uint64_t *cst, uint64_t *tr,
                            hipStream_t st)
 {
-    hipLaunchKernelGGL(k_plane_assemble, dim3(1), dim3(256), 0, st, gsum, plane_gram_tiles(lP), lP, sigma, cst, tr);
+    hipLaunchKernelGGL(k_plane_assemble, dim3(1), dim3(256), 0, st, gsum, lP, sigma, cst, tr);
 }
 
 }  // namespace ra

@@ -63,22 +63,19 @@ __device__ __forceinline__ void pair_contrib(const uint64_t (&lo)[3], const uint
 // thread reads below S').  Partials of round r go to part + r * stride.
 // ---------------------------------------------------------------------------
 template <int KIND, int C>
-__global__ __launch_bounds__(256) void k_rounds(uint64_t *__restrict__ t0, uint64_t *__restrict__ t1,
-                                                uint64_t *__restrict__ t2, uint64_t sub,
-                                                const uint64_t *__restrict__ rho, const uint64_t *__restrict__ kp,
-                                                uint64_t *__restrict__ part, int stride)
+__device__ __forceinline__ void rounds_body(const InstArgs &in, uint64_t sub, int blk, int nblk, int stride,
+                                            uint64_t *red)
 {
     constexpr int NT = KindTraits<KIND>::NT, D = KindTraits<KIND>::D, L = 1 << C;
-    __shared__ uint64_t red[4 * C * 4];
-    const uint64_t ep = KIND == KIND_RANGE ? kp[0] : 0, cc = KIND == KIND_RANGE ? kp[1] : 0;
+    const uint64_t ep = KIND == KIND_RANGE ? in.kp[0] : 0, cc = KIND == KIND_RANGE ? in.kp[1] : 0;
     uint64_t r[C];
 #pragma unroll
-    for (int c = 0; c < C; c++) r[c] = rho[c];
-    uint64_t *T[3] = {t0, t1, t2};
+    for (int c = 0; c < C; c++) r[c] = in.rho[c];
+    uint64_t *T[3] = {in.t0, in.t1, in.t2};
     uint64_t acc[C * 4];
 #pragma unroll
     for (int i = 0; i < C * 4; i++) acc[i] = 0;
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < sub; i += (uint64_t)gridDim.x * blockDim.x) {
+    for (uint64_t i = (uint64_t)blk * blockDim.x + threadIdx.x; i < sub; i += (uint64_t)nblk * blockDim.x) {
         uint64_t v[3][L];
 #pragma unroll
         for (int q = 0; q < NT; q++)
@@ -111,7 +108,35 @@ __global__ __launch_bounds__(256) void k_rounds(uint64_t *__restrict__ t0, uint6
 #pragma unroll
         for (int c = 0; c < C; c++)
 #pragma unroll
-            for (int X = 0; X <= D; X++) part[(size_t)c * stride + (size_t)blockIdx.x * (D + 1) + X] = acc[4 * c + X];
+            for (int X = 0; X <= D; X++) in.part[(size_t)c * stride + (size_t)blk * (D + 1) + X] = acc[4 * c + X];
+}
+
+// ---------------------------------------------------------------------------
+// C consecutive rounds over tables in global memory, fused.  With S the
+// current table size and S' = S / 2^C, thread i loads the 2^C entries
+// i + t S' (t < 2^C) of every table -- the sub-cube of the C variables about
+// to be bound -- and runs the C rounds on them in registers: round r pairs
+// local entries (u, u + 2^(C-1-r)), which are exactly the global pairs of
+// that round.  It then writes the bound value to T[i] (i < S'; no other
+// thread reads below S').  Partials of round r go to part + r * stride.
+// ---------------------------------------------------------------------------
+template <int KIND, int C>
+__global__ __launch_bounds__(256) void k_rounds(InstArgs a, uint64_t sub, int stride)
+{
+    __shared__ uint64_t red[4 * C * 4];
+    rounds_body<KIND, C>(a, sub, blockIdx.x, gridDim.x, stride, red);
+}
+
+// Two independent instances over tables of the same size in one launch:
+// blocks [0, nbA) run instance a, the rest instance b.
+template <int KA, int KB, int C>
+__global__ __launch_bounds__(256) void k_rounds2(InstArgs a, InstArgs b, uint64_t sub, int nbA, int stride)
+{
+    __shared__ uint64_t red[4 * C * 4];
+    if ((int)blockIdx.x < nbA)
+        rounds_body<KA, C>(a, sub, blockIdx.x, nbA, stride, red);
+    else
+        rounds_body<KB, C>(b, sub, blockIdx.x - nbA, gridDim.x - nbA, stride, red);
 }
 
 int round_blocks(uint64_t h)
@@ -120,34 +145,42 @@ int round_blocks(uint64_t h)
     return (int)(b < (uint64_t)kMaxBlocks ? (b ? b : 1) : (uint64_t)kMaxBlocks);
 }
 
-int fused_rounds_max(int kind) { return kind == KIND_RELU ? 3 : 4; }
+int fused_rounds_max(int kind) { return kind == KIND_RELU ? 2 : 2; }
 
 void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t S, const uint64_t *rho,
                    const uint64_t *kp, uint64_t *part, int stride, hipStream_t st)
 {
     const uint64_t sub = S >> C;
     const int nb = round_blocks(sub);
-#define RA_ROUNDS(K, CC) hipLaunchKernelGGL((k_rounds<K, CC>), dim3(nb), dim3(kThreads), 0, st, t0, t1, t2, sub, rho, kp, part, stride)
-#define RA_ROUNDS_K(K)                 \
-    switch (C) {                       \
-    case 1: RA_ROUNDS(K, 1); break;    \
-    case 2: RA_ROUNDS(K, 2); break;    \
-    case 3: RA_ROUNDS(K, 3); break;    \
-    default: RA_ROUNDS(K, 4); break;   \
+    const InstArgs a{t0, t1, t2, rho, kp, part};
+#define RA_ROUNDS(K, CC) hipLaunchKernelGGL((k_rounds<K, CC>), dim3(nb), dim3(kThreads), 0, st, a, sub, stride)
+#define RA_ROUNDS_K(K)               \
+    switch (C) {                     \
+    case 1: RA_ROUNDS(K, 1); break;  \
+    case 2: RA_ROUNDS(K, 2); break;  \
+    case 3: RA_ROUNDS(K, 3); break;  \
+    default: RA_ROUNDS(K, 4); break; \
     }
     switch (kind) {
     case KIND_MATMUL: RA_ROUNDS_K(KIND_MATMUL) break;
     case KIND_RANGE: RA_ROUNDS_K(KIND_RANGE) break;
-    default:
-        switch (C) {
-        case 1: RA_ROUNDS(KIND_RELU, 1); break;
-        case 2: RA_ROUNDS(KIND_RELU, 2); break;
-        default: RA_ROUNDS(KIND_RELU, 3); break;
-        }
-        break;
+    default: RA_ROUNDS_K(KIND_RELU) break;
     }
 #undef RA_ROUNDS_K
 #undef RA_ROUNDS
+}
+
+void launch_rounds_range_relu(int C, const InstArgs &range, const InstArgs &relu, uint64_t S, int stride,
+                              hipStream_t st)
+{
+    const uint64_t sub = S >> C;
+    const int nb = round_blocks(sub);
+    switch (C) {
+    case 1: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 1>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
+    case 2: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 2>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
+    case 3: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 3>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
+    default: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 4>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -156,28 +189,24 @@ void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, ui
 // sum_out is set) the hypercube sum of the summand before the first round.
 // ---------------------------------------------------------------------------
 template <int KIND>
-__global__ __launch_bounds__(256) void k_tail(const uint64_t *__restrict__ t0, const uint64_t *__restrict__ t1,
-                                              const uint64_t *__restrict__ t2, int v, const uint64_t *__restrict__ rho,
-                                              const uint64_t *__restrict__ kp, uint64_t *__restrict__ evals,
-                                              uint64_t *fin0, uint64_t *fin1, uint64_t *fin2, uint64_t *sum_out)
+__device__ __forceinline__ void tail_body(const TailArgs &in, uint64_t *sm, uint64_t (*pacc)[4][kTailThreads])
 {
     constexpr int NT = KindTraits<KIND>::NT, D = KindTraits<KIND>::D;
-    __shared__ uint64_t sm[3 * kTailMax];
-    __shared__ uint64_t red[4 * 4];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, v = in.v;
     const uint32_t S = 1u << v;
     uint64_t *T[3] = {sm, sm + kTailMax, sm + 2 * kTailMax};
-    const uint64_t *G[3] = {t0, t1, t2};
-    for (uint32_t i = threadIdx.x; i < S; i += blockDim.x)
+    const uint64_t *G[3] = {in.t0, in.t1, in.t2};
+    for (uint32_t i = tid; i < S; i += blockDim.x)
 #pragma unroll
         for (int q = 0; q < NT; q++) T[q][i] = G[q][i];
     __syncthreads();
-    const uint64_t ep = KIND == KIND_RANGE ? kp[0] : 0, cc = KIND == KIND_RANGE ? kp[1] : 0;
-    if (v == 0 && sum_out && threadIdx.x == 0) *sum_out = m61::mul(T[0][0], T[1][0]);  // no rounds: the sum is a b
+    const uint64_t ep = KIND == KIND_RANGE ? in.kp[0] : 0, cc = KIND == KIND_RANGE ? in.kp[1] : 0;
+    if (v == 0 && in.sum_out && tid == 0) *in.sum_out = m61::mul(T[0][0], T[1][0]);  // no rounds: the sum is a b
     for (int j = 0; j < v; j++) {
         const uint32_t h = S >> (j + 1);
-        const uint64_t r = rho[j];
+        const uint64_t r = in.rho[j];
         uint64_t acc[4] = {0, 0, 0, 0};
-        for (uint32_t i = threadIdx.x; i < h; i += blockDim.x) {
+        for (uint32_t i = tid; i < h; i += blockDim.x) {
             uint64_t lo[3] = {0, 0, 0}, hi[3] = {0, 0, 0};
 #pragma unroll
             for (int q = 0; q < NT; q++) {
@@ -188,32 +217,82 @@ __global__ __launch_bounds__(256) void k_tail(const uint64_t *__restrict__ t0, c
 #pragma unroll
             for (int q = 0; q < NT; q++) T[q][i] = m61::add(lo[q], m61::mul(r, m61::sub(hi[q], lo[q])));
         }
-        m61::block_sum<4>(acc, red);  // ends with a barrier: folds are visible to the next round
-        if (threadIdx.x == 0) {
 #pragma unroll
-            for (int X = 0; X <= D; X++) evals[(size_t)j * (D + 1) + X] = acc[X];
-            if (j == 0 && sum_out) *sum_out = m61::add(acc[0], acc[1]);  // claimed sum = g_1(0) + g_1(1)
+        for (int X = 0; X <= D; X++) pacc[j][X][tid] = acc[X];
+        __syncthreads();  // folds of round j visible to round j + 1
+    }
+    // per-thread partial sums of every round, reduced once after the last
+    // round (the challenges are known, so no round waits for earlier sums)
+    for (int j = wid; j < v; j += blockDim.x / 64) {
+        uint64_t e[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int X = 0; X <= D; X++) {
+            uint64_t a = 0;
+            for (int t = lane; t < kTailThreads; t += 64) a = m61::add(a, pacc[j][X][t]);
+            e[X] = m61::wave_sum(a);
+        }
+        if (lane == 0) {
+#pragma unroll
+            for (int X = 0; X <= D; X++) in.evals[(size_t)j * (D + 1) + X] = e[X];
+            if (j == 0 && in.sum_out) *in.sum_out = m61::add(e[0], e[1]);  // claimed sum = g_1(0) + g_1(1)
         }
     }
-    if (threadIdx.x == 0) {
-        if (fin0) *fin0 = T[0][0];
-        if (fin1) *fin1 = T[1][0];
-        if (NT > 2 && fin2) *fin2 = T[2][0];
+    if (tid == 0) {
+        if (in.fin0) *in.fin0 = T[0][0];
+        if (in.fin1) *in.fin1 = T[1][0];
+        if (NT > 2 && in.fin2) *in.fin2 = T[2][0];
     }
+}
+
+template <int KIND>
+__global__ __launch_bounds__(256) void k_tail(TailArgs a)
+{
+    __shared__ uint64_t sm[3 * kTailMax];
+    __shared__ uint64_t pacc[kTailMaxLog][4][kTailThreads];
+    tail_body<KIND>(a, sm, pacc);
+}
+
+// The range and ReLU tails in one launch (one workgroup each).
+__global__ __launch_bounds__(256) void k_tail_range_relu(TailArgs a, TailArgs b)
+{
+    __shared__ uint64_t sm[3 * kTailMax];
+    __shared__ uint64_t pacc[kTailMaxLog][4][kTailThreads];
+    if (blockIdx.x == 0)
+        tail_body<KIND_RANGE>(a, sm, pacc);
+    else
+        tail_body<KIND_RELU>(b, sm, pacc);
 }
 
 size_t tail_capacity(int) { return kTailMax; }
 
+static TailArgs tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
+                          const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out)
+{
+    // finals[0..NT) receive the tables' final values
+    return TailArgs{t0, t1, t2, v, rho, kp, evals, finals, finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr,
+                    sum_out};
+}
+
 void launch_tail(int kind, const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
                  const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out, hipStream_t st)
 {
-    // finals[0..NT) receive the tables' final values
-    uint64_t *f0 = finals ? finals : nullptr, *f1 = finals ? finals + 1 : nullptr, *f2 = finals ? finals + 2 : nullptr;
+    const TailArgs a = tail_args(t0, t1, t2, v, rho, kp, evals, finals, sum_out);
     switch (kind) {
-    case KIND_MATMUL: hipLaunchKernelGGL(k_tail<KIND_MATMUL>, dim3(1), dim3(kTailThreads), 0, st, t0, t1, t2, v, rho, kp, evals, f0, f1, f2, sum_out); break;
-    case KIND_RANGE: hipLaunchKernelGGL(k_tail<KIND_RANGE>, dim3(1), dim3(kTailThreads), 0, st, t0, t1, t2, v, rho, kp, evals, f0, f1, f2, sum_out); break;
-    default: hipLaunchKernelGGL(k_tail<KIND_RELU>, dim3(1), dim3(kTailThreads), 0, st, t0, t1, t2, v, rho, kp, evals, f0, f1, f2, sum_out); break;
+    case KIND_MATMUL: hipLaunchKernelGGL(k_tail<KIND_MATMUL>, dim3(1), dim3(kTailThreads), 0, st, a); break;
+    case KIND_RANGE: hipLaunchKernelGGL(k_tail<KIND_RANGE>, dim3(1), dim3(kTailThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL(k_tail<KIND_RELU>, dim3(1), dim3(kTailThreads), 0, st, a); break;
     }
+}
+
+void launch_tail_range_relu(const TailArgs &range, const TailArgs &relu, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_tail_range_relu, dim3(2), dim3(kTailThreads), 0, st, range, relu);
+}
+
+TailArgs make_tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
+                        const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out)
+{
+    return tail_args(t0, t1, t2, v, rho, kp, evals, finals, sum_out);
 }
 
 __global__ __launch_bounds__(256) void k_i32_to_field(const int32_t *__restrict__ src, uint64_t N,

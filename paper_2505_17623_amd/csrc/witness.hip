@@ -40,21 +40,35 @@ template <> __device__ __forceinline__ uint64_t term<int64_t>(uint64_t e, int64_
 }
 template <> __device__ __forceinline__ uint64_t term<uint64_t>(uint64_t e, uint64_t a) { return m61::mul(e, a); }
 
-constexpr uint32_t kBindRowsPerChunk = 8;
-
-int bind_rows_chunks(uint32_t rows) { return (int)((rows + kBindRowsPerChunk - 1) / kBindRowsPerChunk); }
+// Rows are split into chunks; a block reduces one chunk for 64 columns (four
+// waves over interleaved rows, then through LDS), a second pass sums chunks.
+int bind_rows_chunks(uint32_t rows, uint32_t cols)
+{
+    const uint32_t groups = (cols + 63) / 64;
+    uint32_t nch = 1024 / groups;
+    if (nch > 128) nch = 128;
+    if (nch > rows / 4) nch = rows / 4;
+    return nch ? (int)nch : 1;
+}
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_bind_rows(const T *__restrict__ A, uint32_t rows, uint32_t cols,
-                                                   const uint64_t *__restrict__ E, uint64_t *__restrict__ part)
+                                                   const uint64_t *__restrict__ E, uint32_t per_chunk,
+                                                   uint64_t *__restrict__ part)
 {
-    const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= cols) return;
-    const uint32_t r0 = blockIdx.y * kBindRowsPerChunk;
-    const uint32_t r1 = r0 + kBindRowsPerChunk < rows ? r0 + kBindRowsPerChunk : rows;
+    __shared__ uint64_t red[4][64];
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const uint32_t c = blockIdx.x * 64 + lane;
+    const uint32_t r0 = blockIdx.y * per_chunk;
+    const uint32_t r1 = r0 + per_chunk < rows ? r0 + per_chunk : rows;
     uint64_t acc = 0;
-    for (uint32_t r = r0; r < r1; r++) acc = m61::add(acc, term<T>(E[r], A[(size_t)r * cols + c]));
-    part[(size_t)blockIdx.y * cols + c] = acc;
+    if (c < cols)
+        for (uint32_t r = r0 + wid; r < r1; r += 4) acc = m61::add(acc, term<T>(E[r], A[(size_t)r * cols + c]));
+    red[wid][lane] = acc;
+    __syncthreads();
+    if (wid == 0 && c < cols)
+        part[(size_t)blockIdx.y * cols + c] =
+            m61::add(m61::add(red[0][lane], red[1][lane]), m61::add(red[2][lane], red[3][lane]));
 }
 
 __global__ __launch_bounds__(256) void k_sum_chunks(const uint64_t *__restrict__ part, int nchunks, uint32_t cols,
@@ -62,9 +76,14 @@ __global__ __launch_bounds__(256) void k_sum_chunks(const uint64_t *__restrict__
 {
     const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= cols) return;
-    uint64_t acc = 0;
-    for (int q = 0; q < nchunks; q++) acc = m61::add(acc, part[(size_t)q * cols + c]);
-    out[c] = acc;
+    uint64_t a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int q = 0;
+    for (; q + 8 <= nchunks; q += 8)
+#pragma unroll
+        for (int u = 0; u < 8; u++) a[u] = m61::add(a[u], part[(size_t)(q + u) * cols + c]);
+    for (; q < nchunks; q++) a[0] = m61::add(a[0], part[(size_t)q * cols + c]);
+    out[c] = m61::add(m61::add(m61::add(a[0], a[1]), m61::add(a[2], a[3])),
+                      m61::add(m61::add(a[4], a[5]), m61::add(a[6], a[7])));
 }
 
 template <typename T>
@@ -83,13 +102,14 @@ __global__ __launch_bounds__(256) void k_bind_cols(const T *__restrict__ B, uint
 void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,
                       uint64_t *out, hipStream_t st)
 {
-    const int nch = bind_rows_chunks(rows);
-    dim3 grid((cols + 255) / 256, nch);
+    const int nch = bind_rows_chunks(rows, cols);
+    const uint32_t per = (rows + nch - 1) / nch;
+    dim3 grid((cols + 63) / 64, nch);
     switch (dtype) {
-    case RA_I16: hipLaunchKernelGGL(k_bind_rows<int16_t>, grid, dim3(256), 0, st, (const int16_t *)T, rows, cols, E, scratch); break;
-    case RA_I32: hipLaunchKernelGGL(k_bind_rows<int32_t>, grid, dim3(256), 0, st, (const int32_t *)T, rows, cols, E, scratch); break;
-    case RA_I64: hipLaunchKernelGGL(k_bind_rows<int64_t>, grid, dim3(256), 0, st, (const int64_t *)T, rows, cols, E, scratch); break;
-    default: hipLaunchKernelGGL(k_bind_rows<uint64_t>, grid, dim3(256), 0, st, (const uint64_t *)T, rows, cols, E, scratch); break;
+    case RA_I16: hipLaunchKernelGGL(k_bind_rows<int16_t>, grid, dim3(256), 0, st, (const int16_t *)T, rows, cols, E, per, scratch); break;
+    case RA_I32: hipLaunchKernelGGL(k_bind_rows<int32_t>, grid, dim3(256), 0, st, (const int32_t *)T, rows, cols, E, per, scratch); break;
+    case RA_I64: hipLaunchKernelGGL(k_bind_rows<int64_t>, grid, dim3(256), 0, st, (const int64_t *)T, rows, cols, E, per, scratch); break;
+    default: hipLaunchKernelGGL(k_bind_rows<uint64_t>, grid, dim3(256), 0, st, (const uint64_t *)T, rows, cols, E, per, scratch); break;
     }
     hipLaunchKernelGGL(k_sum_chunks, dim3((cols + 255) / 256), dim3(256), 0, st, (const uint64_t *)scratch, nch, cols, out);
 }

@@ -11,10 +11,10 @@
 // Every x-sum above is a linear combination of the entries of the Gram
 // matrix G[q][q'] = sum_x EQ(x) bit_q(x) bit_q'(x) (its diagonal gives the
 // linear terms, since a bit squared is itself).  G is an exact integer
-// contraction over x, so it runs on the matrix cores: EQ(x) is split into
-// nine 7-bit limbs d_t(x), and G_t = Bits^T diag(d_t) Bits is an int8 x int8
-// -> int32 product (v_mfma_i32_32x32x32_i8), recombined as sum_t 2^(7t) G_t
-// modulo p.  The same pass writes EQ(x) and the plane-bound table
+// contraction over x, so it runs on the matrix cores: EQ(x) is written in
+// eight balanced base-256 digits d_t(x) in [-128, 128), and
+// G_t = Bits^T diag(d_t) Bits is an int8 x int8 -> int32 product
+// (v_mfma_i32_32x32x32_i8), recombined as sum_t 256^t G_t modulo p.  The same pass writes EQ(x) and the plane-bound table
 // Bx(x) = sum_q eq(sigma_p, q) bit_q(x) (eight byte lookups per x), the
 // inputs of the rounds over x.
 #include "common.hpp"
@@ -24,7 +24,7 @@ namespace ra {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
-constexpr int kLimbs = 9;    // 7-bit limbs of a field element (63 bits)
+constexpr int kLimbs = 8;    // balanced base-256 digits of a field element
 
 // Output fragment of v_mfma_i32_32x32x32_i8: lane l, register r holds
 // row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
@@ -34,122 +34,142 @@ __host__ __device__ constexpr int frag_row(int l, int r) { return 8 * (r / 4) + 
 __device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (tp == 2 ? 1 : 0); }
 __device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
 
-// One x per thread for the per-x outputs; wave `tp` then accumulates tile
-// pair tp of the Gram matrix over the block's NX = 64 TP outputs.
-template <int TP>
-__global__ __launch_bounds__(64 * TP) void k_plane_gram(const uint64_t *__restrict__ bits, uint64_t N, int lk,
-                                                        const uint64_t *__restrict__ E1,
-                                                        const uint64_t *__restrict__ E2,
-                                                        const uint64_t *__restrict__ lut, uint64_t *__restrict__ EQ,
-                                                        uint64_t *__restrict__ EQ2, uint64_t *__restrict__ Bx,
-                                                        uint64_t *__restrict__ gpart)
+// Block layout of the Gram pass.  A block takes a slab of kSlab outputs at a
+// time: phase X (all waves) computes EQ, Bx and the digits of every output
+// and transposes the bit words into plane-major masks (64 ballots per 64
+// outputs), all into LDS; phase G then streams the slab through the matrix
+// cores.  Wave w accumulates digit w (two digits per wave with one tile pair)
+// for every tile pair, so all waves issue the same instruction sequence and
+// only the LDS address of their digit bytes differs.
+constexpr int kSlab = 4096;
+
+template <int TP> struct GramShape {
+    static constexpr int kWaves = TP == 1 ? 4 : 8;
+    static constexpr int kDigitsPerWave = kLimbs / kWaves;  // 2 or 1
+    static constexpr int kPlanes = 32 * (TP == 1 ? 1 : 2);
+};
+
+// Balanced base-256 digits of e < 2^61: e = sum_t 256^t d_t, d_t in [-128, 128).
+__device__ __forceinline__ void balanced_digits(uint64_t e, int8_t (&d)[kLimbs])
 {
-    constexpr int NX = 64 * TP;
-    __shared__ uint64_t s_lut[8 * 256];                 // Bx byte tables
-    __shared__ uint64_t s_exp[256];                     // byte -> eight 0x00 / 0xFF bytes
-    __shared__ __attribute__((aligned(16))) uint8_t s_d[kLimbs][NX];
-    __shared__ uint64_t s_mq[TP][2][64];                // plane-major bit masks per wave
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    for (int i = tid; i < 8 * 256; i += NX) s_lut[i] = lut[i];
-    for (int i = tid; i < 256; i += NX) {
+    int carry = 0;
+#pragma unroll
+    for (int t = 0; t < kLimbs; t++) {
+        const int v = (int)((e >> (8 * t)) & 255) + carry;
+        carry = v >= 128;
+        d[t] = (int8_t)(v - 256 * carry);
+    }
+}
+
+template <int TP>
+__global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
+    const uint64_t *__restrict__ bits, uint64_t N, int lk, const uint64_t *__restrict__ E1,
+    const uint64_t *__restrict__ E2, const uint64_t *__restrict__ lut, uint64_t *__restrict__ EQ,
+    uint64_t *__restrict__ EQ2, uint64_t *__restrict__ Bx, uint64_t *__restrict__ gpart)
+{
+    using S = GramShape<TP>;
+    constexpr int NT = 64 * S::kWaves, NPL = S::kPlanes, DW = S::kDigitsPerWave;
+    __shared__ uint64_t s_lut[8 * 256];                                   // Bx byte tables
+    __shared__ uint64_t s_exp[256];                                       // byte -> eight 0x00 / 0xFF bytes
+    __shared__ __attribute__((aligned(16))) int8_t s_d[kLimbs][kSlab];    // digits of EQ(x)
+    __shared__ uint64_t s_m[kSlab / 64][NPL];                             // plane masks per 64 outputs
+    // the block's Gram tiles, entry r * 64 + lane of fragment register r; two
+    // halves (digits 0-3, 4-7) so that sums of values below 2^61 cannot wrap
+    __shared__ unsigned long long s_g[2][TP][1024];
+    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
+    for (int i = tid; i < 8 * 256; i += NT) s_lut[i] = lut[i];
+    for (int i = tid; i < 256; i += NT) {
         uint64_t e = 0;
         for (int b = 0; b < 8; b++)
             if ((i >> b) & 1) e |= 0xFFull << (8 * b);
         s_exp[i] = e;
     }
-    const int pt = tile_row(wv, TP), pt2 = tile_col(wv, TP);
-    const int half = lane >> 5;
+    for (int i = tid; i < 2 * TP * 1024; i += NT) (&s_g[0][0][0])[i] = 0;
+    v16i acc[DW][TP];
+#pragma unroll
+    for (int k = 0; k < DW; k++)
+#pragma unroll
+        for (int tp = 0; tp < TP; tp++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) acc[k][tp][r] = 0;
     const uint64_t kmask = (1ull << lk) - 1;
-    const uint64_t nchunks = (N + NX - 1) / NX;
-    v16i acc[kLimbs];
-#pragma unroll
-    for (int t = 0; t < kLimbs; t++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) acc[t][r] = 0;
+    const uint64_t nslabs = (N + kSlab - 1) / kSlab;
     __syncthreads();
 
-    // the next chunk's word and eq factors are loaded one iteration ahead, so
-    // their latency overlaps the matrix-core work of the current chunk
-    uint64_t nw = 0, ne1 = 0, ne2 = 0;
-    {
-        const uint64_t x = (uint64_t)blockIdx.x * NX + tid;
-        if (x < N) {
-            nw = bits[x];
-            ne1 = E1[x >> lk];
-            ne2 = E2[x & kmask];
-        }
-    }
-    for (uint64_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
-        const uint64_t x = ch * NX + tid;
-        const bool valid = x < N;
-        const uint64_t w = nw, e1 = ne1, e2 = ne2;
-        {
-            const uint64_t xn = (ch + gridDim.x) * NX + tid;
-            if (xn < N) {
-                nw = bits[xn];
-                ne1 = E1[xn >> lk];
-                ne2 = E2[xn & kmask];
+    for (uint64_t sl = blockIdx.x; sl < nslabs; sl += gridDim.x) {
+        const uint64_t x0 = sl * kSlab;
+        // phase X: one output per thread per step, 64 consecutive outputs per wave
+#pragma unroll 2
+        for (int it = 0; it < kSlab / NT; it++) {
+            const int xl = it * NT + tid;
+            const uint64_t x = x0 + xl;
+            const bool valid = x < N;
+            uint64_t w = 0, eqx = 0;
+            if (valid) {
+                w = bits[x];
+                eqx = m61::mul(E1[x >> lk], E2[x & kmask]);
+                EQ[x] = eqx;
+                if (EQ2) EQ2[x] = eqx;
             }
-        }
-        uint64_t eqx = 0;
-        if (valid) {
-            eqx = m61::mul(e1, e2);
-            EQ[x] = eqx;
-            if (EQ2) EQ2[x] = eqx;
-        }
-        uint64_t bx = 0;
+            uint64_t bx = 0;
 #pragma unroll
-        for (int b = 0; b < 8; b++) bx = m61::add(bx, s_lut[b * 256 + ((w >> (8 * b)) & 255)]);
-        if (valid) Bx[x] = bx;
+            for (int b = 0; b < 8; b++) bx = m61::add(bx, s_lut[b * 256 + ((w >> (8 * b)) & 255)]);
+            if (valid) Bx[x] = bx;
+            int8_t d[kLimbs];
+            balanced_digits(eqx, d);
 #pragma unroll
-        for (int t = 0; t < kLimbs; t++) s_d[t][tid] = (uint8_t)((eqx >> (7 * t)) & 127);
-        // transpose this wave's 64 words: lane l keeps the masks of planes l%32 and l%32 + 32
-        uint64_t m0 = 0, m1 = 0;
+            for (int t = 0; t < kLimbs; t++) s_d[t][xl] = d[t];
+            uint64_t mine = 0;  // lane q keeps the mask of plane q
 #pragma unroll
-        for (int q = 0; q < (TP == 1 ? 32 : 64); q++) {
-            const uint64_t m = __ballot((int)((w >> q) & 1));
-            if ((lane & 31) == (q & 31)) {
-                if (q < 32) m0 = m;
-                else m1 = m;
+            for (int q = 0; q < NPL; q++) {
+                const uint64_t m = __ballot((int)((w >> q) & 1));
+                if (lane == q) mine = m;
             }
+            if (lane < NPL) s_m[xl >> 6][lane] = mine;
         }
-        s_mq[wv][0][lane] = m0;
-        if (TP > 1) s_mq[wv][1][lane] = m1;
         __syncthreads();
+        // phase G: 32 outputs per step; fragments of both plane tiles, then
+        // this wave's digit(s) for every tile pair
+        for (int ks = 0; ks < kSlab / 32; ks++) {
+            const int g = ks >> 1, sh = 32 * (ks & 1) + 16 * half, xo = 32 * ks + 16 * half;
+            v4i frag[2], mask[2];
 #pragma unroll
-        for (int g = 0; g < TP; g++) {
-            const uint64_t ma = s_mq[g][pt][lane], mb = s_mq[g][pt2][lane];
+            for (int pt = 0; pt < (TP == 1 ? 1 : 2); pt++) {
+                const uint32_t sb = (uint32_t)(s_m[g][32 * pt + (lane & 31)] >> sh) & 0xFFFF;
+                const uint64_t e0 = s_exp[sb & 255], e1 = s_exp[sb >> 8];
+                mask[pt] = v4i{(int)(uint32_t)e0, (int)(uint32_t)(e0 >> 32), (int)(uint32_t)e1, (int)(uint32_t)(e1 >> 32)};
+                frag[pt] = mask[pt] & (int)0x01010101;
+            }
 #pragma unroll
-            for (int ks = 0; ks < 2; ks++) {
-                // 32 x's per step: half 0 of the lanes carries x 0..15, half 1 x 16..31,
-                // in the same byte order for both operands
-                const int sh = 32 * ks + 16 * half;
-                const uint32_t sa = (uint32_t)(ma >> sh) & 0xFFFF, sb = (uint32_t)(mb >> sh) & 0xFFFF;
-                const uint64_t ea0 = s_exp[sa & 255], ea1 = s_exp[sa >> 8];
-                const uint64_t eb0 = s_exp[sb & 255], eb1 = s_exp[sb >> 8];
-                const v4i A = {(int)((uint32_t)ea0 & 0x01010101u), (int)((uint32_t)(ea0 >> 32) & 0x01010101u),
-                               (int)((uint32_t)ea1 & 0x01010101u), (int)((uint32_t)(ea1 >> 32) & 0x01010101u)};
-                const v4i Bm = {(int)(uint32_t)eb0, (int)(uint32_t)(eb0 >> 32), (int)(uint32_t)eb1,
-                                (int)(uint32_t)(eb1 >> 32)};
-                const int xo = 64 * g + sh;
-#pragma unroll
-                for (int t = 0; t < kLimbs; t++) {
-                    const v4i D = *(const v4i *)&s_d[t][xo];
-                    acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, Bm & D, acc[t], 0, 0, 0);
+            for (int k = 0; k < DW; k++) {
+                const v4i D = *(const v4i *)&s_d[wv + k * S::kWaves][xo];
+                const v4i B0 = mask[0] & D;
+                acc[k][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B0, acc[k][0], 0, 0, 0);
+                if (TP > 1) {
+                    const v4i B1 = mask[1] & D;
+                    acc[k][1 % TP] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B1, acc[k][1 % TP], 0, 0, 0);
+                    acc[k][2 % TP] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[1], B1, acc[k][2 % TP], 0, 0, 0);
                 }
             }
         }
         __syncthreads();
     }
-    // recombine the limbs modulo p and write this block's partial tile
-    uint64_t *out = gpart + ((size_t)blockIdx.x * TP + wv) * 1024;
+    // recombine the digits modulo p into the block's tiles
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-        uint64_t f = 0;
+    for (int k = 0; k < DW; k++) {
+        const int t = wv + k * S::kWaves;
+        const uint64_t w256 = 1ull << (8 * t);
 #pragma unroll
-        for (int t = 0; t < kLimbs; t++) f = m61::add(f, m61::mul((uint64_t)(uint32_t)acc[t][r], 1ull << (7 * t)));
-        out[lane * 16 + r] = f;
+        for (int tp = 0; tp < TP; tp++)
+#pragma unroll
+            for (int r = 0; r < 16; r++)
+                atomicAdd(&s_g[t < kLimbs / 2 ? 0 : 1][tp][r * 64 + lane],
+                          (unsigned long long)m61::mul(m61::from_i64(acc[k][tp][r]), w256));
     }
+    __syncthreads();
+    for (int i = tid; i < TP * 1024; i += NT)
+        gpart[(size_t)blockIdx.x * TP * 1024 + i] =
+            m61::add(m61::reduce64((&s_g[0][0][0])[i]), m61::reduce64((&s_g[1][0][0])[i]));
 }
 
 // Sum of the blocks' partial tiles, written as G[q][q'] (64 x 64, both
@@ -171,7 +191,7 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict_
     __syncthreads();
     if (wid != 0) return;
     const uint64_t v = m61::add(m61::add(red[0][lane], red[1][lane]), m61::add(red[2][lane], red[3][lane]));
-    const int tp = e >> 10, l = (e & 1023) >> 4, r = e & 15;
+    const int tp = e >> 10, r = (e & 1023) >> 6, l = e & 63;
     const int q = 32 * tile_row(tp, TP) + frag_row(l, r), q2 = 32 * tile_col(tp, TP) + (l & 31);
     G[q * 64 + q2] = v;
     G[q2 * 64 + q] = v;  // symmetric (the same value when the tile is diagonal)
@@ -267,9 +287,9 @@ int plane_gram_tiles(int lP) { return lP > 5 ? 3 : 1; }
 
 int plane_gram_blocks(uint64_t N, int lP)
 {
-    const int TP = plane_gram_tiles(lP);
-    const uint64_t chunks = (N + 64 * TP - 1) / (64 * TP);
-    return (int)(chunks < 256 ? chunks : 256);
+    (void)lP;
+    const uint64_t slabs = (N + kSlab - 1) / kSlab;
+    return (int)(slabs < 256 ? slabs : 256);
 }
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
@@ -278,9 +298,11 @@ void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const u
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
     if (TP == 1)
-        hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(64), 0, st, bits, N, lk, E1, E2, lut, EQ, EQ2, Bx, gpart);
+        hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(64 * GramShape<1>::kWaves), 0, st, bits, N, lk, E1, E2, lut,
+                           EQ, EQ2, Bx, gpart);
     else
-        hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(192), 0, st, bits, N, lk, E1, E2, lut, EQ, EQ2, Bx, gpart);
+        hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(64 * GramShape<3>::kWaves), 0, st, bits, N, lk, E1, E2, lut,
+                           EQ, EQ2, Bx, gpart);
     hipLaunchKernelGGL(k_gram_reduce, dim3(TP * 16), dim3(256), 0, st, (const uint64_t *)gpart, nb, TP, gsum);
 }
 

@@ -68,6 +68,22 @@ def add_instance(w, group, v, ntab, cmax, lt=10):
         lS -= C
 
 
+def add_xrounds(w, v, relu, lt=11, cmax=3):
+    """Global launches of the rounds over x (range instance, and the ReLU
+    zero-check in the same threads): the first launch reads Bx and the integer
+    R, Y; every launch writes the bound tables (Bx, and D, S with ReLU) at
+    2^-C of the size it read."""
+    lS, first = v, True
+    b, a, u = w.get("range_rounds", ("hbm", 0, "GB"))
+    while lS > lt:
+        C = min(cmax, lS - lt)
+        rd = (8 + 8 * relu) if first else (8 + 16 * relu)
+        a += rd * (1 << lS) + (8 + 16 * relu) * (1 << (lS - C))
+        lS -= C
+        first = False
+    w["range_rounds"] = ("hbm", a, "GB")
+
+
 def group_work(shapes, planes):
     """Algorithmic work per step of each kernel group: (bound, amount, unit)."""
     w = {}
@@ -83,11 +99,8 @@ def group_work(shapes, planes):
         add("bind_cols", "hbm", m * k * 2 + 8 * m, "GB")
         add("witness_minmax", "hbm", 8 * N, "GB")
         add("witness_rescale", "hbm", N * (8 + 4 + 2 + 4 + 4 + 8), "GB")  # C in; R, Rm, Y, Z, bits out
-        add("range_plane", "hbm", N * (8 + 16 + 8 * relu), "GB")         # bits in; EQ, Bx (+EQ) out
-        add_instance(w, "range_rounds", N.bit_length() - 1, 2, 2)      # x rounds: EQ and Bx
-        if relu:
-            add("relu_to_field", "hbm", 24 * N, "GB")
-            add_instance(w, "range_rounds", N.bit_length() - 1, 3, 2)  # ReLU rounds share the launches
+        add("range_plane", "hbm", N * (8 + 8), "GB")                    # bits in; Bx out
+        add_xrounds(w, N.bit_length() - 1, relu)
         add_instance(w, "matmul_rounds", m.bit_length() - 1, 2, 2)
     return w
 

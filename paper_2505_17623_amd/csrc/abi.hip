@@ -33,6 +33,7 @@ struct ra_ctx {
     int phase = 0;  // 0: expects matmul, 1: expects witness, 2: expects range
     uint32_t n = 0, m = 0, k = 0;
     uint64_t *d_eq = nullptr;  // E1 (n words) then E2 (k words)
+    const uint64_t *d_r12 = nullptr;  // the layer's (r1, r2) in the challenge stream
     size_t eq_cap = 0;
     WitParams *d_params = nullptr;
     uint64_t *d_claims = nullptr;  // R~, Rm~, Y~, Z~ at (r1, r2)
@@ -109,12 +110,12 @@ ra_status ensure_eq(ra_ctx *c, size_t words)
 // Kernel groups timed with events when profiling is on.
 enum Group {
     G_EQ = 0, G_GEMM, G_BIND_ROWS, G_BIND_COLS, G_MM_ROUNDS, G_MM_TAIL, G_WIT_MINMAX, G_WIT_RESCALE,
-    G_RANGE_SETUP, G_RANGE_PLANE, G_RANGE_ROUNDS, G_RANGE_TAIL, G_RELU_FIELD, G_RELU_ROUNDS, G_RELU_TAIL,
+    G_RANGE_SETUP, G_RANGE_PLANE, G_RANGE_ROUNDS, G_RANGE_TAIL, G_X_SETUP, G_RELU_ROUNDS, G_RELU_TAIL,
     G_ASSEMBLE, G_COUNT
 };
 const char *const kGroupName[G_COUNT] = {
     "eq_table", "gemm_mfma", "bind_rows", "bind_cols", "matmul_rounds", "matmul_tail", "witness_minmax",
-    "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail", "relu_to_field",
+    "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail", "x_setup",
     "relu_rounds", "relu_tail", "assemble"};
 
 hipEvent_t take_event(ra_ctx *c)
@@ -174,7 +175,8 @@ ra_status finish(ra_ctx *c, const uint64_t *d_src, size_t words)
     return RA_OK;
 }
 
-constexpr int kPartStride = kMaxBlocks * 6;  // words per partial-sum slot
+constexpr int kPartStride = kMaxBlocks * kPartWidth;  // words per partial-sum slot
+static_assert(kXTailThreads <= kMaxBlocks, "tail partials must fit a slot");
 
 int log2_tail() { return log2u(tail_capacity(0)); }
 // rounds of a v-variable instance that run as global (multi-block) launches
@@ -206,7 +208,8 @@ void run_instance(ra_ctx *c, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2,
         }
         const int nb = round_blocks(1ull << (lS - C));
         for (int r = 0; r < C; r++)
-            slots.s[slots.count++] = Slot{nb, width, ev_base + width * (j + r), 0, 0, (j + r == 0) ? sum_out : -1};
+            slots.s[slots.count++] =
+                Slot{nb, width, ev_base + width * (j + r), SLOT_COPY, 0, (j + r == 0) ? sum_out : -1, -1};
         lS -= C;
         j += C;
     }
@@ -399,7 +402,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
                  G_MM_ROUNDS, G_MM_TAIL);
     {
         Timed tm(c, G_ASSEMBLE);
-        launch_assemble(slots, part, kPartStride, tr, s);
+        launch_assemble(slots, part, kPartStride, tr, XConst{}, s);
     }
     if ((st = finish(c, tr, trw)) != RA_OK) return st;
 
@@ -412,6 +415,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     c->n = n;
     c->m = m;
     c->k = k;
+    c->d_r12 = r1;
     c->phase = 1;
     c->cursor += need;
     return RA_OK;
@@ -480,17 +484,19 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     if (c->cursor + need > c->n_chal) return RA_E_CHALLENGES;
     const uint64_t *lam = c->d_chal + c->cursor, *sigma = lam + 4 + lP, *rho2 = sigma + R;
 
-    const int nslots = global_rounds(lN) * (relu ? 2 : 1);
+    const int L = std::min(lN, kXTailLog), nhs = lN > L ? 1 << (lN - L) : 1;
+    const int nslots = std::max(lN, 1);
     if (nslots > kMaxSlots) return RA_E_INVAL;
     const int gtiles = plane_gram_tiles(lP), gblocks = plane_gram_blocks(N, lP);
-    // transcript: [evals 4R][EQ fin][bits_claim][range_sum][relu evals 4 lN][EQ fin][r_at][y_at]
+    // transcript: [evals 4R][(unused)][bits_claim][range_sum][relu evals 4 lN][(unused)][r_at][y_at]
     const size_t F_R = 4 * (size_t)R, RS = F_R + 2, Z0 = F_R + 3, FZ = Z0 + 4 * (size_t)lN, trw = FZ + 3;
     Carve cv;
     const size_t o_cst = cv.take<uint64_t>(C_WORDS);
-    const size_t o_eq = cv.take<uint64_t>(N), o_bx = cv.take<uint64_t>(N);
-    const size_t o_eq2 = cv.take<uint64_t>(relu ? N : 1), o_rf = cv.take<uint64_t>(relu ? N : 1),
-                 o_yf = cv.take<uint64_t>(relu ? N : 1);
-    const size_t o_part = cv.take<uint64_t>((size_t)std::max(nslots, 1) * kPartStride);
+    const size_t o_bx = cv.take<uint64_t>(N);
+    const size_t o_d = cv.take<uint64_t>(relu ? N : 1), o_s = cv.take<uint64_t>(relu ? N : 1);
+    const size_t o_hs = cv.take<uint64_t>(nhs), o_ls = cv.take<uint64_t>(2ull << L);
+    const size_t o_kr = cv.take<uint64_t>(lN + 1), o_kz = cv.take<uint64_t>(lN + 1);
+    const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
     const size_t o_tr = cv.take<uint64_t>(trw);
     const size_t o_lut = cv.take<uint64_t>(8 * 256);
     const size_t o_gp = cv.take<uint64_t>((size_t)gblocks * gtiles * 1024);
@@ -498,60 +504,63 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
     if ((st = ensure_stage(c, trw)) != RA_OK) return st;
-    uint64_t *cst = (uint64_t *)(c->ws + o_cst), *EQ = (uint64_t *)(c->ws + o_eq), *Bx = (uint64_t *)(c->ws + o_bx);
-    uint64_t *EQ2 = (uint64_t *)(c->ws + o_eq2), *Rf = (uint64_t *)(c->ws + o_rf), *Yf = (uint64_t *)(c->ws + o_yf);
+    uint64_t *cst = (uint64_t *)(c->ws + o_cst), *Bx = (uint64_t *)(c->ws + o_bx);
+    uint64_t *D = (uint64_t *)(c->ws + o_d), *S = (uint64_t *)(c->ws + o_s);
+    uint64_t *HS = (uint64_t *)(c->ws + o_hs), *LS = (uint64_t *)(c->ws + o_ls);
+    uint64_t *Kr = (uint64_t *)(c->ws + o_kr), *Kz = (uint64_t *)(c->ws + o_kz);
     uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = (uint64_t *)(c->ws + o_tr);
     uint64_t *lut = (uint64_t *)(c->ws + o_lut), *gpart = (uint64_t *)(c->ws + o_gp), *gsum = (uint64_t *)(c->ws + o_gs);
+    const uint64_t *sigx = sigma + lP, *rz = relu ? rho2 : nullptr;
     hipStream_t s = c->stream;
 
     {
         Timed tm(c, G_RANGE_SETUP);
         launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, lut, s);
     }
-    SlotTable slots;
-    slots.count = 0;
-    {   // plane rounds: Gram matrix on the matrix cores, EQ and Bx per output
+    {   // plane rounds: Gram matrix on the matrix cores, Bx per output
         Timed tm(c, G_RANGE_PLANE);
-        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, EQ, relu ? EQ2 : nullptr, Bx, gpart, gsum, s);
+        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, Bx, gpart, gsum, s);
     }
     {
         Timed tm(c, G_ASSEMBLE);
         launch_plane_assemble(lP, gsum, sigma, cst, tr, s);
     }
-    if (!relu) {  // rounds over x of the range instance
-        run_instance(c, KIND_RANGE, EQ, Bx, nullptr, lN, sigma + lP, cst + C_EP, tr, 4 * lP, 4, tr + F_R, -1, slots,
-                     part, G_RANGE_ROUNDS, G_RANGE_TAIL);
-    } else {  // and the ReLU zero-check of Eq. (6) at (r1, r2), same table size: shared launches
+    {   // rounds over x: the range instance and (same cube, same EQ point) the ReLU zero-check of Eq. (6)
+        Timed tm(c, G_X_SETUP);
+        launch_xsetup(c->d_r12, sigx, rz, lN, L, HS, LS, Kr, Kz, s);
+    }
+    SlotTable slots;
+    slots.count = 0;
+    int j = 0, lS = lN;
+    while (lS > L) {
+        const int C = std::min(kXFuseMax, lS - L);
+        const XArgs xa{Bx, D, S, d_R, d_Y, HS, LS, c->d_r12, sigx + j, rz ? rz + j : nullptr,
+                       part + (size_t)slots.count * kPartStride, lN, L, j};
         {
-            Timed tm(c, G_RELU_FIELD);
-            launch_i32_to_field(d_R, N, Rf, s);
-            launch_i32_to_field(d_Y, N, Yf, s);
+            Timed tm(c, G_RANGE_ROUNDS);
+            launch_xrounds(C, j == 0, relu != 0, xa, 1ull << lS, kPartStride, s);
         }
-        const int lt = log2_tail(), cmax = std::min(fused_rounds_max(KIND_RANGE), fused_rounds_max(KIND_RELU));
-        int j = 0, lS = lN;
-        while (lS > lt) {
-            const int C = std::min(cmax, lS - lt);
-            const InstArgs ra_{EQ, Bx, nullptr, sigma + lP + j, cst + C_EP, part + (size_t)slots.count * kPartStride};
-            const InstArgs rz{EQ2, Rf, Yf, rho2 + j, nullptr, part + (size_t)(slots.count + C) * kPartStride};
-            {
-                Timed tm(c, G_RANGE_ROUNDS);
-                launch_rounds_range_relu(C, ra_, rz, 1ull << lS, kPartStride, s);
-            }
-            const int nb = round_blocks(1ull << (lS - C));
-            for (int r = 0; r < C; r++) slots.s[slots.count++] = Slot{nb, 4, 4 * (lP + j + r), 0, 0, -1};
-            for (int r = 0; r < C; r++) slots.s[slots.count++] = Slot{nb, 4, (int)Z0 + 4 * (j + r), 0, 0, -1};
-            lS -= C;
-            j += C;
-        }
+        const int nb = xround_blocks(1ull << (lS - C));
+        for (int r = 0; r < C; r++)
+            slots.s[slots.count++] = Slot{nb, kPartWidth, 4 * (lP + j + r), SLOT_X, j + r, -1,
+                                          relu ? (int)Z0 + 4 * (j + r) : -1};
+        lS -= C;
+        j += C;
+    }
+    {
+        const XTailArgs ta{Bx, D, S, d_R, d_Y, LS, sigx + j, rz ? rz + j : nullptr,
+                           part + (size_t)slots.count * kPartStride, tr + F_R + 1, tr + FZ + 1, tr + FZ + 2, lS};
         Timed tm(c, G_RANGE_TAIL);
-        launch_tail_range_relu(make_tail_args(EQ, Bx, nullptr, lN - j, sigma + lP + j, cst + C_EP, tr + 4 * (lP + j),
-                                              tr + F_R, nullptr),
-                               make_tail_args(EQ2, Rf, Yf, lN - j, rho2 + j, nullptr, tr + Z0 + 4 * j, tr + FZ, nullptr),
-                               s);
+        launch_xtail(relu != 0, j == 0, ta, kPartStride, s);
+    }
+    for (int jj = 0; jj < lS; jj++) {
+        const int h = 1 << (lS - 1 - jj);
+        slots.s[slots.count++] = Slot{std::min(h, kXTailThreads), kPartWidth, 4 * (lP + j + jj), SLOT_X, j + jj, -1,
+                                      relu ? (int)Z0 + 4 * (j + jj) : -1};
     }
     {
         Timed tm(c, G_ASSEMBLE);
-        launch_assemble(slots, part, kPartStride, tr, s);
+        launch_assemble(slots, part, kPartStride, tr, XConst{cst + C_EP, c->d_r12, Kr, Kz}, s);
     }
     if ((st = finish(c, tr, trw)) != RA_OK) return st;
 

@@ -12,6 +12,11 @@ constexpr int kTailThreads = 256;      // block size of the LDS tail kernel
 constexpr int kTailMaxLog = 10;
 constexpr int kTailMax = 1 << kTailMaxLog;  // largest table the single-workgroup tail takes
 constexpr int kMaxBlocks = 1024;       // blocks of a grid-stride round kernel
+constexpr int kXTailLog = 11;          // the x rounds of the range / ReLU instances finish in LDS
+constexpr int kXTailMax = 1 << kXTailLog;
+constexpr int kXTailThreads = 512;
+constexpr int kXFuseMax = 3;           // x rounds fused per global launch
+constexpr int kPartWidth = 8;          // words per block and round in a partial-sum slot
 constexpr int kMaxSlots = 96;          // per-call partial-sum slots (rounds)
 constexpr int kMaxPlaneLog = 6;        // bit planes per output <= 64 (one word)
 
@@ -21,11 +26,11 @@ constexpr int C_W = 64;     // W_j, sizes P, P/2, ..., 2
 constexpr int C_W2 = 192;   // 2 W_j[i + h] - W_j[i], sizes P/2, ..., 1
 constexpr int C_K = 256;    // K_j, j = 1..lP
 constexpr int C_TAU = 264;  // tau_p
-constexpr int C_EP = 272;   // Ep, c (the kind parameters of KIND_RANGE), Wp, mu
+constexpr int C_EP = 272;   // Ep, c (the range summand over x), Wp, mu
 constexpr int C_WORDS = 280;
 
 // Sum-check instance kinds (see sumcheck.hip).
-enum Kind { KIND_MATMUL = 0, KIND_RANGE = 1, KIND_RELU = 2 };
+enum Kind { KIND_MATMUL = 0 };
 
 // Parameters of the rescale / ReLU witness, written on the device.
 struct WitParams {
@@ -36,13 +41,18 @@ struct WitParams {
 };
 
 // Where the per-block partial sums of one round live and how to combine them.
+enum SlotKind {
+    SLOT_COPY = 0,  // the reduced words are the round's evaluations
+    SLOT_X = 1      // range / ReLU x round: eight sums turned into g(0..3) (xrounds.hip)
+};
 struct Slot {
-    int32_t nblk;      // blocks that wrote partials
-    int32_t width;     // words per block (d + 1, or 6 for a plane round)
+    int32_t nblk;      // blocks (or threads) that wrote partials
+    int32_t width;     // words per block
     int32_t out;       // offset of the round's evaluations in the transcript buffer
-    int32_t kind;      // reserved (0)
-    int32_t round;     // reserved (0)
+    int32_t kind;      // SlotKind
+    int32_t round;     // SLOT_X: the round j over x
     int32_t sum_out;   // >= 0: also write g(0) + g(1) (the instance's claimed sum) there
+    int32_t out2;      // SLOT_X with ReLU: offset of the ReLU round's evaluations, else -1
 };
 struct SlotTable {
     int32_t count;
@@ -86,10 +96,6 @@ struct TailArgs {
 };
 TailArgs make_tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
                         const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out);
-// the range and ReLU instances (same table size) in shared launches
-void launch_rounds_range_relu(int C, const InstArgs &range, const InstArgs &relu, uint64_t S, int stride,
-                              hipStream_t st);
-void launch_tail_range_relu(const TailArgs &range, const TailArgs &relu, hipStream_t st);
 int fused_rounds_max(int kind);
 // C fused rounds over tables of size S (C <= fused_rounds_max); partials of
 // round r at part + r * stride
@@ -97,22 +103,51 @@ void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, ui
                    const uint64_t *kp, uint64_t *part, int stride, hipStream_t st);
 void launch_tail(int kind, const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
                  const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out, hipStream_t st);
-void launch_i32_to_field(const int32_t *src, uint64_t N, uint64_t *dst, hipStream_t st);
 // range constants: lambda/mu/tau_p/sigma_p at `chal`, claims from the witness
 size_t range_consts_words(int lP);
 // also writes the 8 x 256 byte tables of the plane-bound table Bx to lut
 void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,
                         uint64_t *tr_range_sum, uint64_t *lut, hipStream_t st);
 void init_kernel_attributes();
-void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, hipStream_t st);
+// Constants of SLOT_X rounds: kp = (Ep, c) of the range summand, r the EQ
+// point, Kr / Kz the prefix products of the range and ReLU instances.
+struct XConst {
+    const uint64_t *kp, *r, *Kr, *Kz;
+};
+void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, const XConst &xc,
+                     hipStream_t st);
+
+// ---- launchers (xrounds.hip) ----
+struct XArgs {
+    uint64_t *bx, *d, *s;          // Bx in place; D, S (written by the first launch)
+    const int32_t *R, *Y;          // integer R, Y (first launch)
+    const uint64_t *HS, *LS;       // suffix eq heaps
+    const uint64_t *r;             // EQ point (lN words)
+    const uint64_t *rho_a, *rho_z; // binding challenges of the launch's first round
+    uint64_t *part;
+    int lN, L, j;                  // variables, low-part size, first round
+};
+struct XTailArgs {
+    const uint64_t *bx, *d, *s;
+    const int32_t *R, *Y;
+    const uint64_t *LS;
+    const uint64_t *rho_a, *rho_z;
+    uint64_t *part;
+    uint64_t *fin_b, *fin_r, *fin_y;
+    int v;
+};
+void launch_xsetup(const uint64_t *r, const uint64_t *sigx, const uint64_t *rho2, int lN, int L, uint64_t *HS,
+                   uint64_t *LS, uint64_t *Kr, uint64_t *Kz, hipStream_t st);
+int xround_blocks(uint64_t sub);
+void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, hipStream_t st);
+void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStream_t st);
 
 // ---- launchers (planes.hip) ----
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
-// EQ, EQ2 (optional), Bx per x and the Gram matrix G (gsum: 64 x 64 words)
+// Bx per x and the Gram matrix G (gsum: 64 x 64 words)
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *lut, uint64_t *EQ, uint64_t *EQ2, uint64_t *Bx, uint64_t *gpart,
-                       uint64_t *gsum, hipStream_t st);
+                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, uint64_t *gsum, hipStream_t st);
 // round polynomials of the lP plane rounds into tr[0 .. 4 lP)
 void launch_plane_assemble(int lP, const uint64_t *gsum, const uint64_t *sigma, const uint64_t *cst, uint64_t *tr,
                            hipStream_t st);

@@ -78,25 +78,42 @@ __device__ __forceinline__ uint64_t wave_sum(uint64_t v)
     return v;
 }
 
+// LDS words block_sum<NV> needs for a block of nt threads (nt a multiple of 32).
+__host__ __device__ constexpr int block_sum_words(int NV, int nt) { return NV * nt + NV * 16 + NV; }
+
 // Block sum of NV field values per thread; thread 0 of the block ends with
-// the totals in v[].  `lds` must hold NV * (blockDim.x / 64) words.
+// the totals in v[].  `lds` must hold block_sum_words(NV, blockDim.x) words.
+// The values are transposed through LDS and summed in two stages (16
+// interleaved segments per value, then the segments), so no thread runs a
+// long chain of cross-lane exchanges.
 template <int NV>
 __device__ __forceinline__ void block_sum(uint64_t (&v)[NV], uint64_t *lds)
 {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int nt = blockDim.x, tid = threadIdx.x, seg = nt >> 4;
 #pragma unroll
-    for (int i = 0; i < NV; i++) v[i] = wave_sum(v[i]);
-    if (lane == 0)
-#pragma unroll
-        for (int i = 0; i < NV; i++) lds[i * nw + wid] = v[i];
+    for (int q = 0; q < NV; q++) lds[q * nt + tid] = v[q];
     __syncthreads();
-    if (wid == 0) {
-#pragma unroll
-        for (int i = 0; i < NV; i++) {
-            uint64_t x = lane < nw ? lds[i * nw + lane] : 0;
-            v[i] = wave_sum(x);
+    uint64_t *l2 = lds + NV * nt, *l3 = l2 + NV * 16;
+    for (int task = tid; task < NV * 16; task += nt) {
+        const uint64_t *src = lds + (task >> 4) * nt + (task & 15);  // entries g, g + 16, g + 32, ...
+        uint64_t a0 = 0, a1 = 0;
+        for (int e = 0; e < seg; e += 2) {
+            a0 = add(a0, src[16 * e]);
+            a1 = add(a1, src[16 * e + 16]);
         }
+        l2[task] = add(a0, a1);
     }
+    __syncthreads();
+    if (tid < NV) {
+        uint64_t a[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int g = 0; g < 16; g++) a[g & 3] = add(a[g & 3], l2[tid * 16 + g]);
+        l3[tid] = add(add(a[0], a[1]), add(a[2], a[3]));
+    }
+    __syncthreads();
+    if (tid == 0)
+#pragma unroll
+        for (int q = 0; q < NV; q++) v[q] = l3[q];
     __syncthreads();
 }
 

@@ -14,9 +14,9 @@
 // contraction over x, so it runs on the matrix cores: EQ(x) is written in
 // eight balanced base-256 digits d_t(x) in [-128, 128), and
 // G_t = Bits^T diag(d_t) Bits is an int8 x int8 -> int32 product
-// (v_mfma_i32_32x32x32_i8), recombined as sum_t 256^t G_t modulo p.  The same pass writes EQ(x) and the plane-bound table
-// Bx(x) = sum_q eq(sigma_p, q) bit_q(x) (eight byte lookups per x), the
-// inputs of the rounds over x.
+// (v_mfma_i32_32x32x32_i8), recombined as sum_t 256^t G_t modulo p.  The
+// same pass writes the plane-bound table Bx(x) = sum_q eq(sigma_p, q) bit_q(x)
+// (eight byte lookups per x), the input of the rounds over x.
 #include "common.hpp"
 #include "m61.hpp"
 
@@ -35,7 +35,7 @@ __device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (
 __device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
 
 // Block layout of the Gram pass.  A block takes a slab of kSlab outputs at a
-// time: phase X (all waves) computes EQ, Bx and the digits of every output
+// time: phase X (all waves) computes EQ(x), Bx and the digits of every output
 // and transposes the bit words into plane-major masks (64 ballots per 64
 // outputs), all into LDS; phase G then streams the slab through the matrix
 // cores.  Wave w accumulates digit w (two digits per wave with one tile pair)
@@ -64,8 +64,8 @@ __device__ __forceinline__ void balanced_digits(uint64_t e, int8_t (&d)[kLimbs])
 template <int TP>
 __global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
     const uint64_t *__restrict__ bits, uint64_t N, int lk, const uint64_t *__restrict__ E1,
-    const uint64_t *__restrict__ E2, const uint64_t *__restrict__ lut, uint64_t *__restrict__ EQ,
-    uint64_t *__restrict__ EQ2, uint64_t *__restrict__ Bx, uint64_t *__restrict__ gpart)
+    const uint64_t *__restrict__ E2, const uint64_t *__restrict__ lut, uint64_t *__restrict__ Bx,
+    uint64_t *__restrict__ gpart)
 {
     using S = GramShape<TP>;
     constexpr int NT = 64 * S::kWaves, NPL = S::kPlanes, DW = S::kDigitsPerWave;
@@ -108,8 +108,6 @@ __global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
             if (valid) {
                 w = bits[x];
                 eqx = m61::mul(E1[x >> lk], E2[x & kmask]);
-                EQ[x] = eqx;
-                if (EQ2) EQ2[x] = eqx;
             }
             uint64_t bx = 0;
 #pragma unroll
@@ -293,16 +291,15 @@ int plane_gram_blocks(uint64_t N, int lP)
 }
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *lut, uint64_t *EQ, uint64_t *EQ2, uint64_t *Bx, uint64_t *gpart,
-                       uint64_t *gsum, hipStream_t st)
+                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, uint64_t *gsum, hipStream_t st)
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
     if (TP == 1)
         hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(64 * GramShape<1>::kWaves), 0, st, bits, N, lk, E1, E2, lut,
-                           EQ, EQ2, Bx, gpart);
+                           Bx, gpart);
     else
         hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(64 * GramShape<3>::kWaves), 0, st, bits, N, lk, E1, E2, lut,
-                           EQ, EQ2, Bx, gpart);
+                           Bx, gpart);
     hipLaunchKernelGGL(k_gram_reduce, dim3(TP * 16), dim3(256), 0, st, (const uint64_t *)gpart, nb, TP, gsum);
 }
 

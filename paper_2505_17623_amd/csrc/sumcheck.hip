@@ -1,11 +1,7 @@
-// sumcheck.hip -- the prover's sum-check rounds (Sec. II-D) for the three
-// instances of a layer:
-//   KIND_MATMUL  sum_l a(l) b(l)                              degree 2  (Eq. (4))
-//   KIND_RANGE   sum_x EQ(x) (Ep b(x)^2 + c b(x))             degree 3  (range check,
-//                after its plane variables are bound; Ep, c constants)
-//   KIND_RELU    sum_x EQ(x) (R(x)^2 - Y(x)^2)                degree 3  (Eq. (6))
-// and the fused kernel that binds the plane variables of the concatenated
-// range check directly from the packed bit words.
+// sumcheck.hip -- the prover's sum-check rounds (Sec. II-D) of the matrix
+// product instance sum_l a(l) b(l) (degree 2, Eq. (4)), the constants of the
+// concatenated range check, and the transcript assembly.  The rounds over x
+// of the range and ReLU instances are in xrounds.hip.
 //
 // Variables are bound most-significant first, so round j pairs entry i with
 // entry i + h of the current table (h = half its size): both halves stream
@@ -21,13 +17,10 @@ namespace ra {
 
 template <int KIND> struct KindTraits;
 template <> struct KindTraits<KIND_MATMUL> { static constexpr int NT = 2, D = 2; };
-template <> struct KindTraits<KIND_RANGE> { static constexpr int NT = 2, D = 3; };
-template <> struct KindTraits<KIND_RELU> { static constexpr int NT = 3, D = 3; };
 
 // Contribution of one pair (lo = T[i], hi = T[i + h]) to g(X), X = 0..D.
 template <int KIND>
-__device__ __forceinline__ void pair_contrib(const uint64_t (&lo)[3], const uint64_t (&hi)[3], uint64_t ep,
-                                             uint64_t cc, uint64_t (&acc)[4])
+__device__ __forceinline__ void pair_contrib(const uint64_t (&lo)[3], const uint64_t (&hi)[3], uint64_t (&acc)[4])
 {
     constexpr int NT = KindTraits<KIND>::NT, D = KindTraits<KIND>::D;
     uint64_t val[NT], dif[NT];
@@ -38,15 +31,7 @@ __device__ __forceinline__ void pair_contrib(const uint64_t (&lo)[3], const uint
     }
 #pragma unroll
     for (int X = 0; X <= D; X++) {
-        uint64_t f;
-        if (KIND == KIND_MATMUL) {
-            f = m61::mul(val[0], val[1]);
-        } else if (KIND == KIND_RANGE) {
-            f = m61::mul(val[0], m61::mul(val[1], m61::add(m61::mul(ep, val[1]), cc)));
-        } else {
-            f = m61::mul(val[0], m61::mul(m61::sub(val[1], val[2]), m61::add(val[1], val[2])));
-        }
-        acc[X] = m61::add(acc[X], f);
+        acc[X] = m61::add(acc[X], m61::mul(val[0], val[1]));
         if (X < D)
 #pragma unroll
             for (int q = 0; q < NT; q++) val[q] = m61::add(val[q], dif[q]);  // table value at X + 1
@@ -67,7 +52,6 @@ __device__ __forceinline__ void rounds_body(const InstArgs &in, uint64_t sub, in
                                             uint64_t *red)
 {
     constexpr int NT = KindTraits<KIND>::NT, D = KindTraits<KIND>::D, L = 1 << C;
-    const uint64_t ep = KIND == KIND_RANGE ? in.kp[0] : 0, cc = KIND == KIND_RANGE ? in.kp[1] : 0;
     uint64_t r[C];
 #pragma unroll
     for (int c = 0; c < C; c++) r[c] = in.rho[c];
@@ -93,7 +77,7 @@ __device__ __forceinline__ void rounds_body(const InstArgs &in, uint64_t sub, in
                     lo[q] = v[q][u];
                     hi[q] = v[q][u + h];
                 }
-                pair_contrib<KIND>(lo, hi, ep, cc, a4);
+                pair_contrib<KIND>(lo, hi, a4);
 #pragma unroll
                 for (int q = 0; q < NT; q++) v[q][u] = m61::add(lo[q], m61::mul(r[c], m61::sub(hi[q], lo[q])));
             }
@@ -123,20 +107,8 @@ __device__ __forceinline__ void rounds_body(const InstArgs &in, uint64_t sub, in
 template <int KIND, int C>
 __global__ __launch_bounds__(256) void k_rounds(InstArgs a, uint64_t sub, int stride)
 {
-    __shared__ uint64_t red[4 * C * 4];
+    __shared__ uint64_t red[m61::block_sum_words(C * 4, kThreads)];
     rounds_body<KIND, C>(a, sub, blockIdx.x, gridDim.x, stride, red);
-}
-
-// Two independent instances over tables of the same size in one launch:
-// blocks [0, nbA) run instance a, the rest instance b.
-template <int KA, int KB, int C>
-__global__ __launch_bounds__(256) void k_rounds2(InstArgs a, InstArgs b, uint64_t sub, int nbA, int stride)
-{
-    __shared__ uint64_t red[4 * C * 4];
-    if ((int)blockIdx.x < nbA)
-        rounds_body<KA, C>(a, sub, blockIdx.x, nbA, stride, red);
-    else
-        rounds_body<KB, C>(b, sub, blockIdx.x - nbA, gridDim.x - nbA, stride, red);
 }
 
 int round_blocks(uint64_t h)
@@ -145,7 +117,7 @@ int round_blocks(uint64_t h)
     return (int)(b < (uint64_t)kMaxBlocks ? (b ? b : 1) : (uint64_t)kMaxBlocks);
 }
 
-int fused_rounds_max(int kind) { return kind == KIND_RELU ? 2 : 2; }
+int fused_rounds_max(int) { return 2; }
 
 void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t S, const uint64_t *rho,
                    const uint64_t *kp, uint64_t *part, int stride, hipStream_t st)
@@ -161,26 +133,10 @@ void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, ui
     case 3: RA_ROUNDS(K, 3); break;  \
     default: RA_ROUNDS(K, 4); break; \
     }
-    switch (kind) {
-    case KIND_MATMUL: RA_ROUNDS_K(KIND_MATMUL) break;
-    case KIND_RANGE: RA_ROUNDS_K(KIND_RANGE) break;
-    default: RA_ROUNDS_K(KIND_RELU) break;
-    }
+    (void)kind;
+    RA_ROUNDS_K(KIND_MATMUL)
 #undef RA_ROUNDS_K
 #undef RA_ROUNDS
-}
-
-void launch_rounds_range_relu(int C, const InstArgs &range, const InstArgs &relu, uint64_t S, int stride,
-                              hipStream_t st)
-{
-    const uint64_t sub = S >> C;
-    const int nb = round_blocks(sub);
-    switch (C) {
-    case 1: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 1>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
-    case 2: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 2>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
-    case 3: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 3>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
-    default: hipLaunchKernelGGL((k_rounds2<KIND_RANGE, KIND_RELU, 4>), dim3(2 * nb), dim3(kThreads), 0, st, range, relu, sub, nb, stride); break;
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -200,7 +156,6 @@ __device__ __forceinline__ void tail_body(const TailArgs &in, uint64_t *sm, uint
 #pragma unroll
         for (int q = 0; q < NT; q++) T[q][i] = G[q][i];
     __syncthreads();
-    const uint64_t ep = KIND == KIND_RANGE ? in.kp[0] : 0, cc = KIND == KIND_RANGE ? in.kp[1] : 0;
     if (v == 0 && in.sum_out && tid == 0) *in.sum_out = m61::mul(T[0][0], T[1][0]);  // no rounds: the sum is a b
     for (int j = 0; j < v; j++) {
         const uint32_t h = S >> (j + 1);
@@ -213,7 +168,7 @@ __device__ __forceinline__ void tail_body(const TailArgs &in, uint64_t *sm, uint
                 lo[q] = T[q][i];
                 hi[q] = T[q][i + h];
             }
-            pair_contrib<KIND>(lo, hi, ep, cc, acc);
+            pair_contrib<KIND>(lo, hi, acc);
 #pragma unroll
             for (int q = 0; q < NT; q++) T[q][i] = m61::add(lo[q], m61::mul(r, m61::sub(hi[q], lo[q])));
         }
@@ -252,17 +207,6 @@ __global__ __launch_bounds__(256) void k_tail(TailArgs a)
     tail_body<KIND>(a, sm, pacc);
 }
 
-// The range and ReLU tails in one launch (one workgroup each).
-__global__ __launch_bounds__(256) void k_tail_range_relu(TailArgs a, TailArgs b)
-{
-    __shared__ uint64_t sm[3 * kTailMax];
-    __shared__ uint64_t pacc[kTailMaxLog][4][kTailThreads];
-    if (blockIdx.x == 0)
-        tail_body<KIND_RANGE>(a, sm, pacc);
-    else
-        tail_body<KIND_RELU>(b, sm, pacc);
-}
-
 size_t tail_capacity(int) { return kTailMax; }
 
 static TailArgs tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
@@ -277,34 +221,14 @@ void launch_tail(int kind, const uint64_t *t0, const uint64_t *t1, const uint64_
                  const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out, hipStream_t st)
 {
     const TailArgs a = tail_args(t0, t1, t2, v, rho, kp, evals, finals, sum_out);
-    switch (kind) {
-    case KIND_MATMUL: hipLaunchKernelGGL(k_tail<KIND_MATMUL>, dim3(1), dim3(kTailThreads), 0, st, a); break;
-    case KIND_RANGE: hipLaunchKernelGGL(k_tail<KIND_RANGE>, dim3(1), dim3(kTailThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL(k_tail<KIND_RELU>, dim3(1), dim3(kTailThreads), 0, st, a); break;
-    }
-}
-
-void launch_tail_range_relu(const TailArgs &range, const TailArgs &relu, hipStream_t st)
-{
-    hipLaunchKernelGGL(k_tail_range_relu, dim3(2), dim3(kTailThreads), 0, st, range, relu);
+    (void)kind;
+    hipLaunchKernelGGL(k_tail<KIND_MATMUL>, dim3(1), dim3(kTailThreads), 0, st, a);
 }
 
 TailArgs make_tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
                         const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out)
 {
     return tail_args(t0, t1, t2, v, rho, kp, evals, finals, sum_out);
-}
-
-__global__ __launch_bounds__(256) void k_i32_to_field(const int32_t *__restrict__ src, uint64_t N,
-                                                      uint64_t *__restrict__ dst)
-{
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += (uint64_t)gridDim.x * blockDim.x)
-        dst[i] = m61::from_i64(src[i]);
-}
-
-void launch_i32_to_field(const int32_t *src, uint64_t N, uint64_t *dst, hipStream_t st)
-{
-    hipLaunchKernelGGL(k_i32_to_field, dim3(round_blocks(N)), dim3(kThreads), 0, st, src, N, dst);
 }
 
 // ---------------------------------------------------------------------------
@@ -320,7 +244,7 @@ void launch_i32_to_field(const int32_t *src, uint64_t N, uint64_t *dst, hipStrea
 // b_X = b(sigma_{<j}, X, p', x).  A_j and Bw_j are quadratic in X, so the
 // plane kernel sums them at X = 0, 1, 2 and the assembly extends to X = 3.
 // After all plane rounds the summand is EQ(x) (Ep b^2 + (mu Wp - Ep) b) with
-// Ep = eq(tau_p, sigma_p), Wp = W~(sigma_p): the KIND_RANGE instance.
+// Ep = eq(tau_p, sigma_p), Wp = W~(sigma_p), the rounds over x of xrounds.hip.
 // ---------------------------------------------------------------------------
 __host__ __device__ constexpr int off_half(int P, int j) { return P - (P >> (j - 1)); }      // e_j, w2_j
 __host__ __device__ constexpr int off_full(int P, int j) { return 2 * P - 2 * (P >> (j - 1)); }  // W_j
@@ -424,27 +348,43 @@ void launch_range_setup(const uint64_t *chal, const WitParams *params, const uin
 // round evaluations (plane rounds combined as described above).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_assemble(SlotTable slots, const uint64_t *__restrict__ part, int part_stride,
-                                                  uint64_t *__restrict__ tr)
+                                                  uint64_t *__restrict__ tr, XConst xc)
 {
-    __shared__ uint64_t red[6 * 4];
+    __shared__ uint64_t red[m61::block_sum_words(kPartWidth, 256)];
     const int si = blockIdx.x;
     const Slot sl = slots.s[si];
     const uint64_t *p = part + (size_t)si * part_stride;
-    uint64_t acc[6] = {0, 0, 0, 0, 0, 0};
+    uint64_t acc[kPartWidth] = {0, 0, 0, 0, 0, 0, 0, 0};
     for (int b = threadIdx.x; b < sl.nblk; b += blockDim.x)
         for (int i = 0; i < sl.width; i++) acc[i] = m61::add(acc[i], p[(size_t)b * sl.width + i]);
-    m61::block_sum<6>(acc, red);
+    m61::block_sum<kPartWidth>(acc, red);
     if (threadIdx.x != 0) return;
-    {
+    if (sl.kind == SLOT_COPY) {
         for (int i = 0; i < sl.width; i++) tr[sl.out + i] = acc[i];
         if (sl.sum_out >= 0) tr[sl.sum_out] = m61::add(acc[0], acc[1]);  // claimed sum = g_1(0) + g_1(1)
+        return;
+    }
+    // SLOT_X: acc = (A0, A1, Q0, Q1, Q2, Z0, Z1, Z2), see xrounds.hip
+    const int j = sl.round;
+    const uint64_t ep = xc.kp[0], cc = xc.kp[1], rj = xc.r[j];
+    uint64_t sv[4];
+    sv[0] = m61::add(m61::mul(ep, acc[2]), m61::mul(cc, acc[0]));
+    sv[1] = m61::add(m61::mul(ep, acc[3]), m61::mul(cc, acc[1]));
+    sv[2] = m61::add(m61::mul(ep, acc[4]), m61::mul(cc, m61::sub(m61::add(acc[1], acc[1]), acc[0])));
+    sv[3] = m61::add(sv[0], m61::mul(3, m61::sub(sv[2], sv[1])));  // quadratic: s(3) = s(0) + 3 (s(2) - s(1))
+    for (int X = 0; X < 4; X++) tr[sl.out + X] = m61::mul(m61::mul(xc.Kr[j], m61::eq1_small(rj, X)), sv[X]);
+    if (sl.out2 >= 0) {
+        const uint64_t z3 = m61::add(acc[5], m61::mul(3, m61::sub(acc[7], acc[6])));
+        const uint64_t zv[4] = {acc[5], acc[6], acc[7], z3};
+        for (int X = 0; X < 4; X++) tr[sl.out2 + X] = m61::mul(m61::mul(xc.Kz[j], m61::eq1_small(rj, X)), zv[X]);
     }
 }
 
-void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, hipStream_t st)
+void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, const XConst &xc,
+                     hipStream_t st)
 {
     if (slots.count == 0) return;
-    hipLaunchKernelGGL(k_assemble, dim3(slots.count), dim3(256), 0, st, slots, part, part_stride, tr);
+    hipLaunchKernelGGL(k_assemble, dim3(slots.count), dim3(256), 0, st, slots, part, part_stride, tr, xc);
 }
 
 }  // namespace ra

@@ -241,7 +241,7 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
                                                  int32_t *__restrict__ Z, uint64_t *__restrict__ bits,
                                                  uint64_t *__restrict__ claim_part)
 {
-    __shared__ uint64_t red[4 * 4];
+    __shared__ uint64_t red[m61::block_sum_words(4, 256)];
     const WitParams p = *prm;
     if (p.status != 0) return;  // uniform over the grid
     const int s = p.s, t = p.t, relu = p.relu;
@@ -277,7 +277,7 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
 __global__ __launch_bounds__(256) void k_claims_final(const uint64_t *__restrict__ part, int nblk,
                                                       const WitParams *__restrict__ prm, uint64_t *__restrict__ out)
 {
-    __shared__ uint64_t red[4 * 4];
+    __shared__ uint64_t red[m61::block_sum_words(4, 256)];
     uint64_t acc[4] = {0, 0, 0, 0};
     for (int b = threadIdx.x; b < nblk; b += blockDim.x)
         for (int i = 0; i < 4; i++) acc[i] = m61::add(acc[i], part[4 * b + i]);

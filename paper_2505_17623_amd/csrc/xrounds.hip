@@ -1,0 +1,297 @@
+// xrounds.hip -- the rounds over x of the concatenated range check and of
+// the ReLU zero-check (Sec. III-B, Eq. (6)), after the plane variables of
+// the range check are bound.  Both instances sum over the same Boolean cube
+// with the same equality factor EQ(x) = eq(r, x), r = (r1, r2):
+//   range  sum_x EQ(x) (Ep Bx(x)^2 + c Bx(x))          (Bx: bit table bound at sigma_p)
+//   ReLU   sum_x EQ(x) (R(x)^2 - Y(x)^2) = sum_x EQ(x) D(x) S(x),   D = R - Y, S = R + Y.
+// The range instance binds x to sigma_x, the ReLU instance to rho'.
+//
+// EQ is never stored.  With x bound to z_<j in round j it equals
+//   K_j eq1(r_j, X) eq(r_>j, i),      K_j = prod_{l<j} eq1(r_l, z_l),
+// so the round polynomial is K_j eq1(r_j, X) s_j(X) with
+//   s_j(X) = sum_i eq(r_>j, i) h(T_X(i))     (T_X = T_lo + X (T_hi - T_lo)),
+// a quadratic in X.  The kernels accumulate, per round,
+//   range  A_a = sum_i w_i b_a,  Q_a = sum_i w_i b_a^2      (a = 0, 1; Q also at b_2 = 2 b_1 - b_0)
+//   ReLU   Z_a = sum_i w_i d_a s_a                          (a = 0, 1, 2)
+// with w_i = eq(r_>j, i), five field products per pair and instance; the
+// assembly forms s_j(0..2), extrapolates s_j(3) and multiplies by
+// K_j eq1(r_j, X).  The weights eq(r_>j, i) come from two small tables of
+// suffix eq vectors (a high part and a low part of the variables), so they
+// cost one product per thread.  The ReLU tables are kept as D and S; the
+// final values give R = (D + S) / 2 and Y = (S - D) / 2.
+#include "common.hpp"
+#include "m61.hpp"
+
+namespace ra {
+
+// ---------------------------------------------------------------------------
+// Set-up: suffix eq tables and the prefix products K_j of both instances.
+//   HS heap: table s (2^s entries at offset 2^s) = eq(r_{lN-L-s .. lN-L-1}, .)
+//   LS heap: table s (2^s entries at offset 2^s) = eq(r_{lN-s .. lN-1}, .)
+//   Kr[j] = prod_{l<j} eq1(r_l, sigma_x,l),  Kz[j] = prod_{l<j} eq1(r_l, rho'_l)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t eq_suffix(const uint64_t *r, int first, int s, uint64_t i)
+{
+    uint64_t a = 1;
+    for (int t = 0; t < s; t++) a = m61::mul(a, m61::eq1_bit(r[first + t], (uint32_t)(i >> (s - 1 - t)) & 1u));
+    return a;
+}
+
+__global__ __launch_bounds__(256) void k_xsetup(const uint64_t *__restrict__ r, const uint64_t *__restrict__ sigx,
+                                                const uint64_t *__restrict__ rho2, int lN, int L, int nhs,
+                                                uint64_t *__restrict__ HS, uint64_t *__restrict__ LS,
+                                                uint64_t *__restrict__ Kr, uint64_t *__restrict__ Kz)
+{
+    const int gid = blockIdx.x * blockDim.x + threadIdx.x;
+    const int nls = 1 << (L + 1);
+    if (gid == 0 || gid == 64) {  // two waves walk the prefix products
+        const uint64_t *z = gid == 0 ? sigx : rho2;
+        uint64_t *K = gid == 0 ? Kr : Kz;
+        if (z) {
+            uint64_t a = 1;
+            for (int j = 0; j < lN; j++) {
+                K[j] = a;
+                const uint64_t e = m61::add(m61::mul(r[j], z[j]), m61::mul(m61::sub(1, r[j]), m61::sub(1, z[j])));
+                a = m61::mul(a, e);
+            }
+            K[lN] = a;
+        }
+    }
+    if (gid >= 1 && gid < nhs) {
+        const int s = 31 - __clz(gid);
+        HS[gid] = eq_suffix(r, lN - L - s, s, (uint64_t)(gid - (1 << s)));
+    }
+    const int e = gid - nhs;
+    if (e >= 1 && e < nls) {
+        const int s = 31 - __clz(e);
+        LS[e] = eq_suffix(r, lN - s, s, (uint64_t)(e - (1 << s)));
+    }
+}
+
+void launch_xsetup(const uint64_t *r, const uint64_t *sigx, const uint64_t *rho2, int lN, int L, uint64_t *HS,
+                   uint64_t *LS, uint64_t *Kr, uint64_t *Kz, hipStream_t st)
+{
+    const int nhs = lN > L ? 1 << (lN - L) : 1, total = nhs + (1 << (L + 1));
+    hipLaunchKernelGGL(k_xsetup, dim3((total + 255) / 256), dim3(256), 0, st, r, sigx, rho2, lN, L, nhs, HS, LS, Kr,
+                       Kz);
+}
+
+// Contributions of one pair with weight w.
+__device__ __forceinline__ void range_pair(uint64_t w, uint64_t b0, uint64_t b1, uint64_t *acc)
+{
+    const uint64_t eb0 = m61::mul(w, b0), eb1 = m61::mul(w, b1);
+    const uint64_t eb2 = m61::sub(m61::add(eb1, eb1), eb0), b2 = m61::sub(m61::add(b1, b1), b0);
+    acc[0] = m61::add(acc[0], eb0);
+    acc[1] = m61::add(acc[1], eb1);
+    acc[2] = m61::add(acc[2], m61::mul(eb0, b0));
+    acc[3] = m61::add(acc[3], m61::mul(eb1, b1));
+    acc[4] = m61::add(acc[4], m61::mul(eb2, b2));
+}
+
+__device__ __forceinline__ void relu_pair(uint64_t w, uint64_t d0, uint64_t d1, uint64_t s0, uint64_t s1,
+                                          uint64_t *acc)
+{
+    const uint64_t ed0 = m61::mul(w, d0), ed1 = m61::mul(w, d1);
+    const uint64_t ed2 = m61::sub(m61::add(ed1, ed1), ed0), s2 = m61::sub(m61::add(s1, s1), s0);
+    acc[5] = m61::add(acc[5], m61::mul(ed0, s0));
+    acc[6] = m61::add(acc[6], m61::mul(ed1, s1));
+    acc[7] = m61::add(acc[7], m61::mul(ed2, s2));
+}
+
+__device__ __forceinline__ uint64_t fold(uint64_t lo, uint64_t hi, uint64_t z)
+{
+    return m61::add(lo, m61::mul(z, m61::sub(hi, lo)));
+}
+
+// ---------------------------------------------------------------------------
+// C fused rounds j .. j + C - 1 over tables of S = 2^lS entries (lS = lN - j).
+// Thread i (< S' = S / 2^C) owns the entries i + t S' (t < 2^C), the sub-cube
+// of the C variables being bound; it runs the C rounds on them in registers
+// and writes the bound value to index i.  The pair (u, u + h) of local round
+// c has weight eq(r_{j+c+1 .. j+C-1}, u) eq(r_{j+C ..}, i), built from the
+// thread's eq(r_{j+C ..}, i) = HS[.] LS[.] by halving.  With FIRST the inputs
+// are Bx and the integer R, Y; D and S are written.  Partials of round c go to
+// part + c * stride + 8 blk.
+// ---------------------------------------------------------------------------
+template <int C, bool FIRST, bool RELU>
+__global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stride)
+{
+    constexpr int NL = 1 << C;
+    __shared__ uint64_t red[m61::block_sum_words(C * (RELU ? 8 : 5), kThreads)];
+    uint64_t acc[C][8];
+#pragma unroll
+    for (int c = 0; c < C; c++)
+#pragma unroll
+        for (int q = 0; q < 8; q++) acc[c][q] = 0;
+    uint64_t ra[C], rz[C], rr[C];
+#pragma unroll
+    for (int c = 0; c < C; c++) {
+        ra[c] = a.rho_a[c];
+        rz[c] = RELU ? a.rho_z[c] : 0;
+        rr[c] = a.r[a.j + c];
+    }
+    const uint64_t *hs = a.HS + (1ull << (a.lN - a.L - a.j - C));
+    const uint64_t *ls = a.LS + (1ull << a.L);
+    const uint64_t lmask = (1ull << a.L) - 1;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < sub; i += (uint64_t)gridDim.x * blockDim.x) {
+        uint64_t b[NL], d[NL], s[NL];
+#pragma unroll
+        for (int t = 0; t < NL; t++) {
+            b[t] = a.bx[i + t * sub];
+            if (RELU) {
+                if (FIRST) {
+                    const int64_t R = a.R[i + t * sub], Y = a.Y[i + t * sub];
+                    d[t] = m61::from_i64(R - Y);
+                    s[t] = m61::from_i64(R + Y);
+                } else {
+                    d[t] = a.d[i + t * sub];
+                    s[t] = a.s[i + t * sub];
+                }
+            }
+        }
+        // weights: round c uses w[(1 << (C-1-c)) - 1 + u] (indices 0 .. NL-2)
+        uint64_t w[NL];
+        w[0] = m61::mul(hs[i >> a.L], ls[i & lmask]);  // round C - 1 (u empty)
+#pragma unroll
+        for (int c = C - 2; c >= 0; c--) {
+            const int hn = 1 << (C - 1 - c), base = hn - 1, pb = (hn >> 1) - 1;
+            // u = (msb, rest): eq1(r_{j+c+1}, msb) times the weight of `rest` one round later
+#pragma unroll
+            for (int u = 0; u < hn / 2; u++) {
+                const uint64_t hi = m61::mul(rr[c + 1], w[pb + u]);
+                w[base + hn / 2 + u] = hi;
+                w[base + u] = m61::sub(w[pb + u], hi);
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < C; c++) {
+            const int h = NL >> (c + 1), base = h - 1;
+#pragma unroll
+            for (int u = 0; u < h; u++) {
+                range_pair(w[base + u], b[u], b[u + h], acc[c]);
+                b[u] = fold(b[u], b[u + h], ra[c]);
+                if (RELU) {
+                    relu_pair(w[base + u], d[u], d[u + h], s[u], s[u + h], acc[c]);
+                    d[u] = fold(d[u], d[u + h], rz[c]);
+                    s[u] = fold(s[u], s[u + h], rz[c]);
+                }
+            }
+        }
+        a.bx[i] = b[0];
+        if (RELU) {
+            a.d[i] = d[0];
+            a.s[i] = s[0];
+        }
+    }
+    constexpr int NV = RELU ? 8 : 5;
+    uint64_t flat[C * NV];
+#pragma unroll
+    for (int c = 0; c < C; c++)
+#pragma unroll
+        for (int q = 0; q < NV; q++) flat[c * NV + q] = acc[c][q];
+    m61::block_sum<C * NV>(flat, red);
+    if (threadIdx.x == 0)
+#pragma unroll
+        for (int c = 0; c < C; c++)
+#pragma unroll
+            for (int q = 0; q < 8; q++)
+                a.part[(size_t)c * stride + (size_t)blockIdx.x * 8 + q] = q < NV ? flat[c * NV + q] : 0;
+}
+
+int xround_blocks(uint64_t sub)
+{
+    const uint64_t b = (sub + kThreads - 1) / kThreads;
+    return (int)(b < (uint64_t)kMaxBlocks ? (b ? b : 1) : (uint64_t)kMaxBlocks);
+}
+
+void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, hipStream_t st)
+{
+    const uint64_t sub = S >> C;
+    const dim3 g(xround_blocks(sub)), b(kThreads);
+#define RA_X(CC, F, Z) hipLaunchKernelGGL((k_xrounds<CC, F, Z>), g, b, 0, st, a, sub, stride)
+#define RA_X_FZ(CC)                  \
+    if (first) {                     \
+        if (relu) RA_X(CC, true, true); \
+        else RA_X(CC, true, false);     \
+    } else {                         \
+        if (relu) RA_X(CC, false, true); \
+        else RA_X(CC, false, false);     \
+    }
+    switch (C) {
+    case 1: RA_X_FZ(1) break;
+    case 2: RA_X_FZ(2) break;
+    default: RA_X_FZ(3) break;
+    }
+#undef RA_X_FZ
+#undef RA_X
+}
+
+// ---------------------------------------------------------------------------
+// The last v rounds in one workgroup with the tables in LDS.  Round jj pairs
+// i and i + h (h = 2^(v-1-jj)) with weight LS[h + i] = eq(r_>j, i).  Thread
+// t < min(h, blockDim) writes its eight partial sums of round jj to
+// part + jj * stride + 8 t; the assembly reduces them.  With FIRST (no
+// global rounds ran) the inputs are Bx and the integer R, Y.
+// ---------------------------------------------------------------------------
+template <bool RELU>
+__global__ __launch_bounds__(kXTailThreads) void k_xtail(XTailArgs a, int first, int stride)
+{
+    __shared__ uint64_t Tb[kXTailMax], Td[RELU ? kXTailMax : 1], Ts[RELU ? kXTailMax : 1], W[kXTailMax];
+    const int tid = threadIdx.x, v = a.v, S = 1 << v;
+    for (int i = tid; i < S; i += blockDim.x) {
+        Tb[i] = a.bx[i];
+        W[i] = a.LS[i];  // heap entries 1 .. S-1 are the tables of sizes S/2 .. 1
+        if (RELU) {
+            if (first) {
+                const int64_t R = a.R[i], Y = a.Y[i];
+                Td[i] = m61::from_i64(R - Y);
+                Ts[i] = m61::from_i64(R + Y);
+            } else {
+                Td[i] = a.d[i];
+                Ts[i] = a.s[i];
+            }
+        }
+    }
+    __syncthreads();
+    for (int jj = 0; jj < v; jj++) {
+        const int h = S >> (jj + 1);
+        const uint64_t za = a.rho_a[jj], zz = RELU ? a.rho_z[jj] : 0;
+        uint64_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int i = tid; i < h; i += blockDim.x) {
+            const uint64_t w = W[h + i];
+            const uint64_t b0 = Tb[i], b1 = Tb[i + h];
+            range_pair(w, b0, b1, acc);
+            Tb[i] = fold(b0, b1, za);
+            if (RELU) {
+                const uint64_t d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
+                relu_pair(w, d0, d1, s0, s1, acc);
+                Td[i] = fold(d0, d1, zz);
+                Ts[i] = fold(s0, s1, zz);
+            }
+        }
+        if (tid < h) {
+            uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)tid;
+#pragma unroll
+            for (int q = 0; q < 8; q++) o[q] = acc[q];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        *a.fin_b = Tb[0];
+        if (RELU) {
+            const uint64_t inv2 = 1ull << 60;  // (p + 1) / 2
+            *a.fin_r = m61::mul(m61::add(Td[0], Ts[0]), inv2);
+            *a.fin_y = m61::mul(m61::sub(Ts[0], Td[0]), inv2);
+        }
+    }
+}
+
+void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStream_t st)
+{
+    if (relu)
+        hipLaunchKernelGGL(k_xtail<true>, dim3(1), dim3(kXTailThreads), 0, st, a, (int)first, stride);
+    else
+        hipLaunchKernelGGL(k_xtail<false>, dim3(1), dim3(kXTailThreads), 0, st, a, (int)first, stride);
+}
+
+}  // namespace ra

@@ -175,12 +175,10 @@ ra_status finish(ra_ctx *c, const uint64_t *d_src, size_t words)
     return RA_OK;
 }
 
-constexpr int kPartStride = kMaxBlocks * kPartWidth;  // words per partial-sum slot
-static_assert(kXTailThreads <= kMaxBlocks, "tail partials must fit a slot");
+constexpr int kPartStride = kMaxUnits * kPartWidth;  // words per partial-sum slot
+static_assert(kXTailThreads <= kMaxUnits && kMaxBlocks <= kMaxUnits, "partials must fit a slot");
 
 int log2_tail() { return log2u(tail_capacity(0)); }
-// rounds of a v-variable instance that run as global (multi-block) launches
-int global_rounds(int v) { return v > log2_tail() ? v - log2_tail() : 0; }
 
 // One sum-check instance over tables of 2^v entries (in place): fused global
 // launches while the table exceeds the LDS tail, then the tail.  Round j's
@@ -213,9 +211,16 @@ void run_instance(ra_ctx *c, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2,
         lS -= C;
         j += C;
     }
-    Timed tm(c, g_tail);
-    launch_tail(kind, t0, t1, t2, v - j, rho + j, kp, tr + ev_base + width * j, finals,
-                (j == 0 && sum_out >= 0) ? tr + sum_out : nullptr, c->stream);
+    {
+        Timed tm(c, g_tail);
+        const TailArgs ta{t0, t1, t2, v - j, rho + j, part + (size_t)slots.count * kPartStride, kPartStride, finals,
+                          finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr,
+                          (j == 0 && v == 0 && sum_out >= 0) ? tr + sum_out : nullptr};
+        launch_tail(kind, ta, c->stream);
+    }
+    for (int jj = 0; jj < v - j; jj++)
+        slots.s[slots.count++] = Slot{tail_units(1u << (v - j - 1 - jj)), width, ev_base + width * (j + jj), SLOT_COPY,
+                                      0, (j + jj == 0) ? sum_out : -1, -1};
 }
 }  // namespace
 
@@ -362,7 +367,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
 
     ra_status st = ensure_eq(c, (size_t)n + k);
     if (st != RA_OK) return st;
-    const int nslots = std::max(1, global_rounds(lm));
+    const int nslots = std::max(1, lm);
     const size_t trw = 3 + 3 * (size_t)lm;
     Carve cv;
     const size_t o_a = cv.take<uint64_t>(m), o_b = cv.take<uint64_t>(m);
@@ -532,15 +537,16 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     SlotTable slots;
     slots.count = 0;
     int j = 0, lS = lN;
-    while (lS > L) {
-        const int C = std::min(kXFuseMax, lS - L);
+    const int xl = (lN - L + kXFuseMax - 1) / kXFuseMax;  // global launches, rounds spread evenly
+    for (int g = 0; lS > L; g++) {
+        const int C = (lN - L) / xl + (g < (lN - L) % xl ? 1 : 0);
         const XArgs xa{Bx, D, S, d_R, d_Y, HS, LS, c->d_r12, sigx + j, rz ? rz + j : nullptr,
                        part + (size_t)slots.count * kPartStride, lN, L, j};
         {
             Timed tm(c, G_RANGE_ROUNDS);
             launch_xrounds(C, j == 0, relu != 0, xa, 1ull << lS, kPartStride, s);
         }
-        const int nb = xround_blocks(1ull << (lS - C));
+        const int nb = xround_units(1ull << (lS - C), relu != 0);
         for (int r = 0; r < C; r++)
             slots.s[slots.count++] = Slot{nb, kPartWidth, 4 * (lP + j + r), SLOT_X, j + r, -1,
                                           relu ? (int)Z0 + 4 * (j + r) : -1};
@@ -555,7 +561,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     }
     for (int jj = 0; jj < lS; jj++) {
         const int h = 1 << (lS - 1 - jj);
-        slots.s[slots.count++] = Slot{std::min(h, kXTailThreads), kPartWidth, 4 * (lP + j + jj), SLOT_X, j + jj, -1,
+        slots.s[slots.count++] = Slot{xtail_units(h, relu != 0), kPartWidth, 4 * (lP + j + jj), SLOT_X, j + jj, -1,
                                       relu ? (int)Z0 + 4 * (j + jj) : -1};
     }
     {

@@ -12,10 +12,11 @@ constexpr int kTailThreads = 256;      // block size of the LDS tail kernel
 constexpr int kTailMaxLog = 10;
 constexpr int kTailMax = 1 << kTailMaxLog;  // largest table the single-workgroup tail takes
 constexpr int kMaxBlocks = 1024;       // blocks of a grid-stride round kernel
-constexpr int kXTailLog = 11;          // the x rounds of the range / ReLU instances finish in LDS
+constexpr int kXTailLog = 12;          // the x rounds of the range / ReLU instances finish in LDS
 constexpr int kXTailMax = 1 << kXTailLog;
-constexpr int kXTailThreads = 512;
-constexpr int kXFuseMax = 3;           // x rounds fused per global launch
+constexpr int kXTailThreads = 1024;
+constexpr int kXFuseMax = 4;           // x rounds fused per global launch
+constexpr int kMaxUnits = 2048;        // partial-sum producers per round (waves or threads)
 constexpr int kPartWidth = 8;          // words per block and round in a partial-sum slot
 constexpr int kMaxSlots = 96;          // per-call partial-sum slots (rounds)
 constexpr int kMaxPlaneLog = 6;        // bit planes per output <= 64 (one word)
@@ -91,18 +92,18 @@ struct InstArgs {
 struct TailArgs {
     const uint64_t *t0, *t1, *t2;
     int v;
-    const uint64_t *rho, *kp;
-    uint64_t *evals, *fin0, *fin1, *fin2, *sum_out;
+    const uint64_t *rho;
+    uint64_t *part;  // round j's partials at part + j * stride
+    int stride;
+    uint64_t *fin0, *fin1, *fin2, *sum_out;
 };
-TailArgs make_tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
-                        const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out);
+int tail_units(uint32_t h);  // partial-sum producers of a tail round with h pairs
 int fused_rounds_max(int kind);
 // C fused rounds over tables of size S (C <= fused_rounds_max); partials of
 // round r at part + r * stride
 void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t S, const uint64_t *rho,
                    const uint64_t *kp, uint64_t *part, int stride, hipStream_t st);
-void launch_tail(int kind, const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
-                 const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out, hipStream_t st);
+void launch_tail(int kind, const TailArgs &a, hipStream_t st);
 // range constants: lambda/mu/tau_p/sigma_p at `chal`, claims from the witness
 size_t range_consts_words(int lP);
 // also writes the 8 x 256 byte tables of the plane-bound table Bx to lut
@@ -138,7 +139,9 @@ struct XTailArgs {
 };
 void launch_xsetup(const uint64_t *r, const uint64_t *sigx, const uint64_t *rho2, int lN, int L, uint64_t *HS,
                    uint64_t *LS, uint64_t *Kr, uint64_t *Kz, hipStream_t st);
-int xround_blocks(uint64_t sub);
+int xround_blocks(uint64_t sub, bool relu);
+int xround_units(uint64_t sub, bool relu);  // partial-sum producers of a launch
+int xtail_units(int h, bool relu);          // ... of a tail round with h pairs
 void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, hipStream_t st);
 void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStream_t st);
 

@@ -50,6 +50,19 @@ __device__ __forceinline__ uint64_t from_i64(int64_t z)
     return neg(reduce64((uint64_t)(-z)));
 }
 
+// Field element of a signed 32-bit integer.
+__device__ __forceinline__ uint64_t from_i32(int32_t z)
+{
+    return z >= 0 ? (uint64_t)z : P - (uint64_t)(-(int64_t)z);
+}
+
+// a * 2^k for a canonical a and 0 <= k < 61: 2^61 = 1, so the residue rotates.
+__device__ __forceinline__ uint64_t rotl(uint64_t a, int k)
+{
+    const uint64_t r = ((a << k) & P) | (a >> (61 - k));
+    return r == P ? 0 : r;
+}
+
 // e * z for a field element e and a signed integer |z| < 2^31.
 __device__ __forceinline__ uint64_t mul_small(uint64_t e, int32_t z)
 {

@@ -35,19 +35,42 @@ __device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (
 __device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
 
 // Block layout of the Gram pass.  A block takes a slab of kSlab outputs at a
-// time: phase X (all waves) computes EQ(x), Bx and the digits of every output
-// and transposes the bit words into plane-major masks (64 ballots per 64
-// outputs), all into LDS; phase G then streams the slab through the matrix
-// cores.  Wave w accumulates digit w (two digits per wave with one tile pair)
-// for every tile pair, so all waves issue the same instruction sequence and
-// only the LDS address of their digit bytes differs.
-constexpr int kSlab = 4096;
+// time.  Phase X (all waves, one output per thread) computes EQ(x), Bx and
+// the digits of EQ(x), transposes the wave's 64 bit words into plane-major
+// order (a 64 x 64 bit transpose) and stores every plane as bytes 0x00 / 0xFF
+// (rows padded so that the matrix-core fragment reads are free of bank
+// conflicts).  Phase G streams the slab through the matrix cores: wave w
+// accumulates digits w % 4 and w % 4 + 4 for every tile pair over the
+// K-steps of its group (w / 4); a K-step costs two 16-byte fragment reads
+// per plane tile and one per digit.
+constexpr int kSlab = 1024;
+constexpr int kRow = kSlab + 16;  // bytes per plane row in LDS
 
 template <int TP> struct GramShape {
     static constexpr int kWaves = TP == 1 ? 4 : 8;
-    static constexpr int kDigitsPerWave = kLimbs / kWaves;  // 2 or 1
+    static constexpr int kGroups = kWaves / 4;            // K-step groups
+    static constexpr int kDigitsPerWave = kLimbs / 4;     // 2
     static constexpr int kPlanes = 32 * (TP == 1 ? 1 : 2);
 };
+
+// 64 x 64 bit transpose across a wave: lane i holds row i (bit j = entry
+// (i, j)); afterwards lane j holds column j (bit i = entry (i, j)).  Six
+// butterfly stages, each swapping the off-diagonal j x j blocks of every
+// 2j x 2j block with the partner lane i ^ j.
+__device__ __forceinline__ uint64_t wave_transpose64(uint64_t a)
+{
+    const int lane = threadIdx.x & 63;
+    const uint64_t masks[6] = {0x00000000FFFFFFFFull, 0x0000FFFF0000FFFFull, 0x00FF00FF00FF00FFull,
+                               0x0F0F0F0F0F0F0F0Full, 0x3333333333333333ull, 0x5555555555555555ull};
+#pragma unroll
+    for (int st = 0; st < 6; st++) {
+        const int j = 32 >> st;
+        const uint64_t m = masks[st];
+        const uint64_t b = __shfl_xor(a, j, 64);
+        a = (lane & j) ? ((a & ~m) | ((b & ~m) >> j)) : ((a & m) | ((b & m) << j));
+    }
+    return a;
+}
 
 // Balanced base-256 digits of e < 2^61: e = sum_t 256^t d_t, d_t in [-128, 128).
 __device__ __forceinline__ void balanced_digits(uint64_t e, int8_t (&d)[kLimbs])
@@ -69,13 +92,15 @@ __global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
 {
     using S = GramShape<TP>;
     constexpr int NT = 64 * S::kWaves, NPL = S::kPlanes, DW = S::kDigitsPerWave;
+    constexpr int kPlaneBytes = NPL * kRow, kTileBytes = TP * 1024 * 8;
     __shared__ uint64_t s_lut[8 * 256];                                   // Bx byte tables
     __shared__ uint64_t s_exp[256];                                       // byte -> eight 0x00 / 0xFF bytes
     __shared__ __attribute__((aligned(16))) int8_t s_d[kLimbs][kSlab];    // digits of EQ(x)
-    __shared__ uint64_t s_m[kSlab / 64][NPL];                             // plane masks per 64 outputs
-    // the block's Gram tiles, entry r * 64 + lane of fragment register r; two
-    // halves (digits 0-3, 4-7) so that sums of values below 2^61 cannot wrap
-    __shared__ unsigned long long s_g[2][TP][1024];
+    // plane bytes during the slabs; afterwards the block's Gram tiles (entry
+    // r * 64 + lane of fragment register r)
+    __shared__ __attribute__((aligned(16))) int8_t s_u[kPlaneBytes > kTileBytes ? kPlaneBytes : kTileBytes];
+    int8_t *s_b = s_u;
+    unsigned long long(*s_g)[1024] = (unsigned long long(*)[1024])s_u;
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
     for (int i = tid; i < 8 * 256; i += NT) s_lut[i] = lut[i];
     for (int i = tid; i < 256; i += NT) {
@@ -84,7 +109,6 @@ __global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
             if ((i >> b) & 1) e |= 0xFFull << (8 * b);
         s_exp[i] = e;
     }
-    for (int i = tid; i < 2 * TP * 1024; i += NT) (&s_g[0][0][0])[i] = 0;
     v16i acc[DW][TP];
 #pragma unroll
     for (int k = 0; k < DW; k++)
@@ -96,19 +120,38 @@ __global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
     const uint64_t nslabs = (N + kSlab - 1) / kSlab;
     __syncthreads();
 
+    // the global inputs of a slab (bit words and the two eq factors) are read
+    // one slab ahead, so their latency hides behind the previous slab's phase G
+    constexpr int NIT = kSlab / NT;
+    uint64_t pw_[NIT], pe1[NIT], pe2[NIT];
+    auto fetch = [&](uint64_t sl) {
+#pragma unroll
+        for (int it = 0; it < NIT; it++) {
+            const uint64_t x = sl * kSlab + it * NT + tid;
+            const bool valid = sl < nslabs && x < N;
+            pw_[it] = valid ? bits[x] : 0;
+            pe1[it] = valid ? E1[x >> lk] : 0;
+            pe2[it] = valid ? E2[x & kmask] : 0;
+        }
+    };
+    fetch(blockIdx.x);
     for (uint64_t sl = blockIdx.x; sl < nslabs; sl += gridDim.x) {
         const uint64_t x0 = sl * kSlab;
+        uint64_t cw[NIT], ce1[NIT], ce2[NIT];
+#pragma unroll
+        for (int it = 0; it < NIT; it++) {
+            cw[it] = pw_[it];
+            ce1[it] = pe1[it];
+            ce2[it] = pe2[it];
+        }
+        fetch(sl + gridDim.x);
         // phase X: one output per thread per step, 64 consecutive outputs per wave
-#pragma unroll 2
-        for (int it = 0; it < kSlab / NT; it++) {
+#pragma unroll
+        for (int it = 0; it < NIT; it++) {
             const int xl = it * NT + tid;
             const uint64_t x = x0 + xl;
             const bool valid = x < N;
-            uint64_t w = 0, eqx = 0;
-            if (valid) {
-                w = bits[x];
-                eqx = m61::mul(E1[x >> lk], E2[x & kmask]);
-            }
+            const uint64_t w = cw[it], eqx = m61::mul(ce1[it], ce2[it]);
             uint64_t bx = 0;
 #pragma unroll
             for (int b = 0; b < 8; b++) bx = m61::add(bx, s_lut[b * 256 + ((w >> (8 * b)) & 255)]);
@@ -117,57 +160,74 @@ __global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
             balanced_digits(eqx, d);
 #pragma unroll
             for (int t = 0; t < kLimbs; t++) s_d[t][xl] = d[t];
-            uint64_t mine = 0;  // lane q keeps the mask of plane q
+            const uint64_t pw = wave_transpose64(w);  // lane q: plane q over the wave's 64 outputs
+            if (lane < NPL) {
+                int8_t *row = s_b + lane * kRow + (xl & ~63);
 #pragma unroll
-            for (int q = 0; q < NPL; q++) {
-                const uint64_t m = __ballot((int)((w >> q) & 1));
-                if (lane == q) mine = m;
+                for (int c = 0; c < 4; c++) {
+                    const uint64_t e0 = s_exp[(pw >> (16 * c)) & 255], e1 = s_exp[(pw >> (16 * c + 8)) & 255];
+                    *(v4i *)(row + 16 * c) =
+                        v4i{(int)(uint32_t)e0, (int)(uint32_t)(e0 >> 32), (int)(uint32_t)e1, (int)(uint32_t)(e1 >> 32)};
+                }
             }
-            if (lane < NPL) s_m[xl >> 6][lane] = mine;
         }
         __syncthreads();
         // phase G: 32 outputs per step; fragments of both plane tiles, then
-        // this wave's digit(s) for every tile pair
-        for (int ks = 0; ks < kSlab / 32; ks++) {
-            const int g = ks >> 1, sh = 32 * (ks & 1) + 16 * half, xo = 32 * ks + 16 * half;
-            v4i frag[2], mask[2];
+        // this wave's digits for every tile pair.  The next step's fragments
+        // are read from LDS while the current step's products run.
+        constexpr int NPT = TP == 1 ? 1 : 2;
+        const int8_t *mrow = s_b + (lane & 31) * kRow + 16 * half;
+        const int8_t *drow = &s_d[wv & 3][16 * half];
+        v4i nm[NPT], nd[DW];
+        int ks = wv / 4;
 #pragma unroll
-            for (int pt = 0; pt < (TP == 1 ? 1 : 2); pt++) {
-                const uint32_t sb = (uint32_t)(s_m[g][32 * pt + (lane & 31)] >> sh) & 0xFFFF;
-                const uint64_t e0 = s_exp[sb & 255], e1 = s_exp[sb >> 8];
-                mask[pt] = v4i{(int)(uint32_t)e0, (int)(uint32_t)(e0 >> 32), (int)(uint32_t)e1, (int)(uint32_t)(e1 >> 32)};
-                frag[pt] = mask[pt] & (int)0x01010101;
-            }
+        for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * ks);
+#pragma unroll
+        for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab + 32 * ks);
+        for (; ks < kSlab / 32; ks += S::kGroups) {
+            v4i mask[NPT], frag[NPT], D[DW];
+#pragma unroll
+            for (int pt = 0; pt < NPT; pt++) mask[pt] = nm[pt];
+#pragma unroll
+            for (int k = 0; k < DW; k++) D[k] = nd[k];
+            const int kn = ks + S::kGroups < kSlab / 32 ? ks + S::kGroups : ks;  // last step re-reads (unused)
+#pragma unroll
+            for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * kn);
+#pragma unroll
+            for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab + 32 * kn);
+            __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of this step's products
+#pragma unroll
+            for (int pt = 0; pt < NPT; pt++) frag[pt] = mask[pt] & (int)0x01010101;
 #pragma unroll
             for (int k = 0; k < DW; k++) {
-                const v4i D = *(const v4i *)&s_d[wv + k * S::kWaves][xo];
-                const v4i B0 = mask[0] & D;
+                const v4i B0 = mask[0] & D[k];
                 acc[k][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B0, acc[k][0], 0, 0, 0);
                 if (TP > 1) {
-                    const v4i B1 = mask[1] & D;
+                    const v4i B1 = mask[NPT - 1] & D[k];
                     acc[k][1 % TP] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B1, acc[k][1 % TP], 0, 0, 0);
-                    acc[k][2 % TP] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[1], B1, acc[k][2 % TP], 0, 0, 0);
+                    acc[k][2 % TP] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[NPT - 1], B1, acc[k][2 % TP], 0, 0, 0);
                 }
             }
         }
         __syncthreads();
     }
-    // recombine the digits modulo p into the block's tiles
+    // recombine the digits modulo p into the block's tiles: digit t weighs
+    // 2^(8t), a rotation of the 61-bit residue; each wave folds its two digits
+    // before one LDS atomic per entry (8 waves x values below 2^61 < 2^64)
+    for (int i = tid; i < TP * 1024; i += NT) (&s_g[0][0])[i] = 0;
+    __syncthreads();
+    const int t0 = wv & 3;
 #pragma unroll
-    for (int k = 0; k < DW; k++) {
-        const int t = wv + k * S::kWaves;
-        const uint64_t w256 = 1ull << (8 * t);
+    for (int tp = 0; tp < TP; tp++)
 #pragma unroll
-        for (int tp = 0; tp < TP; tp++)
-#pragma unroll
-            for (int r = 0; r < 16; r++)
-                atomicAdd(&s_g[t < kLimbs / 2 ? 0 : 1][tp][r * 64 + lane],
-                          (unsigned long long)m61::mul(m61::from_i64(acc[k][tp][r]), w256));
-    }
+        for (int r = 0; r < 16; r++) {
+            const uint64_t v0 = m61::rotl(m61::from_i32(acc[0][tp][r]), 8 * t0);
+            const uint64_t v1 = m61::rotl(m61::from_i32(acc[1][tp][r]), 8 * t0 + 32);
+            atomicAdd(&s_g[tp][r * 64 + lane], (unsigned long long)m61::add(v0, v1));
+        }
     __syncthreads();
     for (int i = tid; i < TP * 1024; i += NT)
-        gpart[(size_t)blockIdx.x * TP * 1024 + i] =
-            m61::add(m61::reduce64((&s_g[0][0][0])[i]), m61::reduce64((&s_g[1][0][0])[i]));
+        gpart[(size_t)blockIdx.x * TP * 1024 + i] = m61::reduce64((&s_g[0][0])[i]);
 }
 
 // Sum of the blocks' partial tiles, written as G[q][q'] (64 x 64, both

@@ -140,95 +140,60 @@ void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, ui
 }
 
 // ---------------------------------------------------------------------------
-// All remaining rounds in one workgroup once the tables fit in LDS.
-// Writes the evaluations of every round, the tables' final values, and (if
-// sum_out is set) the hypercube sum of the summand before the first round.
+// All remaining rounds in one workgroup once the tables fit in LDS.  Thread
+// t (< min(h, blockDim)) of round j writes its D + 1 partial evaluations to
+// part + j * stride + (D + 1) t; the assembly reduces them.  Also writes the
+// tables' final values and, with no rounds at all, the sum a b.
 // ---------------------------------------------------------------------------
 template <int KIND>
-__device__ __forceinline__ void tail_body(const TailArgs &in, uint64_t *sm, uint64_t (*pacc)[4][kTailThreads])
+__global__ __launch_bounds__(kTailThreads) void k_tail(TailArgs in)
 {
     constexpr int NT = KindTraits<KIND>::NT, D = KindTraits<KIND>::D;
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, v = in.v;
+    __shared__ uint64_t sm[NT][kTailMax];
+    __shared__ uint64_t rc[kTailMaxLog];  // the rounds' challenges, read once
+    const int tid = threadIdx.x, v = in.v;
     const uint32_t S = 1u << v;
-    uint64_t *T[3] = {sm, sm + kTailMax, sm + 2 * kTailMax};
     const uint64_t *G[3] = {in.t0, in.t1, in.t2};
+    if (tid < v) rc[tid] = in.rho[tid];
     for (uint32_t i = tid; i < S; i += blockDim.x)
 #pragma unroll
-        for (int q = 0; q < NT; q++) T[q][i] = G[q][i];
+        for (int q = 0; q < NT; q++) sm[q][i] = G[q][i];
     __syncthreads();
-    if (v == 0 && in.sum_out && tid == 0) *in.sum_out = m61::mul(T[0][0], T[1][0]);  // no rounds: the sum is a b
+    if (v == 0 && in.sum_out && tid == 0) *in.sum_out = m61::mul(sm[0][0], sm[1][0]);  // no rounds: the sum is a b
     for (int j = 0; j < v; j++) {
         const uint32_t h = S >> (j + 1);
-        const uint64_t r = in.rho[j];
+        const uint64_t r = rc[j];
         uint64_t acc[4] = {0, 0, 0, 0};
         for (uint32_t i = tid; i < h; i += blockDim.x) {
             uint64_t lo[3] = {0, 0, 0}, hi[3] = {0, 0, 0};
 #pragma unroll
             for (int q = 0; q < NT; q++) {
-                lo[q] = T[q][i];
-                hi[q] = T[q][i + h];
+                lo[q] = sm[q][i];
+                hi[q] = sm[q][i + h];
             }
             pair_contrib<KIND>(lo, hi, acc);
 #pragma unroll
-            for (int q = 0; q < NT; q++) T[q][i] = m61::add(lo[q], m61::mul(r, m61::sub(hi[q], lo[q])));
+            for (int q = 0; q < NT; q++) sm[q][i] = m61::add(lo[q], m61::mul(r, m61::sub(hi[q], lo[q])));
         }
+        if ((uint32_t)tid < h)
 #pragma unroll
-        for (int X = 0; X <= D; X++) pacc[j][X][tid] = acc[X];
+            for (int X = 0; X <= D; X++) in.part[(size_t)j * in.stride + (size_t)(D + 1) * tid + X] = acc[X];
         __syncthreads();  // folds of round j visible to round j + 1
     }
-    // per-thread partial sums of every round, reduced once after the last
-    // round (the challenges are known, so no round waits for earlier sums)
-    for (int j = wid; j < v; j += blockDim.x / 64) {
-        uint64_t e[4] = {0, 0, 0, 0};
-#pragma unroll
-        for (int X = 0; X <= D; X++) {
-            uint64_t a = 0;
-            for (int t = lane; t < kTailThreads; t += 64) a = m61::add(a, pacc[j][X][t]);
-            e[X] = m61::wave_sum(a);
-        }
-        if (lane == 0) {
-#pragma unroll
-            for (int X = 0; X <= D; X++) in.evals[(size_t)j * (D + 1) + X] = e[X];
-            if (j == 0 && in.sum_out) *in.sum_out = m61::add(e[0], e[1]);  // claimed sum = g_1(0) + g_1(1)
-        }
-    }
     if (tid == 0) {
-        if (in.fin0) *in.fin0 = T[0][0];
-        if (in.fin1) *in.fin1 = T[1][0];
-        if (NT > 2 && in.fin2) *in.fin2 = T[2][0];
+        if (in.fin0) *in.fin0 = sm[0][0];
+        if (in.fin1) *in.fin1 = sm[1][0];
+        if (NT > 2 && in.fin2) *in.fin2 = sm[NT - 1][0];
     }
-}
-
-template <int KIND>
-__global__ __launch_bounds__(256) void k_tail(TailArgs a)
-{
-    __shared__ uint64_t sm[3 * kTailMax];
-    __shared__ uint64_t pacc[kTailMaxLog][4][kTailThreads];
-    tail_body<KIND>(a, sm, pacc);
 }
 
 size_t tail_capacity(int) { return kTailMax; }
+int tail_units(uint32_t h) { return (int)(h < (uint32_t)kTailThreads ? h : kTailThreads); }
 
-static TailArgs tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
-                          const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out)
+void launch_tail(int kind, const TailArgs &a, hipStream_t st)
 {
-    // finals[0..NT) receive the tables' final values
-    return TailArgs{t0, t1, t2, v, rho, kp, evals, finals, finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr,
-                    sum_out};
-}
-
-void launch_tail(int kind, const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
-                 const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out, hipStream_t st)
-{
-    const TailArgs a = tail_args(t0, t1, t2, v, rho, kp, evals, finals, sum_out);
     (void)kind;
     hipLaunchKernelGGL(k_tail<KIND_MATMUL>, dim3(1), dim3(kTailThreads), 0, st, a);
-}
-
-TailArgs make_tail_args(const uint64_t *t0, const uint64_t *t1, const uint64_t *t2, int v, const uint64_t *rho,
-                        const uint64_t *kp, uint64_t *evals, uint64_t *finals, uint64_t *sum_out)
-{
-    return tail_args(t0, t1, t2, v, rho, kp, evals, finals, sum_out);
 }
 
 // ---------------------------------------------------------------------------

@@ -19,6 +19,8 @@
 // suffix eq vectors (a high part and a low part of the variables), so they
 // cost one product per thread.  The ReLU tables are kept as D and S; the
 // final values give R = (D + S) / 2 and Y = (S - D) / 2.
+#include <algorithm>
+
 #include "common.hpp"
 #include "m61.hpp"
 
@@ -76,7 +78,7 @@ void launch_xsetup(const uint64_t *r, const uint64_t *sigx, const uint64_t *rho2
                        Kz);
 }
 
-// Contributions of one pair with weight w.
+// Contributions of one pair with weight w: range to acc[0..5), ReLU to acc[0..3).
 __device__ __forceinline__ void range_pair(uint64_t w, uint64_t b0, uint64_t b1, uint64_t *acc)
 {
     const uint64_t eb0 = m61::mul(w, b0), eb1 = m61::mul(w, b1);
@@ -93,9 +95,9 @@ __device__ __forceinline__ void relu_pair(uint64_t w, uint64_t d0, uint64_t d1, 
 {
     const uint64_t ed0 = m61::mul(w, d0), ed1 = m61::mul(w, d1);
     const uint64_t ed2 = m61::sub(m61::add(ed1, ed1), ed0), s2 = m61::sub(m61::add(s1, s1), s0);
-    acc[5] = m61::add(acc[5], m61::mul(ed0, s0));
-    acc[6] = m61::add(acc[6], m61::mul(ed1, s1));
-    acc[7] = m61::add(acc[7], m61::mul(ed2, s2));
+    acc[0] = m61::add(acc[0], m61::mul(ed0, s0));
+    acc[1] = m61::add(acc[1], m61::mul(ed1, s1));
+    acc[2] = m61::add(acc[2], m61::mul(ed2, s2));
 }
 
 __device__ __forceinline__ uint64_t fold(uint64_t lo, uint64_t hi, uint64_t z)
@@ -103,42 +105,110 @@ __device__ __forceinline__ uint64_t fold(uint64_t lo, uint64_t hi, uint64_t z)
     return m61::add(lo, m61::mul(z, m61::sub(hi, lo)));
 }
 
+// Sums of NV values over the 64 lanes of the calling wave, written to
+// out[0 .. NV).  Every wave of the block calls it at the same point (it holds
+// a block barrier); `lw` is the wave's own NV * 68 words of LDS.
+template <int NV>
+__device__ __forceinline__ void wave_sums_to(const uint64_t (&v)[NV], uint64_t *lw, uint64_t *out)
+{
+    constexpr int LS = 68;  // padded stride: 16 lanes read 16 distinct bank pairs
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int q = 0; q < NV; q++) lw[q * LS + lane] = v[q];
+    __syncthreads();
+    for (int t = lane; t < 4 * NV; t += 64) {  // four lanes per value, 16 entries each
+        const uint64_t *src = lw + (t >> 2) * LS + (t & 3);
+        uint64_t a0 = 0, a1 = 0;
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+            a0 = m61::add(a0, src[4 * e]);
+            a1 = m61::add(a1, src[4 * e + 4]);
+        }
+        uint64_t sum = m61::add(a0, a1);
+        sum = m61::add(sum, __shfl_xor(sum, 1, 64));
+        sum = m61::add(sum, __shfl_xor(sum, 2, 64));
+        if ((t & 3) == 0) out[t >> 2] = sum;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // C fused rounds j .. j + C - 1 over tables of S = 2^lS entries (lS = lN - j).
-// Thread i (< S' = S / 2^C) owns the entries i + t S' (t < 2^C), the sub-cube
-// of the C variables being bound; it runs the C rounds on them in registers
-// and writes the bound value to index i.  The pair (u, u + h) of local round
-// c has weight eq(r_{j+c+1 .. j+C-1}, u) eq(r_{j+C ..}, i), built from the
-// thread's eq(r_{j+C ..}, i) = HS[.] LS[.] by halving.  With FIRST the inputs
-// are Bx and the integer R, Y; D and S are written.  Partials of round c go to
-// part + c * stride + 8 blk.
+// Sub-cube i (< S' = S / 2^C) is the set of entries i + t S' (t < 2^C), the
+// values of the C variables being bound; one thread runs the C rounds on one
+// sub-cube in registers and writes the bound value to index i.  The pair
+// (u, u + h) of local round c has weight eq(r_{j+c+1 .. j+C-1}, u)
+// eq(r_{j+C ..}, i), built from eq(r_{j+C ..}, i) = HS[.] LS[.] by halving.
+// With ReLU, waves 0-1 of a block run the range instance and waves 2-3 the
+// ReLU instance on the same 128 sub-cubes (so a wave carries half the work);
+// without, all four waves run the range instance.  With FIRST the inputs are
+// Bx and the integer R, Y; D and S are written.  Each wave writes its sums
+// of round c to part + c * stride + 8 unit (range words 0-4, ReLU 5-7).
 // ---------------------------------------------------------------------------
+template <int C>
+__device__ __forceinline__ void x_weights(uint64_t e, const uint64_t *rr, uint64_t (&w)[1 << C])
+{
+    // round c uses w[(1 << (C-1-c)) - 1 + u] (indices 0 .. 2^C - 2)
+    w[0] = e;  // round C - 1 (u empty)
+#pragma unroll
+    for (int c = C - 2; c >= 0; c--) {
+        const int hn = 1 << (C - 1 - c), base = hn - 1, pb = (hn >> 1) - 1;
+        // u = (msb, rest): eq1(r_{j+c+1}, msb) times the weight of `rest` one round later
+#pragma unroll
+        for (int u = 0; u < hn / 2; u++) {
+            const uint64_t hi = m61::mul(rr[c + 1], w[pb + u]);
+            w[base + hn / 2 + u] = hi;
+            w[base + u] = m61::sub(w[pb + u], hi);
+        }
+    }
+}
+
 template <int C, bool FIRST, bool RELU>
 __global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stride)
 {
-    constexpr int NL = 1 << C;
-    __shared__ uint64_t red[m61::block_sum_words(C * (RELU ? 8 : 5), kThreads)];
-    uint64_t acc[C][8];
-#pragma unroll
-    for (int c = 0; c < C; c++)
-#pragma unroll
-        for (int q = 0; q < 8; q++) acc[c][q] = 0;
-    uint64_t ra[C], rz[C], rr[C];
+    constexpr int NL = 1 << C, NPB = RELU ? 128 : 256, NVR = 5 * C, NVZ = 3 * C;
+    __shared__ uint64_t lw[4][NVR * 68];
+    const int tid = threadIdx.x, wv = tid >> 6;
+    const bool zw = RELU && wv >= 2;  // wave-uniform
+    const int lt = RELU ? (tid & 127) : tid;
+    const int unit = RELU ? blockIdx.x * 2 + (wv & 1) : blockIdx.x * 4 + wv;
+    uint64_t accr[C][5], accz[C][3];
 #pragma unroll
     for (int c = 0; c < C; c++) {
-        ra[c] = a.rho_a[c];
-        rz[c] = RELU ? a.rho_z[c] : 0;
+#pragma unroll
+        for (int q = 0; q < 5; q++) accr[c][q] = 0;
+#pragma unroll
+        for (int q = 0; q < 3; q++) accz[c][q] = 0;
+    }
+    uint64_t rz[C], rr[C];
+#pragma unroll
+    for (int c = 0; c < C; c++) {
+        rz[c] = zw ? a.rho_z[c] : a.rho_a[c];
         rr[c] = a.r[a.j + c];
     }
     const uint64_t *hs = a.HS + (1ull << (a.lN - a.L - a.j - C));
     const uint64_t *ls = a.LS + (1ull << a.L);
     const uint64_t lmask = (1ull << a.L) - 1;
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < sub; i += (uint64_t)gridDim.x * blockDim.x) {
-        uint64_t b[NL], d[NL], s[NL];
+    for (uint64_t i = (uint64_t)blockIdx.x * NPB + lt; i < sub; i += (uint64_t)gridDim.x * NPB) {
+        uint64_t w[NL];
+        x_weights<C>(m61::mul(hs[i >> a.L], ls[i & lmask]), rr, w);
+        if (!zw) {
+            uint64_t b[NL];
 #pragma unroll
-        for (int t = 0; t < NL; t++) {
-            b[t] = a.bx[i + t * sub];
-            if (RELU) {
+            for (int t = 0; t < NL; t++) b[t] = a.bx[i + t * sub];
+#pragma unroll
+            for (int c = 0; c < C; c++) {
+                const int h = NL >> (c + 1), base = h - 1;
+#pragma unroll
+                for (int u = 0; u < h; u++) {
+                    range_pair(w[base + u], b[u], b[u + h], accr[c]);
+                    b[u] = fold(b[u], b[u + h], rz[c]);
+                }
+            }
+            a.bx[i] = b[0];
+        } else {
+            uint64_t d[NL], s[NL];
+#pragma unroll
+            for (int t = 0; t < NL; t++) {
                 if (FIRST) {
                     const int64_t R = a.R[i + t * sub], Y = a.Y[i + t * sub];
                     d[t] = m61::from_i64(R - Y);
@@ -148,79 +218,66 @@ __global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stri
                     s[t] = a.s[i + t * sub];
                 }
             }
-        }
-        // weights: round c uses w[(1 << (C-1-c)) - 1 + u] (indices 0 .. NL-2)
-        uint64_t w[NL];
-        w[0] = m61::mul(hs[i >> a.L], ls[i & lmask]);  // round C - 1 (u empty)
 #pragma unroll
-        for (int c = C - 2; c >= 0; c--) {
-            const int hn = 1 << (C - 1 - c), base = hn - 1, pb = (hn >> 1) - 1;
-            // u = (msb, rest): eq1(r_{j+c+1}, msb) times the weight of `rest` one round later
+            for (int c = 0; c < C; c++) {
+                const int h = NL >> (c + 1), base = h - 1;
 #pragma unroll
-            for (int u = 0; u < hn / 2; u++) {
-                const uint64_t hi = m61::mul(rr[c + 1], w[pb + u]);
-                w[base + hn / 2 + u] = hi;
-                w[base + u] = m61::sub(w[pb + u], hi);
-            }
-        }
-#pragma unroll
-        for (int c = 0; c < C; c++) {
-            const int h = NL >> (c + 1), base = h - 1;
-#pragma unroll
-            for (int u = 0; u < h; u++) {
-                range_pair(w[base + u], b[u], b[u + h], acc[c]);
-                b[u] = fold(b[u], b[u + h], ra[c]);
-                if (RELU) {
-                    relu_pair(w[base + u], d[u], d[u + h], s[u], s[u + h], acc[c]);
+                for (int u = 0; u < h; u++) {
+                    relu_pair(w[base + u], d[u], d[u + h], s[u], s[u + h], accz[c]);
                     d[u] = fold(d[u], d[u + h], rz[c]);
                     s[u] = fold(s[u], s[u + h], rz[c]);
                 }
             }
-        }
-        a.bx[i] = b[0];
-        if (RELU) {
             a.d[i] = d[0];
             a.s[i] = s[0];
         }
     }
-    constexpr int NV = RELU ? 8 : 5;
-    uint64_t flat[C * NV];
+    // per-wave sums; the range waves' layout covers both (ReLU values in the first 3 C)
+    uint64_t flat[NVR];
 #pragma unroll
     for (int c = 0; c < C; c++)
 #pragma unroll
-        for (int q = 0; q < NV; q++) flat[c * NV + q] = acc[c][q];
-    m61::block_sum<C * NV>(flat, red);
-    if (threadIdx.x == 0)
-#pragma unroll
-        for (int c = 0; c < C; c++)
-#pragma unroll
-            for (int q = 0; q < 8; q++)
-                a.part[(size_t)c * stride + (size_t)blockIdx.x * 8 + q] = q < NV ? flat[c * NV + q] : 0;
+        for (int q = 0; q < 5; q++) flat[c * 5 + q] = zw ? (q < 3 ? accz[c][q] : 0) : accr[c][q];
+    __shared__ uint64_t tot[4][NVR];
+    wave_sums_to<NVR>(flat, lw[wv], tot[wv]);
+    __syncthreads();
+    const int lane = tid & 63;
+    if (lane < C * 8) {
+        const int c = lane >> 3, q = lane & 7;
+        uint64_t v;
+        if (!zw) v = q < 5 ? tot[wv][c * 5 + q] : 0;
+        else v = tot[wv][c * 5 + q - 5];
+        if (zw ? q >= 5 : (q < 5 || !RELU)) a.part[(size_t)c * stride + (size_t)unit * 8 + q] = v;
+    }
 }
 
-int xround_blocks(uint64_t sub)
+int xround_blocks(uint64_t sub, bool relu)
 {
-    const uint64_t b = (sub + kThreads - 1) / kThreads;
-    return (int)(b < (uint64_t)kMaxBlocks ? (b ? b : 1) : (uint64_t)kMaxBlocks);
+    const uint64_t per = relu ? 128 : 256, cap = relu ? kMaxUnits / 2 : kMaxUnits / 4;
+    const uint64_t b = (sub + per - 1) / per;
+    return (int)(b < cap ? (b ? b : 1) : cap);
 }
+
+int xround_units(uint64_t sub, bool relu) { return xround_blocks(sub, relu) * (relu ? 2 : 4); }
 
 void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, hipStream_t st)
 {
     const uint64_t sub = S >> C;
-    const dim3 g(xround_blocks(sub)), b(kThreads);
+    const dim3 g(xround_blocks(sub, relu)), b(kThreads);
 #define RA_X(CC, F, Z) hipLaunchKernelGGL((k_xrounds<CC, F, Z>), g, b, 0, st, a, sub, stride)
-#define RA_X_FZ(CC)                  \
-    if (first) {                     \
-        if (relu) RA_X(CC, true, true); \
-        else RA_X(CC, true, false);     \
-    } else {                         \
+#define RA_X_FZ(CC)                      \
+    if (first) {                         \
+        if (relu) RA_X(CC, true, true);  \
+        else RA_X(CC, true, false);      \
+    } else {                             \
         if (relu) RA_X(CC, false, true); \
         else RA_X(CC, false, false);     \
     }
     switch (C) {
     case 1: RA_X_FZ(1) break;
     case 2: RA_X_FZ(2) break;
-    default: RA_X_FZ(3) break;
+    case 3: RA_X_FZ(3) break;
+    default: RA_X_FZ(4) break;
     }
 #undef RA_X_FZ
 #undef RA_X
@@ -228,16 +285,23 @@ void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, in
 
 // ---------------------------------------------------------------------------
 // The last v rounds in one workgroup with the tables in LDS.  Round jj pairs
-// i and i + h (h = 2^(v-1-jj)) with weight LS[h + i] = eq(r_>j, i).  Thread
-// t < min(h, blockDim) writes its eight partial sums of round jj to
-// part + jj * stride + 8 t; the assembly reduces them.  With FIRST (no
-// global rounds ran) the inputs are Bx and the integer R, Y.
+// i and i + h (h = 2^(v-1-jj)) with weight LS[h + i] = eq(r_>j, i).  With
+// ReLU the first half of the threads runs the range instance and the second
+// half the ReLU instance; thread t of a half (t < min(h, half)) writes its
+// sums of round jj to part + jj * stride + 8 t (range words 0-4, ReLU 5-7).
+// With FIRST (no global rounds ran) the inputs are Bx and the integer R, Y.
 // ---------------------------------------------------------------------------
 template <bool RELU>
 __global__ __launch_bounds__(kXTailThreads) void k_xtail(XTailArgs a, int first, int stride)
 {
     __shared__ uint64_t Tb[kXTailMax], Td[RELU ? kXTailMax : 1], Ts[RELU ? kXTailMax : 1], W[kXTailMax];
+    constexpr int NH = RELU ? kXTailThreads / 2 : kXTailThreads;  // threads per instance
     const int tid = threadIdx.x, v = a.v, S = 1 << v;
+    const bool zw = RELU && tid >= NH;  // wave-uniform
+    const int lt = zw ? tid - NH : tid;
+    __shared__ uint64_t zc[2][kXTailLog];  // the rounds' challenges, read once
+    if (tid < v) zc[0][tid] = a.rho_a[tid];
+    if (RELU && tid >= 64 && tid < 64 + v) zc[1][tid - 64] = a.rho_z[tid - 64];
     for (int i = tid; i < S; i += blockDim.x) {
         Tb[i] = a.bx[i];
         W[i] = a.LS[i];  // heap entries 1 .. S-1 are the tables of sizes S/2 .. 1
@@ -255,24 +319,34 @@ __global__ __launch_bounds__(kXTailThreads) void k_xtail(XTailArgs a, int first,
     __syncthreads();
     for (int jj = 0; jj < v; jj++) {
         const int h = S >> (jj + 1);
-        const uint64_t za = a.rho_a[jj], zz = RELU ? a.rho_z[jj] : 0;
+        const uint64_t z = zc[zw ? 1 : 0][jj];
         uint64_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int i = tid; i < h; i += blockDim.x) {
-            const uint64_t w = W[h + i];
-            const uint64_t b0 = Tb[i], b1 = Tb[i + h];
-            range_pair(w, b0, b1, acc);
-            Tb[i] = fold(b0, b1, za);
-            if (RELU) {
-                const uint64_t d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
-                relu_pair(w, d0, d1, s0, s1, acc);
-                Td[i] = fold(d0, d1, zz);
-                Ts[i] = fold(s0, s1, zz);
+        if (!zw) {
+            for (int i = lt; i < h; i += NH) {
+                const uint64_t w = W[h + i], b0 = Tb[i], b1 = Tb[i + h];
+                range_pair(w, b0, b1, acc);
+                Tb[i] = fold(b0, b1, z);
+            }
+        } else {
+            for (int i = lt; i < h; i += NH) {
+                const uint64_t w = W[h + i], d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
+                relu_pair(w, d0, d1, s0, s1, acc + 5);
+                Td[i] = fold(d0, d1, z);
+                Ts[i] = fold(s0, s1, z);
             }
         }
-        if (tid < h) {
-            uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)tid;
+        if (lt < h) {
+            uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)lt;
+            if (!zw) {
 #pragma unroll
-            for (int q = 0; q < 8; q++) o[q] = acc[q];
+                for (int q = 0; q < 5; q++) o[q] = acc[q];
+                if (!RELU)
+#pragma unroll
+                    for (int q = 5; q < 8; q++) o[q] = 0;
+            } else {
+#pragma unroll
+                for (int q = 5; q < 8; q++) o[q] = acc[q];
+            }
         }
         __syncthreads();
     }
@@ -285,6 +359,8 @@ __global__ __launch_bounds__(kXTailThreads) void k_xtail(XTailArgs a, int first,
         }
     }
 }
+
+int xtail_units(int h, bool relu) { return std::min(h, relu ? kXTailThreads / 2 : kXTailThreads); }
 
 void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStream_t st)
 {

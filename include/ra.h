@@ -19,8 +19,12 @@
  *   - Pointers named d_* are device pointers (caller-owned, on the device
  *     that was current when the context was created); h_* and the arrays
  *     inside the proof structs are host pointers (caller-owned).
- *   - All device work is enqueued on the context's HIP stream; every call
- *     synchronises that stream before it returns, so outputs are ready.
+ *   - All device work is ordered on the context's HIP stream (the library
+ *     also runs independent kernel chains on a stream of its own, joined back
+ *     before a call's outputs are staged).  By default every call
+ *     synchronises before it returns, so its outputs are ready.  In deferred
+ *     mode (ra_ctx_set_deferred) the proving calls return once their work is
+ *     enqueued and their host outputs are written at ra_ctx_sync.
  *   - A context is not thread-safe.  Contexts on one device may run
  *     concurrently on different streams.
  *   - Dimensions n, m, k are powers of two >= 1 (Sec. III-A-1 assumes
@@ -83,6 +87,27 @@ ra_status ra_ctx_destroy(ra_ctx *ctx);
 /* Number of challenges consumed so far. */
 ra_status ra_ctx_cursor(const ra_ctx *ctx, uint64_t *consumed);
 const char *ra_status_str(ra_status st);
+
+/* Deferred host outputs, for callers that pipeline many layers without
+ * waiting on each call.
+ *   ra_ctx_set_deferred(ctx, 1): from now on ra_sumcheck_matmul_prove and
+ *     ra_range_prove return once their work and the copy of their transcript
+ *     into pinned staging memory are enqueued; ra_rescale_relu_witness does
+ *     the same when the caller gives t (io->t >= 0: the plane count P is then
+ *     known on the host and io->P is set at once), and otherwise waits for t
+ *     and P as in synchronous mode.  The caller keeps every proof struct, its
+ *     evals arrays and the witness info alive and unread until ra_ctx_sync.
+ *     Argument and state errors are still returned by the call itself; errors
+ *     found on the device (a value outside the given range) are returned by
+ *     ra_ctx_sync, after which the per-layer state of the context is not
+ *     meaningful (create a new context to continue).
+ *   ra_ctx_set_deferred(ctx, 0): completes what is pending and returns to
+ *     synchronous calls (a device error found then is kept for ra_ctx_sync).
+ *   ra_ctx_sync: waits for all enqueued work, writes every pending host
+ *     output, and returns the first error met since the last ra_ctx_sync
+ *     (RA_OK if none).  Harmless in synchronous mode. */
+ra_status ra_ctx_set_deferred(ra_ctx *ctx, int on);
+ra_status ra_ctx_sync(ra_ctx *ctx);
 
 /* Kernel timing for benchmarks.  With profiling on, every group of kernel
  * launches (matrix product, bindings, witness passes, plane rounds, global

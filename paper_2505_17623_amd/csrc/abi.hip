@@ -3,6 +3,7 @@
 // of witness.hip and sumcheck.hip for each entry point.
 #include <algorithm>
 #include <cstring>
+#include <functional>
 #include <new>
 #include <vector>
 
@@ -25,7 +26,9 @@ int log2u(uint64_t x)
 
 struct ra_ctx {
     int device = 0;
-    hipStream_t stream = nullptr;
+    hipStream_t stream = nullptr;  // the caller's stream: every call is ordered on it
+    hipStream_t side = nullptr;    // library stream for independent kernel chains within a call
+    hipEvent_t ev[4] = {};         // fork / join events (timing disabled)
     uint64_t *d_chal = nullptr;
     uint64_t n_chal = 0;
     uint64_t cursor = 0;
@@ -47,8 +50,17 @@ struct ra_ctx {
     // scratch
     char *ws = nullptr;
     size_t ws_cap = 0;
-    uint64_t *h_stage = nullptr;  // pinned host staging
-    size_t stage_cap = 0;
+    uint64_t *h_stage = nullptr;  // pinned host staging of the calls' outputs
+    size_t stage_cap = 0, stage_used = 0;
+    // host outputs waiting for their staged words (written at once in
+    // synchronous mode, at ra_ctx_sync in deferred mode)
+    struct Pending {
+        size_t off;
+        std::function<ra_status(const uint64_t *)> fill;
+    };
+    std::vector<Pending> pending;
+    bool deferred = false;
+    ra_status deferred_err = 0;  // first error met while completing deferred outputs
 };
 
 #define RA_HIP(call)                                      \
@@ -79,19 +91,6 @@ ra_status ensure_ws(ra_ctx *c, size_t bytes)
     const size_t want = std::max(bytes + bytes / 4, (size_t)1 << 20);
     if (hipMalloc((void **)&c->ws, want) != hipSuccess) return RA_E_NOMEM;
     c->ws_cap = want;
-    return RA_OK;
-}
-
-ra_status ensure_stage(ra_ctx *c, size_t words)
-{
-    if (words <= c->stage_cap) return RA_OK;
-    RA_HIP(hipStreamSynchronize(c->stream));
-    if (c->h_stage) RA_HIP(hipHostFree(c->h_stage));
-    c->h_stage = nullptr;
-    c->stage_cap = 0;
-    const size_t want = std::max(words, (size_t)4096);
-    if (hipHostMalloc((void **)&c->h_stage, want * 8, hipHostMallocDefault) != hipSuccess) return RA_E_NOMEM;
-    c->stage_cap = want;
     return RA_OK;
 }
 
@@ -134,10 +133,11 @@ hipEvent_t take_event(ra_ctx *c)
 struct Timed {
     ra_ctx *c;
     int g;
+    hipStream_t s;
     hipEvent_t a = nullptr;
-    Timed(ra_ctx *c_, int g_) : c(c_), g(g_)
+    Timed(ra_ctx *c_, int g_, hipStream_t s_ = nullptr) : c(c_), g(g_), s(s_ ? s_ : c_->stream)
     {
-        if (c->prof_on && (a = take_event(c))) (void)hipEventRecord(a, c->stream);
+        if (c->prof_on && (a = take_event(c))) (void)hipEventRecord(a, s);
     }
     ~Timed()
     {
@@ -147,7 +147,7 @@ struct Timed {
             c->ev_pool.push_back(a);
             return;
         }
-        (void)hipEventRecord(b, c->stream);
+        (void)hipEventRecord(b, s);
         c->ev_pending.push_back({g, {a, b}});
     }
 };
@@ -166,12 +166,82 @@ void flush_profile(ra_ctx *c)
     c->ev_pending.clear();
 }
 
-ra_status finish(ra_ctx *c, const uint64_t *d_src, size_t words)
+// `to` waits for everything enqueued on `from` so far (event slot e).
+ra_status order(ra_ctx *c, hipStream_t from, hipStream_t to, int e)
+{
+    RA_HIP(hipEventRecord(c->ev[e], from));
+    RA_HIP(hipStreamWaitEvent(to, c->ev[e], 0));
+    return RA_OK;
+}
+
+// Write every pending host output from its staged words (the stream has been
+// synchronised).  Returns the first error a fill reports.
+ra_status complete(ra_ctx *c)
+{
+    ra_status first = RA_OK;
+    for (auto &p : c->pending) {
+        const ra_status r = p.fill(c->h_stage + p.off);
+        if (first == RA_OK) first = r;
+    }
+    c->pending.clear();
+    c->stage_used = 0;
+    flush_profile(c);
+    return first;
+}
+
+// Wait for all enqueued work and complete the pending outputs.
+ra_status drain(ra_ctx *c)
+{
+    RA_HIP(hipStreamSynchronize(c->stream));
+    return complete(c);
+}
+
+// Stage `words` device words for a call's host outputs and register `fill`
+// to write them.  Synchronous mode: waits and fills before returning (and
+// returns the fill's status).  Deferred mode: returns once the copy is
+// enqueued; ra_ctx_sync fills.
+ra_status finish(ra_ctx *c, const void *d_src, size_t words, std::function<ra_status(const uint64_t *)> fill)
 {
     RA_HIP(hipGetLastError());
-    RA_HIP(hipMemcpyAsync(c->h_stage, d_src, words * 8, hipMemcpyDeviceToHost, c->stream));
-    RA_HIP(hipStreamSynchronize(c->stream));
-    flush_profile(c);
+    const size_t need = (words + 7) & ~(size_t)7;
+    if (c->stage_used + need > c->stage_cap) {  // grow the staging area once what is in it has landed
+        const ra_status r = drain(c);
+        if (r != RA_OK && c->deferred_err == RA_OK) c->deferred_err = r;
+        if (c->h_stage) RA_HIP(hipHostFree(c->h_stage));
+        c->h_stage = nullptr;
+        c->stage_cap = 0;
+        const size_t want = std::max(2 * need, (size_t)4096);
+        if (hipHostMalloc((void **)&c->h_stage, want * 8, hipHostMallocDefault) != hipSuccess) return RA_E_NOMEM;
+        c->stage_cap = want;
+    }
+    const size_t off = c->stage_used;
+    c->stage_used += need;
+    RA_HIP(hipMemcpyAsync(c->h_stage + off, d_src, words * 8, hipMemcpyDeviceToHost, c->stream));
+    c->pending.push_back({off, std::move(fill)});
+    if (c->deferred) return RA_OK;
+    const ra_status r = drain(c);
+    if (r != RA_OK) return r;
+    const ra_status d = c->deferred_err;
+    c->deferred_err = RA_OK;
+    return d;
+}
+
+// Plane count of the bit table for given s, t, relu (the rule of the witness
+// kernel, Sec. III-A-2 and III-B): s + (t + 2) (1 + relu) planes, rounded up to
+// a power of two.
+ra_status plane_params(int s, int t, int relu, int *P, int *lP)
+{
+    if (t > 29) return RA_E_RANGE;
+    if (s + t + 3 > 61) return RA_E_FIELD_TOO_SMALL;
+    const int Q = s + (t + 2) * (relu ? 2 : 1);
+    int p = 1, l = 0;
+    while (p < Q) {
+        p <<= 1;
+        l++;
+    }
+    if (l > kMaxPlaneLog) return RA_E_RANGE;
+    *P = p;
+    *lP = l;
     return RA_OK;
 }
 
@@ -184,25 +254,25 @@ int log2_tail() { return log2u(tail_capacity(0)); }
 // launches while the table exceeds the LDS tail, then the tail.  Round j's
 // width = D + 1 evaluations go to tr[ev_base + width j]; the tables' final
 // values to finals[0..NT); with sum_out >= 0 the claimed sum to tr[sum_out].
-void run_instance(ra_ctx *c, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v, const uint64_t *rho,
-                  const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals, int sum_out,
-                  SlotTable &slots, uint64_t *part, int g_rounds, int g_tail);
+void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v,
+                  const uint64_t *rho, const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals,
+                  int sum_out, SlotTable &slots, uint64_t *part, int g_rounds, int g_tail);
 
 }  // namespace
 
 namespace {
-void run_instance(ra_ctx *c, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v, const uint64_t *rho,
-                  const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals, int sum_out,
-                  SlotTable &slots, uint64_t *part, int g_rounds, int g_tail)
+void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v,
+                  const uint64_t *rho, const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals,
+                  int sum_out, SlotTable &slots, uint64_t *part, int g_rounds, int g_tail)
 {
     const int cmax = fused_rounds_max(kind), lt = log2_tail();
     int j = 0, lS = v;
     while (lS > lt) {
         const int C = std::min(cmax, lS - lt);
         {
-            Timed tm(c, g_rounds);
+            Timed tm(c, g_rounds, st);
             launch_rounds(kind, C, t0, t1, t2, 1ull << lS, rho + j, kp, part + (size_t)slots.count * kPartStride,
-                          kPartStride, c->stream);
+                          kPartStride, st);
         }
         const int nb = round_blocks(1ull << (lS - C));
         for (int r = 0; r < C; r++)
@@ -212,11 +282,11 @@ void run_instance(ra_ctx *c, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2,
         j += C;
     }
     {
-        Timed tm(c, g_tail);
+        Timed tm(c, g_tail, st);
         const TailArgs ta{t0, t1, t2, v - j, rho + j, part + (size_t)slots.count * kPartStride, kPartStride, finals,
                           finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr,
                           (j == 0 && v == 0 && sum_out >= 0) ? tr + sum_out : nullptr};
-        launch_tail(kind, ta, c->stream);
+        launch_tail(kind, ta, st);
     }
     for (int jj = 0; jj < v - j; jj++)
         slots.s[slots.count++] = Slot{tail_units(1u << (v - j - 1 - jj)), width, ev_base + width * (j + jj), SLOT_COPY,
@@ -262,9 +332,15 @@ ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_cha
     if (st == RA_OK && n_challenges &&
         hipMemcpy(c->d_chal, h_challenges, n_challenges * 8, hipMemcpyHostToDevice) != hipSuccess)
         st = RA_E_HIP;
-    if (st == RA_OK && hipMalloc((void **)&c->d_params, sizeof(WitParams)) != hipSuccess) st = RA_E_NOMEM;
-    if (st == RA_OK && hipMalloc((void **)&c->d_claims, 8 * 8) != hipSuccess) st = RA_E_NOMEM;
-    if (st == RA_OK) st = ensure_stage(c, 4096);
+    if (st == RA_OK && hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess) st = RA_E_HIP;
+    for (int e = 0; e < 4 && st == RA_OK; e++)
+        if (hipEventCreateWithFlags(&c->ev[e], hipEventDisableTiming) != hipSuccess) st = RA_E_HIP;
+    static_assert(sizeof(WitParams) <= 64, "parameters precede the claims");
+    if (st == RA_OK && hipMalloc((void **)&c->d_params, 128) != hipSuccess) st = RA_E_NOMEM;
+    if (st == RA_OK) c->d_claims = (uint64_t *)((char *)c->d_params + 64);
+    if (st == RA_OK && hipHostMalloc((void **)&c->h_stage, 4096 * 8, hipHostMallocDefault) != hipSuccess)
+        st = RA_E_NOMEM;
+    if (st == RA_OK) c->stage_cap = 4096;
     if (st != RA_OK) {
         ra_ctx_destroy(c);
         return st;
@@ -279,10 +355,13 @@ ra_status ra_ctx_destroy(ra_ctx *c)
 {
     if (!c) return RA_E_INVAL;
     if (c->stream || c->ws || c->d_chal) (void)hipStreamSynchronize(c->stream);
+    if (c->side) (void)hipStreamSynchronize(c->side);
     if (c->d_chal) (void)hipFree(c->d_chal);
     if (c->d_eq) (void)hipFree(c->d_eq);
+    for (int e = 0; e < 4; e++)
+        if (c->ev[e]) (void)hipEventDestroy(c->ev[e]);
+    if (c->side) (void)hipStreamDestroy(c->side);
     if (c->d_params) (void)hipFree(c->d_params);
-    if (c->d_claims) (void)hipFree(c->d_claims);
     if (c->ws) (void)hipFree(c->ws);
     if (c->h_stage) (void)hipHostFree(c->h_stage);
     flush_profile(c);
@@ -298,11 +377,33 @@ ra_status ra_ctx_cursor(const ra_ctx *c, uint64_t *consumed)
     return RA_OK;
 }
 
+ra_status ra_ctx_set_deferred(ra_ctx *c, int on)
+{
+    if (!c) return RA_E_INVAL;
+    if (!on && c->deferred) {
+        const ra_status r = drain(c);
+        if (r != RA_OK && c->deferred_err == RA_OK) c->deferred_err = r;
+    }
+    c->deferred = on != 0;
+    return RA_OK;
+}
+
+ra_status ra_ctx_sync(ra_ctx *c)
+{
+    if (!c) return RA_E_INVAL;
+    const ra_status r = drain(c);
+    ra_status first = c->deferred_err != RA_OK ? c->deferred_err : r;
+    c->deferred_err = RA_OK;
+    return first;
+}
+
 ra_status ra_ctx_set_profiling(ra_ctx *c, int on)
 {
     if (!c) return RA_E_INVAL;
-    RA_HIP(hipStreamSynchronize(c->stream));
-    flush_profile(c);
+    {
+        const ra_status r = drain(c);
+        if (r != RA_OK && c->deferred_err == RA_OK) c->deferred_err = r;
+    }
     c->prof_on = on != 0;
     for (int g = 0; g < G_COUNT; g++) {
         c->prof_ms[g] = 0;
@@ -335,10 +436,11 @@ ra_status ra_mle_bind(ra_ctx *c, const void *d_T, ra_dtype dtype, uint32_t rows,
     const size_t o_scr = cv.take<uint64_t>(bind_rows ? (size_t)bind_rows_chunks(rows, cols) * cols : 1);
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
-    st = ensure_stage(c, std::max(v, 1));
-    if (st != RA_OK) return st;
     uint64_t *pt = (uint64_t *)(c->ws + o_pt), *eq = (uint64_t *)(c->ws + o_eq), *scr = (uint64_t *)(c->ws + o_scr);
-    RA_HIP(hipStreamSynchronize(c->stream));  // staging buffer is free
+    // a synchronous utility: land any deferred outputs, then use the staging area for the point
+    st = drain(c);
+    if (st != RA_OK && c->deferred_err == RA_OK) c->deferred_err = st;
+    if ((size_t)v > c->stage_cap) return RA_E_INVAL;  // log2 of a 32-bit dimension
     if (v) std::memcpy(c->h_stage, h_point, (size_t)v * 8);
     RA_HIP(hipMemcpyAsync(pt, c->h_stage, (size_t)std::max(v, 1) * 8, hipMemcpyHostToDevice, c->stream));
     launch_eq_table(pt, v, eq, c->stream);
@@ -376,54 +478,56 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     const size_t o_tr = cv.take<uint64_t>(trw);
     const size_t o_gemm = cv.take<char>(gemm_workspace_bytes(a_dtype == RA_I32, n, m, k));
     if ((st = ensure_ws(c, cv.off)) != RA_OK) return st;
-    if ((st = ensure_stage(c, trw)) != RA_OK) return st;
     uint64_t *a = (uint64_t *)(c->ws + o_a), *b = (uint64_t *)(c->ws + o_b);
     uint64_t *scr = (uint64_t *)(c->ws + o_scr), *part = (uint64_t *)(c->ws + o_part), *tr = (uint64_t *)(c->ws + o_tr);
     uint64_t *E1 = c->d_eq, *E2 = c->d_eq + n;
     hipStream_t s = c->stream;
 
+    // the sum-check chain (eq tables, bindings, rounds) runs on the side
+    // stream; the product C, which it does not need, on the caller's stream
+    hipStream_t z = c->side;
+    if ((st = order(c, s, z, 0)) != RA_OK) return st;
     {
-        Timed tm(c, G_EQ);
-        launch_eq_table(r1, ln, E1, s);
-        launch_eq_table(r2, lk, E2, s);
+        Timed tm(c, G_EQ, z);
+        launch_eq_table(r1, ln, E1, z);
+        launch_eq_table(r2, lk, E2, z);
+    }
+    {
+        Timed tm(c, G_BIND_ROWS, z);
+        launch_bind_rows(d_A, a_dtype, n, m, E1, scr, a, z);
+    }
+    {
+        Timed tm(c, G_BIND_COLS, z);
+        launch_bind_cols(d_B, RA_I16, m, k, E2, b, z);
+    }
+    // transcript: [c0][evals 3 lm][a*][b*]
+    SlotTable slots;
+    slots.count = 0;
+    run_instance(c, z, KIND_MATMUL, a, b, nullptr, lm, rho, nullptr, tr, 1, 3, tr + 1 + 3 * lm, 0, slots, part,
+                 G_MM_ROUNDS, G_MM_TAIL);
+    {
+        Timed tm(c, G_ASSEMBLE, z);
+        launch_assemble(slots, part, kPartStride, tr, XConst{}, z);
     }
     {
         Timed tm(c, G_GEMM);
         launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s);
     }
-    {
-        Timed tm(c, G_BIND_ROWS);
-        launch_bind_rows(d_A, a_dtype, n, m, E1, scr, a, s);
-    }
-    {
-        Timed tm(c, G_BIND_COLS);
-        launch_bind_cols(d_B, RA_I16, m, k, E2, b, s);
-    }
-
-    // transcript: [c0][evals 3 lm][a*][b*]
-    SlotTable slots;
-    slots.count = 0;
-    run_instance(c, KIND_MATMUL, a, b, nullptr, lm, rho, nullptr, tr, 1, 3, tr + 1 + 3 * lm, 0, slots, part,
-                 G_MM_ROUNDS, G_MM_TAIL);
-    {
-        Timed tm(c, G_ASSEMBLE);
-        launch_assemble(slots, part, kPartStride, tr, XConst{}, s);
-    }
-    if ((st = finish(c, tr, trw)) != RA_OK) return st;
-
-    const uint64_t *h = c->h_stage;
-    out->log_m = (uint32_t)lm;
-    out->c0 = h[0];
-    if (lm) std::memcpy(out->evals, h + 1, 3 * (size_t)lm * 8);
-    out->a_star = h[1 + 3 * lm];
-    out->b_star = h[2 + 3 * lm];
+    if ((st = order(c, z, s, 1)) != RA_OK) return st;
     c->n = n;
     c->m = m;
     c->k = k;
     c->d_r12 = r1;
     c->phase = 1;
     c->cursor += need;
-    return RA_OK;
+    return finish(c, tr, trw, [out, lm](const uint64_t *h) {
+        out->log_m = (uint32_t)lm;
+        out->c0 = h[0];
+        if (lm) std::memcpy(out->evals, h + 1, 3 * (size_t)lm * 8);
+        out->a_star = h[1 + 3 * lm];
+        out->b_star = h[2 + 3 * lm];
+        return (ra_status)RA_OK;
+    });
 }
 
 ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uint32_t k, int32_t *d_R,
@@ -436,6 +540,14 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
     if (io->s < 1 || io->s > 16 || io->relu > 1 || io->round_mode > 1 || io->t < -1) return RA_E_INVAL;
     const uint64_t N = (uint64_t)n * k;
     if (bits_words < N) return RA_E_BUFSIZE;
+    // with t given and deferred outputs, the plane count is known on the host
+    // and the call need not wait; otherwise it waits for t and P
+    int hP = 0, hlP = 0;
+    const bool known = c->deferred && io->t >= 0;
+    if (known) {
+        const ra_status pst = plane_params((int)io->s, io->t, (int)io->relu, &hP, &hlP);
+        if (pst != RA_OK) return pst;
+    }
     const int nb = witness_blocks(N);
     Carve cv;
     const size_t o_mm = cv.take<int64_t>(2 * (size_t)nb), o_cl = cv.take<uint64_t>(4 * (size_t)nb);
@@ -452,24 +564,42 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
         launch_witness_rescale(d_C, N, lk, c->d_eq, c->d_eq + n, d_R, d_Rm, d_Y, d_Z, d_bits,
                                (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims, c->stream);
     }
-    RA_HIP(hipGetLastError());
-    WitParams prm;
-    RA_HIP(hipMemcpyAsync(&prm, c->d_params, sizeof(prm), hipMemcpyDeviceToHost, c->stream));
-    if ((st = finish(c, c->d_claims, 4)) != RA_OK) return st;
-    if (prm.status != 0) return prm.status;
-    io->t = prm.t;
-    io->P = (uint32_t)prm.P;
-    io->r_claim = c->h_stage[0];
-    io->rm_claim = c->h_stage[1];
-    io->y_claim = c->h_stage[2];
-    io->z_claim = c->h_stage[3];
-    c->s = (int)io->s;
-    c->relu = (int)io->relu;
-    c->mode = (int)io->round_mode;
-    c->t = prm.t;
-    c->P = prm.P;
-    c->phase = 2;
-    return RA_OK;
+    // parameters (words 0-7) and claims (words 8-11) are staged together
+    auto fill = [c, io, known](const uint64_t *h) {
+        WitParams prm;
+        std::memcpy(&prm, h, sizeof(prm));
+        if (prm.status != 0) return (ra_status)prm.status;
+        io->t = prm.t;
+        io->P = (uint32_t)prm.P;
+        io->r_claim = h[8];
+        io->rm_claim = h[9];
+        io->y_claim = h[10];
+        io->z_claim = h[11];
+        if (!known) {  // the layer state advances once t and P are known
+            c->s = (int)io->s;
+            c->relu = (int)io->relu;
+            c->mode = (int)io->round_mode;
+            c->t = prm.t;
+            c->P = prm.P;
+            c->phase = 2;
+        }
+        return (ra_status)RA_OK;
+    };
+    if (known) {
+        c->s = (int)io->s;
+        c->relu = (int)io->relu;
+        c->mode = (int)io->round_mode;
+        c->t = io->t;
+        c->P = hP;
+        c->phase = 2;
+        io->P = (uint32_t)hP;
+        return finish(c, c->d_params, 12, fill);
+    }
+    const bool was = c->deferred;
+    c->deferred = false;  // this call must wait for t and P
+    st = finish(c, c->d_params, 12, fill);
+    c->deferred = was;
+    return st;
 }
 
 ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, const int32_t *d_Y, uint32_t n,
@@ -508,7 +638,6 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const size_t o_gs = cv.take<uint64_t>(64 * 64);
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
-    if ((st = ensure_stage(c, trw)) != RA_OK) return st;
     uint64_t *cst = (uint64_t *)(c->ws + o_cst), *Bx = (uint64_t *)(c->ws + o_bx);
     uint64_t *D = (uint64_t *)(c->ws + o_d), *S = (uint64_t *)(c->ws + o_s);
     uint64_t *HS = (uint64_t *)(c->ws + o_hs), *LS = (uint64_t *)(c->ws + o_ls);
@@ -518,22 +647,30 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const uint64_t *sigx = sigma + lP, *rz = relu ? rho2 : nullptr;
     hipStream_t s = c->stream;
 
+    // side stream: the eq suffix tables (challenges only), then -- once the
+    // Gram pass is done -- the plane-round polynomials; the caller's stream
+    // runs the Gram pass and the rounds over x
+    hipStream_t z = c->side;
+    if ((st = order(c, s, z, 0)) != RA_OK) return st;
+    {
+        Timed tm(c, G_X_SETUP, z);
+        launch_xsetup(c->d_r12, sigx, rz, lN, L, HS, LS, Kr, Kz, z);
+    }
+    RA_HIP(hipEventRecord(c->ev[1], z));
     {
         Timed tm(c, G_RANGE_SETUP);
         launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, lut, s);
     }
     {   // plane rounds: Gram matrix on the matrix cores, Bx per output
         Timed tm(c, G_RANGE_PLANE);
-        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, Bx, gpart, gsum, s);
+        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, Bx, gpart, s);
     }
+    if ((st = order(c, s, z, 2)) != RA_OK) return st;
     {
-        Timed tm(c, G_ASSEMBLE);
-        launch_plane_assemble(lP, gsum, sigma, cst, tr, s);
+        Timed tm(c, G_ASSEMBLE, z);
+        launch_plane_assemble(lP, N, gpart, gsum, sigma, cst, tr, z);
     }
-    {   // rounds over x: the range instance and (same cube, same EQ point) the ReLU zero-check of Eq. (6)
-        Timed tm(c, G_X_SETUP);
-        launch_xsetup(c->d_r12, sigx, rz, lN, L, HS, LS, Kr, Kz, s);
-    }
+    RA_HIP(hipStreamWaitEvent(s, c->ev[1], 0));
     SlotTable slots;
     slots.count = 0;
     int j = 0, lS = lN;
@@ -568,24 +705,24 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
         Timed tm(c, G_ASSEMBLE);
         launch_assemble(slots, part, kPartStride, tr, XConst{cst + C_EP, c->d_r12, Kr, Kz}, s);
     }
-    if ((st = finish(c, tr, trw)) != RA_OK) return st;
-
-    const uint64_t *h = c->h_stage;
-    out->rounds = (uint32_t)R;
-    std::memcpy(out->evals, h, 4 * (size_t)R * 8);
-    out->bits_claim = h[F_R + 1];
-    out->range_sum = h[RS];
-    out->relu_rounds = relu ? (uint32_t)lN : 0;
-    if (relu) {
-        if (lN) std::memcpy(out->relu_evals, h + Z0, 4 * (size_t)lN * 8);
-        out->r_at = h[FZ + 1];
-        out->y_at = h[FZ + 2];
-    } else {
-        out->r_at = out->y_at = 0;
-    }
+    if ((st = order(c, z, s, 3)) != RA_OK) return st;
     c->phase = 0;
     c->cursor += need;
-    return RA_OK;
+    return finish(c, tr, trw, [out, R, relu, lN, F_R, RS, Z0, FZ](const uint64_t *h) {
+        out->rounds = (uint32_t)R;
+        std::memcpy(out->evals, h, 4 * (size_t)R * 8);
+        out->bits_claim = h[F_R + 1];
+        out->range_sum = h[RS];
+        out->relu_rounds = relu ? (uint32_t)lN : 0;
+        if (relu) {
+            if (lN) std::memcpy(out->relu_evals, h + Z0, 4 * (size_t)lN * 8);
+            out->r_at = h[FZ + 1];
+            out->y_at = h[FZ + 2];
+        } else {
+            out->r_at = out->y_at = 0;
+        }
+        return (ra_status)RA_OK;
+    });
 }
 
 }  // extern "C"

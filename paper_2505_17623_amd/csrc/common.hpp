@@ -148,11 +148,12 @@ void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStre
 // ---- launchers (planes.hip) ----
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
-// Bx per x and the Gram matrix G (gsum: 64 x 64 words)
+// Bx per x and the blocks' partial Gram tiles (plane_gram_blocks x tiles x 1024 words)
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, uint64_t *gsum, hipStream_t st);
+                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, hipStream_t st);
+// the Gram matrix G (gsum: 64 x 64 words) from the partial tiles, then the
 // round polynomials of the lP plane rounds into tr[0 .. 4 lP)
-void launch_plane_assemble(int lP, const uint64_t *gsum, const uint64_t *sigma, const uint64_t *cst, uint64_t *tr,
-                           hipStream_t st);
+void launch_plane_assemble(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const uint64_t *sigma,
+                           const uint64_t *cst, uint64_t *tr, hipStream_t st);
 
 }  // namespace ra

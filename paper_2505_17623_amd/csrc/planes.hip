@@ -351,7 +351,7 @@ int plane_gram_blocks(uint64_t N, int lP)
 }
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, uint64_t *gsum, hipStream_t st)
+                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, hipStream_t st)
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
     if (TP == 1)
@@ -360,13 +360,14 @@ void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const u
     else
         hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(64 * GramShape<3>::kWaves), 0, st, bits, N, lk, E1, E2, lut,
                            Bx, gpart);
-    hipLaunchKernelGGL(k_gram_reduce, dim3(TP * 16), dim3(256), 0, st, (const uint64_t *)gpart, nb, TP, gsum);
 }
 
-void launch_plane_assemble(int lP, const uint64_t *gsum, const uint64_t *sigma, const uint64_t *cst, uint64_t *tr,
-                           hipStream_t st)
+void launch_plane_assemble(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const uint64_t *sigma,
+                           const uint64_t *cst, uint64_t *tr, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_plane_assemble, dim3(1), dim3(256), 0, st, gsum, lP, sigma, cst, tr);
+    const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
+    hipLaunchKernelGGL(k_gram_reduce, dim3(TP * 16), dim3(256), 0, st, gpart, nb, TP, gsum);
+    hipLaunchKernelGGL(k_plane_assemble, dim3(1), dim3(256), 0, st, (const uint64_t *)gsum, lP, sigma, cst, tr);
 }
 
 }  // namespace ra

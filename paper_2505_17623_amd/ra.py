@@ -24,7 +24,7 @@ STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_
           -4: "RA_E_RANGE", -5: "RA_E_CHALLENGES", -6: "RA_E_HIP", -7: "RA_E_STATE",
           -8: "RA_E_BUFSIZE", -9: "RA_E_NOMEM"}
 EXPORTS = ["ra_ctx_create", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str", "ra_ctx_set_profiling",
-           "ra_ctx_profile", "ra_mle_bind",
+           "ra_ctx_profile", "ra_ctx_set_deferred", "ra_ctx_sync", "ra_mle_bind",
            "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify"]
 
 
@@ -84,6 +84,8 @@ def lib():
         L.ra_ctx_destroy.argtypes = [vp]
         L.ra_ctx_cursor.argtypes = [vp, u64p]
         L.ra_ctx_set_profiling.argtypes = [vp, ctypes.c_int]
+        L.ra_ctx_set_deferred.argtypes = [vp, ctypes.c_int]
+        L.ra_ctx_sync.argtypes = [vp]
         L.ra_ctx_profile.argtypes = [vp, ctypes.c_uint32, ctypes.POINTER(ctypes.c_char_p),
                                      ctypes.POINTER(ctypes.c_double), u64p]
         L.ra_status_str.restype = ctypes.c_char_p
@@ -100,6 +102,7 @@ def lib():
                                 ctypes.POINTER(LayerTables), ctypes.POINTER(LayerTranscript),
                                 ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
         for f in (L.ra_ctx_create, L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
+                  L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
                   L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify):
             f.restype = ctypes.c_int32
@@ -128,13 +131,42 @@ _DT = {torch.int16: RA_I16, torch.int32: RA_I32, torch.int64: RA_I64}
 class Context:
     """A prover context: the challenge stream on the device plus per-layer state."""
 
-    def __init__(self, challenges, stream: torch.cuda.Stream | None = None):
+    def __init__(self, challenges, stream: torch.cuda.Stream | None = None, deferred: bool = False):
         self._chal, cp = _u64_array(challenges)
         self.stream = stream or torch.cuda.current_stream()
         h = ctypes.c_void_p()
         _check(lib().ra_ctx_create(P61, cp, len(self._chal), ctypes.c_void_p(self.stream.cuda_stream),
                                    ctypes.byref(h)), "ra_ctx_create")
         self.h = h
+        self._fills = []  # Python-side results completed at sync (deferred mode)
+        self.deferred = False
+        if deferred:
+            self.set_deferred(True)
+
+    def set_deferred(self, on: bool):
+        """Deferred mode: proving calls return once enqueued; results are filled by sync()."""
+        _check(lib().ra_ctx_set_deferred(self.h, int(bool(on))), "ra_ctx_set_deferred")
+        if not on:
+            self._run_fills()
+        self.deferred = bool(on)
+
+    def _run_fills(self):
+        fills, self._fills = self._fills, []
+        for f in fills:
+            f()
+
+    def later(self, fill):
+        """Run `fill` now (synchronous mode) or at the next sync (deferred mode)."""
+        if self.deferred:
+            self._fills.append(fill)
+        else:
+            fill()
+
+    def sync(self):
+        """Wait for all enqueued work and complete every deferred result."""
+        code = lib().ra_ctx_sync(self.h)
+        self._run_fills()
+        _check(code, "ra_ctx_sync")
 
     def close(self):
         if self.h:
@@ -181,6 +213,7 @@ def ra_mle_bind(ctx: Context, T: torch.Tensor, bind_rows: bool, point, field: bo
 
 
 def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor):
+    """Returns (C, transcript dict); in deferred mode the dict is filled at ctx.sync()."""
     n, m = A.shape
     m2, k = B.shape
     assert m == m2 and B.dtype == torch.int16
@@ -191,11 +224,16 @@ def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor):
     pr.evals = ev.ctypes.data_as(u64p)
     _check(lib().ra_sumcheck_matmul_prove(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C),
                                           ctypes.byref(pr)), "ra_sumcheck_matmul_prove")
-    return C, dict(c0=int(pr.c0), mm_evals=[int(x) for x in ev[:3 * lm]], a_star=int(pr.a_star),
-                   b_star=int(pr.b_star))
+    res = {}
+    ctx.later(lambda: res.update(c0=int(pr.c0), mm_evals=[int(x) for x in ev[:3 * lm]], a_star=int(pr.a_star),
+                                 b_star=int(pr.b_star)))
+    return C, res
 
 
 def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1):
+    """Returns ((R, Rm, Y, Z, bits), info).  info.t and info.P are set on return
+    (at once when t is given); the claims in info are final after ctx.sync()
+    in deferred mode."""
     n, k = C.shape
     dev = C.device
     R = torch.empty((n, k), dtype=torch.int32, device=dev)
@@ -210,6 +248,7 @@ def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, m
 
 
 def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
+    """Returns the range / ReLU transcript dict (filled at ctx.sync() in deferred mode)."""
     n, k = R.shape
     N = n * k
     lN = N.bit_length() - 1
@@ -221,19 +260,27 @@ def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
     pr.relu_evals = zev.ctypes.data_as(u64p)
     _check(lib().ra_range_prove(ctx.h, _dptr(bits), _dptr(R), _dptr(Y), n, k, ctypes.byref(info),
                                 ctypes.byref(pr)), "ra_range_prove")
-    return dict(rs_evals=[int(x) for x in ev], range_sum=int(pr.range_sum), bits_claim=int(pr.bits_claim),
-                zc_evals=[int(x) for x in zev[:4 * pr.relu_rounds]], r_at=int(pr.r_at), y_at=int(pr.y_at))
+    res = {}
+    ctx.later(lambda: res.update(rs_evals=[int(x) for x in ev], range_sum=int(pr.range_sum),
+                                 bits_claim=int(pr.bits_claim), zc_evals=[int(x) for x in zev[:4 * pr.relu_rounds]],
+                                 r_at=int(pr.r_at), y_at=int(pr.y_at)))
+    return res
 
 
 def prove_layer(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1):
-    """The three calls of one layer; returns device tensors and the transcript."""
+    """The three calls of one layer; returns device tensors and the transcript
+    (complete at once, or after ctx.sync() in deferred mode)."""
     C, mm = ra_sumcheck_matmul_prove(ctx, A, B)
     (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t)
     rs = ra_range_prove(ctx, bits, R, Y, info)
-    tr = dict(mm)
-    tr.update(rs)
-    tr.update(t=int(info.t), P=int(info.P), r_claim=int(info.r_claim), rm_claim=int(info.rm_claim),
-              y_claim=int(info.y_claim), z_claim=int(info.z_claim), s=s, relu=int(bool(relu)), mode=mode)
+    tr = {}
+
+    def fill():
+        tr.update(mm)
+        tr.update(rs)
+        tr.update(t=int(info.t), P=int(info.P), r_claim=int(info.r_claim), rm_claim=int(info.rm_claim),
+                  y_claim=int(info.y_claim), z_claim=int(info.z_claim), s=s, relu=int(bool(relu)), mode=mode)
+    ctx.later(fill)
     return dict(C=C, R=R, Rm=Rm, Y=Y, Z=Z, bits=bits, transcript=tr)
 
 
@@ -241,10 +288,11 @@ def to_device(a: np.ndarray, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
-def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None):
+def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None):
     """Prove every layer of a workload in order.  A layer's input is the
     previous output on the device (MLP chains) or the workload's link (im2col)
-    applied on the host.  X / Bs may hold device copies of the inputs."""
+    applied on the host.  X / Bs may hold device copies of the inputs; ts may
+    give each layer's range parameter t (else it is derived from the data)."""
     X = to_device(workload.X, device) if X is None else X
     Bs = [to_device(L.B, device) for L in workload.layers] if Bs is None else Bs
     outs = []
@@ -256,7 +304,8 @@ def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None):
             A = Z
         else:
             A = to_device(workload.links[li](Z.cpu().numpy()), device)
-        res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode)
+        t = -1 if ts is None else int(ts[li])
+        res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t)
         res["A"] = A
         Z = res["Z"]
         outs.append(res)

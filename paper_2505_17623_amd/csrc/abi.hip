@@ -50,7 +50,8 @@ struct ra_ctx {
     // scratch
     char *ws = nullptr;
     size_t ws_cap = 0;
-    uint64_t *h_stage = nullptr;  // pinned host staging of the calls' outputs
+    uint64_t *h_stage = nullptr;  // pinned host memory the kernels write the calls' outputs to
+    uint64_t *d_stage = nullptr;  // its device address
     size_t stage_cap = 0, stage_used = 0;
     // host outputs waiting for their staged words (written at once in
     // synchronous mode, at ra_ctx_sync in deferred mode)
@@ -196,27 +197,40 @@ ra_status drain(ra_ctx *c)
     return complete(c);
 }
 
-// Stage `words` device words for a call's host outputs and register `fill`
-// to write them.  Synchronous mode: waits and fills before returning (and
-// returns the fill's status).  Deferred mode: returns once the copy is
-// enqueued; ra_ctx_sync fills.
-ra_status finish(ra_ctx *c, const void *d_src, size_t words, std::function<ra_status(const uint64_t *)> fill)
+ra_status alloc_stage(ra_ctx *c, size_t words)
 {
-    RA_HIP(hipGetLastError());
+    if (c->h_stage) RA_HIP(hipHostFree(c->h_stage));
+    c->h_stage = c->d_stage = nullptr;
+    c->stage_cap = 0;
+    if (hipHostMalloc((void **)&c->h_stage, words * 8, hipHostMallocMapped) != hipSuccess) return RA_E_NOMEM;
+    RA_HIP(hipHostGetDevicePointer((void **)&c->d_stage, c->h_stage, 0));
+    c->stage_cap = words;
+    return RA_OK;
+}
+
+// Reserve `words` of pinned host memory for a call's outputs; the kernels
+// write them there directly.  *off receives the offset (host: h_stage + off,
+// device: d_stage + off).  Call before enqueueing the call's kernels.
+ra_status stage_take(ra_ctx *c, size_t words, size_t *off)
+{
     const size_t need = (words + 7) & ~(size_t)7;
-    if (c->stage_used + need > c->stage_cap) {  // grow the staging area once what is in it has landed
+    if (c->stage_used + need > c->stage_cap) {  // grow once what is pending has been written out
         const ra_status r = drain(c);
         if (r != RA_OK && c->deferred_err == RA_OK) c->deferred_err = r;
-        if (c->h_stage) RA_HIP(hipHostFree(c->h_stage));
-        c->h_stage = nullptr;
-        c->stage_cap = 0;
-        const size_t want = std::max(2 * need, (size_t)4096);
-        if (hipHostMalloc((void **)&c->h_stage, want * 8, hipHostMallocDefault) != hipSuccess) return RA_E_NOMEM;
-        c->stage_cap = want;
+        const ra_status a = alloc_stage(c, std::max(2 * need, (size_t)4096));
+        if (a != RA_OK) return a;
     }
-    const size_t off = c->stage_used;
+    *off = c->stage_used;
     c->stage_used += need;
-    RA_HIP(hipMemcpyAsync(c->h_stage + off, d_src, words * 8, hipMemcpyDeviceToHost, c->stream));
+    return RA_OK;
+}
+
+// Register `fill` to turn the call's staged words (at `off`) into its host
+// outputs.  Synchronous mode: waits, fills and returns the fill's status.
+// Deferred mode: returns at once; ra_ctx_sync fills.
+ra_status finish(ra_ctx *c, size_t off, std::function<ra_status(const uint64_t *)> fill)
+{
+    RA_HIP(hipGetLastError());
     c->pending.push_back({off, std::move(fill)});
     if (c->deferred) return RA_OK;
     const ra_status r = drain(c);
@@ -338,9 +352,7 @@ ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_cha
     static_assert(sizeof(WitParams) <= 64, "parameters precede the claims");
     if (st == RA_OK && hipMalloc((void **)&c->d_params, 128) != hipSuccess) st = RA_E_NOMEM;
     if (st == RA_OK) c->d_claims = (uint64_t *)((char *)c->d_params + 64);
-    if (st == RA_OK && hipHostMalloc((void **)&c->h_stage, 4096 * 8, hipHostMallocDefault) != hipSuccess)
-        st = RA_E_NOMEM;
-    if (st == RA_OK) c->stage_cap = 4096;
+    if (st == RA_OK) st = alloc_stage(c, 4096);
     if (st != RA_OK) {
         ra_ctx_destroy(c);
         return st;
@@ -475,11 +487,12 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     const size_t o_a = cv.take<uint64_t>(m), o_b = cv.take<uint64_t>(m);
     const size_t o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n, m) * m);
     const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
-    const size_t o_tr = cv.take<uint64_t>(trw);
     const size_t o_gemm = cv.take<char>(gemm_workspace_bytes(a_dtype == RA_I32, n, m, k));
     if ((st = ensure_ws(c, cv.off)) != RA_OK) return st;
     uint64_t *a = (uint64_t *)(c->ws + o_a), *b = (uint64_t *)(c->ws + o_b);
-    uint64_t *scr = (uint64_t *)(c->ws + o_scr), *part = (uint64_t *)(c->ws + o_part), *tr = (uint64_t *)(c->ws + o_tr);
+    size_t o_tr = 0;
+    if ((st = stage_take(c, trw, &o_tr)) != RA_OK) return st;
+    uint64_t *scr = (uint64_t *)(c->ws + o_scr), *part = (uint64_t *)(c->ws + o_part), *tr = c->d_stage + o_tr;
     uint64_t *E1 = c->d_eq, *E2 = c->d_eq + n;
     hipStream_t s = c->stream;
 
@@ -520,7 +533,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     c->d_r12 = r1;
     c->phase = 1;
     c->cursor += need;
-    return finish(c, tr, trw, [out, lm](const uint64_t *h) {
+    return finish(c, o_tr, [out, lm](const uint64_t *h) {
         out->log_m = (uint32_t)lm;
         out->c0 = h[0];
         if (lm) std::memcpy(out->evals, h + 1, 3 * (size_t)lm * 8);
@@ -554,6 +567,8 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
     const int lk = log2u(k);
+    size_t o_st = 0;
+    if ((st = stage_take(c, 12, &o_st)) != RA_OK) return st;
     {
         Timed tm(c, G_WIT_MINMAX);
         launch_witness_params(d_C, N, (int)io->s, (int)io->relu, (int)io->round_mode, io->t,
@@ -562,7 +577,7 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
     {
         Timed tm(c, G_WIT_RESCALE);
         launch_witness_rescale(d_C, N, lk, c->d_eq, c->d_eq + n, d_R, d_Rm, d_Y, d_Z, d_bits,
-                               (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims, c->stream);
+                               (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims, c->d_stage + o_st, c->stream);
     }
     // parameters (words 0-7) and claims (words 8-11) are staged together
     auto fill = [c, io, known](const uint64_t *h) {
@@ -593,11 +608,11 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
         c->P = hP;
         c->phase = 2;
         io->P = (uint32_t)hP;
-        return finish(c, c->d_params, 12, fill);
+        return finish(c, o_st, fill);
     }
     const bool was = c->deferred;
     c->deferred = false;  // this call must wait for t and P
-    st = finish(c, c->d_params, 12, fill);
+    st = finish(c, o_st, fill);
     c->deferred = was;
     return st;
 }
@@ -632,7 +647,6 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const size_t o_hs = cv.take<uint64_t>(nhs), o_ls = cv.take<uint64_t>(2ull << L);
     const size_t o_kr = cv.take<uint64_t>(lN + 1), o_kz = cv.take<uint64_t>(lN + 1);
     const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
-    const size_t o_tr = cv.take<uint64_t>(trw);
     const size_t o_lut = cv.take<uint64_t>(8 * 256);
     const size_t o_gp = cv.take<uint64_t>((size_t)gblocks * gtiles * 1024);
     const size_t o_gs = cv.take<uint64_t>(64 * 64);
@@ -642,7 +656,9 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     uint64_t *D = (uint64_t *)(c->ws + o_d), *S = (uint64_t *)(c->ws + o_s);
     uint64_t *HS = (uint64_t *)(c->ws + o_hs), *LS = (uint64_t *)(c->ws + o_ls);
     uint64_t *Kr = (uint64_t *)(c->ws + o_kr), *Kz = (uint64_t *)(c->ws + o_kz);
-    uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = (uint64_t *)(c->ws + o_tr);
+    size_t o_tr = 0;
+    if ((st = stage_take(c, trw, &o_tr)) != RA_OK) return st;
+    uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = c->d_stage + o_tr;
     uint64_t *lut = (uint64_t *)(c->ws + o_lut), *gpart = (uint64_t *)(c->ws + o_gp), *gsum = (uint64_t *)(c->ws + o_gs);
     const uint64_t *sigx = sigma + lP, *rz = relu ? rho2 : nullptr;
     hipStream_t s = c->stream;
@@ -708,7 +724,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     if ((st = order(c, z, s, 3)) != RA_OK) return st;
     c->phase = 0;
     c->cursor += need;
-    return finish(c, tr, trw, [out, R, relu, lN, F_R, RS, Z0, FZ](const uint64_t *h) {
+    return finish(c, o_tr, [out, R, relu, lN, F_R, RS, Z0, FZ](const uint64_t *h) {
         out->rounds = (uint32_t)R;
         std::memcpy(out->evals, h, 4 * (size_t)R * 8);
         out->bits_claim = h[F_R + 1];

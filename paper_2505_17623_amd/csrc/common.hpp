@@ -18,6 +18,8 @@ constexpr int kXTailThreads = 1024;
 constexpr int kXFuseMax = 4;           // x rounds fused per global launch
 constexpr int kMaxUnits = 2048;        // partial-sum producers per round (waves or threads)
 constexpr int kPartWidth = 8;          // words per block and round in a partial-sum slot
+
+
 constexpr int kMaxSlots = 96;          // per-call partial-sum slots (rounds)
 constexpr int kMaxPlaneLog = 6;        // bit planes per output <= 64 (one word)
 
@@ -76,9 +78,10 @@ void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, co
 int witness_blocks(uint64_t N);
 void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mode, int t_in, int64_t *mm_part,
                            WitParams *params, hipStream_t st);
+// mirror (optional): 12 words, the parameters (words 0-7) and the claims (8-11)
 void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
                             uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
-                            const WitParams *params, uint64_t *claims_out, hipStream_t st);
+                            const WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st);
 
 // ---- launchers (sumcheck.hip) ----
 int round_blocks(uint64_t h);

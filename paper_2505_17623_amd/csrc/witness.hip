@@ -137,15 +137,16 @@ int witness_blocks(uint64_t N)
     return (int)(b < (uint64_t)kMaxBlocks ? b : (uint64_t)kMaxBlocks);
 }
 
-__global__ __launch_bounds__(256) void k_minmax(const int64_t *__restrict__ C, uint64_t N, int64_t *__restrict__ part)
+__device__ __forceinline__ int64_t rescale(int64_t c, int s, int mode)
+{
+    const int64_t half = mode == RA_ROUND_NEAREST ? (int64_t)1 << (s - 1) : 0;
+    return (c + half) >> s;  // arithmetic shift = floor division by 2^s
+}
+
+// Block min / max of v into (mn, mx) of thread 0.
+__device__ __forceinline__ void block_minmax(int64_t &mn, int64_t &mx)
 {
     __shared__ int64_t smin[4], smax[4];
-    int64_t mn = INT64_MAX, mx = INT64_MIN;
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += (uint64_t)gridDim.x * blockDim.x) {
-        const int64_t c = C[i];
-        mn = c < mn ? c : mn;
-        mx = c > mx ? c : mx;
-    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         const int64_t a = __shfl_xor(mn, off, 64), b = __shfl_xor(mx, off, 64);
@@ -158,47 +159,41 @@ __global__ __launch_bounds__(256) void k_minmax(const int64_t *__restrict__ C, u
         smax[wid] = mx;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x == 0)
         for (int w = 1; w < (int)(blockDim.x >> 6); w++) {
             mn = smin[w] < mn ? smin[w] : mn;
             mx = smax[w] > mx ? smax[w] : mx;
         }
+    __syncthreads();
+}
+
+// Pass 1: min and max of C per block, then one block combines them and sets
+// t, P and the status.
+__global__ __launch_bounds__(256) void k_minmax(const int64_t *__restrict__ C, uint64_t N, int64_t *__restrict__ part)
+{
+    int64_t mn = INT64_MAX, mx = INT64_MIN;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += (uint64_t)gridDim.x * blockDim.x) {
+        const int64_t c = C[i];
+        mn = c < mn ? c : mn;
+        mx = c > mx ? c : mx;
+    }
+    block_minmax(mn, mx);
+    if (threadIdx.x == 0) {
         part[2 * blockIdx.x] = mn;
         part[2 * blockIdx.x + 1] = mx;
     }
 }
 
-__device__ __forceinline__ int64_t rescale(int64_t c, int s, int mode)
-{
-    const int64_t half = mode == RA_ROUND_NEAREST ? (int64_t)1 << (s - 1) : 0;
-    return (c + half) >> s;  // arithmetic shift = floor division by 2^s
-}
-
 __global__ __launch_bounds__(256) void k_wit_params(const int64_t *__restrict__ part, int nblk, int s, int relu,
                                                     int mode, int t_in, WitParams *__restrict__ prm)
 {
-    __shared__ int64_t smin[4], smax[4];
     int64_t mn = INT64_MAX, mx = INT64_MIN;
     for (int b = threadIdx.x; b < nblk; b += blockDim.x) {
         mn = part[2 * b] < mn ? part[2 * b] : mn;
         mx = part[2 * b + 1] > mx ? part[2 * b + 1] : mx;
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const int64_t a = __shfl_xor(mn, off, 64), b = __shfl_xor(mx, off, 64);
-        mn = a < mn ? a : mn;
-        mx = b > mx ? b : mx;
-    }
-    if ((threadIdx.x & 63) == 0) {
-        smin[threadIdx.x >> 6] = mn;
-        smax[threadIdx.x >> 6] = mx;
-    }
-    __syncthreads();
+    block_minmax(mn, mx);
     if (threadIdx.x != 0) return;
-    for (int w = 1; w < (int)(blockDim.x >> 6); w++) {
-        mn = smin[w] < mn ? smin[w] : mn;
-        mx = smax[w] > mx ? smax[w] : mx;
-    }
     WitParams p;
     p.status = 0;
     p.s = s;
@@ -234,6 +229,9 @@ __global__ __launch_bounds__(256) void k_wit_params(const int64_t *__restrict__ 
     *prm = p;
 }
 
+// Pass 2: R, Rm, Y, Z, the bit word and per-block claims, then one block
+// sums the claims (R~, Rm~, Y~, Z~ at (r1, r2)) and mirrors the parameters and
+// claims to `mirror` (12 words) when it is given.
 __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, uint64_t N, int lk,
                                                  const WitParams *__restrict__ prm, const uint64_t *__restrict__ E1,
                                                  const uint64_t *__restrict__ E2, int32_t *__restrict__ R,
@@ -275,15 +273,24 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
 }
 
 __global__ __launch_bounds__(256) void k_claims_final(const uint64_t *__restrict__ part, int nblk,
-                                                      const WitParams *__restrict__ prm, uint64_t *__restrict__ out)
+                                                      const WitParams *__restrict__ prm, uint64_t *__restrict__ out,
+                                                      uint64_t *__restrict__ mirror)
 {
     __shared__ uint64_t red[m61::block_sum_words(4, 256)];
+    const WitParams p = *prm;
     uint64_t acc[4] = {0, 0, 0, 0};
-    for (int b = threadIdx.x; b < nblk; b += blockDim.x)
-        for (int i = 0; i < 4; i++) acc[i] = m61::add(acc[i], part[4 * b + i]);
+    if (p.status == 0)
+        for (int b = threadIdx.x; b < nblk; b += blockDim.x)
+            for (int i = 0; i < 4; i++) acc[i] = m61::add(acc[i], part[4 * b + i]);
     m61::block_sum<4>(acc, red);
-    if (threadIdx.x == 0 && prm->status == 0)
+    if (threadIdx.x != 0) return;
+    if (p.status == 0)
         for (int i = 0; i < 4; i++) out[i] = acc[i];
+    if (mirror) {
+        const uint64_t *pw = (const uint64_t *)prm;
+        for (int i = 0; i < 8; i++) mirror[i] = i * 8 < (int)sizeof(WitParams) ? pw[i] : 0;
+        for (int i = 0; i < 4; i++) mirror[8 + i] = acc[i];
+    }
 }
 
 void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mode, int t_in, int64_t *mm_part,
@@ -291,18 +298,19 @@ void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mo
 {
     const int nb = witness_blocks(N);
     hipLaunchKernelGGL(k_minmax, dim3(nb), dim3(kThreads), 0, st, C, N, mm_part);
-    hipLaunchKernelGGL(k_wit_params, dim3(1), dim3(256), 0, st, (const int64_t *)mm_part, nb, s, relu, mode, t_in, params);
+    hipLaunchKernelGGL(k_wit_params, dim3(1), dim3(256), 0, st, (const int64_t *)mm_part, nb, s, relu, mode, t_in,
+                       params);
 }
 
 void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
                             uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
-                            const WitParams *params, uint64_t *claims_out, hipStream_t st)
+                            const WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st)
 {
     const int nb = witness_blocks(N);
     hipLaunchKernelGGL(k_rescale, dim3(nb), dim3(kThreads), 0, st, C, N, lk, params, E1, E2, R, Rm, Y, Z, bits,
                        claim_part);
     hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, (const uint64_t *)claim_part, nb, params,
-                       claims_out);
+                       claims_out, mirror);
 }
 
 }  // namespace ra

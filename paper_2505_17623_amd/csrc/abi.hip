@@ -520,7 +520,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
                  G_MM_ROUNDS, G_MM_TAIL);
     {
         Timed tm(c, G_ASSEMBLE, z);
-        launch_assemble(slots, part, kPartStride, tr, XConst{}, z);
+        launch_assemble(slots, part, kPartStride, tr, XConst{}, PlaneArgs{}, z);
     }
     {
         Timed tm(c, G_GEMM);
@@ -663,30 +663,16 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const uint64_t *sigx = sigma + lP, *rz = relu ? rho2 : nullptr;
     hipStream_t s = c->stream;
 
-    // side stream: the eq suffix tables (challenges only), then -- once the
-    // Gram pass is done -- the plane-round polynomials; the caller's stream
-    // runs the Gram pass and the rounds over x
-    hipStream_t z = c->side;
-    if ((st = order(c, s, z, 0)) != RA_OK) return st;
-    {
-        Timed tm(c, G_X_SETUP, z);
-        launch_xsetup(c->d_r12, sigx, rz, lN, L, HS, LS, Kr, Kz, z);
-    }
-    RA_HIP(hipEventRecord(c->ev[1], z));
     {
         Timed tm(c, G_RANGE_SETUP);
-        launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, lut, s);
+        const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz};
+        launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, lut, xs, s);
     }
     {   // plane rounds: Gram matrix on the matrix cores, Bx per output
         Timed tm(c, G_RANGE_PLANE);
         launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, Bx, gpart, s);
+        launch_gram_reduce(lP, N, gpart, gsum, s);
     }
-    if ((st = order(c, s, z, 2)) != RA_OK) return st;
-    {
-        Timed tm(c, G_ASSEMBLE, z);
-        launch_plane_assemble(lP, N, gpart, gsum, sigma, cst, tr, z);
-    }
-    RA_HIP(hipStreamWaitEvent(s, c->ev[1], 0));
     SlotTable slots;
     slots.count = 0;
     int j = 0, lS = lN;
@@ -717,11 +703,11 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
         slots.s[slots.count++] = Slot{xtail_units(h, relu != 0), kPartWidth, 4 * (lP + j + jj), SLOT_X, j + jj, -1,
                                       relu ? (int)Z0 + 4 * (j + jj) : -1};
     }
-    {
+    {   // the x rounds' polynomials and (further workgroups) the plane rounds'
         Timed tm(c, G_ASSEMBLE);
-        launch_assemble(slots, part, kPartStride, tr, XConst{cst + C_EP, c->d_r12, Kr, Kz}, s);
+        launch_assemble(slots, part, kPartStride, tr, XConst{cst + C_EP, c->d_r12, Kr, Kz},
+                        PlaneArgs{gsum, sigma, cst, tr, lP}, s);
     }
-    if ((st = order(c, z, s, 3)) != RA_OK) return st;
     c->phase = 0;
     c->cursor += need;
     return finish(c, o_tr, [out, R, relu, lN, F_R, RS, Z0, FZ](const uint64_t *h) {

@@ -62,6 +62,14 @@ struct SlotTable {
     Slot s[kMaxSlots];
 };
 
+// Set-up of the rounds over x (xsetup.hpp): r the EQ point, sigma_x and rho'
+// (nullptr without ReLU), lN variables, L of them in the low part.
+struct XSetupArgs {
+    const uint64_t *r, *sigx, *rho2;
+    int lN, L, nhs;  // nhs = 2^(lN - L) (1 if lN <= L)
+    uint64_t *HS, *LS, *Kr, *Kz;
+};
+
 // ---- launchers (witness.hip) ----
 void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st);
 // ---- launchers (gemm.hip) ----
@@ -109,17 +117,26 @@ void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, ui
 void launch_tail(int kind, const TailArgs &a, hipStream_t st);
 // range constants: lambda/mu/tau_p/sigma_p at `chal`, claims from the witness
 size_t range_consts_words(int lP);
-// also writes the 8 x 256 byte tables of the plane-bound table Bx to lut
+// also writes the 8 x 256 byte tables of the plane-bound table Bx to lut, and
+// (further workgroups) the set-up of the rounds over x
 void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,
-                        uint64_t *tr_range_sum, uint64_t *lut, hipStream_t st);
+                        uint64_t *tr_range_sum, uint64_t *lut, const XSetupArgs &xs, hipStream_t st);
 void init_kernel_attributes();
 // Constants of SLOT_X rounds: kp = (Ep, c) of the range summand, r the EQ
 // point, Kr / Kz the prefix products of the range and ReLU instances.
 struct XConst {
     const uint64_t *kp, *r, *Kr, *Kz;
 };
+// Plane rounds of the range check, evaluated by extra workgroups of the
+// assembly (plane_round.hpp): G, sigma_p, the constant block, transcript
+// words 0 .. 4 lP.  lP = 0: none.
+struct PlaneArgs {
+    const uint64_t *G, *sigma, *cst;
+    uint64_t *tr;
+    int lP;
+};
 void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, const XConst &xc,
-                     hipStream_t st);
+                     const PlaneArgs &pa, hipStream_t st);
 
 // ---- launchers (xrounds.hip) ----
 struct XArgs {
@@ -140,8 +157,7 @@ struct XTailArgs {
     uint64_t *fin_b, *fin_r, *fin_y;
     int v;
 };
-void launch_xsetup(const uint64_t *r, const uint64_t *sigx, const uint64_t *rho2, int lN, int L, uint64_t *HS,
-                   uint64_t *LS, uint64_t *Kr, uint64_t *Kz, hipStream_t st);
+int x_setup_threads(int lN, int L);
 int xround_blocks(uint64_t sub, bool relu);
 int xround_units(uint64_t sub, bool relu);  // partial-sum producers of a launch
 int xtail_units(int h, bool relu);          // ... of a tail round with h pairs
@@ -154,9 +170,7 @@ int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each w
 // Bx per x and the blocks' partial Gram tiles (plane_gram_blocks x tiles x 1024 words)
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
                        const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, hipStream_t st);
-// the Gram matrix G (gsum: 64 x 64 words) from the partial tiles, then the
-// round polynomials of the lP plane rounds into tr[0 .. 4 lP)
-void launch_plane_assemble(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const uint64_t *sigma,
-                           const uint64_t *cst, uint64_t *tr, hipStream_t st);
+// the Gram matrix G (gsum: 64 x 64 words, both triangles) from the partial tiles
+void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, hipStream_t st);
 
 }  // namespace ra

@@ -255,92 +255,6 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict_
     G[q2 * 64 + q] = v;  // symmetric (the same value when the tile is diagonal)
 }
 
-// Round polynomials of the plane rounds from G.  One block of 256 threads;
-// the rounds are independent given G, so all of them are evaluated at once.
-// For round j (ny = 2^(j-1) bound-variable patterns y, np = P / 2^j suffixes p'):
-//   Q_ab(p') = sum_{y,y'} c_y c_y' G[(y,a,p')][(y',b,p')],  L_a(p') = sum_y c_y G[(y,a,p')][(y,a,p')],
-// giving sum_x EQ b_a b_b and sum_x EQ b_a; b_2 = 2 b_1 - b_0 is extrapolated.
-__global__ __launch_bounds__(256) void k_plane_assemble(const uint64_t *__restrict__ Gg, int lP,
-                                                        const uint64_t *__restrict__ sigma,
-                                                        const uint64_t *__restrict__ cst, uint64_t *__restrict__ tr)
-{
-    __shared__ uint64_t G[64][65];
-    __shared__ uint64_t c[64];              // round j's c_y at (1 << (j - 1)) - 1 + y
-    __shared__ uint64_t part[6][96];        // [j][(combo np + p') ny + y]
-    __shared__ uint64_t lin[6][64];         // [j][a np + p']
-    __shared__ uint64_t contrib[6][32][6];  // [j][p'][A0 A1 A2 B0 B1 B2]
-    const int tid = threadIdx.x, P = 1 << lP, nf = 3 * (P / 2);
-    for (int i = tid; i < P * P; i += blockDim.x) G[i / P][i % P] = Gg[(i / P) * 64 + (i % P)];
-    for (int i = tid; i < P - 1; i += blockDim.x) {
-        int j = 1;
-        while (i >= (1 << j) - 1) j++;
-        const int y = i - ((1 << (j - 1)) - 1);
-        uint64_t a = 1;
-        for (int k = 0; k < j - 1; k++) a = m61::mul(a, m61::eq1_bit(sigma[k], (y >> (j - 2 - k)) & 1));
-        c[i] = a;
-    }
-    __syncthreads();
-    for (int t = tid; t < lP * nf; t += blockDim.x) {
-        const int j = t / nf + 1, r = t % nf, ny = 1 << (j - 1), np = P >> j, lo = lP - j;
-        const int combo = r / (np * ny), rem = r % (np * ny), p = rem / ny, y = rem % ny;
-        const int xa = combo == 1 ? 1 : 0, xb = combo == 0 ? 0 : 1;
-        const uint64_t *cj = c + (ny - 1);
-        const int qa = (y << (lo + 1)) | (xa << lo) | p;
-        uint64_t sacc = 0;
-        for (int y2 = 0; y2 < ny; y2++) sacc = m61::add(sacc, m61::mul(cj[y2], G[qa][(y2 << (lo + 1)) | (xb << lo) | p]));
-        part[j - 1][r] = m61::mul(cj[y], sacc);
-    }
-    for (int t = tid; t < lP * P; t += blockDim.x) {
-        const int j = t / P + 1, r = t % P, ny = 1 << (j - 1), np = P >> j, lo = lP - j;
-        if (r >= 2 * np) continue;
-        const int xa = r / np, p = r % np;
-        const uint64_t *cj = c + (ny - 1);
-        uint64_t sacc = 0;
-        for (int y = 0; y < ny; y++) {
-            const int q = (y << (lo + 1)) | (xa << lo) | p;
-            sacc = m61::add(sacc, m61::mul(cj[y], G[q][q]));
-        }
-        lin[j - 1][r] = sacc;
-    }
-    __syncthreads();
-    for (int t = tid; t < lP * 32; t += blockDim.x) {
-        const int j = t / 32 + 1, p = t % 32, ny = 1 << (j - 1), np = P >> j;
-        if (p >= np) continue;
-        uint64_t Q[3] = {0, 0, 0};
-        for (int combo = 0; combo < 3; combo++)
-            for (int y = 0; y < ny; y++) Q[combo] = m61::add(Q[combo], part[j - 1][(combo * np + p) * ny + y]);
-        const uint64_t L0 = lin[j - 1][p], L1 = lin[j - 1][np + p];
-        const uint64_t Q2 = m61::add(m61::sub(m61::mul(4, Q[1]), m61::mul(4, Q[2])), Q[0]);
-        const uint64_t L2 = m61::sub(m61::add(L1, L1), L0);
-        const int oh = P - (P >> (j - 1));
-        const uint64_t e = cst[C_E + oh + p], w2 = cst[C_W2 + oh + p];
-        const uint64_t *Wj = cst + C_W + (2 * P - 2 * (P >> (j - 1)));
-        uint64_t *o = contrib[j - 1][p];
-        o[0] = m61::mul(e, m61::sub(Q[0], L0));
-        o[1] = m61::mul(e, m61::sub(Q[1], L1));
-        o[2] = m61::mul(e, m61::sub(Q2, L2));
-        o[3] = m61::mul(Wj[p], L0);
-        o[4] = m61::mul(Wj[p + np], L1);
-        o[5] = m61::mul(w2, L2);
-    }
-    __syncthreads();
-    if (tid < lP) {
-        const int j = tid + 1, np = P >> j;
-        uint64_t A[4] = {0, 0, 0, 0}, B[4] = {0, 0, 0, 0};
-        for (int p = 0; p < np; p++)
-            for (int X = 0; X < 3; X++) {
-                A[X] = m61::add(A[X], contrib[j - 1][p][X]);
-                B[X] = m61::add(B[X], contrib[j - 1][p][3 + X]);
-            }
-        // quadratic extension to X = 3: f(3) = f(0) + 3 (f(2) - f(1))
-        A[3] = m61::add(A[0], m61::mul(3, m61::sub(A[2], A[1])));
-        B[3] = m61::add(B[0], m61::mul(3, m61::sub(B[2], B[1])));
-        const uint64_t K = cst[C_K + j - 1], tau = cst[C_TAU + j - 1], mu = cst[C_EP + 3];
-        for (int X = 0; X < 4; X++)
-            tr[4 * (j - 1) + X] = m61::add(m61::mul(m61::mul(K, m61::eq1_small(tau, X)), A[X]), m61::mul(mu, B[X]));
-    }
-}
-
 int plane_gram_tiles(int lP) { return lP > 5 ? 3 : 1; }
 
 int plane_gram_blocks(uint64_t N, int lP)
@@ -362,12 +276,10 @@ void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const u
                            Bx, gpart);
 }
 
-void launch_plane_assemble(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const uint64_t *sigma,
-                           const uint64_t *cst, uint64_t *tr, hipStream_t st)
+void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, hipStream_t st)
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
     hipLaunchKernelGGL(k_gram_reduce, dim3(TP * 16), dim3(256), 0, st, gpart, nb, TP, gsum);
-    hipLaunchKernelGGL(k_plane_assemble, dim3(1), dim3(256), 0, st, (const uint64_t *)gsum, lP, sigma, cst, tr);
 }
 
 }  // namespace ra

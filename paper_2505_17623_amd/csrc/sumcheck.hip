@@ -12,6 +12,8 @@
 // rho (T[i + h] - T[i]) for i < h (thread i alone reads i and i + h).
 #include "common.hpp"
 #include "m61.hpp"
+#include "plane_round.hpp"
+#include "xsetup.hpp"
 
 namespace ra {
 
@@ -227,8 +229,12 @@ __global__ __launch_bounds__(256) void k_range_setup(const uint64_t *__restrict_
                                                      const WitParams *__restrict__ prm,
                                                      const uint64_t *__restrict__ claims, int lP,
                                                      uint64_t *__restrict__ cst, uint64_t *__restrict__ range_sum,
-                                                     uint64_t *__restrict__ lut)
+                                                     uint64_t *__restrict__ lut, XSetupArgs xs)
 {
+    if (blockIdx.x > 0) {  // the set-up of the rounds over x
+        x_setup_body(xs, (blockIdx.x - 1) * blockDim.x + threadIdx.x);
+        return;
+    }
     __shared__ uint64_t c[C_WORDS];
     __shared__ uint64_t eqs[64];
     const int P = 1 << lP, tid = threadIdx.x;
@@ -302,10 +308,14 @@ __global__ __launch_bounds__(256) void k_range_setup(const uint64_t *__restrict_
     }
 }
 
+int x_setup_threads(int lN, int L) { return (lN > L ? 1 << (lN - L) : 1) + (1 << (L + 1)); }
+
 void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,
-                        uint64_t *tr_range_sum, uint64_t *lut, hipStream_t st)
+                        uint64_t *tr_range_sum, uint64_t *lut, const XSetupArgs &xs, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_range_setup, dim3(1), dim3(256), 0, st, chal, params, claims, lP, cst, tr_range_sum, lut);
+    const int xb = (x_setup_threads(xs.lN, xs.L) + 255) / 256;
+    hipLaunchKernelGGL(k_range_setup, dim3(1 + xb), dim3(256), 0, st, chal, params, claims, lP, cst, tr_range_sum,
+                       lut, xs);
 }
 
 // ---------------------------------------------------------------------------
@@ -313,10 +323,14 @@ void launch_range_setup(const uint64_t *chal, const WitParams *params, const uin
 // round evaluations (plane rounds combined as described above).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_assemble(SlotTable slots, const uint64_t *__restrict__ part, int part_stride,
-                                                  uint64_t *__restrict__ tr, XConst xc)
+                                                  uint64_t *__restrict__ tr, XConst xc, PlaneArgs pa)
 {
     __shared__ uint64_t red[m61::block_sum_words(kPartWidth, 256)];
     const int si = blockIdx.x;
+    if (si >= slots.count) {  // a plane round
+        plane_round(pa, si - slots.count + 1);
+        return;
+    }
     const Slot sl = slots.s[si];
     const uint64_t *p = part + (size_t)si * part_stride;
     uint64_t acc[kPartWidth] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -346,10 +360,10 @@ __global__ __launch_bounds__(256) void k_assemble(SlotTable slots, const uint64_
 }
 
 void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, const XConst &xc,
-                     hipStream_t st)
+                     const PlaneArgs &pa, hipStream_t st)
 {
-    if (slots.count == 0) return;
-    hipLaunchKernelGGL(k_assemble, dim3(slots.count), dim3(256), 0, st, slots, part, part_stride, tr, xc);
+    if (slots.count + pa.lP == 0) return;
+    hipLaunchKernelGGL(k_assemble, dim3(slots.count + pa.lP), dim3(256), 0, st, slots, part, part_stride, tr, xc, pa);
 }
 
 }  // namespace ra

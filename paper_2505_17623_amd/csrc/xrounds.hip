@@ -26,58 +26,6 @@
 
 namespace ra {
 
-// ---------------------------------------------------------------------------
-// Set-up: suffix eq tables and the prefix products K_j of both instances.
-//   HS heap: table s (2^s entries at offset 2^s) = eq(r_{lN-L-s .. lN-L-1}, .)
-//   LS heap: table s (2^s entries at offset 2^s) = eq(r_{lN-s .. lN-1}, .)
-//   Kr[j] = prod_{l<j} eq1(r_l, sigma_x,l),  Kz[j] = prod_{l<j} eq1(r_l, rho'_l)
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ uint64_t eq_suffix(const uint64_t *r, int first, int s, uint64_t i)
-{
-    uint64_t a = 1;
-    for (int t = 0; t < s; t++) a = m61::mul(a, m61::eq1_bit(r[first + t], (uint32_t)(i >> (s - 1 - t)) & 1u));
-    return a;
-}
-
-__global__ __launch_bounds__(256) void k_xsetup(const uint64_t *__restrict__ r, const uint64_t *__restrict__ sigx,
-                                                const uint64_t *__restrict__ rho2, int lN, int L, int nhs,
-                                                uint64_t *__restrict__ HS, uint64_t *__restrict__ LS,
-                                                uint64_t *__restrict__ Kr, uint64_t *__restrict__ Kz)
-{
-    const int gid = blockIdx.x * blockDim.x + threadIdx.x;
-    const int nls = 1 << (L + 1);
-    if (gid == 0 || gid == 64) {  // two waves walk the prefix products
-        const uint64_t *z = gid == 0 ? sigx : rho2;
-        uint64_t *K = gid == 0 ? Kr : Kz;
-        if (z) {
-            uint64_t a = 1;
-            for (int j = 0; j < lN; j++) {
-                K[j] = a;
-                const uint64_t e = m61::add(m61::mul(r[j], z[j]), m61::mul(m61::sub(1, r[j]), m61::sub(1, z[j])));
-                a = m61::mul(a, e);
-            }
-            K[lN] = a;
-        }
-    }
-    if (gid >= 1 && gid < nhs) {
-        const int s = 31 - __clz(gid);
-        HS[gid] = eq_suffix(r, lN - L - s, s, (uint64_t)(gid - (1 << s)));
-    }
-    const int e = gid - nhs;
-    if (e >= 1 && e < nls) {
-        const int s = 31 - __clz(e);
-        LS[e] = eq_suffix(r, lN - s, s, (uint64_t)(e - (1 << s)));
-    }
-}
-
-void launch_xsetup(const uint64_t *r, const uint64_t *sigx, const uint64_t *rho2, int lN, int L, uint64_t *HS,
-                   uint64_t *LS, uint64_t *Kr, uint64_t *Kz, hipStream_t st)
-{
-    const int nhs = lN > L ? 1 << (lN - L) : 1, total = nhs + (1 << (L + 1));
-    hipLaunchKernelGGL(k_xsetup, dim3((total + 255) / 256), dim3(256), 0, st, r, sigx, rho2, lN, L, nhs, HS, LS, Kr,
-                       Kz);
-}
-
 // Contributions of one pair with weight w: range to acc[0..5), ReLU to acc[0..3).
 __device__ __forceinline__ void range_pair(uint64_t w, uint64_t b0, uint64_t b1, uint64_t *acc)
 {

@@ -636,7 +636,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
 
     const int L = std::min(lN, kXTailLog), nhs = lN > L ? 1 << (lN - L) : 1;
     const int nslots = std::max(lN, 1);
-    if (nslots > kMaxSlots) return RA_E_INVAL;
+    if (nslots > kMaxSlots || lN > 62) return RA_E_INVAL;
     const int gtiles = plane_gram_tiles(lP), gblocks = plane_gram_blocks(N, lP);
     // transcript: [evals 4R][(unused)][bits_claim][range_sum][relu evals 4 lN][(unused)][r_at][y_at]
     const size_t F_R = 4 * (size_t)R, RS = F_R + 2, Z0 = F_R + 3, FZ = Z0 + 4 * (size_t)lN, trw = FZ + 3;

@@ -91,6 +91,19 @@ __device__ __forceinline__ uint64_t wave_sum(uint64_t v)
     return v;
 }
 
+// Inclusive prefix product over the 64 lanes of a wave (lane i gets
+// v_0 v_1 ... v_i); six shift-and-multiply steps.
+__device__ __forceinline__ uint64_t wave_prefix_mul(uint64_t v)
+{
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t u = __shfl_up(v, off, 64);
+        if (lane >= off) v = mul(v, u);
+    }
+    return v;
+}
+
 // LDS words block_sum<NV> needs for a block of nt threads (nt a multiple of 32).
 __host__ __device__ constexpr int block_sum_words(int NV, int nt) { return NV * nt + NV * 16 + NV; }
 

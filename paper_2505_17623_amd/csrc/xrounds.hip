@@ -268,32 +268,71 @@ __global__ __launch_bounds__(kXTailThreads) void k_xtail(XTailArgs a, int first,
     for (int jj = 0; jj < v; jj++) {
         const int h = S >> (jj + 1);
         const uint64_t z = zc[zw ? 1 : 0][jj];
-        uint64_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (!zw) {
-            for (int i = lt; i < h; i += NH) {
-                const uint64_t w = W[h + i], b0 = Tb[i], b1 = Tb[i + h];
-                range_pair(w, b0, b1, acc);
-                Tb[i] = fold(b0, b1, z);
+        if (h > NH / 2) {  // many pairs: one thread per pair
+            uint64_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            if (!zw) {
+                for (int i = lt; i < h; i += NH) {
+                    const uint64_t w = W[h + i], b0 = Tb[i], b1 = Tb[i + h];
+                    range_pair(w, b0, b1, acc);
+                    Tb[i] = fold(b0, b1, z);
+                }
+            } else {
+                for (int i = lt; i < h; i += NH) {
+                    const uint64_t w = W[h + i], d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
+                    relu_pair(w, d0, d1, s0, s1, acc + 5);
+                    Td[i] = fold(d0, d1, z);
+                    Ts[i] = fold(s0, s1, z);
+                }
+            }
+            if (lt < h) {
+                uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)lt;
+                if (!zw) {
+#pragma unroll
+                    for (int q = 0; q < 5; q++) o[q] = acc[q];
+                    if (!RELU)
+#pragma unroll
+                        for (int q = 5; q < 8; q++) o[q] = 0;
+                } else {
+#pragma unroll
+                    for (int q = 5; q < 8; q++) o[q] = acc[q];
+                }
             }
         } else {
-            for (int i = lt; i < h; i += NH) {
-                const uint64_t w = W[h + i], d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
-                relu_pair(w, d0, d1, s0, s1, acc + 5);
-                Td[i] = fold(d0, d1, z);
-                Ts[i] = fold(s0, s1, z);
-            }
-        }
-        if (lt < h) {
-            uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)lt;
-            if (!zw) {
-#pragma unroll
-                for (int q = 0; q < 5; q++) o[q] = acc[q];
-                if (!RELU)
-#pragma unroll
-                    for (int q = 5; q < 8; q++) o[q] = 0;
-            } else {
-#pragma unroll
-                for (int q = 5; q < 8; q++) o[q] = acc[q];
+            // few pairs: four lanes per pair, each at most two products.
+            // Role 0, 1, 2 take the terms at b_0, b_1, b_2 = 2 b_1 - b_0 (range:
+            // w b_a and w b_a^2; ReLU: (w d_a) s_a); role 3 folds the tables.
+            const int role = lt & 3;
+            for (int i = lt >> 2; i < h; i += NH / 4) {
+                const uint64_t w = W[h + i];
+                uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)i;
+                if (!zw) {
+                    const uint64_t b0 = Tb[i], b1 = Tb[i + h];
+                    const uint64_t u = role == 0 ? b0 : role == 1 ? b1 : role == 2 ? m61::sub(m61::add(b1, b1), b0)
+                                                                                   : m61::sub(b1, b0);
+                    const uint64_t xv = m61::mul(role == 3 ? z : w, u);
+                    if (role == 3) {
+                        Tb[i] = m61::add(b0, xv);
+                    } else {
+                        const uint64_t yv = m61::mul(xv, u);
+                        if (role < 2) o[role] = xv;  // A_0, A_1
+                        o[2 + role] = yv;            // Q_0, Q_1, Q_2
+                        if (!RELU && role == 0) o[5] = o[6] = o[7] = 0;
+                    }
+                } else {
+                    const uint64_t d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
+                    const uint64_t u = role == 0 ? d0 : role == 1 ? d1 : role == 2 ? m61::sub(m61::add(d1, d1), d0)
+                                                                                   : m61::sub(d1, d0);
+                    const uint64_t vv = role == 0 ? s0 : role == 1 ? s1 : role == 2 ? m61::sub(m61::add(s1, s1), s0)
+                                                                                    : m61::sub(s1, s0);
+                    const uint64_t xv = m61::mul(role == 3 ? z : w, u);
+                    const uint64_t yv = m61::mul(role == 3 ? z : xv, vv);
+                    if (role == 3) {
+                        Td[i] = m61::add(d0, xv);
+                        Ts[i] = m61::add(s0, yv);
+                    } else {
+                        o[5 + role] = yv;  // Z_0, Z_1, Z_2
+                    }
+                }
             }
         }
         __syncthreads();
@@ -308,7 +347,11 @@ __global__ __launch_bounds__(kXTailThreads) void k_xtail(XTailArgs a, int first,
     }
 }
 
-int xtail_units(int h, bool relu) { return std::min(h, relu ? kXTailThreads / 2 : kXTailThreads); }
+int xtail_units(int h, bool relu)
+{
+    const int nh = relu ? kXTailThreads / 2 : kXTailThreads;
+    return h > nh / 2 ? std::min(h, nh) : h;  // one unit per pair when four lanes share a pair
+}
 
 void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStream_t st)
 {

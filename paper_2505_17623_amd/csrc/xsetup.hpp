@@ -20,18 +20,16 @@ __device__ __forceinline__ uint64_t eq_suffix(const uint64_t *r, int first, int 
 __device__ __forceinline__ void x_setup_body(const XSetupArgs &a, int gid)
 {
     const int lN = a.lN, L = a.L, nhs = a.nhs, nls = 1 << (L + 1);
-    if (gid == 0 || gid == 64) {  // two waves walk the prefix products
-        const uint64_t *z = gid == 0 ? a.sigx : a.rho2;
-        uint64_t *K = gid == 0 ? a.Kr : a.Kz;
-        if (z) {
-            uint64_t acc = 1;
-            for (int j = 0; j < lN; j++) {
-                K[j] = acc;
-                const uint64_t e =
-                    m61::add(m61::mul(a.r[j], z[j]), m61::mul(m61::sub(1, a.r[j]), m61::sub(1, z[j])));
-                acc = m61::mul(acc, e);
-            }
-            K[lN] = acc;
+    if (gid < 128) {  // waves 0 and 1: prefix products of the two instances (lN < 64)
+        const uint64_t *z = gid < 64 ? a.sigx : a.rho2;
+        uint64_t *K = gid < 64 ? a.Kr : a.Kz;
+        const int j = gid & 63;
+        if (z) {  // wave-uniform
+            uint64_t e = 1;
+            if (j < lN) e = m61::add(m61::mul(a.r[j], z[j]), m61::mul(m61::sub(1, a.r[j]), m61::sub(1, z[j])));
+            const uint64_t inc = m61::wave_prefix_mul(e);  // prod_{l <= j}
+            if (j < lN) K[j + 1] = inc;
+            if (j == 0) K[0] = 1;
         }
     }
     if (gid == 1) a.HS[0] = a.LS[0] = 0;  // unused heap slots

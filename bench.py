@@ -27,10 +27,15 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0
-# 32x32->64-bit integer multiply-adds (v_mad_u64_u32 / v_mad_i64_i32): one per
-# lane per clock, 256 CUs x 64 lanes x 2.4 GHz ("ALU peak")
-IMUL_PEAK_G = 256 * 64 * 2.4
+# Peaks (MI355X, published / derived from unit counts, "Roofline"):
+#   hbm   8 TB/s HBM3E
+#   mfma  5.0 POP/s dense int8 matrix-core operations
+#   alu   32-bit integer multiplies (v_mad_u64_u32 partial products), one per
+#         lane per clock: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+PEAKS = {"hbm": (8000.0, "GB/s", 1e9), "mfma": (5000.0, "TOP/s", 1e12),
+         "alu": (256 * 4 * 16 * 2.4, "Gmul/s", 1e9)}
+MULS_PER_FIELD_MUL = 4      # 32x32 -> 64 partial products of a product in F_p, p = 2^61 - 1
+X_TAIL_LOG, X_FUSE_MAX, MM_TAIL_LOG, MM_FUSE = 12, 4, 10, 2
 
 
 def layer_shapes(wl):
@@ -57,52 +62,124 @@ def elements_folded(shapes, planes):
     return tot
 
 
-def add_instance(w, group, v, ntab, cmax, lt=10):
-    """Global (multi-block) launches of one sum-check instance: each fused
-    launch of C rounds reads the 2^lS-entry tables and writes 2^(lS-C)."""
-    lS = v
-    while lS > lt:
-        C = min(cmax, lS - lt)
-        b, a, u = w.get(group, ("hbm", 0, "GB"))
-        w[group] = ("hbm", a + 8 * ntab * ((1 << lS) + (1 << (lS - C))), "GB")
-        lS -= C
-
-
-def add_xrounds(w, v, relu, lt=11, cmax=3):
-    """Global launches of the rounds over x (range instance, and the ReLU
-    zero-check in the same threads): the first launch reads Bx and the integer
-    R, Y; every launch writes the bound tables (Bx, and D, S with ReLU) at
-    2^-C of the size it read."""
-    lS, first = v, True
-    b, a, u = w.get("range_rounds", ("hbm", 0, "GB"))
-    while lS > lt:
-        C = min(cmax, lS - lt)
-        rd = (8 + 8 * relu) if first else (8 + 16 * relu)
-        a += rd * (1 << lS) + (8 + 16 * relu) * (1 << (lS - C))
-        lS -= C
-        first = False
-    w["range_rounds"] = ("hbm", a, "GB")
+def x_schedule(lN):
+    """Rounds over x per global launch, then the tail's, as the library runs them."""
+    L = min(lN, X_TAIL_LOG)
+    launches = []
+    if lN > L:
+        xl = (lN - L + X_FUSE_MAX - 1) // X_FUSE_MAX
+        launches = [(lN - L) // xl + (1 if g < (lN - L) % xl else 0) for g in range(xl)]
+    return launches, L
 
 
 def group_work(shapes, planes):
-    """Algorithmic work per step of each kernel group: (bound, amount, unit)."""
-    w = {}
+    """Algorithmic work per step of each kernel group: {group: (bound, amount)}
+    with amount in bytes (hbm), int8 operations (mfma) or 32-bit multiplies
+    (alu, 4 per field multiplication), plus the fold groups' HBM bytes."""
+    w, hbm2 = {}, {}
 
-    def add(g, bound, amt, unit):
-        b, a, u = w.get(g, (bound, 0, unit))
-        w[g] = (bound, a + amt, u)
+    def add(g, bound, amt, d=w):
+        b, a = d.get(g, (bound, 0))
+        d[g] = (bound, a + amt)
 
     for (n, m, k, ab, _, relu), P in zip(shapes, planes):
         N = n * k
-        add("gemm_mfma", "mfma", 2 * n * m * k, "GOP")                # 2 n m k integer ops (algorithmic)
-        add("bind_rows", "hbm", n * m * ab + 8 * m, "GB")
-        add("bind_cols", "hbm", m * k * 2 + 8 * m, "GB")
-        add("witness_minmax", "hbm", 8 * N, "GB")
-        add("witness_rescale", "hbm", N * (8 + 4 + 2 + 4 + 4 + 8), "GB")  # C in; R, Rm, Y, Z, bits out
-        add("range_plane", "hbm", N * (8 + 8), "GB")                    # bits in; Bx out
-        add_xrounds(w, N.bit_length() - 1, relu)
-        add_instance(w, "matmul_rounds", m.bit_length() - 1, 2, 2)
-    return w
+        LA = 2 if ab == 2 else 4
+        # exact product on the matrix cores: LA x 2 int8 limb products of 2 n m k operations
+        add("gemm_mfma", "mfma", 2 * n * m * k * LA * 2)
+        add("bind_rows", "hbm", n * m * ab + 8 * m)
+        add("bind_cols", "hbm", m * k * 2 + 8 * m)
+        add("witness_minmax", "hbm", 8 * N)
+        add("witness_rescale", "hbm", N * (8 + 4 + 2 + 4 + 4 + 8))  # C in; R, Rm, Y, Z, bits out
+        # Gram matrix of the plane rounds: per output, tile pairs x 32 x 32 x 2 x 8 digits
+        TP = 3 if P > 32 else 1
+        add("range_plane", "mfma", N * TP * 1024 * 2 * 8)
+        # rounds over x: per pair, 6 field products (range) and 7 (ReLU)
+        lN = N.bit_length() - 1
+        per_pair = 6 + 7 * relu
+        launches, L = x_schedule(lN)
+        j = 0
+        first = True
+        for C in launches:
+            lS = lN - j
+            for c in range(C):
+                add("range_rounds", "alu", MULS_PER_FIELD_MUL * per_pair * (1 << (lS - c - 1)))
+            rd = (8 + 8 * relu) if first else (8 + 16 * relu)
+            add("range_rounds", "hbm", rd * (1 << lS) + (8 + 16 * relu) * (1 << (lS - C)), hbm2)
+            first = False
+            j += C
+        for jj in range(lN - j):
+            add("range_tail", "alu", MULS_PER_FIELD_MUL * per_pair * (1 << (lN - j - jj - 1)))
+        # matrix sum-check: per pair 3 products (X = 0, 1, 2) and 2 folds
+        lm = m.bit_length() - 1
+        for jj in range(lm):
+            add("matmul_rounds" if lm - jj > MM_TAIL_LOG else "matmul_tail", "alu",
+                MULS_PER_FIELD_MUL * 5 * (1 << (lm - jj - 1)))
+    return w, hbm2
+
+
+# Kernel -> group, for hardware-counter summaries (rocprofv3 kernel names).
+KERNEL_GROUP = [("k_gemm_mfma", "gemm_mfma"), ("k_split_", "gemm_mfma"), ("k_zero_i64", "gemm_mfma"),
+                ("k_bind_rows", "bind_rows"), ("k_sum_chunks", "bind_rows"), ("k_bind_cols", "bind_cols"),
+                ("k_minmax", "witness_minmax"), ("k_wit_params", "witness_minmax"),
+                ("k_rescale", "witness_rescale"), ("k_claims_final", "witness_rescale"),
+                ("k_plane_gram", "range_plane"), ("k_gram_reduce", "range_plane"),
+                ("k_xrounds", "range_rounds"), ("k_xtail", "range_tail"), ("k_range_setup", "range_setup"),
+                ("k_rounds", "matmul_rounds"), ("k_tail", "matmul_tail"), ("k_eq_table", "eq_table"),
+                ("k_assemble", "assemble")]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def sources_digest():
+    """SHA-256 over the library sources: counters taken on other sources are stale."""
+    import hashlib
+    h = hashlib.sha256()
+    for d in ("paper_2505_17623_amd/csrc", "include"):
+        for f in sorted(os.listdir(os.path.join(ROOT, d))):
+            with open(os.path.join(ROOT, d, f), "rb") as fh:
+                h.update(f.encode() + fh.read())
+    return h.hexdigest()
+
+
+def traffic_of(group, cfg):
+    """Measured HBM bytes per step of a kernel group (profiles/traffic.json), or
+    None when they were taken on other sources or another workload."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except OSError:
+        return None
+    if t.get("sources_sha256") != sources_digest() or t.get("config") != cfg:
+        return None
+    return t["groups"].get(group)
+
+
+def pmc_summary(fetch_csv, write_csv, cfg, steps_run, calib_mib):
+    """HBM bytes per step and kernel group from two rocprofv3 --pmc runs
+    (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the same
+    counter reads for the plain copy of calib_mib MiB that bench.py makes with
+    --copy-calibration."""
+    import csv
+    import collections
+    out = {}
+    for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        per_kernel = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == name:
+                per_kernel[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        copies = [max(v) for k, v in per_kernel.items() if "copyBuffer" in k]
+        factor = max(copies) / (calib_mib * 1024.0)
+        groups = collections.defaultdict(float)
+        for k, v in per_kernel.items():
+            g = next((grp for pre, grp in KERNEL_GROUP if pre in k), None)
+            if g:
+                groups[g] += sum(v) / steps_run / factor * 1024.0  # bytes per step
+        out[name] = (factor, dict(groups))
+    groups = {g: round(out["FETCH_SIZE"][1].get(g, 0) + out["WRITE_SIZE"][1].get(g, 0))
+              for g in set(out["FETCH_SIZE"][1]) | set(out["WRITE_SIZE"][1])}
+    return dict(config=cfg, sources_sha256=sources_digest(), calibration_mib=calib_mib,
+                fetch_factor=round(out["FETCH_SIZE"][0], 4), write_factor=round(out["WRITE_SIZE"][0], 4),
+                groups=groups, fetch=out["FETCH_SIZE"][1], write=out["WRITE_SIZE"][1])
 
 
 def cpu_baseline(cfg):
@@ -137,7 +214,18 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, copy a MIB-sized device buffer once (a plain copy kernel "
                          "of known size, to scale hardware byte counters)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc runs of this bench (FETCH_SIZE, WRITE_SIZE) into "
+                         "profiles/traffic.json and print it; no GPU work")
     args = ap.parse_args()
+    if args.pmc_summary:
+        steps_run = max(args.warmup, 1) + 1 + 2 * args.steps
+        t = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.config, steps_run,
+                        args.copy_calibration or 256)
+        with open(TRAFFIC_FILE, "w") as fh:
+            json.dump(t, fh, indent=1)
+        print(json.dumps(t, indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py: this prover runs on one GPU; --gpus {args.gpus} is not supported "
               f"(sharding is described in DESIGN.md but not built)", file=sys.stderr)
@@ -201,28 +289,26 @@ def main():
     value = el * args.steps / elapsed
 
     # roofline of the dominant kernel group
-    work = group_work(shapes, planes)
+    work, fold_bytes = group_work(shapes, planes)
     dom = max((g for g in prof if g in work), key=lambda g: prof[g][0])
-    bound, amount, unit = work[dom]
+    bound, amount = work[dom]
+    peak, runit, scale = PEAKS[bound]
     dom_ms, dom_launches = prof[dom]
     dom_s_per_step = dom_ms / 1e3 / args.steps
-    if bound == "hbm":
-        achieved, peak, runit = amount / dom_s_per_step / 1e9, HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved, peak, runit = amount / dom_s_per_step / 1e9, IMUL_PEAK_G, "Gimul/s"
+    achieved = amount / dom_s_per_step / scale
     roofline = dict(kernel=dom, bound=bound, achieved=round(achieved, 2), peak=peak, unit=runit,
-                    frac=round(achieved / peak, 4), traffic=None,
+                    frac=round(achieved / peak, 4), traffic=traffic_of(dom, args.config),
                     launches_per_step=dom_launches / args.steps, ms_per_step=round(dom_ms / args.steps, 4))
     groups = {g: dict(ms_per_step=round(v[0] / args.steps, 4), launches_per_step=v[1] / args.steps)
               for g, v in sorted(prof.items(), key=lambda kv: -kv[1][0]) if v[1]}
     for g, d in groups.items():
-        if g in work:
-            b, a, u = work[g]
-            s_per = d["ms_per_step"] / 1e3
-            if s_per > 0:
-                d["achieved"] = round(a / s_per / 1e9, 2)
-                d["unit"] = "GB/s" if b == "hbm" else "Gimul/s"
-                d["frac"] = round(d["achieved"] / (HBM_PEAK_GBS if b == "hbm" else IMUL_PEAK_G), 4)
+        s_per = d["ms_per_step"] / 1e3
+        if g in work and s_per > 0:
+            b, a = work[g]
+            pk, u, sc = PEAKS[b]
+            d.update(bound=b, achieved=round(a / s_per / sc, 2), unit=u, frac=round(a / s_per / sc / pk, 4))
+        if g in fold_bytes and s_per > 0:
+            d["hbm_frac"] = round(fold_bytes[g][1] / s_per / 1e9 / PEAKS["hbm"][0], 4)
 
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device=dev).fill_(1)

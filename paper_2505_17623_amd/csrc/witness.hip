@@ -6,6 +6,8 @@
 
 namespace ra {
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+
 // ---------------------------------------------------------------------------
 // eq table (Eq. (1) / chi vector of Sec. II-C):
 //   out[i] = prod_j (z_j i_j + (1 - z_j)(1 - i_j)),  i_1 = MSB of i.
@@ -114,9 +116,60 @@ void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, co
     hipLaunchKernelGGL(k_sum_chunks, dim3((cols + 255) / 256), dim3(256), 0, st, (const uint64_t *)scratch, nch, cols, out);
 }
 
+// int16 entries, cols >= 8: E[c] = e_hi 2^31 + e_lo (e_lo < 2^31), so
+// sum_c E[c] z_c = 2^31 sum e_hi z + sum e_lo z with both sums exact in int64
+// (|e z| < 2^46, at most cols / 64 terms per lane): two v_mad_i64_i32 per
+// entry and one reduction mod p per lane.  A wave takes four rows and reads
+// each eq value once for all of them; lanes take 8 consecutive columns (one
+// 16-byte load per row).
+constexpr int kBindRowsPerWave = 4;
+
+__global__ __launch_bounds__(256) void k_bind_cols16(const int16_t *__restrict__ B, uint32_t rows, uint32_t cols,
+                                                     const uint64_t *__restrict__ E, uint64_t *__restrict__ out)
+{
+    constexpr int RW = kBindRowsPerWave;
+    const uint32_t r0 = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) * RW;  // wave-uniform
+    const int lane = threadIdx.x & 63;
+    if (r0 >= rows) return;
+    int64_t lo[RW], hi[RW];
+#pragma unroll
+    for (int rr = 0; rr < RW; rr++) lo[rr] = hi[rr] = 0;
+    for (uint32_t c0 = 8 * lane; c0 < cols; c0 += 512) {
+        int32_t el[8], eh[8];
+#pragma unroll
+        for (int t = 0; t < 8; t++) {
+            const uint64_t e = E[c0 + t];
+            el[t] = (int32_t)(e & 0x7FFFFFFFull);
+            eh[t] = (int32_t)(e >> 31);
+        }
+#pragma unroll
+        for (int rr = 0; rr < RW; rr++) {
+            if (r0 + rr >= rows) break;
+            const v4i z4 = *(const v4i *)&B[(size_t)(r0 + rr) * cols + c0];
+#pragma unroll
+            for (int t = 0; t < 8; t++) {
+                const int32_t z = (int32_t)(int16_t)(z4[t >> 1] >> (16 * (t & 1)));
+                lo[rr] += (int64_t)el[t] * z;
+                hi[rr] += (int64_t)eh[t] * z;
+            }
+        }
+    }
+#pragma unroll
+    for (int rr = 0; rr < RW; rr++) {
+        const uint64_t v = m61::wave_sum(m61::add(m61::from_i64(lo[rr]), m61::rotl(m61::from_i64(hi[rr]), 31)));
+        if (lane == 0 && r0 + rr < rows) out[r0 + rr] = v;
+    }
+}
+
 void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *out,
                       hipStream_t st)
 {
+    if (dtype == RA_I16 && cols >= 8 && ((uintptr_t)T & 15) == 0) {
+        const uint32_t waves = (rows + kBindRowsPerWave - 1) / kBindRowsPerWave;
+        hipLaunchKernelGGL(k_bind_cols16, dim3((waves + 3) / 4), dim3(256), 0, st, (const int16_t *)T, rows, cols, E,
+                           out);
+        return;
+    }
     dim3 grid((rows + 3) / 4);  // four waves (rows) per block
     switch (dtype) {
     case RA_I16: hipLaunchKernelGGL(k_bind_cols<int16_t>, grid, dim3(256), 0, st, (const int16_t *)T, rows, cols, E, out); break;

@@ -34,23 +34,23 @@ __host__ __device__ constexpr int frag_row(int l, int r) { return 8 * (r / 4) + 
 __device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (tp == 2 ? 1 : 0); }
 __device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
 
-// Block layout of the Gram pass.  A block takes a slab of kSlab outputs at a
-// time.  Phase X (all waves, one output per thread) computes EQ(x), Bx and
-// the digits of EQ(x), transposes the wave's 64 bit words into plane-major
-// order (a 64 x 64 bit transpose) and stores every plane as bytes 0x00 / 0xFF
-// (rows padded so that the matrix-core fragment reads are free of bank
-// conflicts).  Phase G streams the slab through the matrix cores: wave w
-// accumulates digits w % 4 and w % 4 + 4 for every tile pair over the
-// K-steps of its group (w / 4); a K-step costs two 16-byte fragment reads
-// per plane tile and one per digit.
-constexpr int kSlab = 1024;
+// Block layout of the Gram pass: twelve waves with two roles, working on
+// slabs of kSlab outputs through a double-buffered LDS area.
+//   producers (waves 0-7, one output per thread): EQ(x), Bx and the digits
+//     of EQ(x); the wave's 64 bit words transposed into plane-major order (a
+//     64 x 64 bit transpose) and stored as bytes 0x00 / 0xFF, rows padded so
+//     the matrix-core fragment reads are free of bank conflicts;
+//   consumers (waves 8-15, two per SIMD): wave c accumulates digit c for
+//     every tile pair over the slab's K-steps on the matrix cores.
+// While the consumers stream slab i the producers build slab i + 1; one
+// barrier per slab hands the buffers over.
+constexpr int kSlab = 512;
 constexpr int kRow = kSlab + 16;  // bytes per plane row in LDS
+constexpr int kProducers = 8, kConsumers = 8, kGramThreads = 64 * (kProducers + kConsumers);
 
 template <int TP> struct GramShape {
-    static constexpr int kWaves = TP == 1 ? 4 : 8;
-    static constexpr int kGroups = kWaves / 4;            // K-step groups
-    static constexpr int kDigitsPerWave = kLimbs / 4;     // 2
     static constexpr int kPlanes = 32 * (TP == 1 ? 1 : 2);
+    static constexpr int kDigitsPerWave = kLimbs / kConsumers;  // 1
 };
 
 // 64 x 64 bit transpose across a wave: lane i holds row i (bit j = entry
@@ -85,148 +85,142 @@ __device__ __forceinline__ void balanced_digits(uint64_t e, int8_t (&d)[kLimbs])
 }
 
 template <int TP>
-__global__ __launch_bounds__(64 * GramShape<TP>::kWaves) void k_plane_gram(
+__global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const uint64_t *__restrict__ bits, uint64_t N, int lk, const uint64_t *__restrict__ E1,
     const uint64_t *__restrict__ E2, const uint64_t *__restrict__ lut, uint64_t *__restrict__ Bx,
     uint64_t *__restrict__ gpart)
 {
     using S = GramShape<TP>;
-    constexpr int NT = 64 * S::kWaves, NPL = S::kPlanes, DW = S::kDigitsPerWave;
+    constexpr int NPL = S::kPlanes, DW = S::kDigitsPerWave, NPT = TP == 1 ? 1 : 2;
+    constexpr int NP = 64 * kProducers;               // producer threads
     constexpr int kPlaneBytes = NPL * kRow, kTileBytes = TP * 1024 * 8;
-    __shared__ uint64_t s_lut[8 * 256];                                   // Bx byte tables
-    __shared__ uint64_t s_exp[256];                                       // byte -> eight 0x00 / 0xFF bytes
-    __shared__ __attribute__((aligned(16))) int8_t s_d[kLimbs][kSlab];    // digits of EQ(x)
-    // plane bytes during the slabs; afterwards the block's Gram tiles (entry
+    static_assert(2 * kPlaneBytes >= kTileBytes, "the tiles reuse the plane buffers");
+    __shared__ uint64_t s_lut[8 * 256];                                    // Bx byte tables
+    __shared__ uint64_t s_exp[256];                                        // byte -> eight 0x00 / 0xFF bytes
+    __shared__ __attribute__((aligned(16))) int8_t s_d[2][kLimbs][kSlab];  // digits of EQ(x)
+    // plane bytes of two slabs; afterwards the block's Gram tiles (entry
     // r * 64 + lane of fragment register r)
-    __shared__ __attribute__((aligned(16))) int8_t s_u[kPlaneBytes > kTileBytes ? kPlaneBytes : kTileBytes];
-    int8_t *s_b = s_u;
+    __shared__ __attribute__((aligned(16))) int8_t s_u[2 * kPlaneBytes];
     unsigned long long(*s_g)[1024] = (unsigned long long(*)[1024])s_u;
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
-    for (int i = tid; i < 8 * 256; i += NT) s_lut[i] = lut[i];
-    for (int i = tid; i < 256; i += NT) {
+    const bool producer = wv < kProducers;  // wave-uniform
+    const int cw = wv - kProducers;         // consumer index = its digit
+    for (int i = tid; i < 8 * 256; i += kGramThreads) s_lut[i] = lut[i];
+    for (int i = tid; i < 256; i += kGramThreads) {
         uint64_t e = 0;
         for (int b = 0; b < 8; b++)
             if ((i >> b) & 1) e |= 0xFFull << (8 * b);
         s_exp[i] = e;
     }
-    v16i acc[DW][TP];
+    const uint64_t kmask = (1ull << lk) - 1;
+    const uint64_t nslabs = (N + kSlab - 1) / kSlab;
+    const uint64_t mine = nslabs > blockIdx.x ? (nslabs - blockIdx.x + gridDim.x - 1) / gridDim.x : 0;
+    __syncthreads();  // byte tables ready
+    // The two roles run separate loops with the same barriers (one per slab),
+    // so the consumers' accumulators are not live in the producers' code.
+    if (producer) {
+        // a slab's global inputs are read one slab ahead
+        uint64_t pw = 0, pe1 = 0, pe2 = 0;
+        auto fetch = [&](uint64_t i) {
+            const uint64_t x = (blockIdx.x + i * gridDim.x) * kSlab + tid;
+            const bool valid = i < mine && x < N;
+            pw = valid ? bits[x] : 0;
+            pe1 = valid ? E1[x >> lk] : 0;
+            pe2 = valid ? E2[x & kmask] : 0;
+        };
+        fetch(0);
+        for (uint64_t i = 0; i <= mine; i++) {
+            if (i < mine) {  // build slab i into buffer i % 2
+                const int buf = (int)(i & 1);
+                const uint64_t x = (blockIdx.x + i * gridDim.x) * kSlab + tid;
+                const bool valid = x < N;
+                const uint64_t w = pw, eqx = m61::mul(pe1, pe2);
+                fetch(i + 1);
+                uint64_t bx = 0;
 #pragma unroll
-    for (int k = 0; k < DW; k++)
+                for (int b = 0; b < 8; b++) bx = m61::add(bx, s_lut[b * 256 + ((w >> (8 * b)) & 255)]);
+                if (valid) Bx[x] = bx;
+                int8_t d[kLimbs];
+                balanced_digits(eqx, d);
+#pragma unroll
+                for (int t = 0; t < kLimbs; t++) s_d[buf][t][tid] = d[t];
+                const uint64_t pwt = wave_transpose64(w);  // lane q: plane q over the wave's 64 outputs
+                if (lane < NPL) {
+                    int8_t *row = s_u + buf * kPlaneBytes + lane * kRow + (tid & ~63);
+#pragma unroll
+                    for (int c = 0; c < 4; c++) {
+                        const uint64_t e0 = s_exp[(pwt >> (16 * c)) & 255], e1 = s_exp[(pwt >> (16 * c + 8)) & 255];
+                        *(v4i *)(row + 16 * c) = v4i{(int)(uint32_t)e0, (int)(uint32_t)(e0 >> 32), (int)(uint32_t)e1,
+                                                     (int)(uint32_t)(e1 >> 32)};
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        __syncthreads();  // the consumers have cleared the tiles
+        __syncthreads();  // and added their digits
+    } else {
+        v16i acc[DW][TP];
+#pragma unroll
+        for (int k = 0; k < DW; k++)
+#pragma unroll
+            for (int tp = 0; tp < TP; tp++)
+#pragma unroll
+                for (int r = 0; r < 16; r++) acc[k][tp][r] = 0;
+        for (uint64_t i = 0; i <= mine; i++) {
+            if (i > 0) {  // consume slab i - 1 from buffer (i - 1) % 2
+                const int buf = (int)((i - 1) & 1);
+                const int8_t *mrow = s_u + buf * kPlaneBytes + (lane & 31) * kRow + 16 * half;
+                const int8_t *drow = &s_d[buf][cw][16 * half];
+                v4i nm[NPT], nd[DW];
+#pragma unroll
+                for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow);
+#pragma unroll
+                for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab);
+                for (int ks = 0; ks < kSlab / 32; ks++) {
+                    v4i mask[NPT], frag[NPT], D[DW];
+#pragma unroll
+                    for (int pt = 0; pt < NPT; pt++) mask[pt] = nm[pt];
+#pragma unroll
+                    for (int k = 0; k < DW; k++) D[k] = nd[k];
+                    const int kn = ks + 1 < kSlab / 32 ? ks + 1 : ks;  // the last step re-reads (unused)
+#pragma unroll
+                    for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * kn);
+#pragma unroll
+                    for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab + 32 * kn);
+                    __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of this step's products
+#pragma unroll
+                    for (int pt = 0; pt < NPT; pt++) frag[pt] = mask[pt] & (int)0x01010101;
+#pragma unroll
+                    for (int k = 0; k < DW; k++) {
+                        const v4i B0 = mask[0] & D[k];
+                        acc[k][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B0, acc[k][0], 0, 0, 0);
+                        if (TP > 1) {
+                            const v4i B1 = mask[NPT - 1] & D[k];
+                            acc[k][1 % TP] =
+                                __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B1, acc[k][1 % TP], 0, 0, 0);
+                            acc[k][2 % TP] =
+                                __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[NPT - 1], B1, acc[k][2 % TP], 0, 0, 0);
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        // recombine the digits modulo p into the block's tiles: digit t weighs
+        // 2^(8t), a rotation of the 61-bit residue; one LDS atomic per entry
+        // and consumer wave (8 waves x values below 2^61 < 2^64)
+        for (int i = tid - 64 * kProducers; i < TP * 1024; i += 64 * kConsumers) (&s_g[0][0])[i] = 0;
+        __syncthreads();
 #pragma unroll
         for (int tp = 0; tp < TP; tp++)
 #pragma unroll
-            for (int r = 0; r < 16; r++) acc[k][tp][r] = 0;
-    const uint64_t kmask = (1ull << lk) - 1;
-    const uint64_t nslabs = (N + kSlab - 1) / kSlab;
-    __syncthreads();
-
-    // the global inputs of a slab (bit words and the two eq factors) are read
-    // one slab ahead, so their latency hides behind the previous slab's phase G
-    constexpr int NIT = kSlab / NT;
-    uint64_t pw_[NIT], pe1[NIT], pe2[NIT];
-    auto fetch = [&](uint64_t sl) {
-#pragma unroll
-        for (int it = 0; it < NIT; it++) {
-            const uint64_t x = sl * kSlab + it * NT + tid;
-            const bool valid = sl < nslabs && x < N;
-            pw_[it] = valid ? bits[x] : 0;
-            pe1[it] = valid ? E1[x >> lk] : 0;
-            pe2[it] = valid ? E2[x & kmask] : 0;
-        }
-    };
-    fetch(blockIdx.x);
-    for (uint64_t sl = blockIdx.x; sl < nslabs; sl += gridDim.x) {
-        const uint64_t x0 = sl * kSlab;
-        uint64_t cw[NIT], ce1[NIT], ce2[NIT];
-#pragma unroll
-        for (int it = 0; it < NIT; it++) {
-            cw[it] = pw_[it];
-            ce1[it] = pe1[it];
-            ce2[it] = pe2[it];
-        }
-        fetch(sl + gridDim.x);
-        // phase X: one output per thread per step, 64 consecutive outputs per wave
-#pragma unroll
-        for (int it = 0; it < NIT; it++) {
-            const int xl = it * NT + tid;
-            const uint64_t x = x0 + xl;
-            const bool valid = x < N;
-            const uint64_t w = cw[it], eqx = m61::mul(ce1[it], ce2[it]);
-            uint64_t bx = 0;
-#pragma unroll
-            for (int b = 0; b < 8; b++) bx = m61::add(bx, s_lut[b * 256 + ((w >> (8 * b)) & 255)]);
-            if (valid) Bx[x] = bx;
-            int8_t d[kLimbs];
-            balanced_digits(eqx, d);
-#pragma unroll
-            for (int t = 0; t < kLimbs; t++) s_d[t][xl] = d[t];
-            const uint64_t pw = wave_transpose64(w);  // lane q: plane q over the wave's 64 outputs
-            if (lane < NPL) {
-                int8_t *row = s_b + lane * kRow + (xl & ~63);
-#pragma unroll
-                for (int c = 0; c < 4; c++) {
-                    const uint64_t e0 = s_exp[(pw >> (16 * c)) & 255], e1 = s_exp[(pw >> (16 * c + 8)) & 255];
-                    *(v4i *)(row + 16 * c) =
-                        v4i{(int)(uint32_t)e0, (int)(uint32_t)(e0 >> 32), (int)(uint32_t)e1, (int)(uint32_t)(e1 >> 32)};
-                }
-            }
-        }
-        __syncthreads();
-        // phase G: 32 outputs per step; fragments of both plane tiles, then
-        // this wave's digits for every tile pair.  The next step's fragments
-        // are read from LDS while the current step's products run.
-        constexpr int NPT = TP == 1 ? 1 : 2;
-        const int8_t *mrow = s_b + (lane & 31) * kRow + 16 * half;
-        const int8_t *drow = &s_d[wv & 3][16 * half];
-        v4i nm[NPT], nd[DW];
-        int ks = wv / 4;
-#pragma unroll
-        for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * ks);
-#pragma unroll
-        for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab + 32 * ks);
-        for (; ks < kSlab / 32; ks += S::kGroups) {
-            v4i mask[NPT], frag[NPT], D[DW];
-#pragma unroll
-            for (int pt = 0; pt < NPT; pt++) mask[pt] = nm[pt];
-#pragma unroll
-            for (int k = 0; k < DW; k++) D[k] = nd[k];
-            const int kn = ks + S::kGroups < kSlab / 32 ? ks + S::kGroups : ks;  // last step re-reads (unused)
-#pragma unroll
-            for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * kn);
-#pragma unroll
-            for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab + 32 * kn);
-            __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of this step's products
-#pragma unroll
-            for (int pt = 0; pt < NPT; pt++) frag[pt] = mask[pt] & (int)0x01010101;
-#pragma unroll
-            for (int k = 0; k < DW; k++) {
-                const v4i B0 = mask[0] & D[k];
-                acc[k][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B0, acc[k][0], 0, 0, 0);
-                if (TP > 1) {
-                    const v4i B1 = mask[NPT - 1] & D[k];
-                    acc[k][1 % TP] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B1, acc[k][1 % TP], 0, 0, 0);
-                    acc[k][2 % TP] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[NPT - 1], B1, acc[k][2 % TP], 0, 0, 0);
-                }
-            }
-        }
+            for (int r = 0; r < 16; r++)
+                atomicAdd(&s_g[tp][r * 64 + lane],
+                          (unsigned long long)m61::rotl(m61::from_i32(acc[0][tp][r]), 8 * cw));
         __syncthreads();
     }
-    // recombine the digits modulo p into the block's tiles: digit t weighs
-    // 2^(8t), a rotation of the 61-bit residue; each wave folds its two digits
-    // before one LDS atomic per entry (8 waves x values below 2^61 < 2^64)
-    for (int i = tid; i < TP * 1024; i += NT) (&s_g[0][0])[i] = 0;
-    __syncthreads();
-    const int t0 = wv & 3;
-#pragma unroll
-    for (int tp = 0; tp < TP; tp++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-            const uint64_t v0 = m61::rotl(m61::from_i32(acc[0][tp][r]), 8 * t0);
-            const uint64_t v1 = m61::rotl(m61::from_i32(acc[1][tp][r]), 8 * t0 + 32);
-            atomicAdd(&s_g[tp][r * 64 + lane], (unsigned long long)m61::add(v0, v1));
-        }
-    __syncthreads();
-    for (int i = tid; i < TP * 1024; i += NT)
+    for (int i = tid; i < TP * 1024; i += kGramThreads)
         gpart[(size_t)blockIdx.x * TP * 1024 + i] = m61::reduce64((&s_g[0][0])[i]);
 }
 
@@ -269,11 +263,9 @@ void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const u
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
     if (TP == 1)
-        hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(64 * GramShape<1>::kWaves), 0, st, bits, N, lk, E1, E2, lut,
-                           Bx, gpart);
+        hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, lut, Bx, gpart);
     else
-        hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(64 * GramShape<3>::kWaves), 0, st, bits, N, lk, E1, E2, lut,
-                           Bx, gpart);
+        hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, lut, Bx, gpart);
 }
 
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, hipStream_t st)

@@ -73,15 +73,13 @@ __device__ __forceinline__ uint64_t wave_transpose64(uint64_t a)
 }
 
 // Balanced base-256 digits of e < 2^61: e = sum_t 256^t d_t, d_t in [-128, 128).
-__device__ __forceinline__ void balanced_digits(uint64_t e, int8_t (&d)[kLimbs])
+// With f = e + sum_t 128 256^t (no overflow: e < 2^61), the plain bytes f_t
+// give d_t = f_t - 128, whose int8 bit pattern is f_t with the top bit flipped;
+// so the eight digit bytes are those of f xor 0x80...80.
+__device__ __forceinline__ uint64_t balanced_digit_bytes(uint64_t e)
 {
-    int carry = 0;
-#pragma unroll
-    for (int t = 0; t < kLimbs; t++) {
-        const int v = (int)((e >> (8 * t)) & 255) + carry;
-        carry = v >= 128;
-        d[t] = (int8_t)(v - 256 * carry);
-    }
+    constexpr uint64_t kHalf = 0x8080808080808080ull;
+    return (e + kHalf) ^ kHalf;
 }
 
 template <int TP>
@@ -136,14 +134,13 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
                 const bool valid = x < N;
                 const uint64_t w = pw, eqx = m61::mul(pe1, pe2);
                 fetch(i + 1);
-                uint64_t bx = 0;
+                uint64_t bx = 0;  // eight values below 2^61: the plain sum stays below 2^64
 #pragma unroll
-                for (int b = 0; b < 8; b++) bx = m61::add(bx, s_lut[b * 256 + ((w >> (8 * b)) & 255)]);
-                if (valid) Bx[x] = bx;
-                int8_t d[kLimbs];
-                balanced_digits(eqx, d);
+                for (int b = 0; b < 8; b++) bx += s_lut[b * 256 + ((w >> (8 * b)) & 255)];
+                if (valid) Bx[x] = m61::reduce64(bx);
+                const uint64_t db = balanced_digit_bytes(eqx);
 #pragma unroll
-                for (int t = 0; t < kLimbs; t++) s_d[buf][t][tid] = d[t];
+                for (int t = 0; t < kLimbs; t++) s_d[buf][t][tid] = (int8_t)(db >> (8 * t));
                 const uint64_t pwt = wave_transpose64(w);  // lane q: plane q over the wave's 64 outputs
                 if (lane < NPL) {
                     int8_t *row = s_u + buf * kPlaneBytes + lane * kRow + (tid & ~63);

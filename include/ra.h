@@ -19,12 +19,11 @@
  *   - Pointers named d_* are device pointers (caller-owned, on the device
  *     that was current when the context was created); h_* and the arrays
  *     inside the proof structs are host pointers (caller-owned).
- *   - All device work is ordered on the context's HIP stream (the library
- *     also runs independent kernel chains on a stream of its own, joined back
- *     before a call's outputs are staged).  By default every call
- *     synchronises before it returns, so its outputs are ready.  In deferred
- *     mode (ra_ctx_set_deferred) the proving calls return once their work is
- *     enqueued and their host outputs are written at ra_ctx_sync.
+ *   - All device work is ordered on the context's HIP stream.  By default
+ *     every call synchronises before it returns, so its outputs are ready.
+ *     In deferred mode (ra_ctx_set_deferred) the proving calls return once
+ *     their work is enqueued and their host outputs are written at
+ *     ra_ctx_sync.
  *   - A context is not thread-safe.  Contexts on one device may run
  *     concurrently on different streams.
  *   - Dimensions n, m, k are powers of two >= 1 (Sec. III-A-1 assumes

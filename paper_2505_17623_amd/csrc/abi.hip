@@ -27,8 +27,6 @@ int log2u(uint64_t x)
 struct ra_ctx {
     int device = 0;
     hipStream_t stream = nullptr;  // the caller's stream: every call is ordered on it
-    hipStream_t side = nullptr;    // library stream for independent kernel chains within a call
-    hipEvent_t ev[4] = {};         // fork / join events (timing disabled)
     uint64_t *d_chal = nullptr;
     uint64_t n_chal = 0;
     uint64_t cursor = 0;
@@ -165,14 +163,6 @@ void flush_profile(ra_ctx *c)
         c->ev_pool.push_back(p.second.second);
     }
     c->ev_pending.clear();
-}
-
-// `to` waits for everything enqueued on `from` so far (event slot e).
-ra_status order(ra_ctx *c, hipStream_t from, hipStream_t to, int e)
-{
-    RA_HIP(hipEventRecord(c->ev[e], from));
-    RA_HIP(hipStreamWaitEvent(to, c->ev[e], 0));
-    return RA_OK;
 }
 
 // Write every pending host output from its staged words (the stream has been
@@ -346,9 +336,6 @@ ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_cha
     if (st == RA_OK && n_challenges &&
         hipMemcpy(c->d_chal, h_challenges, n_challenges * 8, hipMemcpyHostToDevice) != hipSuccess)
         st = RA_E_HIP;
-    if (st == RA_OK && hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess) st = RA_E_HIP;
-    for (int e = 0; e < 4 && st == RA_OK; e++)
-        if (hipEventCreateWithFlags(&c->ev[e], hipEventDisableTiming) != hipSuccess) st = RA_E_HIP;
     static_assert(sizeof(WitParams) <= 64, "parameters precede the claims");
     if (st == RA_OK && hipMalloc((void **)&c->d_params, 128) != hipSuccess) st = RA_E_NOMEM;
     if (st == RA_OK) c->d_claims = (uint64_t *)((char *)c->d_params + 64);
@@ -367,12 +354,8 @@ ra_status ra_ctx_destroy(ra_ctx *c)
 {
     if (!c) return RA_E_INVAL;
     if (c->stream || c->ws || c->d_chal) (void)hipStreamSynchronize(c->stream);
-    if (c->side) (void)hipStreamSynchronize(c->side);
     if (c->d_chal) (void)hipFree(c->d_chal);
     if (c->d_eq) (void)hipFree(c->d_eq);
-    for (int e = 0; e < 4; e++)
-        if (c->ev[e]) (void)hipEventDestroy(c->ev[e]);
-    if (c->side) (void)hipStreamDestroy(c->side);
     if (c->d_params) (void)hipFree(c->d_params);
     if (c->ws) (void)hipFree(c->ws);
     if (c->h_stage) (void)hipHostFree(c->h_stage);
@@ -496,10 +479,9 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     uint64_t *E1 = c->d_eq, *E2 = c->d_eq + n;
     hipStream_t s = c->stream;
 
-    // the sum-check chain (eq tables, bindings, rounds) runs on the side
-    // stream; the product C, which it does not need, on the caller's stream
-    hipStream_t z = c->side;
-    if ((st = order(c, s, z, 0)) != RA_OK) return st;
+    // the sum-check chain (eq tables, bindings, rounds), then the product C,
+    // all on the caller's stream
+    hipStream_t z = s;
     {
         Timed tm(c, G_EQ, z);
         launch_eq_table(r1, ln, E1, z);
@@ -526,7 +508,6 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
         Timed tm(c, G_GEMM);
         launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s);
     }
-    if ((st = order(c, z, s, 1)) != RA_OK) return st;
     c->n = n;
     c->m = m;
     c->k = k;

@@ -35,7 +35,7 @@ sys.path.insert(0, ROOT)
 PEAKS = {"hbm": (8000.0, "GB/s", 1e9), "mfma": (5000.0, "TOP/s", 1e12),
          "alu": (256 * 4 * 16 * 2.4, "Gmul/s", 1e9)}
 MULS_PER_FIELD_MUL = 4      # 32x32 -> 64 partial products of a product in F_p, p = 2^61 - 1
-X_TAIL_LOG, X_FUSE_MAX, MM_TAIL_LOG, MM_FUSE = 12, 4, 10, 2
+X_TAIL_LOG, X_BLOCK_MAX, X_FUSE_MAX, MM_TAIL_LOG, MM_FUSE = 8, 10, 4, 10, 2
 
 
 def layer_shapes(wl):
@@ -63,13 +63,14 @@ def elements_folded(shapes, planes):
 
 
 def x_schedule(lN):
-    """Rounds over x per global launch, then the tail's, as the library runs them."""
-    L = min(lN, X_TAIL_LOG)
-    launches = []
-    if lN > L:
-        xl = (lN - L + X_FUSE_MAX - 1) // X_FUSE_MAX
-        launches = [(lN - L) // xl + (1 if g < (lN - L) % xl else 0) for g in range(xl)]
-    return launches, L
+    """Rounds over x per launch, as the library runs them: register passes of
+    X_FUSE_MAX rounds, one pass of B rounds per workgroup in LDS (B = 0: none),
+    and the last pass of v rounds."""
+    v = min(lN, X_TAIL_LOG)
+    rem, reg = lN - v, 0
+    while rem - reg > X_BLOCK_MAX:
+        reg += X_FUSE_MAX
+    return [X_FUSE_MAX] * (reg // X_FUSE_MAX), rem - reg, v
 
 
 def group_work(shapes, planes):
@@ -97,16 +98,14 @@ def group_work(shapes, planes):
         # rounds over x: per pair, 6 field products (range) and 7 (ReLU)
         lN = N.bit_length() - 1
         per_pair = 6 + 7 * relu
-        launches, L = x_schedule(lN)
+        regs, B, v = x_schedule(lN)
         j = 0
-        first = True
-        for C in launches:
+        for C in regs + ([B] if B else []):
             lS = lN - j
             for c in range(C):
                 add("range_rounds", "alu", MULS_PER_FIELD_MUL * per_pair * (1 << (lS - c - 1)))
-            rd = (8 + 8 * relu) if first else (8 + 16 * relu)
+            rd = (8 + 8 * relu) if j == 0 else (8 + 16 * relu)
             add("range_rounds", "hbm", rd * (1 << lS) + (8 + 16 * relu) * (1 << (lS - C)), hbm2)
-            first = False
             j += C
         for jj in range(lN - j):
             add("range_tail", "alu", MULS_PER_FIELD_MUL * per_pair * (1 << (lN - j - jj - 1)))
@@ -124,7 +123,7 @@ KERNEL_GROUP = [("k_gemm_mfma", "gemm_mfma"), ("k_split_", "gemm_mfma"), ("k_zer
                 ("k_minmax", "witness_minmax"), ("k_wit_params", "witness_minmax"),
                 ("k_rescale", "witness_rescale"), ("k_claims_final", "witness_rescale"),
                 ("k_plane_gram", "range_plane"), ("k_gram_reduce", "range_plane"),
-                ("k_xrounds", "range_rounds"), ("k_xtail", "range_tail"), ("k_range_setup", "range_setup"),
+                ("k_xrounds", "range_rounds"), ("k_xblock", "range_rounds"), ("k_range_setup", "range_setup"),
                 ("k_rounds", "matmul_rounds"), ("k_tail", "matmul_tail"), ("k_eq_table", "eq_table"),
                 ("k_assemble", "assemble")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")

@@ -250,7 +250,7 @@ ra_status plane_params(int s, int t, int relu, int *P, int *lP)
 }
 
 constexpr int kPartStride = kMaxUnits * kPartWidth;  // words per partial-sum slot
-static_assert(kXTailThreads <= kMaxUnits && kMaxBlocks <= kMaxUnits, "partials must fit a slot");
+static_assert((1 << kXTailLog) <= kMaxUnits && kMaxBlocks <= kMaxUnits, "partials must fit a slot");
 
 int log2_tail() { return log2u(tail_capacity(0)); }
 
@@ -615,7 +615,14 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     if (c->cursor + need > c->n_chal) return RA_E_CHALLENGES;
     const uint64_t *lam = c->d_chal + c->cursor, *sigma = lam + 4 + lP, *rho2 = sigma + R;
 
-    const int L = std::min(lN, kXTailLog), nhs = lN > L ? 1 << (lN - L) : 1;
+    const int L = std::min(lN, kXSplitLog), nhs = lN > L ? 1 << (lN - L) : 1;
+    // Rounds over x: register passes of kXFuseMax rounds while more than
+    // kXTailLog + kXBlockMax variables remain, then one pass of Bp rounds per
+    // workgroup in LDS, then the last pass (one workgroup).
+    const int v = std::min(lN, kXTailLog), rem = lN - v;
+    int reg = 0;
+    while (rem - reg > kXBlockMax) reg += kXFuseMax;
+    const int Bp = rem - reg;
     const int nslots = std::max(lN, 1);
     if (nslots > kMaxSlots || lN > 62) return RA_E_INVAL;
     const int gtiles = plane_gram_tiles(lP), gblocks = plane_gram_blocks(N, lP);
@@ -627,6 +634,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const size_t o_d = cv.take<uint64_t>(relu ? N : 1), o_s = cv.take<uint64_t>(relu ? N : 1);
     const size_t o_hs = cv.take<uint64_t>(nhs), o_ls = cv.take<uint64_t>(2ull << L);
     const size_t o_kr = cv.take<uint64_t>(lN + 1), o_kz = cv.take<uint64_t>(lN + 1);
+    const size_t o_wsh = cv.take<uint64_t>(1ull << Bp);
     const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
     const size_t o_lut = cv.take<uint64_t>(8 * 256);
     const size_t o_gp = cv.take<uint64_t>((size_t)gblocks * gtiles * 1024);
@@ -637,6 +645,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     uint64_t *D = (uint64_t *)(c->ws + o_d), *S = (uint64_t *)(c->ws + o_s);
     uint64_t *HS = (uint64_t *)(c->ws + o_hs), *LS = (uint64_t *)(c->ws + o_ls);
     uint64_t *Kr = (uint64_t *)(c->ws + o_kr), *Kz = (uint64_t *)(c->ws + o_kz);
+    uint64_t *WSh = (uint64_t *)(c->ws + o_wsh);
     size_t o_tr = 0;
     if ((st = stage_take(c, trw, &o_tr)) != RA_OK) return st;
     uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = c->d_stage + o_tr;
@@ -646,7 +655,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
 
     {
         Timed tm(c, G_RANGE_SETUP);
-        const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz};
+        const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
         launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, lut, xs, s);
     }
     {   // plane rounds: Gram matrix on the matrix cores, Bx per output
@@ -654,40 +663,62 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
         launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, Bx, gpart, s);
         launch_gram_reduce(lP, N, gpart, gsum, s);
     }
-    SlotTable slots;
-    slots.count = 0;
+    // Each x launch's extra workgroups assemble the rounds of the launch
+    // before it; the first one also evaluates the plane rounds, the last
+    // assembles its own.
+    const XConst xc{cst + C_EP, c->d_r12, Kr, Kz};
+    XJobs jobs{};
+    jobs.nplane = lP;
+    jobs.stride = kPartStride;
+    jobs.tr = tr;
+    jobs.xc = xc;
+    jobs.pa = PlaneArgs{gsum, sigma, cst, tr, lP};
+    auto next_jobs = [&](int j0, int nr, int units) {
+        jobs.nplane = 0;
+        jobs.nslot = nr;
+        jobs.part = part + (size_t)j0 * kPartStride;
+        for (int r = 0; r < nr; r++)
+            jobs.s[r] = Slot{units, kPartWidth, 4 * (lP + j0 + r), SLOT_X, j0 + r, -1,
+                             relu ? (int)Z0 + 4 * (j0 + r) : -1};
+    };
     int j = 0, lS = lN;
-    const int xl = (lN - L + kXFuseMax - 1) / kXFuseMax;  // global launches, rounds spread evenly
-    for (int g = 0; lS > L; g++) {
-        const int C = (lN - L) / xl + (g < (lN - L) % xl ? 1 : 0);
+    for (; j < reg; j += kXFuseMax, lS -= kXFuseMax) {
         const XArgs xa{Bx, D, S, d_R, d_Y, HS, LS, c->d_r12, sigx + j, rz ? rz + j : nullptr,
-                       part + (size_t)slots.count * kPartStride, lN, L, j};
+                       part + (size_t)j * kPartStride, lN, L, j};
         {
             Timed tm(c, G_RANGE_ROUNDS);
-            launch_xrounds(C, j == 0, relu != 0, xa, 1ull << lS, kPartStride, s);
+            launch_xrounds(kXFuseMax, j == 0, relu != 0, xa, 1ull << lS, kPartStride, jobs, s);
         }
-        const int nb = xround_units(1ull << (lS - C), relu != 0);
-        for (int r = 0; r < C; r++)
-            slots.s[slots.count++] = Slot{nb, kPartWidth, 4 * (lP + j + r), SLOT_X, j + r, -1,
-                                          relu ? (int)Z0 + 4 * (j + r) : -1};
-        lS -= C;
-        j += C;
+        next_jobs(j, kXFuseMax, xround_units(1ull << (lS - kXFuseMax), relu != 0));
     }
+    XBlockArgs xb{Bx, D, S, d_R, d_Y, HS, LS, c->d_r12, WSh, nullptr, nullptr, nullptr, kPartStride, lN, L, 0, 0, 0,
+                  tr, 0, 0, tr + F_R + 1, tr + FZ + 1, tr + FZ + 2, xc};
+    if (Bp > 0) {
+        xb.rho_a = sigx + j;
+        xb.rho_z = rz ? rz + j : nullptr;
+        xb.part = part + (size_t)j * kPartStride;
+        xb.j = j;
+        xb.B = Bp;
+        xb.lS = lS;
+        {
+            Timed tm(c, G_RANGE_ROUNDS);
+            launch_xblock(relu != 0, j == 0, xb, jobs, s);
+        }
+        next_jobs(j, Bp, 1 << (lS - Bp));
+        j += Bp;
+        lS -= Bp;
+    }
+    xb.W = LS;  // the last pass's window r_{j+1 .. lN-1} ends at the last variable
+    xb.rho_a = sigx + j;
+    xb.rho_z = rz ? rz + j : nullptr;
+    xb.j = j;
+    xb.B = lS;
+    xb.lS = lS;
+    xb.out0 = 4 * (lP + j);
+    xb.out2 = relu ? (int)Z0 + 4 * j : -1;
     {
-        const XTailArgs ta{Bx, D, S, d_R, d_Y, LS, sigx + j, rz ? rz + j : nullptr,
-                           part + (size_t)slots.count * kPartStride, tr + F_R + 1, tr + FZ + 1, tr + FZ + 2, lS};
         Timed tm(c, G_RANGE_TAIL);
-        launch_xtail(relu != 0, j == 0, ta, kPartStride, s);
-    }
-    for (int jj = 0; jj < lS; jj++) {
-        const int h = 1 << (lS - 1 - jj);
-        slots.s[slots.count++] = Slot{xtail_units(h, relu != 0), kPartWidth, 4 * (lP + j + jj), SLOT_X, j + jj, -1,
-                                      relu ? (int)Z0 + 4 * (j + jj) : -1};
-    }
-    {   // the x rounds' polynomials and (further workgroups) the plane rounds'
-        Timed tm(c, G_ASSEMBLE);
-        launch_assemble(slots, part, kPartStride, tr, XConst{cst + C_EP, c->d_r12, Kr, Kz},
-                        PlaneArgs{gsum, sigma, cst, tr, lP}, s);
+        launch_xblock(relu != 0, j == 0, xb, jobs, s);
     }
     c->phase = 0;
     c->cursor += need;

@@ -12,10 +12,10 @@ constexpr int kTailThreads = 256;      // block size of the LDS tail kernel
 constexpr int kTailMaxLog = 10;
 constexpr int kTailMax = 1 << kTailMaxLog;  // largest table the single-workgroup tail takes
 constexpr int kMaxBlocks = 1024;       // blocks of a grid-stride round kernel
-constexpr int kXTailLog = 12;          // the x rounds of the range / ReLU instances finish in LDS
-constexpr int kXTailMax = 1 << kXTailLog;
-constexpr int kXTailThreads = 1024;
-constexpr int kXFuseMax = 4;           // x rounds fused per global launch
+constexpr int kXSplitLog = 12;         // x rounds: variables in the low part of the suffix eq heaps
+constexpr int kXTailLog = 8;           // x rounds: the last pass binds at most this many variables
+constexpr int kXBlockMax = 10;         // x rounds: variables bound by one workgroup in LDS (sub-cube 2^B)
+constexpr int kXFuseMax = 4;           // x rounds fused per thread in registers
 constexpr int kMaxUnits = 2048;        // partial-sum producers per round (waves or threads)
 constexpr int kPartWidth = 8;          // words per block and round in a partial-sum slot
 
@@ -68,6 +68,8 @@ struct XSetupArgs {
     const uint64_t *r, *sigx, *rho2;
     int lN, L, nhs;  // nhs = 2^(lN - L) (1 if lN <= L)
     uint64_t *HS, *LS, *Kr, *Kz;
+    uint64_t *WS;    // weights of the LDS pass over rounds wj .. wj + wB - 1 (wB = 0: none)
+    int wj, wB;
 };
 
 // ---- launchers (witness.hip) ----
@@ -148,21 +150,42 @@ struct XArgs {
     uint64_t *part;
     int lN, L, j;                  // variables, low-part size, first round
 };
-struct XTailArgs {
-    const uint64_t *bx, *d, *s;
-    const int32_t *R, *Y;
-    const uint64_t *LS;
-    const uint64_t *rho_a, *rho_z;
-    uint64_t *part;
-    uint64_t *fin_b, *fin_r, *fin_y;
-    int v;
+// Work for extra workgroups of an x-round launch: assemble nslot slots whose
+// partials lie at part + q * stride (q < nslot), then evaluate plane rounds
+// 1 .. nplane (plane_round.hpp).
+constexpr int kXJobsMax = 12;
+struct XJobs {
+    int nslot, nplane;
+    const uint64_t *part;
+    int stride;
+    uint64_t *tr;
+    XConst xc;
+    PlaneArgs pa;
+    Slot s[kXJobsMax];
 };
-int x_setup_threads(int lN, int L);
-int xround_blocks(uint64_t sub, bool relu);
-int xround_units(uint64_t sub, bool relu);  // partial-sum producers of a launch
-int xtail_units(int h, bool relu);          // ... of a tail round with h pairs
-void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, hipStream_t st);
-void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStream_t st);
+int xround_units(uint64_t sub, bool relu);  // partial-sum producers of a register pass
+// C rounds per thread in registers over a table of S entries (sub-cube i:
+// entries i + t S / 2^C).
+void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, const XJobs &jobs,
+                    hipStream_t st);
+// B rounds per workgroup in LDS over a table of 2^lS entries: sub-cube k (one
+// workgroup) holds entries k + t 2^(lS - B).  With lS == B it is the last
+// pass: its rounds' evaluations go to tr and the bound values to fin_*.
+struct XBlockArgs {
+    uint64_t *bx, *d, *s;           // tables; the bound values are written to index k
+    const int32_t *R, *Y;           // integer R, Y (first pass)
+    const uint64_t *HS, *LS, *r;    // suffix eq heaps, EQ point
+    const uint64_t *W;              // heap of the weights inside a sub-cube (table s at 2^s, s < B)
+    const uint64_t *rho_a, *rho_z;  // binding challenges of the pass's first round
+    uint64_t *part;                 // pass: round c's partials at part + c * stride + 8 k
+    int stride;
+    int lN, L, j, B, lS;
+    uint64_t *tr;                   // last pass: round c at tr + out0 + 4 c (ReLU: out2 + 4 c)
+    int out0, out2;
+    uint64_t *fin_b, *fin_r, *fin_y;
+    XConst xc;
+};
+void launch_xblock(bool relu, bool first, const XBlockArgs &a, const XJobs &jobs, hipStream_t st);
 
 // ---- launchers (planes.hip) ----
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)

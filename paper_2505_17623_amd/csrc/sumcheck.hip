@@ -12,6 +12,7 @@
 // rho (T[i + h] - T[i]) for i < h (thread i alone reads i and i + h).
 #include "common.hpp"
 #include "m61.hpp"
+#include "assemble.hpp"
 #include "plane_round.hpp"
 #include "xsetup.hpp"
 
@@ -223,25 +224,43 @@ __device__ __forceinline__ uint64_t eq1(uint64_t a, uint64_t b)
     return m61::add(m61::mul(a, b), m61::mul(m61::sub(1, a), m61::sub(1, b)));
 }
 
-// One block of 256 threads.  chal points at lambda1: lambda1..3, mu,
-// tau_p (lP), sigma (lP + ...).
+// Block 0 (256 threads): the constant block; chal points at lambda1:
+// lambda1..3, mu, tau_p (lP), sigma (lP + ...).  Further blocks: the set-up of
+// the rounds over x.  Every operand is first staged in LDS.
 __global__ __launch_bounds__(256) void k_range_setup(const uint64_t *__restrict__ chal,
                                                      const WitParams *__restrict__ prm,
                                                      const uint64_t *__restrict__ claims, int lP,
                                                      uint64_t *__restrict__ cst, uint64_t *__restrict__ range_sum,
                                                      uint64_t *__restrict__ lut, XSetupArgs xs)
 {
+    const int tid = threadIdx.x;
     if (blockIdx.x > 0) {  // the set-up of the rounds over x
-        x_setup_body(xs, (blockIdx.x - 1) * blockDim.x + threadIdx.x);
+        __shared__ uint64_t rl[64], sl[64], zl[64];
+        if (tid < xs.lN) {
+            rl[tid] = xs.r[tid];
+            sl[tid] = xs.sigx[tid];
+            zl[tid] = xs.rho2 ? xs.rho2[tid] : 0;
+        }
+        __syncthreads();
+        x_setup_body(xs, (blockIdx.x - 1) * blockDim.x + tid, rl, sl, zl);
         return;
     }
     __shared__ uint64_t c[C_WORDS];
     __shared__ uint64_t eqs[64];
-    const int P = 1 << lP, tid = threadIdx.x;
-    const int s = prm->s, t = prm->t, relu = prm->relu;
-    const uint64_t *lam = chal, mu = chal[3], *tau = chal + 4, *sig = chal + 4 + lP;
+    __shared__ uint64_t ch[4 + 2 * kMaxPlaneLog], cl[3];
+    __shared__ int pv[3];
+    const int P = 1 << lP;
+    if (tid < 4 + 2 * lP) ch[tid] = chal[tid];
+    if (tid >= 64 && tid < 67) cl[tid - 64] = claims[tid - 64];
+    if (tid == 128) {
+        pv[0] = prm->s;
+        pv[1] = prm->t;
+        pv[2] = prm->relu;
+    }
     for (int i = tid; i < C_WORDS; i += blockDim.x) c[i] = 0;
     __syncthreads();
+    const int s = pv[0], t = pv[1], relu = pv[2];
+    const uint64_t *lam = ch, mu = ch[3], *tau = ch + 4, *sig = ch + 4 + lP;
     // W_1 = W: plane q holds bit b of group g -> lambda_g 2^b
     for (int q = tid; q < P; q += blockDim.x) {
         int g = -1, b = 0;
@@ -258,6 +277,15 @@ __global__ __launch_bounds__(256) void k_range_setup(const uint64_t *__restrict_
         uint64_t acc = 1;
         for (int i = 0; i < lP - j; i++) acc = m61::mul(acc, m61::eq1_bit(tau[j + i], (p >> (lP - j - 1 - i)) & 1));
         c[C_E + idx] = acc;
+    }
+    // eq(sigma_p, q) for every plane (for the byte tables below)
+    for (int q = tid; q < 64; q += blockDim.x) {
+        uint64_t a = 0;
+        if (q < P) {
+            a = 1;
+            for (int i = 0; i < lP; i++) a = m61::mul(a, m61::eq1_bit(sig[i], (q >> (lP - 1 - i)) & 1));
+        }
+        eqs[q] = a;
     }
     __syncthreads();
     for (int j = 1; j <= lP; j++) {  // W_{j+1} = W_j bound at sigma_j; w2_j = 2 W_j[p + h] - W_j[p]
@@ -283,37 +311,26 @@ __global__ __launch_bounds__(256) void k_range_setup(const uint64_t *__restrict_
         c[C_EP + 2] = Wp;
         c[C_EP + 3] = mu;
         // claimed sum mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~); claims = (R~, Rm~, Y~, Z~)
-        uint64_t H = m61::add(m61::mul(lam[0], claims[1]), m61::mul(lam[1], m61::add(claims[0], 1ull << (t + 1))));
-        if (relu) H = m61::add(H, m61::mul(lam[2], claims[2]));
+        uint64_t H = m61::add(m61::mul(lam[0], cl[1]), m61::mul(lam[1], m61::add(cl[0], 1ull << (t + 1))));
+        if (relu) H = m61::add(H, m61::mul(lam[2], cl[2]));
         *range_sum = m61::mul(mu, H);
-    }
-    // eq(sigma_p, q) for every plane, then the byte tables of Bx(x) = sum_q eq(sigma_p, q) bit_q(x):
-    // lut[b][v] = sum over the set bits i of v of eq(sigma_p, 8 b + i)
-    for (int q = tid; q < 64; q += blockDim.x) {
-        uint64_t a = 0;
-        if (q < P) {
-            a = 1;
-            for (int i = 0; i < lP; i++) a = m61::mul(a, m61::eq1_bit(sig[i], (q >> (lP - 1 - i)) & 1));
-        }
-        eqs[q] = a;
     }
     __syncthreads();
     for (int i = tid; i < C_WORDS; i += blockDim.x) cst[i] = c[i];
+    // lut[b][v] = sum over the set bits i of v of eq(sigma_p, 8 b + i)
     for (int i = tid; i < 8 * 256; i += blockDim.x) {
         const int b = i >> 8, v = i & 255;
         uint64_t a = 0;
         for (int k = 0; k < 8; k++)
-            if ((v >> k) & 1) a = m61::add(a, eqs[8 * b + k]);
-        lut[i] = a;
+            if ((v >> k) & 1) a += eqs[8 * b + k];
+        lut[i] = m61::canon(a);
     }
 }
-
-int x_setup_threads(int lN, int L) { return (lN > L ? 1 << (lN - L) : 1) + (1 << (L + 1)); }
 
 void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,
                         uint64_t *tr_range_sum, uint64_t *lut, const XSetupArgs &xs, hipStream_t st)
 {
-    const int xb = (x_setup_threads(xs.lN, xs.L) + 255) / 256;
+    const int xb = (x_setup_count(xs) + 255) / 256;
     hipLaunchKernelGGL(k_range_setup, dim3(1 + xb), dim3(256), 0, st, chal, params, claims, lP, cst, tr_range_sum,
                        lut, xs);
 }
@@ -325,38 +342,13 @@ void launch_range_setup(const uint64_t *chal, const WitParams *params, const uin
 __global__ __launch_bounds__(256) void k_assemble(SlotTable slots, const uint64_t *__restrict__ part, int part_stride,
                                                   uint64_t *__restrict__ tr, XConst xc, PlaneArgs pa)
 {
-    __shared__ uint64_t red[m61::block_sum_words(kPartWidth, 256)];
+    __shared__ uint64_t lds[kJobLdsWords];
     const int si = blockIdx.x;
     if (si >= slots.count) {  // a plane round
-        plane_round(pa, si - slots.count + 1);
+        plane_round(pa, si - slots.count + 1, lds);
         return;
     }
-    const Slot sl = slots.s[si];
-    const uint64_t *p = part + (size_t)si * part_stride;
-    uint64_t acc[kPartWidth] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int b = threadIdx.x; b < sl.nblk; b += blockDim.x)
-        for (int i = 0; i < sl.width; i++) acc[i] = m61::add(acc[i], p[(size_t)b * sl.width + i]);
-    m61::block_sum<kPartWidth>(acc, red);
-    if (threadIdx.x != 0) return;
-    if (sl.kind == SLOT_COPY) {
-        for (int i = 0; i < sl.width; i++) tr[sl.out + i] = acc[i];
-        if (sl.sum_out >= 0) tr[sl.sum_out] = m61::add(acc[0], acc[1]);  // claimed sum = g_1(0) + g_1(1)
-        return;
-    }
-    // SLOT_X: acc = (A0, A1, Q0, Q1, Q2, Z0, Z1, Z2), see xrounds.hip
-    const int j = sl.round;
-    const uint64_t ep = xc.kp[0], cc = xc.kp[1], rj = xc.r[j];
-    uint64_t sv[4];
-    sv[0] = m61::add(m61::mul(ep, acc[2]), m61::mul(cc, acc[0]));
-    sv[1] = m61::add(m61::mul(ep, acc[3]), m61::mul(cc, acc[1]));
-    sv[2] = m61::add(m61::mul(ep, acc[4]), m61::mul(cc, m61::sub(m61::add(acc[1], acc[1]), acc[0])));
-    sv[3] = m61::add(sv[0], m61::mul(3, m61::sub(sv[2], sv[1])));  // quadratic: s(3) = s(0) + 3 (s(2) - s(1))
-    for (int X = 0; X < 4; X++) tr[sl.out + X] = m61::mul(m61::mul(xc.Kr[j], m61::eq1_small(rj, X)), sv[X]);
-    if (sl.out2 >= 0) {
-        const uint64_t z3 = m61::add(acc[5], m61::mul(3, m61::sub(acc[7], acc[6])));
-        const uint64_t zv[4] = {acc[5], acc[6], acc[7], z3};
-        for (int X = 0; X < 4; X++) tr[sl.out2 + X] = m61::mul(m61::mul(xc.Kz[j], m61::eq1_small(rj, X)), zv[X]);
-    }
+    assemble_slot(slots.s[si], part + (size_t)si * part_stride, tr, xc, lds);
 }
 
 void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, const XConst &xc,

@@ -10,48 +10,68 @@
 //   K_j eq1(r_j, X) eq(r_>j, i),      K_j = prod_{l<j} eq1(r_l, z_l),
 // so the round polynomial is K_j eq1(r_j, X) s_j(X) with
 //   s_j(X) = sum_i eq(r_>j, i) h(T_X(i))     (T_X = T_lo + X (T_hi - T_lo)),
-// a quadratic in X.  The kernels accumulate, per round,
-//   range  A_a = sum_i w_i b_a,  Q_a = sum_i w_i b_a^2      (a = 0, 1; Q also at b_2 = 2 b_1 - b_0)
-//   ReLU   Z_a = sum_i w_i d_a s_a                          (a = 0, 1, 2)
-// with w_i = eq(r_>j, i), five field products per pair and instance; the
-// assembly forms s_j(0..2), extrapolates s_j(3) and multiplies by
+// a quadratic in X.  The kernels accumulate, per round, with w_i = eq(r_>j, i),
+//   range  A_a = sum_i w_i b_a (a = 0, 1),  Q_a = sum_i w_i b_a^2 (a = 0, 1),  M = sum_i w_i b_0 b_1
+//   ReLU   Z_a = sum_i w_i d_a s_a (a = 0, 1),  U = sum_i w_i (d_0 + d_1)(s_0 + s_1)
+// five products per pair and instance.  The values at X = 2 follow from
+// b_2 = 2 b_1 - b_0 (and likewise d_2, s_2):
+//   A_2 = 2 A_1 - A_0,  Q_2 = Q_0 + 4 (Q_1 - M),  Z_2 = 3 Z_0 + 6 Z_1 - 2 U;
+// the assembly forms s_j(0..2), extrapolates s_j(3) and multiplies by
 // K_j eq1(r_j, X).  The weights eq(r_>j, i) come from two small tables of
 // suffix eq vectors (a high part and a low part of the variables), so they
 // cost one product per thread.  The ReLU tables are kept as D and S; the
 // final values give R = (D + S) / 2 and Y = (S - D) / 2.
+//
+// Arithmetic inside the kernels uses loose residues (m61.hpp): products and
+// differences are folded below 2^61 + 8 without a final comparison, sums of
+// at most four folded terms are added to a folded accumulator before it is
+// folded again, and every value leaving a kernel is canonical.
 #include <algorithm>
 
+#include "assemble.hpp"
 #include "common.hpp"
 #include "m61.hpp"
+#include "plane_round.hpp"
 
 namespace ra {
 
-// Contributions of one pair with weight w: range to acc[0..5), ReLU to acc[0..3).
+// Terms of one pair with weight w, added to acc without folding (each term
+// is a folded value): range acc[0..5) = A_0, A_1, Q_0, Q_1, M; ReLU
+// acc[0..3) = Z_0, Z_1, U.  Inputs are folded or canonical.
 __device__ __forceinline__ void range_pair(uint64_t w, uint64_t b0, uint64_t b1, uint64_t *acc)
 {
-    const uint64_t eb0 = m61::mul(w, b0), eb1 = m61::mul(w, b1);
-    const uint64_t eb2 = m61::sub(m61::add(eb1, eb1), eb0), b2 = m61::sub(m61::add(b1, b1), b0);
-    acc[0] = m61::add(acc[0], eb0);
-    acc[1] = m61::add(acc[1], eb1);
-    acc[2] = m61::add(acc[2], m61::mul(eb0, b0));
-    acc[3] = m61::add(acc[3], m61::mul(eb1, b1));
-    acc[4] = m61::add(acc[4], m61::mul(eb2, b2));
+    const uint64_t eb0 = m61::lmul(w, b0), eb1 = m61::lmul(w, b1);
+    acc[0] += eb0;
+    acc[1] += eb1;
+    acc[2] += m61::lmul(eb0, b0);
+    acc[3] += m61::lmul(eb1, b1);
+    acc[4] += m61::lmul(eb0, b1);
 }
 
 __device__ __forceinline__ void relu_pair(uint64_t w, uint64_t d0, uint64_t d1, uint64_t s0, uint64_t s1,
                                           uint64_t *acc)
 {
-    const uint64_t ed0 = m61::mul(w, d0), ed1 = m61::mul(w, d1);
-    const uint64_t ed2 = m61::sub(m61::add(ed1, ed1), ed0), s2 = m61::sub(m61::add(s1, s1), s0);
-    acc[0] = m61::add(acc[0], m61::mul(ed0, s0));
-    acc[1] = m61::add(acc[1], m61::mul(ed1, s1));
-    acc[2] = m61::add(acc[2], m61::mul(ed2, s2));
+    const uint64_t ed0 = m61::lmul(w, d0), ed1 = m61::lmul(w, d1);
+    acc[0] += m61::lmul(ed0, s0);
+    acc[1] += m61::lmul(ed1, s1);
+    acc[2] += m61::lmul(ed0 + ed1, s0 + s1);  // sums of two folded values are loose
 }
 
+template <int NV>
+__device__ __forceinline__ void fold_all(uint64_t *acc)
+{
+#pragma unroll
+    for (int q = 0; q < NV; q++) acc[q] = m61::fold(acc[q]);
+}
+
+// lo + z (hi - lo), folded.
 __device__ __forceinline__ uint64_t fold(uint64_t lo, uint64_t hi, uint64_t z)
 {
-    return m61::add(lo, m61::mul(z, m61::sub(hi, lo)));
+    return m61::fold(lo + m61::lmul(z, m61::lsub(hi, lo)));
 }
+
+// Field value of a small signed integer (|v| < 2^62), folded.
+__device__ __forceinline__ uint64_t small_to_field(int64_t v) { return m61::fold((uint64_t)v + 4 * m61::P); }
 
 // Sums of NV values over the 64 lanes of the calling wave, written to
 // out[0 .. NV).  Every wave of the block calls it at the same point (it holds
@@ -103,43 +123,52 @@ __device__ __forceinline__ void x_weights(uint64_t e, const uint64_t *rr, uint64
         // u = (msb, rest): eq1(r_{j+c+1}, msb) times the weight of `rest` one round later
 #pragma unroll
         for (int u = 0; u < hn / 2; u++) {
-            const uint64_t hi = m61::mul(rr[c + 1], w[pb + u]);
+            const uint64_t hi = m61::lmul(rr[c + 1], w[pb + u]);
             w[base + hn / 2 + u] = hi;
-            w[base + u] = m61::sub(w[pb + u], hi);
+            w[base + u] = m61::lsub(w[pb + u], hi);
         }
     }
 }
 
-template <int C, bool FIRST, bool RELU>
-__global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stride)
+// The sub-cubes of one thread for one instance (ZW: ReLU, else range); the
+// sums of round c are added to acc[c] (folded values).
+// eq(r_{lN-nvar .. lN-1}, k) from the suffix heaps (folded or canonical).
+__device__ __forceinline__ uint64_t suffix_weight(const uint64_t *HS, const uint64_t *LS, int nvar, int L, uint64_t k)
 {
-    constexpr int NL = 1 << C, NPB = RELU ? 128 : 256, NVR = 5 * C, NVZ = 3 * C;
-    __shared__ uint64_t lw[4][NVR * 68];
-    const int tid = threadIdx.x, wv = tid >> 6;
-    const bool zw = RELU && wv >= 2;  // wave-uniform
-    const int lt = RELU ? (tid & 127) : tid;
-    const int unit = RELU ? blockIdx.x * 2 + (wv & 1) : blockIdx.x * 4 + wv;
-    uint64_t accr[C][5], accz[C][3];
+    if (nvar <= L) return LS[(1ull << nvar) + k];
+    return m61::lmul(HS[(1ull << (nvar - L)) + (k >> L)], LS[(1ull << L) + (k & ((1ull << L) - 1))]);
+}
+
+// Extra workgroup q of an x-round launch (256 threads): assemble a slot of
+// the launch before, or evaluate a plane round.
+__device__ __forceinline__ void x_job(const XJobs &jobs, int q, uint64_t *lds)
+{
+    if (q < jobs.nslot) assemble_slot(jobs.s[q], jobs.part + (size_t)q * jobs.stride, jobs.tr, jobs.xc, lds);
+    else if (q - jobs.nslot < jobs.nplane) plane_round(jobs.pa, q - jobs.nslot + 1, lds);
+}
+
+// The sub-cubes of one thread for one instance (ZW: ReLU, else range); the
+// sums of round c are added to acc[c] (folded values).
+template <int C, bool FIRST, bool ZW>
+__device__ __forceinline__ void x_sub_cubes(const XArgs &a, uint64_t sub, uint64_t i0, uint64_t step,
+                                            uint64_t (&acc)[C][ZW ? 3 : 5])
+{
+    constexpr int NL = 1 << C, NV = ZW ? 3 : 5;
 #pragma unroll
-    for (int c = 0; c < C; c++) {
+    for (int c = 0; c < C; c++)
 #pragma unroll
-        for (int q = 0; q < 5; q++) accr[c][q] = 0;
-#pragma unroll
-        for (int q = 0; q < 3; q++) accz[c][q] = 0;
-    }
+        for (int q = 0; q < NV; q++) acc[c][q] = 0;
     uint64_t rz[C], rr[C];
 #pragma unroll
     for (int c = 0; c < C; c++) {
-        rz[c] = zw ? a.rho_z[c] : a.rho_a[c];
+        rz[c] = ZW ? a.rho_z[c] : a.rho_a[c];
         rr[c] = a.r[a.j + c];
     }
-    const uint64_t *hs = a.HS + (1ull << (a.lN - a.L - a.j - C));
-    const uint64_t *ls = a.LS + (1ull << a.L);
-    const uint64_t lmask = (1ull << a.L) - 1;
-    for (uint64_t i = (uint64_t)blockIdx.x * NPB + lt; i < sub; i += (uint64_t)gridDim.x * NPB) {
+    const int nvar = a.lN - a.j - C;
+    for (uint64_t i = i0; i < sub; i += step) {
         uint64_t w[NL];
-        x_weights<C>(m61::mul(hs[i >> a.L], ls[i & lmask]), rr, w);
-        if (!zw) {
+        x_weights<C>(suffix_weight(a.HS, a.LS, nvar, a.L, i), rr, w);
+        if (!ZW) {
             uint64_t b[NL];
 #pragma unroll
             for (int t = 0; t < NL; t++) b[t] = a.bx[i + t * sub];
@@ -148,19 +177,20 @@ __global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stri
                 const int h = NL >> (c + 1), base = h - 1;
 #pragma unroll
                 for (int u = 0; u < h; u++) {
-                    range_pair(w[base + u], b[u], b[u + h], accr[c]);
+                    range_pair(w[base + u], b[u], b[u + h], acc[c]);
                     b[u] = fold(b[u], b[u + h], rz[c]);
+                    if ((u & 3) == 3 || u == h - 1) fold_all<NV>(acc[c]);
                 }
             }
-            a.bx[i] = b[0];
+            a.bx[i] = m61::canon(b[0]);
         } else {
             uint64_t d[NL], s[NL];
 #pragma unroll
             for (int t = 0; t < NL; t++) {
                 if (FIRST) {
                     const int64_t R = a.R[i + t * sub], Y = a.Y[i + t * sub];
-                    d[t] = m61::from_i64(R - Y);
-                    s[t] = m61::from_i64(R + Y);
+                    d[t] = small_to_field(R - Y);
+                    s[t] = small_to_field(R + Y);
                 } else {
                     d[t] = a.d[i + t * sub];
                     s[t] = a.s[i + t * sub];
@@ -171,35 +201,70 @@ __global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stri
                 const int h = NL >> (c + 1), base = h - 1;
 #pragma unroll
                 for (int u = 0; u < h; u++) {
-                    relu_pair(w[base + u], d[u], d[u + h], s[u], s[u + h], accz[c]);
+                    relu_pair(w[base + u], d[u], d[u + h], s[u], s[u + h], acc[c]);
                     d[u] = fold(d[u], d[u + h], rz[c]);
                     s[u] = fold(s[u], s[u + h], rz[c]);
+                    if ((u & 3) == 3 || u == h - 1) fold_all<NV>(acc[c]);
                 }
             }
-            a.d[i] = d[0];
-            a.s[i] = s[0];
+            a.d[i] = m61::canon(d[0]);
+            a.s[i] = m61::canon(s[0]);
         }
     }
+}
+
+template <int C>
+constexpr int xrounds_lds_words()
+{
+    return 4 * (5 * C) * 68 + 4 * (5 * C) > kJobLdsWords ? 4 * (5 * C) * 68 + 4 * (5 * C) : kJobLdsWords;
+}
+
+// Workgroups below nmain run the rounds; the others are jobs.
+template <int C, bool FIRST, bool RELU>
+__global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stride, XJobs jobs, int nmain)
+{
+    constexpr int NPB = RELU ? 128 : 256, NVR = 5 * C;
+    __shared__ uint64_t smem[xrounds_lds_words<C>()];
+    if ((int)blockIdx.x >= nmain) {
+        x_job(jobs, blockIdx.x - nmain, smem);
+        return;
+    }
+    uint64_t *tot = smem + 4 * NVR * 68;
+    const int tid = threadIdx.x, wv = tid >> 6;
+    const bool zw = RELU && wv >= 2;  // wave-uniform
+    const int lt = RELU ? (tid & 127) : tid;
+    const int unit = RELU ? blockIdx.x * 2 + (wv & 1) : blockIdx.x * 4 + wv;
+    const uint64_t i0 = (uint64_t)blockIdx.x * NPB + lt, step = (uint64_t)nmain * NPB;
     // per-wave sums; the range waves' layout covers both (ReLU values in the first 3 C)
     uint64_t flat[NVR];
+    if (!zw) {
+        uint64_t acc[C][5];
+        x_sub_cubes<C, FIRST, false>(a, sub, i0, step, acc);
 #pragma unroll
-    for (int c = 0; c < C; c++)
+        for (int c = 0; c < C; c++)
 #pragma unroll
-        for (int q = 0; q < 5; q++) flat[c * 5 + q] = zw ? (q < 3 ? accz[c][q] : 0) : accr[c][q];
-    __shared__ uint64_t tot[4][NVR];
-    wave_sums_to<NVR>(flat, lw[wv], tot[wv]);
+            for (int q = 0; q < 5; q++) flat[c * 5 + q] = m61::canon(acc[c][q]);
+    } else {
+        uint64_t acc[C][3];
+        x_sub_cubes<C, FIRST, true>(a, sub, i0, step, acc);
+#pragma unroll
+        for (int c = 0; c < C; c++)
+#pragma unroll
+            for (int q = 0; q < 5; q++) flat[c * 5 + q] = q < 3 ? m61::canon(acc[c][q]) : 0;
+    }
+    wave_sums_to<NVR>(flat, smem + wv * NVR * 68, tot + wv * NVR);
     __syncthreads();
     const int lane = tid & 63;
     if (lane < C * 8) {
         const int c = lane >> 3, q = lane & 7;
         uint64_t v;
-        if (!zw) v = q < 5 ? tot[wv][c * 5 + q] : 0;
-        else v = tot[wv][c * 5 + q - 5];
+        if (!zw) v = q < 5 ? tot[wv * NVR + c * 5 + q] : 0;
+        else v = tot[wv * NVR + c * 5 + q - 5];
         if (zw ? q >= 5 : (q < 5 || !RELU)) a.part[(size_t)c * stride + (size_t)unit * 8 + q] = v;
     }
 }
 
-int xround_blocks(uint64_t sub, bool relu)
+static int xround_blocks(uint64_t sub, bool relu)
 {
     const uint64_t per = relu ? 128 : 256, cap = relu ? kMaxUnits / 2 : kMaxUnits / 4;
     const uint64_t b = (sub + per - 1) / per;
@@ -208,11 +273,13 @@ int xround_blocks(uint64_t sub, bool relu)
 
 int xround_units(uint64_t sub, bool relu) { return xround_blocks(sub, relu) * (relu ? 2 : 4); }
 
-void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, hipStream_t st)
+void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, const XJobs &jobs,
+                    hipStream_t st)
 {
     const uint64_t sub = S >> C;
-    const dim3 g(xround_blocks(sub, relu)), b(kThreads);
-#define RA_X(CC, F, Z) hipLaunchKernelGGL((k_xrounds<CC, F, Z>), g, b, 0, st, a, sub, stride)
+    const int nmain = xround_blocks(sub, relu);
+    const dim3 g(nmain + jobs.nslot + jobs.nplane), b(kThreads);
+#define RA_X(CC, F, Z) hipLaunchKernelGGL((k_xrounds<CC, F, Z>), g, b, 0, st, a, sub, stride, jobs, nmain)
 #define RA_X_FZ(CC)                      \
     if (first) {                         \
         if (relu) RA_X(CC, true, true);  \
@@ -232,133 +299,184 @@ void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, in
 }
 
 // ---------------------------------------------------------------------------
-// The last v rounds in one workgroup with the tables in LDS.  Round jj pairs
-// i and i + h (h = 2^(v-1-jj)) with weight LS[h + i] = eq(r_>j, i).  With
-// ReLU the first half of the threads runs the range instance and the second
-// half the ReLU instance; thread t of a half (t < min(h, half)) writes its
-// sums of round jj to part + jj * stride + 8 t (range words 0-4, ReLU 5-7).
-// With FIRST (no global rounds ran) the inputs are Bx and the integer R, Y.
+// B rounds per workgroup with the sub-cube in LDS.  Workgroup k loads the
+// 2^B entries k + t 2^(lS - B) of each table (threads 0-127 the range table,
+// 128-255 the ReLU tables D and S; all 256 the range table without ReLU).
+// Round c pairs u and u + h (h = 2^(B-1-c)) with weight
+//   eq(r_{j+c+1 .. j+B-1}, u) eq(r_{j+B ..}, k) = W[h + u] e_k,
+// W the heap of suffix eq tables of the window r_{j+1 .. j+B-1} (set-up: the
+// WS heap, or for the last pass the LS heap), e_k from the suffix heaps.  Each thread keeps its sums of a
+// round in LDS; at the end the workgroup reduces them per round and either
+// writes one partial per round (several sub-cubes) or, for the single
+// sub-cube of the last pass, the round polynomials themselves.
 // ---------------------------------------------------------------------------
+constexpr int kXbMax = 1 << kXBlockMax;
+// Thread-rounds (sum over the rounds of min(h, threads per instance)) for
+// B <= 10: range 256 + 256 + 255 without ReLU, 128 + 128 + 128 + 127 with it.
+constexpr int kXbRoundsR = 767, kXbRoundsZ = 511;
+// LDS layout (words): Tb, Td, Ts, W (kXbMax each), challenges (3 x 16), the
+// per-thread round sums (range 5, ReLU 3 words), the reduced sums (8 per round).
+constexpr int kXbLdsWords = 4 * kXbMax + 48 + 5 * kXbRoundsR + 3 * kXbRoundsZ + 8 * kXBlockMax;
+static_assert(kXbLdsWords >= kJobLdsWords, "jobs share the workgroup's LDS");
+
 template <bool RELU>
-__global__ __launch_bounds__(kXTailThreads) void k_xtail(XTailArgs a, int first, int stride)
+__global__ __launch_bounds__(256) void k_xblock(XBlockArgs a, int first, XJobs jobs, int nmain)
 {
-    __shared__ uint64_t Tb[kXTailMax], Td[RELU ? kXTailMax : 1], Ts[RELU ? kXTailMax : 1], W[kXTailMax];
-    constexpr int NH = RELU ? kXTailThreads / 2 : kXTailThreads;  // threads per instance
-    const int tid = threadIdx.x, v = a.v, S = 1 << v;
-    const bool zw = RELU && tid >= NH;  // wave-uniform
-    const int lt = zw ? tid - NH : tid;
-    __shared__ uint64_t zc[2][kXTailLog];  // the rounds' challenges, read once
-    if (tid < v) zc[0][tid] = a.rho_a[tid];
-    if (RELU && tid >= 64 && tid < 64 + v) zc[1][tid - 64] = a.rho_z[tid - 64];
-    for (int i = tid; i < S; i += blockDim.x) {
-        Tb[i] = a.bx[i];
-        W[i] = a.LS[i];  // heap entries 1 .. S-1 are the tables of sizes S/2 .. 1
-        if (RELU) {
-            if (first) {
-                const int64_t R = a.R[i], Y = a.Y[i];
-                Td[i] = m61::from_i64(R - Y);
-                Ts[i] = m61::from_i64(R + Y);
-            } else {
-                Td[i] = a.d[i];
-                Ts[i] = a.s[i];
-            }
+    __shared__ uint64_t smem[kXbLdsWords];
+    if ((int)blockIdx.x >= nmain) {
+        x_job(jobs, blockIdx.x - nmain, smem);
+        return;
+    }
+    uint64_t *Tb = smem, *Td = Tb + kXbMax, *Ts = Td + kXbMax, *W = Ts + kXbMax;
+    uint64_t *rw = W + kXbMax, *za = rw + 16, *zz = za + 16;
+    uint64_t *pr = zz + 16, *pz = pr + 5 * kXbRoundsR, *red = pz + 3 * kXbRoundsZ;
+    constexpr int NI = RELU ? 128 : 256;  // threads per instance
+    const int tid = threadIdx.x, B = a.B, S = 1 << B;
+    const bool zw = RELU && tid >= NI;  // wave-uniform
+    const int lt = zw ? tid - NI : tid;
+    const uint64_t k = blockIdx.x, nsub = 1ull << (a.lS - B);
+    // the binding challenges of the B rounds
+    if (tid >= 64 && tid < 64 + B) za[tid - 64] = a.rho_a[tid - 64];
+    if (RELU && tid >= 128 && tid < 128 + B) zz[tid - 128] = a.rho_z[tid - 128];
+    // the sub-cube: at most kXbMax / NI entries per thread, all loads issued first
+    constexpr int NQ = kXbMax / NI;
+    if (!zw) {
+        uint64_t v[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            const int t = lt + q * NI;
+            v[q] = t < S ? a.bx[k + (uint64_t)t * nsub] : 0;
         }
+#pragma unroll
+        for (int q = 0; q < NQ; q++)
+            if (lt + q * NI < S) Tb[lt + q * NI] = v[q];
+    } else if (first) {
+        int32_t vr[NQ], vy[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            const int t = lt + q * NI;
+            vr[q] = t < S ? a.R[k + (uint64_t)t * nsub] : 0;
+            vy[q] = t < S ? a.Y[k + (uint64_t)t * nsub] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; q++)
+            if (lt + q * NI < S) {
+                Td[lt + q * NI] = small_to_field((int64_t)vr[q] - vy[q]);
+                Ts[lt + q * NI] = small_to_field((int64_t)vr[q] + vy[q]);
+            }
+    } else {
+        uint64_t vd[NQ], vs[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            const int t = lt + q * NI;
+            vd[q] = t < S ? a.d[k + (uint64_t)t * nsub] : 0;
+            vs[q] = t < S ? a.s[k + (uint64_t)t * nsub] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; q++)
+            if (lt + q * NI < S) {
+                Td[lt + q * NI] = vd[q];
+                Ts[lt + q * NI] = vs[q];
+            }
+    }
+    // weights W[h + u] e_k of the pairs of every round (W: table s at offset 2^s)
+    const uint64_t ek = suffix_weight(a.HS, a.LS, a.lN - a.j - B, a.L, k);
+    for (int e0 = tid + 1; e0 < S; e0 += 4 * blockDim.x) {
+        uint64_t v[4];
+#pragma unroll
+        for (int q = 0; q < 4; q++) v[q] = e0 + q * (int)blockDim.x < S ? a.W[e0 + q * blockDim.x] : 0;
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            if (e0 + q * (int)blockDim.x < S) W[e0 + q * blockDim.x] = m61::lmul(v[q], ek);
     }
     __syncthreads();
-    for (int jj = 0; jj < v; jj++) {
-        const int h = S >> (jj + 1);
-        const uint64_t z = zc[zw ? 1 : 0][jj];
-        if (h > NH / 2) {  // many pairs: one thread per pair
-            uint64_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-            if (!zw) {
-                for (int i = lt; i < h; i += NH) {
-                    const uint64_t w = W[h + i], b0 = Tb[i], b1 = Tb[i + h];
-                    range_pair(w, b0, b1, acc);
-                    Tb[i] = fold(b0, b1, z);
-                }
-            } else {
-                for (int i = lt; i < h; i += NH) {
-                    const uint64_t w = W[h + i], d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
-                    relu_pair(w, d0, d1, s0, s1, acc + 5);
-                    Td[i] = fold(d0, d1, z);
-                    Ts[i] = fold(s0, s1, z);
-                }
+    int off = 0;
+    for (int c = 0; c < B; c++) {
+        const int h = S >> (c + 1), n = h < NI ? h : NI;
+        if (!zw) {
+            const uint64_t z = za[c];
+            uint64_t acc[5] = {0, 0, 0, 0, 0};
+            for (int u = lt; u < h; u += NI) {
+                const uint64_t w = W[h + u], b0 = Tb[u], b1 = Tb[u + h];
+                range_pair(w, b0, b1, acc);
+                fold_all<5>(acc);
+                Tb[u] = fold(b0, b1, z);
             }
-            if (lt < h) {
-                uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)lt;
-                if (!zw) {
+            if (lt < n)
 #pragma unroll
-                    for (int q = 0; q < 5; q++) o[q] = acc[q];
-                    if (!RELU)
-#pragma unroll
-                        for (int q = 5; q < 8; q++) o[q] = 0;
-                } else {
-#pragma unroll
-                    for (int q = 5; q < 8; q++) o[q] = acc[q];
-                }
-            }
+                for (int q = 0; q < 5; q++) pr[(off + lt) * 5 + q] = acc[q];
         } else {
-            // few pairs: four lanes per pair, each at most two products.
-            // Role 0, 1, 2 take the terms at b_0, b_1, b_2 = 2 b_1 - b_0 (range:
-            // w b_a and w b_a^2; ReLU: (w d_a) s_a); role 3 folds the tables.
-            const int role = lt & 3;
-            for (int i = lt >> 2; i < h; i += NH / 4) {
-                const uint64_t w = W[h + i];
-                uint64_t *o = a.part + (size_t)jj * stride + 8 * (size_t)i;
-                if (!zw) {
-                    const uint64_t b0 = Tb[i], b1 = Tb[i + h];
-                    const uint64_t u = role == 0 ? b0 : role == 1 ? b1 : role == 2 ? m61::sub(m61::add(b1, b1), b0)
-                                                                                   : m61::sub(b1, b0);
-                    const uint64_t xv = m61::mul(role == 3 ? z : w, u);
-                    if (role == 3) {
-                        Tb[i] = m61::add(b0, xv);
-                    } else {
-                        const uint64_t yv = m61::mul(xv, u);
-                        if (role < 2) o[role] = xv;  // A_0, A_1
-                        o[2 + role] = yv;            // Q_0, Q_1, Q_2
-                        if (!RELU && role == 0) o[5] = o[6] = o[7] = 0;
-                    }
-                } else {
-                    const uint64_t d0 = Td[i], d1 = Td[i + h], s0 = Ts[i], s1 = Ts[i + h];
-                    const uint64_t u = role == 0 ? d0 : role == 1 ? d1 : role == 2 ? m61::sub(m61::add(d1, d1), d0)
-                                                                                   : m61::sub(d1, d0);
-                    const uint64_t vv = role == 0 ? s0 : role == 1 ? s1 : role == 2 ? m61::sub(m61::add(s1, s1), s0)
-                                                                                    : m61::sub(s1, s0);
-                    const uint64_t xv = m61::mul(role == 3 ? z : w, u);
-                    const uint64_t yv = m61::mul(role == 3 ? z : xv, vv);
-                    if (role == 3) {
-                        Td[i] = m61::add(d0, xv);
-                        Ts[i] = m61::add(s0, yv);
-                    } else {
-                        o[5 + role] = yv;  // Z_0, Z_1, Z_2
-                    }
-                }
+            const uint64_t z = zz[c];
+            uint64_t acc[3] = {0, 0, 0};
+            for (int u = lt; u < h; u += NI) {
+                const uint64_t w = W[h + u];
+                const uint64_t d0 = Td[u], d1 = Td[u + h], s0 = Ts[u], s1 = Ts[u + h];
+                relu_pair(w, d0, d1, s0, s1, acc);
+                fold_all<3>(acc);
+                Td[u] = fold(d0, d1, z);
+                Ts[u] = fold(s0, s1, z);
             }
+            if (lt < n)
+#pragma unroll
+                for (int q = 0; q < 3; q++) pz[(off + lt) * 3 + q] = acc[q];
         }
+        off += n;
         __syncthreads();
     }
-    if (tid == 0) {
-        *a.fin_b = Tb[0];
-        if (RELU) {
-            const uint64_t inv2 = 1ull << 60;  // (p + 1) / 2
-            *a.fin_r = m61::mul(m61::add(Td[0], Ts[0]), inv2);
-            *a.fin_y = m61::mul(m61::sub(Ts[0], Td[0]), inv2);
+    // per-round sums: sum q = 8 c + w over the round's thread entries (folded
+    // values), eight lanes per sum, four terms added before each fold
+    const int ntask = 64 * B;
+    for (int task = tid; task < ntask; task += blockDim.x) {  // ntask is a multiple of 64: whole waves iterate
+        const int q = task >> 3, part = task & 7, c = q >> 3, w = q & 7;
+        int o = 0;
+        for (int cc = 0; cc < c; cc++) o += (S >> (cc + 1)) < NI ? (S >> (cc + 1)) : NI;
+        const int n = (S >> (c + 1)) < NI ? (S >> (c + 1)) : NI;
+        const uint64_t *src = w < 5 ? pr + (size_t)o * 5 + w : pz + (size_t)o * 3 + (w - 5);
+        const int st = w < 5 ? 5 : 3;
+        uint64_t v = 0;
+        if (w < 5 || RELU) {
+            int e = part;
+            for (; e + 24 < n; e += 32) v = m61::fold(v + src[e * st] + src[(e + 8) * st] + src[(e + 16) * st] + src[(e + 24) * st]);
+            for (; e < n; e += 8) v = m61::fold(v + src[e * st]);
+        }
+        v = m61::fold(v + __shfl_xor(v, 1, 64));
+        v = m61::fold(v + __shfl_xor(v, 2, 64));
+        v = m61::fold(v + __shfl_xor(v, 4, 64));
+        if (part == 0) red[q] = m61::canon(v);
+    }
+    __syncthreads();
+    if (nsub > 1) {
+        if (tid < 8 * B) a.part[(size_t)(tid >> 3) * a.stride + 8 * k + (tid & 7)] = red[tid];
+        if (tid == 0) a.bx[k] = m61::canon(Tb[0]);
+        if (RELU && tid == NI) {
+            a.d[k] = m61::canon(Td[0]);
+            a.s[k] = m61::canon(Ts[0]);
+        }
+    } else {
+        // round c's evaluation X of instance zr by thread 8 c + 4 zr + X
+        if (tid < 8 * B) {
+            const int c = tid >> 3, zr = (tid >> 2) & 1, X = tid & 3;
+            if (!zr || RELU)
+                a.tr[(zr ? a.out2 : a.out0) + 4 * c + X] = x_round_eval(red + 8 * c, a.j + c, X, zr != 0, a.xc);
+        }
+        if (tid == 0) {
+            *a.fin_b = m61::canon(Tb[0]);
+            if (RELU) {
+                const uint64_t inv2 = 1ull << 60;  // (p + 1) / 2
+                const uint64_t d = m61::canon(Td[0]), sv = m61::canon(Ts[0]);
+                *a.fin_r = m61::mul(m61::add(d, sv), inv2);
+                *a.fin_y = m61::mul(m61::sub(sv, d), inv2);
+            }
         }
     }
 }
 
-int xtail_units(int h, bool relu)
+void launch_xblock(bool relu, bool first, const XBlockArgs &a, const XJobs &jobs, hipStream_t st)
 {
-    const int nh = relu ? kXTailThreads / 2 : kXTailThreads;
-    return h > nh / 2 ? std::min(h, nh) : h;  // one unit per pair when four lanes share a pair
-}
-
-void launch_xtail(bool relu, bool first, const XTailArgs &a, int stride, hipStream_t st)
-{
-    if (relu)
-        hipLaunchKernelGGL(k_xtail<true>, dim3(1), dim3(kXTailThreads), 0, st, a, (int)first, stride);
-    else
-        hipLaunchKernelGGL(k_xtail<false>, dim3(1), dim3(kXTailThreads), 0, st, a, (int)first, stride);
+    const int nmain = 1 << (a.lS - a.B);
+    const dim3 g(nmain + jobs.nslot + jobs.nplane), b(kThreads);
+    if (relu) hipLaunchKernelGGL(k_xblock<true>, g, b, 0, st, a, (int)first, jobs, nmain);
+    else hipLaunchKernelGGL(k_xblock<false>, g, b, 0, st, a, (int)first, jobs, nmain);
 }
 
 }  // namespace ra

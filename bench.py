@@ -118,7 +118,7 @@ def group_work(shapes, planes):
 
 
 # Kernel -> group, for hardware-counter summaries (rocprofv3 kernel names).
-KERNEL_GROUP = [("k_gemm_mfma", "gemm_mfma"), ("k_split_", "gemm_mfma"), ("k_zero_i64", "gemm_mfma"),
+KERNEL_GROUP = [("k_gemm_mfma", "gemm_mfma"), ("k_split", "gemm_mfma"), ("k_zero_i64", "gemm_mfma"),
                 ("k_bind_rows", "bind_rows"), ("k_sum_chunks", "bind_rows"), ("k_bind_cols", "bind_cols"),
                 ("k_minmax", "witness_minmax"), ("k_wit_params", "witness_minmax"),
                 ("k_rescale", "witness_rescale"), ("k_claims_final", "witness_rescale"),

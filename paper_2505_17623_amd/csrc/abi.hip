@@ -255,46 +255,40 @@ static_assert((1 << kXTailLog) <= kMaxUnits && kMaxBlocks <= kMaxUnits, "partial
 int log2_tail() { return log2u(tail_capacity(0)); }
 
 // One sum-check instance over tables of 2^v entries (in place): fused global
-// launches while the table exceeds the LDS tail, then the tail.  Round j's
-// width = D + 1 evaluations go to tr[ev_base + width j]; the tables' final
-// values to finals[0..NT); with sum_out >= 0 the claimed sum to tr[sum_out].
+// launches while the table exceeds the LDS tail, then the tail, which also
+// assembles every round.  Round j's width = D + 1 evaluations go to
+// tr[ev_base + width j]; the tables' final values to finals[0..NT); with
+// sum_out >= 0 the claimed sum to tr[sum_out].
 void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v,
-                  const uint64_t *rho, const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals,
-                  int sum_out, SlotTable &slots, uint64_t *part, int g_rounds, int g_tail);
-
-}  // namespace
-
-namespace {
-void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v,
-                  const uint64_t *rho, const uint64_t *kp, uint64_t *tr, int ev_base, int width, uint64_t *finals,
-                  int sum_out, SlotTable &slots, uint64_t *part, int g_rounds, int g_tail)
+                  const uint64_t *rho, uint64_t *tr, int ev_base, int width, uint64_t *finals, int sum_out,
+                  uint64_t *part, int g_rounds, int g_tail)
 {
     const int cmax = fused_rounds_max(kind), lt = log2_tail();
+    XJobs jobs{};
+    jobs.part = part;
+    jobs.stride = kPartStride;
+    jobs.tr = tr;
     int j = 0, lS = v;
     while (lS > lt) {
         const int C = std::min(cmax, lS - lt);
         {
             Timed tm(c, g_rounds, st);
-            launch_rounds(kind, C, t0, t1, t2, 1ull << lS, rho + j, kp, part + (size_t)slots.count * kPartStride,
+            launch_rounds(kind, C, t0, t1, t2, 1ull << lS, rho + j, nullptr, part + (size_t)jobs.nslot * kPartStride,
                           kPartStride, st);
         }
         const int nb = round_blocks(1ull << (lS - C));
         for (int r = 0; r < C; r++)
-            slots.s[slots.count++] =
+            jobs.s[jobs.nslot++] =
                 Slot{nb, width, ev_base + width * (j + r), SLOT_COPY, 0, (j + r == 0) ? sum_out : -1, -1};
         lS -= C;
         j += C;
     }
     {
         Timed tm(c, g_tail, st);
-        const TailArgs ta{t0, t1, t2, v - j, rho + j, part + (size_t)slots.count * kPartStride, kPartStride, finals,
-                          finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr,
-                          (j == 0 && v == 0 && sum_out >= 0) ? tr + sum_out : nullptr};
-        launch_tail(kind, ta, st);
+        const TailArgs ta{t0, t1, t2, v - j, rho + j, tr, ev_base, j, sum_out, finals,
+                          finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr};
+        launch_tail(kind, ta, jobs, st);
     }
-    for (int jj = 0; jj < v - j; jj++)
-        slots.s[slots.count++] = Slot{tail_units(1u << (v - j - 1 - jj)), width, ev_base + width * (j + jj), SLOT_COPY,
-                                      0, (j + jj == 0) ? sum_out : -1, -1};
 }
 }  // namespace
 
@@ -484,26 +478,20 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     hipStream_t z = s;
     {
         Timed tm(c, G_EQ, z);
-        launch_eq_table(r1, ln, E1, z);
-        launch_eq_table(r2, lk, E2, z);
+        launch_eq_tables(r1, ln, E1, r2, lk, E2, z);
     }
+    ChunkSum cs{};
     {
         Timed tm(c, G_BIND_ROWS, z);
-        launch_bind_rows(d_A, a_dtype, n, m, E1, scr, a, z);
+        cs = launch_bind_rows_chunks(d_A, a_dtype, n, m, E1, scr, a, z);
     }
-    {
+    {   // B bound on its columns; extra workgroups finish the row binding of A
         Timed tm(c, G_BIND_COLS, z);
-        launch_bind_cols(d_B, RA_I16, m, k, E2, b, z);
+        launch_bind_cols(d_B, RA_I16, m, k, E2, b, z, &cs);
     }
     // transcript: [c0][evals 3 lm][a*][b*]
-    SlotTable slots;
-    slots.count = 0;
-    run_instance(c, z, KIND_MATMUL, a, b, nullptr, lm, rho, nullptr, tr, 1, 3, tr + 1 + 3 * lm, 0, slots, part,
-                 G_MM_ROUNDS, G_MM_TAIL);
-    {
-        Timed tm(c, G_ASSEMBLE, z);
-        launch_assemble(slots, part, kPartStride, tr, XConst{}, PlaneArgs{}, z);
-    }
+    run_instance(c, z, KIND_MATMUL, a, b, nullptr, lm, rho, tr, 1, 3, tr + 1 + 3 * lm, 0, part, G_MM_ROUNDS,
+                 G_MM_TAIL);
     {
         Timed tm(c, G_GEMM);
         launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s);

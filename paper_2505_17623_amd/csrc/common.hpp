@@ -74,6 +74,9 @@ struct XSetupArgs {
 
 // ---- launchers (witness.hip) ----
 void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st);
+// both tables of a product's two sides in one launch
+void launch_eq_tables(const uint64_t *z1, int v1, uint64_t *out1, const uint64_t *z2, int v2, uint64_t *out2,
+                      hipStream_t st);
 // ---- launchers (gemm.hip) ----
 constexpr uint32_t kGemmMaxInner = 32768;  // exactness bound of the int32 limb accumulators
 size_t gemm_workspace_bytes(int a_is_i32, uint32_t n, uint32_t m, uint32_t k);
@@ -83,8 +86,19 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
 int bind_rows_chunks(uint32_t rows, uint32_t cols);
 void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,
                       uint64_t *out, hipStream_t st);
+// The second pass of a row binding (out = sum of the chunk rows of part).
+struct ChunkSum {
+    const uint64_t *part;
+    int nch;
+    uint32_t cols;
+    uint64_t *out;
+};
+// first pass of a row binding only; the returned ChunkSum finishes it
+ChunkSum launch_bind_rows_chunks(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E,
+                                 uint64_t *scratch, uint64_t *out, hipStream_t st);
+// cs (optional): also finish a row binding, in the same launch where possible
 void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *out,
-                      hipStream_t st);
+                      hipStream_t st, const ChunkSum *cs = nullptr);
 int witness_blocks(uint64_t N);
 void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mode, int t_in, int64_t *mm_part,
                            WitParams *params, hipStream_t st);
@@ -102,21 +116,26 @@ struct InstArgs {
     const uint64_t *rho, *kp;
     uint64_t *part;
 };
+// The last v rounds (rounds j0 .. j0 + v - 1 of the instance): round j's
+// D + 1 evaluations go to tr[ev + (D + 1) j], with sum_out >= 0 and j0 == 0
+// also g_0(0) + g_0(1) to tr[sum_out]; the tables' final values to fin*.
 struct TailArgs {
     const uint64_t *t0, *t1, *t2;
     int v;
     const uint64_t *rho;
-    uint64_t *part;  // round j's partials at part + j * stride
-    int stride;
-    uint64_t *fin0, *fin1, *fin2, *sum_out;
+    uint64_t *tr;
+    int ev, j0, sum_out;
+    uint64_t *fin0, *fin1, *fin2;
 };
-int tail_units(uint32_t h);  // partial-sum producers of a tail round with h pairs
 int fused_rounds_max(int kind);
 // C fused rounds over tables of size S (C <= fused_rounds_max); partials of
 // round r at part + r * stride
 void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t S, const uint64_t *rho,
                    const uint64_t *kp, uint64_t *part, int stride, hipStream_t st);
-void launch_tail(int kind, const TailArgs &a, hipStream_t st);
+struct XJobs;
+// The tail workgroup, plus one workgroup per slot in jobs (SLOT_COPY slots of
+// the global rounds before it).
+void launch_tail(int kind, const TailArgs &a, const XJobs &jobs, hipStream_t st);
 // range constants: lambda/mu/tau_p/sigma_p at `chal`, claims from the witness
 size_t range_consts_words(int lP);
 // also writes the 8 x 256 byte tables of the plane-bound table Bx to lut, and

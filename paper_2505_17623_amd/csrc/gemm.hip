@@ -35,10 +35,11 @@ __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
 // limb: the low byte shifted by -128 (a xor of the sign bit), the top limb
 // as is.
 template <typename TA, int LA>
-__global__ __launch_bounds__(256) void k_split_a(const TA *__restrict__ A, uint32_t n, uint32_t m, uint32_t np,
-                                                 uint32_t mp, int8_t *__restrict__ Al, int64_t *__restrict__ rowsum)
+__device__ __forceinline__ void split_a_block(const TA *__restrict__ A, uint32_t n, uint32_t m, uint32_t np,
+                                              uint32_t mp, int8_t *__restrict__ Al, int64_t *__restrict__ rowsum,
+                                              uint32_t blk)
 {
-    const uint32_t row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const uint32_t row = blk * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= np) return;  // wave-uniform
     const size_t plane = (size_t)np * mp;
@@ -109,12 +110,13 @@ __global__ __launch_bounds__(256) void k_split_a(const TA *__restrict__ A, uint3
 // B, zero padded) and the column sums of every 64-row tile, colpart[ti][j].
 // The 64 x 64 tile goes through LDS; four threads take one column's 64 bytes
 // (16 each), so a wave writes whole 64-byte segments.
-__global__ __launch_bounds__(256) void k_split_bt(const int16_t *__restrict__ B, uint32_t m, uint32_t k, uint32_t mp,
-                                                  uint32_t kp, int8_t *__restrict__ Bt, int64_t *__restrict__ colpart)
+__device__ __forceinline__ void split_bt_block(const int16_t *__restrict__ B, uint32_t m, uint32_t k, uint32_t mp,
+                                               uint32_t kp, int8_t *__restrict__ Bt, int64_t *__restrict__ colpart,
+                                               uint32_t bx, uint32_t by)
 {
     __shared__ int16_t t[64][66];
     __shared__ int32_t cs[4][64];
-    const uint32_t l0 = blockIdx.y * 64, j0 = blockIdx.x * 64;
+    const uint32_t l0 = by * 64, j0 = bx * 64;
     const int tid = threadIdx.x;
     {   // load: thread -> row tid / 4, 16 consecutive columns
         const int r = tid >> 2, c = (tid & 3) * 16;
@@ -160,7 +162,23 @@ __global__ __launch_bounds__(256) void k_split_bt(const int16_t *__restrict__ B,
     cs[tid & 3][jj] = sum;
     __syncthreads();
     if (tid < 64 && j0 + tid < k)
-        colpart[(size_t)blockIdx.y * kp + j0 + tid] = (int64_t)cs[0][tid] + cs[1][tid] + cs[2][tid] + cs[3][tid];
+        colpart[(size_t)by * kp + j0 + tid] = (int64_t)cs[0][tid] + cs[1][tid] + cs[2][tid] + cs[3][tid];
+}
+
+// Both operands in one launch: workgroups below na split rows of A (four per
+// workgroup), the others 64 x 64 tiles of B.
+template <typename TA, int LA>
+__global__ __launch_bounds__(256) void k_split(const TA *__restrict__ A, uint32_t n, uint32_t m, uint32_t np,
+                                               uint32_t mp, int8_t *__restrict__ Al, int64_t *__restrict__ rowsum,
+                                               uint32_t na, const int16_t *__restrict__ B, uint32_t k, uint32_t kp,
+                                               int8_t *__restrict__ Bt, int64_t *__restrict__ colpart)
+{
+    if (blockIdx.x < na) {
+        split_a_block<TA, LA>(A, n, m, np, mp, Al, rowsum, blockIdx.x);
+        return;
+    }
+    const uint32_t t = blockIdx.x - na, tx = kp / 64;
+    split_bt_block(B, m, k, mp, kp, Bt, colpart, t % tx, t / tx);
 }
 
 // 64 x 64 output tile per block; wave (wr, wc) owns the 32 x 32 sub-tile.
@@ -255,11 +273,13 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
     int64_t *rowsum = (int64_t *)p;
     p += ((size_t)8 * n + 255) & ~(size_t)255;
     int64_t *colpart = (int64_t *)p;
+    const uint32_t na = (np + 3) / 4, nb = (kp / 64) * (mp / 64);
     if (a_is_i32)
-        hipLaunchKernelGGL((k_split_a<int32_t, 4>), dim3((np + 3) / 4), dim3(256), 0, st, (const int32_t *)A, n, m, np, mp, Al, rowsum);
+        hipLaunchKernelGGL((k_split<int32_t, 4>), dim3(na + nb), dim3(256), 0, st, (const int32_t *)A, n, m, np, mp, Al,
+                           rowsum, na, B, k, kp, Bt, colpart);
     else
-        hipLaunchKernelGGL((k_split_a<int16_t, 2>), dim3((np + 3) / 4), dim3(256), 0, st, (const int16_t *)A, n, m, np, mp, Al, rowsum);
-    hipLaunchKernelGGL(k_split_bt, dim3(kp / 64, mp / 64), dim3(256), 0, st, B, m, k, mp, kp, Bt, colpart);
+        hipLaunchKernelGGL((k_split<int16_t, 2>), dim3(na + nb), dim3(256), 0, st, (const int16_t *)A, n, m, np, mp, Al,
+                           rowsum, na, B, k, kp, Bt, colpart);
     const dim3 grid(kp / kTile, np / kTile);
     if (a_is_i32)
         hipLaunchKernelGGL(k_gemm_mfma<4>, grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,

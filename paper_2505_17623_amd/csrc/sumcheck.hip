@@ -21,24 +21,22 @@ namespace ra {
 template <int KIND> struct KindTraits;
 template <> struct KindTraits<KIND_MATMUL> { static constexpr int NT = 2, D = 2; };
 
-// Contribution of one pair (lo = T[i], hi = T[i + h]) to g(X), X = 0..D.
+// Contribution of one pair (lo = T[i], hi = T[i + h]) to g(X), X = 0..D:
+// acc[X] += a_X b_X with T_X = lo + X (hi - lo), added without folding (each
+// term is a folded value; callers fold at least every fourth pair).
 template <int KIND>
 __device__ __forceinline__ void pair_contrib(const uint64_t (&lo)[3], const uint64_t (&hi)[3], uint64_t (&acc)[4])
 {
-    constexpr int NT = KindTraits<KIND>::NT, D = KindTraits<KIND>::D;
-    uint64_t val[NT], dif[NT];
-#pragma unroll
-    for (int q = 0; q < NT; q++) {
-        val[q] = lo[q];
-        dif[q] = m61::sub(hi[q], lo[q]);
-    }
-#pragma unroll
-    for (int X = 0; X <= D; X++) {
-        acc[X] = m61::add(acc[X], m61::mul(val[0], val[1]));
-        if (X < D)
-#pragma unroll
-            for (int q = 0; q < NT; q++) val[q] = m61::add(val[q], dif[q]);  // table value at X + 1
-    }
+    const uint64_t a2 = m61::lsub(2 * hi[0], lo[0]), b2 = m61::lsub(2 * hi[1], lo[1]);
+    acc[0] += m61::lmul(lo[0], lo[1]);
+    acc[1] += m61::lmul(hi[0], hi[1]);
+    acc[2] += m61::lmul(a2, b2);
+}
+
+// lo + r (hi - lo), folded.
+__device__ __forceinline__ uint64_t fold_to(uint64_t lo, uint64_t hi, uint64_t r)
+{
+    return m61::fold(lo + m61::lmul(r, m61::lsub(hi, lo)));
 }
 
 // ---------------------------------------------------------------------------
@@ -82,13 +80,16 @@ __device__ __forceinline__ void rounds_body(const InstArgs &in, uint64_t sub, in
                 }
                 pair_contrib<KIND>(lo, hi, a4);
 #pragma unroll
-                for (int q = 0; q < NT; q++) v[q][u] = m61::add(lo[q], m61::mul(r[c], m61::sub(hi[q], lo[q])));
+                for (int q = 0; q < NT; q++) v[q][u] = fold_to(lo[q], hi[q], r[c]);
+                if ((u & 3) == 3 || u == h - 1)
+#pragma unroll
+                    for (int X = 0; X <= D; X++) a4[X] = m61::fold(a4[X]);
             }
 #pragma unroll
-            for (int X = 0; X <= D; X++) acc[4 * c + X] = m61::add(acc[4 * c + X], a4[X]);
+            for (int X = 0; X <= D; X++) acc[4 * c + X] = m61::fold(acc[4 * c + X] + a4[X]);
         }
 #pragma unroll
-        for (int q = 0; q < NT; q++) T[q][i] = v[q][0];
+        for (int q = 0; q < NT; q++) T[q][i] = m61::canon(v[q][0]);
     }
     m61::block_sum<C * 4>(acc, red);
     if (threadIdx.x == 0)
@@ -143,60 +144,103 @@ void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, ui
 }
 
 // ---------------------------------------------------------------------------
-// All remaining rounds in one workgroup once the tables fit in LDS.  Thread
-// t (< min(h, blockDim)) of round j writes its D + 1 partial evaluations to
-// part + j * stride + (D + 1) t; the assembly reduces them.  Also writes the
-// tables' final values and, with no rounds at all, the sum a b.
+// All remaining rounds in one workgroup once the tables fit in LDS, and the
+// assembly of the whole instance: workgroup 0 runs the rounds, keeps each
+// thread's sums of a round in LDS, reduces them per round and writes the
+// rounds' evaluations (and, for round 0, the claimed sum g(0) + g(1)); the
+// further workgroups assemble the slots of the global rounds before it.
+// Also writes the tables' final values and, with no rounds at all, the sum a b.
 // ---------------------------------------------------------------------------
+constexpr int kTailRounds = 767;  // sum over rounds of min(h, 256) for tables of <= 1024 entries
+constexpr int kTailLdsWords = 2 * kTailMax + 3 * kTailRounds + 3 * kTailMaxLog + kTailMaxLog;
+constexpr int kTailSmem = kTailLdsWords > kJobLdsWords ? kTailLdsWords : kJobLdsWords;
+
 template <int KIND>
-__global__ __launch_bounds__(kTailThreads) void k_tail(TailArgs in)
+__global__ __launch_bounds__(kTailThreads) void k_tail(TailArgs in, XJobs jobs)
 {
-    constexpr int NT = KindTraits<KIND>::NT, D = KindTraits<KIND>::D;
-    __shared__ uint64_t sm[NT][kTailMax];
-    __shared__ uint64_t rc[kTailMaxLog];  // the rounds' challenges, read once
-    const int tid = threadIdx.x, v = in.v;
-    const uint32_t S = 1u << v;
-    const uint64_t *G[3] = {in.t0, in.t1, in.t2};
+    constexpr int D = KindTraits<KIND>::D;
+    __shared__ uint64_t smem[kTailSmem];
+    if (blockIdx.x > 0) {
+        const int q = blockIdx.x - 1;
+        assemble_slot(jobs.s[q], jobs.part + (size_t)q * jobs.stride, jobs.tr, jobs.xc, smem);
+        return;
+    }
+    uint64_t *ta = smem, *tb = ta + kTailMax, *pe = tb + kTailMax, *red = pe + 3 * kTailRounds, *rc = red + 3 * kTailMaxLog;
+    const int tid = threadIdx.x, v = in.v, NI = blockDim.x;
+    const int S = 1 << v;
     if (tid < v) rc[tid] = in.rho[tid];
-    for (uint32_t i = tid; i < S; i += blockDim.x)
+    for (int i0 = tid; i0 < S; i0 += 4 * NI) {  // loads first
+        uint64_t x[4], y[4];
 #pragma unroll
-        for (int q = 0; q < NT; q++) sm[q][i] = G[q][i];
+        for (int q = 0; q < 4; q++) {
+            const int i = i0 + q * NI;
+            x[q] = i < S ? in.t0[i] : 0;
+            y[q] = i < S ? in.t1[i] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            if (i0 + q * NI < S) {
+                ta[i0 + q * NI] = x[q];
+                tb[i0 + q * NI] = y[q];
+            }
+    }
     __syncthreads();
-    if (v == 0 && in.sum_out && tid == 0) *in.sum_out = m61::mul(sm[0][0], sm[1][0]);  // no rounds: the sum is a b
+    if (v == 0 && in.j0 == 0 && in.sum_out >= 0 && tid == 0)
+        in.tr[in.sum_out] = m61::mul(ta[0], tb[0]);  // no rounds: the sum is a b
+    int off = 0;
     for (int j = 0; j < v; j++) {
-        const uint32_t h = S >> (j + 1);
+        const int h = S >> (j + 1), n = h < NI ? h : NI;
         const uint64_t r = rc[j];
         uint64_t acc[4] = {0, 0, 0, 0};
-        for (uint32_t i = tid; i < h; i += blockDim.x) {
-            uint64_t lo[3] = {0, 0, 0}, hi[3] = {0, 0, 0};
-#pragma unroll
-            for (int q = 0; q < NT; q++) {
-                lo[q] = sm[q][i];
-                hi[q] = sm[q][i + h];
-            }
+        for (int i = tid; i < h; i += NI) {
+            const uint64_t lo[3] = {ta[i], tb[i], 0}, hi[3] = {ta[i + h], tb[i + h], 0};
             pair_contrib<KIND>(lo, hi, acc);
 #pragma unroll
-            for (int q = 0; q < NT; q++) sm[q][i] = m61::add(lo[q], m61::mul(r, m61::sub(hi[q], lo[q])));
+            for (int X = 0; X <= D; X++) acc[X] = m61::fold(acc[X]);
+            ta[i] = fold_to(lo[0], hi[0], r);
+            tb[i] = fold_to(lo[1], hi[1], r);
         }
-        if ((uint32_t)tid < h)
+        if (tid < n)
 #pragma unroll
-            for (int X = 0; X <= D; X++) in.part[(size_t)j * in.stride + (size_t)(D + 1) * tid + X] = acc[X];
+            for (int X = 0; X <= D; X++) pe[(off + tid) * 3 + X] = acc[X];
+        off += n;
         __syncthreads();  // folds of round j visible to round j + 1
     }
+    // per-round sums: eight lanes per (round, X), four terms before each fold
+    const int ntask = 24 * v;
+    for (int task = tid; task < ((ntask + 63) & ~63); task += NI) {  // whole waves iterate together
+        uint64_t acc = 0;
+        const int q = task >> 3, part = task & 7;
+        if (task < ntask) {
+            const int j = q / 3, X = q % 3;
+            int o = 0;
+            for (int jj = 0; jj < j; jj++) o += (S >> (jj + 1)) < NI ? (S >> (jj + 1)) : NI;
+            const int n = (S >> (j + 1)) < NI ? (S >> (j + 1)) : NI;
+            const uint64_t *src = pe + (size_t)o * 3 + X;
+            int e = part;
+            for (; e + 24 < n; e += 32) acc = m61::fold(acc + src[3 * e] + src[3 * (e + 8)] + src[3 * (e + 16)] + src[3 * (e + 24)]);
+            for (; e < n; e += 8) acc = m61::fold(acc + src[3 * e]);
+        }
+        acc = m61::fold(acc + __shfl_xor(acc, 1, 64));
+        acc = m61::fold(acc + __shfl_xor(acc, 2, 64));
+        acc = m61::fold(acc + __shfl_xor(acc, 4, 64));
+        if (task < ntask && part == 0) red[q] = m61::canon(acc);
+    }
+    __syncthreads();
+    if (tid < 3 * v) in.tr[in.ev + 3 * in.j0 + tid] = red[tid];
+    if (tid == 0 && in.j0 == 0 && v > 0 && in.sum_out >= 0) in.tr[in.sum_out] = m61::add(red[0], red[1]);
     if (tid == 0) {
-        if (in.fin0) *in.fin0 = sm[0][0];
-        if (in.fin1) *in.fin1 = sm[1][0];
-        if (NT > 2 && in.fin2) *in.fin2 = sm[NT - 1][0];
+        if (in.fin0) *in.fin0 = m61::canon(ta[0]);
+        if (in.fin1) *in.fin1 = m61::canon(tb[0]);
     }
 }
 
 size_t tail_capacity(int) { return kTailMax; }
-int tail_units(uint32_t h) { return (int)(h < (uint32_t)kTailThreads ? h : kTailThreads); }
 
-void launch_tail(int kind, const TailArgs &a, hipStream_t st)
+void launch_tail(int kind, const TailArgs &a, const XJobs &jobs, hipStream_t st)
 {
     (void)kind;
-    hipLaunchKernelGGL(k_tail<KIND_MATMUL>, dim3(1), dim3(kTailThreads), 0, st, a);
+    hipLaunchKernelGGL(k_tail<KIND_MATMUL>, dim3(1 + jobs.nslot), dim3(kTailThreads), 0, st, a, jobs);
 }
 
 // ---------------------------------------------------------------------------
@@ -245,8 +289,9 @@ __global__ __launch_bounds__(256) void k_range_setup(const uint64_t *__restrict_
         x_setup_body(xs, (blockIdx.x - 1) * blockDim.x + tid, rl, sl, zl);
         return;
     }
+    using namespace m61;
     __shared__ uint64_t c[C_WORDS];
-    __shared__ uint64_t eqs[64];
+    __shared__ uint64_t eqs[64], eqt[kMaxPlaneLog];
     __shared__ uint64_t ch[4 + 2 * kMaxPlaneLog], cl[3];
     __shared__ int pv[3];
     const int P = 1 << lP;
@@ -275,56 +320,62 @@ __global__ __launch_bounds__(256) void k_range_setup(const uint64_t *__restrict_
         while (idx >= off_half(P, j + 1)) j++;
         const int p = idx - off_half(P, j);
         uint64_t acc = 1;
-        for (int i = 0; i < lP - j; i++) acc = m61::mul(acc, m61::eq1_bit(tau[j + i], (p >> (lP - j - 1 - i)) & 1));
-        c[C_E + idx] = acc;
+        for (int i = 0; i < lP - j; i++) {
+            const uint64_t z = tau[j + i];
+            acc = lmul(acc, ((p >> (lP - j - 1 - i)) & 1) ? z : lsub(1, z));
+        }
+        c[C_E + idx] = canon(acc);
     }
     // eq(sigma_p, q) for every plane (for the byte tables below)
     for (int q = tid; q < 64; q += blockDim.x) {
         uint64_t a = 0;
         if (q < P) {
             a = 1;
-            for (int i = 0; i < lP; i++) a = m61::mul(a, m61::eq1_bit(sig[i], (q >> (lP - 1 - i)) & 1));
+            for (int i = 0; i < lP; i++) a = lmul(a, ((q >> (lP - 1 - i)) & 1) ? sig[i] : lsub(1, sig[i]));
         }
-        eqs[q] = a;
+        eqs[q] = canon(a);
     }
+    if (tid < lP) eqt[tid] = eq1(tau[tid], sig[tid]);  // eq(tau_j, sigma_j)
     __syncthreads();
-    for (int j = 1; j <= lP; j++) {  // W_{j+1} = W_j bound at sigma_j; w2_j = 2 W_j[p + h] - W_j[p]
-        const int h = P >> j;
-        const uint64_t *Wj = c + C_W + off_full(P, j);
-        for (int p = tid; p < h; p += blockDim.x) {
-            c[C_W2 + off_half(P, j) + p] = m61::sub(m61::add(Wj[p + h], Wj[p + h]), Wj[p]);
-            if (j < lP) c[C_W + off_full(P, j + 1) + p] = m61::add(Wj[p], m61::mul(sig[j - 1], m61::sub(Wj[p + h], Wj[p])));
-        }
-        __syncthreads();
-    }
-    if (tid == 0) {
-        uint64_t K = 1;
-        for (int j = 1; j <= lP; j++) {
-            c[C_K + j - 1] = K;
-            c[C_TAU + j - 1] = tau[j - 1];
-            K = m61::mul(K, eq1(tau[j - 1], sig[j - 1]));
-        }
-        const uint64_t *Wl = c + C_W + off_full(P, lP);
-        const uint64_t Wp = m61::add(Wl[0], m61::mul(sig[lP - 1], m61::sub(Wl[1], Wl[0])));
-        c[C_EP] = K;                                           // Ep
-        c[C_EP + 1] = m61::sub(m61::mul(mu, Wp), K);           // c = mu Wp - Ep
-        c[C_EP + 2] = Wp;
-        c[C_EP + 3] = mu;
-        // claimed sum mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~); claims = (R~, Rm~, Y~, Z~)
-        uint64_t H = m61::add(m61::mul(lam[0], cl[1]), m61::mul(lam[1], m61::add(cl[0], 1ull << (t + 1))));
-        if (relu) H = m61::add(H, m61::mul(lam[2], cl[2]));
-        *range_sum = m61::mul(mu, H);
-    }
-    __syncthreads();
-    for (int i = tid; i < C_WORDS; i += blockDim.x) cst[i] = c[i];
     // lut[b][v] = sum over the set bits i of v of eq(sigma_p, 8 b + i)
     for (int i = tid; i < 8 * 256; i += blockDim.x) {
         const int b = i >> 8, v = i & 255;
         uint64_t a = 0;
         for (int k = 0; k < 8; k++)
             if ((v >> k) & 1) a += eqs[8 * b + k];
-        lut[i] = m61::canon(a);
+        lut[i] = canon(a);
     }
+    // W_{j+1} = W_j bound at sigma_j; w2_j = 2 W_j[p + h] - W_j[p]; the last
+    // thread carries K_j = prod_{i<j} eq(tau_i, sigma_i) along
+    uint64_t K = 1;
+    for (int j = 1; j <= lP; j++) {
+        const int h = P >> j;
+        const uint64_t *Wj = c + C_W + off_full(P, j);
+        for (int p = tid; p < h; p += blockDim.x) {
+            c[C_W2 + off_half(P, j) + p] = canon(lsub(2 * Wj[p + h], Wj[p]));
+            if (j < lP) c[C_W + off_full(P, j + 1) + p] = canon(Wj[p] + lmul(sig[j - 1], lsub(Wj[p + h], Wj[p])));
+        }
+        if (tid == 255) {
+            c[C_K + j - 1] = canon(K);
+            c[C_TAU + j - 1] = tau[j - 1];
+            K = lmul(K, eqt[j - 1]);
+        }
+        __syncthreads();
+    }
+    if (tid == 255) {
+        const uint64_t *Wl = c + C_W + off_full(P, lP);
+        const uint64_t Wp = fold(Wl[0] + lmul(sig[lP - 1], lsub(Wl[1], Wl[0])));
+        c[C_EP] = canon(K);                     // Ep
+        c[C_EP + 1] = canon(lsub(lmul(mu, Wp), K));  // c = mu Wp - Ep
+        c[C_EP + 2] = canon(Wp);
+        c[C_EP + 3] = mu;
+        // claimed sum mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~); claims = (R~, Rm~, Y~, Z~)
+        uint64_t H = lmul(lam[0], cl[1]) + lmul(lam[1], fold(cl[0] + (1ull << (t + 1))));
+        if (relu) H = fold(H) + lmul(lam[2], cl[2]);
+        *range_sum = canon(lmul(mu, fold(H)));
+    }
+    __syncthreads();
+    for (int i = tid; i < C_WORDS; i += blockDim.x) cst[i] = c[i];
 }
 
 void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,

@@ -12,21 +12,47 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 // eq table (Eq. (1) / chi vector of Sec. II-C):
 //   out[i] = prod_j (z_j i_j + (1 - z_j)(1 - i_j)),  i_1 = MSB of i.
 // ---------------------------------------------------------------------------
-__global__ void k_eq_table(const uint64_t *__restrict__ z, int v, uint64_t *__restrict__ out)
+// Workgroups below nb1 fill the first table (point z1, v1 variables), the
+// others the second; the point is staged in LDS first.
+__global__ __launch_bounds__(256) void k_eq_tables(const uint64_t *__restrict__ z1, int v1, uint64_t *__restrict__ out1,
+                                                   int nb1, const uint64_t *__restrict__ z2, int v2,
+                                                   uint64_t *__restrict__ out2)
+{
+    __shared__ uint64_t zl[64];
+    const bool second = (int)blockIdx.x >= nb1;
+    const uint64_t *z = second ? z2 : z1;
+    const int v = second ? v2 : v1, blk = second ? blockIdx.x - nb1 : blockIdx.x;
+    const int nblk = second ? gridDim.x - nb1 : nb1;
+    uint64_t *out = second ? out2 : out1;
+    if ((int)threadIdx.x < v) zl[threadIdx.x] = z[threadIdx.x];
+    __syncthreads();
+    const uint64_t n = 1ull << v;
+    for (uint64_t i = (uint64_t)blk * blockDim.x + threadIdx.x; i < n; i += (uint64_t)nblk * blockDim.x) {
+        uint64_t acc = 1;
+        for (int j = 0; j < v; j++) {
+            const uint64_t zj = zl[j];
+            acc = m61::lmul(acc, ((i >> (v - 1 - j)) & 1) ? zj : m61::lsub(1, zj));
+        }
+        out[i] = m61::canon(acc);
+    }
+}
+
+static int eq_blocks(int v)
 {
     const uint64_t n = 1ull << v;
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x) {
-        uint64_t acc = 1;
-        for (int j = 0; j < v; j++) acc = m61::mul(acc, m61::eq1_bit(z[j], (uint32_t)(i >> (v - 1 - j)) & 1u));
-        out[i] = acc;
-    }
+    return (int)((n + kThreads - 1) / kThreads < 4096 ? (n + kThreads - 1) / kThreads : 4096);
 }
 
 void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st)
 {
-    const uint64_t n = 1ull << v;
-    const int blocks = (int)((n + kThreads - 1) / kThreads < 4096 ? (n + kThreads - 1) / kThreads : 4096);
-    hipLaunchKernelGGL(k_eq_table, dim3(blocks), dim3(kThreads), 0, st, z, v, out);
+    hipLaunchKernelGGL(k_eq_tables, dim3(eq_blocks(v)), dim3(kThreads), 0, st, z, v, out, eq_blocks(v), z, v, out);
+}
+
+void launch_eq_tables(const uint64_t *z1, int v1, uint64_t *out1, const uint64_t *z2, int v2, uint64_t *out2,
+                      hipStream_t st)
+{
+    const int nb1 = eq_blocks(v1), nb2 = eq_blocks(v2);
+    hipLaunchKernelGGL(k_eq_tables, dim3(nb1 + nb2), dim3(kThreads), 0, st, z1, v1, out1, nb1, z2, v2, out2);
 }
 
 // ---------------------------------------------------------------------------
@@ -73,20 +99,29 @@ __global__ __launch_bounds__(256) void k_bind_rows(const T *__restrict__ A, uint
             m61::add(m61::add(red[0][lane], red[1][lane]), m61::add(red[2][lane], red[3][lane]));
 }
 
-__global__ __launch_bounds__(256) void k_sum_chunks(const uint64_t *__restrict__ part, int nchunks, uint32_t cols,
-                                                    uint64_t *__restrict__ out)
+// The chunk sums of a row binding: 64 columns per workgroup, four threads
+// per column (consecutive lanes), four terms added before each fold.
+__device__ __forceinline__ void sum_chunks_block(const ChunkSum &cs, uint32_t blk)
 {
-    const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= cols) return;
-    uint64_t a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    int q = 0;
-    for (; q + 8 <= nchunks; q += 8)
-#pragma unroll
-        for (int u = 0; u < 8; u++) a[u] = m61::add(a[u], part[(size_t)(q + u) * cols + c]);
-    for (; q < nchunks; q++) a[0] = m61::add(a[0], part[(size_t)q * cols + c]);
-    out[c] = m61::add(m61::add(m61::add(a[0], a[1]), m61::add(a[2], a[3])),
-                      m61::add(m61::add(a[4], a[5]), m61::add(a[6], a[7])));
+    const uint32_t c = blk * 64 + (threadIdx.x >> 2), cols = cs.cols;
+    const int q0 = threadIdx.x & 3, nch = cs.nch;
+    const uint64_t *p = cs.part;
+    uint64_t acc = 0;
+    if (c < cols) {
+        int q = q0;
+        for (; q + 12 < nch; q += 16)
+            acc = m61::fold(acc + p[(size_t)q * cols + c] + p[(size_t)(q + 4) * cols + c] +
+                            p[(size_t)(q + 8) * cols + c] + p[(size_t)(q + 12) * cols + c]);
+        for (; q < nch; q += 4) acc = m61::fold(acc + p[(size_t)q * cols + c]);
+    }
+    acc = m61::fold(acc + __shfl_xor(acc, 1, 64));
+    acc = m61::fold(acc + __shfl_xor(acc, 2, 64));
+    if (c < cols && q0 == 0) cs.out[c] = m61::canon(acc);
 }
+
+__global__ __launch_bounds__(256) void k_sum_chunks(ChunkSum cs) { sum_chunks_block(cs, blockIdx.x); }
+
+static int sum_chunks_blocks(uint32_t cols) { return (int)((cols + 63) / 64); }
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_bind_cols(const T *__restrict__ B, uint32_t rows, uint32_t cols,
@@ -113,7 +148,23 @@ void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, co
     case RA_I64: hipLaunchKernelGGL(k_bind_rows<int64_t>, grid, dim3(256), 0, st, (const int64_t *)T, rows, cols, E, per, scratch); break;
     default: hipLaunchKernelGGL(k_bind_rows<uint64_t>, grid, dim3(256), 0, st, (const uint64_t *)T, rows, cols, E, per, scratch); break;
     }
-    hipLaunchKernelGGL(k_sum_chunks, dim3((cols + 255) / 256), dim3(256), 0, st, (const uint64_t *)scratch, nch, cols, out);
+    const ChunkSum cs{scratch, nch, cols, out};
+    hipLaunchKernelGGL(k_sum_chunks, dim3(sum_chunks_blocks(cols)), dim3(256), 0, st, cs);
+}
+
+ChunkSum launch_bind_rows_chunks(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E,
+                                 uint64_t *scratch, uint64_t *out, hipStream_t st)
+{
+    const int nch = bind_rows_chunks(rows, cols);
+    const uint32_t per = (rows + nch - 1) / nch;
+    dim3 grid((cols + 63) / 64, nch);
+    switch (dtype) {
+    case RA_I16: hipLaunchKernelGGL(k_bind_rows<int16_t>, grid, dim3(256), 0, st, (const int16_t *)T, rows, cols, E, per, scratch); break;
+    case RA_I32: hipLaunchKernelGGL(k_bind_rows<int32_t>, grid, dim3(256), 0, st, (const int32_t *)T, rows, cols, E, per, scratch); break;
+    case RA_I64: hipLaunchKernelGGL(k_bind_rows<int64_t>, grid, dim3(256), 0, st, (const int64_t *)T, rows, cols, E, per, scratch); break;
+    default: hipLaunchKernelGGL(k_bind_rows<uint64_t>, grid, dim3(256), 0, st, (const uint64_t *)T, rows, cols, E, per, scratch); break;
+    }
+    return ChunkSum{scratch, nch, cols, out};
 }
 
 // int16 entries, cols >= 8: E[c] = e_hi 2^31 + e_lo (e_lo < 2^31), so
@@ -125,8 +176,13 @@ void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, co
 constexpr int kBindRowsPerWave = 4;
 
 __global__ __launch_bounds__(256) void k_bind_cols16(const int16_t *__restrict__ B, uint32_t rows, uint32_t cols,
-                                                     const uint64_t *__restrict__ E, uint64_t *__restrict__ out)
+                                                     const uint64_t *__restrict__ E, uint64_t *__restrict__ out,
+                                                     uint32_t nmain, ChunkSum cs)
 {
+    if (blockIdx.x >= nmain) {  // the chunk sums of the other side's binding
+        sum_chunks_block(cs, blockIdx.x - nmain);
+        return;
+    }
     constexpr int RW = kBindRowsPerWave;
     const uint32_t r0 = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) * RW;  // wave-uniform
     const int lane = threadIdx.x & 63;
@@ -162,14 +218,17 @@ __global__ __launch_bounds__(256) void k_bind_cols16(const int16_t *__restrict__
 }
 
 void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *out,
-                      hipStream_t st)
+                      hipStream_t st, const ChunkSum *cs)
 {
     if (dtype == RA_I16 && cols >= 8 && ((uintptr_t)T & 15) == 0) {
-        const uint32_t waves = (rows + kBindRowsPerWave - 1) / kBindRowsPerWave;
-        hipLaunchKernelGGL(k_bind_cols16, dim3((waves + 3) / 4), dim3(256), 0, st, (const int16_t *)T, rows, cols, E,
-                           out);
+        const uint32_t waves = (rows + kBindRowsPerWave - 1) / kBindRowsPerWave, nmain = (waves + 3) / 4;
+        const ChunkSum none{nullptr, 0, 0, nullptr};
+        const uint32_t extra = cs ? sum_chunks_blocks(cs->cols) : 0;
+        hipLaunchKernelGGL(k_bind_cols16, dim3(nmain + extra), dim3(256), 0, st, (const int16_t *)T, rows, cols, E,
+                           out, nmain, cs ? *cs : none);
         return;
     }
+    if (cs) hipLaunchKernelGGL(k_sum_chunks, dim3(sum_chunks_blocks(cs->cols)), dim3(256), 0, st, *cs);
     dim3 grid((rows + 3) / 4);  // four waves (rows) per block
     switch (dtype) {
     case RA_I16: hipLaunchKernelGGL(k_bind_cols<int16_t>, grid, dim3(256), 0, st, (const int16_t *)T, rows, cols, E, out); break;

@@ -524,21 +524,34 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
     if (bits_words < N) return RA_E_BUFSIZE;
     // with t given and deferred outputs, the plane count is known on the host
     // and the call need not wait; otherwise it waits for t and P
+    // with t given, the parameters (but for the range check of R, which the
+    // rescale pass makes) are fixed on the host; in deferred mode the call
+    // then need not wait.  Otherwise a min / max pass finds t and P first.
     int hP = 0, hlP = 0;
-    const bool known = c->deferred && io->t >= 0;
-    if (known) {
+    const bool given = io->t >= 0, known = c->deferred && given;
+    WitParams hp{};
+    if (given) {
         const ra_status pst = plane_params((int)io->s, io->t, (int)io->relu, &hP, &hlP);
         if (pst != RA_OK) return pst;
+        hp.status = 0;
+        hp.t = io->t;
+        hp.P = hP;
+        hp.lP = hlP;
+        hp.s = (int)io->s;
+        hp.relu = (int)io->relu;
+        hp.mode = (int)io->round_mode;
+        hp.t_in = io->t;
     }
     const int nb = witness_blocks(N);
     Carve cv;
     const size_t o_mm = cv.take<int64_t>(2 * (size_t)nb), o_cl = cv.take<uint64_t>(4 * (size_t)nb);
+    const size_t o_fl = cv.take<uint32_t>((size_t)nb);
     ra_status st = ensure_ws(c, cv.off);
     if (st != RA_OK) return st;
     const int lk = log2u(k);
     size_t o_st = 0;
     if ((st = stage_take(c, 12, &o_st)) != RA_OK) return st;
-    {
+    if (!given) {
         Timed tm(c, G_WIT_MINMAX);
         launch_witness_params(d_C, N, (int)io->s, (int)io->relu, (int)io->round_mode, io->t,
                               (int64_t *)(c->ws + o_mm), c->d_params, c->stream);
@@ -546,7 +559,8 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
     {
         Timed tm(c, G_WIT_RESCALE);
         launch_witness_rescale(d_C, N, lk, c->d_eq, c->d_eq + n, d_R, d_Rm, d_Y, d_Z, d_bits,
-                               (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims, c->d_stage + o_st, c->stream);
+                               (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims, c->d_stage + o_st, c->stream,
+                               given ? &hp : nullptr, (uint32_t *)(c->ws + o_fl));
     }
     // parameters (words 0-7) and claims (words 8-11) are staged together
     auto fill = [c, io, known](const uint64_t *h) {

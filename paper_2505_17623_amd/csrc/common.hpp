@@ -102,10 +102,14 @@ void launch_bind_cols(const void *T, int dtype, uint32_t rows, uint32_t cols, co
 int witness_blocks(uint64_t N);
 void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mode, int t_in, int64_t *mm_part,
                            WitParams *params, hipStream_t st);
-// mirror (optional): 12 words, the parameters (words 0-7) and the claims (8-11)
+// mirror (optional): 12 words, the parameters (words 0-7) and the claims (8-11).
+// known (optional): parameters computed on the host for a given t (status 0);
+// then no params pass runs before, the range of R is checked here (flags:
+// witness_blocks(N) words) and the parameters are written to params.
 void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
                             uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
-                            const WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st);
+                            WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st,
+                            const WitParams *known = nullptr, uint32_t *flags = nullptr);
 
 // ---- launchers (sumcheck.hip) ----
 int round_blocks(uint64_t h);

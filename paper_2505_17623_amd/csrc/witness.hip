@@ -344,24 +344,31 @@ __global__ __launch_bounds__(256) void k_wit_params(const int64_t *__restrict__ 
 // Pass 2: R, Rm, Y, Z, the bit word and per-block claims, then one block
 // sums the claims (R~, Rm~, Y~, Z~ at (r1, r2)) and mirrors the parameters and
 // claims to `mirror` (12 words) when it is given.
+// With t given (known != 0) the parameters come by value and every workgroup
+// also flags, in flags[block], whether one of its R lies outside the range;
+// the final kernel turns the flags into the status.
 __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, uint64_t N, int lk,
                                                  const WitParams *__restrict__ prm, const uint64_t *__restrict__ E1,
                                                  const uint64_t *__restrict__ E2, int32_t *__restrict__ R,
                                                  uint16_t *__restrict__ Rm, int32_t *__restrict__ Y,
                                                  int32_t *__restrict__ Z, uint64_t *__restrict__ bits,
-                                                 uint64_t *__restrict__ claim_part)
+                                                 uint64_t *__restrict__ claim_part, WitParams hp, int known,
+                                                 uint32_t *__restrict__ flags)
 {
     __shared__ uint64_t red[m61::block_sum_words(4, 256)];
-    const WitParams p = *prm;
+    const WitParams p = known ? hp : *prm;
     if (p.status != 0) return;  // uniform over the grid
     const int s = p.s, t = p.t, relu = p.relu;
     const int64_t half = p.mode == RA_ROUND_NEAREST ? (int64_t)1 << (s - 1) : 0;
     const int64_t shift_r = (int64_t)1 << (t + 1);
     const uint64_t kmask = (1ull << lk) - 1;
     uint64_t acc[4] = {0, 0, 0, 0};
+    int out_of_range = 0;
     for (uint64_t x = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; x < N; x += (uint64_t)gridDim.x * blockDim.x) {
         const int64_t c = C[x] + half;
         const int64_t q = c >> s;
+        // u = R for R >= 0, -R - 1 for R < 0; R in [-2^(t+1), 2^(t+1)) iff u < 2^(t+1)
+        out_of_range |= ((uint64_t)(q >= 0 ? q : -(q + 1)) >> (t + 1)) != 0;
         const int32_t rm = (int32_t)(c - (q << s));
         const int32_t r = (int32_t)q;
         const int32_t y = r < 0 ? -r : r;
@@ -379,17 +386,31 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
         acc[2] = m61::add(acc[2], m61::mul_small(e, y));
         acc[3] = m61::add(acc[3], m61::mul_small(e, z));
     }
+    if (known) {
+        const int any = __syncthreads_or(out_of_range);
+        if (threadIdx.x == 0) flags[blockIdx.x] = (uint32_t)any;
+    }
     m61::block_sum<4>(acc, red);
     if (threadIdx.x == 0)
         for (int i = 0; i < 4; i++) claim_part[4 * blockIdx.x + i] = acc[i];
 }
 
 __global__ __launch_bounds__(256) void k_claims_final(const uint64_t *__restrict__ part, int nblk,
-                                                      const WitParams *__restrict__ prm, uint64_t *__restrict__ out,
-                                                      uint64_t *__restrict__ mirror)
+                                                      WitParams *__restrict__ prm, uint64_t *__restrict__ out,
+                                                      uint64_t *__restrict__ mirror, WitParams hp, int known,
+                                                      const uint32_t *__restrict__ flags)
 {
     __shared__ uint64_t red[m61::block_sum_words(4, 256)];
-    const WitParams p = *prm;
+    WitParams p;
+    if (known) {  // the status from the workgroups' range flags; the parameters for the range call
+        int any = 0;
+        for (int b = threadIdx.x; b < nblk; b += blockDim.x) any |= flags[b] != 0;
+        p = hp;
+        if (__syncthreads_or(any)) p.status = RA_E_RANGE;
+        if (threadIdx.x == 0) *prm = p;
+    } else {
+        p = *prm;
+    }
     uint64_t acc[4] = {0, 0, 0, 0};
     if (p.status == 0)
         for (int b = threadIdx.x; b < nblk; b += blockDim.x)
@@ -399,7 +420,7 @@ __global__ __launch_bounds__(256) void k_claims_final(const uint64_t *__restrict
     if (p.status == 0)
         for (int i = 0; i < 4; i++) out[i] = acc[i];
     if (mirror) {
-        const uint64_t *pw = (const uint64_t *)prm;
+        const uint64_t *pw = (const uint64_t *)&p;
         for (int i = 0; i < 8; i++) mirror[i] = i * 8 < (int)sizeof(WitParams) ? pw[i] : 0;
         for (int i = 0; i < 4; i++) mirror[8 + i] = acc[i];
     }
@@ -416,13 +437,15 @@ void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mo
 
 void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
                             uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
-                            const WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st)
+                            WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st,
+                            const WitParams *known, uint32_t *flags)
 {
     const int nb = witness_blocks(N);
-    hipLaunchKernelGGL(k_rescale, dim3(nb), dim3(kThreads), 0, st, C, N, lk, params, E1, E2, R, Rm, Y, Z, bits,
-                       claim_part);
+    const WitParams hp = known ? *known : WitParams{};
+    hipLaunchKernelGGL(k_rescale, dim3(nb), dim3(kThreads), 0, st, C, N, lk, (const WitParams *)params, E1, E2, R, Rm,
+                       Y, Z, bits, claim_part, hp, known ? 1 : 0, flags);
     hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, (const uint64_t *)claim_part, nb, params,
-                       claims_out, mirror);
+                       claims_out, mirror, hp, known ? 1 : 0, (const uint32_t *)flags);
 }
 
 }  // namespace ra

@@ -18,10 +18,51 @@ namespace ra {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int kTile = 64;   // block tile (rows and columns) and k-chunk
-constexpr int kRowPad = 80; // LDS row stride in bytes (64 + 16)
+constexpr int kTile = 64;    // block tile (rows and columns)
+// LDS stages (k steps of 64) per block: 64 KB for int16 A, 72 KB for int32 A
+template <int LA> constexpr int gemm_stages() { return LA == 2 ? 4 : 3; }
 
 __host__ __device__ inline uint32_t round_up64(uint32_t v) { return (v + 63u) & ~63u; }
+
+// Limb planes are stored as MFMA fragments.  For a block of 32 rows R and a
+// block of 32 bytes q along the inner dimension, the 64 lanes' 16-byte
+// operands of v_mfma_i32_32x32x32_i8 (lane l: row 32 R + (l & 31), bytes
+// 32 q + 16 (l >> 5) .. + 16) lie contiguously in 1 KB, at
+// frag_off(plane, R, q) + 16 l, so one wave moves a whole fragment with one
+// 16-byte load per lane.
+__host__ __device__ inline size_t frag_off(int plane, uint32_t R, uint32_t q, uint32_t nR, uint32_t nQ)
+{
+    return (((size_t)plane * nR + R) * nQ + q) * 1024;
+}
+__host__ __device__ inline uint32_t frag_lane(uint32_t row, uint32_t kb) { return (row & 31) + 32 * ((kb >> 4) & 1); }
+
+typedef __attribute__((address_space(3))) int8_t lds_i8;
+
+// Wait until at most N of the wave's LDS reads are outstanding; the operands
+// of the half that has then landed pass through the wait, so that nothing
+// that uses them is scheduled before it.  (Each step's operands are fresh
+// values, so no register copy of them can precede the wait.)
+template <int N, int LA>
+__device__ __forceinline__ void lds_wait(v4i (&a)[LA], v4i (&b)[2])
+{
+    static_assert(N >= 0 && N < 16, "lgkmcnt field");
+    if constexpr (LA == 2)
+        asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]) : "i"(N) : "memory");
+    else
+        asm volatile("s_waitcnt lgkmcnt(%6)"
+                     : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1])
+                     : "i"(N)
+                     : "memory");
+}
+
+// s_waitcnt that waits until at most N vector-memory operations of the wave
+// are outstanding (expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void vm_wait()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
 
 // Byte gathers: v_perm_b32 picks bytes of {hi, lo} (selector bytes 0-3 from
 // lo, 4-7 from hi, 0x0c gives zero).
@@ -42,7 +83,6 @@ __device__ __forceinline__ void split_a_block(const TA *__restrict__ A, uint32_t
     const uint32_t row = blk * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= np) return;  // wave-uniform
-    const size_t plane = (size_t)np * mp;
     int64_t s = 0;
     for (uint32_t c = lane * 16; c < mp; c += 1024) {
         v4i out[LA];
@@ -99,7 +139,8 @@ __device__ __forceinline__ void split_a_block(const TA *__restrict__ A, uint32_t
             for (int u = 0; u < LA; u++) out[u] = v4i{0, 0, 0, 0};
         }
 #pragma unroll
-        for (int u = 0; u < LA; u++) *(v4i *)&Al[u * plane + (size_t)row * mp + c] = out[u];
+        for (int u = 0; u < LA; u++)
+            *(v4i *)&Al[frag_off(u, row >> 5, c >> 5, np >> 5, mp >> 5) + 16 * frag_lane(row, c)] = out[u];
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
@@ -139,7 +180,6 @@ __device__ __forceinline__ void split_bt_block(const int16_t *__restrict__ B, ui
     __syncthreads();
     const int jj = tid >> 2, ch = (tid & 3) * 16;
     const uint32_t j = j0 + jj;
-    const size_t plane = (size_t)kp * mp;
     v4i o0, o1;
     int32_t sum = 0;
 #pragma unroll
@@ -157,8 +197,9 @@ __device__ __forceinline__ void split_bt_block(const int16_t *__restrict__ B, ui
         o0[w] = (int)lo;
         o1[w] = (int)hi;
     }
-    *(v4i *)&Bt[(size_t)j * mp + l0 + ch] = o0;
-    *(v4i *)&Bt[plane + (size_t)j * mp + l0 + ch] = o1;
+    const uint32_t kb = l0 + ch;
+    *(v4i *)&Bt[frag_off(0, j >> 5, kb >> 5, kp >> 5, mp >> 5) + 16 * frag_lane(j, kb)] = o0;
+    *(v4i *)&Bt[frag_off(1, j >> 5, kb >> 5, kp >> 5, mp >> 5) + 16 * frag_lane(j, kb)] = o1;
     cs[tid & 3][jj] = sum;
     __syncthreads();
     if (tid < 64 && j0 + tid < k)
@@ -182,60 +223,118 @@ __global__ __launch_bounds__(256) void k_split(const TA *__restrict__ A, uint32_
 }
 
 // 64 x 64 output tile per block; wave (wr, wc) owns the 32 x 32 sub-tile.
-template <int LA>
+// The k dimension goes in steps of 64 bytes through S LDS stages: every step
+// needs F = 2 (2 LA + 4) fragments (two 32-byte halves of A: LA limbs x 2
+// row blocks, and of B: 2 limbs x 2 column blocks), F / 4 per wave, fetched
+// straight into LDS (global_load_lds_dwordx4) S - 1 steps ahead.  Each limb
+// pair (u, v) has its own accumulator, so the MFMAs of a step do not wait on
+// each other.  Tiles are ordered so that the blocks on one XCD (block b runs
+// on XCD b mod 8) share columns of B.
+template <int LA, int S>
 __global__ __launch_bounds__(256) void k_gemm_mfma(const int8_t *__restrict__ Al, const int8_t *__restrict__ Bt,
                                                    const int64_t *__restrict__ rowsum,
                                                    const int64_t *__restrict__ colpart, int ntiles, int64_t cA,
                                                    uint32_t n, uint32_t m, uint32_t k, uint32_t np, uint32_t mp,
                                                    uint32_t kp, int64_t *__restrict__ C)
 {
-    constexpr int W = LA + 1;  // limb weights 0 .. LA
-    __shared__ __attribute__((aligned(16))) int8_t As[LA][kTile][kRowPad];
-    __shared__ __attribute__((aligned(16))) int8_t Bs[2][kTile][kRowPad];
-    __shared__ int64_t s_cs[4][kTile];
+    constexpr int F1 = 2 * LA + 4, F = 2 * F1, FW = F / 4;
+    static_assert(F % 4 == 0, "fragments per wave");
+    static_assert(S >= 2, "a stage read while the next fills");
+    __shared__ __attribute__((aligned(1024))) int8_t stage[S][F][1024];
+    __shared__ int64_t s_cs[4][kTile], s_rs[kTile];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wr = wv >> 1, wc = wv & 1, half = lane >> 5;
-    const uint32_t i0 = blockIdx.y * kTile, j0 = blockIdx.x * kTile;
-    const size_t aplane = (size_t)np * mp, bplane = (size_t)kp * mp;
-    {   // column sums of this block's columns over all row tiles of B: wave w takes tiles w, w + 4, ...
-        int64_t cs[4] = {0, 0, 0, 0};
-        if (j0 + lane < k) {
-            int ti = wv;
-            for (; ti + 12 < ntiles; ti += 16)
+    const uint32_t nbi = np / kTile, nblk = nbi * (kp / kTile);
+    uint32_t t = blockIdx.x;
+    if ((nblk & 7) == 0) t = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
+    const uint32_t bi = t % nbi, bj = t / nbi, i0 = bi * kTile, j0 = bj * kTile;
+    const uint32_t nR = np >> 5, nC = kp >> 5, nQ = mp >> 5, nS = mp >> 6;
+    const int8_t *src[FW];
 #pragma unroll
-                for (int q = 0; q < 4; q++) cs[q] += colpart[(size_t)(ti + 4 * q) * kp + j0 + lane];
-            for (; ti < ntiles; ti += 4) cs[0] += colpart[(size_t)ti * kp + j0 + lane];
-        }
-        s_cs[wv][lane] = cs[0] + cs[1] + cs[2] + cs[3];
+    for (int e = 0; e < FW; e++) {
+        const int f = FW * wv + e, kk = f / F1, f1 = f % F1;
+        src[e] = (f1 < 2 * LA ? Al + frag_off(f1 >> 1, 2 * bi + (f1 & 1), kk, nR, nQ)
+                              : Bt + frag_off((f1 - 2 * LA) >> 1, 2 * bj + ((f1 - 2 * LA) & 1), kk, nC, nQ)) +
+                 16 * lane;
     }
-    v16i acc[W];
+    auto issue = [&](uint32_t q, int sl) {
 #pragma unroll
-    for (int w = 0; w < W; w++)
+        for (int e = 0; e < FW; e++)
+            __builtin_amdgcn_global_load_lds((const void *)(src[e] + (size_t)q * 2048),
+                                             (__attribute__((address_space(3))) void *)&stage[sl][FW * wv + e][0], 16,
+                                             0, 0);
+    };
+    // column sums of this block's columns over all row tiles of B (wave w takes
+    // tiles w, w + 4, ...) and the row sums of its rows: loads issued first,
+    // values used after the loop
+    int64_t cs[4] = {0, 0, 0, 0}, rs = 0;
+    if (j0 + lane < k) {
+        int ti = wv;
+        for (; ti + 12 < ntiles; ti += 16)
+#pragma unroll
+            for (int q = 0; q < 4; q++) cs[q] += colpart[(size_t)(ti + 4 * q) * kp + j0 + lane];
+        for (; ti < ntiles; ti += 4) cs[0] += colpart[(size_t)ti * kp + j0 + lane];
+    }
+    if (tid < kTile && i0 + tid < n) rs = rowsum[i0 + tid];
+    // accumulators: int16 A, one per limb pair (index 2 u + v); int32 A, one per
+    // weight u + v (the step's MFMAs, in (k half, v, u) order, update each at
+    // most every third instruction)
+    constexpr int NACC = LA == 2 ? 4 : LA + 1;
+    v16i acc[NACC];
+#pragma unroll
+    for (int w = 0; w < NACC; w++)
 #pragma unroll
         for (int r = 0; r < 16; r++) acc[w][r] = 0;
-    const int lr = tid >> 2, lp = (tid & 3) * 16;  // staging: row, 16-byte piece
-    for (uint32_t k0 = 0; k0 < mp; k0 += kTile) {
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_i8 *)&stage[0][0][0] + 16 * lane;
 #pragma unroll
-        for (int u = 0; u < LA; u++)
-            *(v4i *)&As[u][lr][lp] = *(const v4i *)&Al[u * aplane + (size_t)(i0 + lr) * mp + k0 + lp];
+    for (int q = 0; q < S - 1; q++)
+        if ((uint32_t)q < nS) issue(q, q);
+    for (uint32_t q = 0; q < nS; q++) {
+        // this wave's fragments of step q have landed once at most (S - 2) later
+        // steps are in flight
+        if (q + S - 2 < nS) vm_wait<(S - 2) * FW>();
+        else vm_wait<0>();
+        // every wave's fragments of step q have landed, and every wave is done
+        // with step q - 1 (a plain barrier: a fence here would also wait for
+        // the steps still in flight)
+        asm volatile("s_barrier" ::: "memory");
+        if (q + S - 1 < nS) issue(q + S - 1, (q + S - 1) % S);
+        // The operands are read with explicit LDS reads: the compiler cannot
+        // tell which stage a pending LDS DMA writes and would otherwise wait
+        // for all of them before any LDS read.  The second 32-byte half is
+        // still being read while the first half's MFMAs run.
+        const uint32_t sa = lds0 + (q % S) * (F * 1024) + 1024 * wr, sb = sa + 1024 * (wc - wr);
+        v4i a[2][LA], b[2][2];
 #pragma unroll
-        for (int v = 0; v < 2; v++)
-            *(v4i *)&Bs[v][lr][lp] = *(const v4i *)&Bt[v * bplane + (size_t)(j0 + lr) * mp + k0 + lp];
-        __syncthreads();
-#pragma unroll
-        for (int ks = 0; ks < 2; ks++) {
-            const int ko = 32 * ks + 16 * half;
-            v4i a[LA], b[2];
-#pragma unroll
-            for (int u = 0; u < LA; u++) a[u] = *(const v4i *)&As[u][32 * wr + (lane & 31)][ko];
-#pragma unroll
-            for (int v = 0; v < 2; v++) b[v] = *(const v4i *)&Bs[v][32 * wc + (lane & 31)][ko];
+        for (int kk = 0; kk < 2; kk++) {
 #pragma unroll
             for (int u = 0; u < LA; u++)
+                asm volatile("ds_read_b128 %0, %1 offset:%2"
+                             : "=v"(a[kk][u])
+                             : "v"(sa), "i"((kk * F1 + 2 * u) * 1024)
+                             : "memory");
 #pragma unroll
-                for (int v = 0; v < 2; v++) acc[u + v] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[u], b[v], acc[u + v], 0, 0, 0);
+            for (int v = 0; v < 2; v++)
+                asm volatile("ds_read_b128 %0, %1 offset:%2"
+                             : "=v"(b[kk][v])
+                             : "v"(sb), "i"((kk * F1 + 2 * LA + 2 * v) * 1024)
+                             : "memory");
         }
-        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 2; kk++) {
+            if (kk == 0) lds_wait<LA + 2, LA>(a[0], b[0]);
+            else lds_wait<0, LA>(a[1], b[1]);
+#pragma unroll
+            for (int v = 0; v < 2; v++)
+#pragma unroll
+                for (int u = 0; u < LA; u++) {
+                    const int w = LA == 2 ? 2 * u + v : u + v;
+                    acc[w] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[kk][u], b[kk][v], acc[w], 0, 0, 0);
+                }
+        }
     }
+    s_cs[wv][lane] = cs[0] + cs[1] + cs[2] + cs[3];
+    if (tid < kTile) s_rs[tid] = rs;
+    __syncthreads();
     // recombination in wrap-around 64-bit arithmetic: exact because C itself fits int64
     const int cl = 32 * wc + (lane & 31);
     const uint32_t col = j0 + cl;
@@ -243,11 +342,14 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const int8_t *__restrict__ Al
     const uint64_t corr = (uint64_t)cA * (uint64_t)colsum - (uint64_t)(128 * cA) * m;
 #pragma unroll
     for (int r = 0; r < 16; r++) {
-        const uint32_t row = i0 + 32 * wr + 8 * (r / 4) + 4 * half + (r % 4);
+        const uint32_t lrow = 32 * wr + 8 * (r / 4) + 4 * half + (r % 4), row = i0 + lrow;
         if (row < n && col < k) {
-            uint64_t c = corr + 128 * (uint64_t)rowsum[row];
+            uint64_t c = corr + 128 * (uint64_t)s_rs[lrow];
 #pragma unroll
-            for (int w = 0; w < W; w++) c += (uint64_t)(int64_t)acc[w][r] << (8 * w);
+            for (int w = 0; w < NACC; w++) {
+                const int wt = LA == 2 ? (w >> 1) + (w & 1) : w;  // weight 256^wt
+                c += (uint64_t)(int64_t)acc[w][r] << (8 * wt);
+            }
             C[(size_t)row * k + col] = (int64_t)c;
         }
     }
@@ -280,13 +382,13 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
     else
         hipLaunchKernelGGL((k_split<int16_t, 2>), dim3(na + nb), dim3(256), 0, st, (const int16_t *)A, n, m, np, mp, Al,
                            rowsum, na, B, k, kp, Bt, colpart);
-    const dim3 grid(kp / kTile, np / kTile);
+    const dim3 grid((kp / kTile) * (np / kTile));
     if (a_is_i32)
-        hipLaunchKernelGGL(k_gemm_mfma<4>, grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
+        hipLaunchKernelGGL((k_gemm_mfma<4, gemm_stages<4>()>), grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
                            (const int64_t *)rowsum, (const int64_t *)colpart, ntiles, (int64_t)8421504, n, m, k, np,
                            mp, kp, C);
     else
-        hipLaunchKernelGGL(k_gemm_mfma<2>, grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
+        hipLaunchKernelGGL((k_gemm_mfma<2, gemm_stages<2>()>), grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
                            (const int64_t *)rowsum, (const int64_t *)colpart, ntiles, (int64_t)128, n, m, k, np, mp,
                            kp, C);
 }

@@ -126,7 +126,8 @@ KERNEL_GROUP = [("k_gemm_mfma", "gemm_mfma"), ("k_split", "gemm_mfma"), ("k_zero
                 ("k_xrounds", "range_rounds"), ("k_xblock", "range_rounds"), ("k_range_setup", "range_setup"),
                 ("k_rounds", "matmul_rounds"), ("k_tail", "matmul_tail"), ("k_eq_table", "eq_table"),
                 ("k_assemble", "assemble")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+def traffic_file(cfg):
+    return os.path.join(ROOT, "profiles", f"traffic_config{cfg}.json")
 
 
 def sources_digest():
@@ -141,10 +142,10 @@ def sources_digest():
 
 
 def traffic_of(group, cfg):
-    """Measured HBM bytes per step of a kernel group (profiles/traffic.json), or
+    """Measured HBM bytes per step of a kernel group (profiles/traffic_config<cfg>.json), or
     None when they were taken on other sources or another workload."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(traffic_file(cfg)) as fh:
             t = json.load(fh)
     except OSError:
         return None
@@ -215,13 +216,13 @@ def main():
                          "of known size, to scale hardware byte counters)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc runs of this bench (FETCH_SIZE, WRITE_SIZE) into "
-                         "profiles/traffic.json and print it; no GPU work")
+                         "profiles/traffic_config<C>.json and print it; no GPU work")
     args = ap.parse_args()
     if args.pmc_summary:
         steps_run = max(args.warmup, 1) + 1 + 2 * args.steps
         t = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.config, steps_run,
                         args.copy_calibration or 256)
-        with open(TRAFFIC_FILE, "w") as fh:
+        with open(traffic_file(args.config), "w") as fh:
             json.dump(t, fh, indent=1)
         print(json.dumps(t, indent=1))
         return

@@ -108,13 +108,11 @@ ra_status ensure_eq(ra_ctx *c, size_t words)
 // Kernel groups timed with events when profiling is on.
 enum Group {
     G_EQ = 0, G_GEMM, G_BIND_ROWS, G_BIND_COLS, G_MM_ROUNDS, G_MM_TAIL, G_WIT_MINMAX, G_WIT_RESCALE,
-    G_RANGE_SETUP, G_RANGE_PLANE, G_RANGE_ROUNDS, G_RANGE_TAIL, G_X_SETUP, G_RELU_ROUNDS, G_RELU_TAIL,
-    G_ASSEMBLE, G_COUNT
+    G_RANGE_SETUP, G_RANGE_PLANE, G_RANGE_ROUNDS, G_RANGE_TAIL, G_COUNT
 };
 const char *const kGroupName[G_COUNT] = {
     "eq_table", "gemm_mfma", "bind_rows", "bind_cols", "matmul_rounds", "matmul_tail", "witness_minmax",
-    "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail", "x_setup",
-    "relu_rounds", "relu_tail", "assemble"};
+    "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail"};
 
 hipEvent_t take_event(ra_ctx *c)
 {

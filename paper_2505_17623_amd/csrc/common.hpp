@@ -57,10 +57,6 @@ struct Slot {
     int32_t sum_out;   // >= 0: also write g(0) + g(1) (the instance's claimed sum) there
     int32_t out2;      // SLOT_X with ReLU: offset of the ReLU round's evaluations, else -1
 };
-struct SlotTable {
-    int32_t count;
-    Slot s[kMaxSlots];
-};
 
 // Set-up of the rounds over x (xsetup.hpp): r the EQ point, sigma_x and rho'
 // (nullptr without ReLU), lN variables, L of them in the low part.
@@ -153,15 +149,14 @@ struct XConst {
     const uint64_t *kp, *r, *Kr, *Kz;
 };
 // Plane rounds of the range check, evaluated by extra workgroups of the
-// assembly (plane_round.hpp): G, sigma_p, the constant block, transcript
-// words 0 .. 4 lP.  lP = 0: none.
+// first x-round launch (plane_round.hpp): G, sigma_p, the constant block,
+// transcript words 0 .. 4 lP.  lP = 0: none.
 struct PlaneArgs {
     const uint64_t *G, *sigma, *cst;
     uint64_t *tr;
     int lP;
 };
-void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, const XConst &xc,
-                     const PlaneArgs &pa, hipStream_t st);
+
 
 // ---- launchers (xrounds.hip) ----
 struct XArgs {

@@ -34,7 +34,7 @@ __host__ __device__ constexpr int frag_row(int l, int r) { return 8 * (r / 4) + 
 __device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (tp == 2 ? 1 : 0); }
 __device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
 
-// Block layout of the Gram pass: twelve waves with two roles, working on
+// Block layout of the Gram pass: sixteen waves with two roles, working on
 // slabs of kSlab outputs through a double-buffered LDS area.
 //   producers (waves 0-7, one output per thread): EQ(x), Bx and the digits
 //     of EQ(x); the wave's 64 bit words transposed into plane-major order (a
@@ -90,7 +90,6 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
 {
     using S = GramShape<TP>;
     constexpr int NPL = S::kPlanes, DW = S::kDigitsPerWave, NPT = TP == 1 ? 1 : 2;
-    constexpr int NP = 64 * kProducers;               // producer threads
     constexpr int kPlaneBytes = NPL * kRow, kTileBytes = TP * 1024 * 8;
     static_assert(2 * kPlaneBytes >= kTileBytes, "the tiles reuse the plane buffers");
     __shared__ uint64_t s_lut[8 * 256];                                    // Bx byte tables

@@ -1,14 +1,15 @@
 // sumcheck.hip -- the prover's sum-check rounds (Sec. II-D) of the matrix
-// product instance sum_l a(l) b(l) (degree 2, Eq. (4)), the constants of the
-// concatenated range check, and the transcript assembly.  The rounds over x
-// of the range and ReLU instances are in xrounds.hip.
+// product instance sum_l a(l) b(l) (degree 2, Eq. (4)) and the constants of
+// the concatenated range check.  The rounds over x of the range and ReLU
+// instances are in xrounds.hip.
 //
 // Variables are bound most-significant first, so round j pairs entry i with
 // entry i + h of the current table (h = half its size): both halves stream
 // contiguously.  The challenges are known before the first round (the
 // verifier's coins are a given stream), so every round is launched back to
-// back; a round writes per-block partial sums that one assembly kernel
-// reduces at the end, and folds the tables in place: T[i] <- T[i] +
+// back; the global rounds write per-block partial sums, and the LDS tail that
+// finishes the instance also reduces them (extra workgroups) and its own
+// rounds into the transcript.  Tables fold in place: T[i] <- T[i] +
 // rho (T[i + h] - T[i]) for i < h (thread i alone reads i and i + h).
 #include "common.hpp"
 #include "m61.hpp"
@@ -386,32 +387,6 @@ void launch_range_setup(const uint64_t *chal, const WitParams *params, const uin
                        lut, xs);
 }
 
-// ---------------------------------------------------------------------------
-// Transcript assembly: reduce every slot's per-block partials and write the
-// round evaluations (plane rounds combined as described above).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_assemble(SlotTable slots, const uint64_t *__restrict__ part, int part_stride,
-                                                  uint64_t *__restrict__ tr, XConst xc, PlaneArgs pa)
-{
-    __shared__ uint64_t lds[kJobLdsWords];
-    const int si = blockIdx.x;
-    if (si >= slots.count) {  // a plane round
-        plane_round(pa, si - slots.count + 1, lds);
-        return;
-    }
-    assemble_slot(slots.s[si], part + (size_t)si * part_stride, tr, xc, lds);
-}
-
-void launch_assemble(const SlotTable &slots, const uint64_t *part, int part_stride, uint64_t *tr, const XConst &xc,
-                     const PlaneArgs &pa, hipStream_t st)
-{
-    if (slots.count + pa.lP == 0) return;
-    hipLaunchKernelGGL(k_assemble, dim3(slots.count + pa.lP), dim3(256), 0, st, slots, part, part_stride, tr, xc, pa);
-}
-
-}  // namespace ra
-
-namespace ra {
 // Kernel attributes set once per process (none needed at present).
 void init_kernel_attributes() {}
 }  // namespace ra

@@ -122,7 +122,7 @@ KERNEL_GROUP = [("k_gemm_mfma", "gemm_mfma"), ("k_split", "gemm_mfma"), ("k_zero
                 ("k_bind_rows", "bind_rows"), ("k_sum_chunks", "bind_rows"), ("k_bind_cols", "bind_cols"),
                 ("k_minmax", "witness_minmax"), ("k_wit_params", "witness_minmax"),
                 ("k_rescale", "witness_rescale"), ("k_claims_final", "witness_rescale"),
-                ("k_plane_gram", "range_plane"), ("k_gram_reduce", "range_plane"),
+                ("k_plane_gram", "range_plane"), ("k_gram_reduce", "range_setup"),
                 ("k_xrounds", "range_rounds"), ("k_xblock", "range_rounds"), ("k_range_setup", "range_setup"),
                 ("k_rounds", "matmul_rounds"), ("k_tail", "matmul_tail"), ("k_eq_table", "eq_table"),
                 ("k_assemble", "assemble")]

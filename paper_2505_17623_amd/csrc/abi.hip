@@ -636,7 +636,6 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const size_t o_kr = cv.take<uint64_t>(lN + 1), o_kz = cv.take<uint64_t>(lN + 1);
     const size_t o_wsh = cv.take<uint64_t>(1ull << Bp);
     const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
-    const size_t o_lut = cv.take<uint64_t>(8 * 256);
     const size_t o_gp = cv.take<uint64_t>((size_t)gblocks * gtiles * 1024);
     const size_t o_gs = cv.take<uint64_t>(64 * 64);
     ra_status st = ensure_ws(c, cv.off);
@@ -649,19 +648,19 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     size_t o_tr = 0;
     if ((st = stage_take(c, trw, &o_tr)) != RA_OK) return st;
     uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = c->d_stage + o_tr;
-    uint64_t *lut = (uint64_t *)(c->ws + o_lut), *gpart = (uint64_t *)(c->ws + o_gp), *gsum = (uint64_t *)(c->ws + o_gs);
+    uint64_t *gpart = (uint64_t *)(c->ws + o_gp), *gsum = (uint64_t *)(c->ws + o_gs);
     const uint64_t *sigx = sigma + lP, *rz = relu ? rho2 : nullptr;
     hipStream_t s = c->stream;
 
-    {
-        Timed tm(c, G_RANGE_SETUP);
-        const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
-        launch_range_setup(lam, c->d_params, c->d_claims, lP, cst, tr + RS, lut, xs, s);
-    }
     {   // plane rounds: Gram matrix on the matrix cores, Bx per output
         Timed tm(c, G_RANGE_PLANE);
-        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, lut, Bx, gpart, s);
-        launch_gram_reduce(lP, N, gpart, gsum, s);
+        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, sigma, Bx, gpart, s);
+    }
+    {   // the Gram matrix; further workgroups: the constant block and the x set-up
+        Timed tm(c, G_RANGE_SETUP);
+        const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
+        const RangeConsts rc{lam, c->d_params, c->d_claims, lP, cst, tr + RS};
+        launch_gram_reduce(lP, N, gpart, gsum, rc, xs, s);
     }
     // Each x launch's extra workgroups assemble the rounds of the launch
     // before it; the first one also evaluates the plane rounds, the last

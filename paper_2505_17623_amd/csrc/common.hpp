@@ -136,12 +136,16 @@ struct XJobs;
 // The tail workgroup, plus one workgroup per slot in jobs (SLOT_COPY slots of
 // the global rounds before it).
 void launch_tail(int kind, const TailArgs &a, const XJobs &jobs, hipStream_t st);
-// range constants: lambda/mu/tau_p/sigma_p at `chal`, claims from the witness
-size_t range_consts_words(int lP);
-// also writes the 8 x 256 byte tables of the plane-bound table Bx to lut, and
-// (further workgroups) the set-up of the rounds over x
-void launch_range_setup(const uint64_t *chal, const WitParams *params, const uint64_t *claims, int lP, uint64_t *cst,
-                        uint64_t *tr_range_sum, uint64_t *lut, const XSetupArgs &xs, hipStream_t st);
+// Constant block of the plane rounds (rsetup.hpp): lambda/mu/tau_p/sigma_p at
+// chal, the witness parameters and claims; writes cst (C_WORDS) and the
+// claimed sum of the range instance.
+struct RangeConsts {
+    const uint64_t *chal;
+    const WitParams *prm;
+    const uint64_t *claims;
+    int lP;
+    uint64_t *cst, *range_sum;
+};
 void init_kernel_attributes();
 // Constants of SLOT_X rounds: kp = (Ep, c) of the range summand, r the EQ
 // point, Kr / Kz the prefix products of the range and ReLU instances.
@@ -208,10 +212,13 @@ void launch_xblock(bool relu, bool first, const XBlockArgs &a, const XJobs &jobs
 // ---- launchers (planes.hip) ----
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
-// Bx per x and the blocks' partial Gram tiles (plane_gram_blocks x tiles x 1024 words)
+// Bx per x and the blocks' partial Gram tiles (plane_gram_blocks x tiles x 1024
+// words); sig: sigma_p (lP words)
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, hipStream_t st);
-// the Gram matrix G (gsum: 64 x 64 words, both triangles) from the partial tiles
-void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, hipStream_t st);
+                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, hipStream_t st);
+// the Gram matrix G (gsum: 64 x 64 words, both triangles) from the partial
+// tiles; further workgroups run the set-up of the range check (rc, xs)
+void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,
+                        const XSetupArgs &xs, hipStream_t st);
 
 }  // namespace ra

@@ -19,6 +19,7 @@
 // (eight byte lookups per x), the input of the rounds over x.
 #include "common.hpp"
 #include "m61.hpp"
+#include "rsetup.hpp"
 
 namespace ra {
 
@@ -85,7 +86,7 @@ __device__ __forceinline__ uint64_t balanced_digit_bytes(uint64_t e)
 template <int TP>
 __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const uint64_t *__restrict__ bits, uint64_t N, int lk, const uint64_t *__restrict__ E1,
-    const uint64_t *__restrict__ E2, const uint64_t *__restrict__ lut, uint64_t *__restrict__ Bx,
+    const uint64_t *__restrict__ E2, const uint64_t *__restrict__ sig, int lP, uint64_t *__restrict__ Bx,
     uint64_t *__restrict__ gpart)
 {
     using S = GramShape<TP>;
@@ -93,6 +94,7 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     constexpr int kPlaneBytes = NPL * kRow, kTileBytes = TP * 1024 * 8;
     static_assert(2 * kPlaneBytes >= kTileBytes, "the tiles reuse the plane buffers");
     __shared__ uint64_t s_lut[8 * 256];                                    // Bx byte tables
+    __shared__ uint64_t s_eqs[64];                                         // eq(sigma_p, q)
     __shared__ uint64_t s_exp[256];                                        // byte -> eight 0x00 / 0xFF bytes
     __shared__ __attribute__((aligned(16))) int8_t s_d[2][kLimbs][kSlab];  // digits of EQ(x)
     // plane bytes of two slabs; afterwards the block's Gram tiles (entry
@@ -102,7 +104,17 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
     const bool producer = wv < kProducers;  // wave-uniform
     const int cw = wv - kProducers;         // consumer index = its digit
-    for (int i = tid; i < 8 * 256; i += kGramThreads) s_lut[i] = lut[i];
+    if (tid < 64) {  // eq(sigma_p, q) for every plane q
+        uint64_t a = 0;
+        if (tid < (1 << lP)) {
+            a = 1;
+            for (int i = 0; i < lP; i++) {
+                const uint64_t z = sig[i];
+                a = m61::lmul(a, ((tid >> (lP - 1 - i)) & 1) ? z : m61::lsub(1, z));
+            }
+        }
+        s_eqs[tid] = m61::canon(a);
+    }
     for (int i = tid; i < 256; i += kGramThreads) {
         uint64_t e = 0;
         for (int b = 0; b < 8; b++)
@@ -112,6 +124,16 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const uint64_t kmask = (1ull << lk) - 1;
     const uint64_t nslabs = (N + kSlab - 1) / kSlab;
     const uint64_t mine = nslabs > blockIdx.x ? (nslabs - blockIdx.x + gridDim.x - 1) / gridDim.x : 0;
+    __syncthreads();
+    // byte tables of Bx(x) = sum_q eq(sigma_p, q) bit_q(x): lut[b][v] = sum
+    // over the set bits i of v of eq(sigma_p, 8 b + i)
+    for (int i = tid; i < 8 * 256; i += kGramThreads) {
+        const int b = i >> 8, v = i & 255;
+        uint64_t a = 0;
+        for (int k = 0; k < 8; k++)
+            if ((v >> k) & 1) a += s_eqs[8 * b + k];  // eight values below 2^61
+        s_lut[i] = m61::canon(a);
+    }
     __syncthreads();  // byte tables ready
     // The two roles run separate loops with the same barriers (one per slab),
     // so the consumers' accumulators are not live in the producers' code.
@@ -223,22 +245,40 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
 // Sum of the blocks' partial tiles, written as G[q][q'] (64 x 64, both
 // triangles).  Each block covers 64 tile entries; its four waves split the
 // partial blocks and combine through LDS.
+// Workgroups below nred: 16 entries of G each, sixteen lanes per entry (lane
+// group g sums the partial tiles of blocks g, g + 16, ...), then LDS.  The
+// next workgroup writes the constant block of the plane rounds, the others
+// run the set-up of the rounds over x.
 __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict__ gpart, int nblk, int TP,
-                                                     uint64_t *__restrict__ G)
+                                                     uint64_t *__restrict__ G, int nred, RangeConsts rc,
+                                                     XSetupArgs xs)
 {
-    __shared__ uint64_t red[4][64];
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, entries = TP * 1024;
-    const int e = blockIdx.x * 64 + lane;
-    uint64_t a[4] = {0, 0, 0, 0};
-    int b = wid;
-    for (; b + 12 < nblk; b += 16)
-#pragma unroll
-        for (int u = 0; u < 4; u++) a[u] = m61::add(a[u], gpart[(size_t)(b + 4 * u) * entries + e]);
-    for (; b < nblk; b += 4) a[0] = m61::add(a[0], gpart[(size_t)b * entries + e]);
-    red[wid][lane] = m61::add(m61::add(a[0], a[1]), m61::add(a[2], a[3]));
+    if ((int)blockIdx.x > nred) {
+        x_setup_block(xs, blockIdx.x - nred - 1);
+        return;
+    }
+    if ((int)blockIdx.x == nred) {
+        range_consts_block(rc);
+        return;
+    }
+    __shared__ uint64_t red[16][17];
+    const int tid = threadIdx.x, el = tid & 15, g = tid >> 4, entries = TP * 1024;
+    const int e = blockIdx.x * 16 + el;
+    uint64_t a = 0;
+    int b = g;
+    for (; b + 48 < nblk; b += 64) {  // four partials per iteration, loads first, one fold
+        const uint64_t v0 = gpart[(size_t)b * entries + e], v1 = gpart[(size_t)(b + 16) * entries + e];
+        const uint64_t v2 = gpart[(size_t)(b + 32) * entries + e], v3 = gpart[(size_t)(b + 48) * entries + e];
+        a = m61::fold(a + v0 + v1 + v2 + v3);
+    }
+    for (; b < nblk; b += 16) a = m61::fold(a + gpart[(size_t)b * entries + e]);
+    red[g][el] = a;
     __syncthreads();
-    if (wid != 0) return;
-    const uint64_t v = m61::add(m61::add(red[0][lane], red[1][lane]), m61::add(red[2][lane], red[3][lane]));
+    if (tid >= 16) return;
+    uint64_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 16; q += 4) v = m61::fold(v + red[q][el] + red[q + 1][el] + red[q + 2][el] + red[q + 3][el]);
+    v = m61::canon(v);
     const int tp = e >> 10, r = (e & 1023) >> 6, l = e & 63;
     const int q = 32 * tile_row(tp, TP) + frag_row(l, r), q2 = 32 * tile_col(tp, TP) + (l & 31);
     G[q * 64 + q2] = v;
@@ -255,19 +295,23 @@ int plane_gram_blocks(uint64_t N, int lP)
 }
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *lut, uint64_t *Bx, uint64_t *gpart, hipStream_t st)
+                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, hipStream_t st)
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
     if (TP == 1)
-        hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, lut, Bx, gpart);
+        hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
+                           gpart);
     else
-        hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, lut, Bx, gpart);
+        hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
+                           gpart);
 }
 
-void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, hipStream_t st)
+void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,
+                        const XSetupArgs &xs, hipStream_t st)
 {
-    const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
-    hipLaunchKernelGGL(k_gram_reduce, dim3(TP * 16), dim3(256), 0, st, gpart, nb, TP, gsum);
+    const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP), nred = TP * 64;
+    const int xb = (x_setup_count(xs) + 255) / 256;
+    hipLaunchKernelGGL(k_gram_reduce, dim3(nred + 1 + xb), dim3(256), 0, st, gpart, nb, TP, gsum, nred, rc, xs);
 }
 
 }  // namespace ra

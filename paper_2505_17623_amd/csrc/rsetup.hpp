@@ -1,0 +1,130 @@
+// rsetup.hpp -- set-up of the concatenated range check: the constant block
+// of the plane rounds and the tables of the rounds over x (xsetup.hpp).  Run
+// by extra workgroups of the Gram reduction (planes.hip).
+#pragma once
+#include "common.hpp"
+#include "m61.hpp"
+#include "xsetup.hpp"
+
+namespace ra {
+
+// ---------------------------------------------------------------------------
+// Concatenated range check: constants of the plane rounds.
+//
+// Over b(q, x) (q = plane, first log P variables) the summand is
+//   eq(tau_p, q) EQ(x) b (b - 1) + mu W(q) EQ(x) b,   EQ(x) = eq((r1, r2), x),
+// W(q) = lambda_g 2^bit.  While plane variable j is free (x still Boolean):
+//   g_j(X) = K_j eq(tau_j, X) A_j(X) + mu Bw_j(X),
+//   A_j(X)  = sum_x EQ(x) sum_p' eq(tau_{>j}, p') b_X (b_X - 1),
+//   Bw_j(X) = sum_x EQ(x) sum_p' W_j(X, p') b_X,
+// where K_j = eq(tau_{<j}, sigma_{<j}), W_j is W bound at sigma_{<j}, and
+// b_X = b(sigma_{<j}, X, p', x).  A_j and Bw_j are quadratic in X, so the
+// plane kernel sums them at X = 0, 1, 2 and the assembly extends to X = 3.
+// After all plane rounds the summand is EQ(x) (Ep b^2 + (mu Wp - Ep) b) with
+// Ep = eq(tau_p, sigma_p), Wp = W~(sigma_p), the rounds over x of xrounds.hip.
+// ---------------------------------------------------------------------------
+__host__ __device__ constexpr int off_half(int P, int j) { return P - (P >> (j - 1)); }      // e_j, w2_j
+__host__ __device__ constexpr int off_full(int P, int j) { return 2 * P - 2 * (P >> (j - 1)); }  // W_j
+
+__device__ __forceinline__ uint64_t eq1(uint64_t a, uint64_t b)
+{
+    return m61::add(m61::mul(a, b), m61::mul(m61::sub(1, a), m61::sub(1, b)));
+}
+
+// Workgroup q (of x_setup_blocks) of the set-up of the rounds over x; the
+// challenges are first staged in LDS.
+__device__ __forceinline__ void x_setup_block(const XSetupArgs &xs, int q)
+{
+    const int tid = threadIdx.x;
+    __shared__ uint64_t rl[64], sl[64], zl[64];
+    if (tid < xs.lN) {
+        rl[tid] = xs.r[tid];
+        sl[tid] = xs.sigx[tid];
+        zl[tid] = xs.rho2 ? xs.rho2[tid] : 0;
+    }
+    __syncthreads();
+    x_setup_body(xs, q * blockDim.x + tid, rl, sl, zl);
+}
+
+// The constant block of the plane rounds (one workgroup of at least 256
+// threads); chal points at lambda1: lambda1..3, mu, tau_p (lP), sigma
+// (lP + ...).  Every operand is first staged in LDS.
+__device__ __forceinline__ void range_consts_block(const RangeConsts &rc)
+{
+    const uint64_t *chal = rc.chal, *claims = rc.claims;
+    const WitParams *prm = rc.prm;
+    const int lP = rc.lP, tid = threadIdx.x;
+    uint64_t *cst = rc.cst, *range_sum = rc.range_sum;
+    using namespace m61;
+    __shared__ uint64_t c[C_WORDS];
+    __shared__ uint64_t eqt[kMaxPlaneLog];
+    __shared__ uint64_t ch[4 + 2 * kMaxPlaneLog], cl[3];
+    __shared__ int pv[3];
+    const int P = 1 << lP;
+    if (tid < 4 + 2 * lP) ch[tid] = chal[tid];
+    if (tid >= 64 && tid < 67) cl[tid - 64] = claims[tid - 64];
+    if (tid == 128) {
+        pv[0] = prm->s;
+        pv[1] = prm->t;
+        pv[2] = prm->relu;
+    }
+    for (int i = tid; i < C_WORDS; i += blockDim.x) c[i] = 0;
+    __syncthreads();
+    const int s = pv[0], t = pv[1], relu = pv[2];
+    const uint64_t *lam = ch, mu = ch[3], *tau = ch + 4, *sig = ch + 4 + lP;
+    // W_1 = W: plane q holds bit b of group g -> lambda_g 2^b
+    for (int q = tid; q < P; q += blockDim.x) {
+        int g = -1, b = 0;
+        if (q < s) g = 0, b = q;
+        else if (q < s + t + 2) g = 1, b = q - s;
+        else if (relu && q < s + 2 * t + 4) g = 2, b = q - s - t - 2;
+        c[C_W + q] = g < 0 ? 0 : m61::mul(lam[g], 1ull << b);
+    }
+    // e_j[p] = eq(tau_{j+1..lP}, p) for all rounds j at once
+    for (int idx = tid; idx < P - 1; idx += blockDim.x) {
+        int j = 1;
+        while (idx >= off_half(P, j + 1)) j++;
+        const int p = idx - off_half(P, j);
+        uint64_t acc = 1;
+        for (int i = 0; i < lP - j; i++) {
+            const uint64_t z = tau[j + i];
+            acc = lmul(acc, ((p >> (lP - j - 1 - i)) & 1) ? z : lsub(1, z));
+        }
+        c[C_E + idx] = canon(acc);
+    }
+    if (tid < lP) eqt[tid] = eq1(tau[tid], sig[tid]);  // eq(tau_j, sigma_j)
+    __syncthreads();
+    // W_{j+1} = W_j bound at sigma_j; w2_j = 2 W_j[p + h] - W_j[p]; the last
+    // thread carries K_j = prod_{i<j} eq(tau_i, sigma_i) along
+    uint64_t K = 1;
+    for (int j = 1; j <= lP; j++) {
+        const int h = P >> j;
+        const uint64_t *Wj = c + C_W + off_full(P, j);
+        for (int p = tid; p < h; p += blockDim.x) {
+            c[C_W2 + off_half(P, j) + p] = canon(lsub(2 * Wj[p + h], Wj[p]));
+            if (j < lP) c[C_W + off_full(P, j + 1) + p] = canon(Wj[p] + lmul(sig[j - 1], lsub(Wj[p + h], Wj[p])));
+        }
+        if (tid == 255) {  // (the workgroup has at least 256 threads)
+            c[C_K + j - 1] = canon(K);
+            c[C_TAU + j - 1] = tau[j - 1];
+            K = lmul(K, eqt[j - 1]);
+        }
+        __syncthreads();
+    }
+    if (tid == 255) {
+        const uint64_t *Wl = c + C_W + off_full(P, lP);
+        const uint64_t Wp = fold(Wl[0] + lmul(sig[lP - 1], lsub(Wl[1], Wl[0])));
+        c[C_EP] = canon(K);                     // Ep
+        c[C_EP + 1] = canon(lsub(lmul(mu, Wp), K));  // c = mu Wp - Ep
+        c[C_EP + 2] = canon(Wp);
+        c[C_EP + 3] = mu;
+        // claimed sum mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~); claims = (R~, Rm~, Y~, Z~)
+        uint64_t H = lmul(lam[0], cl[1]) + lmul(lam[1], fold(cl[0] + (1ull << (t + 1))));
+        if (relu) H = fold(H) + lmul(lam[2], cl[2]);
+        *range_sum = canon(lmul(mu, fold(H)));
+    }
+    __syncthreads();
+    for (int i = tid; i < C_WORDS; i += blockDim.x) cst[i] = c[i];
+}
+
+}  // namespace ra

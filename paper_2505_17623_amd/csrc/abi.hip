@@ -256,10 +256,12 @@ int log2_tail() { return log2u(tail_capacity(0)); }
 // launches while the table exceeds the LDS tail, then the tail, which also
 // assembles every round.  Round j's width = D + 1 evaluations go to
 // tr[ev_base + width j]; the tables' final values to finals[0..NT); with
-// sum_out >= 0 the claimed sum to tr[sum_out].
+// sum_out >= 0 the claimed sum to tr[sum_out].  With tail_out given, the
+// tail is not launched: its arguments and jobs go to tail_out / jobs_out for
+// a launch that carries it as extra workgroups.
 void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v,
                   const uint64_t *rho, uint64_t *tr, int ev_base, int width, uint64_t *finals, int sum_out,
-                  uint64_t *part, int g_rounds, int g_tail)
+                  uint64_t *part, int g_rounds, int g_tail, TailArgs *tail_out = nullptr, XJobs *jobs_out = nullptr)
 {
     const int cmax = fused_rounds_max(kind), lt = log2_tail();
     XJobs jobs{};
@@ -281,12 +283,15 @@ void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t
         lS -= C;
         j += C;
     }
-    {
-        Timed tm(c, g_tail, st);
-        const TailArgs ta{t0, t1, t2, v - j, rho + j, tr, ev_base, j, sum_out, finals,
-                          finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr};
-        launch_tail(kind, ta, jobs, st);
+    const TailArgs ta{t0, t1, t2, v - j, rho + j, tr, ev_base, j, sum_out, finals,
+                      finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr};
+    if (tail_out) {
+        *tail_out = ta;
+        *jobs_out = jobs;
+        return;
     }
+    Timed tm(c, g_tail, st);
+    launch_tail(kind, ta, jobs, st);
 }
 }  // namespace
 
@@ -487,12 +492,15 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
         Timed tm(c, G_BIND_COLS, z);
         launch_bind_cols(d_B, RA_I16, m, k, E2, b, z, &cs);
     }
-    // transcript: [c0][evals 3 lm][a*][b*]
+    // transcript: [c0][evals 3 lm][a*][b*]; the instance's tail runs as extra
+    // workgroups of the product launch
+    TailArgs ta{};
+    XJobs tjobs{};
     run_instance(c, z, KIND_MATMUL, a, b, nullptr, lm, rho, tr, 1, 3, tr + 1 + 3 * lm, 0, part, G_MM_ROUNDS,
-                 G_MM_TAIL);
+                 G_MM_TAIL, &ta, &tjobs);
     {
         Timed tm(c, G_GEMM);
-        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s);
+        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s, &ta, &tjobs);
     }
     c->n = n;
     c->m = m;

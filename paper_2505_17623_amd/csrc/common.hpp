@@ -76,8 +76,12 @@ void launch_eq_tables(const uint64_t *z1, int v1, uint64_t *out1, const uint64_t
 // ---- launchers (gemm.hip) ----
 constexpr uint32_t kGemmMaxInner = 32768;  // exactness bound of the int32 limb accumulators
 size_t gemm_workspace_bytes(int a_is_i32, uint32_t n, uint32_t m, uint32_t k);
+struct TailArgs;
+struct XJobs;
+// ta, jobs (optional): the matrix instance's tail (launch_tail) as extra
+// workgroups of the product launch
 void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
-                      void *ws, hipStream_t st);
+                      void *ws, hipStream_t st, const TailArgs *ta = nullptr, const XJobs *jobs = nullptr);
 // rows binding: out[c] = sum_r E[r] T[r, c]; needs scratch of bind_rows_chunks(rows, cols) * cols words
 int bind_rows_chunks(uint32_t rows, uint32_t cols);
 void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,

@@ -12,6 +12,7 @@
 // at most two limb products share a weight, so |S_w| <= 2 m 2^14 fits int32
 // for m <= 32768, and the int64 recombination is exact.
 #include "common.hpp"
+#include "tail.hpp"
 
 namespace ra {
 
@@ -230,20 +231,30 @@ __global__ __launch_bounds__(256) void k_split(const TA *__restrict__ A, uint32_
 // pair (u, v) has its own accumulator, so the MFMAs of a step do not wait on
 // each other.  Tiles are ordered so that the blocks on one XCD (block b runs
 // on XCD b mod 8) share columns of B.
+//
+// Workgroups past the last tile run the last rounds of the product's
+// sum-check instance (tail.hpp), which needs only the bound vectors, in the
+// stage area's LDS: the single-workgroup tail then runs beside the tiles
+// instead of after them.
 template <int LA, int S>
 __global__ __launch_bounds__(256) void k_gemm_mfma(const int8_t *__restrict__ Al, const int8_t *__restrict__ Bt,
                                                    const int64_t *__restrict__ rowsum,
                                                    const int64_t *__restrict__ colpart, int ntiles, int64_t cA,
                                                    uint32_t n, uint32_t m, uint32_t k, uint32_t np, uint32_t mp,
-                                                   uint32_t kp, int64_t *__restrict__ C)
+                                                   uint32_t kp, int64_t *__restrict__ C, TailArgs ta, XJobs jobs)
 {
     constexpr int F1 = 2 * LA + 4, F = 2 * F1, FW = F / 4;
     static_assert(F % 4 == 0, "fragments per wave");
     static_assert(S >= 2, "a stage read while the next fills");
+    static_assert(kTailSmem * 8 <= S * F * 1024, "the tail fits the stage area");
     __shared__ __attribute__((aligned(1024))) int8_t stage[S][F][1024];
     __shared__ int64_t s_cs[4][kTile], s_rs[kTile];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wr = wv >> 1, wc = wv & 1, half = lane >> 5;
     const uint32_t nbi = np / kTile, nblk = nbi * (kp / kTile);
+    if (blockIdx.x >= nblk) {  // workgroup-uniform
+        tail_block<KIND_MATMUL>(ta, jobs, (int)(blockIdx.x - nblk), (uint64_t *)&stage[0][0][0]);
+        return;
+    }
     uint32_t t = blockIdx.x;
     if ((nblk & 7) == 0) t = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
     const uint32_t bi = t % nbi, bj = t / nbi, i0 = bi * kTile, j0 = bj * kTile;
@@ -363,7 +374,7 @@ size_t gemm_workspace_bytes(int a_is_i32, uint32_t n, uint32_t m, uint32_t k)
 }
 
 void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
-                      void *ws, hipStream_t st)
+                      void *ws, hipStream_t st, const TailArgs *ta, const XJobs *jobs)
 {
     const uint32_t np = round_up64(n), mp = round_up64(m), kp = round_up64(k);
     const int LA = a_is_i32 ? 4 : 2, ntiles = (int)(mp / 64);
@@ -382,15 +393,21 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
     else
         hipLaunchKernelGGL((k_split<int16_t, 2>), dim3(na + nb), dim3(256), 0, st, (const int16_t *)A, n, m, np, mp, Al,
                            rowsum, na, B, k, kp, Bt, colpart);
-    const dim3 grid((kp / kTile) * (np / kTile));
+    // tail workgroups (and the slot assemblies they bring) after the tiles
+    const TailArgs tnone{};
+    XJobs jnone{};
+    const uint32_t extra = ta ? 1u + (uint32_t)jobs->nslot : 0u;
+    const dim3 grid((kp / kTile) * (np / kTile) + extra);
+    const TailArgs &tav = ta ? *ta : tnone;
+    const XJobs &jv = ta ? *jobs : jnone;
     if (a_is_i32)
         hipLaunchKernelGGL((k_gemm_mfma<4, gemm_stages<4>()>), grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
                            (const int64_t *)rowsum, (const int64_t *)colpart, ntiles, (int64_t)8421504, n, m, k, np,
-                           mp, kp, C);
+                           mp, kp, C, tav, jv);
     else
         hipLaunchKernelGGL((k_gemm_mfma<2, gemm_stages<2>()>), grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
                            (const int64_t *)rowsum, (const int64_t *)colpart, ntiles, (int64_t)128, n, m, k, np, mp,
-                           kp, C);
+                           kp, C, tav, jv);
 }
 
 }  // namespace ra

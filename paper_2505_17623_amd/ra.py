@@ -212,12 +212,15 @@ def ra_mle_bind(ctx: Context, T: torch.Tensor, bind_rows: bool, point, field: bo
     return out
 
 
-def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor):
-    """Returns (C, transcript dict); in deferred mode the dict is filled at ctx.sync()."""
+def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None):
+    """Returns (C, transcript dict); in deferred mode the dict is filled at ctx.sync().
+    C (optional): an int64 n x k device tensor to write the product to."""
     n, m = A.shape
     m2, k = B.shape
     assert m == m2 and B.dtype == torch.int16
-    C = torch.empty((n, k), dtype=torch.int64, device=A.device)
+    if C is None:
+        C = torch.empty((n, k), dtype=torch.int64, device=A.device)
+    assert C.shape == (n, k) and C.dtype == torch.int64 and C.is_contiguous()
     lm = m.bit_length() - 1
     ev = np.zeros(max(3 * lm, 1), dtype=np.uint64)
     pr = MatmulProof()
@@ -230,17 +233,25 @@ def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor):
     return C, res
 
 
-def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1):
+def witness_outputs(n: int, k: int, device):
+    """Device tensors (R, Rm, Y, Z, bits) for a witness call on an n x k product."""
+    return (torch.empty((n, k), dtype=torch.int32, device=device),
+            torch.empty((n, k), dtype=torch.int16, device=device),   # uint16 bits
+            torch.empty((n, k), dtype=torch.int32, device=device),
+            torch.empty((n, k), dtype=torch.int32, device=device),
+            torch.empty(n * k, dtype=torch.int64, device=device))    # uint64 words
+
+
+def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1,
+                            outs=None):
     """Returns ((R, Rm, Y, Z, bits), info).  info.t and info.P are set on return
     (at once when t is given); the claims in info are final after ctx.sync()
-    in deferred mode."""
+    in deferred mode.  outs (optional): the five output tensors, as made by
+    witness_outputs."""
     n, k = C.shape
-    dev = C.device
-    R = torch.empty((n, k), dtype=torch.int32, device=dev)
-    Rm = torch.empty((n, k), dtype=torch.int16, device=dev)   # uint16 bits
-    Y = torch.empty((n, k), dtype=torch.int32, device=dev)
-    Z = torch.empty((n, k), dtype=torch.int32, device=dev)
-    bits = torch.empty(n * k, dtype=torch.int64, device=dev)  # uint64 words
+    R, Rm, Y, Z, bits = witness_outputs(n, k, C.device) if outs is None else outs
+    for tsr, dt in ((R, torch.int32), (Rm, torch.int16), (Y, torch.int32), (Z, torch.int32), (bits, torch.int64)):
+        assert tsr.dtype == dt and tsr.numel() == n * k and tsr.is_contiguous()
     info = WitnessInfo(s=s, relu=int(bool(relu)), round_mode=mode, t=t)
     _check(lib().ra_rescale_relu_witness(ctx.h, _dptr(C), n, k, _dptr(R), _dptr(Rm), _dptr(Y), _dptr(Z),
                                          _dptr(bits), n * k, ctypes.byref(info)), "ra_rescale_relu_witness")
@@ -267,11 +278,20 @@ def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
     return res
 
 
-def prove_layer(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1):
+def prove_layer(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1,
+                bufs: dict | None = None):
     """The three calls of one layer; returns device tensors and the transcript
-    (complete at once, or after ctx.sync() in deferred mode)."""
-    C, mm = ra_sumcheck_matmul_prove(ctx, A, B)
-    (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t)
+    (complete at once, or after ctx.sync() in deferred mode).  bufs (optional):
+    a dict that keeps the layer's device outputs, made on first use and
+    written again by later calls with it (a caller proving the same shapes
+    repeatedly saves the allocations)."""
+    n, k = A.shape[0], B.shape[1]
+    if bufs is not None and "C" not in bufs:
+        bufs["C"] = torch.empty((n, k), dtype=torch.int64, device=A.device)
+        bufs["wit"] = witness_outputs(n, k, A.device)
+    C, mm = ra_sumcheck_matmul_prove(ctx, A, B, None if bufs is None else bufs["C"])
+    (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t,
+                                                        None if bufs is None else bufs["wit"])
     rs = ra_range_prove(ctx, bits, R, Y, info)
     tr = {}
 
@@ -288,11 +308,16 @@ def to_device(a: np.ndarray, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
-def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None):
+def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None):
     """Prove every layer of a workload in order.  A layer's input is the
     previous output on the device (MLP chains) or the workload's link (im2col)
     applied on the host.  X / Bs may hold device copies of the inputs; ts may
-    give each layer's range parameter t (else it is derived from the data)."""
+    give each layer's range parameter t (else it is derived from the data);
+    bufs (optional) is a list of per-layer output dicts (prove_layer), grown
+    on first use."""
+    if bufs is not None:
+        while len(bufs) < len(workload.layers):
+            bufs.append({})
     X = to_device(workload.X, device) if X is None else X
     Bs = [to_device(L.B, device) for L in workload.layers] if Bs is None else Bs
     outs = []
@@ -305,7 +330,8 @@ def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=Non
         else:
             A = to_device(workload.links[li](Z.cpu().numpy()), device)
         t = -1 if ts is None else int(ts[li])
-        res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t)
+        res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t,
+                          None if bufs is None else bufs[li])
         res["A"] = A
         Z = res["Z"]
         outs.append(res)

@@ -34,6 +34,8 @@ struct ra_ctx {
     int phase = 0;  // 0: expects matmul, 1: expects witness, 2: expects range
     uint32_t n = 0, m = 0, k = 0;
     uint64_t *d_eq = nullptr;  // E1 (n words) then E2 (k words)
+    uint64_t *d_acc = nullptr;  // row-binding accumulators of the fused front (zero between calls)
+    size_t acc_cap = 0;
     const uint64_t *d_r12 = nullptr;  // the layer's (r1, r2) in the challenge stream
     size_t eq_cap = 0;
     WitParams *d_params = nullptr;
@@ -105,14 +107,29 @@ ra_status ensure_eq(ra_ctx *c, size_t words)
     return RA_OK;
 }
 
+// Row-binding accumulators for m columns (2 m words).  They are zero between
+// calls: the first reader of each word clears it.
+ra_status ensure_acc(ra_ctx *c, size_t m)
+{
+    if (2 * m <= c->acc_cap) return RA_OK;
+    RA_HIP(hipStreamSynchronize(c->stream));
+    if (c->d_acc) RA_HIP(hipFree(c->d_acc));
+    c->d_acc = nullptr;
+    c->acc_cap = 0;
+    if (hipMalloc((void **)&c->d_acc, 2 * m * 8) != hipSuccess) return RA_E_NOMEM;
+    RA_HIP(hipMemset(c->d_acc, 0, 2 * m * 8));
+    c->acc_cap = 2 * m;
+    return RA_OK;
+}
+
 // Kernel groups timed with events when profiling is on.
 enum Group {
     G_EQ = 0, G_GEMM, G_BIND_ROWS, G_BIND_COLS, G_MM_ROUNDS, G_MM_TAIL, G_WIT_MINMAX, G_WIT_RESCALE,
-    G_RANGE_SETUP, G_RANGE_PLANE, G_RANGE_ROUNDS, G_RANGE_TAIL, G_COUNT
+    G_RANGE_SETUP, G_RANGE_PLANE, G_RANGE_ROUNDS, G_RANGE_TAIL, G_FRONT, G_COUNT
 };
 const char *const kGroupName[G_COUNT] = {
     "eq_table", "gemm_mfma", "bind_rows", "bind_cols", "matmul_rounds", "matmul_tail", "witness_minmax",
-    "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail"};
+    "witness_rescale", "range_setup", "range_plane", "range_rounds", "range_tail", "matmul_front"};
 
 hipEvent_t take_event(ra_ctx *c)
 {
@@ -261,7 +278,8 @@ int log2_tail() { return log2u(tail_capacity(0)); }
 // a launch that carries it as extra workgroups.
 void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t1, uint64_t *t2, int v,
                   const uint64_t *rho, uint64_t *tr, int ev_base, int width, uint64_t *finals, int sum_out,
-                  uint64_t *part, int g_rounds, int g_tail, TailArgs *tail_out = nullptr, XJobs *jobs_out = nullptr)
+                  uint64_t *part, int g_rounds, int g_tail, TailArgs *tail_out = nullptr, XJobs *jobs_out = nullptr,
+                  uint64_t *acc0 = nullptr)
 {
     const int cmax = fused_rounds_max(kind), lt = log2_tail();
     XJobs jobs{};
@@ -274,7 +292,7 @@ void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t
         {
             Timed tm(c, g_rounds, st);
             launch_rounds(kind, C, t0, t1, t2, 1ull << lS, rho + j, nullptr, part + (size_t)jobs.nslot * kPartStride,
-                          kPartStride, st);
+                          kPartStride, st, j == 0 ? acc0 : nullptr);
         }
         const int nb = round_blocks(1ull << (lS - C));
         for (int r = 0; r < C; r++)
@@ -284,7 +302,7 @@ void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t
         j += C;
     }
     const TailArgs ta{t0, t1, t2, v - j, rho + j, tr, ev_base, j, sum_out, finals,
-                      finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr};
+                      finals ? finals + 1 : nullptr, finals ? finals + 2 : nullptr, j == 0 ? acc0 : nullptr};
     if (tail_out) {
         *tail_out = ta;
         *jobs_out = jobs;
@@ -353,6 +371,7 @@ ra_status ra_ctx_destroy(ra_ctx *c)
     if (c->stream || c->ws || c->d_chal) (void)hipStreamSynchronize(c->stream);
     if (c->d_chal) (void)hipFree(c->d_chal);
     if (c->d_eq) (void)hipFree(c->d_eq);
+    if (c->d_acc) (void)hipFree(c->d_acc);
     if (c->d_params) (void)hipFree(c->d_params);
     if (c->ws) (void)hipFree(c->ws);
     if (c->h_stage) (void)hipHostFree(c->h_stage);
@@ -479,28 +498,37 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     // the sum-check chain (eq tables, bindings, rounds), then the product C,
     // all on the caller's stream
     hipStream_t z = s;
-    {
-        Timed tm(c, G_EQ, z);
-        launch_eq_tables(r1, ln, E1, r2, lk, E2, z);
-    }
-    ChunkSum cs{};
-    {
-        Timed tm(c, G_BIND_ROWS, z);
-        cs = launch_bind_rows_chunks(d_A, a_dtype, n, m, E1, scr, a, z);
-    }
-    {   // B bound on its columns; extra workgroups finish the row binding of A
-        Timed tm(c, G_BIND_COLS, z);
-        launch_bind_cols(d_B, RA_I16, m, k, E2, b, z, &cs);
+    // The fused front (one launch: limb split, both bindings, eq tables) where
+    // the shapes allow; else eq tables, row binding, column binding.
+    const bool fused = front_supported(a_dtype == RA_I32, n, m, k, d_A, d_B);
+    if (fused) {
+        if ((st = ensure_acc(c, m)) != RA_OK) return st;
+        Timed tm(c, G_FRONT, z);
+        launch_front(d_A, a_dtype == RA_I32, d_B, n, m, k, r1, ln, r2, lk, c->d_acc, b, E1, E2, c->ws + o_gemm, z);
+    } else {
+        {
+            Timed tm(c, G_EQ, z);
+            launch_eq_tables(r1, ln, E1, r2, lk, E2, z);
+        }
+        ChunkSum cs{};
+        {
+            Timed tm(c, G_BIND_ROWS, z);
+            cs = launch_bind_rows_chunks(d_A, a_dtype, n, m, E1, scr, a, z);
+        }
+        {   // B bound on its columns; extra workgroups finish the row binding of A
+            Timed tm(c, G_BIND_COLS, z);
+            launch_bind_cols(d_B, RA_I16, m, k, E2, b, z, &cs);
+        }
     }
     // transcript: [c0][evals 3 lm][a*][b*]; the instance's tail runs as extra
     // workgroups of the product launch
     TailArgs ta{};
     XJobs tjobs{};
     run_instance(c, z, KIND_MATMUL, a, b, nullptr, lm, rho, tr, 1, 3, tr + 1 + 3 * lm, 0, part, G_MM_ROUNDS,
-                 G_MM_TAIL, &ta, &tjobs);
+                 G_MM_TAIL, &ta, &tjobs, fused ? c->d_acc : nullptr);
     {
         Timed tm(c, G_GEMM);
-        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s, &ta, &tjobs);
+        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s, &ta, &tjobs, fused);
     }
     c->n = n;
     c->m = m;

@@ -80,8 +80,19 @@ struct TailArgs;
 struct XJobs;
 // ta, jobs (optional): the matrix instance's tail (launch_tail) as extra
 // workgroups of the product launch
+// split_done: the limb planes are already in ws (launch_front)
 void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
-                      void *ws, hipStream_t st, const TailArgs *ta = nullptr, const XJobs *jobs = nullptr);
+                      void *ws, hipStream_t st, const TailArgs *ta = nullptr, const XJobs *jobs = nullptr,
+                      bool split_done = false);
+// The fused front of the matrix call (one launch): the product's limb split
+// into ws, the row binding of A at r1 added into acc (2 m words: low 32 bits,
+// high bits; zero on entry), the column binding of B at r2 into b, and the
+// eq tables E1 (n words) and E2 (k words).  front_supported tells whether the
+// shapes and alignments allow it.
+bool front_supported(int a_is_i32, uint32_t n, uint32_t m, uint32_t k, const void *A, const void *B);
+void launch_front(const void *A, int a_is_i32, const int16_t *B, uint32_t n, uint32_t m, uint32_t k,
+                  const uint64_t *r1, int ln, const uint64_t *r2, int lk, uint64_t *acc, uint64_t *b, uint64_t *E1,
+                  uint64_t *E2, void *ws, hipStream_t st);
 // rows binding: out[c] = sum_r E[r] T[r, c]; needs scratch of bind_rows_chunks(rows, cols) * cols words
 int bind_rows_chunks(uint32_t rows, uint32_t cols);
 void launch_bind_rows(const void *T, int dtype, uint32_t rows, uint32_t cols, const uint64_t *E, uint64_t *scratch,
@@ -119,6 +130,7 @@ struct InstArgs {
     uint64_t *t0, *t1, *t2;
     const uint64_t *rho, *kp;
     uint64_t *part;
+    uint64_t *acc;  // optional: t0's values as accumulated by launch_front (read, turned into t0, cleared)
 };
 // The last v rounds (rounds j0 .. j0 + v - 1 of the instance): round j's
 // D + 1 evaluations go to tr[ev + (D + 1) j], with sum_out >= 0 and j0 == 0
@@ -130,12 +142,14 @@ struct TailArgs {
     uint64_t *tr;
     int ev, j0, sum_out;
     uint64_t *fin0, *fin1, *fin2;
+    uint64_t *acc;  // optional (j0 == 0 only): t0's values as accumulated by launch_front, read and cleared
 };
 int fused_rounds_max(int kind);
 // C fused rounds over tables of size S (C <= fused_rounds_max); partials of
 // round r at part + r * stride
+// acc (optional): t0's values accumulated by launch_front (read, cleared)
 void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t S, const uint64_t *rho,
-                   const uint64_t *kp, uint64_t *part, int stride, hipStream_t st);
+                   const uint64_t *kp, uint64_t *part, int stride, hipStream_t st, uint64_t *acc = nullptr);
 struct XJobs;
 // The tail workgroup, plus one workgroup per slot in jobs (SLOT_COPY slots of
 // the global rounds before it).

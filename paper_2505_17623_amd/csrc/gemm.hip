@@ -223,6 +223,219 @@ __global__ __launch_bounds__(256) void k_split(const TA *__restrict__ A, uint32_
     split_bt_block(B, m, k, mp, kp, Bt, colpart, t % tx, t / tx);
 }
 
+// ---------------------------------------------------------------------------
+// The front of the matrix call in one launch.  Every role reads only the
+// operands A, B and the challenge point (r1, r2), so they run side by side:
+//   - the limb split of A and B for the exact product (above);
+//   - the row binding a(l) = sum_i eq(r1, i) A[i, l] and the column binding
+//     b(l) = sum_j B[l, j] eq(r2, j) of Eq. (4);
+//   - the eq tables E1 = eq(r1, .), E2 = eq(r2, .) for the later calls.
+// The binding roles build eq values from two small factor tables in LDS:
+// with lb = v / 2 low variables, eq(z, i) = H[i >> lb] L[i mod 2^lb], where H
+// is the eq vector of the first v - lb coordinates of z and L that of the
+// last lb (Eq. (1) factors over the coordinates).
+// ---------------------------------------------------------------------------
+constexpr int kFrontMaxLog = 16;   // largest log n, log k of the fused front (factor tables <= 256 words)
+
+// H (2^(v - v/2) words) and L (2^(v/2) words) for the point z (v <= 16);
+// folded values.  The caller synchronises.
+__device__ __forceinline__ void eq_factors(const uint64_t *__restrict__ z, int v, uint64_t *H, uint64_t *L)
+{
+    const int lb = v / 2, hb = v - lb, nh = 1 << hb;
+    for (int i = threadIdx.x; i < nh + (1 << lb); i += blockDim.x) {
+        const bool high = i < nh;
+        const int idx = high ? i : i - nh, nv = high ? hb : lb, j0 = high ? 0 : hb;
+        uint64_t acc = 1;
+        for (int j = 0; j < nv; j++) {
+            const uint64_t zj = z[j0 + j];
+            acc = m61::lmul(acc, ((idx >> (nv - 1 - j)) & 1) ? zj : m61::lsub(1, zj));
+        }
+        (high ? H : L)[idx] = acc;
+    }
+}
+
+// Row binding of one chunk of rows for 64 columns.  A lane takes 16 bytes
+// (CPL entries) of a row per step; G lanes cover the 64 columns and RS row
+// slots interleave.  Each eq value e (< 2^62) is cut into NL limbs of LB bits,
+// so sum_i e_i z_i is accumulated exactly in int64 per limb (|limb z| < 2^46
+// for int16, < 2^52 for int32, at most 2^11 rows per lane), then reduced
+// mod p once.  The chunk's canonical sums are added to acc (low 32 bits at
+// acc[c], the rest at acc[m + c]), which the first reader of a turns into
+// field values and clears.
+template <typename T>
+__device__ __forceinline__ void front_rowbind(const T *__restrict__ A, uint32_t n, uint32_t m, const uint64_t *r1,
+                                              int ln, uint32_t rpc, uint32_t blk, uint64_t *acc, uint64_t *tab,
+                                              uint64_t *red)
+{
+    constexpr int CPL = 16 / (int)sizeof(T), G = 64 / CPL, RS = 256 / G;
+    constexpr int NL = sizeof(T) == 2 ? 2 : 3, LB = sizeof(T) == 2 ? 31 : 21;
+    constexpr uint64_t LMASK = (1ull << LB) - 1;
+    uint64_t *H = tab, *Lt = tab + 256;
+    eq_factors(r1, ln, H, Lt);
+    __syncthreads();
+    const uint32_t ncb = m / 64, cb = blk % ncb, ch = blk / ncb;
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const uint32_t c = cb * 64 + g * CPL, r0 = ch * rpc, re = r0 + rpc < n ? r0 + rpc : n;
+    const int lb = ln / 2;
+    const uint32_t lmask = (1u << lb) - 1;
+    int64_t s[CPL][NL];
+#pragma unroll
+    for (int q = 0; q < CPL; q++)
+#pragma unroll
+        for (int l = 0; l < NL; l++) s[q][l] = 0;
+    for (uint32_t rb = r0 + slot; rb < re; rb += 4 * RS) {
+        v4i z4[4];
+        uint64_t e[4];
+#pragma unroll
+        for (int u = 0; u < 4; u++) {  // loads first
+            const uint32_t r = rb + u * RS;
+            z4[u] = r < re ? *(const v4i *)&A[(size_t)r * m + c] : v4i{0, 0, 0, 0};
+            e[u] = r < re ? m61::lmul(H[r >> lb], Lt[r & lmask]) : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            int64_t el[NL];
+#pragma unroll
+            for (int l = 0; l < NL; l++) el[l] = (int64_t)(l == NL - 1 ? e[u] >> (LB * l) : (e[u] >> (LB * l)) & LMASK);
+#pragma unroll
+            for (int q = 0; q < CPL; q++) {
+                const int32_t z = sizeof(T) == 2 ? (int32_t)(int16_t)(z4[u][q >> 1] >> (16 * (q & 1))) : z4[u][q];
+#pragma unroll
+                for (int l = 0; l < NL; l++) s[q][l] += el[l] * z;
+            }
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < CPL; q++) {
+        uint64_t v = 0;
+#pragma unroll
+        for (int l = 0; l < NL; l++) v = m61::add(v, m61::rotl(m61::from_i64(s[q][l]), LB * l));
+        red[slot * 65 + g * CPL + q] = v;
+    }
+    __syncthreads();
+    if (tid < 64) {
+        uint64_t v = 0;
+#pragma unroll 4
+        for (int u = 0; u < RS; u++) v = m61::fold(v + red[u * 65 + tid]);
+        v = m61::canon(v);
+        atomicAdd((unsigned long long *)&acc[cb * 64 + tid], (unsigned long long)(v & 0xFFFFFFFFull));
+        atomicAdd((unsigned long long *)&acc[m + cb * 64 + tid], (unsigned long long)(v >> 32));
+    }
+}
+
+// Column binding of four rows per wave (16 per workgroup): lanes take 8
+// consecutive columns per step (one 16-byte load per row); eq(r2, c) =
+// e_hi 2^31 + e_lo is accumulated exactly per half in int64, one reduction
+// mod p per lane and row.
+constexpr int kFrontColRows = 16;
+
+__device__ __forceinline__ void front_colbind(const int16_t *__restrict__ B, uint32_t rows, uint32_t cols,
+                                              const uint64_t *r2, int lk, uint32_t blk, uint64_t *out, uint64_t *tab)
+{
+    constexpr int RW = 4;
+    uint64_t *H = tab, *Lt = tab + 256;
+    eq_factors(r2, lk, H, Lt);
+    __syncthreads();
+    const int lb = lk / 2;
+    const uint32_t lmask = (1u << lb) - 1;
+    const uint32_t r0 = blk * kFrontColRows + (threadIdx.x >> 6) * RW;  // wave-uniform
+    const int lane = threadIdx.x & 63;
+    if (r0 >= rows) return;
+    int64_t lo[RW], hi[RW];
+#pragma unroll
+    for (int rr = 0; rr < RW; rr++) lo[rr] = hi[rr] = 0;
+    for (uint32_t c0 = 8 * lane; c0 < cols; c0 += 512) {
+        v4i z4[RW];
+#pragma unroll
+        for (int rr = 0; rr < RW; rr++)
+            z4[rr] = r0 + rr < rows ? *(const v4i *)&B[(size_t)(r0 + rr) * cols + c0] : v4i{0, 0, 0, 0};
+        int32_t el[8], eh[8];
+#pragma unroll
+        for (int t = 0; t < 8; t++) {
+            const uint32_t cc = c0 + t;
+            const uint64_t e = m61::lmul(H[cc >> lb], Lt[cc & lmask]);  // < 2^61 + 8
+            el[t] = (int32_t)(e & 0x7FFFFFFFull);
+            eh[t] = (int32_t)(e >> 31);
+        }
+#pragma unroll
+        for (int rr = 0; rr < RW; rr++)
+#pragma unroll
+            for (int t = 0; t < 8; t++) {
+                const int32_t z = (int32_t)(int16_t)(z4[rr][t >> 1] >> (16 * (t & 1)));
+                lo[rr] += (int64_t)el[t] * z;
+                hi[rr] += (int64_t)eh[t] * z;
+            }
+    }
+#pragma unroll
+    for (int rr = 0; rr < RW; rr++) {
+        const uint64_t v = m61::wave_sum(m61::add(m61::from_i64(lo[rr]), m61::rotl(m61::from_i64(hi[rr]), 31)));
+        if (lane == 0 && r0 + rr < rows) out[r0 + rr] = v;
+    }
+}
+
+// 1024 entries of eq(z, .) (v <= 16 variables), canonical.
+__device__ __forceinline__ void front_eq(const uint64_t *z, int v, uint64_t *out, uint32_t blk, uint64_t *tab)
+{
+    uint64_t *H = tab, *Lt = tab + 256;
+    eq_factors(z, v, H, Lt);
+    __syncthreads();
+    const int lb = v / 2;
+    const uint32_t lmask = (1u << lb) - 1, nv = 1u << v;
+#pragma unroll
+    for (int u = 0; u < 4; u++) {
+        const uint32_t i = blk * 1024 + u * 256 + threadIdx.x;
+        if (i < nv) out[i] = m61::canon(m61::lmul(H[i >> lb], Lt[i & lmask]));
+    }
+}
+
+struct FrontArgs {
+    const void *A;
+    const int16_t *B;
+    uint32_t n, m, k, np, mp, kp;
+    int8_t *Al;
+    int64_t *rowsum;
+    int8_t *Bt;
+    int64_t *colpart;
+    const uint64_t *r1, *r2;
+    int ln, lk;
+    uint64_t *acc;       // row binding accumulators (2 m words, zero on entry)
+    uint64_t *b;         // column binding (m words)
+    uint64_t *E1, *E2;   // eq tables for the later calls
+    uint32_t rpc;        // rows per row-binding chunk
+    uint32_t n_rb, n_cb, n_sb, n_sa, n_e1;  // workgroups per role, in launch order (then E2)
+};
+
+template <typename TA, int LA>
+__global__ __launch_bounds__(256) void k_front(FrontArgs f)
+{
+    __shared__ uint64_t tab[512];
+    __shared__ uint64_t red[(256 / (64 / (16 / (int)sizeof(TA)))) * 65];
+    uint32_t b = blockIdx.x;
+    if (b < f.n_rb) {
+        front_rowbind<TA>((const TA *)f.A, f.n, f.m, f.r1, f.ln, f.rpc, b, f.acc, tab, red);
+        return;
+    }
+    b -= f.n_rb;
+    if (b < f.n_cb) {
+        front_colbind(f.B, f.m, f.k, f.r2, f.lk, b, f.b, tab);
+        return;
+    }
+    b -= f.n_cb;
+    if (b < f.n_sb) {
+        const uint32_t tx = f.kp / 64;
+        split_bt_block(f.B, f.m, f.k, f.mp, f.kp, f.Bt, f.colpart, b % tx, b / tx);
+        return;
+    }
+    b -= f.n_sb;
+    if (b < f.n_sa) {
+        split_a_block<TA, LA>((const TA *)f.A, f.n, f.m, f.np, f.mp, f.Al, f.rowsum, b);
+        return;
+    }
+    b -= f.n_sa;
+    if (b < f.n_e1) front_eq(f.r1, f.ln, f.E1, b, tab);
+    else front_eq(f.r2, f.lk, f.E2, b - f.n_e1, tab);
+}
+
 // 64 x 64 output tile per block; wave (wr, wc) owns the 32 x 32 sub-tile.
 // The k dimension goes in steps of 64 bytes through S LDS stages: every step
 // needs F = 2 (2 LA + 4) fragments (two 32-byte halves of A: LA limbs x 2
@@ -373,26 +586,89 @@ size_t gemm_workspace_bytes(int a_is_i32, uint32_t n, uint32_t m, uint32_t k)
     return LA * np * mp + 2 * kp * mp + 8 * (size_t)n + 8 * (mp / 64) * kp + 3 * 256;
 }
 
+struct GemmWs {
+    int8_t *Al, *Bt;
+    int64_t *rowsum, *colpart;
+};
+
+static GemmWs gemm_ws(void *ws, int LA, uint32_t n, uint32_t np, uint32_t mp, uint32_t kp)
+{
+    char *p = (char *)ws;
+    GemmWs w;
+    w.Al = (int8_t *)p;
+    p += ((size_t)LA * np * mp + 255) & ~(size_t)255;
+    w.Bt = (int8_t *)p;
+    p += ((size_t)2 * kp * mp + 255) & ~(size_t)255;
+    w.rowsum = (int64_t *)p;
+    p += ((size_t)8 * n + 255) & ~(size_t)255;
+    w.colpart = (int64_t *)p;
+    return w;
+}
+
+bool front_supported(int a_is_i32, uint32_t n, uint32_t m, uint32_t k, const void *A, const void *B)
+{
+    (void)a_is_i32;
+    auto lg = [](uint32_t x) { int l = 0; while ((1u << l) < x) l++; return l; };
+    return lg(n) <= kFrontMaxLog && lg(k) <= kFrontMaxLog && m >= 64 && k >= 8 && ((uintptr_t)A & 15) == 0 &&
+           ((uintptr_t)B & 15) == 0;
+}
+
+void launch_front(const void *A, int a_is_i32, const int16_t *B, uint32_t n, uint32_t m, uint32_t k,
+                  const uint64_t *r1, int ln, const uint64_t *r2, int lk, uint64_t *acc, uint64_t *b, uint64_t *E1,
+                  uint64_t *E2, void *ws, hipStream_t st)
+{
+    const uint32_t np = round_up64(n), mp = round_up64(m), kp = round_up64(k);
+    const int LA = a_is_i32 ? 4 : 2;
+    const GemmWs w = gemm_ws(ws, LA, n, np, mp, kp);
+    FrontArgs f{};
+    f.A = A;
+    f.B = B;
+    f.n = n;
+    f.m = m;
+    f.k = k;
+    f.np = np;
+    f.mp = mp;
+    f.kp = kp;
+    f.Al = w.Al;
+    f.rowsum = w.rowsum;
+    f.Bt = w.Bt;
+    f.colpart = w.colpart;
+    f.r1 = r1;
+    f.r2 = r2;
+    f.ln = ln;
+    f.lk = lk;
+    f.acc = acc;
+    f.b = b;
+    f.E1 = E1;
+    f.E2 = E2;
+    // about eight rows per lane and chunk: 256 rows (int16) or 128 (int32)
+    f.rpc = a_is_i32 ? 128 : 256;
+    f.n_rb = (m / 64) * ((n + f.rpc - 1) / f.rpc);
+    f.n_cb = (m + kFrontColRows - 1) / kFrontColRows;
+    f.n_sb = (kp / 64) * (mp / 64);
+    f.n_sa = (np + 3) / 4;
+    f.n_e1 = (n + 1023) / 1024;
+    const uint32_t n_e2 = (k + 1023) / 1024;
+    const dim3 grid(f.n_rb + f.n_cb + f.n_sb + f.n_sa + f.n_e1 + n_e2);
+    if (a_is_i32) hipLaunchKernelGGL((k_front<int32_t, 4>), grid, dim3(256), 0, st, f);
+    else hipLaunchKernelGGL((k_front<int16_t, 2>), grid, dim3(256), 0, st, f);
+}
+
 void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
-                      void *ws, hipStream_t st, const TailArgs *ta, const XJobs *jobs)
+                      void *ws, hipStream_t st, const TailArgs *ta, const XJobs *jobs, bool split_done)
 {
     const uint32_t np = round_up64(n), mp = round_up64(m), kp = round_up64(k);
     const int LA = a_is_i32 ? 4 : 2, ntiles = (int)(mp / 64);
-    char *p = (char *)ws;
-    int8_t *Al = (int8_t *)p;
-    p += ((size_t)LA * np * mp + 255) & ~(size_t)255;
-    int8_t *Bt = (int8_t *)p;
-    p += ((size_t)2 * kp * mp + 255) & ~(size_t)255;
-    int64_t *rowsum = (int64_t *)p;
-    p += ((size_t)8 * n + 255) & ~(size_t)255;
-    int64_t *colpart = (int64_t *)p;
+    const GemmWs w = gemm_ws(ws, LA, n, np, mp, kp);
     const uint32_t na = (np + 3) / 4, nb = (kp / 64) * (mp / 64);
-    if (a_is_i32)
-        hipLaunchKernelGGL((k_split<int32_t, 4>), dim3(na + nb), dim3(256), 0, st, (const int32_t *)A, n, m, np, mp, Al,
-                           rowsum, na, B, k, kp, Bt, colpart);
-    else
-        hipLaunchKernelGGL((k_split<int16_t, 2>), dim3(na + nb), dim3(256), 0, st, (const int16_t *)A, n, m, np, mp, Al,
-                           rowsum, na, B, k, kp, Bt, colpart);
+    if (!split_done) {
+        if (a_is_i32)
+            hipLaunchKernelGGL((k_split<int32_t, 4>), dim3(na + nb), dim3(256), 0, st, (const int32_t *)A, n, m, np,
+                               mp, w.Al, w.rowsum, na, B, k, kp, w.Bt, w.colpart);
+        else
+            hipLaunchKernelGGL((k_split<int16_t, 2>), dim3(na + nb), dim3(256), 0, st, (const int16_t *)A, n, m, np,
+                               mp, w.Al, w.rowsum, na, B, k, kp, w.Bt, w.colpart);
+    }
     // tail workgroups (and the slot assemblies they bring) after the tiles
     const TailArgs tnone{};
     XJobs jnone{};
@@ -401,13 +677,13 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
     const TailArgs &tav = ta ? *ta : tnone;
     const XJobs &jv = ta ? *jobs : jnone;
     if (a_is_i32)
-        hipLaunchKernelGGL((k_gemm_mfma<4, gemm_stages<4>()>), grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
-                           (const int64_t *)rowsum, (const int64_t *)colpart, ntiles, (int64_t)8421504, n, m, k, np,
-                           mp, kp, C, tav, jv);
+        hipLaunchKernelGGL((k_gemm_mfma<4, gemm_stages<4>()>), grid, dim3(256), 0, st, (const int8_t *)w.Al,
+                           (const int8_t *)w.Bt, (const int64_t *)w.rowsum, (const int64_t *)w.colpart, ntiles,
+                           (int64_t)8421504, n, m, k, np, mp, kp, C, tav, jv);
     else
-        hipLaunchKernelGGL((k_gemm_mfma<2, gemm_stages<2>()>), grid, dim3(256), 0, st, (const int8_t *)Al, (const int8_t *)Bt,
-                           (const int64_t *)rowsum, (const int64_t *)colpart, ntiles, (int64_t)128, n, m, k, np, mp,
-                           kp, C, tav, jv);
+        hipLaunchKernelGGL((k_gemm_mfma<2, gemm_stages<2>()>), grid, dim3(256), 0, st, (const int8_t *)w.Al,
+                           (const int8_t *)w.Bt, (const int64_t *)w.rowsum, (const int64_t *)w.colpart, ntiles,
+                           (int64_t)128, n, m, k, np, mp, kp, C, tav, jv);
 }
 
 }  // namespace ra

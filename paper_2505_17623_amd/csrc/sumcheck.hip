@@ -45,7 +45,8 @@ __device__ __forceinline__ void rounds_body(const InstArgs &in, uint64_t sub, in
 #pragma unroll
         for (int q = 0; q < NT; q++)
 #pragma unroll
-            for (int t = 0; t < L; t++) v[q][t] = T[q][i + t * sub];
+            for (int t = 0; t < L; t++)
+                v[q][t] = (q == 0 && in.acc) ? take_acc(in.acc, i + t * sub, sub << C) : T[q][i + t * sub];
 #pragma unroll
         for (int c = 0; c < C; c++) {
             const int h = L >> (c + 1);
@@ -104,11 +105,11 @@ int round_blocks(uint64_t h)
 int fused_rounds_max(int) { return 2; }
 
 void launch_rounds(int kind, int C, uint64_t *t0, uint64_t *t1, uint64_t *t2, uint64_t S, const uint64_t *rho,
-                   const uint64_t *kp, uint64_t *part, int stride, hipStream_t st)
+                   const uint64_t *kp, uint64_t *part, int stride, hipStream_t st, uint64_t *acc)
 {
     const uint64_t sub = S >> C;
     const int nb = round_blocks(sub);
-    const InstArgs a{t0, t1, t2, rho, kp, part};
+    const InstArgs a{t0, t1, t2, rho, kp, part, acc};
 #define RA_ROUNDS(K, CC) hipLaunchKernelGGL((k_rounds<K, CC>), dim3(nb), dim3(kThreads), 0, st, a, sub, stride)
 #define RA_ROUNDS_K(K)               \
     switch (C) {                     \

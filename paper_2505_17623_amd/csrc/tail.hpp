@@ -25,6 +25,18 @@ __device__ __forceinline__ void pair_contrib(const uint64_t (&lo)[3], const uint
     acc[2] += m61::lmul(a2, b2);
 }
 
+// Entry i of a row binding accumulated by the front launch over a table of
+// S entries: acc[i] holds the sum of the chunks' low 32 bits, acc[S + i] the
+// sum of their high bits, so the value is acc[i] + 2^32 acc[S + i] mod p.
+// The pair is cleared for the next call.  Canonical result.
+__device__ __forceinline__ uint64_t take_acc(uint64_t *acc, uint64_t i, uint64_t S)
+{
+    const uint64_t lo = acc[i], hi = acc[S + i];
+    acc[i] = 0;
+    acc[S + i] = 0;
+    return m61::add(m61::canon(lo), m61::rotl(m61::canon(hi), 32));
+}
+
 // lo + r (hi - lo), folded.
 __device__ __forceinline__ uint64_t fold_to(uint64_t lo, uint64_t hi, uint64_t r)
 {
@@ -61,7 +73,7 @@ __device__ __forceinline__ void tail_block(const TailArgs &in, const XJobs &jobs
 #pragma unroll
         for (int q = 0; q < 4; q++) {
             const int i = i0 + q * NI;
-            x[q] = i < S ? in.t0[i] : 0;
+            x[q] = i < S ? (in.acc ? take_acc(in.acc, i, S) : in.t0[i]) : 0;
             y[q] = i < S ? in.t1[i] : 0;
         }
 #pragma unroll

@@ -97,6 +97,9 @@ SHAPES = [
     (1, 4, 16384, 5, False, 1, 3000),   # N beyond the range instance's LDS tail
     (128, 64, 128, 11, True, 0, 3000),  # N beyond the ReLU instance's LDS tail, several GEMM tiles
     (32, 32, 64, 6, True, 1, 3000),
+    (1, 64, 8, 7, True, 0, 3000),       # fused front: one row, the narrowest B it takes
+    (2048, 64, 8, 10, True, 0, 3000),   # fused front: eight row chunks of A accumulated
+    (64, 2048, 16, 10, False, 1, 3000), # fused front feeding a global round (m beyond the LDS tail)
 ]
 
 

@@ -347,6 +347,41 @@ __global__ __launch_bounds__(256) void k_wit_params(const int64_t *__restrict__ 
 // With t given (known != 0) the parameters come by value and every workgroup
 // also flags, in flags[block], whether one of its R lies outside the range;
 // the final kernel turns the flags into the status.
+// Claims of V outputs (consecutive x): sum_i e_i z_i for e_i = E1[row] E2[col]
+// (folded, < 2^61 + 8) and integers |z_i| <= 2^30 (R, Y, Z fit t <= 29; a
+// value outside the given range makes the call fail, its claims unused).
+// Each e_i is cut as e_hi 2^31 + e_lo, the two sums are exact in int64 (four
+// terms below 2^61 each), then reduced mod p once.
+template <int V>
+__device__ __forceinline__ uint64_t claim_terms(const uint64_t (&el)[V], const uint64_t (&eh)[V],
+                                                const int32_t (&z)[V])
+{
+    uint64_t lo = 0, hi = 0;  // two's complement sums (exact for |z| <= 2^30)
+#pragma unroll
+    for (int i = 0; i < V; i++) {
+        lo += (uint64_t)((int64_t)el[i] * z[i]);
+        hi += (uint64_t)((int64_t)eh[i] * z[i]);
+    }
+    return m61::fold(m61::from_i64((int64_t)lo) + m61::rotl(m61::from_i64((int64_t)hi), 31));
+}
+
+// Blocks of the rescale pass: V = 4 outputs per thread, one pass over N for
+// up to kMaxBlocks blocks (never more blocks than witness_blocks(N)).
+static int rescale_blocks(uint64_t N)
+{
+    const uint64_t b = (N + 4 * kThreads - 1) / (4 * kThreads);
+    return (int)(b < (uint64_t)kMaxBlocks ? b : (uint64_t)kMaxBlocks);
+}
+
+// Pass 2: R, Rm, Y, Z, the bit word and per-block claims, then one block
+// sums the claims (R~, Rm~, Y~, Z~ at (r1, r2)) and mirrors the parameters and
+// claims to `mirror` (12 words) when it is given.
+// With t given (known != 0) the parameters come by value and every workgroup
+// also flags, in flags[block], whether one of its R lies outside the range;
+// the final kernel turns the flags into the status.
+// A thread takes V consecutive outputs per step (V = 4: 16-byte loads and
+// stores; V = 1 for N < 4 or unaligned buffers).
+template <int V>
 __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, uint64_t N, int lk,
                                                  const WitParams *__restrict__ prm, const uint64_t *__restrict__ E1,
                                                  const uint64_t *__restrict__ E2, int32_t *__restrict__ R,
@@ -355,6 +390,9 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
                                                  uint64_t *__restrict__ claim_part, WitParams hp, int known,
                                                  uint32_t *__restrict__ flags)
 {
+    typedef long long v2l __attribute__((ext_vector_type(2)));
+    typedef int v4i_t __attribute__((ext_vector_type(4)));
+    typedef unsigned short v4u16 __attribute__((ext_vector_type(4)));
     __shared__ uint64_t red[m61::block_sum_words(4, 256)];
     const WitParams p = known ? hp : *prm;
     if (p.status != 0) return;  // uniform over the grid
@@ -364,27 +402,61 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
     const uint64_t kmask = (1ull << lk) - 1;
     uint64_t acc[4] = {0, 0, 0, 0};
     int out_of_range = 0;
-    for (uint64_t x = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; x < N; x += (uint64_t)gridDim.x * blockDim.x) {
-        const int64_t c = C[x] + half;
-        const int64_t q = c >> s;
-        // u = R for R >= 0, -R - 1 for R < 0; R in [-2^(t+1), 2^(t+1)) iff u < 2^(t+1)
-        out_of_range |= ((uint64_t)(q >= 0 ? q : -(q + 1)) >> (t + 1)) != 0;
-        const int32_t rm = (int32_t)(c - (q << s));
-        const int32_t r = (int32_t)q;
-        const int32_t y = r < 0 ? -r : r;
-        const int32_t z = relu ? (r > 0 ? r : 0) : r;
-        R[x] = r;
-        Rm[x] = (uint16_t)rm;
-        Y[x] = y;
-        Z[x] = z;
-        uint64_t w = (uint64_t)rm | ((uint64_t)(q + shift_r) << s);
-        if (relu) w |= (uint64_t)y << (s + t + 2);
-        bits[x] = w;
-        const uint64_t e = m61::mul(E1[x >> lk], E2[x & kmask]);
-        acc[0] = m61::add(acc[0], m61::mul_small(e, r));
-        acc[1] = m61::add(acc[1], m61::mul_small(e, rm));
-        acc[2] = m61::add(acc[2], m61::mul_small(e, y));
-        acc[3] = m61::add(acc[3], m61::mul_small(e, z));
+    const uint64_t ng = N / V;
+    for (uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; g < ng; g += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t x0 = g * V;
+        int64_t c[V];
+        uint64_t el[V], eh[V];
+        if constexpr (V == 4) {
+            const v2l c01 = *(const v2l *)&C[x0], c23 = *(const v2l *)&C[x0 + 2];
+            c[0] = c01[0];
+            c[1] = c01[1];
+            c[2] = c23[0];
+            c[3] = c23[1];
+        } else {
+            c[0] = C[x0];
+        }
+#pragma unroll
+        for (int i = 0; i < V; i++) {
+            const uint64_t x = x0 + i;
+            const uint64_t e = m61::lmul(E1[x >> lk], E2[x & kmask]);
+            el[i] = e & 0x7FFFFFFFull;
+            eh[i] = e >> 31;
+        }
+        int32_t r[V], rm[V], y[V], z[V];
+        uint64_t w[V];
+#pragma unroll
+        for (int i = 0; i < V; i++) {
+            const int64_t cc = c[i] + half;
+            const int64_t q = cc >> s;
+            // u = R for R >= 0, -R - 1 for R < 0; R in [-2^(t+1), 2^(t+1)) iff u < 2^(t+1)
+            out_of_range |= ((uint64_t)(q >= 0 ? q : -(q + 1)) >> (t + 1)) != 0;
+            rm[i] = (int32_t)(cc - (q << s));
+            r[i] = (int32_t)q;
+            y[i] = r[i] < 0 ? -r[i] : r[i];
+            z[i] = relu ? (r[i] > 0 ? r[i] : 0) : r[i];
+            w[i] = (uint64_t)rm[i] | ((uint64_t)(q + shift_r) << s);
+            if (relu) w[i] |= (uint64_t)y[i] << (s + t + 2);
+        }
+        if constexpr (V == 4) {
+            *(v4i_t *)&R[x0] = v4i_t{r[0], r[1], r[2], r[3]};
+            *(v4i_t *)&Y[x0] = v4i_t{y[0], y[1], y[2], y[3]};
+            *(v4i_t *)&Z[x0] = v4i_t{z[0], z[1], z[2], z[3]};
+            *(v4u16 *)&Rm[x0] = v4u16{(unsigned short)rm[0], (unsigned short)rm[1], (unsigned short)rm[2],
+                                      (unsigned short)rm[3]};
+            *(v2l *)&bits[x0] = v2l{(long long)w[0], (long long)w[1]};
+            *(v2l *)&bits[x0 + 2] = v2l{(long long)w[2], (long long)w[3]};
+        } else {
+            R[x0] = r[0];
+            Y[x0] = y[0];
+            Z[x0] = z[0];
+            Rm[x0] = (uint16_t)rm[0];
+            bits[x0] = w[0];
+        }
+        acc[0] = m61::fold(acc[0] + claim_terms<V>(el, eh, r));
+        acc[1] = m61::fold(acc[1] + claim_terms<V>(el, eh, rm));
+        acc[2] = m61::fold(acc[2] + claim_terms<V>(el, eh, y));
+        acc[3] = m61::fold(acc[3] + claim_terms<V>(el, eh, z));
     }
     if (known) {
         const int any = __syncthreads_or(out_of_range);
@@ -440,10 +512,16 @@ void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t
                             WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st,
                             const WitParams *known, uint32_t *flags)
 {
-    const int nb = witness_blocks(N);
     const WitParams hp = known ? *known : WitParams{};
-    hipLaunchKernelGGL(k_rescale, dim3(nb), dim3(kThreads), 0, st, C, N, lk, (const WitParams *)params, E1, E2, R, Rm,
-                       Y, Z, bits, claim_part, hp, known ? 1 : 0, flags);
+    const bool vec = N >= 4 && (((uintptr_t)C | (uintptr_t)R | (uintptr_t)Y | (uintptr_t)Z | (uintptr_t)bits) & 15) == 0 &&
+                     ((uintptr_t)Rm & 7) == 0;
+    const int nb = vec ? rescale_blocks(N) : witness_blocks(N);
+    if (vec)
+        hipLaunchKernelGGL(k_rescale<4>, dim3(nb), dim3(kThreads), 0, st, C, N, lk, (const WitParams *)params, E1, E2,
+                           R, Rm, Y, Z, bits, claim_part, hp, known ? 1 : 0, flags);
+    else
+        hipLaunchKernelGGL(k_rescale<1>, dim3(nb), dim3(kThreads), 0, st, C, N, lk, (const WitParams *)params, E1, E2,
+                           R, Rm, Y, Z, bits, claim_part, hp, known ? 1 : 0, flags);
     hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, (const uint64_t *)claim_part, nb, params,
                        claims_out, mirror, hp, known ? 1 : 0, (const uint32_t *)flags);
 }

@@ -190,43 +190,46 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
                 const int buf = (int)((i - 1) & 1);
                 const int8_t *mrow = s_u + buf * kPlaneBytes + (lane & 31) * kRow + 16 * half;
                 const int8_t *drow = &s_d[buf][cw][16 * half];
-                v4i nm[NPT], nd[DW];
+                // The plane bytes are 0x00 / 0xFF, i.e. -bit as int8: they are the
+                // A operand as they stand (the tiles accumulate -G_t, negated in
+                // the recombination), and masked with the digits they give B.
+                // Two register sets alternate over the K-steps, so the reads of
+                // step ks + 1 are in flight during the products of step ks.
+                v4i m0[NPT], d0[DW], m1[NPT], d1[DW];
+                auto load = [&](v4i (&m)[NPT], v4i (&d)[DW], int ks) {
 #pragma unroll
-                for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow);
+                    for (int pt = 0; pt < NPT; pt++) m[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * ks);
 #pragma unroll
-                for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab);
-                for (int ks = 0; ks < kSlab / 32; ks++) {
-                    v4i mask[NPT], frag[NPT], D[DW];
-#pragma unroll
-                    for (int pt = 0; pt < NPT; pt++) mask[pt] = nm[pt];
-#pragma unroll
-                    for (int k = 0; k < DW; k++) D[k] = nd[k];
-                    const int kn = ks + 1 < kSlab / 32 ? ks + 1 : ks;  // the last step re-reads (unused)
-#pragma unroll
-                    for (int pt = 0; pt < NPT; pt++) nm[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * kn);
-#pragma unroll
-                    for (int k = 0; k < DW; k++) nd[k] = *(const v4i *)(drow + 4 * k * kSlab + 32 * kn);
-                    __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of this step's products
-#pragma unroll
-                    for (int pt = 0; pt < NPT; pt++) frag[pt] = mask[pt] & (int)0x01010101;
+                    for (int k = 0; k < DW; k++) d[k] = *(const v4i *)(drow + kConsumers * k * kSlab + 32 * ks);
+                };
+                auto step = [&](const v4i (&m)[NPT], const v4i (&d)[DW]) {
 #pragma unroll
                     for (int k = 0; k < DW; k++) {
-                        const v4i B0 = mask[0] & D[k];
-                        acc[k][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B0, acc[k][0], 0, 0, 0);
+                        const v4i B0 = m[0] & d[k];
+                        acc[k][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(m[0], B0, acc[k][0], 0, 0, 0);
                         if (TP > 1) {
-                            const v4i B1 = mask[NPT - 1] & D[k];
+                            const v4i B1 = m[NPT - 1] & d[k];
                             acc[k][1 % TP] =
-                                __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[0], B1, acc[k][1 % TP], 0, 0, 0);
+                                __builtin_amdgcn_mfma_i32_32x32x32_i8(m[0], B1, acc[k][1 % TP], 0, 0, 0);
                             acc[k][2 % TP] =
-                                __builtin_amdgcn_mfma_i32_32x32x32_i8(frag[NPT - 1], B1, acc[k][2 % TP], 0, 0, 0);
+                                __builtin_amdgcn_mfma_i32_32x32x32_i8(m[NPT - 1], B1, acc[k][2 % TP], 0, 0, 0);
                         }
                     }
+                };
+                static_assert((kSlab / 32) % 2 == 0, "K-steps come in pairs");
+                load(m0, d0, 0);
+                for (int ks = 0; ks < kSlab / 32; ks += 2) {
+                    load(m1, d1, ks + 1);
+                    step(m0, d0);
+                    if (ks + 2 < kSlab / 32) load(m0, d0, ks + 2);
+                    step(m1, d1);
                 }
             }
             __syncthreads();
         }
         // recombine the digits modulo p into the block's tiles: digit t weighs
-        // 2^(8t), a rotation of the 61-bit residue; one LDS atomic per entry
+        // 2^(8t), a rotation of the 61-bit residue (of -acc: the A operand
+        // held -bit); one LDS atomic per entry
         // and consumer wave (8 waves x values below 2^61 < 2^64)
         for (int i = tid - 64 * kProducers; i < TP * 1024; i += 64 * kConsumers) (&s_g[0][0])[i] = 0;
         __syncthreads();
@@ -235,7 +238,7 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
 #pragma unroll
             for (int r = 0; r < 16; r++)
                 atomicAdd(&s_g[tp][r * 64 + lane],
-                          (unsigned long long)m61::rotl(m61::from_i32(acc[0][tp][r]), 8 * cw));
+                          (unsigned long long)m61::rotl(m61::from_i32(-acc[0][tp][r]), 8 * cw));
         __syncthreads();
     }
     for (int i = tid; i < TP * 1024; i += kGramThreads)

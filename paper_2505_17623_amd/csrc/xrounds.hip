@@ -299,171 +299,166 @@ void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, in
 }
 
 // ---------------------------------------------------------------------------
-// B rounds per workgroup with the sub-cube in LDS.  Workgroup k loads the
-// 2^B entries k + t 2^(lS - B) of each table (threads 0-127 the range table,
-// 128-255 the ReLU tables D and S; all 256 the range table without ReLU).
-// Round c pairs u and u + h (h = 2^(B-1-c)) with weight
+// B rounds per sub-cube, one wave per sub-cube and instance.  Sub-cube k
+// holds the 2^B entries k + u 2^(lS - B) (u < 2^B) of each table; entry u
+// lives in lane u mod 64, slot u / 64 of the wave.  Round c pairs u and
+// u + h (h = 2^(B-1-c)) with weight
 //   eq(r_{j+c+1 .. j+B-1}, u) eq(r_{j+B ..}, k) = W[h + u] e_k,
 // W the heap of suffix eq tables of the window r_{j+1 .. j+B-1} (set-up: the
-// WS heap, or for the last pass the LS heap), e_k from the suffix heaps.  Each thread keeps its sums of a
-// round in LDS; at the end the workgroup reduces them per round and either
-// writes one partial per round (several sub-cubes) or, for the single
-// sub-cube of the last pass, the round polynomials themselves.
+// WS heap, or for the last pass the LS heap), e_k from the suffix heaps.
+// While h >= 64 both entries of a pair sit in the same lane, so those rounds
+// run in registers; the later ones take the partner from lane u + h by a
+// cross-lane read.  No workgroup barrier is needed after the weights are
+// staged.  The sums of a round are formed with the weights W alone and
+// multiplied by e_k once, after the wave's lanes are summed (through a
+// wave-private LDS area).  A pass over several sub-cubes writes one partial
+// per round and sub-cube; the last pass (one sub-cube) writes the round
+// polynomials and the final values.
+// Workgroups take two sub-cubes with ReLU (waves 2i, 2i + 1: the range and
+// the ReLU instance of sub-cube 2 blk + i), else four (one wave each).
 // ---------------------------------------------------------------------------
 constexpr int kXbMax = 1 << kXBlockMax;
-// Thread-rounds (sum over the rounds of min(h, threads per instance)) for
-// B <= 10: range 256 + 256 + 255 without ReLU, 128 + 128 + 128 + 127 with it.
-constexpr int kXbRoundsR = 767, kXbRoundsZ = 511;
-// LDS layout (words): Tb, Td, Ts, W (kXbMax each), challenges (3 x 16), the
-// per-thread round sums (range 5, ReLU 3 words), the reduced sums (8 per round).
-constexpr int kXbLdsWords = 4 * kXbMax + 48 + 5 * kXbRoundsR + 3 * kXbRoundsZ + 8 * kXBlockMax;
+constexpr int kXbRedStride = 65;                                   // LDS words per summed value (64 lanes + pad)
+constexpr int kXbRedWords = 5 * kXBlockMax * kXbRedStride + 8 * kXBlockMax;  // per wave
+constexpr int kXbLdsWords = kXbMax + 4 * kXbRedWords;
 static_assert(kXbLdsWords >= kJobLdsWords, "jobs share the workgroup's LDS");
 
-template <bool RELU>
-__global__ __launch_bounds__(256) void k_xblock(XBlockArgs a, int first, XJobs jobs, int nmain)
+// Value of lane (lane + h) of the wave (h < 64; lanes past the end read
+// their own value, unused).
+__device__ __forceinline__ uint64_t lane_down(uint64_t v, int h) { return __shfl_down(v, (unsigned)h, 64); }
+
+template <int B, bool ZW, bool RELU>
+__device__ __forceinline__ void xb_wave(const XBlockArgs &a, bool first, uint64_t k, uint64_t nsub,
+                                        const uint64_t *__restrict__ W, uint64_t *red)
 {
-    __shared__ uint64_t smem[kXbLdsWords];
-    if ((int)blockIdx.x >= nmain) {
-        x_job(jobs, blockIdx.x - nmain, smem);
-        return;
-    }
-    uint64_t *Tb = smem, *Td = Tb + kXbMax, *Ts = Td + kXbMax, *W = Ts + kXbMax;
-    uint64_t *rw = W + kXbMax, *za = rw + 16, *zz = za + 16;
-    uint64_t *pr = zz + 16, *pz = pr + 5 * kXbRoundsR, *red = pz + 3 * kXbRoundsZ;
-    constexpr int NI = RELU ? 128 : 256;  // threads per instance
-    const int tid = threadIdx.x, B = a.B, S = 1 << B;
-    const bool zw = RELU && tid >= NI;  // wave-uniform
-    const int lt = zw ? tid - NI : tid;
-    const uint64_t k = blockIdx.x, nsub = 1ull << (a.lS - B);
-    // the binding challenges of the B rounds
-    if (tid >= 64 && tid < 64 + B) za[tid - 64] = a.rho_a[tid - 64];
-    if (RELU && tid >= 128 && tid < 128 + B) zz[tid - 128] = a.rho_z[tid - 128];
-    // the sub-cube: at most kXbMax / NI entries per thread, all loads issued first
-    constexpr int NQ = kXbMax / NI;
-    if (!zw) {
-        uint64_t v[NQ];
+    constexpr int S = 1 << B, NV = ZW ? 3 : 5, E = S >= 64 ? S / 64 : 1, NR = B > 0 ? B : 1;
+    const int lane = threadIdx.x & 63;
+    const uint64_t *rho = ZW ? a.rho_z : a.rho_a;
+    // the sub-cube: range t0 = Bx; ReLU t0 = D, t1 = S.  All loads issued first.
+    uint64_t t0[E], t1[E];
+    if (!ZW) {
 #pragma unroll
-        for (int q = 0; q < NQ; q++) {
-            const int t = lt + q * NI;
-            v[q] = t < S ? a.bx[k + (uint64_t)t * nsub] : 0;
+        for (int e = 0; e < E; e++) {
+            const int u = e * 64 + lane;
+            t0[e] = u < S ? a.bx[k + (uint64_t)u * nsub] : 0;
+            t1[e] = 0;
         }
-#pragma unroll
-        for (int q = 0; q < NQ; q++)
-            if (lt + q * NI < S) Tb[lt + q * NI] = v[q];
     } else if (first) {
-        int32_t vr[NQ], vy[NQ];
+        int32_t vr[E], vy[E];
 #pragma unroll
-        for (int q = 0; q < NQ; q++) {
-            const int t = lt + q * NI;
-            vr[q] = t < S ? a.R[k + (uint64_t)t * nsub] : 0;
-            vy[q] = t < S ? a.Y[k + (uint64_t)t * nsub] : 0;
+        for (int e = 0; e < E; e++) {
+            const int u = e * 64 + lane;
+            vr[e] = u < S ? a.R[k + (uint64_t)u * nsub] : 0;
+            vy[e] = u < S ? a.Y[k + (uint64_t)u * nsub] : 0;
         }
 #pragma unroll
-        for (int q = 0; q < NQ; q++)
-            if (lt + q * NI < S) {
-                Td[lt + q * NI] = small_to_field((int64_t)vr[q] - vy[q]);
-                Ts[lt + q * NI] = small_to_field((int64_t)vr[q] + vy[q]);
-            }
+        for (int e = 0; e < E; e++) {
+            t0[e] = small_to_field((int64_t)vr[e] - vy[e]);
+            t1[e] = small_to_field((int64_t)vr[e] + vy[e]);
+        }
     } else {
-        uint64_t vd[NQ], vs[NQ];
 #pragma unroll
-        for (int q = 0; q < NQ; q++) {
-            const int t = lt + q * NI;
-            vd[q] = t < S ? a.d[k + (uint64_t)t * nsub] : 0;
-            vs[q] = t < S ? a.s[k + (uint64_t)t * nsub] : 0;
+        for (int e = 0; e < E; e++) {
+            const int u = e * 64 + lane;
+            t0[e] = u < S ? a.d[k + (uint64_t)u * nsub] : 0;
+            t1[e] = u < S ? a.s[k + (uint64_t)u * nsub] : 0;
         }
-#pragma unroll
-        for (int q = 0; q < NQ; q++)
-            if (lt + q * NI < S) {
-                Td[lt + q * NI] = vd[q];
-                Ts[lt + q * NI] = vs[q];
-            }
     }
-    // weights W[h + u] e_k of the pairs of every round (W: table s at offset 2^s)
-    const uint64_t ek = suffix_weight(a.HS, a.LS, a.lN - a.j - B, a.L, k);
-    for (int e0 = tid + 1; e0 < S; e0 += 4 * blockDim.x) {
-        uint64_t v[4];
+    uint64_t z[NR];
 #pragma unroll
-        for (int q = 0; q < 4; q++) v[q] = e0 + q * (int)blockDim.x < S ? a.W[e0 + q * blockDim.x] : 0;
+    for (int c = 0; c < B; c++) z[c] = rho[c];
+    // round c's sums of this lane go to red[(c NV + q) kXbRedStride + lane]
 #pragma unroll
-        for (int q = 0; q < 4; q++)
-            if (e0 + q * (int)blockDim.x < S) W[e0 + q * blockDim.x] = m61::lmul(v[q], ek);
-    }
-    __syncthreads();
-    int off = 0;
     for (int c = 0; c < B; c++) {
-        const int h = S >> (c + 1), n = h < NI ? h : NI;
-        if (!zw) {
-            const uint64_t z = za[c];
-            uint64_t acc[5] = {0, 0, 0, 0, 0};
-            for (int u = lt; u < h; u += NI) {
-                const uint64_t w = W[h + u], b0 = Tb[u], b1 = Tb[u + h];
-                range_pair(w, b0, b1, acc);
-                fold_all<5>(acc);
-                Tb[u] = fold(b0, b1, z);
-            }
-            if (lt < n)
+        const int h = S >> (c + 1);
+        uint64_t acc[NV];
 #pragma unroll
-                for (int q = 0; q < 5; q++) pr[(off + lt) * 5 + q] = acc[q];
-        } else {
-            const uint64_t z = zz[c];
-            uint64_t acc[3] = {0, 0, 0};
-            for (int u = lt; u < h; u += NI) {
-                const uint64_t w = W[h + u];
-                const uint64_t d0 = Td[u], d1 = Td[u + h], s0 = Ts[u], s1 = Ts[u + h];
-                relu_pair(w, d0, d1, s0, s1, acc);
-                fold_all<3>(acc);
-                Td[u] = fold(d0, d1, z);
-                Ts[u] = fold(s0, s1, z);
-            }
-            if (lt < n)
+        for (int q = 0; q < NV; q++) acc[q] = 0;
+        if (h >= 64) {  // both entries of every pair in this lane: slots e and e + h / 64
+            const int hs = h / 64;
 #pragma unroll
-                for (int q = 0; q < 3; q++) pz[(off + lt) * 3 + q] = acc[q];
+            for (int e = 0; e < E / 2; e++) {
+                if (e < hs) {
+                    const uint64_t w = W[h + e * 64 + lane];
+                    if (!ZW) {
+                        range_pair(w, t0[e], t0[e + hs], acc);
+                        t0[e] = fold(t0[e], t0[e + hs], z[c]);
+                    } else {
+                        relu_pair(w, t0[e], t0[e + hs], t1[e], t1[e + hs], acc);
+                        t0[e] = fold(t0[e], t0[e + hs], z[c]);
+                        t1[e] = fold(t1[e], t1[e + hs], z[c]);
+                    }
+                    fold_all<NV>(acc);
+                }
+            }
+        } else {  // lane u < h pairs with lane u + h (slot 0)
+            const uint64_t p0 = lane_down(t0[0], h), p1 = ZW ? lane_down(t1[0], h) : 0;
+            if (lane < h) {
+                const uint64_t w = W[h + lane];
+                if (!ZW) {
+                    range_pair(w, t0[0], p0, acc);
+                    t0[0] = fold(t0[0], p0, z[c]);
+                } else {
+                    relu_pair(w, t0[0], p0, t1[0], p1, acc);
+                    t0[0] = fold(t0[0], p0, z[c]);
+                    t1[0] = fold(t1[0], p1, z[c]);
+                }
+                fold_all<NV>(acc);
+            }
         }
-        off += n;
-        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < NV; q++) red[(c * NV + q) * kXbRedStride + lane] = acc[q];
     }
-    // per-round sums: sum q = 8 c + w over the round's thread entries (folded
-    // values), eight lanes per sum, four terms added before each fold
-    const int ntask = 64 * B;
-    for (int task = tid; task < ntask; task += blockDim.x) {  // ntask is a multiple of 64: whole waves iterate
-        const int q = task >> 3, part = task & 7, c = q >> 3, w = q & 7;
-        int o = 0;
-        for (int cc = 0; cc < c; cc++) o += (S >> (cc + 1)) < NI ? (S >> (cc + 1)) : NI;
-        const int n = (S >> (c + 1)) < NI ? (S >> (c + 1)) : NI;
-        const uint64_t *src = w < 5 ? pr + (size_t)o * 5 + w : pz + (size_t)o * 3 + (w - 5);
-        const int st = w < 5 ? 5 : 3;
-        uint64_t v = 0;
-        if (w < 5 || RELU) {
-            int e = part;
-            for (; e + 24 < n; e += 32) v = m61::fold(v + src[e * st] + src[(e + 8) * st] + src[(e + 16) * st] + src[(e + 24) * st]);
-            for (; e < n; e += 8) v = m61::fold(v + src[e * st]);
+    // lane sums of every (round, value) through the wave's LDS area: lane v
+    // sums value v over the 64 lanes, four terms before each fold
+    const uint64_t ek = suffix_weight(a.HS, a.LS, a.lN - a.j - B, a.L, k);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    uint64_t *tot = red + 5 * kXBlockMax * kXbRedStride;  // 8 words per round: the sums at e_k
+    static_assert(kXBlockMax * 5 <= 64, "one lane per summed value");
+    if (lane < B * NV) {
+        const uint64_t *src = red + lane * kXbRedStride;
+        uint64_t v0 = 0, v1 = 0;
+#pragma unroll
+        for (int l = 0; l < 64; l += 8) {
+            v0 = m61::fold(v0 + src[l] + src[l + 1] + src[l + 2] + src[l + 3]);
+            v1 = m61::fold(v1 + src[l + 4] + src[l + 5] + src[l + 6] + src[l + 7]);
         }
-        v = m61::fold(v + __shfl_xor(v, 1, 64));
-        v = m61::fold(v + __shfl_xor(v, 2, 64));
-        v = m61::fold(v + __shfl_xor(v, 4, 64));
-        if (part == 0) red[q] = m61::canon(v);
+        const int c = lane / NV, q = lane % NV;
+        tot[8 * c + (ZW ? 5 : 0) + q] = m61::canon(m61::lmul(m61::fold(v0 + v1), ek));
     }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (nsub > 1) {
-        if (tid < 8 * B) a.part[(size_t)(tid >> 3) * a.stride + 8 * k + (tid & 7)] = red[tid];
-        if (tid == 0) a.bx[k] = m61::canon(Tb[0]);
-        if (RELU && tid == NI) {
-            a.d[k] = m61::canon(Td[0]);
-            a.s[k] = m61::canon(Ts[0]);
+        // round c's partial of sub-cube k: words 0-4 range, 5-7 ReLU (zero without it)
+        for (int t = lane; t < 8 * B; t += 64) {  // 8 B may exceed the wave
+            const int c = t >> 3, w = t & 7;
+            const bool mine = ZW ? w >= 5 : w < 5;
+            if (mine) a.part[(size_t)c * a.stride + 8 * k + w] = tot[t];
+            else if (!RELU) a.part[(size_t)c * a.stride + 8 * k + w] = 0;
+        }
+        if (lane == 0) {
+            if (!ZW) a.bx[k] = m61::canon(t0[0]);
+            else {
+                a.d[k] = m61::canon(t0[0]);
+                a.s[k] = m61::canon(t1[0]);
+            }
         }
     } else {
-        // round c's evaluation X of instance zr by thread 8 c + 4 zr + X
-        if (tid < 8 * B) {
-            const int c = tid >> 3, zr = (tid >> 2) & 1, X = tid & 3;
-            if (!zr || RELU)
-                a.tr[(zr ? a.out2 : a.out0) + 4 * c + X] = x_round_eval(red + 8 * c, a.j + c, X, zr != 0, a.xc);
+        // round c's evaluation X by lane 4 c + X
+        for (int t = lane; t < 4 * B; t += 64) {
+            const int c = t >> 2, X = t & 3;
+            const int out = ZW ? a.out2 : a.out0;
+            if (out >= 0) a.tr[out + 4 * c + X] = x_round_eval(tot + 8 * c, a.j + c, X, ZW, a.xc);
         }
-        if (tid == 0) {
-            *a.fin_b = m61::canon(Tb[0]);
-            if (RELU) {
+        if (lane == 0) {
+            if (!ZW) {
+                *a.fin_b = m61::canon(t0[0]);
+            } else {
                 const uint64_t inv2 = 1ull << 60;  // (p + 1) / 2
-                const uint64_t d = m61::canon(Td[0]), sv = m61::canon(Ts[0]);
+                const uint64_t d = m61::canon(t0[0]), sv = m61::canon(t1[0]);
                 *a.fin_r = m61::mul(m61::add(d, sv), inv2);
                 *a.fin_y = m61::mul(m61::sub(sv, d), inv2);
             }
@@ -471,12 +466,43 @@ __global__ __launch_bounds__(256) void k_xblock(XBlockArgs a, int first, XJobs j
     }
 }
 
+template <bool RELU, int B>
+__global__ __launch_bounds__(256) void k_xblock(XBlockArgs a, int first, XJobs jobs, int nmain)
+{
+    __shared__ uint64_t smem[kXbLdsWords];
+    if ((int)blockIdx.x >= nmain) {
+        x_job(jobs, blockIdx.x - nmain, smem);
+        return;
+    }
+    constexpr int S = 1 << B, PER = RELU ? 2 : 4;  // sub-cubes per workgroup
+    const int tid = threadIdx.x, wv = tid >> 6;
+    uint64_t *W = smem;  // W[1 .. S), shared by the workgroup's sub-cubes
+    for (int e = tid + 1; e < S; e += 256) W[e] = a.W[e];
+    __syncthreads();
+    const uint64_t nsub = 1ull << (a.lS - B);
+    const uint64_t k = (uint64_t)blockIdx.x * PER + (RELU ? (wv >> 1) : wv);
+    if (k >= nsub) return;  // wave-uniform, after the only barrier
+    uint64_t *red = smem + kXbMax + wv * kXbRedWords;
+    if (RELU && (wv & 1)) xb_wave<B, true, RELU>(a, first != 0, k, nsub, W, red);
+    else xb_wave<B, false, RELU>(a, first != 0, k, nsub, W, red);
+}
+
 void launch_xblock(bool relu, bool first, const XBlockArgs &a, const XJobs &jobs, hipStream_t st)
 {
-    const int nmain = 1 << (a.lS - a.B);
+    const int per = relu ? 2 : 4;
+    const uint64_t nsub = 1ull << (a.lS - a.B);
+    const int nmain = (int)((nsub + per - 1) / per);
     const dim3 g(nmain + jobs.nslot + jobs.nplane), b(kThreads);
-    if (relu) hipLaunchKernelGGL(k_xblock<true>, g, b, 0, st, a, (int)first, jobs, nmain);
-    else hipLaunchKernelGGL(k_xblock<false>, g, b, 0, st, a, (int)first, jobs, nmain);
+#define RA_XB(BB)                                                                                 \
+    case BB:                                                                                      \
+        if (relu) hipLaunchKernelGGL((k_xblock<true, BB>), g, b, 0, st, a, (int)first, jobs, nmain);  \
+        else hipLaunchKernelGGL((k_xblock<false, BB>), g, b, 0, st, a, (int)first, jobs, nmain);      \
+        break;
+    switch (a.B) {
+        RA_XB(0) RA_XB(1) RA_XB(2) RA_XB(3) RA_XB(4) RA_XB(5) RA_XB(6) RA_XB(7) RA_XB(8) RA_XB(9)
+        default: RA_XB(10)
+    }
+#undef RA_XB
 }
 
 }  // namespace ra

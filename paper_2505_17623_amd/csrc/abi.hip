@@ -39,6 +39,8 @@ struct ra_ctx {
     const uint64_t *d_r12 = nullptr;  // the layer's (r1, r2) in the challenge stream
     size_t eq_cap = 0;
     WitParams *d_params = nullptr;
+    char *d_wit = nullptr;  // the witness's per-workgroup partials (min/max, claims, range flags)
+    ClaimsJob pend_claims{};  // a deferred witness call's last step, run by the range call's set-up
     uint64_t *d_claims = nullptr;  // R~, Rm~, Y~, Z~ at (r1, r2)
     int s = 0, relu = 0, mode = 0, t = 0, P = 0;
     // kernel-group timing (ra_ctx_set_profiling)
@@ -81,6 +83,11 @@ struct Carve {
         return o;
     }
 };
+
+// The witness partials: min / max (2 words), claims (4 words) and a range
+// flag (4 bytes) per workgroup, for at most kMaxBlocks workgroups.
+constexpr size_t kWitMinMax = 0, kWitClaims = 16 * kMaxBlocks, kWitFlags = kWitClaims + 32 * kMaxBlocks,
+                 kWitBytes = kWitFlags + 4 * kMaxBlocks;
 
 ra_status ensure_ws(ra_ctx *c, size_t bytes)
 {
@@ -198,6 +205,10 @@ ra_status complete(ra_ctx *c)
 // Wait for all enqueued work and complete the pending outputs.
 ra_status drain(ra_ctx *c)
 {
+    if (c->pend_claims.nblk > 0) {  // a witness call's last step not yet taken by a range call
+        launch_claims_final(c->pend_claims, c->stream);
+        c->pend_claims.nblk = 0;
+    }
     RA_HIP(hipStreamSynchronize(c->stream));
     return complete(c);
 }
@@ -219,10 +230,13 @@ ra_status alloc_stage(ra_ctx *c, size_t words)
 ra_status stage_take(ra_ctx *c, size_t words, size_t *off)
 {
     const size_t need = (words + 7) & ~(size_t)7;
-    if (c->stage_used + need > c->stage_cap) {  // grow once what is pending has been written out
+    if (c->stage_used + need > c->stage_cap) {
+        // grow to four times what is pending (a caller that keeps many calls
+        // pending soon stops growing) once it has been written out
+        const size_t want = std::max({4 * (c->stage_used + need), 2 * c->stage_cap, (size_t)4096});
         const ra_status r = drain(c);
         if (r != RA_OK && c->deferred_err == RA_OK) c->deferred_err = r;
-        const ra_status a = alloc_stage(c, std::max(2 * need, (size_t)4096));
+        const ra_status a = alloc_stage(c, want);
         if (a != RA_OK) return a;
     }
     *off = c->stage_used;
@@ -353,6 +367,7 @@ ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_cha
         st = RA_E_HIP;
     static_assert(sizeof(WitParams) <= 64, "parameters precede the claims");
     if (st == RA_OK && hipMalloc((void **)&c->d_params, 128) != hipSuccess) st = RA_E_NOMEM;
+    if (st == RA_OK && hipMalloc((void **)&c->d_wit, kWitBytes) != hipSuccess) st = RA_E_NOMEM;
     if (st == RA_OK) c->d_claims = (uint64_t *)((char *)c->d_params + 64);
     if (st == RA_OK) st = alloc_stage(c, 4096);
     if (st != RA_OK) {
@@ -373,6 +388,7 @@ ra_status ra_ctx_destroy(ra_ctx *c)
     if (c->d_eq) (void)hipFree(c->d_eq);
     if (c->d_acc) (void)hipFree(c->d_acc);
     if (c->d_params) (void)hipFree(c->d_params);
+    if (c->d_wit) (void)hipFree(c->d_wit);
     if (c->ws) (void)hipFree(c->ws);
     if (c->h_stage) (void)hipHostFree(c->h_stage);
     flush_profile(c);
@@ -576,25 +592,24 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
         hp.mode = (int)io->round_mode;
         hp.t_in = io->t;
     }
-    const int nb = witness_blocks(N);
-    Carve cv;
-    const size_t o_mm = cv.take<int64_t>(2 * (size_t)nb), o_cl = cv.take<uint64_t>(4 * (size_t)nb);
-    const size_t o_fl = cv.take<uint32_t>((size_t)nb);
-    ra_status st = ensure_ws(c, cv.off);
-    if (st != RA_OK) return st;
+    static_assert(kMaxBlocks >= 1, "witness partials");  // witness_blocks(N) <= kMaxBlocks
+    ra_status st = RA_OK;
     const int lk = log2u(k);
     size_t o_st = 0;
     if ((st = stage_take(c, 12, &o_st)) != RA_OK) return st;
     if (!given) {
         Timed tm(c, G_WIT_MINMAX);
         launch_witness_params(d_C, N, (int)io->s, (int)io->relu, (int)io->round_mode, io->t,
-                              (int64_t *)(c->ws + o_mm), c->d_params, c->stream);
+                              (int64_t *)(c->d_wit + kWitMinMax), c->d_params, c->stream);
     }
-    {
+    {   // A call that does not wait (deferred, t given) leaves its last step, the
+        // sum of the claims, to the range call that must follow (its set-up
+        // launch), or to the next wait on the context.
         Timed tm(c, G_WIT_RESCALE);
         launch_witness_rescale(d_C, N, lk, c->d_eq, c->d_eq + n, d_R, d_Rm, d_Y, d_Z, d_bits,
-                               (uint64_t *)(c->ws + o_cl), c->d_params, c->d_claims, c->d_stage + o_st, c->stream,
-                               given ? &hp : nullptr, (uint32_t *)(c->ws + o_fl));
+                               (uint64_t *)(c->d_wit + kWitClaims), c->d_params, c->d_claims, c->d_stage + o_st,
+                               c->stream, given ? &hp : nullptr, (uint32_t *)(c->d_wit + kWitFlags),
+                               known ? &c->pend_claims : nullptr);
     }
     // parameters (words 0-7) and claims (words 8-11) are staged together
     auto fill = [c, io, known](const uint64_t *h) {
@@ -695,7 +710,8 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     {   // the Gram matrix; further workgroups: the constant block and the x set-up
         Timed tm(c, G_RANGE_SETUP);
         const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
-        const RangeConsts rc{lam, c->d_params, c->d_claims, lP, cst, tr + RS};
+        const RangeConsts rc{lam, c->d_params, c->d_claims, lP, cst, tr + RS, c->pend_claims};
+        c->pend_claims.nblk = 0;  // taken by this launch
         launch_gram_reduce(lP, N, gpart, gsum, rc, xs, s);
     }
     // Each x launch's extra workgroups assemble the rounds of the launch

@@ -117,10 +117,13 @@ void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mo
 // known (optional): parameters computed on the host for a given t (status 0);
 // then no params pass runs before, the range of R is checked here (flags:
 // witness_blocks(N) words) and the parameters are written to params.
+struct ClaimsJob;
+// defer (optional): the last step is not launched but returned there, for a
+// later launch to run (ClaimsJob).
 void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
                             uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
                             WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st,
-                            const WitParams *known = nullptr, uint32_t *flags = nullptr);
+                            const WitParams *known = nullptr, uint32_t *flags = nullptr, ClaimsJob *defer = nullptr);
 
 // ---- launchers (sumcheck.hip) ----
 int round_blocks(uint64_t h);
@@ -154,15 +157,31 @@ struct XJobs;
 // The tail workgroup, plus one workgroup per slot in jobs (SLOT_COPY slots of
 // the global rounds before it).
 void launch_tail(int kind, const TailArgs &a, const XJobs &jobs, hipStream_t st);
+// The witness's last step (claims.hpp): the claims summed from nblk
+// workgroup partials (4 words each), the status from their range flags when
+// t was given (known: parameters hp), written to prm, out (4 words) and the
+// staged transcript words `mirror` (12 words: parameters, claims).
+struct ClaimsJob {
+    const uint64_t *part;
+    int nblk;  // 0: no job
+    WitParams *prm;
+    uint64_t *out, *mirror;
+    WitParams hp;
+    int known;
+    const uint32_t *flags;
+};
+void launch_claims_final(const ClaimsJob &j, hipStream_t st);
 // Constant block of the plane rounds (rsetup.hpp): lambda/mu/tau_p/sigma_p at
 // chal, the witness parameters and claims; writes cst (C_WORDS) and the
-// claimed sum of the range instance.
+// claimed sum of the range instance.  cj (nblk > 0): the witness's deferred
+// last step, run first by the same workgroup.
 struct RangeConsts {
     const uint64_t *chal;
     const WitParams *prm;
     const uint64_t *claims;
     int lP;
     uint64_t *cst, *range_sum;
+    ClaimsJob cj;
 };
 void init_kernel_attributes();
 // Constants of SLOT_X rounds: kp = (Ep, c) of the range summand, r the EQ

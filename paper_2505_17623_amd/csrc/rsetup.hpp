@@ -2,6 +2,7 @@
 // of the plane rounds and the tables of the rounds over x (xsetup.hpp).  Run
 // by extra workgroups of the Gram reduction (planes.hip).
 #pragma once
+#include "claims.hpp"
 #include "common.hpp"
 #include "m61.hpp"
 #include "xsetup.hpp"
@@ -60,13 +61,21 @@ __device__ __forceinline__ void range_consts_block(const RangeConsts &rc)
     __shared__ uint64_t eqt[kMaxPlaneLog];
     __shared__ uint64_t ch[4 + 2 * kMaxPlaneLog], cl[3];
     __shared__ int pv[3];
+    __shared__ uint64_t wres[12];
     const int P = 1 << lP;
+    if (rc.cj.nblk > 0) {  // the witness's last step first: its parameters and claims come back in wres
+        __shared__ uint64_t red[m61::block_sum_words(4, 256)];
+        claims_final_block(rc.cj, red, wres);
+    }
     if (tid < 4 + 2 * lP) ch[tid] = chal[tid];
-    if (tid >= 64 && tid < 67) cl[tid - 64] = claims[tid - 64];
+    if (tid >= 64 && tid < 67) cl[tid - 64] = rc.cj.nblk > 0 ? wres[8 + tid - 64] : claims[tid - 64];
     if (tid == 128) {
-        pv[0] = prm->s;
-        pv[1] = prm->t;
-        pv[2] = prm->relu;
+        WitParams wp;
+        if (rc.cj.nblk > 0) __builtin_memcpy(&wp, wres, sizeof(WitParams));
+        else wp = *prm;
+        pv[0] = wp.s;
+        pv[1] = wp.t;
+        pv[2] = wp.relu;
     }
     for (int i = tid; i < C_WORDS; i += blockDim.x) c[i] = 0;
     __syncthreads();

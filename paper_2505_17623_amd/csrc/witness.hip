@@ -1,5 +1,6 @@
 // witness.hip -- eq tables, exact integer matrix product, multilinear binding
 // of matrix sides, and the rescale / ReLU / bit-plane witness.
+#include "claims.hpp"
 #include "common.hpp"
 #include "m61.hpp"
 #include "ra.h"
@@ -467,35 +468,15 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
         for (int i = 0; i < 4; i++) claim_part[4 * blockIdx.x + i] = acc[i];
 }
 
-__global__ __launch_bounds__(256) void k_claims_final(const uint64_t *__restrict__ part, int nblk,
-                                                      WitParams *__restrict__ prm, uint64_t *__restrict__ out,
-                                                      uint64_t *__restrict__ mirror, WitParams hp, int known,
-                                                      const uint32_t *__restrict__ flags)
+__global__ __launch_bounds__(256) void k_claims_final(ClaimsJob j)
 {
     __shared__ uint64_t red[m61::block_sum_words(4, 256)];
-    WitParams p;
-    if (known) {  // the status from the workgroups' range flags; the parameters for the range call
-        int any = 0;
-        for (int b = threadIdx.x; b < nblk; b += blockDim.x) any |= flags[b] != 0;
-        p = hp;
-        if (__syncthreads_or(any)) p.status = RA_E_RANGE;
-        if (threadIdx.x == 0) *prm = p;
-    } else {
-        p = *prm;
-    }
-    uint64_t acc[4] = {0, 0, 0, 0};
-    if (p.status == 0)
-        for (int b = threadIdx.x; b < nblk; b += blockDim.x)
-            for (int i = 0; i < 4; i++) acc[i] = m61::add(acc[i], part[4 * b + i]);
-    m61::block_sum<4>(acc, red);
-    if (threadIdx.x != 0) return;
-    if (p.status == 0)
-        for (int i = 0; i < 4; i++) out[i] = acc[i];
-    if (mirror) {
-        const uint64_t *pw = (const uint64_t *)&p;
-        for (int i = 0; i < 8; i++) mirror[i] = i * 8 < (int)sizeof(WitParams) ? pw[i] : 0;
-        for (int i = 0; i < 4; i++) mirror[8 + i] = acc[i];
-    }
+    claims_final_block(j, red, nullptr);
+}
+
+void launch_claims_final(const ClaimsJob &j, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, j);
 }
 
 void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mode, int t_in, int64_t *mm_part,
@@ -510,7 +491,7 @@ void launch_witness_params(const int64_t *C, uint64_t N, int s, int relu, int mo
 void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2, int32_t *R,
                             uint16_t *Rm, int32_t *Y, int32_t *Z, uint64_t *bits, uint64_t *claim_part,
                             WitParams *params, uint64_t *claims_out, uint64_t *mirror, hipStream_t st,
-                            const WitParams *known, uint32_t *flags)
+                            const WitParams *known, uint32_t *flags, ClaimsJob *defer)
 {
     const WitParams hp = known ? *known : WitParams{};
     const bool vec = N >= 4 && (((uintptr_t)C | (uintptr_t)R | (uintptr_t)Y | (uintptr_t)Z | (uintptr_t)bits) & 15) == 0 &&
@@ -522,8 +503,9 @@ void launch_witness_rescale(const int64_t *C, uint64_t N, int lk, const uint64_t
     else
         hipLaunchKernelGGL(k_rescale<1>, dim3(nb), dim3(kThreads), 0, st, C, N, lk, (const WitParams *)params, E1, E2,
                            R, Rm, Y, Z, bits, claim_part, hp, known ? 1 : 0, flags);
-    hipLaunchKernelGGL(k_claims_final, dim3(1), dim3(kThreads), 0, st, (const uint64_t *)claim_part, nb, params,
-                       claims_out, mirror, hp, known ? 1 : 0, (const uint32_t *)flags);
+    const ClaimsJob j{claim_part, nb, params, claims_out, mirror, hp, known ? 1 : 0, flags};
+    if (defer) *defer = j;
+    else launch_claims_final(j, st);
 }
 
 }  // namespace ra

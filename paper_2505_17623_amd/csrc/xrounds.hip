@@ -367,6 +367,7 @@ __device__ __forceinline__ void xb_wave(const XBlockArgs &a, bool first, uint64_
     uint64_t z[NR];
 #pragma unroll
     for (int c = 0; c < B; c++) z[c] = rho[c];
+    const uint64_t ek = suffix_weight(a.HS, a.LS, a.lN - a.j - B, a.L, k);  // loaded with the tables
     // round c's sums of this lane go to red[(c NV + q) kXbRedStride + lane]
 #pragma unroll
     for (int c = 0; c < B; c++) {
@@ -411,7 +412,6 @@ __device__ __forceinline__ void xb_wave(const XBlockArgs &a, bool first, uint64_
     }
     // lane sums of every (round, value) through the wave's LDS area: lane v
     // sums value v over the 64 lanes, four terms before each fold
-    const uint64_t ek = suffix_weight(a.HS, a.LS, a.lN - a.j - B, a.L, k);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");

@@ -228,7 +228,7 @@ def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor, C: 
     _check(lib().ra_sumcheck_matmul_prove(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C),
                                           ctypes.byref(pr)), "ra_sumcheck_matmul_prove")
     res = {}
-    ctx.later(lambda: res.update(c0=int(pr.c0), mm_evals=[int(x) for x in ev[:3 * lm]], a_star=int(pr.a_star),
+    ctx.later(lambda: res.update(c0=int(pr.c0), mm_evals=ev[:3 * lm].tolist(), a_star=int(pr.a_star),
                                  b_star=int(pr.b_star)))
     return C, res
 
@@ -272,8 +272,8 @@ def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
     _check(lib().ra_range_prove(ctx.h, _dptr(bits), _dptr(R), _dptr(Y), n, k, ctypes.byref(info),
                                 ctypes.byref(pr)), "ra_range_prove")
     res = {}
-    ctx.later(lambda: res.update(rs_evals=[int(x) for x in ev], range_sum=int(pr.range_sum),
-                                 bits_claim=int(pr.bits_claim), zc_evals=[int(x) for x in zev[:4 * pr.relu_rounds]],
+    ctx.later(lambda: res.update(rs_evals=ev.tolist(), range_sum=int(pr.range_sum),
+                                 bits_claim=int(pr.bits_claim), zc_evals=zev[:4 * pr.relu_rounds].tolist(),
                                  r_at=int(pr.r_at), y_at=int(pr.y_at)))
     return res
 

@@ -250,14 +250,21 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
 // partial blocks and combine through LDS.
 // Workgroups below nred: 16 entries of G each, sixteen lanes per entry (lane
 // group g sums the partial tiles of blocks g, g + 16, ...), then LDS.  The
-// next workgroup writes the constant block of the plane rounds, the others
-// run the set-up of the rounds over x.
+// next workgroup writes the constant block of the plane rounds, with a
+// deferred witness step the one after sums the witness claims (and the
+// claimed sum of the range instance), the others run the set-up of the
+// rounds over x.
 __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict__ gpart, int nblk, int TP,
                                                      uint64_t *__restrict__ G, int nred, RangeConsts rc,
                                                      XSetupArgs xs)
 {
-    if ((int)blockIdx.x > nred) {
-        x_setup_block(xs, blockIdx.x - nred - 1);
+    const int ncj = rc.cj.nblk > 0 ? 1 : 0;  // a deferred witness step: one more workgroup
+    if ((int)blockIdx.x > nred + ncj) {
+        x_setup_block(xs, blockIdx.x - nred - 1 - ncj);
+        return;
+    }
+    if (ncj && (int)blockIdx.x == nred + 1) {
+        witness_claims_block(rc);
         return;
     }
     if ((int)blockIdx.x == nred) {
@@ -314,7 +321,8 @@ void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsu
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP), nred = TP * 64;
     const int xb = (x_setup_count(xs) + 255) / 256;
-    hipLaunchKernelGGL(k_gram_reduce, dim3(nred + 1 + xb), dim3(256), 0, st, gpart, nb, TP, gsum, nred, rc, xs);
+    const int ncj = rc.cj.nblk > 0 ? 1 : 0;
+    hipLaunchKernelGGL(k_gram_reduce, dim3(nred + 1 + ncj + xb), dim3(256), 0, st, gpart, nb, TP, gsum, nred, rc, xs);
 }
 
 }  // namespace ra

@@ -47,6 +47,30 @@ __device__ __forceinline__ void x_setup_block(const XSetupArgs &xs, int q)
     x_setup_body(xs, q * blockDim.x + tid, rl, sl, zl);
 }
 
+// Claimed sum of the range instance: mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~)
+// (l3 with ReLU only); claims = (R~, Rm~, Y~, Z~).  Canonical.
+__device__ __forceinline__ uint64_t range_claimed_sum(const uint64_t *lam, uint64_t mu, const uint64_t *cl, int t,
+                                                      int relu)
+{
+    using namespace m61;
+    uint64_t H = lmul(lam[0], cl[1]) + lmul(lam[1], fold(cl[0] + (1ull << (t + 1))));
+    if (relu) H = fold(H) + lmul(lam[2], cl[2]);
+    return canon(lmul(mu, fold(H)));
+}
+
+// A deferred witness call's last step (claims.hpp) and, from its claims,
+// the claimed sum of the range instance; one workgroup of 256 threads.
+__device__ __forceinline__ void witness_claims_block(const RangeConsts &rc)
+{
+    __shared__ uint64_t red[m61::block_sum_words(4, 256)];
+    __shared__ uint64_t wres[12];
+    claims_final_block(rc.cj, red, wres);
+    if (threadIdx.x == 0) {
+        const uint64_t lam[3] = {rc.chal[0], rc.chal[1], rc.chal[2]};
+        *rc.range_sum = range_claimed_sum(lam, rc.chal[3], wres + 8, rc.cj.hp.t, rc.cj.hp.relu);
+    }
+}
+
 // The constant block of the plane rounds (one workgroup of at least 256
 // threads); chal points at lambda1: lambda1..3, mu, tau_p (lP), sigma
 // (lP + ...).  Every operand is first staged in LDS.
@@ -61,18 +85,14 @@ __device__ __forceinline__ void range_consts_block(const RangeConsts &rc)
     __shared__ uint64_t eqt[kMaxPlaneLog];
     __shared__ uint64_t ch[4 + 2 * kMaxPlaneLog], cl[3];
     __shared__ int pv[3];
-    __shared__ uint64_t wres[12];
     const int P = 1 << lP;
-    if (rc.cj.nblk > 0) {  // the witness's last step first: its parameters and claims come back in wres
-        __shared__ uint64_t red[m61::block_sum_words(4, 256)];
-        claims_final_block(rc.cj, red, wres);
-    }
+    // with the witness's last step deferred (t given), the parameters are the
+    // job's and the claimed sum is left to witness_claims_block
+    const bool deferred = rc.cj.nblk > 0;
     if (tid < 4 + 2 * lP) ch[tid] = chal[tid];
-    if (tid >= 64 && tid < 67) cl[tid - 64] = rc.cj.nblk > 0 ? wres[8 + tid - 64] : claims[tid - 64];
+    if (!deferred && tid >= 64 && tid < 67) cl[tid - 64] = claims[tid - 64];
     if (tid == 128) {
-        WitParams wp;
-        if (rc.cj.nblk > 0) __builtin_memcpy(&wp, wres, sizeof(WitParams));
-        else wp = *prm;
+        const WitParams wp = deferred ? rc.cj.hp : *prm;
         pv[0] = wp.s;
         pv[1] = wp.t;
         pv[2] = wp.relu;
@@ -127,10 +147,7 @@ __device__ __forceinline__ void range_consts_block(const RangeConsts &rc)
         c[C_EP + 1] = canon(lsub(lmul(mu, Wp), K));  // c = mu Wp - Ep
         c[C_EP + 2] = canon(Wp);
         c[C_EP + 3] = mu;
-        // claimed sum mu (l1 Rm~ + l2 (R~ + 2^(t+1)) + l3 Y~); claims = (R~, Rm~, Y~, Z~)
-        uint64_t H = lmul(lam[0], cl[1]) + lmul(lam[1], fold(cl[0] + (1ull << (t + 1))));
-        if (relu) H = fold(H) + lmul(lam[2], cl[2]);
-        *range_sum = canon(lmul(mu, fold(H)));
+        if (!deferred) *range_sum = range_claimed_sum(lam, mu, cl, t, relu);
     }
     __syncthreads();
     for (int i = tid; i < C_WORDS; i += blockDim.x) cst[i] = c[i];

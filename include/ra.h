@@ -90,11 +90,15 @@ const char *ra_status_str(ra_status st);
 /* Deferred host outputs, for callers that pipeline many layers without
  * waiting on each call.
  *   ra_ctx_set_deferred(ctx, 1): from now on ra_sumcheck_matmul_prove and
- *     ra_range_prove return once their work and the copy of their transcript
- *     into pinned staging memory are enqueued; ra_rescale_relu_witness does
+ *     ra_range_prove return once their work is enqueued; ra_rescale_relu_witness does
  *     the same when the caller gives t (io->t >= 0: the plane count P is then
  *     known on the host and io->P is set at once), and otherwise waits for t
- *     and P as in synchronous mode.  The caller keeps every proof struct, its
+ *     and P as in synchronous mode.  A witness call that does not wait leaves
+ *     the last sum of its claims to the range call that follows it (or to
+ *     the next wait on the context); nothing else observes the difference.
+ *     The kernels write transcripts straight into the context's pinned area,
+ *     which grows (after writing out what is pending) when the calls kept
+ *     pending outgrow it.  The caller keeps every proof struct, its
  *     evals arrays and the witness info alive and unread until ra_ctx_sync.
  *     Argument and state errors are still returned by the call itself; errors
  *     found on the device (a value outside the given range) are returned by

@@ -191,6 +191,23 @@ ra_status ra_rescale_relu_witness(ra_ctx *ctx, const int64_t *d_C, uint32_t n, u
                                   uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits,
                                   uint64_t bits_words, ra_witness_info *io);
 
+/* Optional: announce the next ra_rescale_relu_witness call (same layer) before
+ * its ra_sumcheck_matmul_prove, so that the witness of Alg. 1 step 9 and Sec.
+ * III-B is computed inside the exact product, from each entry of C while it
+ * is still in registers (C is still written).  Call it between layers (the
+ * context expects a matrix call).  The arguments are those the witness call
+ * will pass: s, relu, round_mode and a given t >= 0 (the plane count P
+ * follows from them), and the output buffers with the capacity of d_bits.
+ * The witness call then only sums its claims if its arguments are exactly
+ * these (and bits_words covers n * k); any other witness call, or a product
+ * the fusion does not take, runs the witness in full, so the results never
+ * depend on the plan.  The plan is used by one layer.
+ * Errors: RA_E_INVAL for a null buffer, t < 0 or parameters the witness call
+ * would reject; RA_E_RANGE / RA_E_FIELD_TOO_SMALL as that call would return
+ * them for s and t; RA_E_STATE when called between a layer's calls. */
+ra_status ra_witness_plan(ra_ctx *ctx, uint32_t s, uint32_t relu, uint32_t round_mode, int32_t t, int32_t *d_R,
+                          uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words);
+
 /* Transcript of the range sum-check and the ReLU zero-check. */
 typedef struct {
     uint32_t rounds;       /* out: log P + log N */

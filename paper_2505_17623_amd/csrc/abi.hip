@@ -41,6 +41,19 @@ struct ra_ctx {
     WitParams *d_params = nullptr;
     char *d_wit = nullptr;  // the witness's per-workgroup partials (min/max, claims, range flags)
     ClaimsJob pend_claims{};  // a deferred witness call's last step, run by the range call's set-up
+    // the next witness call as announced by ra_witness_plan (fused into the
+    // product when `fused`, with `ntiles` partials)
+    struct WitPlan {
+        bool valid = false, fused = false;
+        uint32_t s = 0, relu = 0, mode = 0;
+        int32_t t = -1;
+        int32_t *R = nullptr;
+        uint16_t *Rm = nullptr;
+        int32_t *Y = nullptr, *Z = nullptr;
+        uint64_t *bits = nullptr;
+        uint64_t bits_words = 0;
+        uint32_t ntiles = 0;
+    } plan;
     uint64_t *d_claims = nullptr;  // R~, Rm~, Y~, Z~ at (r1, r2)
     int s = 0, relu = 0, mode = 0, t = 0, P = 0;
     // kernel-group timing (ra_ctx_set_profiling)
@@ -542,9 +555,26 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     XJobs tjobs{};
     run_instance(c, z, KIND_MATMUL, a, b, nullptr, lm, rho, tr, 1, 3, tr + 1 + 3 * lm, 0, part, G_MM_ROUNDS,
                  G_MM_TAIL, &ta, &tjobs, fused ? c->d_acc : nullptr);
+    // an announced witness (ra_witness_plan) runs in the product's epilogue
+    // when every output tile has a partial slot
+    WitEpi we{};
+    bool fuse_w = false;
+    if (c->plan.valid) {
+        const uint32_t nt = gemm_tiles(n, k);
+        fuse_w = nt <= (uint32_t)kMaxBlocks && c->plan.bits_words >= (uint64_t)n * k;
+        if (fuse_w) {
+            const auto &pl = c->plan;
+            we = WitEpi{(int)pl.s, pl.t, (int)pl.relu, pl.mode == RA_ROUND_NEAREST ? (int64_t)1 << (pl.s - 1) : 0,
+                        E1, E2, pl.R, pl.Rm, pl.Y, pl.Z, pl.bits, (uint64_t *)(c->d_wit + kWitClaims),
+                        (uint32_t *)(c->d_wit + kWitFlags)};
+            c->plan.ntiles = nt;
+        }
+        c->plan.fused = fuse_w;
+    }
     {
         Timed tm(c, G_GEMM);
-        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s, &ta, &tjobs, fused);
+        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s, &ta, &tjobs, fused,
+                         fuse_w ? &we : nullptr);
     }
     c->n = n;
     c->m = m;
@@ -560,6 +590,32 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
         out->b_star = h[2 + 3 * lm];
         return (ra_status)RA_OK;
     });
+}
+
+ra_status ra_witness_plan(ra_ctx *c, uint32_t s, uint32_t relu, uint32_t round_mode, int32_t t, int32_t *d_R,
+                          uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words)
+{
+    if (!c || !d_R || !d_Rm || !d_Y || !d_Z || !d_bits) return RA_E_INVAL;
+    if (c->phase != 0) return RA_E_STATE;
+    if (s < 1 || s > 16 || relu > 1 || round_mode > 1 || t < 0) return RA_E_INVAL;
+    int P = 0, lP = 0;
+    const ra_status pst = plane_params((int)s, t, (int)relu, &P, &lP);
+    if (pst != RA_OK) return pst;
+    auto &pl = c->plan;
+    pl.valid = true;
+    pl.fused = false;
+    pl.s = s;
+    pl.relu = relu;
+    pl.mode = round_mode;
+    pl.t = t;
+    pl.R = d_R;
+    pl.Rm = d_Rm;
+    pl.Y = d_Y;
+    pl.Z = d_Z;
+    pl.bits = d_bits;
+    pl.bits_words = bits_words;
+    pl.ntiles = 0;
+    return RA_OK;
 }
 
 ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uint32_t k, int32_t *d_R,
@@ -597,12 +653,29 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
     const int lk = log2u(k);
     size_t o_st = 0;
     if ((st = stage_take(c, 12, &o_st)) != RA_OK) return st;
+    // the product's epilogue made the outputs and per-tile partials if this
+    // call is the one announced; the plan is spent either way
+    const auto pl = c->plan;
+    c->plan.valid = c->plan.fused = false;
+    const bool planned = pl.valid && pl.fused && given && io->s == pl.s && io->relu == pl.relu &&
+                         io->round_mode == pl.mode && io->t == pl.t && d_R == pl.R && d_Rm == pl.Rm && d_Y == pl.Y &&
+                         d_Z == pl.Z && d_bits == pl.bits;
+    if (planned) {
+        const ClaimsJob j{(const uint64_t *)(c->d_wit + kWitClaims), (int)pl.ntiles, c->d_params, c->d_claims,
+                          c->d_stage + o_st, hp, 1, (const uint32_t *)(c->d_wit + kWitFlags)};
+        if (known) {
+            c->pend_claims = j;
+        } else {
+            Timed tm(c, G_WIT_RESCALE);
+            launch_claims_final(j, c->stream);
+        }
+    }
     if (!given) {
         Timed tm(c, G_WIT_MINMAX);
         launch_witness_params(d_C, N, (int)io->s, (int)io->relu, (int)io->round_mode, io->t,
                               (int64_t *)(c->d_wit + kWitMinMax), c->d_params, c->stream);
     }
-    {   // A call that does not wait (deferred, t given) leaves its last step, the
+    if (!planned) {   // A call that does not wait (deferred, t given) leaves its last step, the
         // sum of the claims, to the range call that must follow (its set-up
         // launch), or to the next wait on the context.
         Timed tm(c, G_WIT_RESCALE);

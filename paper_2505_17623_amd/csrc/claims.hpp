@@ -11,6 +11,48 @@
 
 namespace ra {
 
+// Claims of V outputs: sum_i e_i z_i for e_i = E1[row] E2[col]
+// (folded, < 2^61 + 8) and integers |z_i| <= 2^30 (R, Y, Z fit t <= 29; a
+// value outside the given range makes the call fail, its claims unused).
+// Each e_i is cut as e_hi 2^31 + e_lo, the two sums are exact in int64 (four
+// terms below 2^61 each), then reduced mod p once.
+template <int V>
+__device__ __forceinline__ uint64_t claim_terms(const uint64_t (&el)[V], const uint64_t (&eh)[V],
+                                                const int32_t (&z)[V])
+{
+    uint64_t lo = 0, hi = 0;  // two's complement sums (exact for |z| <= 2^30)
+#pragma unroll
+    for (int i = 0; i < V; i++) {
+        lo += (uint64_t)((int64_t)el[i] * z[i]);
+        hi += (uint64_t)((int64_t)eh[i] * z[i]);
+    }
+    return m61::fold(m61::from_i64((int64_t)lo) + m61::rotl(m61::from_i64((int64_t)hi), 31));
+}
+
+// One output of the rescale / ReLU witness (Sec. II-A, III-B) from its
+// product entry c: R = floor((c + half) / 2^s), the shifted remainder Rm,
+// Y = |R|, Z = ReLU(R) (or R), and the bit word (planes of Rm, R + 2^(t+1)
+// and, with ReLU, Y).  *oor is set when R lies outside [-2^(t+1), 2^(t+1)).
+struct WitOut {
+    int32_t r, rm, y, z;
+    uint64_t w;
+};
+__device__ __forceinline__ WitOut witness_entry(int64_t c, int s, int t, int relu, int64_t half, int &oor)
+{
+    WitOut o;
+    const int64_t cc = c + half;
+    const int64_t q = cc >> s;
+    // u = R for R >= 0, -R - 1 for R < 0; R in [-2^(t+1), 2^(t+1)) iff u < 2^(t+1)
+    oor |= ((uint64_t)(q >= 0 ? q : -(q + 1)) >> (t + 1)) != 0;
+    o.rm = (int32_t)(cc - (q << s));
+    o.r = (int32_t)q;
+    o.y = o.r < 0 ? -o.r : o.r;
+    o.z = relu ? (o.r > 0 ? o.r : 0) : o.r;
+    o.w = (uint64_t)o.rm | ((uint64_t)(q + ((int64_t)1 << (t + 1))) << s);
+    if (relu) o.w |= (uint64_t)o.y << (s + t + 2);
+    return o;
+}
+
 // red: m61::block_sum_words(4, blockDim.x) words of LDS; res (LDS, optional):
 // receives the parameters (words 0-7) and the claims (8-11), visible to the
 // workgroup after the function's last barrier.

@@ -80,10 +80,27 @@ struct TailArgs;
 struct XJobs;
 // ta, jobs (optional): the matrix instance's tail (launch_tail) as extra
 // workgroups of the product launch
-// split_done: the limb planes are already in ws (launch_front)
+// The rescale / ReLU witness fused into the product's epilogue
+// (ra_witness_plan): parameters, the eq tables of (r1, r2), the outputs, and
+// per output tile four claim partials and a range flag (claims.hpp).
+struct WitEpi {
+    int s, t, relu;
+    int64_t half;
+    const uint64_t *E1, *E2;
+    int32_t *R;
+    uint16_t *Rm;
+    int32_t *Y, *Z;
+    uint64_t *bits;
+    uint64_t *claim_part;
+    uint32_t *flags;
+};
+// Output tiles of the product (one workgroup and one witness partial each).
+uint32_t gemm_tiles(uint32_t n, uint32_t k);
+// split_done: the limb planes are already in ws (launch_front); we
+// (optional): the witness fused into the epilogue
 void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
                       void *ws, hipStream_t st, const TailArgs *ta = nullptr, const XJobs *jobs = nullptr,
-                      bool split_done = false);
+                      bool split_done = false, const WitEpi *we = nullptr);
 // The fused front of the matrix call (one launch): the product's limb split
 // into ws, the row binding of A at r1 added into acc (2 m words: low 32 bits,
 // high bits; zero on entry), the column binding of B at r2 into b, and the

@@ -12,6 +12,7 @@
 // at most two limb products share a weight, so |S_w| <= 2 m 2^14 fits int32
 // for m <= 32768, and the int64 recombination is exact.
 #include "common.hpp"
+#include "claims.hpp"
 #include "tail.hpp"
 
 namespace ra {
@@ -449,13 +450,15 @@ __global__ __launch_bounds__(256) void k_front(FrontArgs f)
 // sum-check instance (tail.hpp), which needs only the bound vectors, in the
 // stage area's LDS: the single-workgroup tail then runs beside the tiles
 // instead of after them.
-template <int LA, int S>
-__global__ __launch_bounds__(256) void k_gemm_mfma(const int8_t *__restrict__ Al, const int8_t *__restrict__ Bt,
+template <int LA, int S, bool WIT>
+__global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__ Al, const int8_t *__restrict__ Bt,
                                                    const int64_t *__restrict__ rowsum,
                                                    const int64_t *__restrict__ colpart, int ntiles, int64_t cA,
                                                    uint32_t n, uint32_t m, uint32_t k, uint32_t np, uint32_t mp,
-                                                   uint32_t kp, int64_t *__restrict__ C, TailArgs ta, XJobs jobs)
+                                                   uint32_t kp, int64_t *__restrict__ C, TailArgs ta, XJobs jobs,
+                                                   WitEpi we)
 {
+    static_assert(m61::block_sum_words(4, 256) * 8 <= S * (2 * (2 * LA + 4)) * 1024, "claims sum in the stage area");
     constexpr int F1 = 2 * LA + 4, F = 2 * F1, FW = F / 4;
     static_assert(F % 4 == 0, "fragments per wave");
     static_assert(S >= 2, "a stage read while the next fills");
@@ -564,17 +567,63 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const int8_t *__restrict__ Al
     const uint32_t col = j0 + cl;
     const int64_t colsum = s_cs[0][cl] + s_cs[1][cl] + s_cs[2][cl] + s_cs[3][cl];
     const uint64_t corr = (uint64_t)cA * (uint64_t)colsum - (uint64_t)(128 * cA) * m;
+    // with the witness fused (WIT): each entry also gives R, Rm, Y, Z and the
+    // bit word, and the tile's sums of the four claims at (r1, r2) and its
+    // range flag go to the tile's partial (claims.hpp); exact limb sums over
+    // groups of four entries, as in the standalone witness pass
+    uint64_t cacc[4] = {0, 0, 0, 0};
+    int oor = 0;
+    const uint64_t e2 = (WIT && col < k) ? we.E2[col] : 0;
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-        const uint32_t lrow = 32 * wr + 8 * (r / 4) + 4 * half + (r % 4), row = i0 + lrow;
-        if (row < n && col < k) {
-            uint64_t c = corr + 128 * (uint64_t)s_rs[lrow];
+    for (int r0 = 0; r0 < 16; r0 += 4) {
+        uint64_t el[4], eh[4];
+        int32_t vr[4], vrm[4], vy[4], vz[4];
 #pragma unroll
-            for (int w = 0; w < NACC; w++) {
-                const int wt = LA == 2 ? (w >> 1) + (w & 1) : w;  // weight 256^wt
-                c += (uint64_t)(int64_t)acc[w][r] << (8 * wt);
+        for (int i = 0; i < 4; i++) {
+            const int r = r0 + i;
+            const uint32_t lrow = 32 * wr + 8 * (r / 4) + 4 * half + (r % 4), row = i0 + lrow;
+            el[i] = eh[i] = 0;
+            vr[i] = vrm[i] = vy[i] = vz[i] = 0;
+            if (row < n && col < k) {
+                uint64_t c = corr + 128 * (uint64_t)s_rs[lrow];
+#pragma unroll
+                for (int w = 0; w < NACC; w++) {
+                    const int wt = LA == 2 ? (w >> 1) + (w & 1) : w;  // weight 256^wt
+                    c += (uint64_t)(int64_t)acc[w][r] << (8 * wt);
+                }
+                const size_t x = (size_t)row * k + col;
+                C[x] = (int64_t)c;
+                if (WIT) {
+                    const WitOut o = witness_entry((int64_t)c, we.s, we.t, we.relu, we.half, oor);
+                    we.R[x] = o.r;
+                    we.Rm[x] = (uint16_t)o.rm;
+                    we.Y[x] = o.y;
+                    we.Z[x] = o.z;
+                    we.bits[x] = o.w;
+                    const uint64_t e = m61::lmul(we.E1[row], e2);
+                    el[i] = e & 0x7FFFFFFFull;
+                    eh[i] = e >> 31;
+                    vr[i] = o.r;
+                    vrm[i] = o.rm;
+                    vy[i] = o.y;
+                    vz[i] = o.z;
+                }
             }
-            C[(size_t)row * k + col] = (int64_t)c;
+        }
+        if (WIT) {
+            cacc[0] = m61::fold(cacc[0] + claim_terms<4>(el, eh, vr));
+            cacc[1] = m61::fold(cacc[1] + claim_terms<4>(el, eh, vrm));
+            cacc[2] = m61::fold(cacc[2] + claim_terms<4>(el, eh, vy));
+            cacc[3] = m61::fold(cacc[3] + claim_terms<4>(el, eh, vz));
+        }
+    }
+    if (WIT) {  // the stage area is free: every wave has passed the barrier above
+        const int any = __syncthreads_or(oor);
+        m61::block_sum<4>(cacc, (uint64_t *)&stage[0][0][0]);
+        if (tid == 0) {
+#pragma unroll
+            for (int q = 0; q < 4; q++) we.claim_part[4 * (size_t)blockIdx.x + q] = cacc[q];
+            we.flags[blockIdx.x] = (uint32_t)any;
         }
     }
 }
@@ -654,8 +703,11 @@ void launch_front(const void *A, int a_is_i32, const int16_t *B, uint32_t n, uin
     else hipLaunchKernelGGL((k_front<int16_t, 2>), grid, dim3(256), 0, st, f);
 }
 
+uint32_t gemm_tiles(uint32_t n, uint32_t k) { return (round_up64(k) / kTile) * (round_up64(n) / kTile); }
+
 void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C, uint32_t n, uint32_t m, uint32_t k,
-                      void *ws, hipStream_t st, const TailArgs *ta, const XJobs *jobs, bool split_done)
+                      void *ws, hipStream_t st, const TailArgs *ta, const XJobs *jobs, bool split_done,
+                      const WitEpi *we)
 {
     const uint32_t np = round_up64(n), mp = round_up64(m), kp = round_up64(k);
     const int LA = a_is_i32 ? 4 : 2, ntiles = (int)(mp / 64);
@@ -676,14 +728,20 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
     const dim3 grid((kp / kTile) * (np / kTile) + extra);
     const TailArgs &tav = ta ? *ta : tnone;
     const XJobs &jv = ta ? *jobs : jnone;
-    if (a_is_i32)
-        hipLaunchKernelGGL((k_gemm_mfma<4, gemm_stages<4>()>), grid, dim3(256), 0, st, (const int8_t *)w.Al,
-                           (const int8_t *)w.Bt, (const int64_t *)w.rowsum, (const int64_t *)w.colpart, ntiles,
-                           (int64_t)8421504, n, m, k, np, mp, kp, C, tav, jv);
-    else
-        hipLaunchKernelGGL((k_gemm_mfma<2, gemm_stages<2>()>), grid, dim3(256), 0, st, (const int8_t *)w.Al,
-                           (const int8_t *)w.Bt, (const int64_t *)w.rowsum, (const int64_t *)w.colpart, ntiles,
-                           (int64_t)128, n, m, k, np, mp, kp, C, tav, jv);
+    const WitEpi wnone{};
+    const WitEpi &wv = we ? *we : wnone;
+#define RA_GEMM(LAV, CA, W)                                                                                        \
+    hipLaunchKernelGGL((k_gemm_mfma<LAV, gemm_stages<LAV>(), W>), grid, dim3(256), 0, st, (const int8_t *)w.Al,    \
+                       (const int8_t *)w.Bt, (const int64_t *)w.rowsum, (const int64_t *)w.colpart, ntiles,        \
+                       (int64_t)(CA), n, m, k, np, mp, kp, C, tav, jv, wv)
+    if (a_is_i32) {
+        if (we) RA_GEMM(4, 8421504, true);
+        else RA_GEMM(4, 8421504, false);
+    } else {
+        if (we) RA_GEMM(2, 128, true);
+        else RA_GEMM(2, 128, false);
+    }
+#undef RA_GEMM
 }
 
 }  // namespace ra

@@ -348,24 +348,6 @@ __global__ __launch_bounds__(256) void k_wit_params(const int64_t *__restrict__ 
 // With t given (known != 0) the parameters come by value and every workgroup
 // also flags, in flags[block], whether one of its R lies outside the range;
 // the final kernel turns the flags into the status.
-// Claims of V outputs (consecutive x): sum_i e_i z_i for e_i = E1[row] E2[col]
-// (folded, < 2^61 + 8) and integers |z_i| <= 2^30 (R, Y, Z fit t <= 29; a
-// value outside the given range makes the call fail, its claims unused).
-// Each e_i is cut as e_hi 2^31 + e_lo, the two sums are exact in int64 (four
-// terms below 2^61 each), then reduced mod p once.
-template <int V>
-__device__ __forceinline__ uint64_t claim_terms(const uint64_t (&el)[V], const uint64_t (&eh)[V],
-                                                const int32_t (&z)[V])
-{
-    uint64_t lo = 0, hi = 0;  // two's complement sums (exact for |z| <= 2^30)
-#pragma unroll
-    for (int i = 0; i < V; i++) {
-        lo += (uint64_t)((int64_t)el[i] * z[i]);
-        hi += (uint64_t)((int64_t)eh[i] * z[i]);
-    }
-    return m61::fold(m61::from_i64((int64_t)lo) + m61::rotl(m61::from_i64((int64_t)hi), 31));
-}
-
 // Blocks of the rescale pass: V = 4 outputs per thread, one pass over N for
 // up to kMaxBlocks blocks (never more blocks than witness_blocks(N)).
 static int rescale_blocks(uint64_t N)
@@ -399,7 +381,6 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
     if (p.status != 0) return;  // uniform over the grid
     const int s = p.s, t = p.t, relu = p.relu;
     const int64_t half = p.mode == RA_ROUND_NEAREST ? (int64_t)1 << (s - 1) : 0;
-    const int64_t shift_r = (int64_t)1 << (t + 1);
     const uint64_t kmask = (1ull << lk) - 1;
     uint64_t acc[4] = {0, 0, 0, 0};
     int out_of_range = 0;
@@ -428,16 +409,12 @@ __global__ __launch_bounds__(256) void k_rescale(const int64_t *__restrict__ C, 
         uint64_t w[V];
 #pragma unroll
         for (int i = 0; i < V; i++) {
-            const int64_t cc = c[i] + half;
-            const int64_t q = cc >> s;
-            // u = R for R >= 0, -R - 1 for R < 0; R in [-2^(t+1), 2^(t+1)) iff u < 2^(t+1)
-            out_of_range |= ((uint64_t)(q >= 0 ? q : -(q + 1)) >> (t + 1)) != 0;
-            rm[i] = (int32_t)(cc - (q << s));
-            r[i] = (int32_t)q;
-            y[i] = r[i] < 0 ? -r[i] : r[i];
-            z[i] = relu ? (r[i] > 0 ? r[i] : 0) : r[i];
-            w[i] = (uint64_t)rm[i] | ((uint64_t)(q + shift_r) << s);
-            if (relu) w[i] |= (uint64_t)y[i] << (s + t + 2);
+            const WitOut o = witness_entry(c[i], s, t, relu, half, out_of_range);
+            r[i] = o.r;
+            rm[i] = o.rm;
+            y[i] = o.y;
+            z[i] = o.z;
+            w[i] = o.w;
         }
         if constexpr (V == 4) {
             *(v4i_t *)&R[x0] = v4i_t{r[0], r[1], r[2], r[3]};

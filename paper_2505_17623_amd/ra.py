@@ -25,7 +25,7 @@ STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_
           -8: "RA_E_BUFSIZE", -9: "RA_E_NOMEM"}
 EXPORTS = ["ra_ctx_create", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str", "ra_ctx_set_profiling",
            "ra_ctx_profile", "ra_ctx_set_deferred", "ra_ctx_sync", "ra_mle_bind",
-           "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify"]
+           "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify", "ra_witness_plan"]
 
 
 class RAError(RuntimeError):
@@ -96,6 +96,8 @@ def lib():
                                                ctypes.c_uint32, vp, ctypes.POINTER(MatmulProof)]
         L.ra_rescale_relu_witness.argtypes = [vp, vp, ctypes.c_uint32, ctypes.c_uint32, vp, vp, vp, vp, vp,
                                               u64, ctypes.POINTER(WitnessInfo)]
+        L.ra_witness_plan.argtypes = [vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int32, vp, vp,
+                                      vp, vp, vp, u64]
         L.ra_range_prove.argtypes = [vp, vp, vp, vp, ctypes.c_uint32, ctypes.c_uint32,
                                      ctypes.POINTER(WitnessInfo), ctypes.POINTER(RangeProof)]
         L.ra_verify.argtypes = [u64, u64p, u64, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
@@ -104,7 +106,7 @@ def lib():
         for f in (L.ra_ctx_create, L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
-                  L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify):
+                  L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify, L.ra_witness_plan):
             f.restype = ctypes.c_int32
         _lib = L
     return _lib
@@ -258,6 +260,14 @@ def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, m
     return (R, Rm, Y, Z, bits), info
 
 
+def ra_witness_plan(ctx: Context, s: int, relu: bool, mode: int, t: int, outs):
+    """Announce the next witness call (given t, output tensors as made by
+    witness_outputs) so that the next matrix call computes it in its product."""
+    R, Rm, Y, Z, bits = outs
+    _check(lib().ra_witness_plan(ctx.h, s, int(bool(relu)), mode, t, _dptr(R), _dptr(Rm), _dptr(Y), _dptr(Z),
+                                 _dptr(bits), bits.numel()), "ra_witness_plan")
+
+
 def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
     """Returns the range / ReLU transcript dict (filled at ctx.sync() in deferred mode)."""
     n, k = R.shape
@@ -279,19 +289,24 @@ def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
 
 
 def prove_layer(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1,
-                bufs: dict | None = None):
+                bufs: dict | None = None, plan: bool = True):
     """The three calls of one layer; returns device tensors and the transcript
     (complete at once, or after ctx.sync() in deferred mode).  bufs (optional):
     a dict that keeps the layer's device outputs, made on first use and
     written again by later calls with it (a caller proving the same shapes
-    repeatedly saves the allocations)."""
+    repeatedly saves the allocations).  With t given and plan set, the
+    witness is announced (ra_witness_plan) and computed inside the product."""
     n, k = A.shape[0], B.shape[1]
     if bufs is not None and "C" not in bufs:
         bufs["C"] = torch.empty((n, k), dtype=torch.int64, device=A.device)
         bufs["wit"] = witness_outputs(n, k, A.device)
+    wit = None if bufs is None else bufs["wit"]
+    if t >= 0 and plan:  # t given: the witness is announced and computed inside the product
+        if wit is None:
+            wit = witness_outputs(n, k, A.device)
+        ra_witness_plan(ctx, s, relu, mode, t, wit)
     C, mm = ra_sumcheck_matmul_prove(ctx, A, B, None if bufs is None else bufs["C"])
-    (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t,
-                                                        None if bufs is None else bufs["wit"])
+    (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t, wit)
     rs = ra_range_prove(ctx, bits, R, Y, info)
     tr = {}
 
@@ -308,7 +323,7 @@ def to_device(a: np.ndarray, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
-def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None):
+def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, plan=True):
     """Prove every layer of a workload in order.  A layer's input is the
     previous output on the device (MLP chains) or the workload's link (im2col)
     applied on the host.  X / Bs may hold device copies of the inputs; ts may
@@ -331,7 +346,7 @@ def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=Non
             A = to_device(workload.links[li](Z.cpu().numpy()), device)
         t = -1 if ts is None else int(ts[li])
         res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t,
-                          None if bufs is None else bufs[li])
+                          None if bufs is None else bufs[li], plan)
         res["A"] = A
         Z = res["Z"]
         outs.append(res)

@@ -30,14 +30,24 @@ def digest_i64(a) -> str:
     return digest(np.asarray(a).astype("<i8"))
 
 
+@pytest.mark.parametrize("mode", ["sync", "bench"])
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
-def test_full_workload_matches_oracle(cfg):
+def test_full_workload_matches_oracle(cfg, mode):
+    """sync: each call waits, t is derived from the data.  bench: the launch
+    configuration bench.py times -- deferred outputs, each layer's t given
+    (so the witness is announced and computed inside the product), output
+    buffers kept across steps, one sync."""
     from paper_2505_17623_amd import ra
     path = os.path.join(GOLD, f"full_cfg{cfg}.json")
     gold = json.load(open(path))
     wl = inputs.workload(cfg, "full")
-    ctx = ra.Context(wl.challenges)
-    got = ra.prove_network(ctx, wl)
+    if mode == "sync":
+        ctx = ra.Context(wl.challenges)
+        got = ra.prove_network(ctx, wl)
+    else:
+        ctx = ra.Context(wl.challenges, deferred=True)
+        got = ra.prove_network(ctx, wl, ts=[o["transcript"]["t"] for o in gold["layers"]], bufs=[])
+        ctx.sync()
     assert len(got) == len(gold["layers"])
     used = 0
     for li, (g, o) in enumerate(zip(got, gold["layers"])):

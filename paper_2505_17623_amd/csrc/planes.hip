@@ -73,10 +73,11 @@ __device__ __forceinline__ uint64_t wave_transpose64(uint64_t a)
     return a;
 }
 
-// Balanced base-256 digits of e < 2^61: e = sum_t 256^t d_t, d_t in [-128, 128).
-// With f = e + sum_t 128 256^t (no overflow: e < 2^61), the plain bytes f_t
+// Balanced base-256 digits of e < 2^62: e = sum_t 256^t d_t, d_t in [-128, 128).
+// With f = e + sum_t 128 256^t (no overflow: e < 2^62), the plain bytes f_t
 // give d_t = f_t - 128, whose int8 bit pattern is f_t with the top bit flipped;
-// so the eight digit bytes are those of f xor 0x80...80.
+// so the eight digit bytes are those of f xor 0x80...80.  The digits add up to
+// e itself, so a folded (not canonical) e gives the same G modulo p.
 __device__ __forceinline__ uint64_t balanced_digit_bytes(uint64_t e)
 {
     constexpr uint64_t kHalf = 0x8080808080808080ull;
@@ -124,6 +125,17 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const uint64_t kmask = (1ull << lk) - 1;
     const uint64_t nslabs = (N + kSlab - 1) / kSlab;
     const uint64_t mine = nslabs > blockIdx.x ? (nslabs - blockIdx.x + gridDim.x - 1) / gridDim.x : 0;
+    // a slab's global inputs are read one slab ahead; the first slab's before
+    // the byte tables are built
+    uint64_t pw = 0, pe1 = 0, pe2 = 0;
+    auto fetch = [&](uint64_t i) {
+        const uint64_t x = (blockIdx.x + i * gridDim.x) * kSlab + tid;
+        const bool valid = i < mine && x < N;
+        pw = valid ? bits[x] : 0;
+        pe1 = valid ? E1[x >> lk] : 0;
+        pe2 = valid ? E2[x & kmask] : 0;
+    };
+    if (producer) fetch(0);
     __syncthreads();
     // byte tables of Bx(x) = sum_q eq(sigma_p, q) bit_q(x): lut[b][v] = sum
     // over the set bits i of v of eq(sigma_p, 8 b + i)
@@ -138,22 +150,12 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     // The two roles run separate loops with the same barriers (one per slab),
     // so the consumers' accumulators are not live in the producers' code.
     if (producer) {
-        // a slab's global inputs are read one slab ahead
-        uint64_t pw = 0, pe1 = 0, pe2 = 0;
-        auto fetch = [&](uint64_t i) {
-            const uint64_t x = (blockIdx.x + i * gridDim.x) * kSlab + tid;
-            const bool valid = i < mine && x < N;
-            pw = valid ? bits[x] : 0;
-            pe1 = valid ? E1[x >> lk] : 0;
-            pe2 = valid ? E2[x & kmask] : 0;
-        };
-        fetch(0);
         for (uint64_t i = 0; i <= mine; i++) {
             if (i < mine) {  // build slab i into buffer i % 2
                 const int buf = (int)(i & 1);
                 const uint64_t x = (blockIdx.x + i * gridDim.x) * kSlab + tid;
                 const bool valid = x < N;
-                const uint64_t w = pw, eqx = m61::mul(pe1, pe2);
+                const uint64_t w = pw, eqx = m61::lmul(pe1, pe2);  // folded, < 2^61 + 8
                 fetch(i + 1);
                 uint64_t bx = 0;  // eight values below 2^61: the plain sum stays below 2^64
 #pragma unroll

@@ -327,15 +327,15 @@ static_assert(kXbLdsWords >= kJobLdsWords, "jobs share the workgroup's LDS");
 // their own value, unused).
 __device__ __forceinline__ uint64_t lane_down(uint64_t v, int h) { return __shfl_down(v, (unsigned)h, 64); }
 
-template <int B, bool ZW, bool RELU>
-__device__ __forceinline__ void xb_wave(const XBlockArgs &a, bool first, uint64_t k, uint64_t nsub,
-                                        const uint64_t *__restrict__ W, uint64_t *red)
+// The sub-cube of one wave: range t0 = Bx; ReLU t0 = D, t1 = S (from R, Y in
+// the first pass); all loads issued at once.
+template <int B, bool ZW>
+__device__ __forceinline__ void xb_load(const XBlockArgs &a, bool first, uint64_t k, uint64_t nsub,
+                                        uint64_t (&t0)[(1 << B) >= 64 ? (1 << B) / 64 : 1],
+                                        uint64_t (&t1)[(1 << B) >= 64 ? (1 << B) / 64 : 1])
 {
-    constexpr int S = 1 << B, NV = ZW ? 3 : 5, E = S >= 64 ? S / 64 : 1, NR = B > 0 ? B : 1;
+    constexpr int S = 1 << B, E = S >= 64 ? S / 64 : 1;
     const int lane = threadIdx.x & 63;
-    const uint64_t *rho = ZW ? a.rho_z : a.rho_a;
-    // the sub-cube: range t0 = Bx; ReLU t0 = D, t1 = S.  All loads issued first.
-    uint64_t t0[E], t1[E];
     if (!ZW) {
 #pragma unroll
         for (int e = 0; e < E; e++) {
@@ -364,10 +364,20 @@ __device__ __forceinline__ void xb_wave(const XBlockArgs &a, bool first, uint64_
             t1[e] = u < S ? a.s[k + (uint64_t)u * nsub] : 0;
         }
     }
+}
+
+// The B rounds of one wave over its sub-cube (t0, t1 from xb_load; W staged).
+template <int B, bool ZW, bool RELU>
+__device__ __forceinline__ void xb_wave(const XBlockArgs &a, uint64_t k, uint64_t nsub, const uint64_t *__restrict__ W,
+                                        uint64_t *red, uint64_t ek, uint64_t (&t0)[(1 << B) >= 64 ? (1 << B) / 64 : 1],
+                                        uint64_t (&t1)[(1 << B) >= 64 ? (1 << B) / 64 : 1])
+{
+    constexpr int S = 1 << B, NV = ZW ? 3 : 5, E = S >= 64 ? S / 64 : 1, NR = B > 0 ? B : 1;
+    const int lane = threadIdx.x & 63;
+    const uint64_t *rho = ZW ? a.rho_z : a.rho_a;
     uint64_t z[NR];
 #pragma unroll
     for (int c = 0; c < B; c++) z[c] = rho[c];
-    const uint64_t ek = suffix_weight(a.HS, a.LS, a.lN - a.j - B, a.L, k);  // loaded with the tables
     // round c's sums of this lane go to red[(c NV + q) kXbRedStride + lane]
 #pragma unroll
     for (int c = 0; c < B; c++) {
@@ -474,17 +484,26 @@ __global__ __launch_bounds__(256) void k_xblock(XBlockArgs a, int first, XJobs j
         x_job(jobs, blockIdx.x - nmain, smem);
         return;
     }
-    constexpr int S = 1 << B, PER = RELU ? 2 : 4;  // sub-cubes per workgroup
+    constexpr int S = 1 << B, PER = RELU ? 2 : 4, E = S >= 64 ? S / 64 : 1;  // sub-cubes per workgroup
     const int tid = threadIdx.x, wv = tid >> 6;
+    const uint64_t nsub = 1ull << (a.lS - B);
+    const uint64_t k = (uint64_t)blockIdx.x * PER + (RELU ? (wv >> 1) : wv);
+    const bool live = k < nsub, zw = RELU && (wv & 1);  // wave-uniform
+    // the wave's sub-cube and weight e_k are fetched while the window
+    // weights are staged: the two global latencies overlap
+    uint64_t t0[E], t1[E], ek = 0;
+    if (live) {
+        if (zw) xb_load<B, true>(a, first != 0, k, nsub, t0, t1);
+        else xb_load<B, false>(a, first != 0, k, nsub, t0, t1);
+        ek = suffix_weight(a.HS, a.LS, a.lN - a.j - B, a.L, k);
+    }
     uint64_t *W = smem;  // W[1 .. S), shared by the workgroup's sub-cubes
     for (int e = tid + 1; e < S; e += 256) W[e] = a.W[e];
     __syncthreads();
-    const uint64_t nsub = 1ull << (a.lS - B);
-    const uint64_t k = (uint64_t)blockIdx.x * PER + (RELU ? (wv >> 1) : wv);
-    if (k >= nsub) return;  // wave-uniform, after the only barrier
+    if (!live) return;  // after the only barrier
     uint64_t *red = smem + kXbMax + wv * kXbRedWords;
-    if (RELU && (wv & 1)) xb_wave<B, true, RELU>(a, first != 0, k, nsub, W, red);
-    else xb_wave<B, false, RELU>(a, first != 0, k, nsub, W, red);
+    if (zw) xb_wave<B, true, RELU>(a, k, nsub, W, red, ek, t0, t1);
+    else xb_wave<B, false, RELU>(a, k, nsub, W, red, ek, t0, t1);
 }
 
 void launch_xblock(bool relu, bool first, const XBlockArgs &a, const XJobs &jobs, hipStream_t st)

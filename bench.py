@@ -90,6 +90,9 @@ def group_work(shapes, planes):
         add("gemm_mfma", "mfma", 2 * n * m * k * LA * 2)
         add("bind_rows", "hbm", n * m * ab + 8 * m)
         add("bind_cols", "hbm", m * k * 2 + 8 * m)
+        # the fused front: both bindings read A and B once and write the eq
+        # tables (its limb split reads them again; that is the product's work)
+        add("matmul_front", "hbm", n * m * ab + m * k * 2 + 8 * (n + k))
         add("witness_minmax", "hbm", 8 * N)
         add("witness_rescale", "hbm", N * (8 + 4 + 2 + 4 + 4 + 8))  # C in; R, Rm, Y, Z, bits out
         # Gram matrix of the plane rounds: per output, tile pairs x 32 x 32 x 2 x 8 digits
@@ -118,7 +121,8 @@ def group_work(shapes, planes):
 
 
 # Kernel -> group, for hardware-counter summaries (rocprofv3 kernel names).
-KERNEL_GROUP = [("k_gemm_mfma", "gemm_mfma"), ("k_split", "gemm_mfma"), ("k_zero_i64", "gemm_mfma"),
+KERNEL_GROUP = [("k_front", "matmul_front"), ("k_gemm_mfma", "gemm_mfma"), ("k_split", "gemm_mfma"),
+                ("k_zero_i64", "gemm_mfma"),
                 ("k_bind_rows", "bind_rows"), ("k_sum_chunks", "bind_rows"), ("k_bind_cols", "bind_cols"),
                 ("k_minmax", "witness_minmax"), ("k_wit_params", "witness_minmax"),
                 ("k_rescale", "witness_rescale"), ("k_claims_final", "witness_rescale"),

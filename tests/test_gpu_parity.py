@@ -198,3 +198,24 @@ def test_matmul_extreme_values(ra, a_dtype, n, m, k):
     assert np.array_equal(C.cpu().numpy(), o["C"])
     for key in ("c0", "mm_evals", "a_star", "b_star"):
         assert mm[key] == o[key], key
+
+
+@pytest.mark.parametrize("a_dtype,n,m,k", [(np.int16, 4096, 128, 512), (np.int32, 4096, 64, 512),
+                                           (np.int32, 8192, 256, 64)])
+def test_product_many_tiles(ra, a_dtype, n, m, k):
+    """Products with more output tiles than compute units (the register-
+    streamed product kernel) at the edges of the limb split; C against the
+    exact integer product."""
+    rng = np.random.default_rng(n + m + k + 1)
+    info = np.iinfo(a_dtype)
+    A = rng.integers(info.min, info.max, size=(n, m), dtype=np.int64, endpoint=True).astype(a_dtype)
+    B = rng.integers(-32768, 32767, size=(m, k), dtype=np.int64, endpoint=True).astype(np.int16)
+    A[0, :] = info.min
+    B[:, 0] = -32768
+    A[1, :] = info.max
+    B[:, 1] = 32767
+    chal = inputs.xorshift64_stream(999 + n, 512)
+    ctx = ra.Context(chal)
+    C, _ = ra.ra_sumcheck_matmul_prove(ctx, torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
+    want = A.astype(np.int64) @ B.astype(np.int64)  # |C| < 2^53: exact in int64
+    assert np.array_equal(C.cpu().numpy(), want)

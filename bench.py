@@ -85,8 +85,12 @@ def group_work(shapes, planes):
 
     for (n, m, k, ab, _, relu), P in zip(shapes, planes):
         N = n * k
-        LA = 2 if ab == 2 else 4
-        # exact product on the matrix cores: LA x 2 int8 limb products of 2 n m k operations
+        # exact product on the matrix cores: LA x 2 int8 limb products of 2 n m k
+        # operations.  int32 activations are the previous layer's ReLU outputs,
+        # in [0, 2^24): their top limb plane is zero and the product skips it,
+        # so three limbs are counted (a tile that needs the fourth does more
+        # work than is counted here)
+        LA = 2 if ab == 2 else 3
         add("gemm_mfma", "mfma", 2 * n * m * k * LA * 2)
         add("bind_rows", "hbm", n * m * ab + 8 * m)
         add("bind_cols", "hbm", m * k * 2 + 8 * m)

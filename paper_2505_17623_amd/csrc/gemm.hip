@@ -75,16 +75,19 @@ __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel)
 
 // A (n x m) -> limb planes Al[u][np][mp] (zero padded) and rowsum(A).  One
 // wave per row; a lane takes 16 consecutive entries and writes 16 bytes per
-// limb: the low byte shifted by -128 (a xor of the sign bit), the top limb
-// as is.
+// limb: the lower limbs shifted by -128 (a xor of the sign bit), the top limb
+// as is.  For int32, rowlimb[row] = 3 when the row's top plane is all zero
+// (every entry in [0, 2^24), as the ReLU outputs of a layer are), else 4: a
+// product tile whose rows all have three limbs skips plane 3.
 template <typename TA, int LA>
 __device__ __forceinline__ void split_a_block(const TA *__restrict__ A, uint32_t n, uint32_t m, uint32_t np,
                                               uint32_t mp, int8_t *__restrict__ Al, int64_t *__restrict__ rowsum,
-                                              uint32_t blk)
+                                              int32_t *__restrict__ rowlimb, uint32_t blk)
 {
     const uint32_t row = blk * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= np) return;  // wave-uniform
+    uint32_t top = 0;       // OR of the top plane's words
     int64_t s = 0;
     for (uint32_t c = lane * 16; c < mp; c += 1024) {
         v4i out[LA];
@@ -140,6 +143,7 @@ __device__ __forceinline__ void split_a_block(const TA *__restrict__ A, uint32_t
 #pragma unroll
             for (int u = 0; u < LA; u++) out[u] = v4i{0, 0, 0, 0};
         }
+        top |= (uint32_t)(out[LA - 1][0] | out[LA - 1][1] | out[LA - 1][2] | out[LA - 1][3]);
 #pragma unroll
         for (int u = 0; u < LA; u++)
             *(v4i *)&Al[frag_off(u, row >> 5, c >> 5, np >> 5, mp >> 5) + 16 * frag_lane(row, c)] = out[u];
@@ -147,6 +151,11 @@ __device__ __forceinline__ void split_a_block(const TA *__restrict__ A, uint32_t
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
     if (lane == 0 && row < n) rowsum[row] = s;
+    if (LA == 4) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) top |= (uint32_t)__shfl_xor((int)top, off, 64);
+        if (lane == 0) rowlimb[row] = top ? 4 : 3;
+    }
 }
 
 // B (m x k) -> transposed limb planes Bt[v][kp][mp] (row j holds column j of
@@ -213,11 +222,12 @@ __device__ __forceinline__ void split_bt_block(const int16_t *__restrict__ B, ui
 template <typename TA, int LA>
 __global__ __launch_bounds__(256) void k_split(const TA *__restrict__ A, uint32_t n, uint32_t m, uint32_t np,
                                                uint32_t mp, int8_t *__restrict__ Al, int64_t *__restrict__ rowsum,
-                                               uint32_t na, const int16_t *__restrict__ B, uint32_t k, uint32_t kp,
+                                               int32_t *__restrict__ rowlimb, uint32_t na,
+                                               const int16_t *__restrict__ B, uint32_t k, uint32_t kp,
                                                int8_t *__restrict__ Bt, int64_t *__restrict__ colpart)
 {
     if (blockIdx.x < na) {
-        split_a_block<TA, LA>(A, n, m, np, mp, Al, rowsum, blockIdx.x);
+        split_a_block<TA, LA>(A, n, m, np, mp, Al, rowsum, rowlimb, blockIdx.x);
         return;
     }
     const uint32_t t = blockIdx.x - na, tx = kp / 64;
@@ -395,6 +405,7 @@ struct FrontArgs {
     uint32_t n, m, k, np, mp, kp;
     int8_t *Al;
     int64_t *rowsum;
+    int32_t *rowlimb;
     int8_t *Bt;
     int64_t *colpart;
     const uint64_t *r1, *r2;
@@ -429,7 +440,7 @@ __global__ __launch_bounds__(256) void k_front(FrontArgs f)
     }
     b -= f.n_sb;
     if (b < f.n_sa) {
-        split_a_block<TA, LA>((const TA *)f.A, f.n, f.m, f.np, f.mp, f.Al, f.rowsum, b);
+        split_a_block<TA, LA>((const TA *)f.A, f.n, f.m, f.np, f.mp, f.Al, f.rowsum, f.rowlimb, b);
         return;
     }
     b -= f.n_sa;
@@ -437,81 +448,38 @@ __global__ __launch_bounds__(256) void k_front(FrontArgs f)
     else front_eq(f.r2, f.lk, f.E2, b - f.n_e1, tab);
 }
 
-// 64 x 64 output tile per block; wave (wr, wc) owns the 32 x 32 sub-tile.
-// The k dimension goes in steps of 64 bytes through S LDS stages: every step
-// needs F = 2 (2 LA + 4) fragments (two 32-byte halves of A: LA limbs x 2
-// row blocks, and of B: 2 limbs x 2 column blocks), F / 4 per wave, fetched
-// straight into LDS (global_load_lds_dwordx4) S - 1 steps ahead.  Each limb
-// pair (u, v) has its own accumulator, so the MFMAs of a step do not wait on
-// each other.  Tiles are ordered so that the blocks on one XCD (block b runs
-// on XCD b mod 8) share columns of B.
-//
-// Workgroups past the last tile run the last rounds of the product's
-// sum-check instance (tail.hpp), which needs only the bound vectors, in the
-// stage area's LDS: the single-workgroup tail then runs beside the tiles
-// instead of after them.
-template <int LA, int S, bool WIT>
-__global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__ Al, const int8_t *__restrict__ Bt,
-                                                   const int64_t *__restrict__ rowsum,
-                                                   const int64_t *__restrict__ colpart, int ntiles, int64_t cA,
-                                                   uint32_t n, uint32_t m, uint32_t k, uint32_t np, uint32_t mp,
-                                                   uint32_t kp, int64_t *__restrict__ C, TailArgs ta, XJobs jobs,
-                                                   WitEpi we)
+// The k loop of one 64 x 64 tile: LE limb planes of A (LE <= LA; planes past
+// LE are zero for every row of the tile) and two of B.  Every step needs
+// F = 2 (2 LE + 4) fragments (two 32-byte halves of A: LE limbs x 2 row
+// blocks, and of B: 2 limbs x 2 column blocks), F / 4 per wave, fetched
+// straight into LDS (global_load_lds_dwordx4) S - 1 steps ahead.
+template <int LA, int LE, int S>
+__device__ __forceinline__ void gemm_loop(const int8_t *__restrict__ Al, const int8_t *__restrict__ Bt, uint32_t bi,
+                                          uint32_t bj, uint32_t nR, uint32_t nC, uint32_t nQ, uint32_t nS,
+                                          int8_t *stage0, v16i (&acc)[LA == 2 ? 4 : LA + 1])
 {
-    static_assert(m61::block_sum_words(4, 256) * 8 <= S * (2 * (2 * LA + 4)) * 1024, "claims sum in the stage area");
-    constexpr int F1 = 2 * LA + 4, F = 2 * F1, FW = F / 4;
+    constexpr int F1 = 2 * LE + 4, F = 2 * F1, FW = F / 4;
     static_assert(F % 4 == 0, "fragments per wave");
     static_assert(S >= 2, "a stage read while the next fills");
-    static_assert(kTailSmem * 8 <= S * F * 1024, "the tail fits the stage area");
-    __shared__ __attribute__((aligned(1024))) int8_t stage[S][F][1024];
-    __shared__ int64_t s_cs[4][kTile], s_rs[kTile];
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wr = wv >> 1, wc = wv & 1, half = lane >> 5;
-    const uint32_t nbi = np / kTile, nblk = nbi * (kp / kTile);
-    if (blockIdx.x >= nblk) {  // workgroup-uniform
-        tail_block<KIND_MATMUL>(ta, jobs, (int)(blockIdx.x - nblk), (uint64_t *)&stage[0][0][0]);
-        return;
-    }
-    uint32_t t = blockIdx.x;
-    if ((nblk & 7) == 0) t = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
-    const uint32_t bi = t % nbi, bj = t / nbi, i0 = bi * kTile, j0 = bj * kTile;
-    const uint32_t nR = np >> 5, nC = kp >> 5, nQ = mp >> 5, nS = mp >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wr = wv >> 1, wc = wv & 1;
     const int8_t *src[FW];
 #pragma unroll
     for (int e = 0; e < FW; e++) {
         const int f = FW * wv + e, kk = f / F1, f1 = f % F1;
-        src[e] = (f1 < 2 * LA ? Al + frag_off(f1 >> 1, 2 * bi + (f1 & 1), kk, nR, nQ)
-                              : Bt + frag_off((f1 - 2 * LA) >> 1, 2 * bj + ((f1 - 2 * LA) & 1), kk, nC, nQ)) +
+        src[e] = (f1 < 2 * LE ? Al + frag_off(f1 >> 1, 2 * bi + (f1 & 1), kk, nR, nQ)
+                              : Bt + frag_off((f1 - 2 * LE) >> 1, 2 * bj + ((f1 - 2 * LE) & 1), kk, nC, nQ)) +
                  16 * lane;
     }
     auto issue = [&](uint32_t q, int sl) {
 #pragma unroll
         for (int e = 0; e < FW; e++)
             __builtin_amdgcn_global_load_lds((const void *)(src[e] + (size_t)q * 2048),
-                                             (__attribute__((address_space(3))) void *)&stage[sl][FW * wv + e][0], 16,
-                                             0, 0);
+                                             (__attribute__((address_space(3))) void *)(stage0 +
+                                                                                        ((size_t)sl * F + FW * wv + e) *
+                                                                                            1024),
+                                             16, 0, 0);
     };
-    // column sums of this block's columns over all row tiles of B (wave w takes
-    // tiles w, w + 4, ...) and the row sums of its rows: loads issued first,
-    // values used after the loop
-    int64_t cs[4] = {0, 0, 0, 0}, rs = 0;
-    if (j0 + lane < k) {
-        int ti = wv;
-        for (; ti + 12 < ntiles; ti += 16)
-#pragma unroll
-            for (int q = 0; q < 4; q++) cs[q] += colpart[(size_t)(ti + 4 * q) * kp + j0 + lane];
-        for (; ti < ntiles; ti += 4) cs[0] += colpart[(size_t)ti * kp + j0 + lane];
-    }
-    if (tid < kTile && i0 + tid < n) rs = rowsum[i0 + tid];
-    // accumulators: int16 A, one per limb pair (index 2 u + v); int32 A, one per
-    // weight u + v (the step's MFMAs, in (k half, v, u) order, update each at
-    // most every third instruction)
-    constexpr int NACC = LA == 2 ? 4 : LA + 1;
-    v16i acc[NACC];
-#pragma unroll
-    for (int w = 0; w < NACC; w++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) acc[w][r] = 0;
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_i8 *)&stage[0][0][0] + 16 * lane;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_i8 *)stage0 + 16 * lane;
 #pragma unroll
     for (int q = 0; q < S - 1; q++)
         if ((uint32_t)q < nS) issue(q, q);
@@ -530,11 +498,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__
         // for all of them before any LDS read.  The second 32-byte half is
         // still being read while the first half's MFMAs run.
         const uint32_t sa = lds0 + (q % S) * (F * 1024) + 1024 * wr, sb = sa + 1024 * (wc - wr);
-        v4i a[2][LA], b[2][2];
+        v4i a[2][LE], b[2][2];
 #pragma unroll
         for (int kk = 0; kk < 2; kk++) {
 #pragma unroll
-            for (int u = 0; u < LA; u++)
+            for (int u = 0; u < LE; u++)
                 asm volatile("ds_read_b128 %0, %1 offset:%2"
                              : "=v"(a[kk][u])
                              : "v"(sa), "i"((kk * F1 + 2 * u) * 1024)
@@ -543,26 +511,94 @@ __global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__
             for (int v = 0; v < 2; v++)
                 asm volatile("ds_read_b128 %0, %1 offset:%2"
                              : "=v"(b[kk][v])
-                             : "v"(sb), "i"((kk * F1 + 2 * LA + 2 * v) * 1024)
+                             : "v"(sb), "i"((kk * F1 + 2 * LE + 2 * v) * 1024)
                              : "memory");
         }
 #pragma unroll
         for (int kk = 0; kk < 2; kk++) {
-            if (kk == 0) lds_wait<LA + 2, LA>(a[0], b[0]);
-            else lds_wait<0, LA>(a[1], b[1]);
+            if (kk == 0) lds_wait<LE + 2, LE>(a[0], b[0]);
+            else lds_wait<0, LE>(a[1], b[1]);
+            // limb pairs (u, v) in an order that puts at least two other MFMAs
+            // between two updates of one accumulator: int16 A has one
+            // accumulator per pair (2 u + v), int32 A one per weight u + v
 #pragma unroll
-            for (int v = 0; v < 2; v++)
-#pragma unroll
-                for (int u = 0; u < LA; u++) {
-                    const int w = LA == 2 ? 2 * u + v : u + v;
-                    acc[w] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[kk][u], b[kk][v], acc[w], 0, 0, 0);
-                }
+            for (int i = 0; i < 2 * LE; i++) {
+                const int u = LE == 3 ? (i < 3 ? i : i == 3 ? 2 : i - 4) : i % LE;
+                const int v = LE == 3 ? (i >= 3) : i / LE;
+                const int w = LA == 2 ? 2 * u + v : u + v;
+                acc[w] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[kk][u], b[kk][v], acc[w], 0, 0, 0);
+            }
         }
+    }
+}
+
+// 64 x 64 output tile per block; wave (wr, wc) owns the 32 x 32 sub-tile,
+// and each limb pair (u, v) accumulates apart, so the MFMAs of a step do not
+// wait on each other.  Tiles are ordered so that the blocks on one XCD
+// (block b runs on XCD b mod 8) share columns of B.  An int32 tile whose
+// rows' top planes are all zero (rowlimb) runs the loop over three planes.
+//
+// Workgroups past the last tile run the last rounds of the product's
+// sum-check instance (tail.hpp), which needs only the bound vectors, in the
+// stage area's LDS: the single-workgroup tail then runs beside the tiles
+// instead of after them.
+template <int LA, int S, bool WIT>
+__global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__ Al, const int8_t *__restrict__ Bt,
+                                                   const int64_t *__restrict__ rowsum,
+                                                   const int32_t *__restrict__ rowlimb,
+                                                   const int64_t *__restrict__ colpart, int ntiles, uint32_t n,
+                                                   uint32_t m, uint32_t k, uint32_t np, uint32_t mp, uint32_t kp,
+                                                   int64_t *__restrict__ C, TailArgs ta, XJobs jobs, WitEpi we)
+{
+    static_assert(m61::block_sum_words(4, 256) * 8 <= S * (2 * (2 * LA + 4)) * 1024, "claims sum in the stage area");
+    constexpr int F = 2 * (2 * LA + 4);
+    static_assert(kTailSmem * 8 <= S * F * 1024, "the tail fits the stage area");
+    __shared__ __attribute__((aligned(1024))) int8_t stage[S][F][1024];
+    __shared__ int64_t s_cs[4][kTile], s_rs[kTile];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wr = wv >> 1, wc = wv & 1, half = lane >> 5;
+    const uint32_t nbi = np / kTile, nblk = nbi * (kp / kTile);
+    if (blockIdx.x >= nblk) {  // workgroup-uniform
+        tail_block<KIND_MATMUL>(ta, jobs, (int)(blockIdx.x - nblk), (uint64_t *)&stage[0][0][0]);
+        return;
+    }
+    uint32_t t = blockIdx.x;
+    if ((nblk & 7) == 0) t = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
+    const uint32_t bi = t % nbi, bj = t / nbi, i0 = bi * kTile, j0 = bj * kTile;
+    const uint32_t nR = np >> 5, nC = kp >> 5, nQ = mp >> 5, nS = mp >> 6;
+    // column sums of this block's columns over all row tiles of B (wave w takes
+    // tiles w, w + 4, ...) and the row sums of its rows: loads issued first,
+    // values used after the loop
+    int64_t cs[4] = {0, 0, 0, 0}, rs = 0;
+    if (j0 + lane < k) {
+        int ti = wv;
+        for (; ti + 12 < ntiles; ti += 16)
+#pragma unroll
+            for (int q = 0; q < 4; q++) cs[q] += colpart[(size_t)(ti + 4 * q) * kp + j0 + lane];
+        for (; ti < ntiles; ti += 4) cs[0] += colpart[(size_t)ti * kp + j0 + lane];
+    }
+    if (tid < kTile && i0 + tid < n) rs = rowsum[i0 + tid];
+    // limbs of each row (int32 A): does any row of the tile need plane 3
+    int rl = 2;
+    if (LA == 4) rl = tid < kTile && i0 + tid < n ? rowlimb[i0 + tid] : 3;
+    // accumulators: int16 A, one per limb pair (index 2 u + v); int32 A, one per
+    // weight u + v
+    constexpr int NACC = LA == 2 ? 4 : LA + 1;
+    v16i acc[NACC];
+#pragma unroll
+    for (int w = 0; w < NACC; w++)
+#pragma unroll
+        for (int r = 0; r < 16; r++) acc[w][r] = 0;
+    if (LA == 4) {
+        if (__syncthreads_or(rl > 3)) gemm_loop<LA, LA, S>(Al, Bt, bi, bj, nR, nC, nQ, nS, &stage[0][0][0], acc);
+        else gemm_loop<LA, 3, S>(Al, Bt, bi, bj, nR, nC, nQ, nS, &stage[0][0][0], acc);
+    } else {
+        gemm_loop<LA, LA, S>(Al, Bt, bi, bj, nR, nC, nQ, nS, &stage[0][0][0], acc);
     }
     s_cs[wv][lane] = cs[0] + cs[1] + cs[2] + cs[3];
     if (tid < kTile) s_rs[tid] = rs;
     __syncthreads();
     // recombination in wrap-around 64-bit arithmetic: exact because C itself fits int64
+    constexpr int64_t cA = LA == 2 ? 128 : 128 + 128 * 256 + 128 * 65536;
     const int cl = 32 * wc + (lane & 31);
     const uint32_t col = j0 + cl;
     const int64_t colsum = s_cs[0][cl] + s_cs[1][cl] + s_cs[2][cl] + s_cs[3][cl];
@@ -632,12 +668,13 @@ size_t gemm_workspace_bytes(int a_is_i32, uint32_t n, uint32_t m, uint32_t k)
 {
     const size_t np = round_up64(n), mp = round_up64(m), kp = round_up64(k);
     const int LA = a_is_i32 ? 4 : 2;
-    return LA * np * mp + 2 * kp * mp + 8 * (size_t)n + 8 * (mp / 64) * kp + 3 * 256;
+    return LA * np * mp + 2 * kp * mp + 8 * (size_t)n + 4 * (size_t)np + 8 * (mp / 64) * kp + 4 * 256;
 }
 
 struct GemmWs {
     int8_t *Al, *Bt;
     int64_t *rowsum, *colpart;
+    int32_t *rowlimb;
 };
 
 static GemmWs gemm_ws(void *ws, int LA, uint32_t n, uint32_t np, uint32_t mp, uint32_t kp)
@@ -650,6 +687,8 @@ static GemmWs gemm_ws(void *ws, int LA, uint32_t n, uint32_t np, uint32_t mp, ui
     p += ((size_t)2 * kp * mp + 255) & ~(size_t)255;
     w.rowsum = (int64_t *)p;
     p += ((size_t)8 * n + 255) & ~(size_t)255;
+    w.rowlimb = (int32_t *)p;
+    p += ((size_t)4 * np + 255) & ~(size_t)255;
     w.colpart = (int64_t *)p;
     return w;
 }
@@ -680,6 +719,7 @@ void launch_front(const void *A, int a_is_i32, const int16_t *B, uint32_t n, uin
     f.kp = kp;
     f.Al = w.Al;
     f.rowsum = w.rowsum;
+    f.rowlimb = w.rowlimb;
     f.Bt = w.Bt;
     f.colpart = w.colpart;
     f.r1 = r1;
@@ -716,10 +756,10 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
     if (!split_done) {
         if (a_is_i32)
             hipLaunchKernelGGL((k_split<int32_t, 4>), dim3(na + nb), dim3(256), 0, st, (const int32_t *)A, n, m, np,
-                               mp, w.Al, w.rowsum, na, B, k, kp, w.Bt, w.colpart);
+                               mp, w.Al, w.rowsum, w.rowlimb, na, B, k, kp, w.Bt, w.colpart);
         else
             hipLaunchKernelGGL((k_split<int16_t, 2>), dim3(na + nb), dim3(256), 0, st, (const int16_t *)A, n, m, np,
-                               mp, w.Al, w.rowsum, na, B, k, kp, w.Bt, w.colpart);
+                               mp, w.Al, w.rowsum, w.rowlimb, na, B, k, kp, w.Bt, w.colpart);
     }
     // tail workgroups (and the slot assemblies they bring) after the tiles
     const TailArgs tnone{};
@@ -730,16 +770,16 @@ void launch_gemm_mfma(const void *A, int a_is_i32, const int16_t *B, int64_t *C,
     const XJobs &jv = ta ? *jobs : jnone;
     const WitEpi wnone{};
     const WitEpi &wv = we ? *we : wnone;
-#define RA_GEMM(LAV, CA, W)                                                                                        \
+#define RA_GEMM(LAV, W)                                                                                            \
     hipLaunchKernelGGL((k_gemm_mfma<LAV, gemm_stages<LAV>(), W>), grid, dim3(256), 0, st, (const int8_t *)w.Al,    \
-                       (const int8_t *)w.Bt, (const int64_t *)w.rowsum, (const int64_t *)w.colpart, ntiles,        \
-                       (int64_t)(CA), n, m, k, np, mp, kp, C, tav, jv, wv)
+                       (const int8_t *)w.Bt, (const int64_t *)w.rowsum, (const int32_t *)w.rowlimb,                \
+                       (const int64_t *)w.colpart, ntiles, n, m, k, np, mp, kp, C, tav, jv, wv)
     if (a_is_i32) {
-        if (we) RA_GEMM(4, 8421504, true);
-        else RA_GEMM(4, 8421504, false);
+        if (we) RA_GEMM(4, true);
+        else RA_GEMM(4, false);
     } else {
-        if (we) RA_GEMM(2, 128, true);
-        else RA_GEMM(2, 128, false);
+        if (we) RA_GEMM(2, true);
+        else RA_GEMM(2, false);
     }
 #undef RA_GEMM
 }

@@ -203,9 +203,8 @@ def test_matmul_extreme_values(ra, a_dtype, n, m, k):
 @pytest.mark.parametrize("a_dtype,n,m,k", [(np.int16, 4096, 128, 512), (np.int32, 4096, 64, 512),
                                            (np.int32, 8192, 256, 64)])
 def test_product_many_tiles(ra, a_dtype, n, m, k):
-    """Products with more output tiles than compute units (the register-
-    streamed product kernel) at the edges of the limb split; C against the
-    exact integer product."""
+    """Products with more output tiles than compute units, at the edges of
+    the limb split; C against the exact integer product."""
     rng = np.random.default_rng(n + m + k + 1)
     info = np.iinfo(a_dtype)
     A = rng.integers(info.min, info.max, size=(n, m), dtype=np.int64, endpoint=True).astype(a_dtype)
@@ -218,4 +217,31 @@ def test_product_many_tiles(ra, a_dtype, n, m, k):
     ctx = ra.Context(chal)
     C, _ = ra.ra_sumcheck_matmul_prove(ctx, torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
     want = A.astype(np.int64) @ B.astype(np.int64)  # |C| < 2^53: exact in int64
+    assert np.array_equal(C.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("m", [32, 256])  # the split launch (m < 64) and the fused front
+def test_product_int32_top_plane(ra, m):
+    """int32 rows whose entries all lie in [0, 2^24) have a zero top limb
+    plane; a 64-row tile skips plane 3 only when all its rows do.  Tiles:
+    such rows only (with 0, 2^24 - 1 and a zero row), one entry 2^24, one
+    entry -1, and the full int32 range."""
+    n, k = 256, 128
+    rng = np.random.default_rng(7 + m)
+    hi = (1 << 24) - 1
+    A = rng.integers(0, hi, size=(n, m), dtype=np.int64, endpoint=True)
+    A[0, :] = 0
+    A[1, :] = hi
+    A[2, 0] = hi
+    A[64 + 5, 3] = 1 << 24
+    A[128 + 63, m - 1] = -1
+    A[192:, :] = rng.integers(-2 ** 31, 2 ** 31 - 1, size=(64, m), dtype=np.int64, endpoint=True)
+    A = A.astype(np.int32)
+    B = rng.integers(-32768, 32767, size=(m, k), dtype=np.int64, endpoint=True).astype(np.int16)
+    B[:, 0] = -32768
+    B[:, 1] = 32767
+    chal = inputs.xorshift64_stream(31 + m, 512)
+    ctx = ra.Context(chal)
+    C, _ = ra.ra_sumcheck_matmul_prove(ctx, torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
+    want = A.astype(np.int64) @ B.astype(np.int64)
     assert np.array_equal(C.cpu().numpy(), want)

@@ -48,8 +48,14 @@ template <int N, int LA>
 __device__ __forceinline__ void lds_wait(v4i (&a)[LA], v4i (&b)[2])
 {
     static_assert(N >= 0 && N < 16, "lgkmcnt field");
+    static_assert(LA >= 2 && LA <= 4, "limbs of A");
     if constexpr (LA == 2)
         asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]) : "i"(N) : "memory");
+    else if constexpr (LA == 3)
+        asm volatile("s_waitcnt lgkmcnt(%5)"
+                     : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(b[0]), "+v"(b[1])
+                     : "i"(N)
+                     : "memory");
     else
         asm volatile("s_waitcnt lgkmcnt(%6)"
                      : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1])

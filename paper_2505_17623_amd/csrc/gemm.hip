@@ -574,13 +574,25 @@ __global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__
     // column sums of this block's columns over all row tiles of B (wave w takes
     // tiles w, w + 4, ...) and the row sums of its rows: loads issued first,
     // values used after the loop
-    int64_t cs[4] = {0, 0, 0, 0}, rs = 0;
-    if (j0 + lane < k) {
-        int ti = wv;
-        for (; ti + 12 < ntiles; ti += 16)
+    // (up to 64 row tiles: every load is issued before any is waited for,
+    // one round trip in all; more tiles go through a loop)
+    constexpr int kColRegs = 16;
+    int64_t cs[4] = {0, 0, 0, 0}, rs = 0, cv[kColRegs];
+    const bool col_regs = ntiles <= 4 * kColRegs;
 #pragma unroll
-            for (int q = 0; q < 4; q++) cs[q] += colpart[(size_t)(ti + 4 * q) * kp + j0 + lane];
-        for (; ti < ntiles; ti += 4) cs[0] += colpart[(size_t)ti * kp + j0 + lane];
+    for (int e = 0; e < kColRegs; e++) cv[e] = 0;
+    if (j0 + lane < k) {
+        if (col_regs) {
+#pragma unroll
+            for (int e = 0; e < kColRegs; e++)
+                if (wv + 4 * e < ntiles) cv[e] = colpart[(size_t)(wv + 4 * e) * kp + j0 + lane];
+        } else {
+            int ti = wv;
+            for (; ti + 12 < ntiles; ti += 16)
+#pragma unroll
+                for (int q = 0; q < 4; q++) cs[q] += colpart[(size_t)(ti + 4 * q) * kp + j0 + lane];
+            for (; ti < ntiles; ti += 4) cs[0] += colpart[(size_t)ti * kp + j0 + lane];
+        }
     }
     if (tid < kTile && i0 + tid < n) rs = rowsum[i0 + tid];
     // limbs of each row (int32 A): does any row of the tile need plane 3
@@ -600,6 +612,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__
     } else {
         gemm_loop<LA, LA, S>(Al, Bt, bi, bj, nR, nC, nQ, nS, &stage[0][0][0], acc);
     }
+#pragma unroll
+    for (int e = 0; e < kColRegs; e++) cs[e & 3] += cv[e];
     s_cs[wv][lane] = cs[0] + cs[1] + cs[2] + cs[3];
     if (tid < kTile) s_rs[tid] = rs;
     __syncthreads();

@@ -41,12 +41,23 @@ __device__ __forceinline__ void rounds_body(const InstArgs &in, uint64_t sub, in
 #pragma unroll
     for (int i = 0; i < C * 4; i++) acc[i] = 0;
     for (uint64_t i = (uint64_t)blk * blockDim.x + threadIdx.x; i < sub; i += (uint64_t)nblk * blockDim.x) {
-        uint64_t v[3][L];
+        // every load before the accumulated table's clears (a store between
+        // the loads would keep the later loads behind it)
+        uint64_t v[3][L], vh[L];
 #pragma unroll
         for (int q = 0; q < NT; q++)
 #pragma unroll
-            for (int t = 0; t < L; t++)
-                v[q][t] = (q == 0 && in.acc) ? take_acc(in.acc, i + t * sub, sub << C) : T[q][i + t * sub];
+            for (int t = 0; t < L; t++) v[q][t] = (q == 0 && in.acc) ? in.acc[i + t * sub] : T[q][i + t * sub];
+        if (in.acc) {
+#pragma unroll
+            for (int t = 0; t < L; t++) vh[t] = in.acc[(sub << C) + i + t * sub];
+#pragma unroll
+            for (int t = 0; t < L; t++) {
+                in.acc[i + t * sub] = 0;
+                in.acc[(sub << C) + i + t * sub] = 0;
+                v[0][t] = acc_value(v[0][t], vh[t]);
+            }
+        }
 #pragma unroll
         for (int c = 0; c < C; c++) {
             const int h = L >> (c + 1);

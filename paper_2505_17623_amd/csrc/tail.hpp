@@ -26,14 +26,12 @@ __device__ __forceinline__ void pair_contrib(const uint64_t (&lo)[3], const uint
 }
 
 // Entry i of a row binding accumulated by the front launch over a table of
-// S entries: acc[i] holds the sum of the chunks' low 32 bits, acc[S + i] the
-// sum of their high bits, so the value is acc[i] + 2^32 acc[S + i] mod p.
-// The pair is cleared for the next call.  Canonical result.
-__device__ __forceinline__ uint64_t take_acc(uint64_t *acc, uint64_t i, uint64_t S)
+// S entries: lo = acc[i] holds the sum of the chunks' low 32 bits, hi =
+// acc[S + i] the sum of their high bits, and the value is lo + 2^32 hi mod p.
+// Readers clear both words for the next call, after all their loads.
+// Canonical result.
+__device__ __forceinline__ uint64_t acc_value(uint64_t lo, uint64_t hi)
 {
-    const uint64_t lo = acc[i], hi = acc[S + i];
-    acc[i] = 0;
-    acc[S + i] = 0;
     return m61::add(m61::canon(lo), m61::rotl(m61::canon(hi), 32));
 }
 
@@ -68,14 +66,23 @@ __device__ __forceinline__ void tail_block(const TailArgs &in, const XJobs &jobs
     const int tid = threadIdx.x, v = in.v, NI = blockDim.x;
     const int S = 1 << v;
     if (tid < v) rc[tid] = in.rho[tid];
-    for (int i0 = tid; i0 < S; i0 += 4 * NI) {  // loads first
-        uint64_t x[4], y[4];
+    for (int i0 = tid; i0 < S; i0 += 4 * NI) {  // loads first, then the clears of an accumulated table
+        uint64_t x[4], xh[4], y[4];
 #pragma unroll
         for (int q = 0; q < 4; q++) {
             const int i = i0 + q * NI;
-            x[q] = i < S ? (in.acc ? take_acc(in.acc, i, S) : in.t0[i]) : 0;
+            x[q] = i < S ? (in.acc ? in.acc[i] : in.t0[i]) : 0;
+            xh[q] = i < S && in.acc ? in.acc[S + i] : 0;
             y[q] = i < S ? in.t1[i] : 0;
         }
+        if (in.acc)
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+                if (i0 + q * NI < S) {
+                    in.acc[i0 + q * NI] = 0;
+                    in.acc[S + i0 + q * NI] = 0;
+                    x[q] = acc_value(x[q], xh[q]);
+                }
 #pragma unroll
         for (int q = 0; q < 4; q++)
             if (i0 + q * NI < S) {

@@ -100,6 +100,8 @@ SHAPES = [
     (1, 64, 8, 7, True, 0, 3000),       # fused front: one row, the narrowest B it takes
     (2048, 64, 8, 10, True, 0, 3000),   # fused front: eight row chunks of A accumulated
     (64, 2048, 16, 10, False, 1, 3000), # fused front feeding a global round (m beyond the LDS tail)
+    (4, 4096, 8, 8, True, 0, 3000),     # two global rounds reading the fused front's accumulators
+    (2, 8192, 8, 9, False, 1, 3000),    # three global rounds
 ]
 
 

@@ -21,8 +21,10 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kTile = 64;    // block tile (rows and columns)
-// LDS stages (k steps of 64) per block: 64 KB for int16 A, 72 KB for int32 A
-template <int LA> constexpr int gemm_stages() { return LA == 2 ? 4 : 3; }
+// LDS stages (k steps of 64) per block: 48 KB for int16 A (three blocks fit
+// a CU, so the matrix tail's workgroup runs beside two tiles per CU), 72 KB
+// for int32 A.  A fourth stage for int16 A was slower.
+template <int LA> constexpr int gemm_stages() { return 3; }
 
 __host__ __device__ inline uint32_t round_up64(uint32_t v) { return (v + 63u) & ~63u; }
 

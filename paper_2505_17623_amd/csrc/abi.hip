@@ -9,6 +9,7 @@
 
 #include "common.hpp"
 #include "ra.h"
+#include "xsetup.hpp"
 
 using namespace ra;
 
@@ -776,29 +777,38 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const uint64_t *sigx = sigma + lP, *rz = relu ? rho2 : nullptr;
     hipStream_t s = c->stream;
 
+    // With a register pass (reg > 0) the set-up of the rounds over x runs in
+    // the Gram pass (its consumer waves, while the first slab is built) and
+    // the Gram reduction, the constant block and a deferred witness step ride
+    // in the register pass's launch; the plane rounds are then evaluated one
+    // launch later.  Otherwise a launch of its own runs all of that between
+    // the Gram pass and the first x launch.
+    const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
+    const bool riding = reg > 0 && x_setup_count(xs) <= plane_gram_set_up_threads(N, lP);
+    const RangeConsts rc{lam, c->d_params, c->d_claims, lP, cst, tr + RS, c->pend_claims};
+    c->pend_claims.nblk = 0;  // taken by this call's launches
+    const RangeRiders riders{gpart, gblocks, gtiles, gtiles * 64, gsum, rc};
     {   // plane rounds: Gram matrix on the matrix cores, Bx per output
         Timed tm(c, G_RANGE_PLANE);
-        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, sigma, Bx, gpart, s);
+        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, sigma, Bx, gpart, riding ? &xs : nullptr, s);
     }
-    {   // the Gram matrix; further workgroups: the constant block and the x set-up
+    if (!riding) {  // the Gram matrix; further workgroups: the constant block and the x set-up
         Timed tm(c, G_RANGE_SETUP);
-        const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
-        const RangeConsts rc{lam, c->d_params, c->d_claims, lP, cst, tr + RS, c->pend_claims};
-        c->pend_claims.nblk = 0;  // taken by this launch
         launch_gram_reduce(lP, N, gpart, gsum, rc, xs, s);
     }
     // Each x launch's extra workgroups assemble the rounds of the launch
-    // before it; the first one also evaluates the plane rounds, the last
-    // assembles its own.
+    // before it; the first one also evaluates the plane rounds (the second
+    // one when the Gram reduction rides in the first), the last assembles
+    // its own.
     const XConst xc{cst + C_EP, c->d_r12, Kr, Kz};
     XJobs jobs{};
-    jobs.nplane = lP;
+    jobs.nplane = riding ? 0 : lP;
     jobs.stride = kPartStride;
     jobs.tr = tr;
     jobs.xc = xc;
     jobs.pa = PlaneArgs{gsum, sigma, cst, tr, lP};
     auto next_jobs = [&](int j0, int nr, int units) {
-        jobs.nplane = 0;
+        jobs.nplane = riding && j0 == 0 ? lP : 0;
         jobs.nslot = nr;
         jobs.part = part + (size_t)j0 * kPartStride;
         for (int r = 0; r < nr; r++)
@@ -811,7 +821,8 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
                        part + (size_t)j * kPartStride, lN, L, j};
         {
             Timed tm(c, G_RANGE_ROUNDS);
-            launch_xrounds(kXFuseMax, j == 0, relu != 0, xa, 1ull << lS, kPartStride, jobs, s);
+            launch_xrounds(kXFuseMax, j == 0, relu != 0, xa, 1ull << lS, kPartStride, jobs, s,
+                           riding && j == 0 ? &riders : nullptr);
         }
         next_jobs(j, kXFuseMax, xround_units(1ull << (lS - kXFuseMax), relu != 0));
     }

@@ -240,10 +240,21 @@ struct XJobs {
     Slot s[kXJobsMax];
 };
 int xround_units(uint64_t sub, bool relu);  // partial-sum producers of a register pass
+// Range-call work that rides in the first register pass's launch, after its
+// jobs: nred workgroups sum the Gram pass's partial tiles (gpart, nblk
+// blocks, TP tile pairs) into gsum, one writes the constant block (rc), and
+// with a deferred witness step (rc.cj.nblk > 0) one more sums its claims.
+struct RangeRiders {
+    const uint64_t *gpart;
+    int nblk, TP, nred;
+    uint64_t *gsum;
+    RangeConsts rc;
+};
+int range_riders(const RangeRiders &r);  // workgroups the riders take
 // C rounds per thread in registers over a table of S entries (sub-cube i:
 // entries i + t S / 2^C).
 void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, const XJobs &jobs,
-                    hipStream_t st);
+                    hipStream_t st, const RangeRiders *riders = nullptr);
 // B rounds per workgroup in LDS over a table of 2^lS entries: sub-cube k (one
 // workgroup) holds entries k + t 2^(lS - B).  With lS == B it is the last
 // pass: its rounds' evaluations go to tr and the bound values to fin_*.
@@ -266,10 +277,14 @@ void launch_xblock(bool relu, bool first, const XBlockArgs &a, const XJobs &jobs
 // ---- launchers (planes.hip) ----
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
+// threads of the Gram pass that can run the set-up of the rounds over x
+int plane_gram_set_up_threads(uint64_t N, int lP);
 // Bx per x and the blocks' partial Gram tiles (plane_gram_blocks x tiles x 1024
-// words); sig: sigma_p (lP words)
+// words); sig: sigma_p (lP words).  With xs (x_setup_count(*xs) at most
+// plane_gram_set_up_threads), the pass also runs the set-up of the rounds
+// over x, which depends on challenges only.
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, hipStream_t st);
+                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st);
 // the Gram matrix G (gsum: 64 x 64 words, both triangles) from the partial
 // tiles; further workgroups run the set-up of the range check (rc, xs)
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,

@@ -1,0 +1,50 @@
+// gram_reduce.hpp -- the sum of the Gram pass's per-block partial tiles
+// (plane rounds of the concatenated range check, Sec. III-B), shared by the
+// reduction launch and the extra workgroups of the first x-round launch that
+// run it beside the rounds.
+#pragma once
+#include "common.hpp"
+#include "m61.hpp"
+
+namespace ra {
+
+// Output fragment of v_mfma_i32_32x32x32_i8: lane l, register r holds
+// row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
+__host__ __device__ constexpr int frag_row(int l, int r) { return 8 * (r / 4) + 4 * (l / 32) + (r % 4); }
+
+// Tile pairs of the symmetric 64 x 64 Gram matrix: (0,0), (0,1), (1,1).
+__device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (tp == 2 ? 1 : 0); }
+__device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
+
+// Workgroup blk (256 threads) of the reduction: 16 entries of G, sixteen
+// lanes per entry (lane group g sums the partial tiles of blocks g, g + 16,
+// ...), then LDS; G[q][q'] is written in both triangles.
+constexpr int kGramReduceLdsWords = 16 * 17;
+__device__ __forceinline__ void gram_reduce_block(const uint64_t *__restrict__ gpart, int nblk, int TP,
+                                                  uint64_t *__restrict__ G, int blk, uint64_t *lds)
+{
+    uint64_t(*red)[17] = (uint64_t(*)[17])lds;
+    const int tid = threadIdx.x, el = tid & 15, g = tid >> 4, entries = TP * 1024;
+    const int e = blk * 16 + el;
+    uint64_t a = 0;
+    int b = g;
+    for (; b + 48 < nblk; b += 64) {  // four partials per iteration, loads first, one fold
+        const uint64_t v0 = gpart[(size_t)b * entries + e], v1 = gpart[(size_t)(b + 16) * entries + e];
+        const uint64_t v2 = gpart[(size_t)(b + 32) * entries + e], v3 = gpart[(size_t)(b + 48) * entries + e];
+        a = m61::fold(a + v0 + v1 + v2 + v3);
+    }
+    for (; b < nblk; b += 16) a = m61::fold(a + gpart[(size_t)b * entries + e]);
+    red[g][el] = a;
+    __syncthreads();
+    if (tid >= 16) return;
+    uint64_t v = 0;
+#pragma unroll
+    for (int q = 0; q < 16; q += 4) v = m61::fold(v + red[q][el] + red[q + 1][el] + red[q + 2][el] + red[q + 3][el]);
+    v = m61::canon(v);
+    const int tp = e >> 10, r = (e & 1023) >> 6, l = e & 63;
+    const int q = 32 * tile_row(tp, TP) + frag_row(l, r), q2 = 32 * tile_col(tp, TP) + (l & 31);
+    G[q * 64 + q2] = v;
+    G[q2 * 64 + q] = v;  // symmetric (the same value when the tile is diagonal)
+}
+
+}  // namespace ra

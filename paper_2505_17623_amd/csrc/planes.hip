@@ -19,6 +19,7 @@
 // (eight byte lookups per x), the input of the rounds over x.
 #include "common.hpp"
 #include "m61.hpp"
+#include "gram_reduce.hpp"
 #include "rsetup.hpp"
 
 namespace ra {
@@ -27,13 +28,6 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 constexpr int kLimbs = 8;    // balanced base-256 digits of a field element
 
-// Output fragment of v_mfma_i32_32x32x32_i8: lane l, register r holds
-// row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
-__host__ __device__ constexpr int frag_row(int l, int r) { return 8 * (r / 4) + 4 * (l / 32) + (r % 4); }
-
-// Tile pairs of the symmetric 64 x 64 Gram matrix: (0,0), (0,1), (1,1).
-__device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (tp == 2 ? 1 : 0); }
-__device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
 
 // Block layout of the Gram pass: sixteen waves with two roles, working on
 // slabs of kSlab outputs through a double-buffered LDS area.
@@ -44,7 +38,9 @@ __device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (
 //   consumers (waves 8-15, two per SIMD): wave c accumulates digit c for
 //     every tile pair over the slab's K-steps on the matrix cores.
 // While the consumers stream slab i the producers build slab i + 1; one
-// barrier per slab hands the buffers over.
+// barrier per slab hands the buffers over.  While the producers build the
+// first slab the consumers are free: with xs_on they run the set-up of the
+// range call's rounds over x (xsetup.hpp), one entry per consumer thread.
 constexpr int kSlab = 512;
 constexpr int kRow = kSlab + 16;  // bytes per plane row in LDS
 constexpr int kProducers = 8, kConsumers = 8, kGramThreads = 64 * (kProducers + kConsumers);
@@ -88,7 +84,7 @@ template <int TP>
 __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const uint64_t *__restrict__ bits, uint64_t N, int lk, const uint64_t *__restrict__ E1,
     const uint64_t *__restrict__ E2, const uint64_t *__restrict__ sig, int lP, uint64_t *__restrict__ Bx,
-    uint64_t *__restrict__ gpart)
+    uint64_t *__restrict__ gpart, int xs_on, XSetupArgs xs)
 {
     using S = GramShape<TP>;
     constexpr int NPL = S::kPlanes, DW = S::kDigitsPerWave, NPT = TP == 1 ? 1 : 2;
@@ -136,6 +132,15 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
         pe2 = valid ? E2[x & kmask] : 0;
     };
     if (producer) fetch(0);
+    // With xs_on the consumer waves also run the set-up of the rounds over x
+    // (it depends on challenges only) while the producers build the first
+    // slab; its challenges are staged here.
+    __shared__ uint64_t s_xr[64], s_xs[64], s_xz[64];
+    if (xs_on && tid < xs.lN) {
+        s_xr[tid] = xs.r[tid];
+        s_xs[tid] = xs.sigx[tid];
+        s_xz[tid] = xs.rho2 ? xs.rho2[tid] : 0;
+    }
     __syncthreads();
     // byte tables of Bx(x) = sum_q eq(sigma_p, q) bit_q(x): lut[b][v] = sum
     // over the set bits i of v of eq(sigma_p, 8 b + i)
@@ -180,6 +185,7 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
         __syncthreads();  // the consumers have cleared the tiles
         __syncthreads();  // and added their digits
     } else {
+        if (xs_on) x_setup_body(xs, blockIdx.x * (64 * kConsumers) + tid - 64 * kProducers, s_xr, s_xs, s_xz);
         v16i acc[DW][TP];
 #pragma unroll
         for (int k = 0; k < DW; k++)
@@ -273,31 +279,13 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict_
         range_consts_block(rc);
         return;
     }
-    __shared__ uint64_t red[16][17];
-    const int tid = threadIdx.x, el = tid & 15, g = tid >> 4, entries = TP * 1024;
-    const int e = blockIdx.x * 16 + el;
-    uint64_t a = 0;
-    int b = g;
-    for (; b + 48 < nblk; b += 64) {  // four partials per iteration, loads first, one fold
-        const uint64_t v0 = gpart[(size_t)b * entries + e], v1 = gpart[(size_t)(b + 16) * entries + e];
-        const uint64_t v2 = gpart[(size_t)(b + 32) * entries + e], v3 = gpart[(size_t)(b + 48) * entries + e];
-        a = m61::fold(a + v0 + v1 + v2 + v3);
-    }
-    for (; b < nblk; b += 16) a = m61::fold(a + gpart[(size_t)b * entries + e]);
-    red[g][el] = a;
-    __syncthreads();
-    if (tid >= 16) return;
-    uint64_t v = 0;
-#pragma unroll
-    for (int q = 0; q < 16; q += 4) v = m61::fold(v + red[q][el] + red[q + 1][el] + red[q + 2][el] + red[q + 3][el]);
-    v = m61::canon(v);
-    const int tp = e >> 10, r = (e & 1023) >> 6, l = e & 63;
-    const int q = 32 * tile_row(tp, TP) + frag_row(l, r), q2 = 32 * tile_col(tp, TP) + (l & 31);
-    G[q * 64 + q2] = v;
-    G[q2 * 64 + q] = v;  // symmetric (the same value when the tile is diagonal)
+    __shared__ uint64_t red[kGramReduceLdsWords];
+    gram_reduce_block(gpart, nblk, TP, G, blockIdx.x, red);
 }
 
 int plane_gram_tiles(int lP) { return lP > 5 ? 3 : 1; }
+
+int plane_gram_set_up_threads(uint64_t N, int lP) { return plane_gram_blocks(N, lP) * 64 * kConsumers; }
 
 int plane_gram_blocks(uint64_t N, int lP)
 {
@@ -307,15 +295,17 @@ int plane_gram_blocks(uint64_t N, int lP)
 }
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, hipStream_t st)
+                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st)
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
+    const XSetupArgs none{};
+    const XSetupArgs &x = xs ? *xs : none;
     if (TP == 1)
         hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
-                           gpart);
+                           gpart, xs ? 1 : 0, x);
     else
         hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
-                           gpart);
+                           gpart, xs ? 1 : 0, x);
 }
 
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,

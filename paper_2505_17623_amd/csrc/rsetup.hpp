@@ -60,31 +60,35 @@ __device__ __forceinline__ uint64_t range_claimed_sum(const uint64_t *lam, uint6
 
 // A deferred witness call's last step (claims.hpp) and, from its claims,
 // the claimed sum of the range instance; one workgroup of 256 threads.
-__device__ __forceinline__ void witness_claims_block(const RangeConsts &rc)
+constexpr int kClaimsLdsWords = m61::block_sum_words(4, 256) + 12;
+__device__ __forceinline__ void witness_claims_block(const RangeConsts &rc, uint64_t *lds)
 {
-    __shared__ uint64_t red[m61::block_sum_words(4, 256)];
-    __shared__ uint64_t wres[12];
+    uint64_t *red = lds, *wres = lds + m61::block_sum_words(4, 256);
     claims_final_block(rc.cj, red, wres);
     if (threadIdx.x == 0) {
         const uint64_t lam[3] = {rc.chal[0], rc.chal[1], rc.chal[2]};
         *rc.range_sum = range_claimed_sum(lam, rc.chal[3], wres + 8, rc.cj.hp.t, rc.cj.hp.relu);
     }
 }
+__device__ __forceinline__ void witness_claims_block(const RangeConsts &rc)
+{
+    __shared__ uint64_t lds[kClaimsLdsWords];
+    witness_claims_block(rc, lds);
+}
 
 // The constant block of the plane rounds (one workgroup of at least 256
 // threads); chal points at lambda1: lambda1..3, mu, tau_p (lP), sigma
 // (lP + ...).  Every operand is first staged in LDS.
-__device__ __forceinline__ void range_consts_block(const RangeConsts &rc)
+constexpr int kConstsLdsWords = C_WORDS + kMaxPlaneLog + 4 + 2 * kMaxPlaneLog + 3 + 2;
+__device__ __forceinline__ void range_consts_block(const RangeConsts &rc, uint64_t *lds)
 {
     const uint64_t *chal = rc.chal, *claims = rc.claims;
     const WitParams *prm = rc.prm;
     const int lP = rc.lP, tid = threadIdx.x;
     uint64_t *cst = rc.cst, *range_sum = rc.range_sum;
     using namespace m61;
-    __shared__ uint64_t c[C_WORDS];
-    __shared__ uint64_t eqt[kMaxPlaneLog];
-    __shared__ uint64_t ch[4 + 2 * kMaxPlaneLog], cl[3];
-    __shared__ int pv[3];
+    uint64_t *c = lds, *eqt = c + C_WORDS, *ch = eqt + kMaxPlaneLog, *cl = ch + 4 + 2 * kMaxPlaneLog;
+    int *pv = (int *)(cl + 3);
     const int P = 1 << lP;
     // with the witness's last step deferred (t given), the parameters are the
     // job's and the claimed sum is left to witness_claims_block
@@ -151,6 +155,11 @@ __device__ __forceinline__ void range_consts_block(const RangeConsts &rc)
     }
     __syncthreads();
     for (int i = tid; i < C_WORDS; i += blockDim.x) cst[i] = c[i];
+}
+__device__ __forceinline__ void range_consts_block(const RangeConsts &rc)
+{
+    __shared__ uint64_t lds[kConstsLdsWords];
+    range_consts_block(rc, lds);
 }
 
 }  // namespace ra

@@ -30,6 +30,8 @@
 
 #include "assemble.hpp"
 #include "common.hpp"
+#include "gram_reduce.hpp"
+#include "rsetup.hpp"
 #include "m61.hpp"
 #include "plane_round.hpp"
 
@@ -221,12 +223,20 @@ constexpr int xrounds_lds_words()
 
 // Workgroups below nmain run the rounds; the others are jobs.
 template <int C, bool FIRST, bool RELU>
-__global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stride, XJobs jobs, int nmain)
+__global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stride, XJobs jobs, int nmain,
+                                                 RangeRiders rr)
 {
     constexpr int NPB = RELU ? 128 : 256, NVR = 5 * C;
     __shared__ uint64_t smem[xrounds_lds_words<C>()];
-    if ((int)blockIdx.x >= nmain) {
-        x_job(jobs, blockIdx.x - nmain, smem);
+    static_assert(xrounds_lds_words<C>() >= kGramReduceLdsWords && xrounds_lds_words<C>() >= kConstsLdsWords &&
+                      xrounds_lds_words<C>() >= kClaimsLdsWords,
+                  "the riders work in the rounds' LDS");
+    if ((int)blockIdx.x >= nmain) {  // workgroup-uniform
+        const int q = blockIdx.x - nmain, nj = jobs.nslot + jobs.nplane;
+        if (q < nj) x_job(jobs, q, smem);
+        else if (q - nj < rr.nred) gram_reduce_block(rr.gpart, rr.nblk, rr.TP, rr.gsum, q - nj, smem);
+        else if (q - nj == rr.nred) range_consts_block(rr.rc, smem);
+        else witness_claims_block(rr.rc, smem);
         return;
     }
     uint64_t *tot = smem + 4 * NVR * 68;
@@ -273,13 +283,17 @@ static int xround_blocks(uint64_t sub, bool relu)
 
 int xround_units(uint64_t sub, bool relu) { return xround_blocks(sub, relu) * (relu ? 2 : 4); }
 
+int range_riders(const RangeRiders &r) { return r.nred + 1 + (r.rc.cj.nblk > 0 ? 1 : 0); }
+
 void launch_xrounds(int C, bool first, bool relu, const XArgs &a, uint64_t S, int stride, const XJobs &jobs,
-                    hipStream_t st)
+                    hipStream_t st, const RangeRiders *riders)
 {
     const uint64_t sub = S >> C;
     const int nmain = xround_blocks(sub, relu);
-    const dim3 g(nmain + jobs.nslot + jobs.nplane), b(kThreads);
-#define RA_X(CC, F, Z) hipLaunchKernelGGL((k_xrounds<CC, F, Z>), g, b, 0, st, a, sub, stride, jobs, nmain)
+    const RangeRiders none{};
+    const RangeRiders &rr = riders ? *riders : none;
+    const dim3 g(nmain + jobs.nslot + jobs.nplane + (riders ? range_riders(rr) : 0)), b(kThreads);
+#define RA_X(CC, F, Z) hipLaunchKernelGGL((k_xrounds<CC, F, Z>), g, b, 0, st, a, sub, stride, jobs, nmain, rr)
 #define RA_X_FZ(CC)                      \
     if (first) {                         \
         if (relu) RA_X(CC, true, true);  \

@@ -185,7 +185,9 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
         __syncthreads();  // the consumers have cleared the tiles
         __syncthreads();  // and added their digits
     } else {
-        if (xs_on) x_setup_body(xs, blockIdx.x * (64 * kConsumers) + tid - 64 * kProducers, s_xr, s_xs, s_xz);
+        // whole waves of the set-up, spread one wave per block before a block's
+        // second wave (wave w of block b takes entries 64 (w B + b) ..)
+        if (xs_on) x_setup_body(xs, (int)(((wv - kProducers) * gridDim.x + blockIdx.x) * 64) + lane, s_xr, s_xs, s_xz);
         v16i acc[DW][TP];
 #pragma unroll
         for (int k = 0; k < DW; k++)

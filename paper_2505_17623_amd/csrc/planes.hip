@@ -258,12 +258,13 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
 // Sum of the blocks' partial tiles, written as G[q][q'] (64 x 64, both
 // triangles).  Each block covers 64 tile entries; its four waves split the
 // partial blocks and combine through LDS.
-// Workgroups below nred: 16 entries of G each, sixteen lanes per entry (lane
-// group g sums the partial tiles of blocks g, g + 16, ...), then LDS.  The
-// next workgroup writes the constant block of the plane rounds, with a
-// deferred witness step the one after sums the witness claims (and the
-// claimed sum of the range instance), the others run the set-up of the
-// rounds over x.
+// The range call's set-up as a launch of its own, for tables too small for a
+// register pass (otherwise these roles ride elsewhere: the set-up of the
+// rounds over x in the Gram pass, the rest in the first register pass).
+// Workgroups below nred: 16 entries of G each (gram_reduce.hpp).  The next
+// workgroup writes the constant block of the plane rounds, with a deferred
+// witness step the one after sums the witness claims (and the claimed sum of
+// the range instance), the others run the set-up of the rounds over x.
 __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict__ gpart, int nblk, int TP,
                                                      uint64_t *__restrict__ G, int nred, RangeConsts rc,
                                                      XSetupArgs xs)

@@ -221,7 +221,9 @@ constexpr int xrounds_lds_words()
     return 4 * (5 * C) * 68 + 4 * (5 * C) > kJobLdsWords ? 4 * (5 * C) * 68 + 4 * (5 * C) : kJobLdsWords;
 }
 
-// Workgroups below nmain run the rounds; the others are jobs.
+// Workgroups below nmain run the rounds; the others are jobs, then (first
+// register pass of a range call) the range riders: the Gram reduction, the
+// constant block and a deferred witness step, in the rounds' LDS.
 template <int C, bool FIRST, bool RELU>
 __global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stride, XJobs jobs, int nmain,
                                                  RangeRiders rr)

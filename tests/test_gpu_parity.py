@@ -247,3 +247,31 @@ def test_product_int32_top_plane(ra, m):
     C, _ = ra.ra_sumcheck_matmul_prove(ctx, torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
     want = A.astype(np.int64) @ B.astype(np.int64)
     assert np.array_equal(C.cpu().numpy(), want)
+
+
+def test_two_register_passes_verified(ra):
+    """2^23 outputs: the rounds over x take two register passes, and the plane
+    rounds are evaluated by the second one's extra workgroups.  The oracle
+    cannot prove a table this large, so the library's host verifier checks
+    the transcript against the opened tables (every chain, final value and
+    opening) and rejects a changed round word.  Synchronous and deferred runs
+    (t given, witness announced) give the same transcript."""
+    n, m, k = 2048, 64, 4096
+    rng = np.random.default_rng(23)
+    A = rng.integers(-2 ** 10, 2 ** 10, size=(n, m)).astype(np.int16)
+    B = rng.integers(-2 ** 10, 2 ** 10, size=(m, k)).astype(np.int16)
+    chal = inputs.xorshift64_stream(2323, 512)
+    Ad, Bd = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    g = ra.prove_layer(ra.Context(chal), Ad, Bd, 8, True, 0)
+    tr = g["transcript"]
+    assert tr["P"] == 64
+    dctx = ra.Context(chal, deferred=True)
+    gd = ra.prove_layer(dctx, Ad, Bd, 8, True, 0, tr["t"])
+    dctx.sync()
+    assert gd["transcript"] == tr
+    L = dict(A=A, B=B, Z=g["Z"].cpu().numpy(), R=g["R"].cpu().numpy(), Rm=g["Rm"].cpu().numpy(),
+             Y=g["Y"].cpu().numpy(), bits=g["bits"].cpu().numpy(), transcript=tr, chained=False)
+    assert ra.ra_verify(chal, [L]) == (0, 0)
+    ev = list(tr["rs_evals"])
+    ev[0] = (int(ev[0]) + 1) % P61
+    assert ra.ra_verify(chal, [dict(L, transcript=dict(tr, rs_evals=ev))])[0] != 0

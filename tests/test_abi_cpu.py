@@ -117,3 +117,32 @@ def test_library_verifier_rejects_tampering(ra):
     def unchained(L):
         A = L["A"].copy(); A.flat[0] += 1; L["A"] = A
     assert check(1, unchained) == 14
+
+
+def test_library_verifier_openings(ra):
+    """Tampers that keep every identity before an opening true (a* b* and
+    r_at^2 - y_at^2 unchanged, or a public matrix entry changed), so only
+    the openings of the final claims against the tables (check 3: a*, b*
+    against A, B; check 10: r_at, y_at against R, Y) can reject them."""
+    wl = inputs.small(2)
+    base = oracle_network(wl)
+    P = ra.P61
+    inv2 = pow(2, P - 2, P)
+
+    def verdict(li, **over):
+        layers = [dict(L, transcript=dict(L["transcript"])) for L in base]
+        for key, val in over.items():
+            if key in ("A", "B"):
+                layers[li][key] = val
+            else:
+                layers[li]["transcript"][key] = val
+        return ra.ra_verify(wl.challenges, layers)
+
+    tr0 = base[0]["transcript"]
+    assert verdict(0, a_star=2 * tr0["a_star"] % P, b_star=tr0["b_star"] * inv2 % P) == (3, 0)
+    assert verdict(0, r_at=(P - tr0["r_at"]) % P) == (10, 0)
+    assert verdict(0, y_at=(P - tr0["y_at"]) % P) == (10, 0)
+    A = base[0]["A"].copy(); A.flat[7] += 1
+    assert verdict(0, A=A) == (3, 0)
+    B = base[1]["B"].copy(); B.flat[3] -= 1
+    assert verdict(1, B=B) == (3, 1)

@@ -409,3 +409,23 @@ def test_tampered_transcript_words_rejected(honest):
         assert verify(res, chal, **{key: (res[key] + 1) % P}) != 0, key
     assert verify(res, chal, t=res["t"] + 1) != 0
     assert verify(res, chal, c0=res["c0"] + P) != 0                  # non-canonical word
+
+
+def test_openings_rejected_when_earlier_identities_hold(honest):
+    """Tampers that keep every identity before an opening true, so only the
+    opening of the final claims against the tables can reject them (Sec. IV:
+    the final sum-check claims are bound to the committed, here opened,
+    tables).  a* -> 2 a*, b* -> b* / 2 keeps a* b*, so the matrix chain and
+    its final identity hold and check 3 must fail; r_at -> -r_at (or y_at ->
+    -y_at) keeps r_at^2 - y_at^2, so the ReLU chain holds and check 10 must
+    fail."""
+    res, chal = honest
+    inv2 = pow(2, P - 2, P)
+    assert verify(res, chal, a_star=2 * res["a_star"] % P, b_star=res["b_star"] * inv2 % P) == 3
+    assert verify(res, chal, r_at=(P - res["r_at"]) % P) == 10
+    assert verify(res, chal, y_at=(P - res["y_at"]) % P) == 10
+    # a public input entry changed: only the opening of a* sees it
+    A = np.array(res["A"], copy=True); A[1, 3] += 1
+    assert verify(res, chal, A=A) == 3
+    B = np.array(res["B"], copy=True); B[2, 0] -= 1
+    assert verify(res, chal, B=B) == 3

@@ -58,6 +58,7 @@ typedef int32_t ra_status;
 #define RA_E_STATE (-7)             /* call out of the per-layer order */
 #define RA_E_BUFSIZE (-8)           /* a caller buffer is too small */
 #define RA_E_NOMEM (-9)             /* device or host allocation failed */
+#define RA_E_SCRATCH (-10)          /* the call needs more than the fixed scratch of ra_mle_bind_noalloc */
 
 typedef enum { RA_I16 = 1, RA_I32 = 2, RA_I64 = 3, RA_FIELD = 4 } ra_dtype;
 
@@ -137,6 +138,26 @@ ra_status ra_ctx_profile(const ra_ctx *ctx, uint32_t index, const char **name, d
  * Consumes no challenges.  RA_E_INVAL on a bad dimension, dtype or point. */
 ra_status ra_mle_bind(ra_ctx *ctx, const void *d_T, ra_dtype dtype, uint32_t rows, uint32_t cols, int bind_rows,
                       const uint64_t *h_point, uint32_t point_len, uint64_t *d_out);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * binding as ra_mle_bind, bit for bit, without a context.  It allocates
+ * nothing and copies nothing: the point is passed to the kernels by value,
+ * and the eq table (2^point_len words) and a row binding's chunk sums live in
+ * a fixed device array of RA_NOALLOC_SCRATCH_BYTES per GPU, held by each GPU
+ * the library runs on until the process ends.
+ *   Arguments as for ra_mle_bind, plus hip_stream (hipStream_t; NULL = the
+ *   null stream) on the current device.  The work is enqueued and the call
+ *   returns without waiting: d_out is ready when the stream is.
+ *   Every call on one GPU shares that GPU's array, so calls whose work
+ *   overlaps on one GPU (other streams or threads) race; calls ordered on one
+ *   stream do not.  Every word a call reads from the array it writes first.
+ *   RA_E_SCRATCH when the eq table plus the row binding's chunk sums exceed
+ *   the array (point_len <= 18 always fits); RA_E_INVAL as ra_mle_bind;
+ *   RA_E_HIP if the array's device address cannot be found. */
+#define RA_NOALLOC_SCRATCH_BYTES (4u << 20)
+ra_status ra_mle_bind_noalloc(const void *d_T, ra_dtype dtype, uint32_t rows, uint32_t cols, int bind_rows,
+                              const uint64_t *h_point, uint32_t point_len, uint64_t *d_out, void *hip_stream);
 
 /* Transcript of the matrix-multiplication sum-check. */
 typedef struct {

@@ -356,6 +356,7 @@ const char *ra_status_str(ra_status st)
     case RA_E_STATE: return "call out of the per-layer order";
     case RA_E_BUFSIZE: return "buffer too small";
     case RA_E_NOMEM: return "allocation failed";
+    case RA_E_SCRATCH: return "needs more than the fixed scratch of ra_mle_bind_noalloc";
     default: return "unknown status";
     }
 }

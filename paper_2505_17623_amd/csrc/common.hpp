@@ -70,6 +70,12 @@ struct XSetupArgs {
 
 // ---- launchers (witness.hip) ----
 void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st);
+// a point of at most 32 variables passed by value (kernel argument)
+struct EqPoint {
+    uint64_t z[32];
+    int v;
+};
+void launch_eq_table_val(const EqPoint &pt, uint64_t *out, hipStream_t st);
 // both tables of a product's two sides in one launch
 void launch_eq_tables(const uint64_t *z1, int v1, uint64_t *out1, const uint64_t *z2, int v2, uint64_t *out2,
                       hipStream_t st);

@@ -13,6 +13,22 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 // eq table (Eq. (1) / chi vector of Sec. II-C):
 //   out[i] = prod_j (z_j i_j + (1 - z_j)(1 - i_j)),  i_1 = MSB of i.
 // ---------------------------------------------------------------------------
+// Entries blk*256 + tid, stepping by nblk*256, of the table of the point zl
+// (in LDS, v variables).
+__device__ __forceinline__ void eq_table_entries(const uint64_t *zl, int v, uint64_t *__restrict__ out, int blk,
+                                                 int nblk)
+{
+    const uint64_t n = 1ull << v;
+    for (uint64_t i = (uint64_t)blk * blockDim.x + threadIdx.x; i < n; i += (uint64_t)nblk * blockDim.x) {
+        uint64_t acc = 1;
+        for (int j = 0; j < v; j++) {
+            const uint64_t zj = zl[j];
+            acc = m61::lmul(acc, ((i >> (v - 1 - j)) & 1) ? zj : m61::lsub(1, zj));
+        }
+        out[i] = m61::canon(acc);
+    }
+}
+
 // Workgroups below nb1 fill the first table (point z1, v1 variables), the
 // others the second; the point is staged in LDS first.
 __global__ __launch_bounds__(256) void k_eq_tables(const uint64_t *__restrict__ z1, int v1, uint64_t *__restrict__ out1,
@@ -27,15 +43,16 @@ __global__ __launch_bounds__(256) void k_eq_tables(const uint64_t *__restrict__ 
     uint64_t *out = second ? out2 : out1;
     if ((int)threadIdx.x < v) zl[threadIdx.x] = z[threadIdx.x];
     __syncthreads();
-    const uint64_t n = 1ull << v;
-    for (uint64_t i = (uint64_t)blk * blockDim.x + threadIdx.x; i < n; i += (uint64_t)nblk * blockDim.x) {
-        uint64_t acc = 1;
-        for (int j = 0; j < v; j++) {
-            const uint64_t zj = zl[j];
-            acc = m61::lmul(acc, ((i >> (v - 1 - j)) & 1) ? zj : m61::lsub(1, zj));
-        }
-        out[i] = m61::canon(acc);
-    }
+    eq_table_entries(zl, v, out, blk, nblk);
+}
+
+// The same table from a point passed by value (no device copy of the point).
+__global__ __launch_bounds__(256) void k_eq_table_val(EqPoint pt, uint64_t *__restrict__ out)
+{
+    __shared__ uint64_t zl[64];
+    if ((int)threadIdx.x < pt.v) zl[threadIdx.x] = pt.z[threadIdx.x];
+    __syncthreads();
+    eq_table_entries(zl, pt.v, out, blockIdx.x, gridDim.x);
 }
 
 static int eq_blocks(int v)
@@ -47,6 +64,11 @@ static int eq_blocks(int v)
 void launch_eq_table(const uint64_t *z, int v, uint64_t *out, hipStream_t st)
 {
     hipLaunchKernelGGL(k_eq_tables, dim3(eq_blocks(v)), dim3(kThreads), 0, st, z, v, out, eq_blocks(v), z, v, out);
+}
+
+void launch_eq_table_val(const EqPoint &pt, uint64_t *out, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_eq_table_val, dim3(eq_blocks(pt.v)), dim3(kThreads), 0, st, pt, out);
 }
 
 void launch_eq_tables(const uint64_t *z1, int v1, uint64_t *out1, const uint64_t *z2, int v2, uint64_t *out2,

@@ -22,10 +22,11 @@ RA_I16, RA_I32, RA_I64, RA_FIELD = 1, 2, 3, 4
 RA_ROUND_NEAREST, RA_ROUND_FLOOR = 0, 1
 STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_FIELD_TOO_SMALL",
           -4: "RA_E_RANGE", -5: "RA_E_CHALLENGES", -6: "RA_E_HIP", -7: "RA_E_STATE",
-          -8: "RA_E_BUFSIZE", -9: "RA_E_NOMEM"}
+          -8: "RA_E_BUFSIZE", -9: "RA_E_NOMEM", -10: "RA_E_SCRATCH"}
 EXPORTS = ["ra_ctx_create", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str", "ra_ctx_set_profiling",
            "ra_ctx_profile", "ra_ctx_set_deferred", "ra_ctx_sync", "ra_mle_bind",
-           "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify", "ra_witness_plan"]
+           "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify", "ra_witness_plan",
+           "ra_mle_bind_noalloc"]
 
 
 class RAError(RuntimeError):
@@ -92,6 +93,8 @@ def lib():
         L.ra_status_str.argtypes = [ctypes.c_int32]
         L.ra_mle_bind.argtypes = [vp, vp, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int, u64p,
                                   ctypes.c_uint32, vp]
+        L.ra_mle_bind_noalloc.argtypes = [vp, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int, u64p,
+                                          ctypes.c_uint32, vp, vp]
         L.ra_sumcheck_matmul_prove.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_uint32, ctypes.c_uint32,
                                                ctypes.c_uint32, vp, ctypes.POINTER(MatmulProof)]
         L.ra_rescale_relu_witness.argtypes = [vp, vp, ctypes.c_uint32, ctypes.c_uint32, vp, vp, vp, vp, vp,
@@ -106,7 +109,8 @@ def lib():
         for f in (L.ra_ctx_create, L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
-                  L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify, L.ra_witness_plan):
+                  L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify, L.ra_witness_plan,
+                  L.ra_mle_bind_noalloc):
             f.restype = ctypes.c_int32
         _lib = L
     return _lib
@@ -211,6 +215,21 @@ def ra_mle_bind(ctx: Context, T: torch.Tensor, bind_rows: bool, point, field: bo
     out = torch.empty(cols if bind_rows else rows, dtype=torch.int64, device=T.device)
     _check(lib().ra_mle_bind(ctx.h, _dptr(T), dt, rows, cols, int(bool(bind_rows)), pp, len(pt), _dptr(out)),
            "ra_mle_bind")
+    return out
+
+
+def ra_mle_bind_noalloc(T: torch.Tensor, bind_rows: bool, point, out: torch.Tensor, field: bool = False,
+                        stream: torch.cuda.Stream | None = None):
+    """ra_mle_bind without a context or allocation: writes `out` (int64,
+    cols or rows entries) on `stream` (default: the current stream) and
+    returns without waiting."""
+    rows, cols = T.shape
+    dt = RA_FIELD if field else _DT[T.dtype]
+    pt, pp = _u64_array(point)
+    assert out.dtype == torch.int64 and out.numel() == (cols if bind_rows else rows) and out.is_contiguous()
+    st = stream or torch.cuda.current_stream()
+    _check(lib().ra_mle_bind_noalloc(_dptr(T), dt, rows, cols, int(bool(bind_rows)), pp, len(pt), _dptr(out),
+                                     ctypes.c_void_p(st.cuda_stream)), "ra_mle_bind_noalloc")
     return out
 
 

@@ -54,6 +54,16 @@ def test_host_side_argument_errors(ra):
     f = ctypes.c_uint32()
     assert L.ra_verify(ra.P61, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == 0
     assert L.ra_verify(5, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == -2
+    # the fixed-scratch binding rejects before touching a device: a table whose
+    # eq table (2^20 words) exceeds the scratch, a bad dimension, a bad point
+    fake = ctypes.c_void_p(1 << 20)
+    pt = np.zeros(20, dtype=np.uint64)
+    assert L.ra_mle_bind_noalloc(fake, ra.RA_I16, 1 << 20, 1, 1, pt.ctypes.data_as(ra.u64p), 20, fake,
+                                 None) == -10
+    assert L.ra_mle_bind_noalloc(fake, ra.RA_I16, 3, 4, 1, pt.ctypes.data_as(ra.u64p), 2, fake, None) == -1
+    assert L.ra_mle_bind_noalloc(fake, ra.RA_I16, 4, 4, 1, pt.ctypes.data_as(ra.u64p), 3, fake, None) == -1
+    big = np.array([ra.P61, 0], dtype=np.uint64)
+    assert L.ra_mle_bind_noalloc(fake, ra.RA_I16, 4, 4, 1, big.ctypes.data_as(ra.u64p), 2, fake, None) == -1
 
 
 def oracle_network(wl):

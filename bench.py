@@ -246,14 +246,11 @@ def main():
     torch.cuda.set_device(0)
     wl = inputs.workload(args.config, "full")
     L = len(wl.layers)
-    steps_total = max(args.warmup, 1) + 4 * args.steps + 2
-    chal = inputs.xorshift64_stream(inputs.CHALLENGE_SEED_BASE + args.config,
-                                    inputs.CHALLENGES_PER_LAYER * L * steps_total)
     dev = torch.device("cuda:0")
     X = ra.to_device(wl.X, dev)
     Bs = [ra.to_device(Ly.B, dev) for Ly in wl.layers]
     torch.cuda.synchronize()
-    ctx = ra.Context(chal)
+    ctx = ra.Context(seed=wl.challenge_seed)
     shapes = layer_shapes(wl)
     print(f"# workload: {wl.name}; layers {shapes}", file=sys.stderr, flush=True)
 

@@ -53,12 +53,13 @@ typedef int32_t ra_status;
 #define RA_E_UNSUPPORTED_PRIME (-2) /* p != 2^61 - 1 */
 #define RA_E_FIELD_TOO_SMALL (-3)   /* s + t + 3 > 61 bits of p (Theorem A.1, condition 1) */
 #define RA_E_RANGE (-4)             /* R outside [-2^(t+1), 2^(t+1)) for a given t, or too many bit planes */
-#define RA_E_CHALLENGES (-5)        /* challenge stream exhausted, or a challenge >= p */
+#define RA_E_SEED (-5)              /* challenge stream: seed 0, a given array exhausted, or a challenge >= p */
 #define RA_E_HIP (-6)               /* a HIP runtime call failed */
 #define RA_E_STATE (-7)             /* call out of the per-layer order */
 #define RA_E_BUFSIZE (-8)           /* a caller buffer is too small */
-#define RA_E_NOMEM (-9)             /* device or host allocation failed */
+#define RA_E_NOT_IMPLEMENTED (-9)   /* valid for the protocol, beyond this GPU path's limits (see below) */
 #define RA_E_SCRATCH (-10)          /* the call needs more than the fixed scratch of ra_mle_bind_noalloc */
+#define RA_E_NOMEM (-11)            /* device or host allocation failed */
 
 typedef enum { RA_I16 = 1, RA_I32 = 2, RA_I64 = 3, RA_FIELD = 4 } ra_dtype;
 
@@ -71,18 +72,37 @@ typedef enum { RA_ROUND_NEAREST = 0, RA_ROUND_FLOOR = 1 } ra_round;
 typedef struct ra_ctx ra_ctx;
 
 /* Create a prover context.
- *   p             must be 2^61 - 1, else RA_E_UNSUPPORTED_PRIME.
- *   h_challenges  the verifier's random challenges (Alg. 1 step 4 and every
- *                 sum-check round of Sec. II-D), n_challenges field elements
- *                 in [0, p); copied to the device once.  They are consumed in
- *                 this order per layer: r1 (log n), r2 (log k), rho (log m),
- *                 lambda1, lambda2, lambda3, mu, tau_p (log P),
- *                 sigma (log P + log N), and with ReLU rho' (log N),
- *                 where N = n k and P is the layer's bit-plane count.
- *   hip_stream    hipStream_t to enqueue on (NULL = the null stream).
- *   out           receives the context. */
-ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, void *hip_stream,
-                        ra_ctx **out);
+ *   p           must be 2^61 - 1, else RA_E_UNSUPPORTED_PRIME.
+ *   seed        state of the verifier's challenge stream (nonzero, else
+ *               RA_E_SEED): xorshift64 with shifts 13, 7, 17 (Marsaglia,
+ *               "Xorshift RNGs", 2003), each challenge the next 64-bit output
+ *               reduced mod p.  The challenges are the verifier's coins of
+ *               Alg. 1 step 4 and of every sum-check round of Sec. II-D,
+ *               consumed in this order per layer: r1 (log n), r2 (log k),
+ *               rho (log m), lambda1, lambda2, lambda3, mu, tau_p (log P),
+ *               sigma (log P + log N), and with ReLU rho' (log N), where
+ *               N = n k and P is the layer's bit-plane count.  The context
+ *               draws them on the host and keeps them on the device, drawing
+ *               more (after waiting for its stream) when a call needs them.
+ *   hip_stream  hipStream_t to enqueue on (NULL = the null stream).
+ *   out         receives the context.
+ * Soundness note: the prover's witness tables (R, Rm, Y, Z, the bit table)
+ * are a function of C alone, so they are fixed before r1, r2 are drawn; a
+ * deployment that replaces the seeded coins by Fiat-Shamir must commit to
+ * (absorb) those tables before deriving r1, r2 (Alg. 1 commits C' in step 7
+ * before the checks that use the point), because the rounding link, the
+ * output link, the recomposition and the zero-check test them only at (r1, r2). */
+ra_status ra_ctx_create(uint64_t p, uint64_t seed, void *hip_stream, ra_ctx **out);
+/* The same with the challenges given: h_challenges holds n_challenges field
+ * elements in [0, p) (else RA_E_SEED), copied to the device once; a call that
+ * needs more than remain returns RA_E_SEED. */
+ra_status ra_ctx_create_stream(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, void *hip_stream,
+                               ra_ctx **out);
+/* Device workspace (bytes) that covers every call of one layer with these
+ * dimensions and at most P bit planes (int32 layer input and ReLU assumed),
+ * for callers that pass their own workspace to the proving calls.  n, m, k,
+ * P powers of two, else RA_E_INVAL. */
+ra_status ra_workspace_size(uint32_t n, uint32_t m, uint32_t k, uint32_t P, size_t *bytes);
 ra_status ra_ctx_destroy(ra_ctx *ctx);
 /* Number of challenges consumed so far. */
 ra_status ra_ctx_cursor(const ra_ctx *ctx, uint64_t *consumed);
@@ -168,27 +188,35 @@ typedef struct {
     uint64_t b_star; /* out: b~(rho, r2) */
 } ra_matmul_proof;
 
+/* Workspace of the three proving calls (d_ws, ws_bytes): NULL uses the
+ * context's own device workspace, grown on demand; otherwise device memory
+ * the caller owns, of at least ra_workspace_size bytes for the layer (else
+ * RA_E_BUFSIZE), not used by anything else until the call's work has run on
+ * the context's stream.  A call only uses it while its own kernels run. */
+
 /* Alg. 1 steps 2 and 4-6 for one layer: computes the witness C = A B exactly
  * (int64), draws r1, r2, binds A's rows at r1 and B's columns at r2 (Eq. (4))
  * and runs the degree-2 sum-check over l in {0,1}^(log m), drawing rho.
  *   d_A     n x m, RA_I16 or RA_I32 (layer input; later layers use the
- *           previous int32 output).  m <= 32768 (the product is formed
- *           exactly from 8-bit limbs with int32 partial sums; beyond that
- *           RA_E_INVAL).
+ *           previous int32 output).
  *   d_B     m x k int16 weights.
  *   d_C     out, n x k int64, the exact product.
  *   out     transcript; out->evals must hold 3 * log2(m) words.
- * The context keeps r1, r2 for the next two calls of this layer. */
+ * The context keeps r1, r2 for the next two calls of this layer.
+ * Limits of this GPU path (RA_E_NOT_IMPLEMENTED): m <= 32768 (the product
+ * is formed exactly from 8-bit limbs with int32 partial sums) and
+ * n k <= 2^31 (the layer's range call). */
 ra_status ra_sumcheck_matmul_prove(ra_ctx *ctx, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
-                                   uint32_t m, uint32_t k, int64_t *d_C, ra_matmul_proof *out);
+                                   uint32_t m, uint32_t k, int64_t *d_C, void *d_ws, size_t ws_bytes,
+                                   ra_matmul_proof *out);
 
 /* Parameters and claims of the rescale / ReLU witness. */
 typedef struct {
-    uint32_t s;          /* in: fractional bits removed, 1..16 */
+    uint32_t s;          /* in: fractional bits removed, >= 1 (this GPU path: <= 16) */
     uint32_t relu;       /* in: 1 = ReLU after the rescale */
     uint32_t round_mode; /* in: ra_round */
     int32_t t;           /* in: -1 = least t with R in [-2^(t+1), 2^(t+1)); >= 0 = given.  out: t used */
-    uint32_t P;          /* out: bit planes, next power of two >= s + (t+2) (1 + relu), at most 64 */
+    uint32_t P;          /* out: bit planes, next power of two >= s + (t+2) (1 + relu) (this GPU path: <= 64) */
     uint64_t r_claim;    /* out: R~(r1, r2) */
     uint64_t rm_claim;   /* out: Rm~(r1, r2) */
     uint64_t y_claim;    /* out: Y~(r1, r2) */
@@ -205,12 +233,13 @@ typedef struct {
  *        bit q - s - t - 2 of Y;  higher planes are zero,
  * picks t (or checks the given one), and returns the claims at (r1, r2).
  *   bits_words  capacity of d_bits in words, at least n * k.
- * Errors: RA_E_RANGE if a given t does not hold R, if t > 29 (R must fit
- * int32) or if more than 64 planes would be needed; RA_E_FIELD_TOO_SMALL if
- * s + t + 3 > 61. */
+ * Errors: RA_E_RANGE if a given t does not hold R; RA_E_FIELD_TOO_SMALL if
+ * s + t + 3 > 61 (Theorem A.1, condition 1); RA_E_INVAL if s = 0.
+ * Limits of this GPU path (RA_E_NOT_IMPLEMENTED): s <= 16 (Rm is uint16),
+ * t <= 29 (R, Y, Z are int32), P <= 64 (one bit word per output). */
 ra_status ra_rescale_relu_witness(ra_ctx *ctx, const int64_t *d_C, uint32_t n, uint32_t k, int32_t *d_R,
                                   uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits,
-                                  uint64_t bits_words, ra_witness_info *io);
+                                  uint64_t bits_words, void *d_ws, size_t ws_bytes, ra_witness_info *io);
 
 /* Optional: announce the next ra_rescale_relu_witness call (same layer) before
  * its ra_sumcheck_matmul_prove, so that the witness of Alg. 1 step 9 and Sec.
@@ -224,8 +253,9 @@ ra_status ra_rescale_relu_witness(ra_ctx *ctx, const int64_t *d_C, uint32_t n, u
  * the fusion does not take, runs the witness in full, so the results never
  * depend on the plan.  The plan is used by one layer.
  * Errors: RA_E_INVAL for a null buffer, t < 0 or parameters the witness call
- * would reject; RA_E_RANGE / RA_E_FIELD_TOO_SMALL as that call would return
- * them for s and t; RA_E_STATE when called between a layer's calls. */
+ * would reject; RA_E_FIELD_TOO_SMALL / RA_E_NOT_IMPLEMENTED as that call
+ * would return them for s and t; RA_E_STATE when called between a layer's
+ * calls. */
 ra_status ra_witness_plan(ra_ctx *ctx, uint32_t s, uint32_t relu, uint32_t round_mode, int32_t t, int32_t *d_R,
                           uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words);
 
@@ -248,9 +278,12 @@ typedef struct {
  * with tau = (tau_p, r1, r2) and W(q) = lambda_group(q) 2^(bit of q), i.e.
  * booleanity of every bit and recomposition of every range-checked value;
  * then with ReLU the zero-check sum_x eq((r1, r2), x) (R(x)^2 - Y(x)^2) = 0
- * of Eq. (6).  Inputs are the buffers the witness call filled and its info. */
+ * of Eq. (6).  Inputs are the buffers the witness call filled and its info.
+ * Limit of this GPU path: N = n k <= 2^31 (the plane rounds' exact int32
+ * sums), else RA_E_NOT_IMPLEMENTED. */
 ra_status ra_range_prove(ra_ctx *ctx, const uint64_t *d_bits, const int32_t *d_R, const int32_t *d_Y, uint32_t n,
-                         uint32_t k, const ra_witness_info *info, ra_range_proof *out);
+                         uint32_t k, const ra_witness_info *info, void *d_ws, size_t ws_bytes,
+                         ra_range_proof *out);
 
 /* Public data of one layer for the verifier (host pointers). */
 typedef struct {
@@ -277,7 +310,8 @@ typedef struct {
     ra_range_proof rng;
 } ra_layer_transcript;
 
-/* Host-only verifier (Sec. IV).  Replays the challenge stream, checks every
+/* Host-only verifier (Sec. IV).  Replays the challenge stream of `seed` (as
+ * ra_ctx_create draws it; seed 0 -> RA_E_SEED), checks every
  * sum-check chain (g_j(0) + g_j(1) against the previous round's value at its
  * challenge, by Lagrange interpolation), every final identity, the rounding
  * link C~ = 2^s R~ + Rm~ - 2^(s-1) (floor mode: no offset), the output link
@@ -290,9 +324,14 @@ typedef struct {
  *                 10 ReLU openings, 11 output link or Z opening, 12 parameters,
  *                 13 malformed layer, 14 chaining.
  *   *failed_layer index of the failing layer (0 when accepted). */
-ra_status ra_verify(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, uint32_t n_layers,
-                    const ra_layer_public *pub, const ra_layer_tables *tables, const ra_layer_transcript *tr,
-                    int32_t *verdict, uint32_t *failed_layer);
+ra_status ra_verify(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_layer_public *pub,
+                    const ra_layer_tables *tables, const ra_layer_transcript *tr, int32_t *verdict,
+                    uint32_t *failed_layer);
+/* The same with the challenges given (as for ra_ctx_create_stream); a stream
+ * too short for the layers gives RA_E_SEED. */
+ra_status ra_verify_stream(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, uint32_t n_layers,
+                           const ra_layer_public *pub, const ra_layer_tables *tables,
+                           const ra_layer_transcript *tr, int32_t *verdict, uint32_t *failed_layer);
 
 #ifdef __cplusplus
 }

@@ -9,6 +9,7 @@
 
 #include "common.hpp"
 #include "ra.h"
+#include "stream.hpp"
 #include "xsetup.hpp"
 
 using namespace ra;
@@ -29,15 +30,17 @@ struct ra_ctx {
     int device = 0;
     hipStream_t stream = nullptr;  // the caller's stream: every call is ordered on it
     uint64_t *d_chal = nullptr;
-    uint64_t n_chal = 0;
-    uint64_t cursor = 0;
+    uint64_t n_chal = 0;   // challenges on the device
+    uint64_t cursor = 0;   // challenges consumed
+    bool seeded = false;   // challenges drawn from `seed` (more are drawn on demand)
+    uint64_t seed = 0;
     // per-layer state between the three prover calls
     int phase = 0;  // 0: expects matmul, 1: expects witness, 2: expects range
     uint32_t n = 0, m = 0, k = 0;
     uint64_t *d_eq = nullptr;  // E1 (n words) then E2 (k words)
     uint64_t *d_acc = nullptr;  // row-binding accumulators of the fused front (zero between calls)
     size_t acc_cap = 0;
-    const uint64_t *d_r12 = nullptr;  // the layer's (r1, r2) in the challenge stream
+    uint64_t r12_off = 0;  // the layer's (r1, r2): offset in the challenge stream
     size_t eq_cap = 0;
     WitParams *d_params = nullptr;
     char *d_wit = nullptr;  // the witness's per-workgroup partials (min/max, claims, range flags)
@@ -87,6 +90,34 @@ struct ra_ctx {
 
 namespace {
 
+ra_status drain(ra_ctx *c);
+
+// Make `need` challenges past the cursor available on the device.  A seeded
+// context draws the stream again from its seed into a larger buffer (after
+// waiting for its stream, so no kernel still reads the old one); a context
+// with given challenges has no more.
+ra_status ensure_chal(ra_ctx *c, uint64_t need)
+{
+    if (c->cursor + need <= c->n_chal) return RA_OK;
+    if (!c->seeded) return RA_E_SEED;
+    const uint64_t want = std::max<uint64_t>({2 * c->n_chal, c->cursor + need, (uint64_t)1 << 16});
+    std::vector<uint64_t> h(want);
+    ra::ChallengeStream cs(c->seed);
+    for (uint64_t i = 0; i < want; i++) h[i] = cs.next();
+    const ra_status r = drain(c);
+    if (r != RA_OK && c->deferred_err == RA_OK) c->deferred_err = r;
+    uint64_t *d = nullptr;
+    if (hipMalloc((void **)&d, want * 8) != hipSuccess) return RA_E_NOMEM;
+    if (hipMemcpy(d, h.data(), want * 8, hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(d);
+        return RA_E_HIP;
+    }
+    if (c->d_chal) RA_HIP(hipFree(c->d_chal));
+    c->d_chal = d;
+    c->n_chal = want;
+    return RA_OK;
+}
+
 // Bump allocator over the context workspace (256-byte aligned pieces).
 struct Carve {
     size_t off = 0;
@@ -102,6 +133,22 @@ struct Carve {
 // flag (4 bytes) per workgroup, for at most kMaxBlocks workgroups.
 constexpr size_t kWitMinMax = 0, kWitClaims = 16 * kMaxBlocks, kWitFlags = kWitClaims + 32 * kMaxBlocks,
                  kWitBytes = kWitFlags + 4 * kMaxBlocks;
+
+ra_status ensure_ws(ra_ctx *c, size_t bytes);
+
+// The workspace of a proving call: the caller's (d_ws, at least `bytes`) or
+// the context's own, grown on demand.
+ra_status call_ws(ra_ctx *c, void *d_ws, size_t ws_bytes, size_t bytes, char **base)
+{
+    if (d_ws) {
+        if (ws_bytes < bytes) return RA_E_BUFSIZE;
+        *base = (char *)d_ws;
+        return RA_OK;
+    }
+    const ra_status st = ensure_ws(c, bytes);
+    *base = c->ws;
+    return st;
+}
 
 ra_status ensure_ws(ra_ctx *c, size_t bytes)
 {
@@ -278,15 +325,15 @@ ra_status finish(ra_ctx *c, size_t off, std::function<ra_status(const uint64_t *
 // a power of two.
 ra_status plane_params(int s, int t, int relu, int *P, int *lP)
 {
-    if (t > 29) return RA_E_RANGE;
     if (s + t + 3 > 61) return RA_E_FIELD_TOO_SMALL;
+    if (t > 29) return RA_E_NOT_IMPLEMENTED;  // R, Y, Z are int32
     const int Q = s + (t + 2) * (relu ? 2 : 1);
     int p = 1, l = 0;
     while (p < Q) {
         p <<= 1;
         l++;
     }
-    if (l > kMaxPlaneLog) return RA_E_RANGE;
+    if (l > kMaxPlaneLog) return RA_E_NOT_IMPLEMENTED;  // one bit word per output
     *P = p;
     *lP = l;
     return RA_OK;
@@ -339,9 +386,74 @@ void run_instance(ra_ctx *c, hipStream_t st, int kind, uint64_t *t0, uint64_t *t
     Timed tm(c, g_tail, st);
     launch_tail(kind, ta, jobs, st);
 }
+// Workspace pieces of a matrix call.
+struct MatmulLayout {
+    size_t o_a, o_b, o_scr, o_part, o_gemm, bytes;
+};
+MatmulLayout matmul_layout(bool a_i32, uint32_t n, uint32_t m, uint32_t k)
+{
+    const int nslots = std::max(1, log2u(m));
+    Carve cv;
+    MatmulLayout l;
+    l.o_a = cv.take<uint64_t>(m);
+    l.o_b = cv.take<uint64_t>(m);
+    l.o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n, m) * m);
+    l.o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
+    l.o_gemm = cv.take<char>(gemm_workspace_bytes(a_i32, n, m, k));
+    l.bytes = cv.off;
+    return l;
+}
+
+// Workspace pieces and pass schedule of a range call over N outputs and 2^lP
+// planes.  Rounds over x: register passes of kXFuseMax rounds while more
+// than kXTailLog + kXBlockMax variables remain, then one pass of Bp rounds
+// per workgroup in LDS, then the last pass (one workgroup).
+struct RangeLayout {
+    int L, nhs, reg, Bp, gtiles, gblocks;
+    size_t o_cst, o_bx, o_d, o_s, o_hs, o_ls, o_kr, o_kz, o_wsh, o_part, o_gp, o_gs, bytes;
+};
+RangeLayout range_layout(uint64_t N, int lP, int relu)
+{
+    RangeLayout l;
+    const int lN = log2u(N);
+    l.L = std::min(lN, kXSplitLog);
+    l.nhs = lN > l.L ? 1 << (lN - l.L) : 1;
+    const int v = std::min(lN, kXTailLog), rem = lN - v;
+    l.reg = 0;
+    while (rem - l.reg > kXBlockMax) l.reg += kXFuseMax;
+    l.Bp = rem - l.reg;
+    l.gtiles = plane_gram_tiles(lP);
+    l.gblocks = plane_gram_blocks(N, lP);
+    const int nslots = std::max(lN, 1);
+    Carve cv;
+    l.o_cst = cv.take<uint64_t>(C_WORDS);
+    l.o_bx = cv.take<uint64_t>(N);
+    l.o_d = cv.take<uint64_t>(relu ? N : 1);
+    l.o_s = cv.take<uint64_t>(relu ? N : 1);
+    l.o_hs = cv.take<uint64_t>(l.nhs);
+    l.o_ls = cv.take<uint64_t>(2ull << l.L);
+    l.o_kr = cv.take<uint64_t>(lN + 1);
+    l.o_kz = cv.take<uint64_t>(lN + 1);
+    l.o_wsh = cv.take<uint64_t>(1ull << l.Bp);
+    l.o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
+    l.o_gp = cv.take<uint64_t>((size_t)l.gblocks * l.gtiles * 1024);
+    l.o_gs = cv.take<uint64_t>(64 * 64);
+    l.bytes = cv.off;
+    return l;
+}
 }  // namespace
 
 extern "C" {
+
+ra_status ra_workspace_size(uint32_t n, uint32_t m, uint32_t k, uint32_t P, size_t *bytes)
+{
+    if (!bytes || !is_pow2(n) || !is_pow2(m) || !is_pow2(k) || !is_pow2(P)) return RA_E_INVAL;
+    const uint64_t N = (uint64_t)n * k;
+    const int lP = log2u(P);
+    if (m > kGemmMaxInner || N > kRangeMaxN || lP > kMaxPlaneLog) return RA_E_NOT_IMPLEMENTED;
+    *bytes = std::max(matmul_layout(true, n, m, k).bytes, range_layout(N, lP, 1).bytes);
+    return RA_OK;
+}
 
 const char *ra_status_str(ra_status st)
 {
@@ -350,36 +462,36 @@ const char *ra_status_str(ra_status st)
     case RA_E_INVAL: return "invalid argument";
     case RA_E_UNSUPPORTED_PRIME: return "unsupported prime (only 2^61 - 1)";
     case RA_E_FIELD_TOO_SMALL: return "field too small: s + t + 3 > 61";
-    case RA_E_RANGE: return "value range: given t does not hold R, or too many bit planes";
-    case RA_E_CHALLENGES: return "challenge stream exhausted or not canonical";
+    case RA_E_RANGE: return "value range: the given t does not hold R";
+    case RA_E_SEED: return "challenge stream: seed 0, given challenges exhausted, or a challenge >= p";
     case RA_E_HIP: return "HIP runtime error";
     case RA_E_STATE: return "call out of the per-layer order";
     case RA_E_BUFSIZE: return "buffer too small";
+    case RA_E_NOT_IMPLEMENTED: return "beyond this GPU path's limits (m <= 32768, s <= 16, t <= 29, P <= 64, N <= 2^31)";
     case RA_E_NOMEM: return "allocation failed";
     case RA_E_SCRATCH: return "needs more than the fixed scratch of ra_mle_bind_noalloc";
     default: return "unknown status";
     }
 }
 
-ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, void *hip_stream,
-                        ra_ctx **out)
+}  // extern "C"
+
+namespace {
+// A context with its fixed device buffers and `n` challenges from h (seeded:
+// h is the stream's first n draws).
+ra_status ctx_create(uint64_t p, const uint64_t *h, uint64_t n, bool seeded, uint64_t seed, void *hip_stream,
+                     ra_ctx **out)
 {
-    if (!out) return RA_E_INVAL;
-    *out = nullptr;
-    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
-    if (n_challenges && !h_challenges) return RA_E_INVAL;
-    for (uint64_t i = 0; i < n_challenges; i++)
-        if (h_challenges[i] >= kP) return RA_E_CHALLENGES;
     ra_ctx *c = new (std::nothrow) ra_ctx();
     if (!c) return RA_E_NOMEM;
+    (void)p;
     c->stream = (hipStream_t)hip_stream;
+    c->seeded = seeded;
+    c->seed = seed;
     ra_status st = RA_OK;
     if (hipGetDevice(&c->device) != hipSuccess) st = RA_E_HIP;
-    if (st == RA_OK && hipMalloc((void **)&c->d_chal, std::max<uint64_t>(n_challenges, 1) * 8) != hipSuccess)
-        st = RA_E_NOMEM;
-    if (st == RA_OK && n_challenges &&
-        hipMemcpy(c->d_chal, h_challenges, n_challenges * 8, hipMemcpyHostToDevice) != hipSuccess)
-        st = RA_E_HIP;
+    if (st == RA_OK && hipMalloc((void **)&c->d_chal, std::max<uint64_t>(n, 1) * 8) != hipSuccess) st = RA_E_NOMEM;
+    if (st == RA_OK && n && hipMemcpy(c->d_chal, h, n * 8, hipMemcpyHostToDevice) != hipSuccess) st = RA_E_HIP;
     static_assert(sizeof(WitParams) <= 64, "parameters precede the claims");
     if (st == RA_OK && hipMalloc((void **)&c->d_params, 128) != hipSuccess) st = RA_E_NOMEM;
     if (st == RA_OK && hipMalloc((void **)&c->d_wit, kWitBytes) != hipSuccess) st = RA_E_NOMEM;
@@ -389,10 +501,38 @@ ra_status ra_ctx_create(uint64_t p, const uint64_t *h_challenges, uint64_t n_cha
         ra_ctx_destroy(c);
         return st;
     }
-    c->n_chal = n_challenges;
+    c->n_chal = n;
     init_kernel_attributes();
     *out = c;
     return RA_OK;
+}
+}  // namespace
+
+extern "C" {
+
+ra_status ra_ctx_create(uint64_t p, uint64_t seed, void *hip_stream, ra_ctx **out)
+{
+    if (!out) return RA_E_INVAL;
+    *out = nullptr;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    if (seed == 0) return RA_E_SEED;
+    const uint64_t n = 1ull << 16;  // first draws; more on demand (ensure_chal)
+    std::vector<uint64_t> h(n);
+    ra::ChallengeStream cs(seed);
+    for (uint64_t i = 0; i < n; i++) h[i] = cs.next();
+    return ctx_create(p, h.data(), n, true, seed, hip_stream, out);
+}
+
+ra_status ra_ctx_create_stream(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, void *hip_stream,
+                               ra_ctx **out)
+{
+    if (!out) return RA_E_INVAL;
+    *out = nullptr;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    if (n_challenges && !h_challenges) return RA_E_INVAL;
+    for (uint64_t i = 0; i < n_challenges; i++)
+        if (h_challenges[i] >= kP) return RA_E_SEED;
+    return ctx_create(p, h_challenges, n_challenges, false, 0, hip_stream, out);
 }
 
 ra_status ra_ctx_destroy(ra_ctx *c)
@@ -496,33 +636,32 @@ ra_status ra_mle_bind(ra_ctx *c, const void *d_T, ra_dtype dtype, uint32_t rows,
 }
 
 ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
-                                   uint32_t m, uint32_t k, int64_t *d_C, ra_matmul_proof *out)
+                                   uint32_t m, uint32_t k, int64_t *d_C, void *d_ws, size_t ws_bytes,
+                                   ra_matmul_proof *out)
 {
     if (!c || !d_A || !d_B || !d_C || !out) return RA_E_INVAL;
     if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k)) return RA_E_INVAL;
     if (a_dtype != RA_I16 && a_dtype != RA_I32) return RA_E_INVAL;
-    if (m > kGemmMaxInner) return RA_E_INVAL;  // exactness of the limb products
+    if (m > kGemmMaxInner) return RA_E_NOT_IMPLEMENTED;  // exactness of the limb products
+    if ((uint64_t)n * k > kRangeMaxN) return RA_E_NOT_IMPLEMENTED;  // the layer's range call could not run
     if (c->phase != 0) return RA_E_STATE;
     const int ln = log2u(n), lm = log2u(m), lk = log2u(k);
     if (lm && !out->evals) return RA_E_INVAL;
     const uint64_t need = (uint64_t)ln + lk + lm;
-    if (c->cursor + need > c->n_chal) return RA_E_CHALLENGES;
+    ra_status st = ensure_chal(c, need);
+    if (st != RA_OK) return st;
     const uint64_t *r1 = c->d_chal + c->cursor, *r2 = r1 + ln, *rho = r2 + lk;
 
-    ra_status st = ensure_eq(c, (size_t)n + k);
-    if (st != RA_OK) return st;
-    const int nslots = std::max(1, lm);
+    if ((st = ensure_eq(c, (size_t)n + k)) != RA_OK) return st;
     const size_t trw = 3 + 3 * (size_t)lm;
-    Carve cv;
-    const size_t o_a = cv.take<uint64_t>(m), o_b = cv.take<uint64_t>(m);
-    const size_t o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n, m) * m);
-    const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
-    const size_t o_gemm = cv.take<char>(gemm_workspace_bytes(a_dtype == RA_I32, n, m, k));
-    if ((st = ensure_ws(c, cv.off)) != RA_OK) return st;
-    uint64_t *a = (uint64_t *)(c->ws + o_a), *b = (uint64_t *)(c->ws + o_b);
+    const MatmulLayout ml = matmul_layout(a_dtype == RA_I32, n, m, k);
+    char *ws = nullptr;
+    if ((st = call_ws(c, d_ws, ws_bytes, ml.bytes, &ws)) != RA_OK) return st;
+    const size_t o_gemm = ml.o_gemm;
+    uint64_t *a = (uint64_t *)(ws + ml.o_a), *b = (uint64_t *)(ws + ml.o_b);
     size_t o_tr = 0;
     if ((st = stage_take(c, trw, &o_tr)) != RA_OK) return st;
-    uint64_t *scr = (uint64_t *)(c->ws + o_scr), *part = (uint64_t *)(c->ws + o_part), *tr = c->d_stage + o_tr;
+    uint64_t *scr = (uint64_t *)(ws + ml.o_scr), *part = (uint64_t *)(ws + ml.o_part), *tr = c->d_stage + o_tr;
     uint64_t *E1 = c->d_eq, *E2 = c->d_eq + n;
     hipStream_t s = c->stream;
 
@@ -535,7 +674,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     if (fused) {
         if ((st = ensure_acc(c, m)) != RA_OK) return st;
         Timed tm(c, G_FRONT, z);
-        launch_front(d_A, a_dtype == RA_I32, d_B, n, m, k, r1, ln, r2, lk, c->d_acc, b, E1, E2, c->ws + o_gemm, z);
+        launch_front(d_A, a_dtype == RA_I32, d_B, n, m, k, r1, ln, r2, lk, c->d_acc, b, E1, E2, ws + o_gemm, z);
     } else {
         {
             Timed tm(c, G_EQ, z);
@@ -575,13 +714,13 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     }
     {
         Timed tm(c, G_GEMM);
-        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, c->ws + o_gemm, s, &ta, &tjobs, fused,
+        launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, ws + o_gemm, s, &ta, &tjobs, fused,
                          fuse_w ? &we : nullptr);
     }
     c->n = n;
     c->m = m;
     c->k = k;
-    c->d_r12 = r1;
+    c->r12_off = c->cursor;
     c->phase = 1;
     c->cursor += need;
     return finish(c, o_tr, [out, lm](const uint64_t *h) {
@@ -599,7 +738,8 @@ ra_status ra_witness_plan(ra_ctx *c, uint32_t s, uint32_t relu, uint32_t round_m
 {
     if (!c || !d_R || !d_Rm || !d_Y || !d_Z || !d_bits) return RA_E_INVAL;
     if (c->phase != 0) return RA_E_STATE;
-    if (s < 1 || s > 16 || relu > 1 || round_mode > 1 || t < 0) return RA_E_INVAL;
+    if (s < 1 || relu > 1 || round_mode > 1 || t < 0) return RA_E_INVAL;
+    if (s > 16) return RA_E_NOT_IMPLEMENTED;  // Rm is uint16
     int P = 0, lP = 0;
     const ra_status pst = plane_params((int)s, t, (int)relu, &P, &lP);
     if (pst != RA_OK) return pst;
@@ -622,12 +762,15 @@ ra_status ra_witness_plan(ra_ctx *c, uint32_t s, uint32_t relu, uint32_t round_m
 
 ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uint32_t k, int32_t *d_R,
                                   uint16_t *d_Rm, int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words,
-                                  ra_witness_info *io)
+                                  void *d_ws, size_t ws_bytes, ra_witness_info *io)
 {
+    (void)d_ws;  // the witness keeps its partials in the context (a deferred
+    (void)ws_bytes;  // call's last step runs in the next call)
     if (!c || !d_C || !d_R || !d_Rm || !d_Y || !d_Z || !d_bits || !io) return RA_E_INVAL;
     if (c->phase != 1) return RA_E_STATE;
     if (n != c->n || k != c->k) return RA_E_INVAL;
-    if (io->s < 1 || io->s > 16 || io->relu > 1 || io->round_mode > 1 || io->t < -1) return RA_E_INVAL;
+    if (io->s < 1 || io->relu > 1 || io->round_mode > 1 || io->t < -1) return RA_E_INVAL;
+    if (io->s > 16) return RA_E_NOT_IMPLEMENTED;  // Rm is uint16
     const uint64_t N = (uint64_t)n * k;
     if (bits_words < N) return RA_E_BUFSIZE;
     // with t given and deferred outputs, the plane count is known on the host
@@ -725,7 +868,7 @@ ra_status ra_rescale_relu_witness(ra_ctx *c, const int64_t *d_C, uint32_t n, uin
 }
 
 ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, const int32_t *d_Y, uint32_t n,
-                         uint32_t k, const ra_witness_info *info, ra_range_proof *out)
+                         uint32_t k, const ra_witness_info *info, void *d_ws, size_t ws_bytes, ra_range_proof *out)
 {
     if (!c || !d_bits || !info || !out || !out->evals) return RA_E_INVAL;
     if (c->phase != 2) return RA_E_STATE;
@@ -737,44 +880,29 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     if (relu && (!d_R || !d_Y || !out->relu_evals)) return RA_E_INVAL;
     const uint64_t N = (uint64_t)n * k;
     const int lP = log2u((uint64_t)c->P), lN = log2u(N), lk = log2u(k), R = lP + lN;
+    if (N > kRangeMaxN) return RA_E_NOT_IMPLEMENTED;  // exact int32 sums of the plane rounds
     const uint64_t need = 4 + (uint64_t)lP + R + (relu ? lN : 0);
-    if (c->cursor + need > c->n_chal) return RA_E_CHALLENGES;
+    ra_status st = ensure_chal(c, need);
+    if (st != RA_OK) return st;
     const uint64_t *lam = c->d_chal + c->cursor, *sigma = lam + 4 + lP, *rho2 = sigma + R;
+    const uint64_t *d_r12 = c->d_chal + c->r12_off;
 
-    const int L = std::min(lN, kXSplitLog), nhs = lN > L ? 1 << (lN - L) : 1;
-    // Rounds over x: register passes of kXFuseMax rounds while more than
-    // kXTailLog + kXBlockMax variables remain, then one pass of Bp rounds per
-    // workgroup in LDS, then the last pass (one workgroup).
-    const int v = std::min(lN, kXTailLog), rem = lN - v;
-    int reg = 0;
-    while (rem - reg > kXBlockMax) reg += kXFuseMax;
-    const int Bp = rem - reg;
-    const int nslots = std::max(lN, 1);
-    if (nslots > kMaxSlots || lN > 62) return RA_E_INVAL;
-    const int gtiles = plane_gram_tiles(lP), gblocks = plane_gram_blocks(N, lP);
+    const RangeLayout rl = range_layout(N, lP, relu);
+    const int L = rl.L, nhs = rl.nhs, reg = rl.reg, Bp = rl.Bp;
+    const int gtiles = rl.gtiles, gblocks = rl.gblocks;
     // transcript: [evals 4R][(unused)][bits_claim][range_sum][relu evals 4 lN][(unused)][r_at][y_at]
     const size_t F_R = 4 * (size_t)R, RS = F_R + 2, Z0 = F_R + 3, FZ = Z0 + 4 * (size_t)lN, trw = FZ + 3;
-    Carve cv;
-    const size_t o_cst = cv.take<uint64_t>(C_WORDS);
-    const size_t o_bx = cv.take<uint64_t>(N);
-    const size_t o_d = cv.take<uint64_t>(relu ? N : 1), o_s = cv.take<uint64_t>(relu ? N : 1);
-    const size_t o_hs = cv.take<uint64_t>(nhs), o_ls = cv.take<uint64_t>(2ull << L);
-    const size_t o_kr = cv.take<uint64_t>(lN + 1), o_kz = cv.take<uint64_t>(lN + 1);
-    const size_t o_wsh = cv.take<uint64_t>(1ull << Bp);
-    const size_t o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
-    const size_t o_gp = cv.take<uint64_t>((size_t)gblocks * gtiles * 1024);
-    const size_t o_gs = cv.take<uint64_t>(64 * 64);
-    ra_status st = ensure_ws(c, cv.off);
-    if (st != RA_OK) return st;
-    uint64_t *cst = (uint64_t *)(c->ws + o_cst), *Bx = (uint64_t *)(c->ws + o_bx);
-    uint64_t *D = (uint64_t *)(c->ws + o_d), *S = (uint64_t *)(c->ws + o_s);
-    uint64_t *HS = (uint64_t *)(c->ws + o_hs), *LS = (uint64_t *)(c->ws + o_ls);
-    uint64_t *Kr = (uint64_t *)(c->ws + o_kr), *Kz = (uint64_t *)(c->ws + o_kz);
-    uint64_t *WSh = (uint64_t *)(c->ws + o_wsh);
+    char *ws = nullptr;
+    if ((st = call_ws(c, d_ws, ws_bytes, rl.bytes, &ws)) != RA_OK) return st;
+    uint64_t *cst = (uint64_t *)(ws + rl.o_cst), *Bx = (uint64_t *)(ws + rl.o_bx);
+    uint64_t *D = (uint64_t *)(ws + rl.o_d), *S = (uint64_t *)(ws + rl.o_s);
+    uint64_t *HS = (uint64_t *)(ws + rl.o_hs), *LS = (uint64_t *)(ws + rl.o_ls);
+    uint64_t *Kr = (uint64_t *)(ws + rl.o_kr), *Kz = (uint64_t *)(ws + rl.o_kz);
+    uint64_t *WSh = (uint64_t *)(ws + rl.o_wsh);
     size_t o_tr = 0;
     if ((st = stage_take(c, trw, &o_tr)) != RA_OK) return st;
-    uint64_t *part = (uint64_t *)(c->ws + o_part), *tr = c->d_stage + o_tr;
-    uint64_t *gpart = (uint64_t *)(c->ws + o_gp), *gsum = (uint64_t *)(c->ws + o_gs);
+    uint64_t *part = (uint64_t *)(ws + rl.o_part), *tr = c->d_stage + o_tr;
+    uint64_t *gpart = (uint64_t *)(ws + rl.o_gp), *gsum = (uint64_t *)(ws + rl.o_gs);
     const uint64_t *sigx = sigma + lP, *rz = relu ? rho2 : nullptr;
     hipStream_t s = c->stream;
 
@@ -784,7 +912,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     // in the register pass's launch; the plane rounds are then evaluated one
     // launch later.  Otherwise a launch of its own runs all of that between
     // the Gram pass and the first x launch.
-    const XSetupArgs xs{c->d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
+    const XSetupArgs xs{d_r12, sigx, rz, lN, L, nhs, HS, LS, Kr, Kz, WSh, reg, Bp};
     const bool riding = reg > 0 && x_setup_count(xs) <= plane_gram_set_up_threads(N, lP);
     const RangeConsts rc{lam, c->d_params, c->d_claims, lP, cst, tr + RS, c->pend_claims};
     c->pend_claims.nblk = 0;  // taken by this call's launches
@@ -801,7 +929,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     // before it; the first one also evaluates the plane rounds (the second
     // one when the Gram reduction rides in the first), the last assembles
     // its own.
-    const XConst xc{cst + C_EP, c->d_r12, Kr, Kz};
+    const XConst xc{cst + C_EP, d_r12, Kr, Kz};
     XJobs jobs{};
     jobs.nplane = riding ? 0 : lP;
     jobs.stride = kPartStride;
@@ -818,7 +946,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     };
     int j = 0, lS = lN;
     for (; j < reg; j += kXFuseMax, lS -= kXFuseMax) {
-        const XArgs xa{Bx, D, S, d_R, d_Y, HS, LS, c->d_r12, sigx + j, rz ? rz + j : nullptr,
+        const XArgs xa{Bx, D, S, d_R, d_Y, HS, LS, d_r12, sigx + j, rz ? rz + j : nullptr,
                        part + (size_t)j * kPartStride, lN, L, j};
         {
             Timed tm(c, G_RANGE_ROUNDS);
@@ -827,7 +955,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
         }
         next_jobs(j, kXFuseMax, xround_units(1ull << (lS - kXFuseMax), relu != 0));
     }
-    XBlockArgs xb{Bx, D, S, d_R, d_Y, HS, LS, c->d_r12, WSh, nullptr, nullptr, nullptr, kPartStride, lN, L, 0, 0, 0,
+    XBlockArgs xb{Bx, D, S, d_R, d_Y, HS, LS, d_r12, WSh, nullptr, nullptr, nullptr, kPartStride, lN, L, 0, 0, 0,
                   tr, 0, 0, tr + F_R + 1, tr + FZ + 1, tr + FZ + 2, xc};
     if (Bp > 0) {
         xb.rho_a = sigx + j;

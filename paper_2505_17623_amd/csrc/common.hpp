@@ -22,6 +22,9 @@ constexpr int kPartWidth = 8;          // words per block and round in a partial
 
 constexpr int kMaxSlots = 96;          // per-call partial-sum slots (rounds)
 constexpr int kMaxPlaneLog = 6;        // bit planes per output <= 64 (one word)
+// outputs per range call: the plane rounds' int32 digit sums of a block (at
+// most 2^23 outputs of |digit| <= 128 per block at this N) stay exact
+constexpr uint64_t kRangeMaxN = 1ull << 31;
 
 // Constant block of the concatenated range check (words), see sumcheck.hip.
 constexpr int C_E = 0;      // e_j[p'] = eq(tau_{>j}, p'), j = 1..lP, sizes P/2, P/4, ..., 1

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "ra.h"
+#include "stream.hpp"
 
 namespace {
 
@@ -154,7 +155,7 @@ int verify_layer(const ra_layer_public &L, const ra_layer_tables &T, const ra_la
 
     const uint64_t need = (uint64_t)ln + lk + lm + 4 + lP + (lP + lN) + (relu ? lN : 0);
     if (*cursor + need > nchal) {
-        *err = RA_E_CHALLENGES;
+        *err = RA_E_SEED;
         return 13;
     }
     const uint64_t *r1 = chal + *cursor, *r2 = r1 + ln, *rho = r2 + lk, *lam = rho + lm;
@@ -242,15 +243,15 @@ int verify_layer(const ra_layer_public &L, const ra_layer_tables &T, const ra_la
 
 }  // namespace
 
-extern "C" ra_status ra_verify(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, uint32_t n_layers,
-                               const ra_layer_public *pub, const ra_layer_tables *tables,
-                               const ra_layer_transcript *tr, int32_t *verdict, uint32_t *failed_layer)
+extern "C" ra_status ra_verify_stream(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges,
+                                      uint32_t n_layers, const ra_layer_public *pub, const ra_layer_tables *tables,
+                                      const ra_layer_transcript *tr, int32_t *verdict, uint32_t *failed_layer)
 {
     if (!verdict || !failed_layer || (n_layers && (!pub || !tables || !tr)) || (n_challenges && !h_challenges))
         return RA_E_INVAL;
     if (p != kP) return RA_E_UNSUPPORTED_PRIME;
     for (uint64_t i = 0; i < n_challenges; i++)
-        if (h_challenges[i] >= kP) return RA_E_CHALLENGES;
+        if (h_challenges[i] >= kP) return RA_E_SEED;
     *verdict = 0;
     *failed_layer = 0;
     uint64_t cursor = 0;
@@ -266,4 +267,27 @@ extern "C" ra_status ra_verify(uint64_t p, const uint64_t *h_challenges, uint64_
         }
     }
     return RA_OK;
+}
+
+// The seeded form draws as many challenges as the layers consume (their
+// dimensions and plane counts as stated; a malformed layer fails its own
+// checks before it reads any) and verifies against them.
+extern "C" ra_status ra_verify(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_layer_public *pub,
+                               const ra_layer_tables *tables, const ra_layer_transcript *tr, int32_t *verdict,
+                               uint32_t *failed_layer)
+{
+    if (!verdict || !failed_layer || (n_layers && (!pub || !tables || !tr))) return RA_E_INVAL;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    if (seed == 0) return RA_E_SEED;
+    uint64_t total = 0;
+    auto lg = [](uint64_t x) { return is_pow2(x) && x <= (1ull << 32) ? log2u(x) : 0; };
+    for (uint32_t l = 0; l < n_layers; l++) {
+        const int ln = lg(pub[l].n), lm = lg(pub[l].m), lk = lg(pub[l].k), lN = ln + lk;
+        const int lP = is_pow2(tr[l].wit.P) && tr[l].wit.P <= 128 ? log2u(tr[l].wit.P) : 0;
+        total += (uint64_t)ln + lk + lm + 4 + 2 * lP + lN + (pub[l].relu ? lN : 0);
+    }
+    std::vector<uint64_t> chal(total ? total : 1);
+    ra::ChallengeStream cs(seed);
+    for (uint64_t i = 0; i < total; i++) chal[i] = cs.next();
+    return ra_verify_stream(p, chal.data(), total, n_layers, pub, tables, tr, verdict, failed_layer);
 }

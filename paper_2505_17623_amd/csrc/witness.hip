@@ -349,15 +349,15 @@ __global__ __launch_bounds__(256) void k_wit_params(const int64_t *__restrict__ 
         if (t_in < 62 && (umax >> (t_in + 1)) != 0) p.status = RA_E_RANGE;
         t = t_in;
     }
-    if (p.status == 0 && t > 29) p.status = RA_E_RANGE;  // R, Y must fit int32
     if (p.status == 0 && s + t + 3 > 61) p.status = RA_E_FIELD_TOO_SMALL;
+    if (p.status == 0 && t > 29) p.status = RA_E_NOT_IMPLEMENTED;  // R, Y must fit int32
     const int Q = s + (t + 2) * (relu ? 2 : 1);
     int P = 1, lP = 0;
     while (P < Q) {
         P <<= 1;
         lP++;
     }
-    if (p.status == 0 && lP > kMaxPlaneLog) p.status = RA_E_RANGE;
+    if (p.status == 0 && lP > kMaxPlaneLog) p.status = RA_E_NOT_IMPLEMENTED;  // one bit word per output
     p.t = t;
     p.P = P;
     p.lP = lP;

@@ -7,9 +7,11 @@ for convolutions), zero-pads dimensions to powers of two, and produces the
 verifier's random challenges as a stream of uniform field elements.
 
 Challenge stream: xorshift64 with shifts (13, 7, 17) (Marsaglia, "Xorshift
-RNGs", J. Stat. Softw. 8(14), 2003); each challenge is the top 61 bits of one
-output, redrawn when all 61 bits are ones, so it is uniform on
-{0, ..., 2^61 - 2}.
+RNGs", J. Stat. Softw. 8(14), 2003) from a nonzero seed; each challenge is
+the next 64-bit output reduced mod p = 2^61 - 1 (values below 8 are twice as
+likely as the rest, a bias of about 2^-61).  This is the Python side's own
+implementation of the published generator; the prover library has its own
+(a context created from a seed), and tests compare the two.
 
 Workloads (fixed-point layers of the shapes the paper's experiments use --
 a 64x64 matrix product with rounding, an MNIST-sized MLP -- plus larger
@@ -38,21 +40,17 @@ CHALLENGES_PER_LAYER = 256
 
 
 def xorshift64_stream(seed: int, count: int) -> np.ndarray:
-    """`count` challenges uniform on {0..2^61-2} from xorshift64(13,7,17)."""
+    """The first `count` challenges of the stream of `seed`: xorshift64(13, 7, 17)
+    outputs reduced mod 2^61 - 1."""
     x = seed & 0xFFFFFFFFFFFFFFFF
     if x == 0:
         raise ValueError("xorshift64 seed must be nonzero")
     out = np.empty(count, dtype=np.uint64)
-    i = 0
-    while i < count:
+    for i in range(count):
         x ^= (x << 13) & 0xFFFFFFFFFFFFFFFF
         x ^= x >> 7
         x ^= (x << 17) & 0xFFFFFFFFFFFFFFFF
-        v = x >> 3
-        if v == MASK61:
-            continue
-        out[i] = v
-        i += 1
+        out[i] = x % MASK61
     return out
 
 
@@ -90,7 +88,8 @@ class Workload:
     layers: List[Layer]
     links: List[Optional[Callable]] = field(default_factory=list)  # links[i]: Z_{i-1} -> A_i
     mode: int = 0                              # 0 nearest (Sec. II-A operator), 1 floor
-    challenges: np.ndarray = None
+    challenges: np.ndarray = None              # the first draws of the stream of challenge_seed
+    challenge_seed: int = 0
     description: str = ""
 
     def layer_input(self, li: int, Z_prev):
@@ -156,8 +155,10 @@ class Flatten:
         return out
 
 
-def _challenges(cfg: int, n_layers: int) -> np.ndarray:
-    return xorshift64_stream(CHALLENGE_SEED_BASE + cfg, CHALLENGES_PER_LAYER * n_layers)
+def _challenges(cfg: int, n_layers: int):
+    """(challenges, challenge_seed) of workload cfg: seed CHALLENGE_SEED_BASE + cfg."""
+    seed = CHALLENGE_SEED_BASE + cfg
+    return xorshift64_stream(seed, CHALLENGES_PER_LAYER * n_layers), seed
 
 
 def cfg1(seed_off: int = 0, n: int = 64, m: int = 64, k: int = 64) -> Workload:
@@ -167,7 +168,7 @@ def cfg1(seed_off: int = 0, n: int = 64, m: int = 64, k: int = 64) -> Workload:
     X = rng.integers(-2 ** 10, 2 ** 10, size=(n, m)).astype(np.int16)
     B = rng.integers(-2 ** 10, 2 ** 10, size=(m, k)).astype(np.int16)
     return Workload(f"single-layer {n}x{m}x{k} int16 s=8 relu", pad2(X), [Layer(pad2(B), 8, True, "L1", k)],
-                    [None], 0, _challenges(1 + seed_off, 1))
+                    [None], 0, *_challenges(1 + seed_off, 1))
 
 
 def mlp(batch: int, widths, f: int, relu_last: bool, cfg: int, std: float = 0.5,
@@ -182,7 +183,7 @@ def mlp(batch: int, widths, f: int, relu_last: bool, cfg: int, std: float = 0.5,
         W = quantise(rng.normal(0.0, std, size=(widths[i], widths[i + 1])), f)
         last = i == len(widths) - 2
         layers.append(Layer(pad2(W), f, (not last) or relu_last, f"L{i + 1}", widths[i + 1]))
-    return Workload(name, X, layers, [None] * len(layers), 0, _challenges(cfg, len(layers)))
+    return Workload(name, X, layers, [None] * len(layers), 0, *_challenges(cfg, len(layers)))
 
 
 def cfg2(batch: int = 64) -> Workload:
@@ -197,7 +198,7 @@ def cfg3(n: int = 1024) -> Workload:
     X = rng.integers(-2 ** 15, 2 ** 15, size=(n, n)).astype(np.int16)
     B = rng.integers(-2 ** 15, 2 ** 15, size=(n, n)).astype(np.int16)
     return Workload(f"single-layer {n}x{n}x{n} int16 s=12 relu", X, [Layer(B, 12, True, "L1", n)], [None], 0,
-                    _challenges(3, 1))
+                    *_challenges(3, 1))
 
 
 def cfg4(batch: int = 32, H: int = 32) -> Workload:
@@ -225,7 +226,7 @@ def cfg4(batch: int = 32, H: int = 32) -> Workload:
              Im2col(batch, H2, H2, 32, 3, 3, 1, 1, 512),
              Im2col(batch, H2, H2, 64, 2, 2, 2, 0, 256),
              Flatten(batch, H4 * H4, 64, next_pow2(H4 * H4 * 64))]
-    return Workload(f"cnn batch {batch} {H}x{H}x3 s=10", X, layers, links, 0, _challenges(4, len(layers)))
+    return Workload(f"cnn batch {batch} {H}x{H}x3 s=10", X, layers, links, 0, *_challenges(4, len(layers)))
 
 
 def cfg5(batch: int = 512, d: int = 4096) -> Workload:

@@ -21,12 +21,12 @@ P61 = (1 << 61) - 1
 RA_I16, RA_I32, RA_I64, RA_FIELD = 1, 2, 3, 4
 RA_ROUND_NEAREST, RA_ROUND_FLOOR = 0, 1
 STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_FIELD_TOO_SMALL",
-          -4: "RA_E_RANGE", -5: "RA_E_CHALLENGES", -6: "RA_E_HIP", -7: "RA_E_STATE",
-          -8: "RA_E_BUFSIZE", -9: "RA_E_NOMEM", -10: "RA_E_SCRATCH"}
-EXPORTS = ["ra_ctx_create", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str", "ra_ctx_set_profiling",
-           "ra_ctx_profile", "ra_ctx_set_deferred", "ra_ctx_sync", "ra_mle_bind",
-           "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify", "ra_witness_plan",
-           "ra_mle_bind_noalloc"]
+          -4: "RA_E_RANGE", -5: "RA_E_SEED", -6: "RA_E_HIP", -7: "RA_E_STATE",
+          -8: "RA_E_BUFSIZE", -9: "RA_E_NOT_IMPLEMENTED", -10: "RA_E_SCRATCH", -11: "RA_E_NOMEM"}
+EXPORTS = ["ra_ctx_create", "ra_ctx_create_stream", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str",
+           "ra_workspace_size", "ra_ctx_set_profiling", "ra_ctx_profile", "ra_ctx_set_deferred", "ra_ctx_sync",
+           "ra_mle_bind", "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify",
+           "ra_verify_stream", "ra_witness_plan", "ra_mle_bind_noalloc"]
 
 
 class RAError(RuntimeError):
@@ -81,7 +81,9 @@ def lib():
             raise ImportError(f"{LIB_PATH} not built; run python -m paper_2505_17623_amd.build")
         L = ctypes.CDLL(LIB_PATH)
         vp = ctypes.c_void_p
-        L.ra_ctx_create.argtypes = [u64, u64p, u64, vp, ctypes.POINTER(vp)]
+        L.ra_ctx_create.argtypes = [u64, u64, vp, ctypes.POINTER(vp)]
+        L.ra_ctx_create_stream.argtypes = [u64, u64p, u64, vp, ctypes.POINTER(vp)]
+        L.ra_workspace_size.argtypes = [ctypes.c_uint32] * 4 + [ctypes.POINTER(ctypes.c_size_t)]
         L.ra_ctx_destroy.argtypes = [vp]
         L.ra_ctx_cursor.argtypes = [vp, u64p]
         L.ra_ctx_set_profiling.argtypes = [vp, ctypes.c_int]
@@ -96,17 +98,19 @@ def lib():
         L.ra_mle_bind_noalloc.argtypes = [vp, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int, u64p,
                                           ctypes.c_uint32, vp, vp]
         L.ra_sumcheck_matmul_prove.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_uint32, ctypes.c_uint32,
-                                               ctypes.c_uint32, vp, ctypes.POINTER(MatmulProof)]
+                                               ctypes.c_uint32, vp, vp, ctypes.c_size_t, ctypes.POINTER(MatmulProof)]
         L.ra_rescale_relu_witness.argtypes = [vp, vp, ctypes.c_uint32, ctypes.c_uint32, vp, vp, vp, vp, vp,
-                                              u64, ctypes.POINTER(WitnessInfo)]
+                                              u64, vp, ctypes.c_size_t, ctypes.POINTER(WitnessInfo)]
         L.ra_witness_plan.argtypes = [vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int32, vp, vp,
                                       vp, vp, vp, u64]
         L.ra_range_prove.argtypes = [vp, vp, vp, vp, ctypes.c_uint32, ctypes.c_uint32,
-                                     ctypes.POINTER(WitnessInfo), ctypes.POINTER(RangeProof)]
-        L.ra_verify.argtypes = [u64, u64p, u64, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
-                                ctypes.POINTER(LayerTables), ctypes.POINTER(LayerTranscript),
-                                ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
-        for f in (L.ra_ctx_create, L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
+                                     ctypes.POINTER(WitnessInfo), vp, ctypes.c_size_t, ctypes.POINTER(RangeProof)]
+        tail = [ctypes.c_uint32, ctypes.POINTER(LayerPublic), ctypes.POINTER(LayerTables),
+                ctypes.POINTER(LayerTranscript), ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
+        L.ra_verify.argtypes = [u64, u64] + tail
+        L.ra_verify_stream.argtypes = [u64, u64p, u64] + tail
+        for f in (L.ra_ctx_create, L.ra_ctx_create_stream, L.ra_workspace_size, L.ra_verify_stream,
+                  L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
                   L.ra_rescale_relu_witness, L.ra_range_prove, L.ra_verify, L.ra_witness_plan,
@@ -135,14 +139,22 @@ _DT = {torch.int16: RA_I16, torch.int32: RA_I32, torch.int64: RA_I64}
 
 
 class Context:
-    """A prover context: the challenge stream on the device plus per-layer state."""
+    """A prover context: the challenge stream on the device plus per-layer
+    state.  Give either `seed` (the library draws the stream: ra_ctx_create)
+    or `challenges` (a given array: ra_ctx_create_stream)."""
 
-    def __init__(self, challenges, stream: torch.cuda.Stream | None = None, deferred: bool = False):
-        self._chal, cp = _u64_array(challenges)
+    def __init__(self, challenges=None, stream: torch.cuda.Stream | None = None, deferred: bool = False,
+                 seed: int | None = None):
+        assert (challenges is None) != (seed is None), "give challenges or seed"
         self.stream = stream or torch.cuda.current_stream()
         h = ctypes.c_void_p()
-        _check(lib().ra_ctx_create(P61, cp, len(self._chal), ctypes.c_void_p(self.stream.cuda_stream),
-                                   ctypes.byref(h)), "ra_ctx_create")
+        sp = ctypes.c_void_p(self.stream.cuda_stream)
+        if seed is not None:
+            _check(lib().ra_ctx_create(P61, seed, sp, ctypes.byref(h)), "ra_ctx_create")
+        else:
+            self._chal, cp = _u64_array(challenges)
+            _check(lib().ra_ctx_create_stream(P61, cp, len(self._chal), sp, ctypes.byref(h)),
+                   "ra_ctx_create_stream")
         self.h = h
         self._fills = []  # Python-side results completed at sync (deferred mode)
         self.deferred = False
@@ -233,9 +245,26 @@ def ra_mle_bind_noalloc(T: torch.Tensor, bind_rows: bool, point, out: torch.Tens
     return out
 
 
-def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None):
+def workspace_size(n: int, m: int, k: int, P: int = 64) -> int:
+    """Bytes of caller workspace that cover every call of an n x m x k layer (ra_workspace_size)."""
+    v = ctypes.c_size_t()
+    _check(lib().ra_workspace_size(n, m, k, P, ctypes.byref(v)), "ra_workspace_size")
+    return int(v.value)
+
+
+def _ws(ws):
+    """(pointer, bytes) of an optional caller workspace tensor (None: the context's own)."""
+    if ws is None:
+        return None, 0
+    assert ws.is_cuda and ws.is_contiguous()
+    return ctypes.c_void_p(ws.data_ptr()), ws.numel() * ws.element_size()
+
+
+def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None,
+                             ws: torch.Tensor | None = None):
     """Returns (C, transcript dict); in deferred mode the dict is filled at ctx.sync().
-    C (optional): an int64 n x k device tensor to write the product to."""
+    C (optional): an int64 n x k device tensor to write the product to.
+    ws (optional): caller-owned device workspace (see workspace_size)."""
     n, m = A.shape
     m2, k = B.shape
     assert m == m2 and B.dtype == torch.int16
@@ -246,7 +275,7 @@ def ra_sumcheck_matmul_prove(ctx: Context, A: torch.Tensor, B: torch.Tensor, C: 
     ev = np.zeros(max(3 * lm, 1), dtype=np.uint64)
     pr = MatmulProof()
     pr.evals = ev.ctypes.data_as(u64p)
-    _check(lib().ra_sumcheck_matmul_prove(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C),
+    _check(lib().ra_sumcheck_matmul_prove(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C), *_ws(ws),
                                           ctypes.byref(pr)), "ra_sumcheck_matmul_prove")
     res = {}
     ctx.later(lambda: res.update(c0=int(pr.c0), mm_evals=ev[:3 * lm].tolist(), a_star=int(pr.a_star),
@@ -264,7 +293,7 @@ def witness_outputs(n: int, k: int, device):
 
 
 def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1,
-                            outs=None):
+                            outs=None, ws: torch.Tensor | None = None):
     """Returns ((R, Rm, Y, Z, bits), info).  info.t and info.P are set on return
     (at once when t is given); the claims in info are final after ctx.sync()
     in deferred mode.  outs (optional): the five output tensors, as made by
@@ -275,7 +304,8 @@ def ra_rescale_relu_witness(ctx: Context, C: torch.Tensor, s: int, relu: bool, m
         assert tsr.dtype == dt and tsr.numel() == n * k and tsr.is_contiguous()
     info = WitnessInfo(s=s, relu=int(bool(relu)), round_mode=mode, t=t)
     _check(lib().ra_rescale_relu_witness(ctx.h, _dptr(C), n, k, _dptr(R), _dptr(Rm), _dptr(Y), _dptr(Z),
-                                         _dptr(bits), n * k, ctypes.byref(info)), "ra_rescale_relu_witness")
+                                         _dptr(bits), n * k, *_ws(ws), ctypes.byref(info)),
+           "ra_rescale_relu_witness")
     return (R, Rm, Y, Z, bits), info
 
 
@@ -287,7 +317,7 @@ def ra_witness_plan(ctx: Context, s: int, relu: bool, mode: int, t: int, outs):
                                  _dptr(bits), bits.numel()), "ra_witness_plan")
 
 
-def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
+def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo, ws: torch.Tensor | None = None):
     """Returns the range / ReLU transcript dict (filled at ctx.sync() in deferred mode)."""
     n, k = R.shape
     N = n * k
@@ -298,7 +328,7 @@ def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
     pr = RangeProof()
     pr.evals = ev.ctypes.data_as(u64p)
     pr.relu_evals = zev.ctypes.data_as(u64p)
-    _check(lib().ra_range_prove(ctx.h, _dptr(bits), _dptr(R), _dptr(Y), n, k, ctypes.byref(info),
+    _check(lib().ra_range_prove(ctx.h, _dptr(bits), _dptr(R), _dptr(Y), n, k, ctypes.byref(info), *_ws(ws),
                                 ctypes.byref(pr)), "ra_range_prove")
     res = {}
     ctx.later(lambda: res.update(rs_evals=ev.tolist(), range_sum=int(pr.range_sum),
@@ -308,7 +338,7 @@ def ra_range_prove(ctx: Context, bits, R, Y, info: WitnessInfo):
 
 
 def prove_layer(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1,
-                bufs: dict | None = None, plan: bool = True):
+                bufs: dict | None = None, plan: bool = True, ws: torch.Tensor | None = None):
     """The three calls of one layer; returns device tensors and the transcript
     (complete at once, or after ctx.sync() in deferred mode).  bufs (optional):
     a dict that keeps the layer's device outputs, made on first use and
@@ -324,9 +354,9 @@ def prove_layer(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bo
         if wit is None:
             wit = witness_outputs(n, k, A.device)
         ra_witness_plan(ctx, s, relu, mode, t, wit)
-    C, mm = ra_sumcheck_matmul_prove(ctx, A, B, None if bufs is None else bufs["C"])
-    (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t, wit)
-    rs = ra_range_prove(ctx, bits, R, Y, info)
+    C, mm = ra_sumcheck_matmul_prove(ctx, A, B, None if bufs is None else bufs["C"], ws)
+    (R, Rm, Y, Z, bits), info = ra_rescale_relu_witness(ctx, C, s, relu, mode, t, wit, ws)
+    rs = ra_range_prove(ctx, bits, R, Y, info, ws)
     tr = {}
 
     def fill():
@@ -342,7 +372,7 @@ def to_device(a: np.ndarray, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
-def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, plan=True):
+def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, plan=True, ws=None):
     """Prove every layer of a workload in order.  A layer's input is the
     previous output on the device (MLP chains) or the workload's link (im2col)
     applied on the host.  X / Bs may hold device copies of the inputs; ts may
@@ -365,7 +395,7 @@ def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=Non
             A = to_device(workload.links[li](Z.cpu().numpy()), device)
         t = -1 if ts is None else int(ts[li])
         res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t,
-                          None if bufs is None else bufs[li], plan)
+                          None if bufs is None else bufs[li], plan, ws)
         res["A"] = A
         Z = res["Z"]
         outs.append(res)
@@ -380,10 +410,13 @@ def unpack_bits(words: np.ndarray, P: int) -> np.ndarray:
 
 
 def ra_verify(challenges, layers):
-    """Host verifier.  `layers` is a list of dicts with numpy arrays A, B, Z,
-    R, Rm, Y, bits (uint64 words) and the transcript dict; returns
-    (verdict, failed_layer)."""
-    chal, cp = _u64_array(challenges)
+    """Host verifier.  `challenges` is a seed (int: ra_verify draws the
+    stream) or an array of challenges (ra_verify_stream).  `layers` is a
+    list of dicts with numpy arrays A, B, Z, R, Rm, Y, bits (uint64 words)
+    and the transcript dict; returns (verdict, failed_layer)."""
+    seeded = isinstance(challenges, (int, np.integer))
+    if not seeded:
+        chal, cp = _u64_array(challenges)
     nl = len(layers)
     pubs = (LayerPublic * nl)()
     tabs = (LayerTables * nl)()
@@ -423,7 +456,11 @@ def ra_verify(challenges, layers):
         t.rng.r_at, t.rng.y_at = tr["r_at"], tr["y_at"]
     verdict = ctypes.c_int32()
     failed = ctypes.c_uint32()
-    _check(lib().ra_verify(P61, cp, len(chal), nl, pubs, tabs, trs, ctypes.byref(verdict), ctypes.byref(failed)),
-           "ra_verify")
+    if seeded:
+        _check(lib().ra_verify(P61, int(challenges), nl, pubs, tabs, trs, ctypes.byref(verdict),
+                               ctypes.byref(failed)), "ra_verify")
+    else:
+        _check(lib().ra_verify_stream(P61, cp, len(chal), nl, pubs, tabs, trs, ctypes.byref(verdict),
+                                      ctypes.byref(failed)), "ra_verify_stream")
     return int(verdict.value), int(failed.value)
 

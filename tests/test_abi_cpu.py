@@ -43,17 +43,29 @@ def test_exports_every_declared_symbol(ra):
 def test_host_side_argument_errors(ra):
     L = ra.lib()
     h = ctypes.c_void_p()
-    assert L.ra_ctx_create(7, None, 0, None, ctypes.byref(h)) == -2       # unsupported prime
-    assert L.ra_ctx_create(ra.P61, None, 0, None, None) == -1             # null out
+    assert L.ra_ctx_create(7, 1, None, ctypes.byref(h)) == -2                     # unsupported prime
+    assert L.ra_ctx_create(ra.P61, 1, None, None) == -1                           # null out
+    assert L.ra_ctx_create(ra.P61, 0, None, ctypes.byref(h)) == -5                # seed 0
+    assert L.ra_ctx_create_stream(7, None, 0, None, ctypes.byref(h)) == -2
     bad = np.array([ra.P61], dtype=np.uint64)
-    assert L.ra_ctx_create(ra.P61, bad.ctypes.data_as(ra.u64p), 1, None, ctypes.byref(h)) == -5
+    assert L.ra_ctx_create_stream(ra.P61, bad.ctypes.data_as(ra.u64p), 1, None, ctypes.byref(h)) == -5
     assert L.ra_ctx_destroy(None) == -1
     for code, name in ra.STATUS.items():
         assert L.ra_status_str(code)
     v = ctypes.c_int32()
     f = ctypes.c_uint32()
-    assert L.ra_verify(ra.P61, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == 0
-    assert L.ra_verify(5, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == -2
+    assert L.ra_verify_stream(ra.P61, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == 0
+    assert L.ra_verify_stream(5, None, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == -2
+    assert L.ra_verify(ra.P61, 1, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == 0
+    assert L.ra_verify(ra.P61, 0, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == -5
+    assert L.ra_verify(5, 1, 0, None, None, None, ctypes.byref(v), ctypes.byref(f)) == -2
+    # workspace size: powers of two only; this GPU path's limits
+    sz = ctypes.c_size_t()
+    assert L.ra_workspace_size(3, 4, 4, 64, ctypes.byref(sz)) == -1
+    assert L.ra_workspace_size(4, 4, 4, 48, ctypes.byref(sz)) == -1
+    assert L.ra_workspace_size(4, 1 << 16, 4, 64, ctypes.byref(sz)) == -9          # m > 32768
+    assert L.ra_workspace_size(1 << 16, 4, 1 << 16, 64, ctypes.byref(sz)) == -9    # N > 2^31
+    assert L.ra_workspace_size(4, 4, 4, 128, ctypes.byref(sz)) == -9               # P > 64
     # the fixed-scratch binding rejects before touching a device: a table whose
     # eq table (2^20 words) exceeds the scratch, a bad dimension, a bad point
     fake = ctypes.c_void_p(1 << 20)
@@ -79,6 +91,18 @@ def test_library_verifier_accepts_oracle_transcripts(ra, cfg):
     wl = inputs.small(cfg)
     layers = oracle_network(wl)
     assert ra.ra_verify(wl.challenges, layers) == (0, 0)
+    # the seeded form draws the stream with the library's own generator: it
+    # accepts only if that stream equals the one the oracle was given
+    assert ra.ra_verify(wl.challenge_seed, layers) == (0, 0)
+    assert ra.ra_verify(wl.challenge_seed + 1, layers)[0] != 0
+
+
+def test_workspace_size_covers_layers(ra):
+    small = ra.workspace_size(64, 64, 64, 64)
+    big = ra.workspace_size(1024, 1024, 1024, 64)
+    assert 0 < small < big
+    # the range call's tables (three of N words with ReLU) bound it below
+    assert big >= 3 * 8 * 1024 * 1024
 
 
 def test_library_verifier_rejects_tampering(ra):

@@ -139,8 +139,8 @@ def test_plan_state_and_arguments(ra):
         ra.ra_witness_plan(ctx, 4, True, 0, -1, outs)      # t must be given
     assert e.value.code == -1
     with pytest.raises(ra.RAError) as e:
-        ra.ra_witness_plan(ctx, 20, True, 0, 3, outs)      # s out of range
-    assert e.value.code == -1
+        ra.ra_witness_plan(ctx, 20, True, 0, 3, outs)      # s beyond this GPU path's 16
+    assert e.value.code == -9
     ra.ra_sumcheck_matmul_prove(ctx, A, A)
     with pytest.raises(ra.RAError) as e:
         ra.ra_witness_plan(ctx, 4, True, 0, 3, outs)       # between a layer's calls

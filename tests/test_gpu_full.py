@@ -33,19 +33,20 @@ def digest_i64(a) -> str:
 @pytest.mark.parametrize("mode", ["sync", "bench"])
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_full_workload_matches_oracle(cfg, mode):
-    """sync: each call waits, t is derived from the data.  bench: the launch
-    configuration bench.py times -- deferred outputs, each layer's t given
+    """sync: each call waits, t is derived from the data, the challenges are
+    the oracle's array.  bench: the launch configuration bench.py times -- a
+    context drawing its own stream from the seed, deferred outputs, each layer's t given
     (so the witness is announced and computed inside the product), output
     buffers kept across steps, one sync."""
     from paper_2505_17623_amd import ra
     path = os.path.join(GOLD, f"full_cfg{cfg}.json")
     gold = json.load(open(path))
     wl = inputs.workload(cfg, "full")
-    if mode == "sync":
+    if mode == "sync":  # the stream the oracle was given
         ctx = ra.Context(wl.challenges)
         got = ra.prove_network(ctx, wl)
-    else:
-        ctx = ra.Context(wl.challenges, deferred=True)
+    else:  # as bench.py: the library draws the stream from the seed
+        ctx = ra.Context(seed=wl.challenge_seed, deferred=True)
         got = ra.prove_network(ctx, wl, ts=[o["transcript"]["t"] for o in gold["layers"]], bufs=[])
         ctx.sync()
     assert len(got) == len(gold["layers"])

@@ -429,3 +429,13 @@ def test_openings_rejected_when_earlier_identities_hold(honest):
     assert verify(res, chal, A=A) == 3
     B = np.array(res["B"], copy=True); B[2, 0] -= 1
     assert verify(res, chal, B=B) == 3
+
+
+def test_challenge_stream_is_xorshift64():
+    """The seeded challenge stream is Marsaglia's xor64 generator (shifts 13,
+    7, 17) reduced mod p: its raw outputs from the example state of that
+    paper, reduced, are the first challenges (tests/golden/xorshift64_marsaglia.json)."""
+    g = json.load(open(os.path.join(GOLD, "xorshift64_marsaglia.json")))
+    got = inputs.xorshift64_stream(g["seed"], len(g["outputs"]))
+    assert [int(x) for x in got] == [o % P for o in g["outputs"]]
+    assert all(int(x) < P for x in inputs.xorshift64_stream(12345, 2000))

@@ -2,6 +2,10 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config C] [--no-cpu-baseline]
 
+Default workload: config 5, two 512x4096x4096 layers (the transformer-block
+MLP at batch 512, s = 12, ReLU after the first), the largest configuration
+and the one the headline is quoted on.
+
 One step proves every layer of a synthetic fixed-point workload (matrix
 sum-check, rescale/ReLU witness, concatenated range sum-check, ReLU
 zero-check) with its inputs already resident in HBM.  Prints one JSON line:
@@ -74,45 +78,57 @@ def x_schedule(lN):
 
 
 def group_work(shapes, planes):
-    """Algorithmic work per step of each kernel group: {group: (bound, amount)}
-    with amount in bytes (hbm), int8 operations (mfma) or 32-bit multiplies
-    (alu, 4 per field multiplication), plus the fold groups' HBM bytes."""
-    w, hbm2 = {}, {}
+    """Algorithmic work per step of each kernel group, as the method defines
+    it (not the dense work an implementation does instead):
+    {group: {"bound": b, "amount": a, "secondary": (b2, a2) or None}}.
+      gemm_mfma      the exact product C = A B: 2 n m k integer operations,
+                     priced at the dense int8 MFMA peak it runs on
+                     (secondary: the int8 limb products it actually issues);
+      matmul_front   HBM bytes: A and B read once (2 or 4 B per entry), the
+                     eq tables written;
+      range_plane    HBM bytes of the plane rounds: the packed bit table in
+                     (P N / 8 B) and the plane-bound table Bx out (8 N B)
+                     (secondary: the int8 MFMA operations of the Gram matrix);
+      range_rounds   HBM bytes of the register/LDS passes over x: each pass
+                     reads its input tables and writes the folded ones
+                     (secondary: 32-bit multiplies, 4 per field product);
+      range_tail, matmul_rounds, matmul_tail  32-bit multiplies (latency-bound
+                     passes over small tables);
+      witness_*      HBM bytes (only when the witness is not fused)."""
+    w = {}
 
-    def add(g, bound, amt, d=w):
-        b, a = d.get(g, (bound, 0))
-        d[g] = (bound, a + amt)
+    def add(g, bound, amt, sec=None):
+        d = w.setdefault(g, {"bound": bound, "amount": 0, "secondary": None})
+        d["amount"] += amt
+        if sec:
+            b2, a2 = d["secondary"] or (sec[0], 0)
+            d["secondary"] = (b2, a2 + sec[1])
 
     for (n, m, k, ab, _, relu), P in zip(shapes, planes):
         N = n * k
-        # exact product on the matrix cores: LA x 2 int8 limb products of 2 n m k
-        # operations.  int32 activations are the previous layer's ReLU outputs,
-        # in [0, 2^24): their top limb plane is zero and the product skips it,
-        # so three limbs are counted (a tile that needs the fourth does more
-        # work than is counted here)
+        # int32 activations are the previous layer's ReLU outputs, in [0, 2^24):
+        # their top limb plane is zero and the product skips it (three limbs)
         LA = 2 if ab == 2 else 3
-        add("gemm_mfma", "mfma", 2 * n * m * k * LA * 2)
+        add("gemm_mfma", "mfma", 2 * n * m * k, ("mfma", 2 * n * m * k * LA * 2))
         add("bind_rows", "hbm", n * m * ab + 8 * m)
         add("bind_cols", "hbm", m * k * 2 + 8 * m)
-        # the fused front: both bindings read A and B once and write the eq
-        # tables (its limb split reads them again; that is the product's work)
         add("matmul_front", "hbm", n * m * ab + m * k * 2 + 8 * (n + k))
         add("witness_minmax", "hbm", 8 * N)
         add("witness_rescale", "hbm", N * (8 + 4 + 2 + 4 + 4 + 8))  # C in; R, Rm, Y, Z, bits out
-        # Gram matrix of the plane rounds: per output, tile pairs x 32 x 32 x 2 x 8 digits
         TP = 3 if P > 32 else 1
-        add("range_plane", "mfma", N * TP * 1024 * 2 * 8)
-        # rounds over x: per pair, 6 field products (range) and 7 (ReLU)
+        add("range_plane", "hbm", P * N // 8 + 8 * N, ("mfma", N * TP * 1024 * 2 * 8))
+        # rounds over x: per pair, 6 field products (range) and 7 (ReLU); each
+        # pass reads Bx (and R, Y as int32 in the first, D and S after) and
+        # writes them folded to 2^-C of their size
         lN = N.bit_length() - 1
         per_pair = 6 + 7 * relu
         regs, B, v = x_schedule(lN)
         j = 0
         for C in regs + ([B] if B else []):
             lS = lN - j
-            for c in range(C):
-                add("range_rounds", "alu", MULS_PER_FIELD_MUL * per_pair * (1 << (lS - c - 1)))
+            muls = sum(MULS_PER_FIELD_MUL * per_pair * (1 << (lS - c - 1)) for c in range(C))
             rd = (8 + 8 * relu) if j == 0 else (8 + 16 * relu)
-            add("range_rounds", "hbm", rd * (1 << lS) + (8 + 16 * relu) * (1 << (lS - C)), hbm2)
+            add("range_rounds", "hbm", rd * (1 << lS) + (8 + 16 * relu) * (1 << (lS - C)), ("alu", muls))
             j += C
         for jj in range(lN - j):
             add("range_tail", "alu", MULS_PER_FIELD_MUL * per_pair * (1 << (lN - j - jj - 1)))
@@ -121,7 +137,7 @@ def group_work(shapes, planes):
         for jj in range(lm):
             add("matmul_rounds" if lm - jj > MM_TAIL_LOG else "matmul_tail", "alu",
                 MULS_PER_FIELD_MUL * 5 * (1 << (lm - jj - 1)))
-    return w, hbm2
+    return w
 
 
 # Kernel -> group, for hardware-counter summaries (rocprofv3 kernel names).
@@ -190,26 +206,83 @@ def pmc_summary(fetch_csv, write_csv, cfg, steps_run, calib_mib):
                 groups=groups, fetch=out["FETCH_SIZE"][1], write=out["WRITE_SIZE"][1])
 
 
-def cpu_baseline(cfg):
-    """The oracle (single thread) on a bounded sample of the same workload."""
-    from oracle import oracle as orc
+def _oracle_sample(cfg):
+    """A bounded sample of workload cfg for the oracle, with the workload's
+    ratio of product work (n m k) to folded elements (about 2 P n k): that
+    ratio is m / (2 P) per layer, so the samples keep every layer's inner
+    dimension m and shrink the batch."""
     from paper_2505_17623_amd import inputs
     if cfg == 3:
-        wl, sample = inputs.cfg3(n=512), "one 512x512x512 layer of the same distribution (s=12, ReLU)"
-    elif cfg == 5:
-        wl, sample = inputs.cfg5(batch=64, d=1024), "MLP 1024-1024-1024 at batch 64, same distribution (s=12)"
-    elif cfg == 4:
-        wl, sample = inputs.cfg4(batch=4, H=32), "the same CNN at batch 4"
-    else:
-        wl, sample = inputs.workload(cfg, "full"), "the full workload"
-    orc.build(force=False)
+        return inputs.cfg3(n=1024), "the full 1024^3 layer"
+    if cfg == 5:
+        return inputs.cfg5(batch=128, d=4096), "MLP 4096-4096-4096 at batch 128 (same m and distribution, s=12)"
+    if cfg == 4:
+        return inputs.cfg4(batch=4, H=32), "the same CNN at batch 4"
+    return inputs.workload(cfg, "full"), "the full workload"
+
+
+def _oracle_worker(cfg):
+    """One oracle run of the sample (child process): (seconds, transcript digest)."""
+    import hashlib
+    from oracle import oracle as orc
+    wl, _ = _oracle_sample(cfg)
     t0 = time.perf_counter()
     res = orc.prove_network(wl)
     dt = time.perf_counter() - t0
-    shapes = layer_shapes(wl)
-    el = elements_folded(shapes, [r["P"] for r in res])
-    return dict(value=el / dt, unit="field elements folded/s", cores=1, kind="oracle",
-                sample=f"{sample}; {el} elements in {dt:.2f} s")
+    keys = ["t", "P", "c0", "mm_evals", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_claim",
+            "range_sum", "rs_evals", "bits_claim", "zc_evals", "r_at", "y_at"]
+    h = hashlib.sha256(json.dumps([[r[k] for k in keys] for r in res]).encode()).hexdigest()
+    return dt, h, [r["P"] for r in res]
+
+
+def host_cores():
+    """Host threads this process may use: the affinity set, at most the
+    16 a one-GPU machine gives a job."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, all_cores=True):
+    """The oracle as it stands (plain C, one thread per process) on a bounded
+    sample of the workload: once alone, then (all_cores) as one copy per host
+    thread in child processes, each checked to give the single run's
+    transcript.  The all-cores rate is copies x elements / wall time."""
+    import multiprocessing as mp
+    from oracle import oracle as orc
+    wl, sample = _oracle_sample(cfg)
+    orc.build(force=False)
+    dt, digest, planes = _oracle_worker(cfg)
+    el = elements_folded(layer_shapes(wl), planes)
+    out = dict(value=el / dt, unit="field elements folded/s", cores=1, kind="oracle",
+               sample=f"{sample}; {el} elements in {dt:.2f} s on one thread",
+               host=dict(cpu_model=cpu_model(), nproc=os.cpu_count(), usable_threads=host_cores()))
+    ncores = host_cores()
+    if all_cores and ncores > 1:
+        ctx = mp.get_context("spawn")  # fresh interpreters: nothing of this process's GPU state
+        t0 = time.perf_counter()
+        with ctx.Pool(ncores) as pool:
+            res = pool.map(_oracle_worker, [cfg] * ncores)
+        wall = time.perf_counter() - t0
+        assert all(h == digest for _, h, _ in res), "oracle copies disagree with the single run"
+        out.update(value=ncores * el / wall, cores=ncores,
+                   sample=out["sample"] + f"; all cores: {ncores} copies in {wall:.2f} s wall, transcripts "
+                   f"identical to the single run",
+                   single_thread_value=round(el / dt, 1))
+    return out
 
 
 def main():
@@ -217,7 +290,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5],
+                    help="workload (default 5: two 512x4096x4096 layers, the largest that fits one GPU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, copy a MIB-sized device buffer once (a plain copy kernel "
@@ -300,27 +374,36 @@ def main():
     el = elements_folded(shapes, planes)
     value = el * args.steps / elapsed
 
-    # roofline of the dominant kernel group
-    work, fold_bytes = group_work(shapes, planes)
+    # roofline of the dominant kernel group: its algorithmic work per launch
+    # (group_work) over its average launch time, measured with HIP events
+    # on the library's stream
+    work = group_work(shapes, planes)
+
+    def rate(bound, amount, s_per_step):
+        peak, unit, scale = PEAKS[bound]
+        a = amount / s_per_step / scale
+        return dict(bound=bound, achieved=round(a, 2), peak=peak, unit=unit, frac=round(a / peak, 4))
+
     dom = max((g for g in prof if g in work), key=lambda g: prof[g][0])
-    bound, amount = work[dom]
-    peak, runit, scale = PEAKS[bound]
     dom_ms, dom_launches = prof[dom]
-    dom_s_per_step = dom_ms / 1e3 / args.steps
-    achieved = amount / dom_s_per_step / scale
-    roofline = dict(kernel=dom, bound=bound, achieved=round(achieved, 2), peak=peak, unit=runit,
-                    frac=round(achieved / peak, 4), traffic=traffic_of(dom, args.config),
-                    launches_per_step=dom_launches / args.steps, ms_per_step=round(dom_ms / args.steps, 4))
+    per_step_s = dom_ms / 1e3 / args.steps
+    launches = dom_launches / args.steps
+    wd = work[dom]
+    traffic = traffic_of(dom, args.config)
+    roofline = dict(kernel=dom, **rate(wd["bound"], wd["amount"], per_step_s),
+                    traffic=None if traffic is None else round(traffic / launches),
+                    algorithmic_per_launch=round(wd["amount"] / launches), launches_per_step=launches,
+                    ms_per_launch=round(dom_ms / dom_launches, 5))
+    if wd["secondary"]:
+        roofline["secondary"] = rate(wd["secondary"][0], wd["secondary"][1], per_step_s)
     groups = {g: dict(ms_per_step=round(v[0] / args.steps, 4), launches_per_step=v[1] / args.steps)
               for g, v in sorted(prof.items(), key=lambda kv: -kv[1][0]) if v[1]}
     for g, d in groups.items():
         s_per = d["ms_per_step"] / 1e3
         if g in work and s_per > 0:
-            b, a = work[g]
-            pk, u, sc = PEAKS[b]
-            d.update(bound=b, achieved=round(a / s_per / sc, 2), unit=u, frac=round(a / s_per / sc / pk, 4))
-        if g in fold_bytes and s_per > 0:
-            d["hbm_frac"] = round(fold_bytes[g][1] / s_per / 1e9 / PEAKS["hbm"][0], 4)
+            d.update(rate(work[g]["bound"], work[g]["amount"], s_per))
+            if work[g]["secondary"]:
+                d["secondary"] = rate(work[g]["secondary"][0], work[g]["secondary"][1], s_per)
 
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device=dev).fill_(1)

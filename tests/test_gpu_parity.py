@@ -275,3 +275,51 @@ def test_two_register_passes_verified(ra):
     ev = list(tr["rs_evals"])
     ev[0] = (int(ev[0]) + 1) % P61
     assert ra.ra_verify(chal, [dict(L, transcript=dict(tr, rs_evals=ev))])[0] != 0
+
+
+@pytest.mark.parametrize("kind", ["int16", "int32_relu", "int32_full"])
+def test_product_large_layer(ra, kind):
+    """A 512 x 128 x 4096 layer (512 product tiles, two per CU, 2^21 outputs):
+    C against numpy's exact int64 product.  int16 (ReLU) and int32_relu
+    (every entry in [0, 2^24), so the tiles skip the top limb plane; no ReLU
+    so that t stays within this path's limits) also run the witness fused
+    into the epilogue (t given, deferred), checked against a numpy rescale,
+    and the whole layer must be accepted by the host verifier (which opens A,
+    B, R, Rm, Y, Z and checks the rounding link against the matrix claim).
+    int32_full: entries over the whole int32 range with its extremes (t would
+    exceed this path's limit of 29, so only the product is checked)."""
+    n, m, k, s = 512, 128, 4096, 16
+    rng = np.random.default_rng({"int16": 1, "int32_relu": 2, "int32_full": 3}[kind])
+    if kind == "int16":
+        A = rng.integers(-32768, 32768, size=(n, m)).astype(np.int16)
+        A.flat[:2] = [-32768, 32767]
+    elif kind == "int32_relu":
+        A = rng.integers(0, 1 << 24, size=(n, m)).astype(np.int32)
+    else:
+        A = rng.integers(-(2 ** 31), 2 ** 31, size=(n, m), dtype=np.int64).astype(np.int32)
+        A.flat[:3] = [-(2 ** 31), 2 ** 31 - 1, 0]
+    B = rng.integers(-32768, 32768, size=(m, k)).astype(np.int16)
+    B.flat[:2] = [-32768, 32767]
+    Cw = A.astype(np.int64) @ B.astype(np.int64)            # |C| <= 128 * 2^46 fits int64
+    seed = 0xC0FFEE + len(kind)
+    if kind == "int32_full":
+        ctx = ra.Context(seed=seed)
+        C, _ = ra.ra_sumcheck_matmul_prove(ctx, torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
+        assert np.array_equal(C.cpu().numpy(), Cw)
+        return
+    relu = kind == "int16"
+    half = 1 << (s - 1)
+    R = (Cw + half) >> s                                     # nearest: floor((C + 2^(s-1)) / 2^s)
+    u = np.where(R >= 0, R, -R - 1).max()
+    t = max(0, int(u).bit_length() - 1)
+    assert s + (t + 2) * (1 + relu) <= 64 and t <= 29
+    ctx = ra.Context(seed=seed, deferred=True)
+    g = ra.prove_layer(ctx, torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda(), s, relu, 0, t)
+    ctx.sync()
+    assert np.array_equal(g["C"].cpu().numpy(), Cw)
+    assert np.array_equal(g["R"].cpu().numpy().astype(np.int64), R)
+    assert np.array_equal(g["Rm"].cpu().numpy().view(np.uint16).astype(np.int64), (Cw + half) & ((1 << s) - 1))
+    assert np.array_equal(g["Z"].cpu().numpy().astype(np.int64), np.maximum(R, 0) if relu else R)
+    L = dict(A=A, B=B, Z=g["Z"].cpu().numpy(), R=g["R"].cpu().numpy(), Rm=g["Rm"].cpu().numpy(),
+             Y=g["Y"].cpu().numpy(), bits=g["bits"].cpu().numpy(), transcript=g["transcript"], chained=False)
+    assert ra.ra_verify(seed, [L]) == (0, 0)

@@ -18,6 +18,7 @@ import numpy as np
 P61 = (1 << 61) - 1
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ra_oracle.c")
+_SRC2 = os.path.join(_HERE, "ra_oracle_fp2.c")   # the same protocol with challenges in F_{p^2}
 _LIB = os.path.join(_HERE, "libra_oracle.so")
 _lib = None
 
@@ -36,7 +37,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC",
-                        _SRC, "-o", tmp], check=True)
+                        _SRC, _SRC2, "-o", tmp], check=True)
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -52,10 +53,28 @@ class LayerInfo(ctypes.Structure):
                 ("r_at", ctypes.c_uint64), ("y_at", ctypes.c_uint64)]
 
 
+class F2(ctypes.Structure):
+    _fields_ = [("re", ctypes.c_uint64), ("im", ctypes.c_uint64)]
+
+
+class LayerInfo2(ctypes.Structure):
+    """orc2_layer_info: the scalars of a layer's transcript over F_{p^2}."""
+    _fields_ = [("t", ctypes.c_int32), ("P", ctypes.c_int32), ("log_p", ctypes.c_int32),
+                ("n_mm_rounds", ctypes.c_int32), ("n_rs_rounds", ctypes.c_int32),
+                ("n_zc_rounds", ctypes.c_int32), ("challenges_used", ctypes.c_int64)] + \
+        [(k, F2) for k in ("c0", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_claim",
+                           "range_sum", "bits_claim", "r_at", "y_at")]
+
+
+F2_SCALARS = ("c0", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_claim", "range_sum", "bits_claim",
+              "r_at", "y_at")
+
+
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC),
+                                                                       os.path.getmtime(_SRC2)):
             build()
         L = ctypes.CDLL(_LIB)
         u64p = ctypes.POINTER(ctypes.c_uint64)
@@ -78,6 +97,13 @@ def lib():
                                                         ctypes.POINTER(LayerInfo)]
         L.orc_verify_layer.argtypes = [ctypes.c_int64] * 3 + [i64p] * 3 + [ctypes.c_int] * 3 + \
             [i64p] * 4 + [u64p] * 3 + [ctypes.POINTER(LayerInfo), u64p, ctypes.c_int64, i64p]
+        L.orc2_mul.argtypes = [u64p, u64p, u64p]
+        L.orc2_inv.argtypes = [u64p, u64p]
+        L.orc2_mle_int.argtypes = [i64p, ctypes.c_int, u64p, u64p]
+        L.orc2_prove_layer.argtypes = [ctypes.c_int64] * 3 + [i64p, i64p] + [ctypes.c_int] * 4 + \
+            [u64p, ctypes.c_int64, i64p] + [i64p] * 5 + [u8p, u64p, u64p, u64p, ctypes.POINTER(LayerInfo2)]
+        L.orc2_verify_layer.argtypes = [ctypes.c_int64] * 3 + [i64p] * 3 + [ctypes.c_int] * 3 + \
+            [i64p] * 4 + [u64p] * 3 + [ctypes.POINTER(LayerInfo2), u64p, ctypes.c_int64, i64p]
         _lib = L
     return _lib
 
@@ -237,3 +263,129 @@ def prove_network(workload, layers_out=None):
         Z = res["Z"]
         results.append(res)
     return results
+
+
+# --- the protocol over F_{p^2} (ra_oracle_fp2.c) ----------------------------
+# Field elements of F_{p^2} = F_p[i] / (i^2 + 1) are pairs (re, im).
+def f2mul(a, b):
+    x, y, out = _u64(list(a)), _u64(list(b)), np.zeros(2, dtype=np.uint64)
+    lib().orc2_mul(_ptr(x, ctypes.c_uint64), _ptr(y, ctypes.c_uint64), _ptr(out, ctypes.c_uint64))
+    return int(out[0]), int(out[1])
+
+
+def f2inv(a):
+    x, out = _u64(list(a)), np.zeros(2, dtype=np.uint64)
+    lib().orc2_inv(_ptr(x, ctypes.c_uint64), _ptr(out, ctypes.c_uint64))
+    return int(out[0]), int(out[1])
+
+
+def mle_int_fp2(table, z):
+    """MLE of an integer table at a point of F_{p^2}^v (list of pairs)."""
+    t = _i64(np.asarray(table).reshape(-1))
+    assert t.size == 1 << len(z)
+    zz = _u64([c for pair in z for c in pair] or [0])
+    out = np.zeros(2, dtype=np.uint64)
+    lib().orc2_mle_int(_ptr(t, ctypes.c_int64), len(z), _ptr(zz, ctypes.c_uint64), _ptr(out, ctypes.c_uint64))
+    return int(out[0]), int(out[1])
+
+
+def _pairs(a, n):
+    return [(int(a[2 * i]), int(a[2 * i + 1])) for i in range(n)]
+
+
+def prove_layer_fp2(A, B, s, relu, mode, chal, cursor=0, t_in=-1):
+    """Prove one layer with challenges in F_{p^2} (pairs of consecutive words
+    of the F_p stream `chal`, from word `cursor`).  Returns a dict like
+    prove_layer's, with every transcript element a pair (re, im)."""
+    A = _i64(A)
+    B = _i64(B)
+    n, m = A.shape
+    k = B.shape[1]
+    N = n * k
+    chal = _u64(chal)
+    cur = np.array([cursor], dtype=np.int64)
+    C, R, Rm, Y, Z = (np.zeros(N, dtype=np.int64) for _ in range(5))
+    bits = np.zeros(128 * N, dtype=np.uint8)
+    lm = m.bit_length() - 1
+    lN = N.bit_length() - 1
+    mm = np.zeros(2 * 3 * max(lm, 1), dtype=np.uint64)
+    rs = np.zeros(2 * 4 * (lN + 7), dtype=np.uint64)
+    zc = np.zeros(2 * 4 * max(lN, 1), dtype=np.uint64)
+    info = LayerInfo2()
+    i64 = ctypes.c_int64
+    rc = lib().orc2_prove_layer(n, m, k, _ptr(A, i64), _ptr(B, i64), s, int(bool(relu)), mode, t_in,
+                                _ptr(chal, ctypes.c_uint64), len(chal), _ptr(cur, i64),
+                                _ptr(C, i64), _ptr(R, i64), _ptr(Rm, i64), _ptr(Y, i64), _ptr(Z, i64),
+                                _ptr(bits, ctypes.c_uint8), _ptr(mm, ctypes.c_uint64),
+                                _ptr(rs, ctypes.c_uint64), _ptr(zc, ctypes.c_uint64), ctypes.byref(info))
+    if rc != 0:
+        raise OracleError(rc)
+    P = info.P
+    out = dict(n=n, m=m, k=k, s=s, relu=int(bool(relu)), mode=mode,
+               C=C.reshape(n, k), R=R.reshape(n, k), Rm=Rm.reshape(n, k), Y=Y.reshape(n, k),
+               Z=Z.reshape(n, k), bits=bits[:P * N].reshape(P, N).copy(),
+               t=info.t, P=P, cursor=int(cur[0]), challenges_used=int(info.challenges_used),
+               mm_evals=_pairs(mm, 3 * info.n_mm_rounds), rs_evals=_pairs(rs, 4 * info.n_rs_rounds),
+               zc_evals=_pairs(zc, 4 * info.n_zc_rounds))
+    for key in F2_SCALARS:
+        v = getattr(info, key)
+        out[key] = (int(v.re), int(v.im))
+    return out
+
+
+def verify_layer_fp2(A, B, Z, s, relu, mode, R, Rm, Y, bits, tr, chal, cursor=0):
+    """The F_{p^2} verifier (checks numbered as verify_layer); returns (verdict, new_cursor)."""
+    A = _i64(A)
+    B = _i64(B)
+    n, m = A.shape
+    k = B.shape[1]
+    N = n * k
+    lm = m.bit_length() - 1
+    lN = N.bit_length() - 1
+    info = LayerInfo2()
+    info.t = tr["t"]
+    info.P = tr["P"]
+    for key in F2_SCALARS:
+        re, im = tr[key]
+        setattr(info, key, F2(int(re) & 0xFFFFFFFFFFFFFFFF, int(im) & 0xFFFFFFFFFFFFFFFF))
+    flat = lambda ev, pad: _u64(np.array([c for pair in ev for c in pair] + [0] * pad, dtype=object).astype(np.uint64))
+    mm, rs, zc = flat(tr["mm_evals"], 6), flat(tr["rs_evals"], 8), flat(tr["zc_evals"], 8)
+    want_rs = 4 * (int(tr["P"]).bit_length() - 1 + lN)
+    if len(tr["mm_evals"]) != 3 * lm or len(tr["rs_evals"]) != want_rs or \
+            len(tr["zc_evals"]) != (4 * lN if relu else 0):
+        return 13, cursor
+    bits = _i64(np.asarray(bits).reshape(-1))
+    if bits.size != int(tr["P"]) * N:
+        return 12, cursor
+    chal = _u64(chal)
+    cur = np.array([cursor], dtype=np.int64)
+    i64 = ctypes.c_int64
+    arrs = [_i64(np.asarray(x).reshape(-1)) for x in (Z, R, Rm, Y)]
+    v = lib().orc2_verify_layer(n, m, k, _ptr(A, i64), _ptr(B, i64), _ptr(arrs[0], i64), s,
+                                int(bool(relu)), mode, _ptr(arrs[1], i64), _ptr(arrs[2], i64),
+                                _ptr(arrs[3], i64), _ptr(bits, i64), _ptr(mm, ctypes.c_uint64),
+                                _ptr(rs, ctypes.c_uint64), _ptr(zc, ctypes.c_uint64), ctypes.byref(info),
+                                _ptr(chal, ctypes.c_uint64), len(chal), _ptr(cur, i64))
+    return int(v), int(cur[0])
+
+
+def prove_network_fp2(workload):
+    """Every layer of a workload over F_{p^2}, the stream read in pairs."""
+    results = []
+    cursor = 0
+    Z = None
+    chal = fp2_stream(workload)
+    for li, layer in enumerate(workload.layers):
+        A = workload.layer_input(li, Z)
+        res = prove_layer_fp2(A, layer.B, layer.s, layer.relu, workload.mode, chal, cursor)
+        cursor = res["cursor"]
+        res["A"] = A
+        Z = res["Z"]
+        results.append(res)
+    return results
+
+
+def fp2_stream(workload):
+    """The F_p stream a workload's F_{p^2} proof reads: twice the draws of its F_p proof."""
+    from paper_2505_17623_amd import inputs
+    return inputs.xorshift64_stream(workload.challenge_seed, 2 * len(workload.challenges))

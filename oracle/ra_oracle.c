@@ -309,27 +309,19 @@ static void plane_weights(uint64_t *W, int P, int s, int t, int relu, const uint
 }
 
 /*
- * Prove one layer.  Inputs: A (n x m), B (m x k) as int64 (values that fit the
- * layer's dtypes), s fractional bits, relu flag, mode (0 = rounding operator
- * of Sec. II-A, 1 = floor), t_in (< 0: least t that holds R; else given).
- * The challenge stream chal[0..nchal) is consumed from *cursor in this order:
- *   r1 (log n), r2 (log k), rho (log m), lambda1..3, mu, tau_p (log P),
- *   sigma (log P + log N), and with ReLU rho' (log N).
- * Outputs: C, R, Rm, Y, Z (n*k each), bits (P*N bytes, plane-major; the buffer
- * must hold 128*N bytes), transcript arrays mm_evals (3 per round), rs_evals
- * (4 per round), zc_evals (4 per round) and the scalars in *info.
+ * The layer's witness (Alg. 1 steps 2 and 9, Sec. III-B) and its range
+ * parameters: C = A B over the integers, R = the rounding of C (mode 0: the
+ * operator of Sec. II-A; 1: floor), the shifted remainder Rm, Y = |R|, the
+ * output Z, the least t >= 0 with -2^(t+1) <= R < 2^(t+1) (t_in >= 0: that
+ * t, checked), the field guard s + t + 3 <= 61 (Theorem A.1) and the plane
+ * count P (a power of two).  Shared by the prover over F_p below and the one
+ * over F_{p^2} (ra_oracle_fp2.c): the witness does not depend on the field.
  */
-int orc_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, int s, int relu,
-                    int mode, int t_in, const uint64_t *chal, int64_t nchal, int64_t *cursor, int64_t *C,
-                    int64_t *R, int64_t *Rm, int64_t *Y, int64_t *Z, uint8_t *bits, uint64_t *mm_evals,
-                    uint64_t *rs_evals, uint64_t *zc_evals, orc_layer_info *info)
+int orc_layer_witness(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, int s, int relu,
+                      int mode, int t_in, int64_t *C, int64_t *R, int64_t *Rm, int64_t *Y, int64_t *Z, int *t_out,
+                      int *P_out, int *lP_out)
 {
-    int ln = ilog2_exact(n), lm = ilog2_exact(m), lk = ilog2_exact(k);
-    if (ln < 0 || lm < 0 || lk < 0 || s < 1 || s > 30 || (mode != 0 && mode != 1)) return ORC_E_INVAL;
     int64_t N = n * k;
-    int lN = ln + lk;
-    memset(info, 0, sizeof(*info));
-
     /* Witness: C = A B over the integers (Alg. 1 step 2). */
     for (int64_t i = 0; i < n; i++)
         for (int64_t j = 0; j < k; j++) C[i * k + j] = 0;
@@ -366,6 +358,46 @@ int orc_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const int
     int P = 1, lP = 0;
     while (P < Q) { P *= 2; lP++; }
     if (P > 128) return ORC_E_RANGE;
+    *t_out = t;
+    *P_out = P;
+    *lP_out = lP;
+    return ORC_OK;
+}
+
+/* The bit table of a layer, exported for the F_{p^2} prover. */
+void orc_fill_planes(uint8_t *bits, int64_t N, int P, int s, int t, int relu, const int64_t *R, const int64_t *Rm,
+                     const int64_t *Y)
+{
+    fill_planes(bits, N, P, s, t, relu, R, Rm, Y);
+}
+
+/*
+ * Prove one layer.  Inputs: A (n x m), B (m x k) as int64 (values that fit the
+ * layer's dtypes), s fractional bits, relu flag, mode (0 = rounding operator
+ * of Sec. II-A, 1 = floor), t_in (< 0: least t that holds R; else given).
+ * The challenge stream chal[0..nchal) is consumed from *cursor in this order:
+ *   r1 (log n), r2 (log k), rho (log m), lambda1..3, mu, tau_p (log P),
+ *   sigma (log P + log N), and with ReLU rho' (log N).
+ * Outputs: C, R, Rm, Y, Z (n*k each), bits (P*N bytes, plane-major; the buffer
+ * must hold 128*N bytes), transcript arrays mm_evals (3 per round), rs_evals
+ * (4 per round), zc_evals (4 per round) and the scalars in *info.
+ */
+int orc_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, int s, int relu,
+                    int mode, int t_in, const uint64_t *chal, int64_t nchal, int64_t *cursor, int64_t *C,
+                    int64_t *R, int64_t *Rm, int64_t *Y, int64_t *Z, uint8_t *bits, uint64_t *mm_evals,
+                    uint64_t *rs_evals, uint64_t *zc_evals, orc_layer_info *info)
+{
+    int ln = ilog2_exact(n), lm = ilog2_exact(m), lk = ilog2_exact(k);
+    if (ln < 0 || lm < 0 || lk < 0 || s < 1 || s > 30 || (mode != 0 && mode != 1)) return ORC_E_INVAL;
+    int64_t N = n * k;
+    int lN = ln + lk;
+    memset(info, 0, sizeof(*info));
+
+    int t = 0, P = 1, lP = 0;
+    {
+        int rc = orc_layer_witness(n, m, k, A, B, s, relu, mode, t_in, C, R, Rm, Y, Z, &t, &P, &lP);
+        if (rc != ORC_OK) return rc;
+    }
     info->t = t;
     info->P = P;
     info->log_p = lP;

@@ -23,6 +23,7 @@ entries per table over its v rounds.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -293,6 +294,9 @@ def main():
     ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5],
                     help="workload (default 5: two 512x4096x4096 layers, the largest that fits one GPU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fp2-steps", type=int, default=10,
+                    help="after the timed region, time this many steps of the same workload proven with "
+                         "challenges in F_{p^2} (reported beside the headline; 0 skips it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, copy a MIB-sized device buffer once (a plain copy kernel "
                          "of known size, to scale hardware byte counters)")
@@ -351,7 +355,12 @@ def main():
         ctx.sync()
         assert all([o["transcript"]["P"] for o in out] == planes for out in outs)
 
-    # timed region: K steps enqueued back to back, completed by one sync
+    # timed region: K steps enqueued back to back, completed by one sync.
+    # The heap built so far (transcripts of the untimed passes) is collected
+    # and frozen first, so that a full garbage collection over it cannot
+    # stall the host inside the timed steps.
+    gc.collect()
+    gc.freeze()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     outs = [ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs) for _ in range(args.steps)]
@@ -405,6 +414,30 @@ def main():
             if work[g]["secondary"]:
                 d["secondary"] = rate(work[g]["secondary"][0], work[g]["secondary"][1], s_per)
 
+    # the same workload with challenges in F_{p^2} (soundness error squared):
+    # each layer call waits for its work, t given, buffers kept across steps
+    fp2 = None
+    if args.fp2_steps > 0:
+        ctx2 = ra.Context(seed=wl.challenge_seed)
+        bufs2 = []
+        for _ in range(2):
+            ra.prove_network_fp2(ctx2, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs2)
+        gc.collect()
+        gc.freeze()
+        torch.cuda.synchronize()
+        u0 = time.perf_counter()
+        outs2 = [ra.prove_network_fp2(ctx2, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs2) for _ in range(args.fp2_steps)]
+        torch.cuda.synchronize()
+        el2 = time.perf_counter() - u0
+        assert all([o["transcript"]["P"] for o in out] == planes for out in outs2)
+        ms2 = 1e3 * el2 / args.fp2_steps
+        fp2 = dict(field="F_p[i]/(i^2+1)", steps=args.fp2_steps, ms_per_step=round(ms2, 4),
+                   ms_per_layer=round(ms2 / L, 4), value=round(el * args.fp2_steps / el2, 1),
+                   unit="field elements folded/s", vs_fp_ms=round(ms2 / ms_step, 3),
+                   note="synchronous per layer (each call waits); not the headline")
+        del outs2, bufs2, ctx2
+        print(f"# F_p^2 leg: {ms2:.3f} ms per step", file=sys.stderr, flush=True)
+
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -426,7 +459,7 @@ def main():
                config=dict(workload=f"config {args.config}: {wl.name}", layers=L,
                            shapes=[list(s[:3]) for s in shapes], planes=planes,
                            elements_folded_per_step=el),
-               roofline=roofline, cpu_baseline=cpu, kernel_groups=groups)
+               roofline=roofline, cpu_baseline=cpu, kernel_groups=groups, field_fp2=fp2)
     print(json.dumps(rec), flush=True)
 
 

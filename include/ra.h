@@ -285,6 +285,49 @@ ra_status ra_range_prove(ra_ctx *ctx, const uint64_t *d_bits, const int32_t *d_R
                          uint32_t k, const ra_witness_info *info, void *d_ws, size_t ws_bytes,
                          ra_range_proof *out);
 
+/* ---- The protocol with challenges in the extension field F_{p^2} ----------
+ * Sec. II-F asks for a field of more than 128 bits.  Over p = 2^61 - 1 a
+ * cheating prover passes a sum-check round with probability about d / p
+ * (Sec. II-D); with the verifier's challenges drawn from F_{p^2} = F_p[i] /
+ * (i^2 + 1) (p = 3 mod 4, so x^2 + 1 is irreducible) it is about d / p^2,
+ * about 2^-120 per round.  The witness (C, R, Rm, Y, Z, the bit table) is the
+ * same integer data; every challenge-dependent value is an element of F_{p^2}.
+ * Challenge j is read from the context's F_p stream as two consecutive
+ * words, stream[2j] + stream[2j + 1] i, in the order of the F_p protocol. */
+typedef struct {
+    uint64_t re, im; /* re + im i, both in [0, p) */
+} ra_fp2;
+
+typedef struct {
+    uint32_t s, relu, round_mode; /* in, as ra_witness_info */
+    int32_t t;                    /* in: -1 = least t holding R, >= 0 = given; out: t used */
+    uint32_t P;                   /* out: bit planes */
+    uint32_t log_m;               /* out: rounds of the matrix instance */
+    ra_fp2 c0, a_star, b_star;    /* out: as ra_matmul_proof */
+    ra_fp2 *mm_evals;             /* in: host buffer of 3 log m elements; out: g_j(0..2) */
+    ra_fp2 r_claim, rm_claim, y_claim, z_claim; /* out: R~, Rm~, Y~, Z~ at (r1, r2) */
+    uint32_t rounds;              /* out: log P + log N */
+    ra_fp2 *rs_evals;             /* in: host buffer of 4 (6 + log N) elements; out: g_j(0..3) */
+    ra_fp2 range_sum, bits_claim; /* out */
+    uint32_t relu_rounds;         /* out: log N with ReLU, else 0 */
+    ra_fp2 *zc_evals;             /* in: host buffer of 4 log N elements (ReLU); out */
+    ra_fp2 r_at, y_at;            /* out: R~(rho'), Y~(rho') */
+} ra_layer_proof_fp2;
+
+/* One whole layer (the three calls of the F_p protocol) with challenges in
+ * F_{p^2}: the exact product d_C, the witness d_R, d_Rm, d_Y, d_Z, d_bits
+ * (as ra_rescale_relu_witness), the matrix sum-check, the claims, the range
+ * sum-check and with ReLU the zero-check, every transcript element in
+ * F_{p^2}.  Call it between layers (RA_E_STATE otherwise); it waits for its
+ * work and consumes 2 (log n + log k + log m + 4 + 2 log P + log N (1 + relu))
+ * words of the stream.  Workspace as for the proving calls
+ * (ra_workspace_size_fp2).  Errors and limits as for the three F_p calls. */
+ra_status ra_prove_layer_fp2(ra_ctx *ctx, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
+                             uint32_t m, uint32_t k, int64_t *d_C, int32_t *d_R, uint16_t *d_Rm, int32_t *d_Y,
+                             int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words, void *d_ws, size_t ws_bytes,
+                             ra_layer_proof_fp2 *io);
+ra_status ra_workspace_size_fp2(uint32_t n, uint32_t m, uint32_t k, size_t *bytes);
+
 /* Public data of one layer for the verifier (host pointers). */
 typedef struct {
     uint32_t n, m, k;
@@ -332,6 +375,14 @@ ra_status ra_verify(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_layer
 ra_status ra_verify_stream(uint64_t p, const uint64_t *h_challenges, uint64_t n_challenges, uint32_t n_layers,
                            const ra_layer_public *pub, const ra_layer_tables *tables,
                            const ra_layer_transcript *tr, int32_t *verdict, uint32_t *failed_layer);
+
+/* The host verifier for layers proven over F_{p^2} (ra_prove_layer_fp2): the
+ * checks of ra_verify with the same verdict numbers, every transcript element
+ * a pair (re, im) in [0, p), the challenges read from the stream of `seed` in
+ * pairs. */
+ra_status ra_verify_fp2(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_layer_public *pub,
+                        const ra_layer_tables *tables, const ra_layer_proof_fp2 *tr, int32_t *verdict,
+                        uint32_t *failed_layer);
 
 #ifdef __cplusplus
 }

@@ -441,9 +441,59 @@ RangeLayout range_layout(uint64_t N, int lP, int relu)
     l.bytes = cv.off;
     return l;
 }
+// Workspace pieces of a layer proven over F_{p^2} (sized for P = 64), and
+// the device transcript's word offsets: c0, a*, b* (0-5), the claims R~, Rm~,
+// Y~, Z~ (6-13), the range instance's claimed sum (14-15), b~(sigma)
+// (16-17), r_at, y_at (18-21), then the matrix rounds (6 words each), the
+// range rounds (8 each, for up to 6 + log N) and the ReLU rounds (8 each).
+constexpr int kF2TrFixed = 22;
+struct Fp2Layout {
+    size_t o_gemm, o_e1, o_e2, o_scr, o_a, o_b, o_eq, o_eqr, o_eqz, o_bx, o_d, o_s, o_sig, o_one, o_gp0, o_gp1, o_g,
+        o_part, o_cpart, o_cst, o_tr, tr_words, bytes;
+};
+Fp2Layout fp2_layout(bool a_i32, uint32_t n, uint32_t m, uint32_t k)
+{
+    const uint64_t N = (uint64_t)n * k, H = N > 1 ? N / 2 : 1;
+    const int lm = log2u(m), lN = log2u(N);
+    const int gt = plane_gram_tiles(kMaxPlaneLog), gb = plane_gram_blocks(N, kMaxPlaneLog);
+    Carve cv;
+    Fp2Layout l;
+    l.o_gemm = cv.take<char>(gemm_workspace_bytes(a_i32, n, m, k));
+    l.o_e1 = cv.take<uint64_t>(2 * (size_t)n);
+    l.o_e2 = cv.take<uint64_t>(2 * (size_t)k);
+    l.o_scr = cv.take<uint64_t>((size_t)bind_rows_chunks(n, m) * m);
+    l.o_a = cv.take<uint64_t>(2 * (size_t)m);
+    l.o_b = cv.take<uint64_t>(2 * (size_t)m);
+    l.o_eq = cv.take<uint64_t>(2 * N);
+    l.o_eqr = cv.take<uint64_t>(2 * H);
+    l.o_eqz = cv.take<uint64_t>(2 * H);
+    l.o_bx = cv.take<uint64_t>(2 * N);
+    l.o_d = cv.take<uint64_t>(2 * H);
+    l.o_s = cv.take<uint64_t>(2 * H);
+    l.o_sig = cv.take<uint64_t>(2 * 64);
+    l.o_one = cv.take<uint64_t>(2);
+    l.o_gp0 = cv.take<uint64_t>((size_t)gb * gt * 1024);
+    l.o_gp1 = cv.take<uint64_t>((size_t)gb * gt * 1024);
+    l.o_g = cv.take<uint64_t>(2 * 4096);
+    l.o_part = cv.take<uint64_t>((size_t)(lm + 2 * lN + 1) * kF2MaxBlocks * 8);
+    l.o_cpart = cv.take<uint64_t>((size_t)kF2MaxBlocks * 8);
+    l.o_cst = cv.take<uint64_t>(8);
+    l.tr_words = kF2TrFixed + 6 * (size_t)lm + 8 * (size_t)(kMaxPlaneLog + lN) + 8 * (size_t)lN;
+    l.o_tr = cv.take<uint64_t>(l.tr_words);
+    l.bytes = cv.off;
+    return l;
+}
 }  // namespace
 
 extern "C" {
+
+ra_status ra_workspace_size_fp2(uint32_t n, uint32_t m, uint32_t k, size_t *bytes)
+{
+    if (!bytes || !is_pow2(n) || !is_pow2(m) || !is_pow2(k)) return RA_E_INVAL;
+    if (m > kGemmMaxInner || (uint64_t)n * k > kRangeMaxN) return RA_E_NOT_IMPLEMENTED;
+    *bytes = fp2_layout(true, n, m, k).bytes;
+    return RA_OK;
+}
 
 ra_status ra_workspace_size(uint32_t n, uint32_t m, uint32_t k, uint32_t P, size_t *bytes)
 {
@@ -1001,6 +1051,234 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
         }
         return (ra_status)RA_OK;
     });
+}
+
+ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
+                             uint32_t m, uint32_t k, int64_t *d_C, int32_t *d_R, uint16_t *d_Rm, int32_t *d_Y,
+                             int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words, void *d_ws, size_t ws_bytes,
+                             ra_layer_proof_fp2 *io)
+{
+    if (!c || !d_A || !d_B || !d_C || !d_R || !d_Rm || !d_Y || !d_Z || !d_bits || !io) return RA_E_INVAL;
+    if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k)) return RA_E_INVAL;
+    if (a_dtype != RA_I16 && a_dtype != RA_I32) return RA_E_INVAL;
+    if (io->s < 1 || io->relu > 1 || io->round_mode > 1 || io->t < -1) return RA_E_INVAL;
+    if (m > kGemmMaxInner || (uint64_t)n * k > kRangeMaxN || io->s > 16) return RA_E_NOT_IMPLEMENTED;
+    if (c->phase != 0) return RA_E_STATE;
+    const uint64_t N = (uint64_t)n * k;
+    if (bits_words < N) return RA_E_BUFSIZE;
+    const int ln = log2u(n), lm = log2u(m), lk = log2u(k), lN = ln + lk, relu = (int)io->relu;
+    if ((lm && !io->mm_evals) || !io->rs_evals || (relu && lN && !io->zc_evals)) return RA_E_INVAL;
+    ra_status st = drain(c);  // a synchronous call: earlier deferred outputs are completed first
+    if (st != RA_OK && c->deferred_err == RA_OK) c->deferred_err = st;
+    const Fp2Layout L = fp2_layout(a_dtype == RA_I32, n, m, k);
+    char *ws = nullptr;
+    if ((st = call_ws(c, d_ws, ws_bytes, L.bytes, &ws)) != RA_OK) return st;
+    hipStream_t s = c->stream;
+    auto tab = [&](size_t off, size_t len) {
+        uint64_t *b = (uint64_t *)(ws + off);
+        return F2Tab{b, b + len};
+    };
+    const uint64_t H = N > 1 ? N / 2 : 1;
+    const F2Tab E1 = tab(L.o_e1, n), E2 = tab(L.o_e2, k), Ta = tab(L.o_a, m), Tb = tab(L.o_b, m);
+    const F2Tab EQ = tab(L.o_eq, N), EQr = tab(L.o_eqr, H), EQz = tab(L.o_eqz, H), Bx = tab(L.o_bx, N);
+    const F2Tab Dt = tab(L.o_d, H), St = tab(L.o_s, H), SIG = tab(L.o_sig, 64), ONE = tab(L.o_one, 1);
+    uint64_t *scr = (uint64_t *)(ws + L.o_scr), *part = (uint64_t *)(ws + L.o_part);
+    uint64_t *cpart = (uint64_t *)(ws + L.o_cpart), *cst = (uint64_t *)(ws + L.o_cst);
+    uint64_t *tr = (uint64_t *)(ws + L.o_tr), *Gre = (uint64_t *)(ws + L.o_g), *Gim = Gre + 4096;
+    const size_t pstride = (size_t)kF2MaxBlocks * 8;
+
+    // the witness: the exact product, then t and P (given: fixed on the host)
+    launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, ws + L.o_gemm, s, nullptr, nullptr, false, nullptr);
+    int P = 0, lP = 0, t = io->t;
+    WitParams hp{};
+    if (t >= 0) {
+        if ((st = plane_params((int)io->s, t, relu, &P, &lP)) != RA_OK) return st;
+        hp.status = 0;
+        hp.t = t;
+        hp.P = P;
+        hp.lP = lP;
+        hp.s = (int)io->s;
+        hp.relu = relu;
+        hp.mode = (int)io->round_mode;
+        hp.t_in = t;
+    } else {
+        launch_witness_params(d_C, N, (int)io->s, relu, (int)io->round_mode, -1, (int64_t *)(c->d_wit + kWitMinMax),
+                              c->d_params, s);
+        WitParams got;
+        RA_HIP(hipMemcpyAsync(&got, c->d_params, sizeof(got), hipMemcpyDeviceToHost, s));
+        RA_HIP(hipStreamSynchronize(s));
+        if (got.status != 0) return got.status;
+        t = got.t;
+        P = got.P;
+        lP = got.lP;
+    }
+    // the challenges, two words each
+    const uint64_t cnt = (uint64_t)ln + lk + lm + 4 + 2 * lP + lN + (relu ? lN : 0);
+    if ((st = ensure_chal(c, 2 * cnt)) != RA_OK) return st;
+    const uint64_t *r1 = c->d_chal + c->cursor, *r2 = r1 + 2 * ln, *rho = r2 + 2 * lk, *lam = rho + 2 * lm;
+    const uint64_t *tau = lam + 8, *sig = tau + 2 * lP, *rho2 = sig + 2 * (lP + lN);
+
+    launch_f2_eq(r1, ln, E1, s);
+    launch_f2_eq(r2, lk, E2, s);
+    // R, Rm, Y, Z, the bit table (the F_p claims this pass also forms are not used)
+    launch_witness_rescale(d_C, N, lk, E1.re, E2.re, d_R, d_Rm, d_Y, d_Z, d_bits, (uint64_t *)(c->d_wit + kWitClaims),
+                           c->d_params, c->d_claims, nullptr, s, io->t >= 0 ? &hp : nullptr,
+                           (uint32_t *)(c->d_wit + kWitFlags), nullptr);
+
+    // matrix instance: a = the rows of A bound at r1, b = the columns of B at
+    // r2 (two F_p bindings each), log m rounds
+    launch_bind_rows(d_A, a_dtype, n, m, E1.re, scr, Ta.re, s);
+    launch_bind_rows(d_A, a_dtype, n, m, E1.im, scr, Ta.im, s);
+    launch_bind_cols(d_B, RA_I16, m, k, E2.re, Tb.re, s);
+    launch_bind_cols(d_B, RA_I16, m, k, E2.im, Tb.im, s);
+    uint64_t *ev_mm = tr + kF2TrFixed, *ev_rs = ev_mm + 6 * (size_t)lm, *ev_zc = ev_rs + 8 * (size_t)(lP + lN);
+    uint64_t *p_mm = part, *p_rs = p_mm + (size_t)lm * pstride, *p_zc = p_rs + (size_t)lN * pstride;
+    for (int j = 0; j < lm; j++) {
+        F2RoundArgs ra{};
+        ra.kind = F2_MATMUL;
+        ra.h = (uint64_t)m >> (j + 1);
+        ra.src[0] = ra.dst[0] = Ta;
+        ra.src[1] = ra.dst[1] = Tb;
+        ra.rho = rho + 2 * j;
+        ra.part = p_mm + (size_t)j * pstride;
+        launch_f2_round(ra, s);
+    }
+    {
+        F2FinishArgs fa{};
+        fa.kind = F2_MATMUL;
+        fa.v = lm;
+        fa.part = p_mm;
+        fa.ev = ev_mm;
+        fa.t[0] = Ta;
+        fa.t[1] = Tb;
+        fa.fin = tr;
+        launch_f2_finish(fa, s);
+    }
+    // the claims at (r1, r2)
+    launch_f2_outer(E1, E2, lk, N, EQ, s);
+    launch_f2_claims(EQ, d_R, d_Rm, d_Y, d_Z, N, cpart, s);
+    launch_f2_sum8(cpart, f2_blocks(N), tr + 6, s);
+    // plane rounds: the Gram matrix's two parts from EQ's two parts (the F_p
+    // Gram pass with EQ as its row table and a one-entry column table), and
+    // the plane-bound table Bx with the two parts of eq(sigma_p, .)
+    launch_f2_eq(sig, lP, SIG, s);
+    launch_f2_eq(sig, 0, ONE, s);
+    const int gt = plane_gram_tiles(lP), gb = plane_gram_blocks(N, lP);
+    uint64_t *gp0 = (uint64_t *)(ws + L.o_gp0), *gp1 = (uint64_t *)(ws + L.o_gp1);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.re, ONE.re, sig, Bx.re, gp0, nullptr, s, SIG.re);
+    launch_f2_gram_sum(gp0, gb, gt, Gre, s);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.im, ONE.re, sig, Bx.im, gp1, nullptr, s, SIG.im);
+    launch_f2_gram_sum(gp1, gb, gt, Gim, s);
+    {
+        F2PlaneArgs pa{};
+        pa.G_re = Gre;
+        pa.G_im = Gim;
+        pa.tau = tau;
+        pa.sig = sig;
+        pa.lam = lam;
+        pa.claims = tr + 6;
+        pa.s = (int)io->s;
+        pa.t = t;
+        pa.relu = relu;
+        pa.P = P;
+        pa.lP = lP;
+        pa.ev = ev_rs;
+        pa.cst = cst;
+        pa.range_sum = tr + 14;
+        launch_f2_planes(pa, s);
+    }
+    // rounds over x of the range instance (tables EQ, Bx), then the ReLU zero-check (EQ, D, S)
+    for (int j = 0; j < lN; j++) {
+        F2RoundArgs ra{};
+        ra.kind = F2_RANGE;
+        ra.first = j == 0;
+        ra.h = N >> (j + 1);
+        ra.src[0] = j == 0 ? EQ : EQr;
+        ra.dst[0] = EQr;
+        ra.src[1] = ra.dst[1] = Bx;
+        ra.rho = sig + 2 * (lP + j);
+        ra.cst = cst;
+        ra.part = p_rs + (size_t)j * pstride;
+        launch_f2_round(ra, s);
+    }
+    {
+        F2FinishArgs fa{};
+        fa.kind = F2_RANGE;
+        fa.v = lN;
+        fa.part = p_rs;
+        fa.ev = ev_rs + 8 * (size_t)lP;
+        fa.t[0] = EQr;
+        fa.t[1] = Bx;
+        fa.fin = tr + 16;
+        launch_f2_finish(fa, s);
+    }
+    if (relu) {
+        for (int j = 0; j < lN; j++) {
+            F2RoundArgs ra{};
+            ra.kind = F2_RELU;
+            ra.first = j == 0;
+            ra.h = N >> (j + 1);
+            ra.src[0] = j == 0 ? EQ : EQz;
+            ra.dst[0] = EQz;
+            ra.src[1] = ra.dst[1] = Dt;
+            ra.src[2] = ra.dst[2] = St;
+            ra.R = d_R;
+            ra.Y = d_Y;
+            ra.rho = rho2 + 2 * j;
+            ra.part = p_zc + (size_t)j * pstride;
+            launch_f2_round(ra, s);
+        }
+        F2FinishArgs fa{};
+        fa.kind = F2_RELU;
+        fa.v = lN;
+        fa.part = p_zc;
+        fa.ev = ev_zc;
+        fa.t[0] = EQz;
+        fa.t[1] = Dt;
+        fa.t[2] = St;
+        fa.fin = tr + 18;
+        fa.R = d_R;
+        fa.Y = d_Y;
+        launch_f2_finish(fa, s);
+    }
+    RA_HIP(hipGetLastError());
+    // the transcript and the witness status into the context's pinned area
+    // (nothing else is pending there: the call drained on entry)
+    const size_t prm_words = (sizeof(WitParams) + 7) / 8;
+    size_t off = 0;
+    if ((st = stage_take(c, L.tr_words + prm_words, &off)) != RA_OK) return st;
+    const uint64_t *h = c->h_stage + off;
+    RA_HIP(hipMemcpyAsync(c->h_stage + off, tr, L.tr_words * 8, hipMemcpyDeviceToHost, s));
+    RA_HIP(hipMemcpyAsync(c->h_stage + off + L.tr_words, c->d_params, sizeof(WitParams), hipMemcpyDeviceToHost, s));
+    RA_HIP(hipStreamSynchronize(s));
+    WitParams prm;
+    std::memcpy(&prm, h + L.tr_words, sizeof(prm));
+    c->stage_used = 0;
+    if (prm.status != 0) return prm.status;  // a given t that does not hold R
+    c->cursor += 2 * cnt;
+    auto pr = [&](size_t o) { return ra_fp2{h[o], h[o + 1]}; };
+    io->t = t;
+    io->P = (uint32_t)P;
+    io->log_m = (uint32_t)lm;
+    io->c0 = pr(0);
+    io->a_star = pr(2);
+    io->b_star = pr(4);
+    io->r_claim = pr(6);
+    io->rm_claim = pr(8);
+    io->y_claim = pr(10);
+    io->z_claim = pr(12);
+    io->range_sum = pr(14);
+    io->bits_claim = pr(16);
+    io->r_at = relu ? pr(18) : ra_fp2{0, 0};
+    io->y_at = relu ? pr(20) : ra_fp2{0, 0};
+    io->rounds = (uint32_t)(lP + lN);
+    io->relu_rounds = relu ? (uint32_t)lN : 0;
+    const size_t omm = kF2TrFixed, ors = omm + 6 * (size_t)lm, ozc = ors + 8 * (size_t)(lP + lN);
+    for (int i = 0; i < 3 * lm; i++) io->mm_evals[i] = pr(omm + 2 * i);
+    for (int i = 0; i < 4 * (lP + lN); i++) io->rs_evals[i] = pr(ors + 2 * i);
+    if (relu)
+        for (int i = 0; i < 4 * lN; i++) io->zc_evals[i] = pr(ozc + 2 * i);
+    return RA_OK;
 }
 
 }  // extern "C"

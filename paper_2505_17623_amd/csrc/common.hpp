@@ -283,6 +283,59 @@ struct XBlockArgs {
 };
 void launch_xblock(bool relu, bool first, const XBlockArgs &a, const XJobs &jobs, hipStream_t st);
 
+// ---- the protocol over F_{p^2} (fp2.hip) ----
+// An F_{p^2} table as two F_p arrays (real and imaginary parts).
+struct F2Tab {
+    uint64_t *re, *im;
+};
+enum { F2_MATMUL = 0, F2_RANGE = 1, F2_RELU = 2 };
+constexpr int kF2MaxBlocks = 512;  // blocks of a round launch (partials per round)
+// blocks of a pass over h pairs (256 threads each, grid-stride beyond kF2MaxBlocks)
+__host__ __device__ inline int f2_blocks(uint64_t h)
+{
+    const uint64_t b = (h + 255) / 256;
+    return (int)(b < (uint64_t)kF2MaxBlocks ? (b ? b : 1) : kF2MaxBlocks);
+}
+// one round over tables of 2h entries: src -> dst (equal but for the first
+// round of the range / ReLU instances); rho and cst point at pairs (re, im)
+struct F2RoundArgs {
+    int kind, first;
+    uint64_t h;
+    F2Tab src[3], dst[3];
+    const int32_t *R, *Y;  // ReLU first round: D = R - Y, S = R + Y
+    const uint64_t *rho;
+    const uint64_t *cst;   // range: c_eq, c_w
+    uint64_t *part;        // f2_blocks(h) x 8 words
+};
+// the evaluations of an instance's v rounds (partials of round j at part +
+// j kF2MaxBlocks 8) and its final words
+struct F2FinishArgs {
+    int kind, v;
+    const uint64_t *part;
+    uint64_t *ev;
+    F2Tab t[3];
+    uint64_t *fin;
+    const int32_t *R, *Y;  // ReLU with no rounds (one output): D, S from R, Y
+};
+struct F2PlaneArgs {
+    const uint64_t *G_re, *G_im;      // 64 x 64
+    const uint64_t *tau, *sig, *lam;  // pairs: tau_p, sigma_p, (lambda1, lambda2, lambda3, mu)
+    const uint64_t *claims;           // R~, Rm~, Y~, Z~ (pairs)
+    int s, t, relu, P, lP;
+    uint64_t *ev;                     // lP rounds x 8 words
+    uint64_t *cst;                    // out: c_eq, c_w
+    uint64_t *range_sum;              // out: the claimed sum
+};
+void launch_f2_eq(const uint64_t *z, int v, F2Tab out, hipStream_t st);
+void launch_f2_outer(F2Tab E1, F2Tab E2, int lk, uint64_t N, F2Tab out, hipStream_t st);
+void launch_f2_claims(F2Tab EQ, const int32_t *R, const uint16_t *Rm, const int32_t *Y, const int32_t *Z, uint64_t N,
+                      uint64_t *part, hipStream_t st);
+void launch_f2_sum8(const uint64_t *part, int nb, uint64_t *out, hipStream_t st);
+void launch_f2_round(const F2RoundArgs &a, hipStream_t st);
+void launch_f2_finish(const F2FinishArgs &a, hipStream_t st);
+void launch_f2_planes(const F2PlaneArgs &a, hipStream_t st);
+void launch_f2_gram_sum(const uint64_t *gpart, int nblk, int TP, uint64_t *G, hipStream_t st);
+
 // ---- launchers (planes.hip) ----
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
@@ -292,8 +345,10 @@ int plane_gram_set_up_threads(uint64_t N, int lP);
 // words); sig: sigma_p (lP words).  With xs (x_setup_count(*xs) at most
 // plane_gram_set_up_threads), the pass also runs the set-up of the rounds
 // over x, which depends on challenges only.
+// eqs (optional): the P values eq(sigma_p, q) given instead of computed from sig.
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st);
+                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st,
+                       const uint64_t *eqs = nullptr);
 // the Gram matrix G (gsum: 64 x 64 words, both triangles) from the partial
 // tiles; further workgroups run the set-up of the range check (rc, xs)
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,

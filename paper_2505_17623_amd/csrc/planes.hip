@@ -84,7 +84,7 @@ template <int TP>
 __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const uint64_t *__restrict__ bits, uint64_t N, int lk, const uint64_t *__restrict__ E1,
     const uint64_t *__restrict__ E2, const uint64_t *__restrict__ sig, int lP, uint64_t *__restrict__ Bx,
-    uint64_t *__restrict__ gpart, int xs_on, XSetupArgs xs)
+    uint64_t *__restrict__ gpart, int xs_on, XSetupArgs xs, const uint64_t *__restrict__ eqs)
 {
     using S = GramShape<TP>;
     constexpr int NPL = S::kPlanes, DW = S::kDigitsPerWave, NPT = TP == 1 ? 1 : 2;
@@ -101,13 +101,17 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
     const bool producer = wv < kProducers;  // wave-uniform
     const int cw = wv - kProducers;         // consumer index = its digit
-    if (tid < 64) {  // eq(sigma_p, q) for every plane q
+    if (tid < 64) {  // eq(sigma_p, q) for every plane q (or the given values)
         uint64_t a = 0;
         if (tid < (1 << lP)) {
-            a = 1;
-            for (int i = 0; i < lP; i++) {
-                const uint64_t z = sig[i];
-                a = m61::lmul(a, ((tid >> (lP - 1 - i)) & 1) ? z : m61::lsub(1, z));
+            if (eqs) {
+                a = eqs[tid];
+            } else {
+                a = 1;
+                for (int i = 0; i < lP; i++) {
+                    const uint64_t z = sig[i];
+                    a = m61::lmul(a, ((tid >> (lP - 1 - i)) & 1) ? z : m61::lsub(1, z));
+                }
             }
         }
         s_eqs[tid] = m61::canon(a);
@@ -298,17 +302,18 @@ int plane_gram_blocks(uint64_t N, int lP)
 }
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
-                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st)
+                       const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st,
+                       const uint64_t *eqs)
 {
     const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
     const XSetupArgs none{};
     const XSetupArgs &x = xs ? *xs : none;
     if (TP == 1)
         hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
-                           gpart, xs ? 1 : 0, x);
+                           gpart, xs ? 1 : 0, x, eqs);
     else
         hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
-                           gpart, xs ? 1 : 0, x);
+                           gpart, xs ? 1 : 0, x, eqs);
 }
 
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,

@@ -291,3 +291,222 @@ extern "C" ra_status ra_verify(uint64_t p, uint64_t seed, uint32_t n_layers, con
     for (uint64_t i = 0; i < total; i++) chal[i] = cs.next();
     return ra_verify_stream(p, chal.data(), total, n_layers, pub, tables, tr, verdict, failed_layer);
 }
+
+// ---------------------------------------------------------------------------
+// The verifier for layers proven with challenges in F_{p^2} = F_p[i] /
+// (i^2 + 1): the checks of verify_layer, same numbering, every transcript
+// element a pair (re, im).
+// ---------------------------------------------------------------------------
+namespace {
+
+struct G2 {
+    uint64_t re, im;
+};
+G2 g2(uint64_t a) { return G2{a, 0}; }
+G2 g2add(G2 a, G2 b) { return G2{fadd(a.re, b.re), fadd(a.im, b.im)}; }
+G2 g2sub(G2 a, G2 b) { return G2{fsub(a.re, b.re), fsub(a.im, b.im)}; }
+G2 g2mul(G2 a, G2 b)
+{
+    return G2{fsub(fmul(a.re, b.re), fmul(a.im, b.im)), fadd(fmul(a.re, b.im), fmul(a.im, b.re))};
+}
+G2 g2scale(G2 a, uint64_t c) { return G2{fmul(a.re, c), fmul(a.im, c)}; }
+bool g2same(G2 a, G2 b) { return a.re == b.re && a.im == b.im; }
+G2 g2of(const ra_fp2 &v) { return G2{v.re, v.im}; }
+G2 g2eq1(G2 a, G2 b) { return g2add(g2mul(a, b), g2mul(g2sub(g2(1), a), g2sub(g2(1), b))); }
+
+G2 lagrange2(const G2 *e, int d, G2 x)
+{
+    G2 acc = g2(0);
+    for (int i = 0; i <= d; i++) {
+        G2 num = g2(1);
+        uint64_t den = 1;
+        for (int j = 0; j <= d; j++) {
+            if (j == i) continue;
+            num = g2mul(num, g2sub(x, g2((uint64_t)j)));
+            den = fmul(den, fint(i - j));
+        }
+        acc = g2add(acc, g2mul(e[i], g2scale(num, fpow(den, kP - 2))));
+    }
+    return acc;
+}
+
+bool chain2(int rounds, int d, G2 claim, const ra_fp2 *evals, const G2 *rho, G2 *final_value)
+{
+    G2 cur = claim;
+    std::vector<G2> g(d + 1);
+    for (int j = 0; j < rounds; j++) {
+        for (int X = 0; X <= d; X++) g[X] = g2of(evals[(size_t)j * (d + 1) + X]);
+        if (!g2same(g2add(g[0], g[1]), cur)) return false;
+        cur = lagrange2(g.data(), d, rho[j]);
+    }
+    *final_value = cur;
+    return true;
+}
+
+G2 bind_all2(std::vector<G2> T, const G2 *z, int v)
+{
+    size_t size = T.size();
+    for (int j = 0; j < v; j++) {
+        const size_t h = size / 2;
+        for (size_t i = 0; i < h; i++) T[i] = g2add(T[i], g2mul(z[j], g2sub(T[i + h], T[i])));
+        size = h;
+    }
+    return T[0];
+}
+
+template <typename I> G2 mle_ints2(const I *tab, size_t len, const G2 *z, int v)
+{
+    std::vector<G2> T(len);
+    for (size_t i = 0; i < len; i++) T[i] = g2(fint((int64_t)tab[i]));
+    return bind_all2(std::move(T), z, v);
+}
+
+G2 eq_points2(const G2 *a, const G2 *b, int v)
+{
+    G2 acc = g2(1);
+    for (int i = 0; i < v; i++) acc = g2mul(acc, g2eq1(a[i], b[i]));
+    return acc;
+}
+
+int verify_layer_fp2(const ra_layer_public &L, const ra_layer_tables &T, const ra_layer_proof_fp2 &tr,
+                     const ra_layer_public *prev, ra::ChallengeStream &cs)
+{
+    const uint32_t n = L.n, m = L.m, k = L.k;
+    if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k) || !L.A || !L.B || !L.Z || !T.R || !T.Rm || !T.Y || !T.bits)
+        return 13;
+    if ((L.a_dtype != RA_I16 && L.a_dtype != RA_I32) || L.s < 1 || L.s > 30 || L.relu > 1 || L.round_mode > 1)
+        return 13;
+    const int ln = log2u(n), lm = log2u(m), lk = log2u(k), lN = ln + lk;
+    const uint64_t N = (uint64_t)n * k;
+    const int s = (int)L.s, relu = (int)L.relu, t = tr.t;
+    if (L.chained) {
+        if (!prev || L.a_dtype != RA_I32 || prev->n != n || prev->k != m) return 14;
+        const int32_t *A = (const int32_t *)L.A;
+        for (uint64_t i = 0; i < (uint64_t)n * m; i++)
+            if (A[i] != prev->Z[i]) return 14;
+    }
+    if (t < 0 || s + t + 3 > 61 || tr.s != L.s || tr.relu != L.relu || tr.round_mode != L.round_mode) return 12;
+    const int Q = s + (t + 2) * (relu ? 2 : 1);
+    int P = 1, lP = 0;
+    while (P < Q) {
+        P <<= 1;
+        lP++;
+    }
+    if ((int)tr.P != P || lP > 6) return 12;
+    if (tr.log_m != (uint32_t)lm || tr.rounds != (uint32_t)(lP + lN) || tr.relu_rounds != (uint32_t)(relu ? lN : 0))
+        return 13;
+    if ((lm && !tr.mm_evals) || !tr.rs_evals || (relu && lN && !tr.zc_evals)) return 13;
+    std::vector<ra_fp2> words = {tr.c0, tr.a_star, tr.b_star, tr.r_claim, tr.rm_claim, tr.y_claim, tr.z_claim,
+                                 tr.range_sum, tr.bits_claim, tr.r_at, tr.y_at};
+    for (int i = 0; i < 3 * lm; i++) words.push_back(tr.mm_evals[i]);
+    for (int i = 0; i < 4 * (lP + lN); i++) words.push_back(tr.rs_evals[i]);
+    if (relu)
+        for (int i = 0; i < 4 * lN; i++) words.push_back(tr.zc_evals[i]);
+    for (const ra_fp2 &w : words)
+        if (w.re >= kP || w.im >= kP) return 12;
+
+    const uint64_t need = (uint64_t)ln + lk + lm + 4 + lP + (lP + lN) + (relu ? lN : 0);
+    std::vector<G2> c(need);
+    for (uint64_t j = 0; j < need; j++) {
+        c[j].re = cs.next();
+        c[j].im = cs.next();
+    }
+    const G2 *r1 = c.data(), *r2 = r1 + ln, *rho = r2 + lk, *lam = rho + lm;
+    const G2 mu = lam[3], *tau_p = lam + 4, *sigma = tau_p + lP, *rho2 = sigma + lP + lN;
+    std::vector<G2> r12(r1, r1 + ln);
+    r12.insert(r12.end(), r2, r2 + lk);
+
+    G2 fin;
+    if (!chain2(lm, 2, g2of(tr.c0), tr.mm_evals, rho, &fin)) return 1;
+    if (!g2same(fin, g2mul(g2of(tr.a_star), g2of(tr.b_star)))) return 2;
+    {
+        std::vector<G2> pa(r1, r1 + ln), pb(rho, rho + lm);
+        pa.insert(pa.end(), rho, rho + lm);
+        pb.insert(pb.end(), r2, r2 + lk);
+        const G2 ea = L.a_dtype == RA_I16 ? mle_ints2((const int16_t *)L.A, (size_t)n * m, pa.data(), ln + lm)
+                                          : mle_ints2((const int32_t *)L.A, (size_t)n * m, pa.data(), ln + lm);
+        const G2 eb = mle_ints2(L.B, (size_t)m * k, pb.data(), lm + lk);
+        if (!g2same(ea, g2of(tr.a_star)) || !g2same(eb, g2of(tr.b_star))) return 3;
+    }
+    {
+        G2 rhs = g2add(g2scale(g2of(tr.r_claim), fint((int64_t)1 << s)), g2of(tr.rm_claim));
+        if (L.round_mode == RA_ROUND_NEAREST) rhs = g2sub(rhs, g2(fint((int64_t)1 << (s - 1))));
+        if (!g2same(rhs, g2of(tr.c0))) return 4;
+    }
+    {
+        G2 H = g2add(g2mul(lam[0], g2of(tr.rm_claim)),
+                     g2mul(lam[1], g2add(g2of(tr.r_claim), g2(fint((int64_t)1 << (t + 1))))));
+        if (relu) H = g2add(H, g2mul(lam[2], g2of(tr.y_claim)));
+        H = g2mul(mu, H);
+        if (!g2same(H, g2of(tr.range_sum))) return 5;
+        if (!chain2(lP + lN, 3, H, tr.rs_evals, sigma, &fin)) return 5;
+        std::vector<G2> W(P, g2(0));
+        int q = 0;
+        for (int b = 0; b < s; b++) W[q++] = g2scale(lam[0], 1ull << b);
+        for (int b = 0; b < t + 2; b++) W[q++] = g2scale(lam[1], 1ull << b);
+        if (relu)
+            for (int b = 0; b < t + 2; b++) W[q++] = g2scale(lam[2], 1ull << b);
+        const G2 wsig = bind_all2(W, sigma, lP);
+        const G2 ep = eq_points2(tau_p, sigma, lP), ex = eq_points2(r12.data(), sigma + lP, lN);
+        const G2 bc = g2of(tr.bits_claim);
+        const G2 want = g2add(g2mul(g2mul(ep, ex), g2mul(bc, g2sub(bc, g2(1)))), g2mul(mu, g2mul(g2mul(wsig, ex), bc)));
+        if (!g2same(fin, want)) return 6;
+        std::vector<G2> eqp(P);
+        for (int qq = 0; qq < P; qq++) {
+            G2 acc = g2(1);
+            for (int i = 0; i < lP; i++)
+                acc = g2mul(acc, ((qq >> (lP - 1 - i)) & 1) ? sigma[i] : g2sub(g2(1), sigma[i]));
+            eqp[qq] = acc;
+        }
+        std::vector<G2> bx(N);
+        for (uint64_t x = 0; x < N; x++) {
+            const uint64_t w = T.bits[x];
+            if (P < 64 && (w >> P)) return 7;
+            G2 acc = g2(0);
+            for (int qq = 0; qq < P; qq++)
+                if ((w >> qq) & 1) acc = g2add(acc, eqp[qq]);
+            bx[x] = acc;
+        }
+        if (!g2same(bind_all2(std::move(bx), sigma + lP, lN), bc)) return 7;
+    }
+    if (!g2same(mle_ints2(T.R, N, r12.data(), lN), g2of(tr.r_claim)) ||
+        !g2same(mle_ints2(T.Rm, N, r12.data(), lN), g2of(tr.rm_claim)) ||
+        !g2same(mle_ints2(T.Y, N, r12.data(), lN), g2of(tr.y_claim)))
+        return 8;
+    if (relu) {
+        if (!chain2(lN, 3, g2(0), tr.zc_evals, rho2, &fin)) return 9;
+        const G2 ex = eq_points2(r12.data(), rho2, lN), ra = g2of(tr.r_at), ya = g2of(tr.y_at);
+        if (!g2same(fin, g2mul(ex, g2sub(g2mul(ra, ra), g2mul(ya, ya))))) return 9;
+        if (!g2same(mle_ints2(T.R, N, rho2, lN), ra) || !g2same(mle_ints2(T.Y, N, rho2, lN), ya)) return 10;
+    }
+    if (relu) {
+        if (!g2same(g2scale(g2of(tr.z_claim), 2), g2add(g2of(tr.r_claim), g2of(tr.y_claim)))) return 11;
+    } else if (!g2same(g2of(tr.z_claim), g2of(tr.r_claim))) {
+        return 11;
+    }
+    if (!g2same(mle_ints2(L.Z, N, r12.data(), lN), g2of(tr.z_claim))) return 11;
+    return 0;
+}
+
+}  // namespace
+
+extern "C" ra_status ra_verify_fp2(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_layer_public *pub,
+                                   const ra_layer_tables *tables, const ra_layer_proof_fp2 *tr, int32_t *verdict,
+                                   uint32_t *failed_layer)
+{
+    if (!verdict || !failed_layer || (n_layers && (!pub || !tables || !tr))) return RA_E_INVAL;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    if (seed == 0) return RA_E_SEED;
+    *verdict = 0;
+    *failed_layer = 0;
+    ra::ChallengeStream cs(seed);
+    for (uint32_t l = 0; l < n_layers; l++) {
+        const int v = verify_layer_fp2(pub[l], tables[l], tr[l], l ? &pub[l - 1] : nullptr, cs);
+        if (v) {
+            *verdict = v;
+            *failed_layer = l;
+            return RA_OK;
+        }
+    }
+    return RA_OK;
+}

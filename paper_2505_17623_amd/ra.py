@@ -26,7 +26,8 @@ STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_
 EXPORTS = ["ra_ctx_create", "ra_ctx_create_stream", "ra_ctx_destroy", "ra_ctx_cursor", "ra_status_str",
            "ra_workspace_size", "ra_ctx_set_profiling", "ra_ctx_profile", "ra_ctx_set_deferred", "ra_ctx_sync",
            "ra_mle_bind", "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify",
-           "ra_verify_stream", "ra_witness_plan", "ra_mle_bind_noalloc"]
+           "ra_verify_stream", "ra_witness_plan", "ra_mle_bind_noalloc", "ra_prove_layer_fp2",
+           "ra_workspace_size_fp2", "ra_verify_fp2"]
 
 
 class RAError(RuntimeError):
@@ -70,6 +71,27 @@ class LayerTranscript(ctypes.Structure):
     _fields_ = [("mm", MatmulProof), ("wit", WitnessInfo), ("rng", RangeProof)]
 
 
+class Fp2(ctypes.Structure):
+    """An element re + im i of F_{p^2} = F_p[i] / (i^2 + 1)."""
+    _fields_ = [("re", u64), ("im", u64)]
+
+
+Fp2p = ctypes.POINTER(Fp2)
+
+
+class LayerProofFp2(ctypes.Structure):
+    _fields_ = [("s", ctypes.c_uint32), ("relu", ctypes.c_uint32), ("round_mode", ctypes.c_uint32),
+                ("t", ctypes.c_int32), ("P", ctypes.c_uint32), ("log_m", ctypes.c_uint32),
+                ("c0", Fp2), ("a_star", Fp2), ("b_star", Fp2), ("mm_evals", Fp2p),
+                ("r_claim", Fp2), ("rm_claim", Fp2), ("y_claim", Fp2), ("z_claim", Fp2),
+                ("rounds", ctypes.c_uint32), ("rs_evals", Fp2p), ("range_sum", Fp2), ("bits_claim", Fp2),
+                ("relu_rounds", ctypes.c_uint32), ("zc_evals", Fp2p), ("r_at", Fp2), ("y_at", Fp2)]
+
+
+FP2_SCALARS = ("c0", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_claim", "range_sum", "bits_claim",
+               "r_at", "y_at")
+
+
 _lib = None
 
 
@@ -109,7 +131,15 @@ def lib():
                 ctypes.POINTER(LayerTranscript), ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
         L.ra_verify.argtypes = [u64, u64] + tail
         L.ra_verify_stream.argtypes = [u64, u64p, u64] + tail
+        L.ra_prove_layer_fp2.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                                         vp, vp, vp, vp, vp, vp, u64, vp, ctypes.c_size_t,
+                                         ctypes.POINTER(LayerProofFp2)]
+        L.ra_workspace_size_fp2.argtypes = [ctypes.c_uint32] * 3 + [ctypes.POINTER(ctypes.c_size_t)]
+        L.ra_verify_fp2.argtypes = [u64, u64, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
+                                    ctypes.POINTER(LayerTables), ctypes.POINTER(LayerProofFp2),
+                                    ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
         for f in (L.ra_ctx_create, L.ra_ctx_create_stream, L.ra_workspace_size, L.ra_verify_stream,
+                  L.ra_prove_layer_fp2, L.ra_workspace_size_fp2, L.ra_verify_fp2,
                   L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
@@ -464,3 +494,119 @@ def ra_verify(challenges, layers):
                                       ctypes.byref(failed)), "ra_verify_stream")
     return int(verdict.value), int(failed.value)
 
+
+
+# --- layers with challenges in F_{p^2} ---------------------------------------
+def workspace_size_fp2(n: int, m: int, k: int) -> int:
+    v = ctypes.c_size_t()
+    _check(lib().ra_workspace_size_fp2(n, m, k, ctypes.byref(v)), "ra_workspace_size_fp2")
+    return int(v.value)
+
+
+def _fp2_list(arr, count):
+    return [(int(arr[i].re), int(arr[i].im)) for i in range(count)]
+
+
+def prove_layer_fp2(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1,
+                    bufs: dict | None = None, ws: torch.Tensor | None = None):
+    """One layer over F_{p^2} (ra_prove_layer_fp2; waits for its work).
+    Returns the device tensors and the transcript, every element a pair (re, im)."""
+    n, m = A.shape
+    k = B.shape[1]
+    dev = A.device
+    if bufs is not None and "C" in bufs:
+        C, (R, Rm, Y, Z, bits) = bufs["C"], bufs["wit"]
+    else:
+        C = torch.empty((n, k), dtype=torch.int64, device=dev)
+        R, Rm, Y, Z, bits = witness_outputs(n, k, dev)
+        if bufs is not None:
+            bufs["C"], bufs["wit"] = C, (R, Rm, Y, Z, bits)
+    N = n * k
+    lm, lN = m.bit_length() - 1, N.bit_length() - 1
+    mm = (Fp2 * max(3 * lm, 1))()
+    rs = (Fp2 * (4 * (6 + lN)))()
+    zc = (Fp2 * max(4 * lN, 1))()
+    pr = LayerProofFp2(s=s, relu=int(bool(relu)), round_mode=mode, t=t)
+    pr.mm_evals, pr.rs_evals, pr.zc_evals = mm, rs, zc
+    _check(lib().ra_prove_layer_fp2(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C), _dptr(R), _dptr(Rm),
+                                    _dptr(Y), _dptr(Z), _dptr(bits), N, *_ws(ws), ctypes.byref(pr)),
+           "ra_prove_layer_fp2")
+    tr = dict(t=int(pr.t), P=int(pr.P), s=s, relu=int(bool(relu)), mode=mode,
+              mm_evals=_fp2_list(mm, 3 * pr.log_m), rs_evals=_fp2_list(rs, 4 * pr.rounds),
+              zc_evals=_fp2_list(zc, 4 * pr.relu_rounds))
+    for key in FP2_SCALARS:
+        v = getattr(pr, key)
+        tr[key] = (int(v.re), int(v.im))
+    return dict(C=C, R=R, Rm=Rm, Y=Y, Z=Z, bits=bits, transcript=tr)
+
+
+def prove_network_fp2(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, ws=None):
+    """Every layer of a workload over F_{p^2}, inputs as in prove_network."""
+    if bufs is not None:
+        while len(bufs) < len(workload.layers):
+            bufs.append({})
+    X = to_device(workload.X, device) if X is None else X
+    Bs = [to_device(L.B, device) for L in workload.layers] if Bs is None else Bs
+    outs, Z = [], None
+    for li, layer in enumerate(workload.layers):
+        if li == 0:
+            A = X
+        elif workload.links[li] is None:
+            A = Z
+        else:
+            A = to_device(workload.links[li](Z.cpu().numpy()), device)
+        t = -1 if ts is None else int(ts[li])
+        res = prove_layer_fp2(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t,
+                              None if bufs is None else bufs[li], ws)
+        res["A"] = A
+        Z = res["Z"]
+        outs.append(res)
+    return outs
+
+
+def ra_verify_fp2(seed: int, layers):
+    """Host verifier for layers proven over F_{p^2}; `layers` as for ra_verify
+    with the transcripts of prove_layer_fp2.  Returns (verdict, failed_layer)."""
+    nl = len(layers)
+    pubs = (LayerPublic * nl)()
+    tabs = (LayerTables * nl)()
+    trs = (LayerProofFp2 * nl)()
+    keep = []
+    for i, L in enumerate(layers):
+        tr = L["transcript"]
+        A = np.ascontiguousarray(L["A"])
+        B = np.ascontiguousarray(L["B"], dtype=np.int16)
+        n, m = A.shape
+        k = B.shape[1]
+        arrs = dict(A=A, B=B, Z=np.ascontiguousarray(L["Z"], dtype=np.int32),
+                    R=np.ascontiguousarray(L["R"], dtype=np.int32),
+                    Rm=np.ascontiguousarray(np.asarray(L["Rm"]).view(np.uint16)),
+                    Y=np.ascontiguousarray(L["Y"], dtype=np.int32),
+                    bits=np.ascontiguousarray(np.asarray(L["bits"]).view(np.uint64)))
+
+        def fp2_array(ev):
+            a = (Fp2 * max(len(ev), 1))()
+            for j, (re, im) in enumerate(ev):
+                a[j].re, a[j].im = re, im
+            return a
+        mm, rs, zc = fp2_array(tr["mm_evals"]), fp2_array(tr["rs_evals"]), fp2_array(tr["zc_evals"])
+        keep += list(arrs.values()) + [mm, rs, zc]
+        pubs[i] = LayerPublic(n, m, k, tr["s"], tr["relu"], tr["mode"], RA_I16 if A.dtype == np.int16 else RA_I32,
+                              arrs["A"].ctypes.data, arrs["B"].ctypes.data, arrs["Z"].ctypes.data,
+                              int(L.get("chained", 0)))
+        tabs[i] = LayerTables(arrs["R"].ctypes.data, arrs["Rm"].ctypes.data, arrs["Y"].ctypes.data,
+                              arrs["bits"].ctypes.data)
+        t = trs[i]
+        t.s, t.relu, t.round_mode, t.t, t.P = tr["s"], tr["relu"], tr["mode"], tr["t"], tr["P"]
+        t.log_m = len(tr["mm_evals"]) // 3
+        t.rounds = len(tr["rs_evals"]) // 4
+        t.relu_rounds = len(tr["zc_evals"]) // 4
+        t.mm_evals, t.rs_evals, t.zc_evals = mm, rs, zc
+        for key in FP2_SCALARS:
+            re, im = tr[key]
+            setattr(t, key, Fp2(re, im))
+    verdict = ctypes.c_int32()
+    failed = ctypes.c_uint32()
+    _check(lib().ra_verify_fp2(P61, int(seed), nl, pubs, tabs, trs, ctypes.byref(verdict), ctypes.byref(failed)),
+           "ra_verify_fp2")
+    return int(verdict.value), int(failed.value)

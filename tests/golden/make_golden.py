@@ -2,7 +2,12 @@
 layer of workload N at full size, with SHA-256 digests of the inputs and of
 every output table.  Calls only the oracle and the seeded input generator.
 
-    python tests/golden/make_golden.py [cfg ...]      (default: 1 2 3 4 5)
+    python tests/golden/make_golden.py [cfg ...]          (default: 1 2 3 4 5)
+    python tests/golden/make_golden.py --fp2 [cfg ...]    -> full_fp2_cfg<N>.json
+
+With --fp2 the oracle proves the workload with challenges in F_{p^2} (the
+seed's stream read in pairs); the witness tables are those of the F_p proof,
+so only the transcript words (pairs re, im) and the digests of Z are kept.
 
 Digest formats: C, R, Rm, Y, Z as little-endian int64 arrays in row-major
 order; the bit table as P x N bytes (0/1), plane-major; A and B as int64.
@@ -34,6 +39,25 @@ def digest_i64(a) -> str:
     return digest(np.asarray(a).astype("<i8"))
 
 
+def main_fp2(cfgs):
+    orc.build(force=False)
+    for cfg in cfgs:
+        wl = inputs.workload(cfg, "full")
+        t0 = time.time()
+        res = orc.prove_network_fp2(wl)
+        layers = [dict(shape=[r["n"], r["m"], r["k"]], s=r["s"], relu=r["relu"], mode=r["mode"],
+                       transcript={k: r[k] for k in TRANSCRIPT}, digests=dict(Z=digest_i64(r["Z"])))
+                  for r in res]
+        out = dict(workload=wl.name, config=cfg, field="F_p[i]/(i^2+1)",
+                   oracle_seconds=round(time.time() - t0, 1), layers=layers,
+                   source="oracle/ra_oracle_fp2.c via tests/golden/make_golden.py --fp2")
+        path = os.path.join(HERE, f"full_fp2_cfg{cfg}.json")
+        with open(path, "w") as f:
+            json.dump(out, f, indent=1)
+        print(f"config {cfg} over F_p^2: {len(layers)} layers, oracle {out['oracle_seconds']} s -> {path}",
+              flush=True)
+
+
 def main(cfgs):
     orc.build(force=False)
     for cfg in cfgs:
@@ -57,4 +81,8 @@ def main(cfgs):
 
 
 if __name__ == "__main__":
-    main([int(a) for a in sys.argv[1:]] or [1, 2, 3, 4, 5])
+    args = sys.argv[1:]
+    if args and args[0] == "--fp2":
+        main_fp2([int(a) for a in args[1:]] or [1, 2, 3, 4, 5])
+    else:
+        main([int(a) for a in args] or [1, 2, 3, 4, 5])

@@ -97,6 +97,10 @@ def lib():
                                                         ctypes.POINTER(LayerInfo)]
         L.orc_verify_layer.argtypes = [ctypes.c_int64] * 3 + [i64p] * 3 + [ctypes.c_int] * 3 + \
             [i64p] * 4 + [u64p] * 3 + [ctypes.POINTER(LayerInfo), u64p, ctypes.c_int64, i64p]
+        L.orc_link_prove.argtypes = [ctypes.c_int64, i64p, u64p, ctypes.c_int64, i64p, u64p, ctypes.c_int64, i64p,
+                                     u64p, u64p, u64p, u64p]
+        L.orc_link_verify.argtypes = [ctypes.c_int64, i64p, u64p, ctypes.c_int64, i64p, ctypes.c_uint64, u64p,
+                                      ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, u64p, ctypes.c_int64, i64p]
         L.orc2_mul.argtypes = [u64p, u64p, u64p]
         L.orc2_inv.argtypes = [u64p, u64p]
         L.orc2_mle_int.argtypes = [i64p, ctypes.c_int, u64p, u64p]
@@ -248,17 +252,76 @@ def verify_layer(A, B, Z, s, relu, mode, R, Rm, Y, bits, tr, chal, cursor=0):
     return int(v), int(cur[0])
 
 
-def prove_network(workload, layers_out=None):
+def link_point(n, m, k, chal, cursor):
+    """The point (r1, rho) at which a layer proven from `cursor` claims A~ (its a*)."""
+    ln, lm, lk = n.bit_length() - 1, m.bit_length() - 1, k.bit_length() - 1
+    c = [int(x) for x in chal[cursor:cursor + ln + lk + lm]]
+    return c[:ln] + c[ln + lk:]
+
+
+def prove_link(Z, src, z, chal, cursor=0):
+    """Gather link (ra_oracle.c, orc_link_prove): reduce A~(z) of A[a] =
+    Z[src[a]] (0 where src < 0) to Z~(y*) W~_z(y*).  Returns a dict with
+    evals (3 per round), claim, z_at, w_at, cursor."""
+    Zf = _i64(np.asarray(Z).reshape(-1))
+    src = _i64(np.asarray(src).reshape(-1))
+    vz = Zf.size.bit_length() - 1
+    zz = _u64(list(z) or [0])
+    chal = _u64(chal)
+    cur = np.array([cursor], dtype=np.int64)
+    ev = np.zeros(3 * max(vz, 1), dtype=np.uint64)
+    out = np.zeros(3, dtype=np.uint64)
+    u64 = ctypes.c_uint64
+    rc = lib().orc_link_prove(src.size, _ptr(src, ctypes.c_int64), _ptr(zz, u64), Zf.size, _ptr(Zf, ctypes.c_int64),
+                              _ptr(chal, u64), len(chal), _ptr(cur, ctypes.c_int64), _ptr(ev, u64),
+                              _ptr(out[0:], u64), _ptr(out[1:], u64), _ptr(out[2:], u64))
+    if rc != 0:
+        raise OracleError(rc)
+    return dict(evals=[int(x) for x in ev[:3 * vz]], claim=int(out[0]), z_at=int(out[1]), w_at=int(out[2]),
+                cursor=int(cur[0]))
+
+
+def verify_link(Z, src, z, a_star, link, chal, cursor=0):
+    """Verifier of a gather link: (0 or 15, new cursor)."""
+    Zf = _i64(np.asarray(Z).reshape(-1))
+    src = _i64(np.asarray(src).reshape(-1))
+    vz = Zf.size.bit_length() - 1
+    if len(link["evals"]) != 3 * vz:
+        return 15, cursor
+    zz = _u64(list(z) or [0])
+    ev = _u64(np.array(list(link["evals"]) + [0] * 3, dtype=object).astype(np.uint64))
+    chal = _u64(chal)
+    cur = np.array([cursor], dtype=np.int64)
+    u64 = ctypes.c_uint64
+    v = lib().orc_link_verify(src.size, _ptr(src, ctypes.c_int64), _ptr(zz, u64), Zf.size, _ptr(Zf, ctypes.c_int64),
+                              int(a_star) & 0xFFFFFFFFFFFFFFFF, _ptr(ev, u64), int(link["claim"]) & 0xFFFFFFFFFFFFFFFF,
+                              int(link["z_at"]) & 0xFFFFFFFFFFFFFFFF, int(link["w_at"]) & 0xFFFFFFFFFFFFFFFF,
+                              _ptr(chal, u64), len(chal), _ptr(cur, ctypes.c_int64))
+    return int(v), int(cur[0])
+
+
+def prove_network(workload, layers_out=None, links=False):
     """Prove every layer of a workload (see paper_2505_17623_amd.inputs) in
     order; a layer's A is the workload's input or the previous output passed
-    through the workload's link.  Returns the list of per-layer results."""
+    through the workload's link.  With links=True every gather link (a layer
+    whose input is a gather of the previous output) is proven right after its
+    layer, from the next challenges (res["link"]).  Returns the list of
+    per-layer results."""
     results = []
     cursor = 0
     Z = None
     for li, layer in enumerate(workload.layers):
         A = workload.layer_input(li, Z)
+        start = cursor
         res = prove_layer(A, layer.B, layer.s, layer.relu, workload.mode, workload.challenges, cursor)
         cursor = res["cursor"]
+        if links and li > 0 and workload.links[li] is not None:
+            n, m = A.shape
+            z = link_point(n, m, layer.B.shape[1], workload.challenges, start)
+            res["link"] = prove_link(Z, workload.link_map(li), z, workload.challenges, cursor)
+            res["link_point"] = z
+            cursor = res["link"]["cursor"]
+            res["cursor"] = cursor
         res["A"] = A
         Z = res["Z"]
         results.append(res)

@@ -649,3 +649,102 @@ done:
     free(r12);
     return verdict;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Layer composition through a gather (Sec. III-C chains layers; the paper  */
+/* is silent on convolutions, whose inputs are gathers of the previous      */
+/* layer's output: im2col, flattening).                                     */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The next layer's input is A[a] = Z[src[a]] for src[a] >= 0 and 0 for
+ * src[a] < 0 (a = row * m + col, na = n * m entries, Z of nz entries).  Its
+ * multilinear extension at a point z of log na variables is
+ *     A~(z) = sum_a eq(z, a) A[a] = sum_y Z[y] W_z[y],
+ *     W_z[y] = sum over the a with src[a] = y of eq(z, a),
+ * a sum over y of the product of two multilinear tables, so a degree-2
+ * sum-check (Sec. II-D) over log nz variables reduces the claim A~(z) to
+ * Z~(y*) W~_z(y*) at the point y* of its challenges.  Z~(y*) is a claim on
+ * the previous layer's output; W~_z(y*) = sum_a eq(z, a) eq(y*, src[a]) is
+ * computable from the public gather map.
+ *
+ * Consumes log nz challenges at *cursor.  evals: 3 log nz words (g_j(0..2)).
+ */
+int orc_link_prove(int64_t na, const int64_t *src, const uint64_t *z, int64_t nz, const int64_t *Z,
+                   const uint64_t *chal, int64_t nchal, int64_t *cursor, uint64_t *evals, uint64_t *claim,
+                   uint64_t *z_at, uint64_t *w_at)
+{
+    int va = ilog2_exact(na), vz = ilog2_exact(nz);
+    if (va < 0 || vz < 0) return ORC_E_INVAL;
+    if (*cursor < 0 || *cursor + vz > nchal) return ORC_E_CHALLENGES;
+    for (int64_t a = 0; a < na; a++)
+        if (src[a] >= nz) return ORC_E_INVAL;
+    uint64_t *eqz = malloc(sizeof(uint64_t) * (size_t)na);
+    uint64_t *W = calloc((size_t)nz, sizeof(uint64_t));
+    uint64_t *T = malloc(sizeof(uint64_t) * (size_t)nz);
+    if (!eqz || !W || !T) {
+        free(eqz);
+        free(W);
+        free(T);
+        return ORC_E_NOMEM;
+    }
+    chi_vector(z, va, eqz);
+    for (int64_t a = 0; a < na; a++)
+        if (src[a] >= 0) W[src[a]] = fadd(W[src[a]], eqz[a]);
+    uint64_t c = 0;
+    for (int64_t y = 0; y < nz; y++) {
+        T[y] = fint(Z[y]);
+        c = fadd(c, fmul(T[y], W[y]));
+    }
+    *claim = c;
+    uint64_t *tabs[2] = {T, W}, finals[2];
+    sumcheck_prove(vz, 2, 2, tabs, summand_matmul, NULL, chal + *cursor, evals, finals);
+    *z_at = finals[0];
+    *w_at = finals[1];
+    *cursor += vz;
+    free(eqz);
+    free(W);
+    free(T);
+    return ORC_OK;
+}
+
+/*
+ * Verifier of a gather link: 0 accept, 15 reject.  a_star is the claim
+ * A~(z) the next layer's matrix sum-check ended with; Z is the previous
+ * layer's (opened) output.  Checks the chain from a_star, the final product
+ * z_at w_at, z_at against Z~(y*) and w_at against sum_a eq(z, a) eq(y*, src[a]).
+ */
+int orc_link_verify(int64_t na, const int64_t *src, const uint64_t *z, int64_t nz, const int64_t *Z,
+                    uint64_t a_star, const uint64_t *evals, uint64_t claim, uint64_t z_at, uint64_t w_at,
+                    const uint64_t *chal, int64_t nchal, int64_t *cursor)
+{
+    int va = ilog2_exact(na), vz = ilog2_exact(nz);
+    if (va < 0 || vz < 0) return 15;
+    if (*cursor < 0 || *cursor + vz > nchal) return 15;
+    const uint64_t *ys = chal + *cursor;
+    *cursor += vz;
+    if (claim != a_star || z_at >= ORC_P || w_at >= ORC_P) return 15;
+    uint64_t fin;
+    if (!sumcheck_chain(vz, 2, claim, evals, ys, &fin)) return 15;
+    if (fin != fmul(z_at, w_at)) return 15;
+    uint64_t ez;
+    if (mle_int(Z, vz, ys, &ez) != 0 || ez != z_at) return 15;
+    uint64_t *ea = malloc(sizeof(uint64_t) * (size_t)na), *ey = malloc(sizeof(uint64_t) * (size_t)nz);
+    if (!ea || !ey) {
+        free(ea);
+        free(ey);
+        return ORC_E_NOMEM;
+    }
+    chi_vector(z, va, ea);
+    chi_vector(ys, vz, ey);
+    uint64_t w = 0;
+    int bad = 0;
+    for (int64_t a = 0; a < na && !bad; a++) {
+        if (src[a] < 0) continue;
+        if (src[a] >= nz) bad = 1;
+        else w = fadd(w, fmul(ea[a], ey[src[a]]));
+    }
+    free(ea);
+    free(ey);
+    return !bad && w == w_at ? 0 : 15;
+}

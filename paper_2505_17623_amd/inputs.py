@@ -100,6 +100,15 @@ class Workload:
         link = self.links[li]
         return np.asarray(Z_prev) if link is None else link(np.asarray(Z_prev))
 
+    def link_map(self, li: int) -> np.ndarray:
+        """The gather map of layer li's input link (layer li - 1's output Z,
+        n' x k', to layer li's A, n x m): an int64 array of n * m source
+        indices (row-major into Z) with -1 where A is zero padding."""
+        link = self.links[li]
+        zr, zc = self.shapes()[li - 1][0], self.layers[li - 1].B.shape[1]
+        idx = (np.arange(zr * zc, dtype=np.int64) + 1).reshape(zr, zc)
+        return link(idx).reshape(-1) - 1
+
     def shapes(self):
         out = []
         n = self.X.shape[0]

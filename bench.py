@@ -294,6 +294,9 @@ def main():
     ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5],
                     help="workload (default 5: two 512x4096x4096 layers, the largest that fits one GPU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--links", action="store_true",
+                    help="also prove the workload's gather links (config 4: im2col and flatten) in every step; "
+                         "each link call waits for the device")
     ap.add_argument("--fp2-steps", type=int, default=10,
                     help="after the timed region, time this many steps of the same workload proven with "
                          "challenges in F_{p^2} (reported beside the headline; 0 skips it)")
@@ -337,7 +340,7 @@ def main():
     # for the device before the whole step is enqueued (deferred outputs)
     first = None
     for i in range(max(args.warmup, 1)):
-        out = ra.prove_network(ctx, wl, dev, X=X, Bs=Bs)
+        out = ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, links=args.links)
         if first is None:
             first = [o["transcript"] for o in out]
         print(f"# warmup step {i} done", file=sys.stderr, flush=True)
@@ -351,7 +354,7 @@ def main():
     ctx.set_deferred(True)
     bufs = []
     for _ in range(2):
-        outs = [ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs) for _ in range(args.steps)]
+        outs = [ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs, links=args.links) for _ in range(args.steps)]
         ctx.sync()
         assert all([o["transcript"]["P"] for o in out] == planes for out in outs)
 
@@ -363,7 +366,7 @@ def main():
     gc.freeze()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    outs = [ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs) for _ in range(args.steps)]
+    outs = [ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs, links=args.links) for _ in range(args.steps)]
     ctx.sync()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -374,7 +377,7 @@ def main():
     ctx.set_profiling(True)
     torch.cuda.synchronize()
     for i in range(args.steps):
-        ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs)
+        ra.prove_network(ctx, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs, links=args.links)
     ctx.sync()
     torch.cuda.synchronize()
     prof = ctx.profile()
@@ -456,7 +459,8 @@ def main():
                warmup=args.warmup, ms_per_step=round(ms_step, 4), ms_per_layer=round(ms_step / L, 4),
                higher_is_better=True, scaling="weak", vs_baseline=None, dtype="u64 (F_p, p=2^61-1)",
                data="synthetic",
-               config=dict(workload=f"config {args.config}: {wl.name}", layers=L,
+               config=dict(workload=f"config {args.config}: {wl.name}" + (" with gather links" if args.links else ""),
+                           layers=L,
                            shapes=[list(s[:3]) for s in shapes], planes=planes,
                            elements_folded_per_step=el),
                roofline=roofline, cpu_baseline=cpu, kernel_groups=groups, field_fp2=fp2)

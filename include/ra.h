@@ -285,6 +285,48 @@ ra_status ra_range_prove(ra_ctx *ctx, const uint64_t *d_bits, const int32_t *d_R
                          uint32_t k, const ra_witness_info *info, void *d_ws, size_t ws_bytes,
                          ra_range_proof *out);
 
+/* ---- Gather links between layers -------------------------------------------
+ * Sec. III-C chains layers through their outputs.  A convolution's input is a
+ * gather of the previous output Z (im2col: each entry read by up to kh kw
+ * patch positions, with zero padding; flattening: a permutation); the paper
+ * says nothing about proving it.  With A[a] = Z[src[a]] (A[a] = 0 where
+ * src[a] = -1), the claim a* = A~(r1, rho) that the layer's matrix sum-check
+ * ends in equals sum_y Z[y] W[y], W[y] = sum over the a with src[a] = y of
+ * eq((r1, rho), a) (a = row * m + col, row variables first).  A degree-2
+ * sum-check (Sec. II-D) over the entries of Z reduces it to Z~(y*) W~(y*) at
+ * the point y* of its challenges: Z~(y*) is a claim on the previous output,
+ * and the verifier computes W~(y*) from the public map. */
+typedef struct {
+    uint32_t rounds; /* out: log2 z_entries */
+    uint64_t *evals; /* in: host buffer of 3 log2 z_entries words; out: g_j(0), g_j(1), g_j(2) */
+    uint64_t claim;  /* out: g_1(0) + g_1(1) = A~(r1, rho), the layer's a* */
+    uint64_t z_at;   /* out: Z~(y*) */
+    uint64_t w_at;   /* out: W~(y*) */
+} ra_link_proof;
+
+/* Prove the gather link of the layer whose three calls (F_p) have just been
+ * made: d_Z is the previous layer's output (z_entries int32, a power of
+ * two, at most 2^31, row-major), d_src the layer's gather map (a_entries =
+ * n m int32 indices into d_Z, or -1), both device pointers owned by the
+ * caller.  Call it after the layer's ra_range_prove and before the next
+ * proving call (RA_E_STATE otherwise); it consumes log2 z_entries challenges.
+ * Outputs as for the proving calls: complete on return, or at ra_ctx_sync in
+ * deferred mode (out and out->evals must stay valid until then).  An index
+ * outside [-1, z_entries) is not followed and makes the call's status
+ * RA_E_INVAL (a synchronous call then consumes no challenges).  Workspace
+ * as for the proving calls (ra_link_workspace_size bytes for the layer's n,
+ * m, or NULL for the context's own). */
+ra_status ra_link_prove(ra_ctx *ctx, const int32_t *d_Z, uint64_t z_entries, const int32_t *d_src,
+                        uint64_t a_entries, void *d_ws, size_t ws_bytes, ra_link_proof *out);
+ra_status ra_link_workspace_size(uint64_t z_entries, uint32_t n, uint32_t m, size_t *bytes);
+/* The gathered input itself on the device: d_A[a] = d_Z[d_src[a]], 0 where
+ * d_src[a] = -1 (a_entries int32 outputs, caller-owned).  Enqueued on the
+ * context's stream, ordered with its proving calls, returns at once; an
+ * index outside [-1, z_entries) is not followed (d_A[a] = 0) and
+ * ra_link_prove refuses the map. */
+ra_status ra_link_gather(ra_ctx *ctx, const int32_t *d_Z, uint64_t z_entries, const int32_t *d_src,
+                         uint64_t a_entries, int32_t *d_A);
+
 /* ---- The protocol with challenges in the extension field F_{p^2} ----------
  * Sec. II-F asks for a field of more than 128 bits.  Over p = 2^61 - 1 a
  * cheating prover passes a sum-check round with probability about d / p
@@ -337,6 +379,8 @@ typedef struct {
     const int16_t *B;  /* m x k */
     const int32_t *Z;  /* n x k, the claimed layer output */
     uint32_t chained;  /* 1: A must equal the previous layer's Z (int32) */
+    const int32_t *link_src; /* NULL, or the gather map of A (n m indices into the previous layer's Z,
+                                -1 = zero): a* is then checked by the layer's link proof, A not opened */
 } ra_layer_public;
 
 /* Opened tables standing in for the paper's commitments (host pointers). */
@@ -351,6 +395,7 @@ typedef struct {
     ra_matmul_proof mm;
     ra_witness_info wit;
     ra_range_proof rng;
+    ra_link_proof link; /* read when the layer's link_src is set */
 } ra_layer_transcript;
 
 /* Host-only verifier (Sec. IV).  Replays the challenge stream of `seed` (as
@@ -365,7 +410,10 @@ typedef struct {
  *                 link, 5 range chain, 6 range final identity, 7 bit-table
  *                 opening, 8 R/Rm/Y openings, 9 ReLU chain or final identity,
  *                 10 ReLU openings, 11 output link or Z opening, 12 parameters,
- *                 13 malformed layer, 14 chaining.
+ *                 13 malformed layer, 14 chaining, 15 gather link (its chain from a*,
+ *                 the final product, Z~(y*) against the previous layer's Z,
+ *                 W~(y*) against the map).  A layer with a link consumes
+ *                 log2 (previous n k) more challenges after its own.
  *   *failed_layer index of the failing layer (0 when accepted). */
 ra_status ra_verify(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_layer_public *pub,
                     const ra_layer_tables *tables, const ra_layer_transcript *tr, int32_t *verdict,
@@ -379,7 +427,8 @@ ra_status ra_verify_stream(uint64_t p, const uint64_t *h_challenges, uint64_t n_
 /* The host verifier for layers proven over F_{p^2} (ra_prove_layer_fp2): the
  * checks of ra_verify with the same verdict numbers, every transcript element
  * a pair (re, im) in [0, p), the challenges read from the stream of `seed` in
- * pairs. */
+ * pairs.  Gather links are proven over F_p only: a layer with link_src set
+ * gives verdict 13. */
 ra_status ra_verify_fp2(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_layer_public *pub,
                         const ra_layer_tables *tables, const ra_layer_proof_fp2 *tr, int32_t *verdict,
                         uint32_t *failed_layer);

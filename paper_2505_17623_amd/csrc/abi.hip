@@ -41,6 +41,7 @@ struct ra_ctx {
     uint64_t *d_acc = nullptr;  // row-binding accumulators of the fused front (zero between calls)
     size_t acc_cap = 0;
     uint64_t r12_off = 0;  // the layer's (r1, r2): offset in the challenge stream
+    bool link_ok = false;  // a layer over F_p has just been proven: its a* may be linked (ra_link_prove)
     size_t eq_cap = 0;
     WitParams *d_params = nullptr;
     char *d_wit = nullptr;  // the witness's per-workgroup partials (min/max, claims, range flags)
@@ -772,6 +773,7 @@ ra_status ra_sumcheck_matmul_prove(ra_ctx *c, const void *d_A, ra_dtype a_dtype,
     c->k = k;
     c->r12_off = c->cursor;
     c->phase = 1;
+    c->link_ok = false;
     c->cursor += need;
     return finish(c, o_tr, [out, lm](const uint64_t *h) {
         out->log_m = (uint32_t)lm;
@@ -1035,6 +1037,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
         launch_xblock(relu != 0, j == 0, xb, jobs, s);
     }
     c->phase = 0;
+    c->link_ok = true;
     c->cursor += need;
     return finish(c, o_tr, [out, R, relu, lN, F_R, RS, Z0, FZ](const uint64_t *h) {
         out->rounds = (uint32_t)R;
@@ -1256,6 +1259,7 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
     c->stage_used = 0;
     if (prm.status != 0) return prm.status;  // a given t that does not hold R
     c->cursor += 2 * cnt;
+    c->link_ok = false;
     auto pr = [&](size_t o) { return ra_fp2{h[o], h[o + 1]}; };
     io->t = t;
     io->P = (uint32_t)P;
@@ -1282,3 +1286,106 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The gather link (link.hip): after a layer's three calls, the claim a* =
+// A~(r1, rho) of its matrix sum-check is reduced to the previous output.
+// ---------------------------------------------------------------------------
+namespace {
+struct LinkLayout {
+    size_t o_W, o_T0, o_part, o_E, o_bad, bytes;
+};
+
+// n + m: the eq tables of the layer's (r1, rho); at most 2^31 + 2^15 words
+LinkLayout link_layout(uint64_t nz, uint64_t eq_words)
+{
+    const int vz = log2u(nz);
+    Carve cv;
+    LinkLayout L{};
+    L.o_W = cv.take<uint64_t>(nz);
+    L.o_T0 = cv.take<uint64_t>(nz > 1 ? nz / 2 : 1);
+    L.o_part = cv.take<uint64_t>((size_t)(vz > 0 ? vz : 1) * kLinkMaxBlocks * 3);
+    L.o_E = cv.take<uint64_t>(eq_words);
+    L.o_bad = cv.take<uint32_t>(1);
+    L.bytes = cv.off;
+    return L;
+}
+}  // namespace
+
+extern "C" ra_status ra_link_gather(ra_ctx *c, const int32_t *d_Z, uint64_t z_entries, const int32_t *d_src,
+                                    uint64_t a_entries, int32_t *d_A)
+{
+    if (!c || !d_Z || !d_src || !d_A) return RA_E_INVAL;
+    if (!is_pow2(z_entries) || !a_entries) return RA_E_INVAL;
+    launch_link_gather(d_Z, z_entries, d_src, a_entries, d_A, c->stream);
+    RA_HIP(hipGetLastError());
+    return RA_OK;
+}
+
+extern "C" ra_status ra_link_workspace_size(uint64_t z_entries, uint32_t n, uint32_t m, size_t *bytes)
+{
+    if (!bytes || !is_pow2(z_entries) || !is_pow2(n) || !is_pow2(m)) return RA_E_INVAL;
+    if (z_entries > kRangeMaxN) return RA_E_NOT_IMPLEMENTED;
+    *bytes = link_layout(z_entries, (uint64_t)n + m).bytes;
+    return RA_OK;
+}
+
+extern "C" ra_status ra_link_prove(ra_ctx *c, const int32_t *d_Z, uint64_t z_entries, const int32_t *d_src,
+                                   uint64_t a_entries, void *d_ws, size_t ws_bytes, ra_link_proof *out)
+{
+    if (!c || !d_Z || !d_src || !out) return RA_E_INVAL;
+    if (!is_pow2(z_entries)) return RA_E_INVAL;
+    if (z_entries > kRangeMaxN) return RA_E_NOT_IMPLEMENTED;
+    if (c->phase != 0 || !c->link_ok) return RA_E_STATE;
+    if (a_entries != (uint64_t)c->n * c->m) return RA_E_INVAL;
+    const int vz = log2u(z_entries), ln = log2u(c->n), lm = log2u(c->m), lk = log2u(c->k);
+    if (vz && !out->evals) return RA_E_INVAL;
+    ra_status st = ensure_chal(c, (uint64_t)vz);
+    if (st != RA_OK) return st;
+    const LinkLayout L = link_layout(z_entries, (uint64_t)c->n + c->m);
+    char *ws = nullptr;
+    if ((st = call_ws(c, d_ws, ws_bytes, L.bytes, &ws)) != RA_OK) return st;
+    // the transcript goes to the pinned area: 3 vz round words, then claim,
+    // Z~(y*), W~(y*) and the map's status
+    const size_t words = 3 * (size_t)vz + 4;
+    size_t off = 0;
+    if ((st = stage_take(c, words, &off)) != RA_OK) return st;
+    hipStream_t s = c->stream;
+    // the eq tables of (r1, rho) go to the link's own workspace (the
+    // context's eq area may still be read by the layer's deferred kernels)
+    uint64_t *E1 = (uint64_t *)(ws + L.o_E), *E2 = E1 + c->n;
+    const uint64_t *r1 = c->d_chal + c->r12_off, *rho = r1 + ln + lk;
+    launch_eq_tables(r1, ln, E1, rho, lm, E2, s);
+    LinkArgs la{};
+    la.src = d_src;
+    la.na = a_entries;
+    la.lm = lm;
+    la.E1 = E1;
+    la.E2 = E2;
+    la.Z = d_Z;
+    la.vz = vz;
+    la.W = (uint64_t *)(ws + L.o_W);
+    la.T0 = (uint64_t *)(ws + L.o_T0);
+    la.rho = c->d_chal + c->cursor;
+    la.part = (uint64_t *)(ws + L.o_part);
+    la.tr = c->d_stage + off;
+    la.fin = la.tr + 3 * (size_t)vz;
+    la.bad = (uint32_t *)(ws + L.o_bad);
+    launch_link(la, s);
+    c->cursor += (uint64_t)vz;
+    c->link_ok = false;
+    const ra_status r = finish(c, off, [out, vz](const uint64_t *h) {
+        if (h[3 * vz + 3]) return (ra_status)RA_E_INVAL;  // a gather index outside [-1, z_entries)
+        out->rounds = (uint32_t)vz;
+        if (vz) std::memcpy(out->evals, h, 3 * (size_t)vz * 8);
+        out->claim = h[3 * vz];
+        out->z_at = h[3 * vz + 1];
+        out->w_at = h[3 * vz + 2];
+        return (ra_status)RA_OK;
+    });
+    if (r != RA_OK && !c->deferred) {  // a refused map consumes nothing
+        c->cursor -= (uint64_t)vz;
+        c->link_ok = true;
+    }
+    return r;
+}

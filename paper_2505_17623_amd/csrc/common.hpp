@@ -336,6 +336,31 @@ void launch_f2_finish(const F2FinishArgs &a, hipStream_t st);
 void launch_f2_planes(const F2PlaneArgs &a, hipStream_t st);
 void launch_f2_gram_sum(const uint64_t *gpart, int nblk, int TP, uint64_t *G, hipStream_t st);
 
+// ---- the gather link between layers (link.hip) ----
+constexpr int kLinkMaxBlocks = 512;  // blocks of a round launch (partials per round)
+constexpr int kLinkTailLog = 11;     // the last rounds, over at most 2^11 entries, run in one workgroup
+__host__ __device__ inline int link_blocks(uint64_t h)
+{
+    const uint64_t b = (h + kThreads - 1) / kThreads;
+    return (int)(b < (uint64_t)kLinkMaxBlocks ? (b ? b : 1) : kLinkMaxBlocks);
+}
+struct LinkArgs {
+    const int32_t *src;        // na gather indices into Z (-1: zero)
+    uint64_t na;
+    int lm;                    // log2 of the next layer's inner dimension m (a = row * m + col)
+    const uint64_t *E1, *E2;   // eq tables of r1 (rows) and rho (columns)
+    const int32_t *Z;          // the previous output, 2^vz entries
+    int vz;
+    uint64_t *W, *T0;          // 2^vz and 2^(vz-1) words
+    const uint64_t *rho;       // vz round challenges
+    uint64_t *part;            // vz x kLinkMaxBlocks x 3 words
+    uint64_t *tr;              // out: 3 vz words
+    uint64_t *fin;             // out: claim, Z~(y*), W~(y*), the map's status (nonzero: an index outside)
+    uint32_t *bad;             // out: nonzero if a gather index is outside [-1, 2^vz)
+};
+void launch_link(const LinkArgs &a, hipStream_t st);
+void launch_link_gather(const int32_t *Z, uint64_t nz, const int32_t *src, uint64_t na, int32_t *A, hipStream_t st);
+
 // ---- launchers (planes.hip) ----
 int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)

@@ -103,6 +103,22 @@ template <typename I> uint64_t mle_ints(const I *tab, size_t len, const uint64_t
     return mle_bind_all(std::move(T), z, v);
 }
 
+// The 2^v values eq(z, y), y's most significant bit paired with z_0 (the
+// order in which mle_bind_all binds): each variable doubles the table.
+std::vector<uint64_t> eq_table(const uint64_t *z, int v)
+{
+    std::vector<uint64_t> T(1, 1);
+    for (int i = 0; i < v; i++) {
+        std::vector<uint64_t> U(T.size() * 2);
+        for (size_t y = 0; y < T.size(); y++) {
+            U[2 * y + 1] = fmul(T[y], z[i]);
+            U[2 * y] = fsub(T[y], U[2 * y + 1]);
+        }
+        T.swap(U);
+    }
+    return T;
+}
+
 uint64_t eq_points(const uint64_t *a, const uint64_t *b, int v)
 {
     uint64_t acc = 1;
@@ -115,10 +131,12 @@ int verify_layer(const ra_layer_public &L, const ra_layer_tables &T, const ra_la
                  ra_status *err)
 {
     const uint32_t n = L.n, m = L.m, k = L.k;
-    if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k) || !L.A || !L.B || !L.Z || !T.R || !T.Rm || !T.Y || !T.bits)
+    if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k) || (!L.A && !L.link_src) || !L.B || !L.Z || !T.R || !T.Rm ||
+        !T.Y || !T.bits)
         return 13;
     if ((L.a_dtype != RA_I16 && L.a_dtype != RA_I32) || L.s < 1 || L.s > 30 || L.relu > 1 || L.round_mode > 1)
         return 13;
+    if (L.link_src && L.chained) return 13;
     const int ln = log2u(n), lm = log2u(m), lk = log2u(k), lN = ln + lk;
     const uint64_t N = (uint64_t)n * k;
     const int s = (int)L.s, relu = (int)L.relu, t = tr.wit.t;
@@ -168,15 +186,20 @@ int verify_layer(const ra_layer_public &L, const ra_layer_tables &T, const ra_la
     uint64_t fin;
     if (!chain(lm, 2, tr.mm.c0, tr.mm.evals, rho, &fin)) return 1;
     if (fin != fmul(tr.mm.a_star, tr.mm.b_star)) return 2;
-    // 3: a* = A~(r1, rho), b* = B~(rho, r2)
+    // 3: a* = A~(r1, rho) (with a gather link: checked by the link, 15), b* = B~(rho, r2)
+    std::vector<uint64_t> pa(r1, r1 + ln);
+    pa.insert(pa.end(), rho, rho + lm);
     {
-        std::vector<uint64_t> pa(r1, r1 + ln), pb(rho, rho + lm);
-        pa.insert(pa.end(), rho, rho + lm);
+        std::vector<uint64_t> pb(rho, rho + lm);
         pb.insert(pb.end(), r2, r2 + lk);
-        const uint64_t ea = L.a_dtype == RA_I16 ? mle_ints((const int16_t *)L.A, (size_t)n * m, pa.data(), ln + lm)
-                                                : mle_ints((const int32_t *)L.A, (size_t)n * m, pa.data(), ln + lm);
+        if (!L.link_src) {
+            const uint64_t ea = L.a_dtype == RA_I16
+                                    ? mle_ints((const int16_t *)L.A, (size_t)n * m, pa.data(), ln + lm)
+                                    : mle_ints((const int32_t *)L.A, (size_t)n * m, pa.data(), ln + lm);
+            if (ea != tr.mm.a_star) return 3;
+        }
         const uint64_t eb = mle_ints(L.B, (size_t)m * k, pb.data(), lm + lk);
-        if (ea != tr.mm.a_star || eb != tr.mm.b_star) return 3;
+        if (eb != tr.mm.b_star) return 3;
     }
     // 4: C = 2^s R + Rm - 2^(s-1) (floor mode: C = 2^s R + Rm), at (r1, r2)
     {
@@ -238,6 +261,36 @@ int verify_layer(const ra_layer_public &L, const ra_layer_tables &T, const ra_la
         return 11;
     }
     if (mle_ints(L.Z, N, r12.data(), lN) != tr.wit.z_claim) return 11;
+    // 15: the gather link A[a] = Z_prev[src[a]]: a* = sum_y Z_prev[y] W[y]
+    // reduced by a degree-2 sum-check to Z_prev~(y*) W~(y*)
+    if (L.link_src) {
+        if (!prev || !prev->Z) return 15;
+        const uint64_t nz = (uint64_t)prev->n * prev->k;
+        const int vz = log2u(nz);
+        const ra_link_proof &lnk = tr.link;
+        if (lnk.rounds != (uint32_t)vz || (vz && !lnk.evals)) return 15;
+        if (*cursor + vz > nchal) {
+            *err = RA_E_SEED;
+            return 15;
+        }
+        const uint64_t *ys = chal + *cursor;
+        *cursor += vz;
+        if (lnk.claim != tr.mm.a_star || lnk.z_at >= kP || lnk.w_at >= kP) return 15;
+        for (int i = 0; i < 3 * vz; i++)
+            if (lnk.evals[i] >= kP) return 15;
+        if (!chain(vz, 2, lnk.claim, lnk.evals, ys, &fin)) return 15;
+        if (fin != fmul(lnk.z_at, lnk.w_at)) return 15;
+        if (mle_ints(prev->Z, nz, ys, vz) != lnk.z_at) return 15;
+        const std::vector<uint64_t> ea = eq_table(pa.data(), ln + lm), ey = eq_table(ys, vz);
+        uint64_t w = 0;
+        for (uint64_t a = 0; a < (uint64_t)n * m; a++) {
+            const int32_t y = L.link_src[a];
+            if (y == -1) continue;
+            if (y < 0 || (uint64_t)y >= nz) return 15;
+            w = fadd(w, fmul(ea[a], ey[y]));
+        }
+        if (w != lnk.w_at) return 15;
+    }
     return 0;
 }
 
@@ -285,6 +338,7 @@ extern "C" ra_status ra_verify(uint64_t p, uint64_t seed, uint32_t n_layers, con
         const int ln = lg(pub[l].n), lm = lg(pub[l].m), lk = lg(pub[l].k), lN = ln + lk;
         const int lP = is_pow2(tr[l].wit.P) && tr[l].wit.P <= 128 ? log2u(tr[l].wit.P) : 0;
         total += (uint64_t)ln + lk + lm + 4 + 2 * lP + lN + (pub[l].relu ? lN : 0);
+        if (pub[l].link_src && l > 0) total += (uint64_t)lg(pub[l - 1].n) + lg(pub[l - 1].k);
     }
     std::vector<uint64_t> chal(total ? total : 1);
     ra::ChallengeStream cs(seed);
@@ -379,6 +433,7 @@ int verify_layer_fp2(const ra_layer_public &L, const ra_layer_tables &T, const r
     const int ln = log2u(n), lm = log2u(m), lk = log2u(k), lN = ln + lk;
     const uint64_t N = (uint64_t)n * k;
     const int s = (int)L.s, relu = (int)L.relu, t = tr.t;
+    if (L.link_src) return 13;  // gather links are proven over F_p only
     if (L.chained) {
         if (!prev || L.a_dtype != RA_I32 || prev->n != n || prev->k != m) return 14;
         const int32_t *A = (const int32_t *)L.A;

@@ -27,7 +27,8 @@ EXPORTS = ["ra_ctx_create", "ra_ctx_create_stream", "ra_ctx_destroy", "ra_ctx_cu
            "ra_workspace_size", "ra_ctx_set_profiling", "ra_ctx_profile", "ra_ctx_set_deferred", "ra_ctx_sync",
            "ra_mle_bind", "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify",
            "ra_verify_stream", "ra_witness_plan", "ra_mle_bind_noalloc", "ra_prove_layer_fp2",
-           "ra_workspace_size_fp2", "ra_verify_fp2"]
+           "ra_workspace_size_fp2", "ra_verify_fp2", "ra_link_prove", "ra_link_workspace_size",
+           "ra_link_gather"]
 
 
 class RAError(RuntimeError):
@@ -59,7 +60,7 @@ class LayerPublic(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint32), ("m", ctypes.c_uint32), ("k", ctypes.c_uint32),
                 ("s", ctypes.c_uint32), ("relu", ctypes.c_uint32), ("round_mode", ctypes.c_uint32),
                 ("a_dtype", ctypes.c_int), ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
-                ("Z", ctypes.c_void_p), ("chained", ctypes.c_uint32)]
+                ("Z", ctypes.c_void_p), ("chained", ctypes.c_uint32), ("link_src", ctypes.c_void_p)]
 
 
 class LayerTables(ctypes.Structure):
@@ -67,8 +68,12 @@ class LayerTables(ctypes.Structure):
                 ("bits", ctypes.c_void_p)]
 
 
+class LinkProof(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.c_uint32), ("evals", u64p), ("claim", u64), ("z_at", u64), ("w_at", u64)]
+
+
 class LayerTranscript(ctypes.Structure):
-    _fields_ = [("mm", MatmulProof), ("wit", WitnessInfo), ("rng", RangeProof)]
+    _fields_ = [("mm", MatmulProof), ("wit", WitnessInfo), ("rng", RangeProof), ("link", LinkProof)]
 
 
 class Fp2(ctypes.Structure):
@@ -135,11 +140,15 @@ def lib():
                                          vp, vp, vp, vp, vp, vp, u64, vp, ctypes.c_size_t,
                                          ctypes.POINTER(LayerProofFp2)]
         L.ra_workspace_size_fp2.argtypes = [ctypes.c_uint32] * 3 + [ctypes.POINTER(ctypes.c_size_t)]
+        L.ra_link_prove.argtypes = [vp, vp, u64, vp, u64, vp, ctypes.c_size_t, ctypes.POINTER(LinkProof)]
+        L.ra_link_workspace_size.argtypes = [u64, ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(ctypes.c_size_t)]
+        L.ra_link_gather.argtypes = [vp, vp, u64, vp, u64, vp]
         L.ra_verify_fp2.argtypes = [u64, u64, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
                                     ctypes.POINTER(LayerTables), ctypes.POINTER(LayerProofFp2),
                                     ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
         for f in (L.ra_ctx_create, L.ra_ctx_create_stream, L.ra_workspace_size, L.ra_verify_stream,
-                  L.ra_prove_layer_fp2, L.ra_workspace_size_fp2, L.ra_verify_fp2,
+                  L.ra_prove_layer_fp2, L.ra_workspace_size_fp2, L.ra_verify_fp2, L.ra_link_prove,
+                  L.ra_link_workspace_size, L.ra_link_gather,
                   L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
@@ -402,13 +411,51 @@ def to_device(a: np.ndarray, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
-def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, plan=True, ws=None):
+def link_prove(ctx: Context, Z_prev: torch.Tensor, src: torch.Tensor, ws: torch.Tensor | None = None):
+    """The gather link of the layer just proven (ra_link_prove): A[a] =
+    Z_prev[src[a]] (-1: zero), src an int32 device tensor of the layer's n m
+    entries.  Returns dict(evals, claim, z_at, w_at), filled at ctx.sync() in
+    deferred mode."""
+    assert Z_prev.dtype == torch.int32 and src.dtype == torch.int32
+    nz = Z_prev.numel()
+    vz = nz.bit_length() - 1
+    ev = np.zeros(max(3 * vz, 1), dtype=np.uint64)
+    pr = LinkProof()
+    pr.evals = ev.ctypes.data_as(u64p)
+    _check(lib().ra_link_prove(ctx.h, _dptr(Z_prev), nz, _dptr(src), src.numel(), *_ws(ws), ctypes.byref(pr)),
+           "ra_link_prove")
+    res = {}
+    ctx.later(lambda: res.update(evals=[int(x) for x in ev[:3 * vz]], claim=int(pr.claim), z_at=int(pr.z_at),
+                                 w_at=int(pr.w_at)))
+    return res
+
+
+def link_gather(ctx: Context, Z_prev: torch.Tensor, src: torch.Tensor, out: torch.Tensor | None = None):
+    """The gathered input A[a] = Z_prev[src[a]] (0 where src = -1) on the
+    device (ra_link_gather; enqueued on the context's stream)."""
+    assert Z_prev.dtype == torch.int32 and src.dtype == torch.int32
+    if out is None:
+        out = torch.empty(src.shape, dtype=torch.int32, device=src.device)
+    _check(lib().ra_link_gather(ctx.h, _dptr(Z_prev), Z_prev.numel(), _dptr(src), src.numel(), _dptr(out)),
+           "ra_link_gather")
+    return out
+
+
+def link_workspace_size(z_entries: int, n: int, m: int) -> int:
+    v = ctypes.c_size_t()
+    _check(lib().ra_link_workspace_size(z_entries, n, m, ctypes.byref(v)), "ra_link_workspace_size")
+    return int(v.value)
+
+
+def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, plan=True, ws=None,
+                  links=False):
     """Prove every layer of a workload in order.  A layer's input is the
     previous output on the device (MLP chains) or the workload's link (im2col)
     applied on the host.  X / Bs may hold device copies of the inputs; ts may
     give each layer's range parameter t (else it is derived from the data);
     bufs (optional) is a list of per-layer output dicts (prove_layer), grown
-    on first use."""
+    on first use.  links=True also proves every gather link right after its
+    layer (res["link"], res["link_src"] the map on the device)."""
     if bufs is not None:
         while len(bufs) < len(workload.layers):
             bufs.append({})
@@ -421,11 +468,20 @@ def prove_network(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=Non
             A = X
         elif workload.links[li] is None:
             A = Z
-        else:
-            A = to_device(workload.links[li](Z.cpu().numpy()), device)
+        else:   # a gather of the previous output (im2col, flatten), on the device
+            keep = bufs[li] if bufs is not None else {}
+            if "src" not in keep:
+                n, m = workload.shapes()[li][:2]
+                keep["src"] = to_device(workload.link_map(li).astype(np.int32).reshape(n, m), device)
+            src = keep["src"]
+            A = link_gather(ctx, Z, src, keep.get("A"))
+            keep["A"] = A
         t = -1 if ts is None else int(ts[li])
         res = prove_layer(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t,
                           None if bufs is None else bufs[li], plan, ws)
+        if links and li > 0 and workload.links[li] is not None:
+            res["link"] = link_prove(ctx, Z, src, ws)
+            res["link_src"] = src
         res["A"] = A
         Z = res["Z"]
         outs.append(res)
@@ -467,9 +523,14 @@ def ra_verify(challenges, layers):
         rs = np.array(tr["rs_evals"] + [0], dtype=np.uint64)
         zc = np.array(tr["zc_evals"] + [0], dtype=np.uint64)
         keep += list(arrs.values()) + [mm, rs, zc]
+        lsrc = None
+        if L.get("link_src") is not None:
+            lsrc = np.ascontiguousarray(L["link_src"], dtype=np.int32)
+            keep.append(lsrc)
         pubs[i] = LayerPublic(n, m, k, tr["s"], tr["relu"], tr["mode"],
                               RA_I16 if A.dtype == np.int16 else RA_I32, arrs["A"].ctypes.data,
-                              arrs["B"].ctypes.data, arrs["Z"].ctypes.data, int(L.get("chained", 0)))
+                              arrs["B"].ctypes.data, arrs["Z"].ctypes.data, int(L.get("chained", 0)),
+                              None if lsrc is None else lsrc.ctypes.data)
         tabs[i] = LayerTables(arrs["R"].ctypes.data, arrs["Rm"].ctypes.data, arrs["Y"].ctypes.data,
                               arrs["bits"].ctypes.data)
         t = trs[i]
@@ -484,6 +545,13 @@ def ra_verify(challenges, layers):
         t.rng.relu_rounds = len(tr["zc_evals"]) // 4
         t.rng.relu_evals = zc.ctypes.data_as(u64p)
         t.rng.r_at, t.rng.y_at = tr["r_at"], tr["y_at"]
+        if L.get("link") is not None:
+            lk = L["link"]
+            le = np.array(list(lk["evals"]) + [0], dtype=np.uint64)
+            keep.append(le)
+            t.link.rounds = len(lk["evals"]) // 3
+            t.link.evals = le.ctypes.data_as(u64p)
+            t.link.claim, t.link.z_at, t.link.w_at = lk["claim"], lk["z_at"], lk["w_at"]
     verdict = ctypes.c_int32()
     failed = ctypes.c_uint32()
     if seeded:

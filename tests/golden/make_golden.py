@@ -4,10 +4,14 @@ every output table.  Calls only the oracle and the seeded input generator.
 
     python tests/golden/make_golden.py [cfg ...]          (default: 1 2 3 4 5)
     python tests/golden/make_golden.py --fp2 [cfg ...]    -> full_fp2_cfg<N>.json
+    python tests/golden/make_golden.py --links [cfg ...]  -> full_links_cfg<N>.json
 
 With --fp2 the oracle proves the workload with challenges in F_{p^2} (the
 seed's stream read in pairs); the witness tables are those of the F_p proof,
 so only the transcript words (pairs re, im) and the digests of Z are kept.
+With --links every gather link of the workload is proven after its layer
+(the later layers then read later challenges): the transcripts, each link's
+words and the digests of Z are kept.
 
 Digest formats: C, R, Rm, Y, Z as little-endian int64 arrays in row-major
 order; the bit table as P x N bytes (0/1), plane-major; A and B as int64.
@@ -58,6 +62,23 @@ def main_fp2(cfgs):
               flush=True)
 
 
+def main_links(cfgs):
+    orc.build(force=False)
+    for cfg in cfgs:
+        wl = inputs.workload(cfg, "full")
+        t0 = time.time()
+        res = orc.prove_network(wl, links=True)
+        layers = [dict(shape=[r["n"], r["m"], r["k"]], transcript={k: r[k] for k in TRANSCRIPT},
+                       link=r.get("link"), digests=dict(Z=digest_i64(r["Z"]))) for r in res]
+        out = dict(workload=wl.name, config=cfg, oracle_seconds=round(time.time() - t0, 1), layers=layers,
+                   cursor=res[-1]["cursor"], source="oracle/ra_oracle.c via tests/golden/make_golden.py --links")
+        path = os.path.join(HERE, f"full_links_cfg{cfg}.json")
+        with open(path, "w") as f:
+            json.dump(out, f, indent=1)
+        print(f"config {cfg} with links: {len(layers)} layers, oracle {out['oracle_seconds']} s -> {path}",
+              flush=True)
+
+
 def main(cfgs):
     orc.build(force=False)
     for cfg in cfgs:
@@ -84,5 +105,7 @@ if __name__ == "__main__":
     args = sys.argv[1:]
     if args and args[0] == "--fp2":
         main_fp2([int(a) for a in args[1:]] or [1, 2, 3, 4, 5])
+    elif args and args[0] == "--links":
+        main_links([int(a) for a in args[1:]] or [4])
     else:
         main([int(a) for a in args] or [1, 2, 3, 4, 5])

@@ -180,3 +180,72 @@ def test_library_verifier_openings(ra):
     assert verdict(0, A=A) == (3, 0)
     B = base[1]["B"].copy(); B.flat[3] -= 1
     assert verdict(1, B=B) == (3, 1)
+
+
+def linked_network(wl):
+    """The oracle's proof of a workload with its gather links, as ra_verify's layers."""
+    outs = orc.prove_network(wl, links=True)
+    layers = []
+    for li, res in enumerate(outs):
+        L = oracle_layer_for_abi(res, wl.layers[li].B, chained=li > 0 and wl.links[li] is None)
+        if "link" in res:
+            L["link_src"] = wl.link_map(li).astype(np.int32)
+            L["link"] = res["link"]
+        layers.append(L)
+    return layers
+
+
+def test_library_verifier_gather_links(ra):
+    """ra_verify on the oracle's proof of the small CNN with its im2col and
+    flatten links: accepted (stream and seed), and each link tamper rejected
+    with verdict 15 at its layer."""
+    wl = inputs.small(4)
+    base = linked_network(wl)
+    assert sum("link" in L for L in base) == len(base) - 1
+    assert ra.ra_verify(wl.challenges, base) == (0, 0)
+    assert ra.ra_verify(wl.challenge_seed, base) == (0, 0)
+    P = ra.P61
+    half = (P + 1) // 2
+
+    def verdict(li, **over):
+        layers = [dict(L) for L in base]
+        layers[li] = dict(layers[li], **over)
+        return ra.ra_verify(wl.challenges, layers)
+
+    for li in (1, 3, 4):
+        lk = base[li]["link"]
+        ev = list(lk["evals"])
+        ev[0] = (ev[0] + 1) % P
+        assert verdict(li, link=dict(lk, evals=ev)) == (15, li)
+        ev = list(lk["evals"])
+        ev[-1] = (ev[-1] + 1) % P
+        assert verdict(li, link=dict(lk, evals=ev)) == (15, li)
+        # the final product kept: only the opening of Z_prev at y* fails
+        assert verdict(li, link=dict(lk, z_at=2 * lk["z_at"] % P, w_at=lk["w_at"] * half % P)) == (15, li)
+        src = base[li]["link_src"].copy()
+        j = int(np.flatnonzero(src >= 0)[0])
+        src[j] = (src[j] + 1) % (base[li - 1]["Z"].size)
+        assert verdict(li, link_src=src) == (15, li)                  # another public map: W~ fails
+        src = base[li]["link_src"].copy()
+        src[0] = base[li - 1]["Z"].size                               # outside the previous output
+        assert verdict(li, link_src=src) == (15, li)
+        assert verdict(li, link=dict(lk, evals=lk["evals"][:-3])) == (15, li)
+    # with a link, A itself is not opened: a* is tied to Z_prev by the link
+    A = base[2]["A"].copy()
+    A.flat[5] += 1
+    assert verdict(2, A=A) == (0, 0)
+    # a changed previous output breaks that layer's own openings first
+    Z = base[1]["Z"].copy()
+    Z.flat[0] += 1
+    assert verdict(1, Z=Z)[0] != 0
+
+
+def test_link_host_side_errors(ra):
+    L = ra.lib()
+    sz = ctypes.c_size_t()
+    assert L.ra_link_workspace_size(3, 4, 4, ctypes.byref(sz)) == -1
+    assert L.ra_link_workspace_size(4, 3, 4, ctypes.byref(sz)) == -1
+    assert L.ra_link_workspace_size(1 << 32, 4, 4, ctypes.byref(sz)) == -9
+    assert L.ra_link_workspace_size(1 << 20, 4, 4, ctypes.byref(sz)) == 0 and sz.value >= 8 << 20
+    pr = ra.LinkProof()
+    assert L.ra_link_prove(None, None, 4, None, 4, None, 0, ctypes.byref(pr)) == -1

@@ -19,6 +19,8 @@ P61 = (1 << 61) - 1
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ra_oracle.c")
 _SRC2 = os.path.join(_HERE, "ra_oracle_fp2.c")   # the same protocol with challenges in F_{p^2}
+_SRC3 = os.path.join(_HERE, "ra_oracle_fs.c")    # the Fiat-Shamir transcript (SHA-256, Merkle root)
+_HDR3 = os.path.join(_HERE, "ra_oracle_fs.h")
 _LIB = os.path.join(_HERE, "libra_oracle.so")
 _lib = None
 
@@ -37,7 +39,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC",
-                        _SRC, _SRC2, "-o", tmp], check=True)
+                        _SRC, _SRC2, _SRC3, "-o", tmp], check=True)
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -70,11 +72,16 @@ F2_SCALARS = ("c0", "a_star", "b_star", "r_claim", "rm_claim", "y_claim", "z_cla
               "r_at", "y_at")
 
 
+class FsState(ctypes.Structure):
+    """orc_fs: the transcript's 32-byte state and the bytes pending since the last draw."""
+    _fields_ = [("S", ctypes.c_uint8 * 32), ("qlen", ctypes.c_uint32), ("Q", ctypes.c_uint8 * 1024)]
+
+
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(_SRC),
-                                                                       os.path.getmtime(_SRC2)):
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(f)
+                                                                       for f in (_SRC, _SRC2, _SRC3, _HDR3)):
             build()
         L = ctypes.CDLL(_LIB)
         u64p = ctypes.POINTER(ctypes.c_uint64)
@@ -101,6 +108,17 @@ def lib():
                                      u64p, u64p, u64p, u64p]
         L.orc_link_verify.argtypes = [ctypes.c_int64, i64p, u64p, ctypes.c_int64, i64p, ctypes.c_uint64, u64p,
                                       ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, u64p, ctypes.c_int64, i64p]
+        u8p_ = ctypes.c_char_p
+        L.orc_sha256.argtypes = [u8p_, ctypes.c_size_t, u8p_]
+        L.orc_witness_root.argtypes = [i64p] * 4 + [u64p, ctypes.c_int64, u8p_]
+        fsp = ctypes.POINTER(FsState)
+        L.orc2_fs_init.argtypes = [fsp, u8p_]
+        L.orc2_fs_absorb.argtypes = [fsp, u8p_, ctypes.c_uint32]
+        L.orc2_fs_draw.argtypes = [fsp, u64p]
+        L.orc2_prove_layer_fs.argtypes = [ctypes.c_int64] * 3 + [i64p, i64p] + [ctypes.c_int] * 4 + \
+            [fsp, u8p_] + [i64p] * 5 + [u8p, u64p, u64p, u64p, ctypes.POINTER(LayerInfo2), u64p, ctypes.c_int64]
+        L.orc2_verify_layer_fs.argtypes = [ctypes.c_int64] * 3 + [i64p] * 3 + [ctypes.c_int] * 3 + \
+            [i64p] * 4 + [u64p] * 3 + [ctypes.POINTER(LayerInfo2), fsp, u8p_]
         L.orc2_mul.argtypes = [u64p, u64p, u64p]
         L.orc2_inv.argtypes = [u64p, u64p]
         L.orc2_mle_int.argtypes = [i64p, ctypes.c_int, u64p, u64p]
@@ -452,3 +470,140 @@ def fp2_stream(workload):
     """The F_p stream a workload's F_{p^2} proof reads: twice the draws of its F_p proof."""
     from paper_2505_17623_amd import inputs
     return inputs.xorshift64_stream(workload.challenge_seed, 2 * len(workload.challenges))
+
+
+# --- the non-interactive protocol: Fiat-Shamir over F_{p^2} (ra_oracle_fs.c) ---
+def sha256(msg: bytes) -> bytes:
+    out = ctypes.create_string_buffer(32)
+    lib().orc_sha256(msg, len(msg), out)
+    return out.raw
+
+
+def witness_root(R, Rm, Y, Z, words) -> bytes:
+    """Merkle root of the witness tables (R, Rm, Y, Z as integers, the packed bit words)."""
+    arrs = [_i64(np.asarray(x).reshape(-1)) for x in (R, Rm, Y, Z)]
+    w = _u64(np.asarray(words).reshape(-1))
+    out = ctypes.create_string_buffer(32)
+    i64 = ctypes.c_int64
+    rc = lib().orc_witness_root(*[_ptr(a, i64) for a in arrs], _ptr(w, ctypes.c_uint64), w.size, out)
+    if rc != 0:
+        raise OracleError(rc)
+    return out.raw
+
+
+def fs_init(domain: bytes) -> FsState:
+    assert len(domain) == 32
+    st = FsState()
+    lib().orc2_fs_init(ctypes.byref(st), domain)
+    return st
+
+
+def fs_absorb(st: FsState, msg: bytes):
+    if lib().orc2_fs_absorb(ctypes.byref(st), msg, len(msg)) != 0:
+        raise OracleError(-1)
+
+
+def fs_draw(st: FsState):
+    out = np.zeros(2, dtype=np.uint64)
+    lib().orc2_fs_draw(ctypes.byref(st), _ptr(out, ctypes.c_uint64))
+    return int(out[0]), int(out[1])
+
+
+def pack_words(planes) -> np.ndarray:
+    """(P, N) 0/1 planes -> N uint64 words, bit q = plane q."""
+    planes = np.asarray(planes)
+    w = np.zeros(planes.shape[1], dtype=np.uint64)
+    for q in range(planes.shape[0]):
+        w |= planes[q].astype(np.uint64) << np.uint64(q)
+    return w
+
+
+def prove_layer_fs(A, B, s, relu, mode, fs: FsState, pub: bytes, t_in=-1):
+    """One layer made non-interactive (orc2_prove_layer_fs): the challenges
+    are drawn from the transcript `fs` (updated in place), pub the caller's
+    32-byte digest of the public inputs.  Returns a dict like
+    prove_layer_fp2's plus "drawn" (every challenge, in order)."""
+    assert len(pub) == 32
+    A = _i64(A)
+    B = _i64(B)
+    n, m = A.shape
+    k = B.shape[1]
+    N = n * k
+    C, R, Rm, Y, Z = (np.zeros(N, dtype=np.int64) for _ in range(5))
+    bits = np.zeros(128 * N, dtype=np.uint8)
+    lm = m.bit_length() - 1
+    lN = N.bit_length() - 1
+    mm = np.zeros(2 * 3 * max(lm, 1), dtype=np.uint64)
+    rs = np.zeros(2 * 4 * (lN + 7), dtype=np.uint64)
+    zc = np.zeros(2 * 4 * max(lN, 1), dtype=np.uint64)
+    cap = 4 * (lN + 64)
+    drawn = np.zeros(2 * cap, dtype=np.uint64)
+    info = LayerInfo2()
+    i64 = ctypes.c_int64
+    rc = lib().orc2_prove_layer_fs(n, m, k, _ptr(A, i64), _ptr(B, i64), s, int(bool(relu)), mode, t_in,
+                                   ctypes.byref(fs), pub, _ptr(C, i64), _ptr(R, i64), _ptr(Rm, i64), _ptr(Y, i64),
+                                   _ptr(Z, i64), _ptr(bits, ctypes.c_uint8), _ptr(mm, ctypes.c_uint64),
+                                   _ptr(rs, ctypes.c_uint64), _ptr(zc, ctypes.c_uint64), ctypes.byref(info),
+                                   _ptr(drawn, ctypes.c_uint64), cap)
+    if rc != 0:
+        raise OracleError(rc)
+    P = info.P
+    out = dict(n=n, m=m, k=k, s=s, relu=int(bool(relu)), mode=mode,
+               C=C.reshape(n, k), R=R.reshape(n, k), Rm=Rm.reshape(n, k), Y=Y.reshape(n, k),
+               Z=Z.reshape(n, k), bits=bits[:P * N].reshape(P, N).copy(), t=info.t, P=P,
+               challenges_used=int(info.challenges_used),
+               mm_evals=_pairs(mm, 3 * info.n_mm_rounds), rs_evals=_pairs(rs, 4 * info.n_rs_rounds),
+               zc_evals=_pairs(zc, 4 * info.n_zc_rounds), drawn=_pairs(drawn, info.challenges_used // 2))
+    for key in F2_SCALARS:
+        v = getattr(info, key)
+        out[key] = (int(v.re), int(v.im))
+    return out
+
+
+def verify_layer_fs(A, B, Z, s, relu, mode, R, Rm, Y, bits, tr, fs: FsState, pub: bytes):
+    """The Fiat-Shamir verifier (orc2_verify_layer_fs): replays the transcript
+    through `fs` (updated in place); returns the verdict (numbers as verify_layer)."""
+    A = _i64(A)
+    B = _i64(B)
+    n, m = A.shape
+    k = B.shape[1]
+    N = n * k
+    lm = m.bit_length() - 1
+    lN = N.bit_length() - 1
+    info = LayerInfo2()
+    info.t = tr["t"]
+    info.P = tr["P"]
+    for key in F2_SCALARS:
+        re, im = tr[key]
+        setattr(info, key, F2(int(re) & 0xFFFFFFFFFFFFFFFF, int(im) & 0xFFFFFFFFFFFFFFFF))
+    flat = lambda ev, pad: _u64(np.array([c for pair in ev for c in pair] + [0] * pad, dtype=object).astype(np.uint64))
+    mm, rs, zc = flat(tr["mm_evals"], 6), flat(tr["rs_evals"], 8), flat(tr["zc_evals"], 8)
+    want_rs = 4 * (int(tr["P"]).bit_length() - 1 + lN)
+    if len(tr["mm_evals"]) != 3 * lm or len(tr["rs_evals"]) != want_rs or \
+            len(tr["zc_evals"]) != (4 * lN if relu else 0):
+        return 13
+    bits = _i64(np.asarray(bits).reshape(-1))
+    if bits.size != int(tr["P"]) * N:
+        return 12
+    i64 = ctypes.c_int64
+    arrs = [_i64(np.asarray(x).reshape(-1)) for x in (Z, R, Rm, Y)]
+    return int(lib().orc2_verify_layer_fs(n, m, k, _ptr(A, i64), _ptr(B, i64), _ptr(arrs[0], i64), s,
+                                          int(bool(relu)), mode, _ptr(arrs[1], i64), _ptr(arrs[2], i64),
+                                          _ptr(arrs[3], i64), _ptr(bits, i64), _ptr(mm, ctypes.c_uint64),
+                                          _ptr(rs, ctypes.c_uint64), _ptr(zc, ctypes.c_uint64), ctypes.byref(info),
+                                          ctypes.byref(fs), pub))
+
+
+def prove_network_fs(workload, domain: bytes, pubs):
+    """Every layer of a workload made non-interactive, one transcript from
+    `domain` through all layers; pubs[li] is layer li's 32-byte public digest."""
+    fs = fs_init(domain)
+    results = []
+    Z = None
+    for li, layer in enumerate(workload.layers):
+        A = workload.layer_input(li, Z)
+        res = prove_layer_fs(A, layer.B, layer.s, layer.relu, workload.mode, fs, pubs[li])
+        res["A"] = A
+        Z = res["Z"]
+        results.append(res)
+    return results

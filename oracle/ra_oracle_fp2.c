@@ -33,6 +33,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include "ra_oracle_fs.h"
+
 typedef unsigned __int128 u128;
 
 #define P2_P ((uint64_t)0x1FFFFFFFFFFFFFFFULL) /* 2^61 - 1 */
@@ -180,13 +182,74 @@ int orc2_mle_int(const int64_t *tab, int v, const uint64_t *z, uint64_t *out)
 /* ------------------------------------------------------------------------ */
 typedef f2 (*summand2_fn)(const f2 *vals, const void *ctx);
 
-static void sumcheck_prove2(int v, int deg, int ntab, f2 **tabs, summand2_fn f, const void *fctx, const f2 *rho,
-                            f2 *evals, f2 *finals)
+/* ------------------------------------------------------------------------ */
+/* Where the challenges come from: the F_p stream read in pairs (the          */
+/* interactive protocol with the verifier's coins given), or the Fiat-Shamir */
+/* transcript of ra_oracle_fs.c (each challenge a hash of what the prover     */
+/* has sent).  Every challenge drawn is also logged, in order.                */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    const uint64_t *chal; /* stream (fs == NULL) */
+    int64_t nchal, *cursor;
+    orc_fs *fs;
+    f2 *log;
+    int64_t nlog, cap;
+    int err;
+} chsrc;
+
+static f2 src_draw(chsrc *src)
+{
+    f2 c = f2of(0);
+    if (src->fs) {
+        uint64_t w[2];
+        orc_fs_draw(src->fs, w);
+        c.re = w[0];
+        c.im = w[1];
+    } else if (*src->cursor < 0 || *src->cursor + 2 > src->nchal) {
+        src->err = P2_E_CHALLENGES;
+    } else {
+        c.re = src->chal[*src->cursor];
+        c.im = src->chal[*src->cursor + 1];
+        if (!f2ok(c)) src->err = P2_E_CHALLENGES;
+        *src->cursor += 2;
+    }
+    if (src->nlog < src->cap) src->log[src->nlog] = c;
+    src->nlog++;
+    return c;
+}
+
+static void src_absorb_bytes(chsrc *src, const uint8_t *b, uint32_t len)
+{
+    if (src->fs && orc_fs_absorb(src->fs, b, len) != 0) src->err = P2_E_INVAL;
+}
+
+static void src_absorb_f2(chsrc *src, const f2 *v, int count)
+{
+    for (int i = 0; i < count; i++) {
+        uint8_t b[16];
+        for (int j = 0; j < 8; j++) {
+            b[j] = (uint8_t)(v[i].re >> (8 * j));
+            b[8 + j] = (uint8_t)(v[i].im >> (8 * j));
+        }
+        src_absorb_bytes(src, b, 16);
+    }
+}
+
+/*
+ * The textbook sum-check prover (Sec. II-D) for sum_{x in {0,1}^v}
+ * f(T_1(x), ..., T_q(x)) over multilinear tables.  Round j (x_j free,
+ * x_1..x_{j-1} bound) sends g_j(X) at X = 0..deg, each table being lo + X
+ * (hi - lo) in the free variable; the message is absorbed, the challenge
+ * rho_j drawn, and every table bound at x_j = rho_j.  The tables are consumed.
+ */
+static void sumcheck_prove2_src(int v, int deg, int ntab, f2 **tabs, summand2_fn f, const void *fctx, chsrc *src,
+                                f2 *rho_out, f2 *evals, f2 *finals)
 {
     size_t size = (size_t)1 << v;
     f2 vals[8];
     for (int j = 0; j < v; j++) {
         size_t h = size / 2;
+        f2 *g = evals + (size_t)j * (deg + 1);
         for (int X = 0; X <= deg; X++) {
             f2 acc = f2of(0);
             for (size_t i = 0; i < h; i++) {
@@ -196,11 +259,13 @@ static void sumcheck_prove2(int v, int deg, int ntab, f2 **tabs, summand2_fn f, 
                 }
                 acc = f2add(acc, f(vals, fctx));
             }
-            evals[(size_t)j * (deg + 1) + X] = acc;
+            g[X] = acc;
         }
+        src_absorb_f2(src, g, deg + 1);
+        const f2 r = src_draw(src);
+        rho_out[j] = r;
         for (int q = 0; q < ntab; q++)
-            for (size_t i = 0; i < h; i++)
-                tabs[q][i] = f2add(tabs[q][i], f2mul(rho[j], f2sub(tabs[q][i + h], tabs[q][i])));
+            for (size_t i = 0; i < h; i++) tabs[q][i] = f2add(tabs[q][i], f2mul(r, f2sub(tabs[q][i + h], tabs[q][i])));
         size = h;
     }
     for (int q = 0; q < ntab; q++) finals[q] = tabs[q][0];
@@ -301,16 +366,43 @@ static int take_challenges(const uint64_t *chal, int64_t nchal, int64_t *cursor,
     return P2_OK;
 }
 
+/* the packed bit table: word x has bit q = plane q (P <= 64) */
+static void pack_words(const uint8_t *bits, int64_t N, int P, uint64_t *words)
+{
+    for (int64_t x = 0; x < N; x++) {
+        uint64_t w = 0;
+        for (int q = 0; q < P && q < 64; q++) w |= (uint64_t)(bits[(size_t)q * N + x] & 1) << q;
+        words[x] = w;
+    }
+}
+
+static void absorb_header(chsrc *src, int64_t n, int64_t m, int64_t k, int s, int relu, int mode, int t, int P,
+                          const uint8_t *pub, const uint8_t *root)
+{
+    const uint32_t h[8] = {(uint32_t)n, (uint32_t)m, (uint32_t)k, (uint32_t)s, (uint32_t)relu, (uint32_t)mode,
+                           (uint32_t)t, (uint32_t)P};
+    uint8_t b[32];
+    for (int i = 0; i < 8; i++)
+        for (int j = 0; j < 4; j++) b[4 * i + j] = (uint8_t)(h[i] >> (8 * j));
+    src_absorb_bytes(src, b, 32);
+    src_absorb_bytes(src, pub, 32);
+    src_absorb_bytes(src, root, 32);
+}
+
 /*
- * Prove one layer over F_{p^2}: the steps of orc_prove_layer (ra_oracle.c)
- * with every challenge-dependent value in F_{p^2}.  bits must hold 128 N
- * bytes; mm_evals 3 log m, rs_evals 4 (log P + log N), zc_evals 4 log N
- * elements.
+ * One layer over F_{p^2}: the steps of orc_prove_layer (ra_oracle.c) with
+ * every challenge-dependent value in F_{p^2}, the challenges drawn from `src`
+ * at the points where the verifier sends them.  With a Fiat-Shamir source the
+ * prover first absorbs the layer header, the caller's public digest `pub` and
+ * the Merkle root of its witness tables; then each message (round values, the
+ * final values and claims) before the challenge that follows it.  bits must
+ * hold 128 N bytes; mm_evals 3 log m, rs_evals 4 (log P + log N), zc_evals
+ * 4 log N elements.
  */
-int orc2_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, int s, int relu, int mode,
-                     int t_in, const uint64_t *chal, int64_t nchal, int64_t *cursor, int64_t *C, int64_t *R,
-                     int64_t *Rm, int64_t *Y, int64_t *Z, uint8_t *bits, f2 *mm_evals, f2 *rs_evals, f2 *zc_evals,
-                     orc2_layer_info *info)
+static int prove_layer_src(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, int s, int relu,
+                           int mode, int t_in, chsrc *src, const uint8_t *pub, int64_t *C, int64_t *R, int64_t *Rm,
+                           int64_t *Y, int64_t *Z, uint8_t *bits, f2 *mm_evals, f2 *rs_evals, f2 *zc_evals,
+                           orc2_layer_info *info)
 {
     int ln = ilog2x(n), lm = ilog2x(m), lk = ilog2x(k);
     if (ln < 0 || lm < 0 || lk < 0 || s < 1 || s > 30 || (mode != 0 && mode != 1)) return P2_E_INVAL;
@@ -326,21 +418,30 @@ int orc2_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const in
     info->n_mm_rounds = lm;
     info->n_rs_rounds = lP + lN;
     info->n_zc_rounds = relu ? lN : 0;
-
     int64_t need = ln + lk + lm + 4 + lP + (lP + lN) + (relu ? lN : 0);
+    if (!src->fs && (*src->cursor < 0 || *src->cursor + 2 * need > src->nchal)) return P2_E_CHALLENGES;
+    orc_fill_planes(bits, N, P, s, t, relu, R, Rm, Y);
+    if (src->fs) {
+        uint64_t *words = malloc(sizeof(uint64_t) * (size_t)N);
+        uint8_t root[32];
+        if (!words || P > 64) {
+            free(words);
+            return P2_E_INVAL;
+        }
+        pack_words(bits, N, P, words);
+        rc = orc_witness_root(R, Rm, Y, Z, words, N, root);
+        free(words);
+        if (rc != 0) return P2_E_NOMEM;
+        absorb_header(src, n, m, k, s, relu, mode, t, P, pub, root);
+    }
+    const int64_t draws0 = src->nlog;
+
     f2 *c = (f2 *)malloc(sizeof(f2) * (size_t)(need > 0 ? need : 1));
     if (!c) return P2_E_NOMEM;
-    int64_t cur0 = *cursor;
-    if ((rc = take_challenges(chal, nchal, cursor, need, c)) != P2_OK) {
-        free(c);
-        return rc;
-    }
-    info->challenges_used = *cursor - cur0;
-    const f2 *r1 = c, *r2 = c + ln, *rho = c + ln + lk, *lam = c + ln + lk + lm;
-    const f2 mu = lam[3];
-    const f2 *tau_p = lam + 4, *sigma = tau_p + lP, *rho2 = sigma + lP + lN;
-
-    orc_fill_planes(bits, N, P, s, t, relu, R, Rm, Y);
+    f2 *r1 = c, *r2 = c + ln, *rho = c + ln + lk, *lam = c + ln + lk + lm;
+    f2 *tau_p = lam + 4, *sigma = tau_p + lP, *rho2 = sigma + lP + lN;
+    for (int i = 0; i < ln; i++) r1[i] = src_draw(src);
+    for (int i = 0; i < lk; i++) r2[i] = src_draw(src);
 
     /* Matrix sum-check (Eq. (4)): a(l) = sum_i chi_i(r1) A[i, l], b(l) = sum_j B[l, j] chi_j(r2). */
     f2 *chi1 = malloc(sizeof(f2) * (size_t)n), *chi2 = malloc(sizeof(f2) * (size_t)k);
@@ -361,7 +462,7 @@ int orc2_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const in
     info->c0 = c0;
     {
         f2 *tabs[2] = {ta, tb}, fin[2];
-        sumcheck_prove2(lm, 2, 2, tabs, sm_matmul, NULL, rho, mm_evals, fin);
+        sumcheck_prove2_src(lm, 2, 2, tabs, sm_matmul, NULL, src, rho, mm_evals, fin);
         info->a_star = fin[0];
         info->b_star = fin[1];
     }
@@ -375,6 +476,13 @@ int orc2_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const in
     mle_int2(Rm, lN, r12, &info->rm_claim);
     mle_int2(Y, lN, r12, &info->y_claim);
     mle_int2(Z, lN, r12, &info->z_claim);
+    {
+        const f2 sent[6] = {info->a_star, info->b_star, info->r_claim, info->rm_claim, info->y_claim, info->z_claim};
+        src_absorb_f2(src, sent, 6);
+    }
+    for (int i = 0; i < 4; i++) lam[i] = src_draw(src);
+    for (int i = 0; i < lP; i++) tau_p[i] = src_draw(src);
+    const f2 mu = lam[3];
 
     /* Concatenated range sum-check over b(plane, x), index plane N + x. */
     {
@@ -401,8 +509,9 @@ int orc2_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const in
         info->range_sum = f2mul(mu, H);
         range2_ctx rcx = {mu};
         f2 *tabs[3] = {teq, tg, tbits}, fin[3];
-        sumcheck_prove2(v, 3, 3, tabs, sm_range, &rcx, sigma, rs_evals, fin);
+        sumcheck_prove2_src(v, 3, 3, tabs, sm_range, &rcx, src, sigma, rs_evals, fin);
         info->bits_claim = fin[2];
+        src_absorb_f2(src, &info->bits_claim, 1);
         free(teq);
         free(tg);
         free(tbits);
@@ -417,19 +526,49 @@ int orc2_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const in
                 ty[x] = f2int(Y[x]);
             }
             f2 *tabs2[3] = {chix, tr, ty}, fin2[3];
-            sumcheck_prove2(lN, 3, 3, tabs2, sm_relu, NULL, rho2, zc_evals, fin2);
+            sumcheck_prove2_src(lN, 3, 3, tabs2, sm_relu, NULL, src, rho2, zc_evals, fin2);
             info->r_at = fin2[1];
             info->y_at = fin2[2];
+            const f2 sent[2] = {info->r_at, info->y_at};
+            src_absorb_f2(src, sent, 2);
             free(tr);
             free(ty);
         }
         free(chix);
     }
+    info->challenges_used = 2 * (src->nlog - draws0);
     free(r12);
     free(chi1);
     free(chi2);
     free(c);
-    return P2_OK;
+    return src->err;
+}
+
+/* The layer with the challenges read from the F_p stream in pairs (word
+ * *cursor on). */
+int orc2_prove_layer(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, int s, int relu, int mode,
+                     int t_in, const uint64_t *chal, int64_t nchal, int64_t *cursor, int64_t *C, int64_t *R,
+                     int64_t *Rm, int64_t *Y, int64_t *Z, uint8_t *bits, f2 *mm_evals, f2 *rs_evals, f2 *zc_evals,
+                     orc2_layer_info *info)
+{
+    chsrc src = {chal, nchal, cursor, NULL, NULL, 0, 0, P2_OK};
+    return prove_layer_src(n, m, k, A, B, s, relu, mode, t_in, &src, NULL, C, R, Rm, Y, Z, bits, mm_evals, rs_evals,
+                           zc_evals, info);
+}
+
+/* The layer made non-interactive: the challenges from the Fiat-Shamir
+ * transcript *fs (carried from layer to layer), pub the caller's 32-byte
+ * digest of the public inputs.  drawn (optional, 2 (log n + log k + log m + 4
+ * + 2 log P + log N (1 + relu)) words) receives every challenge drawn. */
+int orc2_prove_layer_fs(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, int s, int relu,
+                        int mode, int t_in, orc_fs *fs, const uint8_t *pub, int64_t *C, int64_t *R, int64_t *Rm,
+                        int64_t *Y, int64_t *Z, uint8_t *bits, f2 *mm_evals, f2 *rs_evals, f2 *zc_evals,
+                        orc2_layer_info *info, f2 *drawn, int64_t drawn_cap)
+{
+    int64_t cur = 0;
+    chsrc src = {NULL, 0, &cur, fs, drawn, 0, drawn ? drawn_cap : 0, P2_OK};
+    return prove_layer_src(n, m, k, A, B, s, relu, mode, t_in, &src, pub, C, R, Rm, Y, Z, bits, mm_evals, rs_evals,
+                           zc_evals, info);
 }
 
 /*
@@ -549,3 +688,94 @@ done:
     free(r12);
     return verdict;
 }
+
+/*
+ * Verify one layer made non-interactive: replay the prover's transcript
+ * through *fs (header, pub, the Merkle root of the opened tables, then every
+ * message in the prover's order) to recover the challenges, and run the
+ * checks of orc2_verify_layer with them.  bits: the P x N planes (0 or 1).
+ */
+int orc2_verify_layer_fs(int64_t n, int64_t m, int64_t k, const int64_t *A, const int64_t *B, const int64_t *Z,
+                         int s, int relu, int mode, const int64_t *R, const int64_t *Rm, const int64_t *Y,
+                         const int64_t *bits, const f2 *mm_evals, const f2 *rs_evals, const f2 *zc_evals,
+                         const orc2_layer_info *info, orc_fs *fs, const uint8_t *pub)
+{
+    int ln = ilog2x(n), lm = ilog2x(m), lk = ilog2x(k);
+    if (ln < 0 || lm < 0 || lk < 0 || s < 1 || s > 30) return 13;
+    int64_t N = n * k;
+    int lN = ln + lk, t = info->t;
+    if (t < 0 || s + t + 3 > 61) return 12;
+    int Q = s + (t + 2) + (relu ? (t + 2) : 0), P = 1, lP = 0;
+    while (P < Q) { P *= 2; lP++; }
+    if (info->P != P || P > 64) return 12;
+    uint64_t *words = malloc(sizeof(uint64_t) * (size_t)N);
+    if (!words) return 13;
+    for (int64_t x = 0; x < N; x++) {
+        uint64_t w = 0;
+        for (int q = 0; q < P; q++) {
+            int64_t b = bits[(size_t)q * N + x];
+            if (b != 0 && b != 1) {
+                free(words);
+                return 13;
+            }
+            w |= (uint64_t)b << q;
+        }
+        words[x] = w;
+    }
+    uint8_t root[32];
+    int rc = orc_witness_root(R, Rm, Y, Z, words, N, root);
+    free(words);
+    if (rc != 0) return 13;
+    int64_t need = ln + lk + lm + 4 + lP + (lP + lN) + (relu ? lN : 0);
+    f2 *c = malloc(sizeof(f2) * (size_t)(need > 0 ? need : 1));
+    uint64_t *chal = malloc(sizeof(uint64_t) * (size_t)(2 * need + 2));
+    if (!c || !chal) {
+        free(c);
+        free(chal);
+        return 13;
+    }
+    int64_t cur = 0;
+    chsrc src = {NULL, 0, &cur, fs, c, 0, need, P2_OK};
+    absorb_header(&src, n, m, k, s, relu, mode, t, P, pub, root);
+    for (int i = 0; i < ln + lk; i++) src_draw(&src);
+    for (int j = 0; j < lm; j++) {
+        src_absorb_f2(&src, mm_evals + 3 * j, 3);
+        src_draw(&src);
+    }
+    {
+        const f2 sent[6] = {info->a_star, info->b_star, info->r_claim, info->rm_claim, info->y_claim, info->z_claim};
+        src_absorb_f2(&src, sent, 6);
+    }
+    for (int i = 0; i < 4 + lP; i++) src_draw(&src);
+    for (int j = 0; j < lP + lN; j++) {
+        src_absorb_f2(&src, rs_evals + 4 * j, 4);
+        src_draw(&src);
+    }
+    src_absorb_f2(&src, &info->bits_claim, 1);
+    if (relu) {
+        for (int j = 0; j < lN; j++) {
+            src_absorb_f2(&src, zc_evals + 4 * j, 4);
+            src_draw(&src);
+        }
+        const f2 sent[2] = {info->r_at, info->y_at};
+        src_absorb_f2(&src, sent, 2);
+    }
+    int verdict = 13;
+    if (src.err == P2_OK && src.nlog == need) {
+        for (int64_t i = 0; i < need; i++) {
+            chal[2 * i] = c[i].re;
+            chal[2 * i + 1] = c[i].im;
+        }
+        int64_t cur2 = 0;
+        verdict = orc2_verify_layer(n, m, k, A, B, Z, s, relu, mode, R, Rm, Y, bits, mm_evals, rs_evals, zc_evals,
+                                    info, chal, 2 * need, &cur2);
+    }
+    free(c);
+    free(chal);
+    return verdict;
+}
+
+/* exported for the pins: the transcript's state, absorb and draw */
+void orc2_fs_init(orc_fs *t, const uint8_t *domain) { orc_fs_init(t, domain); }
+int orc2_fs_absorb(orc_fs *t, const uint8_t *m, uint32_t len) { return orc_fs_absorb(t, m, len); }
+void orc2_fs_draw(orc_fs *t, uint64_t *out) { orc_fs_draw(t, out); }

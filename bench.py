@@ -300,6 +300,9 @@ def main():
     ap.add_argument("--fp2-steps", type=int, default=10,
                     help="after the timed region, time this many steps of the same workload proven with "
                          "challenges in F_{p^2} (reported beside the headline; 0 skips it)")
+    ap.add_argument("--fs-steps", type=int, default=10,
+                    help="then this many steps of the non-interactive proof (Fiat-Shamir over F_{p^2}, the "
+                         "transcript hashed on the device; reported beside the headline; 0 skips it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed region, copy a MIB-sized device buffer once (a plain copy kernel "
                          "of known size, to scale hardware byte counters)")
@@ -441,6 +444,32 @@ def main():
         del outs2, bufs2, ctx2
         print(f"# F_p^2 leg: {ms2:.3f} ms per step", file=sys.stderr, flush=True)
 
+    # the non-interactive proof: every challenge hashed from the transcript on
+    # the device (witness Merkle root first), one transcript across the steps
+    fsl = None
+    if args.fs_steps > 0:
+        domain, pubs = wl.fs_inputs()
+        ctx3 = ra.Context(fs_domain=domain)
+        bufs3 = []
+        for _ in range(2):
+            ra.prove_network_fp2(ctx3, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs3, pubs=pubs)
+        gc.collect()
+        gc.freeze()
+        torch.cuda.synchronize()
+        u0 = time.perf_counter()
+        outs3 = [ra.prove_network_fp2(ctx3, wl, dev, X=X, Bs=Bs, ts=ts, bufs=bufs3, pubs=pubs)
+                 for _ in range(args.fs_steps)]
+        torch.cuda.synchronize()
+        el3 = time.perf_counter() - u0
+        assert all([o["transcript"]["P"] for o in out] == planes for out in outs3)
+        ms3 = 1e3 * el3 / args.fs_steps
+        fsl = dict(field="F_p[i]/(i^2+1)", transform="Fiat-Shamir, SHA-256 on the device", steps=args.fs_steps,
+                   ms_per_step=round(ms3, 4), ms_per_layer=round(ms3 / L, 4),
+                   value=round(el * args.fs_steps / el3, 1), unit="field elements folded/s",
+                   vs_fp_ms=round(ms3 / ms_step, 3), note="synchronous per layer; not the headline")
+        del outs3, bufs3, ctx3
+        print(f"# non-interactive leg: {ms3:.3f} ms per step", file=sys.stderr, flush=True)
+
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -463,7 +492,8 @@ def main():
                            layers=L,
                            shapes=[list(s[:3]) for s in shapes], planes=planes,
                            elements_folded_per_step=el),
-               roofline=roofline, cpu_baseline=cpu, kernel_groups=groups, field_fp2=fp2)
+               roofline=roofline, cpu_baseline=cpu, kernel_groups=groups, field_fp2=fp2,
+               non_interactive=fsl)
     print(json.dumps(rec), flush=True)
 
 

@@ -433,6 +433,52 @@ ra_status ra_verify_fp2(uint64_t p, uint64_t seed, uint32_t n_layers, const ra_l
                         const ra_layer_tables *tables, const ra_layer_proof_fp2 *tr, int32_t *verdict,
                         uint32_t *failed_layer);
 
+/* ---- The non-interactive protocol: Fiat-Shamir over F_{p^2} ---------------
+ * The paper's protocol is interactive (the verifier's coins; Sec. II-D, Alg.
+ * 1).  Here every challenge is a hash of what the prover has sent before it.
+ * With H = SHA-256 (FIPS 180-4):
+ *   S = H("range-arithmetic fs v1" || domain), domain 32 caller bytes;
+ *   absorb(M) appends M to the bytes Q pending since the last draw;
+ *   a draw sets S = H(S || LE32(|Q|) || Q), empties Q and returns
+ *   (LE64(S[0..8]) mod p) + (LE64(S[8..16]) mod p) i;
+ *   F_{p^2} elements are absorbed as LE64(re) || LE64(im), integers as LE32.
+ * Per layer, in order: absorb LE32 n, m, k, s, relu, round_mode, t, P, the
+ * caller's 32-byte public digest (what binds A and B) and the Merkle root of
+ * the witness tables; draw r1 (log n), r2 (log k); per matrix round absorb
+ * g_j(0..2), draw rho_j; absorb a*, b*, R~, Rm~, Y~, Z~; draw lambda1..3, mu,
+ * tau_p (log P); per range round absorb g_j(0..3), draw sigma_j; absorb
+ * b~(sigma); with ReLU per round absorb g_j(0..3), draw rho'_j, then absorb
+ * r_at, y_at.  The pending bytes carry into the next layer.
+ * Merkle root: the tables R (LE32), Rm (LE16), Y (LE32), Z (LE32) and the bit
+ * words (LE64), each zero-padded to 1024-byte chunks and concatenated; leaf
+ * H(0x00 || chunk); while more than one digest remains, groups of 4 (the
+ * last zero-filled) give H(0x01 || 4 digests); root H(0x02 || LE64(leaves)
+ * || top).  The witness is thus fixed before any challenge that tests it. */
+
+/* A context whose challenges come from a Fiat-Shamir transcript started
+ * from `domain` (32 host bytes), carried from layer to layer on the device.
+ * Only ra_prove_layer_fs draws from it (the stream calls return RA_E_SEED). */
+ra_status ra_ctx_create_fs(uint64_t p, const uint8_t *domain, void *hip_stream, ra_ctx **out);
+
+/* One layer's non-interactive proof: arguments, outputs and workspace
+ * (ra_workspace_size_fp2) as ra_prove_layer_fp2, every challenge drawn on the
+ * device from the context's transcript in the order above.  pub_digest: the
+ * caller's 32 bytes binding the public inputs (host).  root_out (optional,
+ * 32 host bytes): the witness tables' Merkle root.  Waits for its work;
+ * RA_E_STATE on a context without a transcript. */
+ra_status ra_prove_layer_fs(ra_ctx *ctx, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
+                            uint32_t m, uint32_t k, int64_t *d_C, int32_t *d_R, uint16_t *d_Rm, int32_t *d_Y,
+                            int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words, const uint8_t *pub_digest,
+                            void *d_ws, size_t ws_bytes, ra_layer_proof_fp2 *io, uint8_t *root_out);
+
+/* Host verifier of non-interactive proofs: replays each layer's transcript
+ * (pub_digests: n_layers x 32 bytes) to recover its challenges, then applies
+ * the checks of ra_verify_fp2 (same verdict numbers; 13 also for a transcript
+ * that cannot be replayed). */
+ra_status ra_verify_fs(uint64_t p, const uint8_t *domain, uint32_t n_layers, const ra_layer_public *pub,
+                       const ra_layer_tables *tables, const ra_layer_proof_fp2 *tr, const uint8_t *pub_digests,
+                       int32_t *verdict, uint32_t *failed_layer);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,7 @@
  * bit table (N LE64 words, bit q of word x = plane q), each zero-padded to a
  * multiple of 1024 bytes and concatenated: chunk i of 1024 bytes gives the
  * leaf H(0x00 || chunk_i); while more than one digest remains, consecutive
- * digests are grouped by 32 (the last group zero-filled) into H(0x01 || 32
+ * digests are grouped by 4 (the last group zero-filled) into H(0x01 || 4
  * digests); the root is H(0x02 || LE64(leaves) || top).
  *
  * SHA-256 follows FIPS 180-4 Sec. 4-6; its constants are computed from their
@@ -215,12 +215,13 @@ int orc_witness_root(const int64_t *R, const int64_t *Rm, const int64_t *Y, cons
     }
     size_t leaves = count;
     while (count > 1) {
-        size_t next = (count + 31) / 32;
+        size_t next = (count + 3) / 4;
         for (size_t g = 0; g < next; g++) {
-            memset(buf, 0, sizeof(buf));
-            buf[0] = 0x01;
-            for (size_t c = 0; c < 32 && 32 * g + c < count; c++) memcpy(buf + 1 + 32 * c, dig + 32 * (32 * g + c), 32);
-            orc_sha256(buf, sizeof(buf), dig + 32 * g); /* g <= 32 g: the group's inputs are already read */
+            uint8_t node[1 + 4 * 32];
+            memset(node, 0, sizeof(node));
+            node[0] = 0x01;
+            for (size_t c = 0; c < 4 && 4 * g + c < count; c++) memcpy(node + 1 + 32 * c, dig + 32 * (4 * g + c), 32);
+            orc_sha256(node, sizeof(node), dig + 32 * g); /* g <= 4 g: the group's inputs are already read */
         }
         count = next;
     }

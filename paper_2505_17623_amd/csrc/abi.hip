@@ -42,6 +42,7 @@ struct ra_ctx {
     size_t acc_cap = 0;
     uint64_t r12_off = 0;  // the layer's (r1, r2): offset in the challenge stream
     bool link_ok = false;  // a layer over F_p has just been proven: its a* may be linked (ra_link_prove)
+    sha::Transcript *d_fs = nullptr;  // the Fiat-Shamir transcript (ra_ctx_create_fs), on the device
     size_t eq_cap = 0;
     WitParams *d_params = nullptr;
     char *d_wit = nullptr;  // the witness's per-workgroup partials (min/max, claims, range flags)
@@ -450,8 +451,14 @@ RangeLayout range_layout(uint64_t N, int lP, int relu)
 constexpr int kF2TrFixed = 22;
 struct Fp2Layout {
     size_t o_gemm, o_e1, o_e2, o_scr, o_a, o_b, o_eq, o_eqr, o_eqz, o_bx, o_d, o_s, o_sig, o_one, o_gp0, o_gp1, o_g,
-        o_part, o_cpart, o_cst, o_tr, tr_words, bytes;
+        o_part, o_cpart, o_cst, o_tr, tr_words, o_fsch, o_dig0, o_dig1, o_root, o_err, bytes;
 };
+// leaves of the witness tables' Merkle tree (R, Rm, Y, Z int32 / uint16, the bit words)
+uint64_t witness_leaves(uint64_t N)
+{
+    auto ch = [](uint64_t b) { return (b + 1023) / 1024; };
+    return 3 * ch(4 * N) + ch(2 * N) + ch(8 * N);
+}
 Fp2Layout fp2_layout(bool a_i32, uint32_t n, uint32_t m, uint32_t k)
 {
     const uint64_t N = (uint64_t)n * k, H = N > 1 ? N / 2 : 1;
@@ -481,6 +488,12 @@ Fp2Layout fp2_layout(bool a_i32, uint32_t n, uint32_t m, uint32_t k)
     l.o_cst = cv.take<uint64_t>(8);
     l.tr_words = kF2TrFixed + 6 * (size_t)lm + 8 * (size_t)(kMaxPlaneLog + lN) + 8 * (size_t)lN;
     l.o_tr = cv.take<uint64_t>(l.tr_words);
+    // Fiat-Shamir: the layer's drawn challenges (pairs), the Merkle digests, the root, a status word
+    l.o_fsch = cv.take<uint64_t>(2 * ((size_t)log2u(n) + log2u(k) + lm + 4 + 2 * kMaxPlaneLog + 2 * (size_t)lN));
+    l.o_dig0 = cv.take<uint32_t>(8 * witness_leaves(N));
+    l.o_dig1 = cv.take<uint32_t>(8 * ((witness_leaves(N) + 3) / 4));
+    l.o_root = cv.take<uint8_t>(32);
+    l.o_err = cv.take<uint32_t>(1);
     l.bytes = cv.off;
     return l;
 }
@@ -586,11 +599,32 @@ ra_status ra_ctx_create_stream(uint64_t p, const uint64_t *h_challenges, uint64_
     return ctx_create(p, h_challenges, n_challenges, false, 0, hip_stream, out);
 }
 
+ra_status ra_ctx_create_fs(uint64_t p, const uint8_t *domain, void *hip_stream, ra_ctx **out)
+{
+    if (!out || !domain) return RA_E_INVAL;
+    *out = nullptr;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    ra_ctx *c = nullptr;
+    ra_status st = ctx_create(p, nullptr, 0, false, 0, hip_stream, &c);
+    if (st != RA_OK) return st;
+    sha::Transcript t;
+    sha::fs_init(t, domain);
+    if (hipMalloc((void **)&c->d_fs, sizeof(sha::Transcript)) != hipSuccess) st = RA_E_NOMEM;
+    if (st == RA_OK && hipMemcpy(c->d_fs, &t, sizeof(t), hipMemcpyHostToDevice) != hipSuccess) st = RA_E_HIP;
+    if (st != RA_OK) {
+        ra_ctx_destroy(c);
+        return st;
+    }
+    *out = c;
+    return RA_OK;
+}
+
 ra_status ra_ctx_destroy(ra_ctx *c)
 {
     if (!c) return RA_E_INVAL;
     if (c->stream || c->ws || c->d_chal) (void)hipStreamSynchronize(c->stream);
     if (c->d_chal) (void)hipFree(c->d_chal);
+    if (c->d_fs) (void)hipFree(c->d_fs);
     if (c->d_eq) (void)hipFree(c->d_eq);
     if (c->d_acc) (void)hipFree(c->d_acc);
     if (c->d_params) (void)hipFree(c->d_params);
@@ -1286,6 +1320,277 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The non-interactive layer proof (fs.hip): the F_{p^2} protocol with every
+// challenge drawn on the device from the context's Fiat-Shamir transcript.
+// ---------------------------------------------------------------------------
+extern "C" ra_status ra_prove_layer_fs(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const int16_t *d_B, uint32_t n,
+                                       uint32_t m, uint32_t k, int64_t *d_C, int32_t *d_R, uint16_t *d_Rm,
+                                       int32_t *d_Y, int32_t *d_Z, uint64_t *d_bits, uint64_t bits_words,
+                                       const uint8_t *pub_digest, void *d_ws, size_t ws_bytes,
+                                       ra_layer_proof_fp2 *io, uint8_t *root_out)
+{
+    if (!c || !d_A || !d_B || !d_C || !d_R || !d_Rm || !d_Y || !d_Z || !d_bits || !io || !pub_digest)
+        return RA_E_INVAL;
+    if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k)) return RA_E_INVAL;
+    if (a_dtype != RA_I16 && a_dtype != RA_I32) return RA_E_INVAL;
+    if (io->s < 1 || io->relu > 1 || io->round_mode > 1 || io->t < -1) return RA_E_INVAL;
+    if (m > kGemmMaxInner || (uint64_t)n * k > kRangeMaxN || io->s > 16) return RA_E_NOT_IMPLEMENTED;
+    if (!c->d_fs || c->phase != 0) return RA_E_STATE;
+    const uint64_t N = (uint64_t)n * k;
+    if (bits_words < N) return RA_E_BUFSIZE;
+    const int ln = log2u(n), lm = log2u(m), lk = log2u(k), lN = ln + lk, relu = (int)io->relu;
+    if ((lm && !io->mm_evals) || !io->rs_evals || (relu && lN && !io->zc_evals)) return RA_E_INVAL;
+    ra_status st = drain(c);
+    if (st != RA_OK && c->deferred_err == RA_OK) c->deferred_err = st;
+    const Fp2Layout L = fp2_layout(a_dtype == RA_I32, n, m, k);
+    char *ws = nullptr;
+    if ((st = call_ws(c, d_ws, ws_bytes, L.bytes, &ws)) != RA_OK) return st;
+    hipStream_t s = c->stream;
+    auto tab = [&](size_t off, size_t len) {
+        uint64_t *b = (uint64_t *)(ws + off);
+        return F2Tab{b, b + len};
+    };
+    const uint64_t H = N > 1 ? N / 2 : 1;
+    const F2Tab E1 = tab(L.o_e1, n), E2 = tab(L.o_e2, k), Ta = tab(L.o_a, m), Tb = tab(L.o_b, m);
+    const F2Tab EQ = tab(L.o_eq, N), EQr = tab(L.o_eqr, H), EQz = tab(L.o_eqz, H), Bx = tab(L.o_bx, N);
+    const F2Tab Dt = tab(L.o_d, H), St = tab(L.o_s, H), SIG = tab(L.o_sig, 64), ONE = tab(L.o_one, 1);
+    uint64_t *scr = (uint64_t *)(ws + L.o_scr), *part = (uint64_t *)(ws + L.o_part);
+    uint64_t *cpart = (uint64_t *)(ws + L.o_cpart), *cst = (uint64_t *)(ws + L.o_cst);
+    uint64_t *tr = (uint64_t *)(ws + L.o_tr), *Gre = (uint64_t *)(ws + L.o_g), *Gim = Gre + 4096;
+    uint64_t *fsch = (uint64_t *)(ws + L.o_fsch);
+    uint32_t *err = (uint32_t *)(ws + L.o_err);
+    uint8_t *root = (uint8_t *)(ws + L.o_root);
+    const size_t pstride = (size_t)kF2MaxBlocks * 8;
+
+    // the witness: the exact product, t and P, then R, Rm, Y, Z and the bit
+    // table (the F_p claims that pass also forms are not used: its eq tables
+    // are zero here)
+    launch_gemm_mfma(d_A, a_dtype == RA_I32, d_B, d_C, n, m, k, ws + L.o_gemm, s, nullptr, nullptr, false, nullptr);
+    int P = 0, lP = 0, t = io->t;
+    WitParams hp{};
+    if (t >= 0) {
+        if ((st = plane_params((int)io->s, t, relu, &P, &lP)) != RA_OK) return st;
+        hp.status = 0;
+        hp.t = t;
+        hp.P = P;
+        hp.lP = lP;
+        hp.s = (int)io->s;
+        hp.relu = relu;
+        hp.mode = (int)io->round_mode;
+        hp.t_in = t;
+    } else {
+        launch_witness_params(d_C, N, (int)io->s, relu, (int)io->round_mode, -1, (int64_t *)(c->d_wit + kWitMinMax),
+                              c->d_params, s);
+        WitParams got;
+        RA_HIP(hipMemcpyAsync(&got, c->d_params, sizeof(got), hipMemcpyDeviceToHost, s));
+        RA_HIP(hipStreamSynchronize(s));
+        if (got.status != 0) return got.status;
+        t = got.t;
+        P = got.P;
+        lP = got.lP;
+    }
+    launch_fill0(E1.re, n, s);
+    launch_fill0(E2.re, k, s);
+    launch_fill0((uint64_t *)err, 1, s);
+    launch_witness_rescale(d_C, N, lk, E1.re, E2.re, d_R, d_Rm, d_Y, d_Z, d_bits, (uint64_t *)(c->d_wit + kWitClaims),
+                           c->d_params, c->d_claims, nullptr, s, io->t >= 0 ? &hp : nullptr,
+                           (uint32_t *)(c->d_wit + kWitFlags), nullptr);
+    // the witness bound into the transcript before any challenge: its Merkle
+    // root with the layer header and the caller's public digest; r1, r2
+    MerkleArgs ma{};
+    ma.seg[0] = MerkleSeg{(const uint8_t *)d_R, 4 * N, 0};
+    ma.seg[1] = MerkleSeg{(const uint8_t *)d_Rm, 2 * N, 0};
+    ma.seg[2] = MerkleSeg{(const uint8_t *)d_Y, 4 * N, 0};
+    ma.seg[3] = MerkleSeg{(const uint8_t *)d_Z, 4 * N, 0};
+    ma.seg[4] = MerkleSeg{(const uint8_t *)d_bits, 8 * N, 0};
+    launch_merkle_root(ma, (uint32_t *)(ws + L.o_dig0), (uint32_t *)(ws + L.o_dig1), root, s);
+    FsHeader hd{};
+    const uint32_t hw[8] = {n, m, k, io->s, (uint32_t)relu, io->round_mode, (uint32_t)t, (uint32_t)P};
+    for (int i = 0; i < 8; i++)
+        for (int j = 0; j < 4; j++) hd.bytes[4 * i + j] = (uint8_t)(hw[i] >> (8 * j));
+    std::memcpy(hd.bytes + 32, pub_digest, 32);
+    // the layer's challenges (pairs), in the protocol's order
+    uint64_t *r1 = fsch, *r2 = r1 + 2 * ln, *rho = r2 + 2 * lk, *lam = rho + 2 * lm, *tau = lam + 8;
+    uint64_t *sig = tau + 2 * lP, *rho2 = sig + 2 * (lP + lN);
+    launch_fs_header(c->d_fs, hd, root, r1, ln + lk, err, s);
+    launch_f2_eq(r1, ln, E1, s);
+    launch_f2_eq(r2, lk, E2, s);
+
+    // matrix instance: each round folds the previous round's variable, then
+    // evaluates; its values are hashed into the next challenge
+    launch_bind_rows(d_A, a_dtype, n, m, E1.re, scr, Ta.re, s);
+    launch_bind_rows(d_A, a_dtype, n, m, E1.im, scr, Ta.im, s);
+    launch_bind_cols(d_B, RA_I16, m, k, E2.re, Tb.re, s);
+    launch_bind_cols(d_B, RA_I16, m, k, E2.im, Tb.im, s);
+    uint64_t *ev_mm = tr + kF2TrFixed, *ev_rs = ev_mm + 6 * (size_t)lm, *ev_zc = ev_rs + 8 * (size_t)(lP + lN);
+    for (int j = 0; j < lm; j++) {
+        F2FsRoundArgs ra{};
+        ra.kind = F2_MATMUL;
+        ra.fold = j > 0;
+        ra.h = (uint64_t)m >> (j + 1);
+        ra.src[0] = ra.dst[0] = Ta;
+        ra.src[1] = ra.dst[1] = Tb;
+        ra.rho_prev = j > 0 ? rho + 2 * (j - 1) : nullptr;
+        ra.part = part;
+        launch_f2_round_fs(ra, s);
+        launch_fs_round(part, f2_blocks(ra.h), 6, ev_mm + 6 * j, c->d_fs, rho + 2 * j, err, s);
+    }
+    {
+        F2FsFinalArgs fa{};
+        fa.kind = F2_MATMUL;
+        fa.rounds = lm;
+        fa.t[0] = Ta;
+        fa.t[1] = Tb;
+        fa.rho = lm ? rho + 2 * (lm - 1) : nullptr;
+        fa.ev0 = ev_mm;
+        fa.fin = tr;
+        launch_f2_final_fs(fa, s);
+    }
+    // the claims at (r1, r2), then a*, b* and the claims absorbed; lambda,
+    // mu, tau_p drawn
+    launch_f2_outer(E1, E2, lk, N, EQ, s);
+    launch_f2_claims(EQ, d_R, d_Rm, d_Y, d_Z, N, cpart, s);
+    launch_f2_sum8(cpart, f2_blocks(N), tr + 6, s);
+    launch_fs_absorb_draw(c->d_fs, tr + 2, 12, lam, 4 + lP, err, s);
+    // plane rounds: the Gram matrix's two parts (their pass's plane-bound
+    // output is not used: sigma_p does not exist yet), then the rounds, which
+    // draw sigma_p as they go, then Bx with eq(sigma_p, .)
+    launch_fill0(SIG.re, 64, s);
+    launch_f2_eq(lam, 0, ONE, s);
+    const int gt = plane_gram_tiles(lP), gb = plane_gram_blocks(N, lP);
+    uint64_t *gp0 = (uint64_t *)(ws + L.o_gp0), *gp1 = (uint64_t *)(ws + L.o_gp1);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.re, ONE.re, SIG.re, Bx.re, gp0, nullptr, s, SIG.re);
+    launch_f2_gram_sum(gp0, gb, gt, Gre, s);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.im, ONE.re, SIG.re, Bx.im, gp1, nullptr, s, SIG.re);
+    launch_f2_gram_sum(gp1, gb, gt, Gim, s);
+    {
+        F2PlaneArgs pa{};
+        pa.G_re = Gre;
+        pa.G_im = Gim;
+        pa.tau = tau;
+        pa.sig = sig;
+        pa.lam = lam;
+        pa.claims = tr + 6;
+        pa.s = (int)io->s;
+        pa.t = t;
+        pa.relu = relu;
+        pa.P = P;
+        pa.lP = lP;
+        pa.ev = ev_rs;
+        pa.cst = cst;
+        pa.range_sum = tr + 14;
+        pa.fs = c->d_fs;
+        pa.sig_out = sig;
+        pa.err = err;
+        launch_f2_planes(pa, s);
+    }
+    launch_f2_eq(sig, lP, SIG, s);
+    launch_f2_bx(d_bits, N, SIG, P, Bx, s);
+    // rounds over x of the range instance, then the ReLU zero-check
+    for (int j = 0; j < lN; j++) {
+        F2FsRoundArgs ra{};
+        ra.kind = F2_RANGE;
+        ra.fold = j > 0;
+        ra.h = N >> (j + 1);
+        ra.src[0] = j <= 1 ? EQ : EQr;
+        ra.dst[0] = EQr;
+        ra.src[1] = ra.dst[1] = Bx;
+        ra.rho_prev = j > 0 ? sig + 2 * (lP + j - 1) : nullptr;
+        ra.cst = cst;
+        ra.part = part;
+        launch_f2_round_fs(ra, s);
+        launch_fs_round(part, f2_blocks(ra.h), 8, ev_rs + 8 * (size_t)(lP + j), c->d_fs, sig + 2 * (lP + j), err, s);
+    }
+    {
+        F2FsFinalArgs fa{};
+        fa.kind = F2_RANGE;
+        fa.rounds = lN;
+        fa.t[0] = lN >= 2 ? EQr : EQ;
+        fa.t[1] = Bx;
+        fa.rho = lN ? sig + 2 * (lP + lN - 1) : nullptr;
+        fa.fin = tr + 16;
+        launch_f2_final_fs(fa, s);
+    }
+    launch_fs_absorb_draw(c->d_fs, tr + 16, 2, nullptr, 0, err, s);
+    if (relu) {
+        for (int j = 0; j < lN; j++) {
+            F2FsRoundArgs ra{};
+            ra.kind = F2_RELU;
+            ra.fold = j > 0;
+            ra.ints = j <= 1;
+            ra.h = N >> (j + 1);
+            ra.src[0] = j <= 1 ? EQ : EQz;
+            ra.dst[0] = EQz;
+            ra.src[1] = ra.dst[1] = Dt;
+            ra.src[2] = ra.dst[2] = St;
+            ra.R = d_R;
+            ra.Y = d_Y;
+            ra.rho_prev = j > 0 ? rho2 + 2 * (j - 1) : nullptr;
+            ra.part = part;
+            launch_f2_round_fs(ra, s);
+            launch_fs_round(part, f2_blocks(ra.h), 8, ev_zc + 8 * (size_t)j, c->d_fs, rho2 + 2 * j, err, s);
+        }
+        F2FsFinalArgs fa{};
+        fa.kind = F2_RELU;
+        fa.rounds = lN;
+        fa.ints = lN <= 1;
+        fa.t[0] = lN >= 2 ? EQz : EQ;
+        fa.t[1] = Dt;
+        fa.t[2] = St;
+        fa.R = d_R;
+        fa.Y = d_Y;
+        fa.rho = lN ? rho2 + 2 * (lN - 1) : nullptr;
+        fa.fin = tr + 18;
+        launch_f2_final_fs(fa, s);
+        launch_fs_absorb_draw(c->d_fs, tr + 18, 4, nullptr, 0, err, s);
+    }
+    RA_HIP(hipGetLastError());
+    // the transcript, the witness status, the transcript status and the root
+    // into the context's pinned area (nothing else is pending there)
+    const size_t prm_words = (sizeof(WitParams) + 7) / 8;
+    size_t off = 0;
+    if ((st = stage_take(c, L.tr_words + prm_words + 5, &off)) != RA_OK) return st;
+    uint64_t *h = c->h_stage + off;
+    RA_HIP(hipMemcpyAsync(h, tr, L.tr_words * 8, hipMemcpyDeviceToHost, s));
+    RA_HIP(hipMemcpyAsync(h + L.tr_words, c->d_params, sizeof(WitParams), hipMemcpyDeviceToHost, s));
+    RA_HIP(hipMemcpyAsync(h + L.tr_words + prm_words, err, 4, hipMemcpyDeviceToHost, s));
+    RA_HIP(hipMemcpyAsync(h + L.tr_words + prm_words + 1, root, 32, hipMemcpyDeviceToHost, s));
+    RA_HIP(hipStreamSynchronize(s));
+    WitParams prm;
+    std::memcpy(&prm, h + L.tr_words, sizeof(prm));
+    uint32_t e = 0;
+    std::memcpy(&e, h + L.tr_words + prm_words, 4);
+    c->stage_used = 0;
+    if (prm.status != 0) return prm.status;  // a given t that does not hold R
+    if (e) return RA_E_INVAL;                // a transcript message longer than the pending area
+    if (root_out) std::memcpy(root_out, h + L.tr_words + prm_words + 1, 32);
+    auto pr = [&](size_t o) { return ra_fp2{h[o], h[o + 1]}; };
+    io->t = t;
+    io->P = (uint32_t)P;
+    io->log_m = (uint32_t)lm;
+    io->c0 = pr(0);
+    io->a_star = pr(2);
+    io->b_star = pr(4);
+    io->r_claim = pr(6);
+    io->rm_claim = pr(8);
+    io->y_claim = pr(10);
+    io->z_claim = pr(12);
+    io->range_sum = pr(14);
+    io->bits_claim = pr(16);
+    io->r_at = relu ? pr(18) : ra_fp2{0, 0};
+    io->y_at = relu ? pr(20) : ra_fp2{0, 0};
+    io->rounds = (uint32_t)(lP + lN);
+    io->relu_rounds = relu ? (uint32_t)lN : 0;
+    const size_t omm = kF2TrFixed, ors = omm + 6 * (size_t)lm, ozc = ors + 8 * (size_t)(lP + lN);
+    for (int i = 0; i < 3 * lm; i++) io->mm_evals[i] = pr(omm + 2 * i);
+    for (int i = 0; i < 4 * (lP + lN); i++) io->rs_evals[i] = pr(ors + 2 * i);
+    if (relu)
+        for (int i = 0; i < 4 * lN; i++) io->zc_evals[i] = pr(ozc + 2 * i);
+    c->link_ok = false;
+    return RA_OK;
+}
 
 // ---------------------------------------------------------------------------
 // The gather link (link.hip): after a layer's three calls, the claim a* =

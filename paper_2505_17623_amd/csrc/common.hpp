@@ -2,6 +2,8 @@
 // driver of the Range-Arithmetic prover.
 #pragma once
 #include <hip/hip_runtime.h>
+
+#include "sha256.hpp"
 #include <stddef.h>
 #include <stdint.h>
 
@@ -325,6 +327,11 @@ struct F2PlaneArgs {
     uint64_t *ev;                     // lP rounds x 8 words
     uint64_t *cst;                    // out: c_eq, c_w
     uint64_t *range_sum;              // out: the claimed sum
+    // Fiat-Shamir (fs != nullptr): sigma_p is drawn round by round from the
+    // transcript (after each round's values) into sig_out instead of read
+    sha::Transcript *fs = nullptr;
+    uint64_t *sig_out = nullptr;
+    uint32_t *err = nullptr;
 };
 void launch_f2_eq(const uint64_t *z, int v, F2Tab out, hipStream_t st);
 void launch_f2_outer(F2Tab E1, F2Tab E2, int lk, uint64_t N, F2Tab out, hipStream_t st);
@@ -335,6 +342,52 @@ void launch_f2_round(const F2RoundArgs &a, hipStream_t st);
 void launch_f2_finish(const F2FinishArgs &a, hipStream_t st);
 void launch_f2_planes(const F2PlaneArgs &a, hipStream_t st);
 void launch_f2_gram_sum(const uint64_t *gpart, int nblk, int TP, uint64_t *G, hipStream_t st);
+
+// ---- the non-interactive layer proof (fs.hip) ----
+struct MerkleSeg {
+    const uint8_t *p;     // 16-byte aligned
+    uint64_t bytes;
+    uint64_t first_leaf;  // set by launch_merkle_root
+};
+struct MerkleArgs {
+    MerkleSeg seg[5];
+    uint64_t leaves;
+};
+uint64_t merkle_leaves(const MerkleArgs &a);
+// dig0, dig1: merkle_leaves() x 8 words each; root: 32 bytes
+void launch_merkle_root(MerkleArgs a, uint32_t *dig0, uint32_t *dig1, uint8_t *root, hipStream_t st);
+struct FsHeader {
+    uint8_t bytes[64];  // LE32 n, m, k, s, relu, round_mode, t, P, then the 32-byte public digest
+};
+void launch_fs_header(sha::Transcript *fs, const FsHeader &h, const uint8_t *root, uint64_t *out, int ndraw,
+                      uint32_t *err, hipStream_t st);
+void launch_fs_absorb_draw(sha::Transcript *fs, const uint64_t *w, int nw, uint64_t *out, int ndraw, uint32_t *err,
+                           hipStream_t st);
+void launch_fs_round(const uint64_t *part, int nb, int nw, uint64_t *ev, sha::Transcript *fs, uint64_t *out,
+                     uint32_t *err, hipStream_t st);
+// A round whose pass first binds the previous round's variable (fold, tables
+// of 4h entries at src to 2h at dst) and then evaluates on h pairs.
+struct F2FsRoundArgs {
+    int kind, fold, ints;      // ints: the ReLU tables D, S are read from R, Y
+    uint64_t h;
+    F2Tab src[3], dst[3];
+    const int32_t *R, *Y;
+    const uint64_t *rho_prev;  // pair
+    const uint64_t *cst;       // range: c_eq, c_w
+    uint64_t *part;            // f2_blocks(h) x 8 words
+};
+void launch_f2_round_fs(const F2FsRoundArgs &a, hipStream_t st);
+struct F2FsFinalArgs {
+    int kind, rounds, ints;
+    F2Tab t[3];
+    const int32_t *R, *Y;
+    const uint64_t *rho;  // the last challenge (rounds > 0)
+    const uint64_t *ev0;  // the first round's values (matrix c0)
+    uint64_t *fin;
+};
+void launch_f2_final_fs(const F2FsFinalArgs &a, hipStream_t st);
+void launch_f2_bx(const uint64_t *bits, uint64_t N, F2Tab SIG, int P, F2Tab Bx, hipStream_t st);
+void launch_fill0(uint64_t *p, uint64_t n, hipStream_t st);
 
 // ---- the gather link between layers (link.hip) ----
 constexpr int kLinkMaxBlocks = 512;  // blocks of a round launch (partials per round)

@@ -20,6 +20,8 @@
 #include "common.hpp"
 #include "m61.hpp"
 #include "gram_reduce.hpp"
+#include "fs_device.hpp"
+#include "sha256.hpp"
 
 namespace ra {
 
@@ -317,7 +319,9 @@ __global__ __launch_bounds__(256) void k_f2_planes(F2PlaneArgs a)
 {
     constexpr int GS = 65;  // row stride of the staged Gram matrix (odd, so rows start in different banks)
     __shared__ uint64_t g_re[64 * GS], g_im[64 * GS];
-    __shared__ f2 W[64], cpre[32], contrib[4][32], tau[8], sig[8], lam[4], pre[8];
+    __shared__ f2 W[64], cpre[32], contrib[4][32], tau[8], sig[8], lam[4], pre[8], gsh[4];
+    __shared__ uint32_t fsbuf32[kFsLdsBytes / 4];  // the transcript (Fiat-Shamir mode)
+    uint8_t *fsbuf = (uint8_t *)fsbuf32;
     const int tid = threadIdx.x, lP = a.lP, P = a.P;
     for (int e = tid; e < P * P; e += blockDim.x) {
         const int p = e >> lP, q = e & (P - 1);
@@ -326,7 +330,7 @@ __global__ __launch_bounds__(256) void k_f2_planes(F2PlaneArgs a)
     }
     if (tid < lP) {
         tau[tid] = ldp(a.tau + 2 * tid);
-        sig[tid] = ldp(a.sig + 2 * tid);
+        if (!a.fs) sig[tid] = ldp(a.sig + 2 * tid);  // else drawn after each round
     }
     if (tid < 4) lam[tid] = ldp(a.lam + 2 * tid);
     __syncthreads();
@@ -339,13 +343,9 @@ __global__ __launch_bounds__(256) void k_f2_planes(F2PlaneArgs a)
         else if (a.relu && tid < s + 2 * t + 4) w = f2scale(lam[2], 1ull << (tid - s - t - 2));
         W[tid] = tid < P ? w : f2of(0);
     }
-    if (tid == 0) {  // pre[i] = prod over i' < i of eq(tau_i', sigma_i')
-        f2 c = f2of(1);
-        for (int i = 0; i < lP; i++) {
-            pre[i] = c;
-            c = f2mul(c, eq1z(tau[i], sig[i]));
-        }
-        pre[lP] = c;
+    if (tid == 0) {
+        pre[0] = f2of(1);  // pre[i] = prod over i' < i of eq(tau_i', sigma_i'), after round i - 1
+        if (a.fs) fs_pull(a.fs, fsbuf);
     }
     for (int jj = 0; jj < lP; jj++) {
         __syncthreads();
@@ -387,6 +387,23 @@ __global__ __launch_bounds__(256) void k_f2_planes(F2PlaneArgs a)
             f2 g = f2of(0);
             for (int q = 0; q < nq; q++) g = f2add(g, contrib[tid][q]);
             stp(a.ev + 8 * jj + 2 * tid, g);
+            gsh[tid] = g;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            if (a.fs) {  // the round's values absorbed, sigma_jj drawn
+                uint64_t w[8], c[2];
+                for (int q = 0; q < 4; q++) {
+                    w[2 * q] = gsh[q].re;
+                    w[2 * q + 1] = gsh[q].im;
+                }
+                if (!fs_absorb_words_lds(fsbuf, w, 8)) *a.err = 1;
+                fs_draw_lds(fsbuf, c);
+                if (jj == lP - 1) fs_push(a.fs, fsbuf);
+                sig[jj] = f2{c[0], c[1]};
+                stp(a.sig_out + 2 * jj, sig[jj]);
+            }
+            pre[jj + 1] = f2mul(pre[jj], eq1z(tau[jj], sig[jj]));
         }
     }
     __syncthreads();

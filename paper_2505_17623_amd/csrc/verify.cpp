@@ -7,10 +7,13 @@
 // condition 1), the ReLU output link 2 Z = R + Y (Sec. IV), the field guard,
 // and opens the tables handed over in place of commitments by evaluating
 // their multilinear extensions (Eq. (1)) at the challenge points.
+#include <algorithm>
 #include <cstring>
+#include <functional>
 #include <vector>
 
 #include "ra.h"
+#include "sha256.hpp"
 #include "stream.hpp"
 
 namespace {
@@ -422,8 +425,15 @@ G2 eq_points2(const G2 *a, const G2 *b, int v)
     return acc;
 }
 
+// The sizes a layer's challenge source needs (verify_layer_fp2).
+struct LayerShape {
+    int ln, lk, lm, lP, lN, t, P, relu;
+};
+// Fills c with the layer's challenges in protocol order; false: unavailable.
+using DrawFn = std::function<bool(const LayerShape &, std::vector<G2> &)>;
+
 int verify_layer_fp2(const ra_layer_public &L, const ra_layer_tables &T, const ra_layer_proof_fp2 &tr,
-                     const ra_layer_public *prev, ra::ChallengeStream &cs)
+                     const ra_layer_public *prev, const DrawFn &draw)
 {
     const uint32_t n = L.n, m = L.m, k = L.k;
     if (!is_pow2(n) || !is_pow2(m) || !is_pow2(k) || !L.A || !L.B || !L.Z || !T.R || !T.Rm || !T.Y || !T.bits)
@@ -462,10 +472,7 @@ int verify_layer_fp2(const ra_layer_public &L, const ra_layer_tables &T, const r
 
     const uint64_t need = (uint64_t)ln + lk + lm + 4 + lP + (lP + lN) + (relu ? lN : 0);
     std::vector<G2> c(need);
-    for (uint64_t j = 0; j < need; j++) {
-        c[j].re = cs.next();
-        c[j].im = cs.next();
-    }
+    if (!draw(LayerShape{ln, lk, lm, lP, lN, t, P, relu}, c) || c.size() != need) return 13;
     const G2 *r1 = c.data(), *r2 = r1 + ln, *rho = r2 + lk, *lam = rho + lm;
     const G2 mu = lam[3], *tau_p = lam + 4, *sigma = tau_p + lP, *rho2 = sigma + lP + lN;
     std::vector<G2> r12(r1, r1 + ln);
@@ -555,8 +562,150 @@ extern "C" ra_status ra_verify_fp2(uint64_t p, uint64_t seed, uint32_t n_layers,
     *verdict = 0;
     *failed_layer = 0;
     ra::ChallengeStream cs(seed);
+    const DrawFn draw = [&cs](const LayerShape &, std::vector<G2> &c) {
+        for (G2 &x : c) {
+            x.re = cs.next();
+            x.im = cs.next();
+        }
+        return true;
+    };
     for (uint32_t l = 0; l < n_layers; l++) {
-        const int v = verify_layer_fp2(pub[l], tables[l], tr[l], l ? &pub[l - 1] : nullptr, cs);
+        const int v = verify_layer_fp2(pub[l], tables[l], tr[l], l ? &pub[l - 1] : nullptr, draw);
+        if (v) {
+            *verdict = v;
+            *failed_layer = l;
+            return RA_OK;
+        }
+    }
+    return RA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The non-interactive verifier (Fiat-Shamir over F_{p^2}): the challenges are
+// recovered by replaying the prover's transcript (the layer header, the
+// caller's public digest, the Merkle root of the opened tables, then every
+// message in the prover's order), then checked as in ra_verify_fp2.
+// ---------------------------------------------------------------------------
+namespace {
+
+// Merkle root of the witness tables: R (LE32), Rm (LE16), Y (LE32), Z (LE32),
+// the bit words (LE64), each zero-padded to 1 KiB chunks; leaf H(0x00 ||
+// chunk), nodes H(0x01 || 4 digests), root H(0x02 || LE64(leaves) || top).
+void witness_root(const ra_layer_tables &T, const int32_t *Z, uint64_t N, uint8_t out[32])
+{
+    struct Tab {
+        const uint8_t *p;
+        uint64_t bytes;
+    } tabs[5] = {{(const uint8_t *)T.R, 4 * N}, {(const uint8_t *)T.Rm, 2 * N}, {(const uint8_t *)T.Y, 4 * N},
+                 {(const uint8_t *)Z, 4 * N}, {(const uint8_t *)T.bits, 8 * N}};
+    std::vector<uint8_t> dig;
+    for (const Tab &tb : tabs)  // the host is little-endian: the tables' bytes are their LE encodings
+        for (uint64_t off = 0; off < tb.bytes; off += 1024) {
+            sha::Hasher h;
+            h.init();
+            h.byte(0x00);
+            const uint64_t take = std::min<uint64_t>(1024, tb.bytes - off);
+            h.update(tb.p + off, take);
+            for (uint64_t i = take; i < 1024; i++) h.byte(0);
+            uint8_t d[32];
+            h.final(d);
+            dig.insert(dig.end(), d, d + 32);
+        }
+    const uint64_t leaves = dig.size() / 32;
+    uint64_t count = leaves;
+    while (count > 1) {
+        const uint64_t next = (count + 3) / 4;
+        std::vector<uint8_t> up(32 * next);
+        for (uint64_t g = 0; g < next; g++) {
+            sha::Hasher h;
+            h.init();
+            h.byte(0x01);
+            for (uint64_t c = 0; c < 4; c++) {
+                if (4 * g + c < count) h.update(dig.data() + 32 * (4 * g + c), 32);
+                else for (int i = 0; i < 32; i++) h.byte(0);
+            }
+            h.final(up.data() + 32 * g);
+        }
+        dig.swap(up);
+        count = next;
+    }
+    sha::Hasher h;
+    h.init();
+    h.byte(0x02);
+    h.le(leaves, 8);
+    h.update(dig.data(), 32);
+    h.final(out);
+}
+
+bool absorb_f2(sha::Transcript &fs, const ra_fp2 *v, int count)
+{
+    for (int i = 0; i < count; i++) {
+        const uint64_t w[2] = {v[i].re, v[i].im};
+        if (!sha::fs_absorb_words(fs, w, 2)) return false;
+    }
+    return true;
+}
+
+G2 draw2(sha::Transcript &fs)
+{
+    uint64_t w[2];
+    sha::fs_draw(fs, w);
+    return G2{w[0], w[1]};
+}
+
+}  // namespace
+
+extern "C" ra_status ra_verify_fs(uint64_t p, const uint8_t *domain, uint32_t n_layers, const ra_layer_public *pub,
+                                  const ra_layer_tables *tables, const ra_layer_proof_fp2 *tr,
+                                  const uint8_t *pub_digests, int32_t *verdict, uint32_t *failed_layer)
+{
+    if (!verdict || !failed_layer || !domain || (n_layers && (!pub || !tables || !tr || !pub_digests)))
+        return RA_E_INVAL;
+    if (p != kP) return RA_E_UNSUPPORTED_PRIME;
+    *verdict = 0;
+    *failed_layer = 0;
+    sha::Transcript fs;
+    sha::fs_init(fs, domain);
+    for (uint32_t l = 0; l < n_layers; l++) {
+        const ra_layer_public &L = pub[l];
+        const ra_layer_tables &T = tables[l];
+        const ra_layer_proof_fp2 &t = tr[l];
+        const uint8_t *pd = pub_digests + 32 * (size_t)l;
+        const DrawFn replay = [&](const LayerShape &sh, std::vector<G2> &c) {
+            const uint64_t N = (uint64_t)L.n * L.k;
+            uint8_t root[32];
+            witness_root(T, L.Z, N, root);
+            const uint32_t hdr[8] = {L.n, L.m, L.k, L.s, L.relu, L.round_mode, (uint32_t)sh.t, (uint32_t)sh.P};
+            uint8_t hb[32];
+            for (int i = 0; i < 8; i++)
+                for (int j = 0; j < 4; j++) hb[4 * i + j] = (uint8_t)(hdr[i] >> (8 * j));
+            if (!sha::fs_absorb(fs, hb, 32) || !sha::fs_absorb(fs, pd, 32) || !sha::fs_absorb(fs, root, 32))
+                return false;
+            size_t q = 0;
+            for (int i = 0; i < sh.ln + sh.lk; i++) c[q++] = draw2(fs);
+            for (int j = 0; j < sh.lm; j++) {
+                if (!absorb_f2(fs, t.mm_evals + 3 * j, 3)) return false;
+                c[q++] = draw2(fs);
+            }
+            const ra_fp2 sent[6] = {t.a_star, t.b_star, t.r_claim, t.rm_claim, t.y_claim, t.z_claim};
+            if (!absorb_f2(fs, sent, 6)) return false;
+            for (int i = 0; i < 4 + sh.lP; i++) c[q++] = draw2(fs);
+            for (int j = 0; j < sh.lP + sh.lN; j++) {
+                if (!absorb_f2(fs, t.rs_evals + 4 * j, 4)) return false;
+                c[q++] = draw2(fs);
+            }
+            if (!absorb_f2(fs, &t.bits_claim, 1)) return false;
+            if (sh.relu) {
+                for (int j = 0; j < sh.lN; j++) {
+                    if (!absorb_f2(fs, t.zc_evals + 4 * j, 4)) return false;
+                    c[q++] = draw2(fs);
+                }
+                const ra_fp2 fin[2] = {t.r_at, t.y_at};
+                if (!absorb_f2(fs, fin, 2)) return false;
+            }
+            return q == c.size();
+        };
+        const int v = verify_layer_fp2(L, T, t, l ? &pub[l - 1] : nullptr, replay);
         if (v) {
             *verdict = v;
             *failed_layer = l;

@@ -109,6 +109,15 @@ class Workload:
         idx = (np.arange(zr * zc, dtype=np.int64) + 1).reshape(zr, zc)
         return link(idx).reshape(-1) - 1
 
+    def fs_inputs(self):
+        """The caller inputs of a non-interactive proof of this workload: the
+        transcript's 32-byte domain and one 32-byte public digest per layer
+        (synthetic labels; a deployment would bind its model and input)."""
+        import hashlib
+        domain = hashlib.sha256(("range-arithmetic workload " + self.name).encode()).digest()
+        pubs = [hashlib.sha256(f"{self.name} / layer {li}".encode()).digest() for li in range(len(self.layers))]
+        return domain, pubs
+
     def shapes(self):
         out = []
         n = self.X.shape[0]

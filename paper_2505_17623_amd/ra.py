@@ -28,7 +28,8 @@ EXPORTS = ["ra_ctx_create", "ra_ctx_create_stream", "ra_ctx_destroy", "ra_ctx_cu
            "ra_mle_bind", "ra_sumcheck_matmul_prove", "ra_rescale_relu_witness", "ra_range_prove", "ra_verify",
            "ra_verify_stream", "ra_witness_plan", "ra_mle_bind_noalloc", "ra_prove_layer_fp2",
            "ra_workspace_size_fp2", "ra_verify_fp2", "ra_link_prove", "ra_link_workspace_size",
-           "ra_link_gather"]
+           "ra_link_gather", "ra_verify_fs",
+           "ra_ctx_create_fs", "ra_prove_layer_fs"]
 
 
 class RAError(RuntimeError):
@@ -143,12 +144,20 @@ def lib():
         L.ra_link_prove.argtypes = [vp, vp, u64, vp, u64, vp, ctypes.c_size_t, ctypes.POINTER(LinkProof)]
         L.ra_link_workspace_size.argtypes = [u64, ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(ctypes.c_size_t)]
         L.ra_link_gather.argtypes = [vp, vp, u64, vp, u64, vp]
+        L.ra_ctx_create_fs.argtypes = [u64, ctypes.c_char_p, vp, ctypes.POINTER(vp)]
+        L.ra_prove_layer_fs.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                                        vp, vp, vp, vp, vp, vp, u64, ctypes.c_char_p, vp, ctypes.c_size_t,
+                                        ctypes.POINTER(LayerProofFp2), ctypes.c_char_p]
+        L.ra_verify_fs.argtypes = [u64, ctypes.c_char_p, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
+                                   ctypes.POINTER(LayerTables), ctypes.POINTER(LayerProofFp2), ctypes.c_char_p,
+                                   ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
         L.ra_verify_fp2.argtypes = [u64, u64, ctypes.c_uint32, ctypes.POINTER(LayerPublic),
                                     ctypes.POINTER(LayerTables), ctypes.POINTER(LayerProofFp2),
                                     ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_uint32)]
         for f in (L.ra_ctx_create, L.ra_ctx_create_stream, L.ra_workspace_size, L.ra_verify_stream,
                   L.ra_prove_layer_fp2, L.ra_workspace_size_fp2, L.ra_verify_fp2, L.ra_link_prove,
-                  L.ra_link_workspace_size, L.ra_link_gather,
+                  L.ra_link_workspace_size, L.ra_link_gather, L.ra_verify_fs, L.ra_ctx_create_fs,
+                  L.ra_prove_layer_fs,
                   L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
@@ -179,16 +188,21 @@ _DT = {torch.int16: RA_I16, torch.int32: RA_I32, torch.int64: RA_I64}
 
 class Context:
     """A prover context: the challenge stream on the device plus per-layer
-    state.  Give either `seed` (the library draws the stream: ra_ctx_create)
-    or `challenges` (a given array: ra_ctx_create_stream)."""
+    state.  Give `seed` (the library draws the stream: ra_ctx_create),
+    `challenges` (a given array: ra_ctx_create_stream) or `fs_domain` (32
+    bytes: a Fiat-Shamir transcript for non-interactive proofs,
+    ra_ctx_create_fs)."""
 
     def __init__(self, challenges=None, stream: torch.cuda.Stream | None = None, deferred: bool = False,
-                 seed: int | None = None):
-        assert (challenges is None) != (seed is None), "give challenges or seed"
+                 seed: int | None = None, fs_domain: bytes | None = None):
+        assert sum(x is not None for x in (challenges, seed, fs_domain)) == 1, "give challenges, seed or fs_domain"
         self.stream = stream or torch.cuda.current_stream()
         h = ctypes.c_void_p()
         sp = ctypes.c_void_p(self.stream.cuda_stream)
-        if seed is not None:
+        if fs_domain is not None:
+            assert len(fs_domain) == 32
+            _check(lib().ra_ctx_create_fs(P61, bytes(fs_domain), sp, ctypes.byref(h)), "ra_ctx_create_fs")
+        elif seed is not None:
             _check(lib().ra_ctx_create(P61, seed, sp, ctypes.byref(h)), "ra_ctx_create")
         else:
             self._chal, cp = _u64_array(challenges)
@@ -576,9 +590,12 @@ def _fp2_list(arr, count):
 
 
 def prove_layer_fp2(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu: bool, mode: int = 0, t: int = -1,
-                    bufs: dict | None = None, ws: torch.Tensor | None = None):
-    """One layer over F_{p^2} (ra_prove_layer_fp2; waits for its work).
-    Returns the device tensors and the transcript, every element a pair (re, im)."""
+                    bufs: dict | None = None, ws: torch.Tensor | None = None, pub: bytes | None = None):
+    """One layer over F_{p^2} (ra_prove_layer_fp2; waits for its work), or,
+    with pub (the layer's 32-byte public digest) on a Fiat-Shamir context,
+    the non-interactive proof (ra_prove_layer_fs; result["root"] is the
+    witness tables' Merkle root).  Returns the device tensors and the
+    transcript, every element a pair (re, im)."""
     n, m = A.shape
     k = B.shape[1]
     dev = A.device
@@ -596,20 +613,32 @@ def prove_layer_fp2(ctx: Context, A: torch.Tensor, B: torch.Tensor, s: int, relu
     zc = (Fp2 * max(4 * lN, 1))()
     pr = LayerProofFp2(s=s, relu=int(bool(relu)), round_mode=mode, t=t)
     pr.mm_evals, pr.rs_evals, pr.zc_evals = mm, rs, zc
-    _check(lib().ra_prove_layer_fp2(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C), _dptr(R), _dptr(Rm),
-                                    _dptr(Y), _dptr(Z), _dptr(bits), N, *_ws(ws), ctypes.byref(pr)),
-           "ra_prove_layer_fp2")
+    root = None
+    if pub is None:
+        _check(lib().ra_prove_layer_fp2(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C), _dptr(R),
+                                        _dptr(Rm), _dptr(Y), _dptr(Z), _dptr(bits), N, *_ws(ws), ctypes.byref(pr)),
+               "ra_prove_layer_fp2")
+    else:
+        assert len(pub) == 32
+        rb = ctypes.create_string_buffer(32)
+        _check(lib().ra_prove_layer_fs(ctx.h, _dptr(A), _DT[A.dtype], _dptr(B), n, m, k, _dptr(C), _dptr(R),
+                                       _dptr(Rm), _dptr(Y), _dptr(Z), _dptr(bits), N, bytes(pub), *_ws(ws),
+                                       ctypes.byref(pr), rb), "ra_prove_layer_fs")
+        root = rb.raw
     tr = dict(t=int(pr.t), P=int(pr.P), s=s, relu=int(bool(relu)), mode=mode,
               mm_evals=_fp2_list(mm, 3 * pr.log_m), rs_evals=_fp2_list(rs, 4 * pr.rounds),
               zc_evals=_fp2_list(zc, 4 * pr.relu_rounds))
     for key in FP2_SCALARS:
         v = getattr(pr, key)
         tr[key] = (int(v.re), int(v.im))
-    return dict(C=C, R=R, Rm=Rm, Y=Y, Z=Z, bits=bits, transcript=tr)
+    return dict(C=C, R=R, Rm=Rm, Y=Y, Z=Z, bits=bits, transcript=tr, root=root)
 
 
-def prove_network_fp2(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, ws=None):
-    """Every layer of a workload over F_{p^2}, inputs as in prove_network."""
+def prove_network_fp2(ctx: Context, workload, device="cuda", X=None, Bs=None, ts=None, bufs=None, ws=None,
+                      pubs=None):
+    """Every layer of a workload over F_{p^2}, inputs as in prove_network;
+    with pubs (one 32-byte public digest per layer) on a Fiat-Shamir context,
+    the non-interactive proof."""
     if bufs is not None:
         while len(bufs) < len(workload.layers):
             bufs.append({})
@@ -625,16 +654,15 @@ def prove_network_fp2(ctx: Context, workload, device="cuda", X=None, Bs=None, ts
             A = to_device(workload.links[li](Z.cpu().numpy()), device)
         t = -1 if ts is None else int(ts[li])
         res = prove_layer_fp2(ctx, A, Bs[li], layer.s, layer.relu, workload.mode, t,
-                              None if bufs is None else bufs[li], ws)
+                              None if bufs is None else bufs[li], ws, None if pubs is None else pubs[li])
         res["A"] = A
         Z = res["Z"]
         outs.append(res)
     return outs
 
 
-def ra_verify_fp2(seed: int, layers):
-    """Host verifier for layers proven over F_{p^2}; `layers` as for ra_verify
-    with the transcripts of prove_layer_fp2.  Returns (verdict, failed_layer)."""
+def _fp2_layer_structs(layers):
+    """ctypes arrays (public data, tables, transcripts) of layers proven over F_{p^2}."""
     nl = len(layers)
     pubs = (LayerPublic * nl)()
     tabs = (LayerTables * nl)()
@@ -673,8 +701,32 @@ def ra_verify_fp2(seed: int, layers):
         for key in FP2_SCALARS:
             re, im = tr[key]
             setattr(t, key, Fp2(re, im))
+    return pubs, tabs, trs, keep
+
+
+def ra_verify_fp2(seed: int, layers):
+    """Host verifier for layers proven over F_{p^2}; `layers` as for ra_verify
+    with the transcripts of prove_layer_fp2.  Returns (verdict, failed_layer)."""
+    nl = len(layers)
+    pubs, tabs, trs, keep = _fp2_layer_structs(layers)
     verdict = ctypes.c_int32()
     failed = ctypes.c_uint32()
     _check(lib().ra_verify_fp2(P61, int(seed), nl, pubs, tabs, trs, ctypes.byref(verdict), ctypes.byref(failed)),
            "ra_verify_fp2")
+    return int(verdict.value), int(failed.value)
+
+
+def ra_verify_fs(domain: bytes, pub_digests, layers):
+    """Host verifier of non-interactive proofs (Fiat-Shamir over F_{p^2}):
+    domain the transcript's 32 bytes, pub_digests one 32-byte digest per
+    layer, layers as for ra_verify_fp2.  Returns (verdict, failed_layer)."""
+    assert len(domain) == 32 and len(pub_digests) == len(layers)
+    nl = len(layers)
+    pubs, tabs, trs, keep = _fp2_layer_structs(layers)
+    digests = b"".join(bytes(d) for d in pub_digests)
+    assert len(digests) == 32 * nl
+    verdict = ctypes.c_int32()
+    failed = ctypes.c_uint32()
+    _check(lib().ra_verify_fs(P61, bytes(domain), nl, pubs, tabs, trs, digests, ctypes.byref(verdict),
+                              ctypes.byref(failed)), "ra_verify_fs")
     return int(verdict.value), int(failed.value)

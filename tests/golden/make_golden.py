@@ -5,10 +5,14 @@ every output table.  Calls only the oracle and the seeded input generator.
     python tests/golden/make_golden.py [cfg ...]          (default: 1 2 3 4 5)
     python tests/golden/make_golden.py --fp2 [cfg ...]    -> full_fp2_cfg<N>.json
     python tests/golden/make_golden.py --links [cfg ...]  -> full_links_cfg<N>.json
+    python tests/golden/make_golden.py --fs [cfg ...]     -> full_fs_cfg<N>.json
 
 With --fp2 the oracle proves the workload with challenges in F_{p^2} (the
 seed's stream read in pairs); the witness tables are those of the F_p proof,
 so only the transcript words (pairs re, im) and the digests of Z are kept.
+With --fs the oracle proves the workload non-interactively (Fiat-Shamir over
+F_{p^2}, the workload's fs_inputs()): the transcripts, each layer's witness
+root and the digests of Z are kept.
 With --links every gather link of the workload is proven after its layer
 (the later layers then read later challenges): the transcripts, each link's
 words and the digests of Z are kept.
@@ -62,6 +66,28 @@ def main_fp2(cfgs):
               flush=True)
 
 
+def main_fs(cfgs):
+    orc.build(force=False)
+    for cfg in cfgs:
+        wl = inputs.workload(cfg, "full")
+        domain, pubs = wl.fs_inputs()
+        t0 = time.time()
+        res = orc.prove_network_fs(wl, domain, pubs)
+        layers = []
+        for r in res:
+            root = orc.witness_root(r["R"], r["Rm"], r["Y"], r["Z"], orc.pack_words(r["bits"]))
+            layers.append(dict(shape=[r["n"], r["m"], r["k"]], transcript={k: r[k] for k in TRANSCRIPT},
+                               root=root.hex(), digests=dict(Z=digest_i64(r["Z"]))))
+        out = dict(workload=wl.name, config=cfg, field="F_p[i]/(i^2+1)", transform="Fiat-Shamir, SHA-256",
+                   oracle_seconds=round(time.time() - t0, 1), layers=layers,
+                   source="oracle/ra_oracle_fp2.c, oracle/ra_oracle_fs.c via tests/golden/make_golden.py --fs")
+        path = os.path.join(HERE, f"full_fs_cfg{cfg}.json")
+        with open(path, "w") as f:
+            json.dump(out, f, indent=1)
+        print(f"config {cfg} non-interactive: {len(layers)} layers, oracle {out['oracle_seconds']} s -> {path}",
+              flush=True)
+
+
 def main_links(cfgs):
     orc.build(force=False)
     for cfg in cfgs:
@@ -105,6 +131,8 @@ if __name__ == "__main__":
     args = sys.argv[1:]
     if args and args[0] == "--fp2":
         main_fp2([int(a) for a in args[1:]] or [1, 2, 3, 4, 5])
+    elif args and args[0] == "--fs":
+        main_fs([int(a) for a in args[1:]] or [1, 2, 3, 4, 5])
     elif args and args[0] == "--links":
         main_links([int(a) for a in args[1:]] or [4])
     else:

@@ -249,3 +249,61 @@ def test_link_host_side_errors(ra):
     assert L.ra_link_workspace_size(1 << 20, 4, 4, ctypes.byref(sz)) == 0 and sz.value >= 8 << 20
     pr = ra.LinkProof()
     assert L.ra_link_prove(None, None, 4, None, 4, None, 0, ctypes.byref(pr)) == -1
+
+
+def fs_layers(wl, res):
+    from helpers import pack_planes
+    layers = []
+    for li, r in enumerate(res):
+        chained = li > 0 and wl.links[li] is None
+        A = np.ascontiguousarray(r["A"], dtype=np.int32 if chained or np.abs(r["A"]).max() >= 2 ** 15 else np.int16)
+        layers.append(dict(A=A, B=wl.layers[li].B, Z=r["Z"].astype(np.int32), R=r["R"].astype(np.int32),
+                           Rm=r["Rm"].astype(np.uint16), Y=r["Y"].astype(np.int32), bits=pack_planes(r["bits"]),
+                           transcript=r, chained=chained))
+    return layers
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 5])
+def test_library_fs_verifier_on_oracle_proofs(ra, cfg):
+    """ra_verify_fs replays the oracle's non-interactive proofs: accepted;
+    another domain, public digest, round word or witness entry rejected, with
+    the verdict the oracle's own verifier gives."""
+    import hashlib
+    wl = inputs.small(cfg)
+    domain = hashlib.sha256(wl.name.encode()).digest()
+    pubs = [hashlib.sha256(f"{wl.name}/layer {li}".encode()).digest() for li in range(len(wl.layers))]
+    res = orc.prove_network_fs(wl, domain, pubs)
+    layers = fs_layers(wl, res)
+    assert ra.ra_verify_fs(domain, pubs, layers) == (0, 0)
+    assert ra.ra_verify_fs(hashlib.sha256(b"x").digest(), pubs, layers)[0] != 0
+    assert ra.ra_verify_fs(domain, [bytes(32)] + pubs[1:], layers)[0] != 0
+    last = len(layers) - 1
+
+    def both(changed_tr=None, **tables):
+        L = [dict(x) for x in layers]
+        if changed_tr is not None:
+            L[last]["transcript"] = changed_tr
+        L[last].update(tables)
+        got = ra.ra_verify_fs(domain, pubs, L)
+        st = orc.fs_init(domain)
+        v = 0
+        for li, x in enumerate(L):
+            tr = x["transcript"]
+            planes = ra.unpack_bits(x["bits"], tr["P"]).astype(np.int64)
+            v = orc.verify_layer_fs(x["A"], x["B"], x["Z"], tr["s"], tr["relu"], tr["mode"], x["R"],
+                                    x["Rm"], x["Y"], planes, tr, st, pubs[li])
+            if v:
+                break
+        return got, v
+
+    r = res[last]
+    ev = list(r["rs_evals"])
+    ev[3] = ((ev[3][0] + 1) % ra.P61, ev[3][1])
+    (v, li), ov = both(dict(r, rs_evals=ev))
+    assert v != 0 and li == last and v == ov
+    (v, li), ov = both(dict(r, a_star=(r["a_star"][0], (r["a_star"][1] + 5) % ra.P61)))
+    assert v != 0 and li == last and v == ov
+    R = layers[last]["R"].copy()
+    R.flat[0] += 1
+    (v, li), ov = both(R=R)
+    assert v != 0 and li == last and v == ov

@@ -54,8 +54,8 @@ def root_by_definition(R, Rm, Y, Z, words):
     dig = [hashlib.sha256(b"\x00" + data[i:i + 1024]).digest() for i in range(0, len(data), 1024)]
     leaves = len(dig)
     while len(dig) > 1:
-        dig = [hashlib.sha256(b"\x01" + b"".join(dig[i:i + 32]) + bytes(32 * (32 - len(dig[i:i + 32])))).digest()
-               for i in range(0, len(dig), 32)]
+        dig = [hashlib.sha256(b"\x01" + b"".join(dig[i:i + 4]) + bytes(32 * (4 - len(dig[i:i + 4])))).digest()
+               for i in range(0, len(dig), 4)]
     return hashlib.sha256(b"\x02" + leaves.to_bytes(8, "little") + dig[0]).digest()
 
 

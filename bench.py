@@ -155,14 +155,20 @@ def traffic_file(cfg):
     return os.path.join(ROOT, "profiles", f"traffic_config{cfg}.json")
 
 
+# the sources of the kernels a headline step launches (the F_p path) and of
+# their launchers: counters taken on other versions of these are stale
+HEADLINE_SOURCES = ["witness.hip", "gemm.hip", "sumcheck.hip", "planes.hip", "xrounds.hip", "m61.hpp",
+                    "common.hpp", "gram_reduce.hpp", "plane_round.hpp", "xsetup.hpp", "assemble.hpp", "claims.hpp",
+                    "tail.hpp", "rsetup.hpp"]
+
+
 def sources_digest():
-    """SHA-256 over the library sources: counters taken on other sources are stale."""
+    """SHA-256 over the headline path's kernel sources."""
     import hashlib
     h = hashlib.sha256()
-    for d in ("paper_2505_17623_amd/csrc", "include"):
-        for f in sorted(os.listdir(os.path.join(ROOT, d))):
-            with open(os.path.join(ROOT, d, f), "rb") as fh:
-                h.update(f.encode() + fh.read())
+    for f in HEADLINE_SOURCES:
+        with open(os.path.join(ROOT, "paper_2505_17623_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + fh.read())
     return h.hexdigest()
 
 

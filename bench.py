@@ -306,6 +306,9 @@ def main():
     ap.add_argument("--fp2-steps", type=int, default=10,
                     help="after the timed region, time this many steps of the same workload proven with "
                          "challenges in F_{p^2} (reported beside the headline; 0 skips it)")
+    ap.add_argument("--commit-steps", type=int, default=2,
+                    help="then this many steps of Pedersen commitments (secp256k1) to every layer's witness "
+                         "tables R, Rm, Y, Z and the bit words (reported beside the headline; 0 skips it)")
     ap.add_argument("--fs-steps", type=int, default=10,
                     help="then this many steps of the non-interactive proof (Fiat-Shamir over F_{p^2}, the "
                          "transcript hashed on the device; reported beside the headline; 0 skips it)")
@@ -476,6 +479,34 @@ def main():
         del outs3, bufs3, ctx3
         print(f"# non-interactive leg: {ms3:.3f} ms per step", file=sys.stderr, flush=True)
 
+    # commitments to the witness tables of every layer (the tables of the last
+    # headline step, left in `bufs`)
+    com = None
+    if args.commit_steps > 0:
+        import hashlib
+        cctx = ra.Context(seed=wl.challenge_seed)
+        nmax = max(int(b["C"].numel()) for b in bufs)
+        gens = ra.commit_generators(cctx, hashlib.sha256(b"range-arithmetic bench generators").digest(), nmax)
+        tables = []
+        for b in bufs:
+            R, Rm, Y, Z, bits = b["wit"]
+            tables += [(R, None), (Rm, ra.RA_U16), (Y, None), (Z, None), (bits, ra.RA_U64)]
+        for T, d in tables:  # warm up
+            ra.commit(cctx, T, gens, d)
+        torch.cuda.synchronize()
+        c0 = time.perf_counter()
+        for _ in range(args.commit_steps):
+            pts = [ra.commit(cctx, T, gens, d) for T, d in tables]
+        torch.cuda.synchronize()
+        msc = 1e3 * (time.perf_counter() - c0) / args.commit_steps
+        entries = sum(int(T.numel()) for T, _ in tables)
+        com = dict(curve="secp256k1", tables=len(tables), entries_per_step=entries, steps=args.commit_steps,
+                   ms_per_step=round(msc, 3), ms_per_table=round(msc / len(tables), 3),
+                   note="Pedersen vector commitments to the witness tables; not the headline")
+        assert all(len(p) == 64 for p in pts)
+        del gens, cctx
+        print(f"# commitments: {msc:.2f} ms per step ({len(tables)} tables)", file=sys.stderr, flush=True)
+
     if args.copy_calibration:
         src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -499,7 +530,7 @@ def main():
                            shapes=[list(s[:3]) for s in shapes], planes=planes,
                            elements_folded_per_step=el),
                roofline=roofline, cpu_baseline=cpu, kernel_groups=groups, field_fp2=fp2,
-               non_interactive=fsl)
+               non_interactive=fsl, commitments=com)
     print(json.dumps(rec), flush=True)
 
 

@@ -61,7 +61,7 @@ typedef int32_t ra_status;
 #define RA_E_SCRATCH (-10)          /* the call needs more than the fixed scratch of ra_mle_bind_noalloc */
 #define RA_E_NOMEM (-11)            /* device or host allocation failed */
 
-typedef enum { RA_I16 = 1, RA_I32 = 2, RA_I64 = 3, RA_FIELD = 4 } ra_dtype;
+typedef enum { RA_I16 = 1, RA_I32 = 2, RA_I64 = 3, RA_FIELD = 4, RA_U16 = 5, RA_U64 = 6 } ra_dtype;
 
 /* Rounding operator.  RA_ROUND_NEAREST is R(x) = (x + 2^(s-1) - ((x + 2^(s-1))
  * mod 2^s)) / 2^s of Sec. II-A with the floor modulo; the shifted remainder
@@ -326,6 +326,38 @@ ra_status ra_link_workspace_size(uint64_t z_entries, uint32_t n, uint32_t m, siz
  * ra_link_prove refuses the map. */
 ra_status ra_link_gather(ra_ctx *ctx, const int32_t *d_Z, uint64_t z_entries, const int32_t *d_src,
                          uint64_t a_entries, int32_t *d_A);
+
+/* ---- Commitments to the tables: Pedersen vectors on secp256k1 --------------
+ * Sec. II-C commits a vector a by g^a with public generators g of a group in
+ * which discrete logarithms are hard; Sec. IV instantiates the group with
+ * secp256k1 (or BLS12-381).  Here, additively, P = sum_i v_i G_i on
+ * y^2 = x^3 + 7 over F_q, q = 2^256 - 2^32 - 977, for integer tables v.
+ * Generators: G_i = (x, y) for the first counter c = 0, 1, ... with which
+ * x = SHA-256("range-arithmetic generators v1" || domain || LE64(i) ||
+ * LE32(c)) (big-endian, mod q) has x^3 + 7 a square; y is the even root.
+ * A point is returned as 64 big-endian bytes, x then y (the identity as 64
+ * zero bytes).  These commitments are computed and opened here; the
+ * sum-checks of this library run over F_p, p = 2^61 - 1, which is not the
+ * curve's scalar field, so the openings that would replace the opened tables
+ * (Alg. 2, 3) are not built. */
+
+/* Generators first .. first + count - 1 of `domain` (32 host bytes) into
+ * d_gens (device, caller-owned): count x 64 bytes, each x then y as eight
+ * little-endian uint32 limbs (the layout ra_commit reads).  Waits for its
+ * work. */
+ra_status ra_commit_generators(ra_ctx *ctx, const uint8_t *domain, uint64_t first, uint64_t count, void *d_gens);
+/* Workspace of ra_commit for a value type (RA_I16, RA_U16, RA_I32, RA_U64). */
+ra_status ra_commit_workspace_size(ra_dtype dtype, size_t *bytes);
+/* P = sum_{i < n} v_i G_i: d_values n device values of dtype (RA_I16,
+ * RA_U16, RA_I32 or RA_U64: the tables R, Y, Z, Rm, the bit words),
+ * d_gens at least n generators (ra_commit_generators).  out: 64 host bytes.
+ * Waits for its work. */
+ra_status ra_commit(ra_ctx *ctx, const void *d_values, ra_dtype dtype, uint64_t n, const void *d_gens, void *d_ws,
+                    size_t ws_bytes, uint8_t *out);
+/* Host opening check: *ok = 1 if commitment (64 bytes) is sum_i v_i G_i for
+ * the host values and generators (layouts as above), else 0. */
+ra_status ra_commit_open(const void *h_values, ra_dtype dtype, uint64_t n, const void *h_gens,
+                         const uint8_t *commitment, int32_t *ok);
 
 /* ---- The protocol with challenges in the extension field F_{p^2} ----------
  * Sec. II-F asks for a field of more than 128 bits.  Over p = 2^61 - 1 a

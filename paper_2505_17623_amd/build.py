@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libra_mi355x.so")
-SOURCES = ["witness.hip", "gemm.hip", "sumcheck.hip", "planes.hip", "xrounds.hip", "fp2.hip", "link.hip", "fs.hip", "abi.hip", "noalloc.hip", "verify.cpp"]
+SOURCES = ["witness.hip", "gemm.hip", "sumcheck.hip", "planes.hip", "xrounds.hip", "fp2.hip", "link.hip", "fs.hip", "commit.hip", "abi.hip", "noalloc.hip", "verify.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -7,6 +7,7 @@
 #include <new>
 #include <vector>
 
+#include "commit.hpp"
 #include "common.hpp"
 #include "ra.h"
 #include "stream.hpp"
@@ -1693,4 +1694,74 @@ extern "C" ra_status ra_link_prove(ra_ctx *c, const int32_t *d_Z, uint64_t z_ent
         c->link_ok = true;
     }
     return r;
+}
+
+// ---------------------------------------------------------------------------
+// Commitments (commit.hip)
+// ---------------------------------------------------------------------------
+namespace {
+int commit_kind(ra_dtype d)
+{
+    switch (d) {
+    case RA_I16: return 0;
+    case RA_U16: return 1;
+    case RA_I32: return 2;
+    case RA_U64: return 3;
+    default: return -1;
+    }
+}
+}  // namespace
+
+extern "C" ra_status ra_commit_generators(ra_ctx *c, const uint8_t *domain, uint64_t first, uint64_t count,
+                                          void *d_gens)
+{
+    if (!c || !domain || !d_gens) return RA_E_INVAL;
+    if (!count) return RA_OK;
+    ra_status st = drain(c);
+    if (st != RA_OK && c->deferred_err == RA_OK) c->deferred_err = st;
+    char *ws = nullptr;
+    if ((st = call_ws(c, nullptr, 0, 256, &ws)) != RA_OK) return st;
+    hipStream_t s = c->stream;
+    launch_fill0((uint64_t *)ws, 1, s);
+    launch_commit_generators(domain, first, count, (uint32_t *)d_gens, (uint32_t *)ws, s);
+    RA_HIP(hipGetLastError());
+    size_t off = 0;
+    if ((st = stage_take(c, 1, &off)) != RA_OK) return st;
+    RA_HIP(hipMemcpyAsync(c->h_stage + off, ws, 4, hipMemcpyDeviceToHost, s));
+    RA_HIP(hipStreamSynchronize(s));
+    uint32_t err = 0;
+    std::memcpy(&err, c->h_stage + off, 4);
+    c->stage_used = 0;
+    return err ? RA_E_INVAL : RA_OK;  // a counter ran out (probability about 2^-256 per generator)
+}
+
+extern "C" ra_status ra_commit_workspace_size(ra_dtype dtype, size_t *bytes)
+{
+    const int kind = commit_kind(dtype);
+    if (!bytes || kind < 0) return RA_E_INVAL;
+    *bytes = msm_workspace_bytes(kind) + 256;
+    return RA_OK;
+}
+
+extern "C" ra_status ra_commit(ra_ctx *c, const void *d_values, ra_dtype dtype, uint64_t n, const void *d_gens,
+                               void *d_ws, size_t ws_bytes, uint8_t *out)
+{
+    const int kind = commit_kind(dtype);
+    if (!c || (n && (!d_values || !d_gens)) || !out || kind < 0) return RA_E_INVAL;
+    ra_status st = drain(c);
+    if (st != RA_OK && c->deferred_err == RA_OK) c->deferred_err = st;
+    const size_t need = msm_workspace_bytes(kind) + 256;
+    char *ws = nullptr;
+    if ((st = call_ws(c, d_ws, ws_bytes, need, &ws)) != RA_OK) return st;
+    hipStream_t s = c->stream;
+    uint8_t *dout = (uint8_t *)(ws + msm_workspace_bytes(kind));
+    launch_commit(d_values, kind, n, (const uint32_t *)d_gens, ws, dout, s);
+    RA_HIP(hipGetLastError());
+    size_t off = 0;
+    if ((st = stage_take(c, 8, &off)) != RA_OK) return st;
+    RA_HIP(hipMemcpyAsync(c->h_stage + off, dout, 64, hipMemcpyDeviceToHost, s));
+    RA_HIP(hipStreamSynchronize(s));
+    std::memcpy(out, c->h_stage + off, 64);
+    c->stage_used = 0;
+    return RA_OK;
 }

@@ -1,0 +1,24 @@
+// commit.hpp -- launchers of the commitment kernels (commit.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ra {
+
+constexpr int kMsmThreadsPerSlot = 8192;  // threads summing one bit slot's points
+constexpr int kMsmGroup = 16;             // partial sums combined per thread in a reduction step
+
+// Generators first .. first + count - 1 of `domain` (32 bytes), affine, 16
+// little-endian uint32 limbs each (x then y); *err set if a counter runs out.
+void launch_commit_generators(const uint8_t *domain, uint64_t first, uint64_t count, uint32_t *gens, uint32_t *err,
+                              hipStream_t st);
+
+// Scalars: int16, uint16, int32 or uint64 values (kind 0..3).
+int msm_bits(int kind);   // magnitude bits
+int msm_signs(int kind);  // 2 for signed kinds
+size_t msm_workspace_bytes(int kind);
+// sum_i v_i G_i, written as 64 big-endian bytes (x, y; zeros for the identity) to out (device)
+void launch_commit(const void *vals, int kind, uint64_t n, const uint32_t *gens, void *ws, uint8_t *out,
+                   hipStream_t st);
+
+}  // namespace ra

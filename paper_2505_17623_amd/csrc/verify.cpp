@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "ra.h"
+#include "secp256k1.hpp"
 #include "sha256.hpp"
 #include "stream.hpp"
 
@@ -712,5 +713,49 @@ extern "C" ra_status ra_verify_fs(uint64_t p, const uint8_t *domain, uint32_t n_
             return RA_OK;
         }
     }
+    return RA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Opening a commitment on the host: recompute sum_i v_i G_i (double-and-add
+// per value) and compare the affine bytes.
+// ---------------------------------------------------------------------------
+extern "C" ra_status ra_commit_open(const void *h_values, ra_dtype dtype, uint64_t n, const void *h_gens,
+                                    const uint8_t *commitment, int32_t *ok)
+{
+    if (!ok || !commitment || (n && (!h_values || !h_gens))) return RA_E_INVAL;
+    if (dtype != RA_I16 && dtype != RA_U16 && dtype != RA_I32 && dtype != RA_U64) return RA_E_INVAL;
+    const uint32_t *g = (const uint32_t *)h_gens;
+    secp::Jac acc = secp::jac_inf();
+    for (uint64_t i = 0; i < n; i++) {
+        int64_t sv = 0;
+        uint64_t mag = 0;
+        bool neg = false;
+        switch (dtype) {
+        case RA_I16: sv = ((const int16_t *)h_values)[i]; break;
+        case RA_I32: sv = ((const int32_t *)h_values)[i]; break;
+        case RA_U16: mag = ((const uint16_t *)h_values)[i]; break;
+        default: mag = ((const uint64_t *)h_values)[i]; break;
+        }
+        if (dtype == RA_I16 || dtype == RA_I32) {
+            neg = sv < 0;
+            mag = (uint64_t)(neg ? -sv : sv);
+        }
+        if (!mag) continue;
+        secp::Aff G;
+        for (int l = 0; l < 8; l++) {
+            G.x.v[l] = g[16 * i + l];
+            G.y.v[l] = g[16 * i + 8 + l];
+        }
+        secp::Jac term = secp::jac_inf();
+        for (int b = 63; b >= 0; b--) {
+            term = secp::jac_dbl(term);
+            if ((mag >> b) & 1) term = secp::jac_add_aff(term, G);
+        }
+        acc = secp::jac_add(acc, neg ? secp::jac_neg(term) : term);
+    }
+    uint8_t got[64];
+    secp::jac_encode(acc, got);
+    *ok = std::memcmp(got, commitment, 64) == 0 ? 1 : 0;
     return RA_OK;
 }

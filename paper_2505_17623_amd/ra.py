@@ -18,7 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libra_mi355x.so")
 P61 = (1 << 61) - 1
 
-RA_I16, RA_I32, RA_I64, RA_FIELD = 1, 2, 3, 4
+RA_I16, RA_I32, RA_I64, RA_FIELD, RA_U16, RA_U64 = 1, 2, 3, 4, 5, 6
 RA_ROUND_NEAREST, RA_ROUND_FLOOR = 0, 1
 STATUS = {0: "RA_OK", -1: "RA_E_INVAL", -2: "RA_E_UNSUPPORTED_PRIME", -3: "RA_E_FIELD_TOO_SMALL",
           -4: "RA_E_RANGE", -5: "RA_E_SEED", -6: "RA_E_HIP", -7: "RA_E_STATE",
@@ -29,7 +29,8 @@ EXPORTS = ["ra_ctx_create", "ra_ctx_create_stream", "ra_ctx_destroy", "ra_ctx_cu
            "ra_verify_stream", "ra_witness_plan", "ra_mle_bind_noalloc", "ra_prove_layer_fp2",
            "ra_workspace_size_fp2", "ra_verify_fp2", "ra_link_prove", "ra_link_workspace_size",
            "ra_link_gather", "ra_verify_fs",
-           "ra_ctx_create_fs", "ra_prove_layer_fs"]
+           "ra_ctx_create_fs", "ra_prove_layer_fs",
+           "ra_commit_generators", "ra_commit_workspace_size", "ra_commit", "ra_commit_open"]
 
 
 class RAError(RuntimeError):
@@ -145,6 +146,10 @@ def lib():
         L.ra_link_workspace_size.argtypes = [u64, ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(ctypes.c_size_t)]
         L.ra_link_gather.argtypes = [vp, vp, u64, vp, u64, vp]
         L.ra_ctx_create_fs.argtypes = [u64, ctypes.c_char_p, vp, ctypes.POINTER(vp)]
+        L.ra_commit_generators.argtypes = [vp, ctypes.c_char_p, u64, u64, vp]
+        L.ra_commit_workspace_size.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
+        L.ra_commit.argtypes = [vp, vp, ctypes.c_int, u64, vp, vp, ctypes.c_size_t, ctypes.c_char_p]
+        L.ra_commit_open.argtypes = [vp, ctypes.c_int, u64, vp, ctypes.c_char_p, ctypes.POINTER(ctypes.c_int32)]
         L.ra_prove_layer_fs.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                         vp, vp, vp, vp, vp, vp, u64, ctypes.c_char_p, vp, ctypes.c_size_t,
                                         ctypes.POINTER(LayerProofFp2), ctypes.c_char_p]
@@ -157,7 +162,8 @@ def lib():
         for f in (L.ra_ctx_create, L.ra_ctx_create_stream, L.ra_workspace_size, L.ra_verify_stream,
                   L.ra_prove_layer_fp2, L.ra_workspace_size_fp2, L.ra_verify_fp2, L.ra_link_prove,
                   L.ra_link_workspace_size, L.ra_link_gather, L.ra_verify_fs, L.ra_ctx_create_fs,
-                  L.ra_prove_layer_fs,
+                  L.ra_prove_layer_fs, L.ra_commit_generators, L.ra_commit_workspace_size, L.ra_commit,
+                  L.ra_commit_open,
                   L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
@@ -730,3 +736,50 @@ def ra_verify_fs(domain: bytes, pub_digests, layers):
     _check(lib().ra_verify_fs(P61, bytes(domain), nl, pubs, tabs, trs, digests, ctypes.byref(verdict),
                               ctypes.byref(failed)), "ra_verify_fs")
     return int(verdict.value), int(failed.value)
+
+
+# --- Pedersen vector commitments on secp256k1 ---------------------------------
+_CDT = {torch.int16: RA_I16, torch.int32: RA_I32}
+_NDT = {np.dtype(np.int16): RA_I16, np.dtype(np.uint16): RA_U16, np.dtype(np.int32): RA_I32,
+        np.dtype(np.uint64): RA_U64}
+
+
+def commit_generators(ctx: Context, domain: bytes, count: int, first: int = 0, out: torch.Tensor | None = None):
+    """Generators first .. first + count - 1 (ra_commit_generators): a device
+    uint32 tensor of count x 16 limbs (x then y, little-endian)."""
+    assert len(domain) == 32
+    if out is None:
+        out = torch.empty((count, 16), dtype=torch.int32, device="cuda")
+    _check(lib().ra_commit_generators(ctx.h, bytes(domain), first, count, _dptr(out)), "ra_commit_generators")
+    return out
+
+
+def commit(ctx: Context, values: torch.Tensor, gens: torch.Tensor, dtype: int | None = None,
+           ws: torch.Tensor | None = None) -> bytes:
+    """sum_i values[i] G_i as 64 big-endian bytes (ra_commit).  values: an
+    int16 / int32 device tensor, or another 2- or 8-byte tensor with dtype
+    RA_U16 / RA_U64 given."""
+    d = dtype if dtype is not None else _CDT[values.dtype]
+    out = ctypes.create_string_buffer(64)
+    _check(lib().ra_commit(ctx.h, _dptr(values), d, values.numel(), _dptr(gens), *_ws(ws), out), "ra_commit")
+    return out.raw
+
+
+def commit_open(values: np.ndarray, gens_limbs: np.ndarray, commitment: bytes) -> bool:
+    """Host opening check (ra_commit_open) of a commitment to host values."""
+    v = np.ascontiguousarray(values)
+    g = np.ascontiguousarray(gens_limbs, dtype=np.uint32)
+    ok = ctypes.c_int32()
+    _check(lib().ra_commit_open(v.ctypes.data, _NDT[v.dtype], v.size, g.ctypes.data, bytes(commitment),
+                                ctypes.byref(ok)), "ra_commit_open")
+    return bool(ok.value)
+
+
+def point_limbs(points) -> np.ndarray:
+    """Affine points (x, y) as the generator layout: 16 little-endian uint32 limbs each."""
+    out = np.zeros((len(points), 16), dtype=np.uint32)
+    for i, (x, y) in enumerate(points):
+        for l in range(8):
+            out[i, l] = (x >> (32 * l)) & 0xFFFFFFFF
+            out[i, 8 + l] = (y >> (32 * l)) & 0xFFFFFFFF
+    return out

@@ -307,3 +307,45 @@ def test_library_fs_verifier_on_oracle_proofs(ra, cfg):
     R.flat[0] += 1
     (v, li), ov = both(R=R)
     assert v != 0 and li == last and v == ov
+
+
+@pytest.mark.parametrize("dtype", [np.int16, np.uint16, np.int32, np.uint64])
+def test_library_commitment_opening_matches_oracle(ra, dtype):
+    """ra_commit_open (the library's secp256k1 arithmetic, run on the host)
+    accepts the oracle's commitment to the same values and generators and
+    rejects another value vector or another point."""
+    import hashlib
+    from oracle import ec_oracle as ec
+    domain = hashlib.sha256(b"commit abi").digest()
+    gens = ec.generators(domain, 12)
+    limbs = ra.point_limbs(gens)
+    rng = np.random.default_rng(4)
+    info = np.iinfo(dtype)
+    v = rng.integers(info.min, info.max, size=12, dtype=dtype, endpoint=True)
+    v[0] = info.min
+    v[1] = info.max
+    v[2] = 0
+    P = ec.encode(ec.commit([int(x) for x in v], gens))
+    assert ra.commit_open(v, limbs, P)
+    w = v.copy()
+    w[5] = w[5] ^ 1
+    assert not ra.commit_open(w, limbs, P)
+    assert not ra.commit_open(v, limbs, ec.encode(ec.add(ec.decode(P), gens[0])))
+    assert ra.commit_open(np.zeros(12, dtype=dtype), limbs, bytes(64))
+
+
+def test_commitment_field_product_top_limb(ra):
+    """A product whose high half is within 2^-22 of 2^256 leaves more than 32
+    bits above 2^256 after the first reduction: doubling the curve point with
+    x = q - 3 squares q - 3, which does.  The host opening (the same limb code
+    as the device) must agree with the oracle there."""
+    from oracle import ec_oracle as ec
+    x = ec.Q - 3
+    rhs = (pow(x, 3, ec.Q) + 7) % ec.Q
+    y = pow(rhs, (ec.Q + 1) // 4, ec.Q)
+    P = (x, y)
+    assert ec.on_curve(P)
+    limbs = ra.point_limbs([P, ec.G])
+    for vals in ([2, 0], [3, 0], [-5, 7], [2 ** 31 - 1, -(2 ** 31)]):
+        want = ec.encode(ec.commit(vals, [P, ec.G]))
+        assert ra.commit_open(np.array(vals, dtype=np.int32), limbs, want), vals

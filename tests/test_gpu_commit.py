@@ -1,0 +1,116 @@
+"""Pedersen vector commitments on the GPU (ra_commit_generators, ra_commit)
+against the oracle (oracle/ec_oracle.py), through the C ABI: the generators
+limb for limb, commitments byte for byte for every value type and for sizes
+from one value to full-layer tables (the latter on sparse vectors the oracle
+computes, and by homomorphism on dense ones), and the tables of a proven
+layer."""
+import hashlib
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ec_oracle as ec
+from paper_2505_17623_amd import inputs
+
+pytestmark = pytest.mark.gpu
+DOMAIN = hashlib.sha256(b"range-arithmetic commitment tests").digest()
+
+
+@pytest.fixture(scope="module")
+def ra():
+    from paper_2505_17623_amd import ra as ra_mod
+    ra_mod.lib()
+    assert torch.cuda.is_available()
+    return ra_mod
+
+
+@pytest.fixture(scope="module")
+def ctx(ra):
+    return ra.Context(seed=1)
+
+
+def test_generators_match_oracle(ra, ctx):
+    g = ra.commit_generators(ctx, DOMAIN, 64).cpu().numpy().view(np.uint32)
+    assert np.array_equal(g, ra.point_limbs(ec.generators(DOMAIN, 64)))
+    first = (1 << 21) - 3
+    g2 = ra.commit_generators(ctx, DOMAIN, 6, first=first).cpu().numpy().view(np.uint32)
+    assert np.array_equal(g2, ra.point_limbs([ec.generator(DOMAIN, first + i) for i in range(6)]))
+
+
+@pytest.fixture(scope="module")
+def gens_small(ra, ctx):
+    return ra.commit_generators(ctx, DOMAIN, 4096), ec.generators(DOMAIN, 4096)
+
+
+DTYPES = [(np.int16, None), (np.uint16, "RA_U16"), (np.int32, None), (np.uint64, "RA_U64")]
+
+
+@pytest.mark.parametrize("n", [1, 7, 256, 3001])
+@pytest.mark.parametrize("dt,code", DTYPES)
+def test_commit_matches_oracle(ra, ctx, gens_small, n, dt, code):
+    dev_gens, gens = gens_small
+    rng = np.random.default_rng(n + np.dtype(dt).itemsize)
+    info = np.iinfo(dt)
+    v = rng.integers(info.min, info.max, size=n, dtype=dt, endpoint=True)
+    v[: min(n, 3)] = [info.min, info.max, 0][: min(n, 3)]
+    if n > 16:
+        v[rng.random(n) < 0.3] = 0
+    t = torch.from_numpy(v.view(np.int16 if dt == np.uint16 else (np.int64 if dt == np.uint64 else dt))).cuda()
+    got = ra.commit(ctx, t, dev_gens, getattr(ra, code) if code else None)
+    want = ec.encode(ec.commit([int(x) for x in v], gens[:n]))
+    assert got == want
+    assert ra.commit_open(v, ra.point_limbs(gens[:n]), got)
+
+
+def test_commit_zero_and_empty(ra, ctx, gens_small):
+    dev_gens, _ = gens_small
+    assert ra.commit(ctx, torch.zeros(100, dtype=torch.int32).cuda(), dev_gens) == bytes(64)
+    e = torch.zeros(1, dtype=torch.int32).cuda()
+    assert ra.commit(ctx, e[:0], dev_gens) == bytes(64)
+
+
+def test_commit_full_layer(ra, ctx):
+    """2^21 values (the tables of one 512 x 4096 output layer): sparse vectors
+    against the oracle at their positions, and a + b = (a) + (b) on dense ones."""
+    n = 1 << 21
+    gens = ra.commit_generators(ctx, DOMAIN, n)
+    rng = np.random.default_rng(21)
+    pos = np.sort(rng.choice(n, size=40, replace=False))
+    v = np.zeros(n, dtype=np.int32)
+    v[pos] = rng.integers(-(2 ** 31), 2 ** 31, size=40)
+    got = ra.commit(ctx, torch.from_numpy(v).cuda(), gens)
+    want = ec.encode(ec.commit([int(v[i]) for i in pos], [ec.generator(DOMAIN, int(i)) for i in pos]))
+    assert got == want
+    a = rng.integers(-(2 ** 30), 2 ** 30, size=n).astype(np.int32)
+    b = rng.integers(-(2 ** 30), 2 ** 30, size=n).astype(np.int32)
+    ca = ec.decode(ra.commit(ctx, torch.from_numpy(a).cuda(), gens))
+    cb = ec.decode(ra.commit(ctx, torch.from_numpy(b).cuda(), gens))
+    cab = ec.decode(ra.commit(ctx, torch.from_numpy(a + b).cuda(), gens))
+    assert ec.on_curve(ca) and ec.on_curve(cb)
+    assert ec.add(ca, cb) == cab
+    # a full-size u64 table of words (the bit table's layout)
+    w = rng.integers(0, 2 ** 63, size=n, dtype=np.uint64)
+    cw = ec.decode(ra.commit(ctx, torch.from_numpy(w.view(np.int64)).cuda(), gens, ra.RA_U64))
+    w2 = w.copy()
+    w2[pos[:3]] += np.uint64(1)
+    cw2 = ec.decode(ra.commit(ctx, torch.from_numpy(w2.view(np.int64)).cuda(), gens, ra.RA_U64))
+    assert ec.add(cw, ec.commit([1, 1, 1], [ec.generator(DOMAIN, int(i)) for i in pos[:3]])) == cw2
+
+
+def test_commit_layer_tables(ra, ctx):
+    """The witness tables of a proven layer, committed on the GPU, against
+    the oracle and the host opening."""
+    wl = inputs.small(1)
+    got = ra.prove_network(ra.Context(wl.challenges), wl)[0]
+    N = got["R"].numel()
+    dev_gens = ra.commit_generators(ctx, DOMAIN, N)
+    gens = ec.generators(DOMAIN, N)
+    limbs = ra.point_limbs(gens)
+    for name, code in (("R", None), ("Y", None), ("Z", None), ("Rm", "RA_U16"), ("bits", "RA_U64")):
+        t = got[name].reshape(-1)
+        P = ra.commit(ctx, t, dev_gens, getattr(ra, code) if code else None)
+        host = t.cpu().numpy()
+        host = host.view(np.uint16) if name == "Rm" else (host.view(np.uint64) if name == "bits" else host)
+        assert P == ec.encode(ec.commit([int(x) for x in host], gens)), name
+        assert ra.commit_open(host, limbs, P), name

@@ -32,9 +32,11 @@ constexpr int kLimbs = 8;    // balanced base-256 digits of a field element
 // Block layout of the Gram pass: sixteen waves with two roles, working on
 // slabs of kSlab outputs through a double-buffered LDS area.
 //   producers (waves 0-7, one output per thread): EQ(x), Bx and the digits
-//     of EQ(x); the wave's 64 bit words transposed into plane-major order (a
-//     64 x 64 bit transpose) and stored as bytes 0x00 / 0xFF, rows padded so
-//     the matrix-core fragment reads are free of bank conflicts;
+//     of EQ(x); the bit words turned plane-major: in each group of eight
+//     lanes (outputs) every byte's 8 x 8 bit block is transposed across the
+//     lanes, so a lane holds one plane's bits for eight outputs per byte,
+//     stored as bytes 0x00 / 0xFF in rows padded so that the matrix-core
+//     fragment reads are free of bank conflicts;
 //   consumers (waves 8-15, two per SIMD): wave c accumulates digit c for
 //     every tile pair over the slab's K-steps on the matrix cores.
 // While the consumers stream slab i the producers build slab i + 1; one
@@ -50,23 +52,29 @@ template <int TP> struct GramShape {
     static constexpr int kDigitsPerWave = kLimbs / kConsumers;  // 1
 };
 
-// 64 x 64 bit transpose across a wave: lane i holds row i (bit j = entry
-// (i, j)); afterwards lane j holds column j (bit i = entry (i, j)).  Six
-// butterfly stages, each swapping the off-diagonal j x j blocks of every
-// 2j x 2j block with the partner lane i ^ j.
-__device__ __forceinline__ uint64_t wave_transpose64(uint64_t a)
+// 8 x 8 bit transposes across each group of eight lanes, one per byte of a
+// 32-bit word: lane 8 g + i holds row i of every byte's block (bit k of byte
+// b = entry (i, k)) and ends with column i (bit k of byte b = entry (k, i)).
+// Three butterfly stages, each swapping the off-diagonal j x j blocks of
+// every 2j x 2j block with the partner lane i ^ j, taken by DPP moves:
+// xor 1 and xor 2 are quad permutations, xor 4 a half-row mirror followed by
+// a quad reversal (lane i -> 7 - i -> 7 - (i ^ 3) = i ^ 4).
+__device__ __forceinline__ uint32_t dpp_xor1(uint32_t v) { return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false); }
+__device__ __forceinline__ uint32_t dpp_xor2(uint32_t v) { return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false); }
+__device__ __forceinline__ uint32_t dpp_xor4(uint32_t v)
+{
+    return __builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false), 0x1B, 0xF, 0xF, false);
+}
+__device__ __forceinline__ uint32_t butterfly(uint32_t a, uint32_t b, bool upper, int j, uint32_t m)
+{
+    return upper ? ((a & ~m) | ((b & ~m) >> j)) : ((a & m) | ((b & m) << j));
+}
+__device__ __forceinline__ uint32_t byte_blocks_transpose(uint32_t a)
 {
     const int lane = threadIdx.x & 63;
-    const uint64_t masks[6] = {0x00000000FFFFFFFFull, 0x0000FFFF0000FFFFull, 0x00FF00FF00FF00FFull,
-                               0x0F0F0F0F0F0F0F0Full, 0x3333333333333333ull, 0x5555555555555555ull};
-#pragma unroll
-    for (int st = 0; st < 6; st++) {
-        const int j = 32 >> st;
-        const uint64_t m = masks[st];
-        const uint64_t b = __shfl_xor(a, j, 64);
-        a = (lane & j) ? ((a & ~m) | ((b & ~m) >> j)) : ((a & m) | ((b & m) << j));
-    }
-    return a;
+    a = butterfly(a, dpp_xor4(a), lane & 4, 4, 0x0F0F0F0Fu);
+    a = butterfly(a, dpp_xor2(a), lane & 2, 2, 0x33333333u);
+    return butterfly(a, dpp_xor1(a), lane & 1, 1, 0x55555555u);
 }
 
 // Balanced base-256 digits of e < 2^62: e = sum_t 256^t d_t, d_t in [-128, 128).
@@ -173,16 +181,13 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
                 const uint64_t db = balanced_digit_bytes(eqx);
 #pragma unroll
                 for (int t = 0; t < kLimbs; t++) s_d[buf][t][tid] = (int8_t)(db >> (8 * t));
-                const uint64_t pwt = wave_transpose64(w);  // lane q: plane q over the wave's 64 outputs
-                if (lane < NPL) {
-                    int8_t *row = s_u + buf * kPlaneBytes + lane * kRow + (tid & ~63);
+                // lane 8 g + i: byte b = plane 8 b + i over outputs 8 g .. 8 g + 7
+                // of the wave, stored as eight 0x00 / 0xFF bytes in that plane's row
+                const uint32_t lo = byte_blocks_transpose((uint32_t)w), hi = byte_blocks_transpose((uint32_t)(w >> 32));
+                int8_t *col = s_u + buf * kPlaneBytes + (lane & 7) * kRow + (tid & ~63) + 8 * (lane >> 3);
 #pragma unroll
-                    for (int c = 0; c < 4; c++) {
-                        const uint64_t e0 = s_exp[(pwt >> (16 * c)) & 255], e1 = s_exp[(pwt >> (16 * c + 8)) & 255];
-                        *(v4i *)(row + 16 * c) = v4i{(int)(uint32_t)e0, (int)(uint32_t)(e0 >> 32), (int)(uint32_t)e1,
-                                                     (int)(uint32_t)(e1 >> 32)};
-                    }
-                }
+                for (int b = 0; b < NPL / 8; b++)
+                    *(uint64_t *)(col + 8 * b * kRow) = s_exp[((b < 4 ? lo : hi) >> (8 * (b & 3))) & 255];
             }
             __syncthreads();
         }

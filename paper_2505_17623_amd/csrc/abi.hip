@@ -439,7 +439,7 @@ RangeLayout range_layout(uint64_t N, int lP, int relu)
     l.o_kz = cv.take<uint64_t>(lN + 1);
     l.o_wsh = cv.take<uint64_t>(1ull << l.Bp);
     l.o_part = cv.take<uint64_t>((size_t)nslots * kPartStride);
-    l.o_gp = cv.take<uint64_t>((size_t)l.gblocks * l.gtiles * 1024);
+    l.o_gp = cv.take<uint64_t>((size_t)l.gblocks * l.gtiles * kGramTileWords);
     l.o_gs = cv.take<uint64_t>(64 * 64);
     l.bytes = cv.off;
     return l;
@@ -481,8 +481,8 @@ Fp2Layout fp2_layout(bool a_i32, uint32_t n, uint32_t m, uint32_t k)
     l.o_s = cv.take<uint64_t>(2 * H);
     l.o_sig = cv.take<uint64_t>(2 * 64);
     l.o_one = cv.take<uint64_t>(2);
-    l.o_gp0 = cv.take<uint64_t>((size_t)gb * gt * 1024);
-    l.o_gp1 = cv.take<uint64_t>((size_t)gb * gt * 1024);
+    l.o_gp0 = cv.take<uint64_t>((size_t)gb * gt * kGramTileWords);
+    l.o_gp1 = cv.take<uint64_t>((size_t)gb * gt * kGramTileWords);
     l.o_g = cv.take<uint64_t>(2 * 4096);
     l.o_part = cv.take<uint64_t>((size_t)(lm + 2 * lN + 1) * kF2MaxBlocks * 8);
     l.o_cpart = cv.take<uint64_t>((size_t)kF2MaxBlocks * 8);
@@ -1003,7 +1003,7 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const bool riding = reg > 0 && x_setup_count(xs) <= plane_gram_set_up_threads(N, lP);
     const RangeConsts rc{lam, c->d_params, c->d_claims, lP, cst, tr + RS, c->pend_claims};
     c->pend_claims.nblk = 0;  // taken by this call's launches
-    const RangeRiders riders{gpart, gblocks, gtiles, gtiles * 64, gsum, rc};
+    const RangeRiders riders{gpart, gblocks, gtiles, gram_reduce_groups(gtiles), gsum, rc};
     {   // plane rounds: Gram matrix on the matrix cores, Bx per output
         Timed tm(c, G_RANGE_PLANE);
         launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, sigma, Bx, gpart, riding ? &xs : nullptr, s);

@@ -253,11 +253,11 @@ struct XJobs {
 int xround_units(uint64_t sub, bool relu);  // partial-sum producers of a register pass
 // Range-call work that rides in the first register pass's launch, after its
 // jobs: nred workgroups sum the Gram pass's partial tiles (gpart, nblk
-// blocks, TP tile pairs) into gsum, one writes the constant block (rc), and
+// blocks, `tiles` 16 x 16 tiles) into gsum, one writes the constant block (rc), and
 // with a deferred witness step (rc.cj.nblk > 0) one more sums its claims.
 struct RangeRiders {
     const uint64_t *gpart;
-    int nblk, TP, nred;
+    int nblk, tiles, nred;
     uint64_t *gsum;
     RangeConsts rc;
 };
@@ -415,12 +415,17 @@ void launch_link(const LinkArgs &a, hipStream_t st);
 void launch_link_gather(const int32_t *Z, uint64_t nz, const int32_t *src, uint64_t na, int32_t *A, hipStream_t st);
 
 // ---- launchers (planes.hip) ----
-int plane_gram_tiles(int lP);                 // 32x32 tile pairs of the Gram matrix (1 or 3)
-int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * 1024 words)
+// The Gram pass works on 16 x 16 tiles of G on and above the diagonal: 3 for
+// up to 32 planes, 10 for 64; each block of the pass writes kGramTileWords
+// words per tile, and the reduction takes 16 entries per workgroup.
+constexpr int kGramTileWords = 256;
+int plane_gram_tiles(int lP);                 // tiles of the Gram matrix (3 or 10)
+int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * kGramTileWords words)
+inline int gram_reduce_groups(int tiles) { return tiles * kGramTileWords / 16; }
 // threads of the Gram pass that can run the set-up of the rounds over x
 int plane_gram_set_up_threads(uint64_t N, int lP);
-// Bx per x and the blocks' partial Gram tiles (plane_gram_blocks x tiles x 1024
-// words); sig: sigma_p (lP words).  With xs (x_setup_count(*xs) at most
+// Bx per x and the blocks' partial Gram tiles (plane_gram_blocks x tiles x
+// kGramTileWords words); sig: sigma_p (lP words).  With xs (x_setup_count(*xs) at most
 // plane_gram_set_up_threads), the pass also runs the set-up of the rounds
 // over x, which depends on challenges only.
 // eqs (optional): the P values eq(sigma_p, q) given instead of computed from sig.

@@ -433,16 +433,16 @@ void launch_f2_planes(const F2PlaneArgs &a, hipStream_t st)
 }
 
 // The Gram matrix from the partial tiles of one Gram pass.
-__global__ __launch_bounds__(256) void k_f2_gram_sum(const uint64_t *__restrict__ gpart, int nblk, int TP,
+__global__ __launch_bounds__(256) void k_f2_gram_sum(const uint64_t *__restrict__ gpart, int nblk, int tiles,
                                                      uint64_t *__restrict__ G)
 {
     __shared__ uint64_t red[kGramReduceLdsWords];
-    gram_reduce_block(gpart, nblk, TP, G, blockIdx.x, red);
+    gram_reduce_block(gpart, nblk, tiles, G, blockIdx.x, red);
 }
 
-void launch_f2_gram_sum(const uint64_t *gpart, int nblk, int TP, uint64_t *G, hipStream_t st)
+void launch_f2_gram_sum(const uint64_t *gpart, int nblk, int tiles, uint64_t *G, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_f2_gram_sum, dim3(TP * 64), dim3(kThreads), 0, st, gpart, nblk, TP, G);
+    hipLaunchKernelGGL(k_f2_gram_sum, dim3(gram_reduce_groups(tiles)), dim3(kThreads), 0, st, gpart, nblk, tiles, G);
 }
 
 }  // namespace ra

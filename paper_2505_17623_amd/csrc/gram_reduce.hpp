@@ -8,23 +8,32 @@
 
 namespace ra {
 
-// Output fragment of v_mfma_i32_32x32x32_i8: lane l, register r holds
-// row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
-__host__ __device__ constexpr int frag_row(int l, int r) { return 8 * (r / 4) + 4 * (l / 32) + (r % 4); }
+// Output fragment of v_mfma_i32_16x16x64_i8: lane l, register r holds
+// row 4 (l / 16) + r, column l % 16 of the 16 x 16 tile.
+__host__ __device__ constexpr int frag_row(int l, int r) { return 4 * (l / 16) + r; }
 
-// Tile pairs of the symmetric 64 x 64 Gram matrix: (0,0), (0,1), (1,1).
-__device__ __forceinline__ int tile_row(int tp, int TP) { return TP == 1 ? 0 : (tp == 2 ? 1 : 0); }
-__device__ __forceinline__ int tile_col(int tp, int TP) { return TP == 1 ? 0 : (tp == 0 ? 0 : 1); }
+// The 16 x 16 tiles on and above the diagonal of the symmetric Gram matrix,
+// over nb blocks of sixteen planes (nb (nb + 1) / 2 tiles): tile t covers
+// blocks (I, J), I <= J, in the order (0,0), (0,1), .., (0,nb-1), (1,1), ..
+__device__ __forceinline__ void tile_blocks(int t, int nb, int &I, int &J)
+{
+    I = 0;
+    while (t >= nb - I) {
+        t -= nb - I;
+        I++;
+    }
+    J = I + t;
+}
 
 // Workgroup blk (256 threads) of the reduction: 16 entries of G, sixteen
 // lanes per entry (lane group g sums the partial tiles of blocks g, g + 16,
 // ...), then LDS; G[q][q'] is written in both triangles.
 constexpr int kGramReduceLdsWords = 16 * 17;
-__device__ __forceinline__ void gram_reduce_block(const uint64_t *__restrict__ gpart, int nblk, int TP,
+__device__ __forceinline__ void gram_reduce_block(const uint64_t *__restrict__ gpart, int nblk, int tiles,
                                                   uint64_t *__restrict__ G, int blk, uint64_t *lds)
 {
     uint64_t(*red)[17] = (uint64_t(*)[17])lds;
-    const int tid = threadIdx.x, el = tid & 15, g = tid >> 4, entries = TP * 1024;
+    const int tid = threadIdx.x, el = tid & 15, g = tid >> 4, entries = tiles * kGramTileWords;
     const int e = blk * 16 + el;
     uint64_t a = 0;
     int b = g;
@@ -41,8 +50,10 @@ __device__ __forceinline__ void gram_reduce_block(const uint64_t *__restrict__ g
 #pragma unroll
     for (int q = 0; q < 16; q += 4) v = m61::fold(v + red[q][el] + red[q + 1][el] + red[q + 2][el] + red[q + 3][el]);
     v = m61::canon(v);
-    const int tp = e >> 10, r = (e & 1023) >> 6, l = e & 63;
-    const int q = 32 * tile_row(tp, TP) + frag_row(l, r), q2 = 32 * tile_col(tp, TP) + (l & 31);
+    const int t = e / kGramTileWords, r = (e % kGramTileWords) >> 6, l = e & 63;
+    int I, J;
+    tile_blocks(t, tiles == 3 ? 2 : 4, I, J);  // 3 tiles: 32 planes; 10: 64
+    const int q = 16 * I + frag_row(l, r), q2 = 16 * J + (l & 15);
     G[q * 64 + q2] = v;
     G[q2 * 64 + q] = v;  // symmetric (the same value when the tile is diagonal)
 }

@@ -14,7 +14,8 @@
 // contraction over x, so it runs on the matrix cores: EQ(x) is written in
 // eight balanced base-256 digits d_t(x) in [-128, 128), and
 // G_t = Bits^T diag(d_t) Bits is an int8 x int8 -> int32 product
-// (v_mfma_i32_32x32x32_i8), recombined as sum_t 256^t G_t modulo p.  The
+// (v_mfma_i32_16x16x64_i8 over the 16 x 16 tiles on and above the diagonal:
+// G is symmetric), recombined as sum_t 256^t G_t modulo p.  The
 // same pass writes the plane-bound table Bx(x) = sum_q eq(sigma_p, q) bit_q(x)
 // (eight byte lookups per x), the input of the rounds over x.
 #include "common.hpp"
@@ -25,7 +26,6 @@
 namespace ra {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
 constexpr int kLimbs = 8;    // balanced base-256 digits of a field element
 
 
@@ -38,7 +38,8 @@ constexpr int kLimbs = 8;    // balanced base-256 digits of a field element
 //     stored as bytes 0x00 / 0xFF in rows padded so that the matrix-core
 //     fragment reads are free of bank conflicts;
 //   consumers (waves 8-15, two per SIMD): wave c accumulates digit c for
-//     every tile pair over the slab's K-steps on the matrix cores.
+//     every 16 x 16 tile of G on or above the diagonal over the slab's
+//     K-steps of 64 outputs on the matrix cores.
 // While the consumers stream slab i the producers build slab i + 1; one
 // barrier per slab hands the buffers over.  While the producers build the
 // first slab the consumers are free: with xs_on they run the set-up of the
@@ -47,9 +48,12 @@ constexpr int kSlab = 512;
 constexpr int kRow = kSlab + 16;  // bytes per plane row in LDS
 constexpr int kProducers = 8, kConsumers = 8, kGramThreads = 64 * (kProducers + kConsumers);
 
-template <int TP> struct GramShape {
-    static constexpr int kPlanes = 32 * (TP == 1 ? 1 : 2);
-    static constexpr int kDigitsPerWave = kLimbs / kConsumers;  // 1
+// NPL planes (32 or 64) in NB = NPL / 16 blocks of sixteen; tile t < NT
+// covers plane blocks (I, J), I <= J, in the order (0,0), (0,1), .., (1,1), ..
+template <int NPL> struct GramShape {
+    static constexpr int kBlocks = NPL / 16;
+    static constexpr int kTiles = kBlocks * (kBlocks + 1) / 2;
+    static_assert(kLimbs == kConsumers, "one digit per consumer wave");
 };
 
 // 8 x 8 bit transposes across each group of eight lanes, one per byte of a
@@ -88,25 +92,25 @@ __device__ __forceinline__ uint64_t balanced_digit_bytes(uint64_t e)
     return (e + kHalf) ^ kHalf;
 }
 
-template <int TP>
+template <int NPL>
 __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
     const uint64_t *__restrict__ bits, uint64_t N, int lk, const uint64_t *__restrict__ E1,
     const uint64_t *__restrict__ E2, const uint64_t *__restrict__ sig, int lP, uint64_t *__restrict__ Bx,
     uint64_t *__restrict__ gpart, int xs_on, XSetupArgs xs, const uint64_t *__restrict__ eqs)
 {
-    using S = GramShape<TP>;
-    constexpr int NPL = S::kPlanes, DW = S::kDigitsPerWave, NPT = TP == 1 ? 1 : 2;
-    constexpr int kPlaneBytes = NPL * kRow, kTileBytes = TP * 1024 * 8;
+    using S = GramShape<NPL>;
+    constexpr int NB = S::kBlocks, NT = S::kTiles;
+    constexpr int kPlaneBytes = NPL * kRow, kTileBytes = NT * kGramTileWords * 8;
     static_assert(2 * kPlaneBytes >= kTileBytes, "the tiles reuse the plane buffers");
     __shared__ uint64_t s_lut[8 * 256];                                    // Bx byte tables
     __shared__ uint64_t s_eqs[64];                                         // eq(sigma_p, q)
     __shared__ uint64_t s_exp[256];                                        // byte -> eight 0x00 / 0xFF bytes
     __shared__ __attribute__((aligned(16))) int8_t s_d[2][kLimbs][kSlab];  // digits of EQ(x)
-    // plane bytes of two slabs; afterwards the block's Gram tiles (entry
-    // r * 64 + lane of fragment register r)
+    // plane bytes of two slabs; afterwards the block's Gram tiles (tile t,
+    // entry 64 r + lane of fragment register r)
     __shared__ __attribute__((aligned(16))) int8_t s_u[2 * kPlaneBytes];
-    unsigned long long(*s_g)[1024] = (unsigned long long(*)[1024])s_u;
-    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
+    unsigned long long(*s_g)[kGramTileWords] = (unsigned long long(*)[kGramTileWords])s_u;
+    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool producer = wv < kProducers;  // wave-uniform
     const int cw = wv - kProducers;         // consumer index = its digit
     if (tid < 64) {  // eq(sigma_p, q) for every plane q (or the given values)
@@ -197,51 +201,46 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
         // whole waves of the set-up, spread one wave per block before a block's
         // second wave (wave w of block b takes entries 64 (w B + b) ..)
         if (xs_on) x_setup_body(xs, (int)(((wv - kProducers) * gridDim.x + blockIdx.x) * 64) + lane, s_xr, s_xs, s_xz);
-        v16i acc[DW][TP];
+        v4i acc[NT];
 #pragma unroll
-        for (int k = 0; k < DW; k++)
-#pragma unroll
-            for (int tp = 0; tp < TP; tp++)
-#pragma unroll
-                for (int r = 0; r < 16; r++) acc[k][tp][r] = 0;
+        for (int t = 0; t < NT; t++) acc[t] = v4i{0, 0, 0, 0};
         for (uint64_t i = 0; i <= mine; i++) {
             if (i > 0) {  // consume slab i - 1 from buffer (i - 1) % 2
                 const int buf = (int)((i - 1) & 1);
-                const int8_t *mrow = s_u + buf * kPlaneBytes + (lane & 31) * kRow + 16 * half;
-                const int8_t *drow = &s_d[buf][cw][16 * half];
+                // K-step ks covers outputs 64 ks .. 64 ks + 63 of the slab; lane l
+                // holds row l % 16 of a 16-row block and the sixteen outputs
+                // 16 (l / 16) .. of the step, as do the digit bytes it reads
+                const int8_t *frow = s_u + buf * kPlaneBytes + (lane & 15) * kRow + 16 * (lane >> 4);
+                const int8_t *drow = &s_d[buf][cw][16 * (lane >> 4)];
                 // The plane bytes are 0x00 / 0xFF, i.e. -bit as int8: they are the
                 // A operand as they stand (the tiles accumulate -G_t, negated in
                 // the recombination), and masked with the digits they give B.
                 // Two register sets alternate over the K-steps, so the reads of
                 // step ks + 1 are in flight during the products of step ks.
-                v4i m0[NPT], d0[DW], m1[NPT], d1[DW];
-                auto load = [&](v4i (&m)[NPT], v4i (&d)[DW], int ks) {
+                v4i f0[NB], d0, f1[NB], d1;
+                auto load = [&](v4i (&f)[NB], v4i &d, int ks) {
 #pragma unroll
-                    for (int pt = 0; pt < NPT; pt++) m[pt] = *(const v4i *)(mrow + 32 * pt * kRow + 32 * ks);
-#pragma unroll
-                    for (int k = 0; k < DW; k++) d[k] = *(const v4i *)(drow + kConsumers * k * kSlab + 32 * ks);
+                    for (int I = 0; I < NB; I++) f[I] = *(const v4i *)(frow + 16 * I * kRow + 64 * ks);
+                    d = *(const v4i *)(drow + 64 * ks);
                 };
-                auto step = [&](const v4i (&m)[NPT], const v4i (&d)[DW]) {
+                auto step = [&](const v4i (&f)[NB], const v4i &d) {
+                    v4i bj[NB];
 #pragma unroll
-                    for (int k = 0; k < DW; k++) {
-                        const v4i B0 = m[0] & d[k];
-                        acc[k][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(m[0], B0, acc[k][0], 0, 0, 0);
-                        if (TP > 1) {
-                            const v4i B1 = m[NPT - 1] & d[k];
-                            acc[k][1 % TP] =
-                                __builtin_amdgcn_mfma_i32_32x32x32_i8(m[0], B1, acc[k][1 % TP], 0, 0, 0);
-                            acc[k][2 % TP] =
-                                __builtin_amdgcn_mfma_i32_32x32x32_i8(m[NPT - 1], B1, acc[k][2 % TP], 0, 0, 0);
-                        }
-                    }
+                    for (int J = 0; J < NB; J++) bj[J] = f[J] & d;
+                    int t = 0;
+#pragma unroll
+                    for (int I = 0; I < NB; I++)
+#pragma unroll
+                        for (int J = I; J < NB; J++, t++)
+                            acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(f[I], bj[J], acc[t], 0, 0, 0);
                 };
-                static_assert((kSlab / 32) % 2 == 0, "K-steps come in pairs");
-                load(m0, d0, 0);
-                for (int ks = 0; ks < kSlab / 32; ks += 2) {
-                    load(m1, d1, ks + 1);
-                    step(m0, d0);
-                    if (ks + 2 < kSlab / 32) load(m0, d0, ks + 2);
-                    step(m1, d1);
+                static_assert((kSlab / 64) % 2 == 0, "K-steps come in pairs");
+                load(f0, d0, 0);
+                for (int ks = 0; ks < kSlab / 64; ks += 2) {
+                    load(f1, d1, ks + 1);
+                    step(f0, d0);
+                    if (ks + 2 < kSlab / 64) load(f0, d0, ks + 2);
+                    step(f1, d1);
                 }
             }
             __syncthreads();
@@ -250,18 +249,17 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
         // 2^(8t), a rotation of the 61-bit residue (of -acc: the A operand
         // held -bit); one LDS atomic per entry
         // and consumer wave (8 waves x values below 2^61 < 2^64)
-        for (int i = tid - 64 * kProducers; i < TP * 1024; i += 64 * kConsumers) (&s_g[0][0])[i] = 0;
+        for (int i = tid - 64 * kProducers; i < NT * kGramTileWords; i += 64 * kConsumers) (&s_g[0][0])[i] = 0;
         __syncthreads();
 #pragma unroll
-        for (int tp = 0; tp < TP; tp++)
+        for (int t = 0; t < NT; t++)
 #pragma unroll
-            for (int r = 0; r < 16; r++)
-                atomicAdd(&s_g[tp][r * 64 + lane],
-                          (unsigned long long)m61::rotl(m61::from_i32(-acc[0][tp][r]), 8 * cw));
+            for (int r = 0; r < 4; r++)
+                atomicAdd(&s_g[t][r * 64 + lane], (unsigned long long)m61::rotl(m61::from_i32(-acc[t][r]), 8 * cw));
         __syncthreads();
     }
-    for (int i = tid; i < TP * 1024; i += kGramThreads)
-        gpart[(size_t)blockIdx.x * TP * 1024 + i] = m61::reduce64((&s_g[0][0])[i]);
+    for (int i = tid; i < NT * kGramTileWords; i += kGramThreads)
+        gpart[(size_t)blockIdx.x * NT * kGramTileWords + i] = m61::reduce64((&s_g[0][0])[i]);
 }
 
 // Sum of the blocks' partial tiles, written as G[q][q'] (64 x 64, both
@@ -274,7 +272,7 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
 // workgroup writes the constant block of the plane rounds, with a deferred
 // witness step the one after sums the witness claims (and the claimed sum of
 // the range instance), the others run the set-up of the rounds over x.
-__global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict__ gpart, int nblk, int TP,
+__global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict__ gpart, int nblk, int tiles,
                                                      uint64_t *__restrict__ G, int nred, RangeConsts rc,
                                                      XSetupArgs xs)
 {
@@ -292,10 +290,10 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict_
         return;
     }
     __shared__ uint64_t red[kGramReduceLdsWords];
-    gram_reduce_block(gpart, nblk, TP, G, blockIdx.x, red);
+    gram_reduce_block(gpart, nblk, tiles, G, blockIdx.x, red);
 }
 
-int plane_gram_tiles(int lP) { return lP > 5 ? 3 : 1; }
+int plane_gram_tiles(int lP) { return GramShape<32>::kTiles * (lP <= 5) + GramShape<64>::kTiles * (lP > 5); }
 
 int plane_gram_set_up_threads(uint64_t N, int lP) { return plane_gram_blocks(N, lP) * 64 * kConsumers; }
 
@@ -310,24 +308,25 @@ void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const u
                        const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st,
                        const uint64_t *eqs)
 {
-    const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP);
+    const int nb = plane_gram_blocks(N, lP);
     const XSetupArgs none{};
     const XSetupArgs &x = xs ? *xs : none;
-    if (TP == 1)
-        hipLaunchKernelGGL(k_plane_gram<1>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
+    if (lP <= 5)
+        hipLaunchKernelGGL(k_plane_gram<32>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
                            gpart, xs ? 1 : 0, x, eqs);
     else
-        hipLaunchKernelGGL(k_plane_gram<3>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
+        hipLaunchKernelGGL(k_plane_gram<64>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
                            gpart, xs ? 1 : 0, x, eqs);
 }
 
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,
                         const XSetupArgs &xs, hipStream_t st)
 {
-    const int TP = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP), nred = TP * 64;
+    const int tiles = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP), nred = gram_reduce_groups(tiles);
     const int xb = (x_setup_count(xs) + 255) / 256;
     const int ncj = rc.cj.nblk > 0 ? 1 : 0;
-    hipLaunchKernelGGL(k_gram_reduce, dim3(nred + 1 + ncj + xb), dim3(256), 0, st, gpart, nb, TP, gsum, nred, rc, xs);
+    hipLaunchKernelGGL(k_gram_reduce, dim3(nred + 1 + ncj + xb), dim3(256), 0, st, gpart, nb, tiles, gsum, nred, rc,
+                       xs);
 }
 
 }  // namespace ra

@@ -236,7 +236,7 @@ __global__ __launch_bounds__(256) void k_xrounds(XArgs a, uint64_t sub, int stri
     if ((int)blockIdx.x >= nmain) {  // workgroup-uniform
         const int q = blockIdx.x - nmain, nj = jobs.nslot + jobs.nplane;
         if (q < nj) x_job(jobs, q, smem);
-        else if (q - nj < rr.nred) gram_reduce_block(rr.gpart, rr.nblk, rr.TP, rr.gsum, q - nj, smem);
+        else if (q - nj < rr.nred) gram_reduce_block(rr.gpart, rr.nblk, rr.tiles, rr.gsum, q - nj, smem);
         else if (q - nj == rr.nred) range_consts_block(rr.rc, smem);
         else witness_claims_block(rr.rc, smem);
         return;

@@ -394,6 +394,11 @@ __device__ __forceinline__ void xb_wave(const XBlockArgs &a, uint64_t k, uint64_
     uint64_t z[NR];
 #pragma unroll
     for (int c = 0; c < B; c++) z[c] = rho[c];
+    // the last pass: the constants of the evaluation this lane makes (round
+    // lane / 4), fetched before the rounds
+    static_assert(4 * kXTailLog <= 64, "one evaluation per lane in the last pass");
+    XEvalK kc{};
+    if (nsub == 1 && lane < 4 * B) kc = x_eval_consts(a.xc, a.j + (lane >> 2), ZW);
     // round c's sums of this lane go to red[(c NV + q) kXbRedStride + lane]
 #pragma unroll
     for (int c = 0; c < B; c++) {
@@ -477,7 +482,7 @@ __device__ __forceinline__ void xb_wave(const XBlockArgs &a, uint64_t k, uint64_
         for (int t = lane; t < 4 * B; t += 64) {
             const int c = t >> 2, X = t & 3;
             const int out = ZW ? a.out2 : a.out0;
-            if (out >= 0) a.tr[out + 4 * c + X] = x_round_eval(tot + 8 * c, a.j + c, X, ZW, a.xc);
+            if (out >= 0) a.tr[out + 4 * c + X] = x_round_eval(tot + 8 * c, kc, X, ZW);
         }
         if (lane == 0) {
             if (!ZW) {

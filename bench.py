@@ -89,7 +89,8 @@ def group_work(shapes, planes):
                      eq tables written;
       range_plane    HBM bytes of the plane rounds: the packed bit table in
                      (P N / 8 B) and the plane-bound table Bx out (8 N B)
-                     (secondary: the int8 MFMA operations of the Gram matrix);
+                     (secondary: the int8 MFMA operations of the Gram matrix's
+                     16 x 16 tiles on and above the diagonal);
       range_rounds   HBM bytes of the register/LDS passes over x: each pass
                      reads its input tables and writes the folded ones
                      (secondary: 32-bit multiplies, 4 per field product);
@@ -116,8 +117,8 @@ def group_work(shapes, planes):
         add("matmul_front", "hbm", n * m * ab + m * k * 2 + 8 * (n + k))
         add("witness_minmax", "hbm", 8 * N)
         add("witness_rescale", "hbm", N * (8 + 4 + 2 + 4 + 4 + 8))  # C in; R, Rm, Y, Z, bits out
-        TP = 3 if P > 32 else 1
-        add("range_plane", "hbm", P * N // 8 + 8 * N, ("mfma", N * TP * 1024 * 2 * 8))
+        tiles = 10 if P > 32 else 3  # 16 x 16 tiles on and above the Gram matrix's diagonal
+        add("range_plane", "hbm", P * N // 8 + 8 * N, ("mfma", N * tiles * 256 * 2 * 8))
         # rounds over x: per pair, 6 field products (range) and 7 (ReLU); each
         # pass reads Bx (and R, Y as int32 in the first, D and S after) and
         # writes them folded to 2^-C of their size

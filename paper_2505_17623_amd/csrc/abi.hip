@@ -1171,7 +1171,10 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
     launch_bind_cols(d_B, RA_I16, m, k, E2.im, Tb.im, s);
     uint64_t *ev_mm = tr + kF2TrFixed, *ev_rs = ev_mm + 6 * (size_t)lm, *ev_zc = ev_rs + 8 * (size_t)(lP + lN);
     uint64_t *p_mm = part, *p_rs = p_mm + (size_t)lm * pstride, *p_zc = p_rs + (size_t)lN * pstride;
-    for (int j = 0; j < lm; j++) {
+    // each instance: one launch per round while its tables hold more than
+    // 2^kF2TailLog entries, then the rest in one workgroup
+    const int tm = std::min(lm, kF2TailLog), jm = lm - tm;
+    for (int j = 0; j < jm; j++) {
         F2RoundArgs ra{};
         ra.kind = F2_MATMUL;
         ra.h = (uint64_t)m >> (j + 1);
@@ -1180,6 +1183,16 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
         ra.rho = rho + 2 * j;
         ra.part = p_mm + (size_t)j * pstride;
         launch_f2_round(ra, s);
+    }
+    if (tm > 0) {
+        F2TailArgs ta{};
+        ta.kind = F2_MATMUL;
+        ta.v = tm;
+        ta.src[0] = ta.dst[0] = Ta;
+        ta.src[1] = ta.dst[1] = Tb;
+        ta.rho = rho + 2 * jm;
+        ta.part = p_mm + (size_t)jm * pstride;
+        launch_f2_tail(ta, s);
     }
     {
         F2FinishArgs fa{};
@@ -1226,7 +1239,8 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
         launch_f2_planes(pa, s);
     }
     // rounds over x of the range instance (tables EQ, Bx), then the ReLU zero-check (EQ, D, S)
-    for (int j = 0; j < lN; j++) {
+    const int tx = std::min(lN, kF2TailLog), jx = lN - tx;
+    for (int j = 0; j < jx; j++) {
         F2RoundArgs ra{};
         ra.kind = F2_RANGE;
         ra.first = j == 0;
@@ -1238,6 +1252,19 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
         ra.cst = cst;
         ra.part = p_rs + (size_t)j * pstride;
         launch_f2_round(ra, s);
+    }
+    if (tx > 0) {
+        F2TailArgs ta{};
+        ta.kind = F2_RANGE;
+        ta.first = jx == 0;
+        ta.v = tx;
+        ta.src[0] = jx == 0 ? EQ : EQr;
+        ta.dst[0] = EQr;
+        ta.src[1] = ta.dst[1] = Bx;
+        ta.rho = sig + 2 * (lP + jx);
+        ta.cst = cst;
+        ta.part = p_rs + (size_t)jx * pstride;
+        launch_f2_tail(ta, s);
     }
     {
         F2FinishArgs fa{};
@@ -1251,7 +1278,7 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
         launch_f2_finish(fa, s);
     }
     if (relu) {
-        for (int j = 0; j < lN; j++) {
+        for (int j = 0; j < jx; j++) {
             F2RoundArgs ra{};
             ra.kind = F2_RELU;
             ra.first = j == 0;
@@ -1265,6 +1292,21 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
             ra.rho = rho2 + 2 * j;
             ra.part = p_zc + (size_t)j * pstride;
             launch_f2_round(ra, s);
+        }
+        if (tx > 0) {
+            F2TailArgs ta{};
+            ta.kind = F2_RELU;
+            ta.first = jx == 0;
+            ta.v = tx;
+            ta.src[0] = jx == 0 ? EQ : EQz;
+            ta.dst[0] = EQz;
+            ta.src[1] = ta.dst[1] = Dt;
+            ta.src[2] = ta.dst[2] = St;
+            ta.R = d_R;
+            ta.Y = d_Y;
+            ta.rho = rho2 + 2 * jx;
+            ta.part = p_zc + (size_t)jx * pstride;
+            launch_f2_tail(ta, s);
         }
         F2FinishArgs fa{};
         fa.kind = F2_RELU;

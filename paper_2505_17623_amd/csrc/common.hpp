@@ -309,6 +309,19 @@ struct F2RoundArgs {
     const uint64_t *cst;   // range: c_eq, c_w
     uint64_t *part;        // f2_blocks(h) x 8 words
 };
+// the last v rounds (v <= kF2TailLog) of an instance, from its round j0 on,
+// in one workgroup: src -> dst as in F2RoundArgs (first: j0 == 0); rho: the
+// challenges of rounds j0 .. j0 + v - 1; part: round j0's partial slots
+constexpr int kF2TailLog = 10;
+struct F2TailArgs {
+    int kind, first, v;
+    F2Tab src[3], dst[3];
+    const int32_t *R, *Y;
+    const uint64_t *rho;
+    const uint64_t *cst;
+    uint64_t *part;
+};
+void launch_f2_tail(const F2TailArgs &a, hipStream_t st);
 // the evaluations of an instance's v rounds (partials of round j at part +
 // j kF2MaxBlocks 8) and its final words
 struct F2FinishArgs {

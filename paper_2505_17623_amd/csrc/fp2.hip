@@ -15,8 +15,9 @@
 //     parts the F_p Gram pass computes from EQ's two parts;
 //   - every folded table of the rounds.
 // Rounds run one launch per round (a pass over the pairs that evaluates the
-// round polynomial and folds the tables in place), which is slower than the
-// F_p path's fused passes.
+// round polynomial and folds the tables in place) while the tables are
+// large, and the last rounds of an instance in one workgroup over LDS; this
+// is slower than the F_p path's fused passes.
 #include "common.hpp"
 #include "m61.hpp"
 #include "gram_reduce.hpp"
@@ -168,6 +169,47 @@ void launch_f2_sum8(const uint64_t *part, int nb, uint64_t *out, hipStream_t st)
 //   F2_RELU    EQ D S, D = R - Y, S = R + Y         (Eq. (6); degree 3)
 // The first round of the ReLU instance reads R, Y (int32) for D, S.
 // ---------------------------------------------------------------------------
+// The summand of one pair at X = 0..3 added into acc, and the folded values
+// lo + rho (hi - lo) into lo.
+template <int KIND>
+__device__ __forceinline__ void f2_pair(f2 (&lo)[3], const f2 (&hi)[3], f2 rho, f2 ceq, f2 cw, f2 (&acc)[4])
+{
+    constexpr int NT = KIND == F2_RELU ? 3 : 2;
+    f2 v[3], d[3];
+#pragma unroll
+    for (int q = 0; q < NT; q++) {
+        v[q] = lo[q];
+        d[q] = f2sub(hi[q], lo[q]);
+    }
+#pragma unroll
+    for (int X = 0; X < 4; X++) {
+        if (X > 0)
+#pragma unroll
+            for (int q = 0; q < NT; q++) v[q] = f2add(v[q], d[q]);  // the tables at X
+        f2 f;
+        if (KIND == F2_MATMUL) {
+            if (X == 3) break;
+            f = f2mul(v[0], v[1]);
+        } else if (KIND == F2_RANGE) {
+            f = f2mul(f2mul(v[0], v[1]), f2add(f2mul(ceq, f2sub(v[1], f2of(1))), cw));
+        } else {
+            f = f2mul(f2mul(v[0], v[1]), v[2]);
+        }
+        acc[X] = f2add(acc[X], f);
+    }
+#pragma unroll
+    for (int q = 0; q < NT; q++) lo[q] = f2add(lo[q], f2mul(rho, d[q]));
+}
+
+// The ReLU instance's first round reads D = R - Y and S = R + Y from the
+// integer tables.
+__device__ __forceinline__ void f2_relu_ints(const int32_t *R, const int32_t *Y, uint64_t i, f2 &d, f2 &s)
+{
+    const int64_t r = R[i], y = Y[i];
+    d = f2of(m61::from_i64(r - y));
+    s = f2of(m61::from_i64(r + y));
+}
+
 template <int KIND>
 __global__ __launch_bounds__(256) void k_f2_round(F2RoundArgs a)
 {
@@ -186,11 +228,8 @@ __global__ __launch_bounds__(256) void k_f2_round(F2RoundArgs a)
         lo[0] = ldt(a.src[0], i);
         hi[0] = ldt(a.src[0], i + h);
         if (KIND == F2_RELU && a.first) {
-            const int64_t r0 = a.R[i], r1 = a.R[i + h], y0 = a.Y[i], y1 = a.Y[i + h];
-            lo[1] = f2of(m61::from_i64(r0 - y0));
-            hi[1] = f2of(m61::from_i64(r1 - y1));
-            lo[2] = f2of(m61::from_i64(r0 + y0));
-            hi[2] = f2of(m61::from_i64(r1 + y1));
+            f2_relu_ints(a.R, a.Y, i, lo[1], lo[2]);
+            f2_relu_ints(a.R, a.Y, i + h, hi[1], hi[2]);
         } else {
 #pragma unroll
             for (int q = 1; q < NT; q++) {
@@ -198,32 +237,89 @@ __global__ __launch_bounds__(256) void k_f2_round(F2RoundArgs a)
                 hi[q] = ldt(a.src[q], i + h);
             }
         }
-        f2 v[3], d[3];
+        f2_pair<KIND>(lo, hi, rho, ceq, cw, acc);
 #pragma unroll
-        for (int q = 0; q < NT; q++) {
-            v[q] = lo[q];
-            d[q] = f2sub(hi[q], lo[q]);
-        }
-#pragma unroll
-        for (int X = 0; X < 4; X++) {
-            if (X > 0)
-#pragma unroll
-                for (int q = 0; q < NT; q++) v[q] = f2add(v[q], d[q]);  // the tables at X
-            f2 f;
-            if (KIND == F2_MATMUL) {
-                if (X == 3) break;
-                f = f2mul(v[0], v[1]);
-            } else if (KIND == F2_RANGE) {
-                f = f2mul(f2mul(v[0], v[1]), f2add(f2mul(ceq, f2sub(v[1], f2of(1))), cw));
-            } else {
-                f = f2mul(f2mul(v[0], v[1]), v[2]);
-            }
-            acc[X] = f2add(acc[X], f);
-        }
-#pragma unroll
-        for (int q = 0; q < NT; q++) stt(a.dst[q], i, f2add(lo[q], f2mul(rho, d[q])));
+        for (int q = 0; q < NT; q++) stt(a.dst[q], i, lo[q]);
     }
     f2_block_out(acc, red, a.part + 8 * (size_t)blockIdx.x);
+}
+
+// ---------------------------------------------------------------------------
+// The last v <= kF2TailLog rounds of an instance in one workgroup: the tables
+// (2^v entries) are staged in LDS and folded there, round after round; each
+// round's sums go to its first partial slot (the round's other slots are
+// zeroed, so the finish kernel reads the same layout as after k_f2_round),
+// and the final values to index 0 of the destination tables.
+// ---------------------------------------------------------------------------
+template <int KIND>
+__global__ __launch_bounds__(256) void k_f2_tail(F2TailArgs a)
+{
+    constexpr int NT = KIND == F2_RELU ? 3 : 2, S = 1 << kF2TailLog;
+    __shared__ uint64_t T[NT][2][S];  // (re, im) of each table
+    __shared__ uint64_t red[m61::block_sum_words(8, 256)];
+    __shared__ uint64_t rz[2 * kF2TailLog];
+    const int tid = threadIdx.x, n0 = 1 << a.v;
+    f2 ceq = f2of(0), cw = f2of(0);
+    if (KIND == F2_RANGE) {
+        ceq = ldp(a.cst);
+        cw = ldp(a.cst + 2);
+    }
+    if (tid < 2 * a.v) rz[tid] = a.rho[tid];
+    for (int i = tid; i < n0; i += blockDim.x) {
+        f2 t[3];
+        t[0] = ldt(a.src[0], i);
+        if (KIND == F2_RELU && a.first) {
+            f2_relu_ints(a.R, a.Y, i, t[1], t[2]);
+        } else {
+#pragma unroll
+            for (int q = 1; q < NT; q++) t[q] = ldt(a.src[q], i);
+        }
+#pragma unroll
+        for (int q = 0; q < NT; q++) {
+            T[q][0][i] = t[q].re;
+            T[q][1][i] = t[q].im;
+        }
+    }
+    __syncthreads();
+    for (int c = 0; c < a.v; c++) {
+        const int h = n0 >> (c + 1);
+        const f2 rho{rz[2 * c], rz[2 * c + 1]};
+        f2 acc[4] = {f2of(0), f2of(0), f2of(0), f2of(0)};
+        // a pair's entries are read and its fold written by one thread only
+        for (int i = tid; i < h; i += blockDim.x) {
+            f2 lo[3], hi[3];
+#pragma unroll
+            for (int q = 0; q < NT; q++) {
+                lo[q] = f2{T[q][0][i], T[q][1][i]};
+                hi[q] = f2{T[q][0][i + h], T[q][1][i + h]};
+            }
+            f2_pair<KIND>(lo, hi, rho, ceq, cw, acc);
+#pragma unroll
+            for (int q = 0; q < NT; q++) {
+                T[q][0][i] = lo[q].re;
+                T[q][1][i] = lo[q].im;
+            }
+        }
+        uint64_t *part = a.part + (size_t)c * kF2MaxBlocks * 8;
+        const int nb = f2_blocks((uint64_t)h);
+        if (tid >= 1 && tid < nb)
+#pragma unroll
+            for (int q = 0; q < 8; q++) part[8 * tid + q] = 0;
+        f2_block_out(acc, red, part);  // its barriers also order this round's folds before the next reads
+        __syncthreads();
+    }
+    if (tid == 0)
+#pragma unroll
+        for (int q = 0; q < NT; q++) stt(a.dst[q], 0, f2{T[q][0][0], T[q][1][0]});
+}
+
+void launch_f2_tail(const F2TailArgs &a, hipStream_t st)
+{
+    switch (a.kind) {
+    case F2_MATMUL: hipLaunchKernelGGL(k_f2_tail<F2_MATMUL>, dim3(1), dim3(kThreads), 0, st, a); break;
+    case F2_RANGE: hipLaunchKernelGGL(k_f2_tail<F2_RANGE>, dim3(1), dim3(kThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL(k_f2_tail<F2_RELU>, dim3(1), dim3(kThreads), 0, st, a); break;
+    }
 }
 
 void launch_f2_round(const F2RoundArgs &a, hipStream_t st)

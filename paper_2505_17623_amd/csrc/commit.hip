@@ -2,15 +2,17 @@
 // (Sec. II-C commits a vector a as g^a; Sec. IV names the curve), for the
 // integer tables of a layer.
 //
-// The values are small integers (the witness tables hold 16- or 32-bit
-// entries, the bit table 64-bit words), so the product is split by the bits
-// of |v|:  P = sum_k 2^k (B_k^+ - B_k^-),  B_k^+- = the sum of G_i over the
-// i with v_i >= 0 (< 0) and bit k of |v_i| set.  Each (k, sign) slot is a
-// plain masked sum of generators: its threads stride over the points and add
-// the ones whose bit is set (one mixed Jacobian-affine addition each), so the
-// work does not depend on how the values are distributed; partial sums are
-// then added in a tree, and one thread combines the slots by Horner's rule
-// (a doubling per bit) and converts to affine coordinates.
+// The multi-scalar product is the bucket (Pippenger) method with 8-bit
+// windows of |v_i| (two windows for 16-bit values, four for 32-bit, eight
+// for 64-bit words), the sign applied to the point:
+//   P = sum_w 2^(8w) sum_{b=1}^{255} b S_{w,b},  S_{w,b} = sum of sign(v_i) G_i
+//   over the i whose window-w digit of |v_i| is b.
+// A workgroup takes a chunk of values and one window: it sorts the chunk by
+// digit in LDS (a counting sort), then every thread adds an equal run of the
+// sorted list with mixed Jacobian-affine additions, so a heavy bucket is
+// spread over many threads; the runs' partial sums, in bucket order, are
+// added per bucket.  The chunks' bucket sums are then added per bucket, and
+// sum_b b S_{w,b} is formed as sum_k 2^k (sum over the b with bit k set).
 #include <algorithm>
 
 #include "commit.hpp"
@@ -81,18 +83,22 @@ void launch_commit_generators(const uint8_t *domain, uint64_t first, uint64_t co
 }
 
 // ---------------------------------------------------------------------------
-// The bit slots
+// The bucket method
 // ---------------------------------------------------------------------------
-int msm_bits(int kind) { return kind == 2 ? 32 : (kind == 3 ? 64 : 16); }
-int msm_signs(int kind) { return (kind == 0 || kind == 2) ? 2 : 1; }
-constexpr size_t kJacWords = 24;
+constexpr int kPipSub = 4096;              // values a workgroup sorts at a time (two workgroups fit a CU)
+constexpr int kPipRun = kPipSub / 256;     // sorted positions per thread
+constexpr int kPipParts = 256 + 255;       // run partials of one sort, at most
+constexpr int kJacWords = 24;              // X, Y, Z: eight 32-bit limbs each
+
+int msm_windows(int kind) { return kind == 3 ? 8 : (kind == 2 ? 4 : 2); }
 
 size_t msm_workspace_bytes(int kind)
 {
-    const size_t slots = (size_t)msm_bits(kind) * msm_signs(kind);
-    size_t b = slots * kMsmThreadsPerSlot * kJacWords * 4;                      // the threads' partial sums
-    b += slots * ((kMsmThreadsPerSlot + kMsmGroup - 1) / kMsmGroup) * kJacWords * 4;  // one reduction level
-    return b + 256;
+    const size_t W = (size_t)msm_windows(kind), jac = (size_t)kJacWords * 4;
+    return W * kMsmChunks * 256 * jac   // the chunks' bucket sums
+           + W * 256 * jac             // the bucket sums
+           + W * 8 * jac               // their bit sums
+           + 256;
 }
 
 // |v| and its sign for value i
@@ -128,80 +134,225 @@ __device__ __forceinline__ Jac load_jac(const uint32_t *p)
     return j;
 }
 
-// slot s = blockIdx.y: bit k = s mod bits of the values of sign s / bits
-__global__ __launch_bounds__(256) void k_msm_bits(const void *__restrict__ vals, int kind, uint64_t n,
-                                                  const uint32_t *__restrict__ gens, int bits,
-                                                  uint32_t *__restrict__ part)
+// Exclusive prefix sums of one value per thread (256 threads); the total to
+// *total.  sc: 4 words of LDS.
+__device__ __forceinline__ uint32_t block_scan256(uint32_t v, uint32_t *sc, uint32_t *total)
 {
-    const int slot = blockIdx.y, k = slot % bits, want_neg = slot / bits;
-    const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    Jac acc = secp::jac_inf();
-    for (uint64_t i = t; i < n; i += kMsmThreadsPerSlot) {
-        uint64_t mag;
-        int neg;
-        scalar(vals, kind, i, mag, neg);
-        if (neg != want_neg || !((mag >> k) & 1)) continue;
-        Aff g;
-        const uint32_t *gp = gens + 16 * i;
-        for (int l = 0; l < 8; l++) {
-            g.x.v[l] = gp[l];
-            g.y.v[l] = gp[8 + l];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    uint32_t inc = v;
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += t;
+    }
+    if (lane == 63) sc[wv] = inc;
+    __syncthreads();
+    uint32_t before = 0;
+    for (int q = 0; q < wv; q++) before += sc[q];
+    if (total && threadIdx.x == 255) *total = before + inc;
+    const uint32_t ex = before + inc - v;
+    __syncthreads();
+    return ex;
+}
+
+// Workgroup (c, w): the window-w bucket sums of values c L .. c L + L - 1
+// (L = per), in sorts of kPipSub values; written to out[(w C + c) 256 + b].
+__global__ __launch_bounds__(256) void k_pip_buckets(const void *__restrict__ vals, int kind, uint64_t n,
+                                                     const uint32_t *__restrict__ gens, uint64_t per,
+                                                     uint32_t *__restrict__ out)
+{
+    __shared__ uint8_t dig[kPipSub], sgn[kPipSub];
+    __shared__ uint16_t perm[kPipSub];
+    __shared__ uint32_t cnt[256], cur[256], first[256], sc[4], tot[2];
+    __shared__ uint8_t pd[kPipParts];
+    __shared__ uint32_t pp[kPipParts][kJacWords];
+    const int tid = threadIdx.x, w = blockIdx.y, c = blockIdx.x;
+    const uint64_t lo = (uint64_t)c * per, hi = lo + per < n ? lo + per : n;
+    Jac bucket = secp::jac_inf();  // thread b's bucket b (b >= 1)
+    for (uint64_t base = lo; base < hi; base += kPipSub) {
+        const int len = (int)(hi - base < (uint64_t)kPipSub ? hi - base : (uint64_t)kPipSub);
+        cnt[tid] = 0;
+        first[tid] = 0xFFFFFFFFu;
+        __syncthreads();
+        for (int i = tid; i < len; i += 256) {
+            uint64_t mag;
+            int neg;
+            scalar(vals, kind, base + i, mag, neg);
+            const int d = (int)((mag >> (8 * w)) & 255);
+            dig[i] = (uint8_t)d;
+            sgn[i] = (uint8_t)neg;
+            atomicAdd(&cnt[d], 1u);
         }
-        acc = secp::jac_add_aff(acc, g);
+        __syncthreads();
+        // counting sort by digit: perm[start(d) ..] holds the positions of digit d
+        const uint32_t st = block_scan256(cnt[tid], sc, nullptr);
+        cur[tid] = st;
+        if (tid == 1) tot[0] = st;  // the start of digit 1: the number of zero digits
+        __syncthreads();
+        for (int i = tid; i < len; i += 256) perm[atomicAdd(&cur[dig[i]], 1u)] = (uint16_t)i;
+        __syncthreads();
+        // runs of the sorted list past the zero digits: thread t takes [r0, r1)
+        const int skip = (int)tot[0], run = (len - skip + 255) / 256;
+        const int r0 = skip + tid * run < len ? skip + tid * run : len;
+        const int r1 = r0 + run < len ? r0 + run : len;
+        uint32_t np = 0;  // partials of this run: its distinct digits
+        for (int q = r0, prev = -1; q < r1; q++) {
+            const int d = dig[perm[q]];
+            if (d != prev) np++;
+            prev = d;
+        }
+        const uint32_t off = block_scan256(np, sc, &tot[1]);
+        {
+            Jac acc = secp::jac_inf();
+            int cd = -1;
+            uint32_t k = off;
+            for (int q = r0; q < r1; q++) {
+                const int i = perm[q], d = dig[i];
+                if (d != cd) {
+                    if (cd >= 0) {
+                        store_jac(pp[k], acc);
+                        pd[k++] = (uint8_t)cd;
+                    }
+                    acc = secp::jac_inf();
+                    cd = d;
+                }
+                Aff g;
+                const uint32_t *gp = gens + 16 * (base + i);
+                for (int l = 0; l < 8; l++) {
+                    g.x.v[l] = gp[l];
+                    g.y.v[l] = gp[8 + l];
+                }
+                if (sgn[i]) g.y = secp::fe_neg(g.y);
+                acc = secp::jac_add_aff(acc, g);
+            }
+            if (cd >= 0) {
+                store_jac(pp[k], acc);
+                pd[k] = (uint8_t)cd;
+            }
+        }
+        __syncthreads();
+        // The partials are in digit order.  A digit spread over many runs (a
+        // heavy bucket) has many partials: they are summed by a segmented tree,
+        // each round adding to partial k the partial k + s of the same digit
+        // (values read before any is written), until every segment's first
+        // partial holds its sum.
+        const uint32_t nparts = tot[1];
+        if (tid == 0) tot[0] = 1;  // the longest segment
+        for (uint32_t k = tid; k < nparts; k += 256) {
+            if (k == 0 || pd[k] != pd[k - 1]) first[pd[k]] = k;
+            atomicAdd(&cnt[pd[k]], 1u << 16);  // the partials of digit d, above cnt's 13-bit counts
+        }
+        __syncthreads();
+        atomicMax(&tot[0], cnt[tid] >> 16);
+        __syncthreads();
+        for (uint32_t sd = 1; sd < tot[0]; sd <<= 1) {
+            Jac add[2];
+            bool has[2] = {false, false};
+#pragma unroll
+            for (int e = 0; e < 2; e++) {
+                const uint32_t k = tid + 256 * e;
+                if (k + sd < nparts && pd[k + sd] == pd[k]) {
+                    add[e] = secp::jac_add(load_jac(pp[k]), load_jac(pp[k + sd]));
+                    has[e] = true;
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int e = 0; e < 2; e++)
+                if (has[e]) store_jac(pp[tid + 256 * e], add[e]);
+            __syncthreads();
+        }
+        if (tid >= 1 && first[tid] != 0xFFFFFFFFu) bucket = secp::jac_add(bucket, load_jac(pp[first[tid]]));
+        __syncthreads();  // LDS reused by the next sort
     }
-    store_jac(part + ((size_t)slot * kMsmThreadsPerSlot + t) * kJacWords, acc);
+    if (tid >= 1) store_jac(out + (((size_t)w * gridDim.x + c) * 256 + tid) * kJacWords, bucket);
 }
 
-// out[slot][j] = sum of in[slot][j G .. j G + G - 1] (count entries per slot in, stride in_stride)
-__global__ __launch_bounds__(256) void k_msm_reduce(const uint32_t *__restrict__ in, int count, int in_stride,
-                                                    uint32_t *__restrict__ out, int out_stride)
+// Sums of 64 points per group of 64 threads (each thread's point in p[tid])
+// by a tree in LDS; the group's first thread ends with the sum in p.
+__device__ __forceinline__ void group64_tree(uint32_t (*p)[kJacWords])
 {
-    const int slot = blockIdx.y;
-    const int j = blockIdx.x * blockDim.x + threadIdx.x;
-    const int groups = (count + kMsmGroup - 1) / kMsmGroup;
-    if (j >= groups) return;
-    Jac acc = secp::jac_inf();
-    for (int q = j * kMsmGroup; q < std::min(count, (j + 1) * kMsmGroup); q++)
-        acc = secp::jac_add(acc, load_jac(in + ((size_t)slot * in_stride + q) * kJacWords));
-    store_jac(out + ((size_t)slot * out_stride + j) * kJacWords, acc);
+    const int tid = threadIdx.x, j = tid & 63;
+    for (int st = 32; st >= 1; st >>= 1) {
+        __syncthreads();
+        if (j < st) store_jac(p[tid], secp::jac_add(load_jac(p[tid]), load_jac(p[tid + st])));
+    }
+    __syncthreads();
 }
 
-// P = sum_k 2^k (B_k^+ - B_k^-) by Horner's rule, then affine bytes
-__global__ void k_msm_final(const uint32_t *__restrict__ sums, int stride, int bits, int signs,
-                            uint8_t *__restrict__ out)
+// S[w][b] = sum over the C chunks of in[w][c][b]: 64 threads per bucket, each
+// a strided share, then a tree.
+__global__ __launch_bounds__(256) void k_pip_bucket_sums(const uint32_t *__restrict__ in, int W, int C,
+                                                         uint32_t *__restrict__ S)
 {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    __shared__ uint32_t part[256][kJacWords];
+    const int tid = threadIdx.x, g = tid >> 6, j = tid & 63;
+    const int wb = blockIdx.x * 4 + g, w = wb >> 8, b = wb & 255;  // (window, bucket)
     Jac acc = secp::jac_inf();
-    for (int k = bits - 1; k >= 0; k--) {
-        acc = secp::jac_dbl(acc);
-        acc = secp::jac_add(acc, load_jac(sums + (size_t)k * stride * kJacWords));
-        if (signs == 2) acc = secp::jac_add(acc, secp::jac_neg(load_jac(sums + (size_t)(bits + k) * stride * kJacWords)));
+    if (w < W && b >= 1)
+        for (int c = j; c < C; c += 64) acc = secp::jac_add(acc, load_jac(in + (((size_t)w * C + c) * 256 + b) * kJacWords));
+    store_jac(part[tid], acc);
+    group64_tree(part);
+    if (j == 0 && w < W) store_jac(S + ((size_t)w * 256 + b) * kJacWords, load_jac(part[tid]));
+}
+
+// U[w][k] = sum over the b with bit k of S[w][b] (128 buckets): 64 threads
+// per (w, k), two buckets each, then a tree.
+__global__ __launch_bounds__(256) void k_pip_bit_sums(const uint32_t *__restrict__ S, int W, uint32_t *__restrict__ U)
+{
+    __shared__ uint32_t part[256][kJacWords];
+    const int tid = threadIdx.x, g = tid >> 6, j = tid & 63;
+    const int wk = blockIdx.x * 4 + g, w = wk >> 3, k = wk & 7;
+    Jac acc = secp::jac_inf();
+    if (w < W)
+        for (int q = j; q < 128; q += 64) {  // the q-th b with bit k set
+            const int b = ((q >> k) << (k + 1)) | (1 << k) | (q & ((1 << k) - 1));
+            acc = secp::jac_add(acc, load_jac(S + ((size_t)w * 256 + b) * kJacWords));
+        }
+    store_jac(part[tid], acc);
+    group64_tree(part);
+    if (j == 0 && w < W) store_jac(U + ((size_t)w * 8 + k) * kJacWords, load_jac(part[tid]));
+}
+
+// P = sum_w 2^(8w) T_w, T_w = sum_k 2^k U[w][k]: the windows' T_w by one
+// thread each, then Horner over the windows; affine bytes to out.
+__global__ __launch_bounds__(64) void k_pip_final(const uint32_t *__restrict__ U, int W, uint8_t *__restrict__ out)
+{
+    __shared__ uint32_t T[8][kJacWords];
+    const int tid = threadIdx.x;
+    if (tid < W) {
+        Jac t = secp::jac_inf();
+        for (int k = 7; k >= 0; k--) {
+            t = secp::jac_dbl(t);
+            t = secp::jac_add(t, load_jac(U + ((size_t)tid * 8 + k) * kJacWords));
+        }
+        store_jac(T[tid], t);
     }
-    uint8_t b[64];
-    secp::jac_encode(acc, b);
-    for (int i = 0; i < 64; i++) out[i] = b[i];
+    __syncthreads();
+    if (tid == 0) {
+        Jac p = secp::jac_inf();
+        for (int w = W - 1; w >= 0; w--) {
+            for (int q = 0; q < 8; q++) p = secp::jac_dbl(p);
+            p = secp::jac_add(p, load_jac(T[w]));
+        }
+        uint8_t bytes[64];
+        secp::jac_encode(p, bytes);
+        for (int i = 0; i < 64; i++) out[i] = bytes[i];
+    }
 }
 
 void launch_commit(const void *vals, int kind, uint64_t n, const uint32_t *gens, void *ws, uint8_t *out,
                    hipStream_t st)
 {
-    const int bits = msm_bits(kind), slots = bits * msm_signs(kind);
-    uint32_t *p0 = (uint32_t *)ws;
-    uint32_t *p1 = p0 + (size_t)slots * kMsmThreadsPerSlot * kJacWords;
-    hipLaunchKernelGGL(k_msm_bits, dim3(kMsmThreadsPerSlot / 256, slots), dim3(256), 0, st, vals, kind, n, gens, bits,
-                       p0);
-    // tree: 8192 -> 512 -> 32 -> 2 -> 1 partial sums per slot, alternating between the two areas
-    int count = kMsmThreadsPerSlot, stride_in = kMsmThreadsPerSlot;
-    uint32_t *in = p0, *outp = p1;
-    while (count > 1) {
-        const int groups = (count + kMsmGroup - 1) / kMsmGroup;
-        hipLaunchKernelGGL(k_msm_reduce, dim3((groups + 255) / 256, slots), dim3(256), 0, st, in, count, stride_in,
-                           outp, groups);
-        std::swap(in, outp);
-        stride_in = groups;
-        count = groups;
-    }
-    hipLaunchKernelGGL(k_msm_final, dim3(1), dim3(64), 0, st, in, stride_in, bits, msm_signs(kind), out);
+    const int W = msm_windows(kind);
+    const uint64_t subs = (n + kPipSub - 1) / kPipSub;
+    const int C = (int)(subs < (uint64_t)kMsmChunks ? (subs ? subs : 1) : kMsmChunks);
+    const uint64_t per = ((n + C - 1) / C + kPipSub - 1) / kPipSub * kPipSub;  // whole sorts per chunk but the last
+    uint32_t *chunk_sums = (uint32_t *)ws;
+    uint32_t *S = chunk_sums + (size_t)W * kMsmChunks * 256 * kJacWords, *U = S + (size_t)W * 256 * kJacWords;
+    hipLaunchKernelGGL(k_pip_buckets, dim3(C, W), dim3(256), 0, st, vals, kind, n, gens, per, chunk_sums);
+    hipLaunchKernelGGL(k_pip_bucket_sums, dim3(W * 64), dim3(256), 0, st, chunk_sums, W, C, S);
+    hipLaunchKernelGGL(k_pip_bit_sums, dim3(W * 2), dim3(256), 0, st, S, W, U);
+    hipLaunchKernelGGL(k_pip_final, dim3(1), dim3(64), 0, st, U, W, out);
 }
 
 }  // namespace ra

@@ -5,8 +5,7 @@
 
 namespace ra {
 
-constexpr int kMsmThreadsPerSlot = 8192;  // threads summing one bit slot's points
-constexpr int kMsmGroup = 16;             // partial sums combined per thread in a reduction step
+constexpr int kMsmChunks = 256;  // workgroups per window of the bucket method (each a chunk of the values)
 
 // Generators first .. first + count - 1 of `domain` (32 bytes), affine, 16
 // little-endian uint32 limbs each (x then y); *err set if a counter runs out.
@@ -14,8 +13,7 @@ void launch_commit_generators(const uint8_t *domain, uint64_t first, uint64_t co
                               hipStream_t st);
 
 // Scalars: int16, uint16, int32 or uint64 values (kind 0..3).
-int msm_bits(int kind);   // magnitude bits
-int msm_signs(int kind);  // 2 for signed kinds
+int msm_windows(int kind);  // 8-bit windows of the magnitudes
 size_t msm_workspace_bytes(int kind);
 // sum_i v_i G_i, written as 64 big-endian bytes (x, y; zeros for the identity) to out (device)
 void launch_commit(const void *vals, int kind, uint64_t n, const uint32_t *gens, void *ws, uint8_t *out,

@@ -114,3 +114,30 @@ def test_commit_layer_tables(ra, ctx):
         host = host.view(np.uint16) if name == "Rm" else (host.view(np.uint64) if name == "bits" else host)
         assert P == ec.encode(ec.commit([int(x) for x in host], gens)), name
         assert ra.commit_open(host, limbs, P), name
+
+
+def test_commit_heavy_buckets(ra, ctx):
+    """Values whose digits fall in one or two buckets (every run of every
+    sorted chunk holds the same digit, so a bucket's partials are summed by the
+    segmented tree), against sums of the generators formed on the host."""
+    n = 1 << 16
+    dev_gens = ra.commit_generators(ctx, DOMAIN, n)
+    limbs = dev_gens.cpu().numpy().view(np.uint32).reshape(n, 16).astype(object)
+    w = [1 << (32 * k) for k in range(8)]
+    pts = [(sum(l[k] * w[k] for k in range(8)), sum(l[8 + k] * w[k] for k in range(8))) for l in limbs]
+    even = odd = None
+    for i, p in enumerate(pts):
+        if i & 1:
+            odd = ec.add(odd, p)
+        else:
+            even = ec.add(even, p)
+    total = ec.add(even, odd)
+    ones = torch.ones(n, dtype=torch.int32, device="cuda")
+    assert ec.decode(ra.commit(ctx, ones, dev_gens)) == total
+    assert ec.decode(ra.commit(ctx, ones * 257, dev_gens)) == ec.mul(257, total)
+    assert ec.decode(ra.commit(ctx, -ones, dev_gens)) == ec.neg(total)
+    v = ones.clone()
+    v[1::2] = 3 << 16
+    assert ec.decode(ra.commit(ctx, v, dev_gens)) == ec.add(even, ec.mul(3 << 16, odd))
+    u = torch.full((n,), 1 << 40, dtype=torch.int64, device="cuda")
+    assert ec.decode(ra.commit(ctx, u, dev_gens, ra.RA_U64)) == ec.mul(1 << 40, total)

@@ -42,13 +42,14 @@ __device__ __forceinline__ WitOut witness_entry(int64_t c, int s, int t, int rel
     WitOut o;
     const int64_t cc = c + half;
     const int64_t q = cc >> s;
-    // u = R for R >= 0, -R - 1 for R < 0; R in [-2^(t+1), 2^(t+1)) iff u < 2^(t+1)
-    oor |= ((uint64_t)(q >= 0 ? q : -(q + 1)) >> (t + 1)) != 0;
-    o.rm = (int32_t)(cc - (q << s));
+    // qb = R + 2^(t+1): R lies in [-2^(t+1), 2^(t+1)) iff 0 <= qb < 2^(t+2)
+    const int64_t qb = q + ((int64_t)1 << (t + 1));
+    oor |= ((uint64_t)qb >> (t + 2)) != 0;
+    o.rm = (int32_t)((uint32_t)cc & ((1u << s) - 1u));  // cc - 2^s floor(cc / 2^s), s <= 16
     o.r = (int32_t)q;
     o.y = o.r < 0 ? -o.r : o.r;
     o.z = relu ? (o.r > 0 ? o.r : 0) : o.r;
-    o.w = (uint64_t)o.rm | ((uint64_t)(q + ((int64_t)1 << (t + 1))) << s);
+    o.w = (uint64_t)o.rm | ((uint64_t)qb << s);
     if (relu) o.w |= (uint64_t)o.y << (s + t + 2);
     return o;
 }

@@ -563,6 +563,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__
     static_assert(kTailSmem * 8 <= S * F * 1024, "the tail fits the stage area");
     __shared__ __attribute__((aligned(1024))) int8_t stage[S][F][1024];
     __shared__ int64_t s_cs[4][kTile], s_rs[kTile];
+    __shared__ uint64_t s_e1[kTile];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wr = wv >> 1, wc = wv & 1, half = lane >> 5;
     const uint32_t nbi = np / kTile, nblk = nbi * (kp / kTile);
     if (blockIdx.x >= nblk) {  // workgroup-uniform
@@ -597,6 +598,16 @@ __global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__
         }
     }
     if (tid < kTile && i0 + tid < n) rs = rowsum[i0 + tid];
+    // the eq values of the witness claims (E1 of the tile's rows, E2 of this
+    // lane's column), fetched before the loop so that the epilogue waits on
+    // no load
+    const int cl = 32 * wc + (lane & 31);
+    const uint32_t col = j0 + cl;
+    uint64_t e1own = 0, e2 = 0;
+    if (WIT) {
+        if (tid < kTile && i0 + tid < n) e1own = we.E1[i0 + tid];
+        if (col < k) e2 = we.E2[col];
+    }
     // limbs of each row (int32 A): does any row of the tile need plane 3
     int rl = 2;
     if (LA == 4) rl = tid < kTile && i0 + tid < n ? rowlimb[i0 + tid] : 3;
@@ -617,70 +628,94 @@ __global__ __launch_bounds__(256, 2) void k_gemm_mfma(const int8_t *__restrict__
 #pragma unroll
     for (int e = 0; e < kColRegs; e++) cs[e & 3] += cv[e];
     s_cs[wv][lane] = cs[0] + cs[1] + cs[2] + cs[3];
-    if (tid < kTile) s_rs[tid] = rs;
+    if (tid < kTile) {
+        s_rs[tid] = rs;
+        s_e1[tid] = e1own;
+    }
     __syncthreads();
     // recombination in wrap-around 64-bit arithmetic: exact because C itself fits int64
     constexpr int64_t cA = LA == 2 ? 128 : 128 + 128 * 256 + 128 * 65536;
-    const int cl = 32 * wc + (lane & 31);
-    const uint32_t col = j0 + cl;
     const int64_t colsum = s_cs[0][cl] + s_cs[1][cl] + s_cs[2][cl] + s_cs[3][cl];
     const uint64_t corr = (uint64_t)cA * (uint64_t)colsum - (uint64_t)(128 * cA) * m;
-    // with the witness fused (WIT): each entry also gives R, Rm, Y, Z and the
-    // bit word, and the tile's sums of the four claims at (r1, r2) and its
-    // range flag go to the tile's partial (claims.hpp); exact limb sums over
-    // groups of four entries, as in the standalone witness pass
-    uint64_t cacc[4] = {0, 0, 0, 0};
+    // With the witness fused (WIT) each entry also gives R, Rm, Y, Z and the
+    // bit word, and the tile's claims at (r1, r2) and its range flag go to the
+    // tile's partial (claims.hpp).  A lane's entries share its column, so the
+    // lane sums E1[row] z over its sixteen rows and multiplies by E2[col]
+    // once: E1 is cut into 21-bit limbs, so every limb sum is exact in int64
+    // (|limb z| < 2^52).  Rows past n have E1 = 0 and columns past k E2 = 0,
+    // so only the stores and the range flag need the bounds.  Z~ follows from
+    // R~ and Y~: max(R, 0) = (R + |R|) / 2 under ReLU, Z = R otherwise.
+    int64_t cl3[3][3] = {{0, 0, 0}, {0, 0, 0}, {0, 0, 0}};  // [claim R, Rm, Y][limb]
     int oor = 0;
-    const uint64_t e2 = (WIT && col < k) ? we.E2[col] : 0;
+    // Stores address the tile's first entry plus a 32-bit byte offset when
+    // 64 rows of 8-byte entries span less than 2^32 bytes.
+    const bool off32 = k < (1u << 23);
+    const size_t tb = (size_t)i0 * k + j0;
+    const uint32_t xo0 = (32 * wr + 4 * half) * k + cl;
 #pragma unroll
-    for (int r0 = 0; r0 < 16; r0 += 4) {
-        uint64_t el[4], eh[4];
-        int32_t vr[4], vrm[4], vy[4], vz[4];
+    for (int r = 0; r < 16; r++) {
+        const uint32_t lrow = 32 * wr + 8 * (r / 4) + 4 * half + (r % 4), row = i0 + lrow;
+        const bool ok = row < n && col < k;
+        uint64_t c = corr + 128 * (uint64_t)s_rs[lrow];
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            const int r = r0 + i;
-            const uint32_t lrow = 32 * wr + 8 * (r / 4) + 4 * half + (r % 4), row = i0 + lrow;
-            el[i] = eh[i] = 0;
-            vr[i] = vrm[i] = vy[i] = vz[i] = 0;
-            if (row < n && col < k) {
-                uint64_t c = corr + 128 * (uint64_t)s_rs[lrow];
+        for (int w = 0; w < NACC; w++) {
+            const int wt = LA == 2 ? (w >> 1) + (w & 1) : w;  // weight 256^wt
+            c += (uint64_t)(int64_t)acc[w][r] << (8 * wt);
+        }
+        WitOut o{};
+        if (WIT) {
+            int bad = 0;
+            o = witness_entry((int64_t)c, we.s, we.t, we.relu, we.half, bad);
+            oor |= ok ? bad : 0;
+            const uint64_t e1 = s_e1[lrow];  // canonical, 0 past n
+            const int32_t l0 = (int32_t)(e1 & 0x1FFFFF), l1 = (int32_t)((e1 >> 21) & 0x1FFFFF), l2 = (int32_t)(e1 >> 42);
+            const int32_t z[3] = {o.r, o.rm, o.y};
 #pragma unroll
-                for (int w = 0; w < NACC; w++) {
-                    const int wt = LA == 2 ? (w >> 1) + (w & 1) : w;  // weight 256^wt
-                    c += (uint64_t)(int64_t)acc[w][r] << (8 * wt);
+            for (int q = 0; q < 3; q++) {
+                cl3[q][0] += (int64_t)l0 * z[q];
+                cl3[q][1] += (int64_t)l1 * z[q];
+                cl3[q][2] += (int64_t)l2 * z[q];
+            }
+        }
+        if (ok) {
+            const uint32_t xo = xo0 + (8 * (r / 4) + (r % 4)) * k;  // entry offset within the tile
+            if (off32) {
+                *(int64_t *)((char *)(C + tb) + (xo << 3)) = (int64_t)c;
+                if (WIT) {
+                    *(int32_t *)((char *)(we.R + tb) + (xo << 2)) = o.r;
+                    *(uint16_t *)((char *)(we.Rm + tb) + (xo << 1)) = (uint16_t)o.rm;
+                    *(int32_t *)((char *)(we.Y + tb) + (xo << 2)) = o.y;
+                    *(int32_t *)((char *)(we.Z + tb) + (xo << 2)) = o.z;
+                    *(uint64_t *)((char *)(we.bits + tb) + (xo << 3)) = o.w;
                 }
-                const size_t x = (size_t)row * k + col;
+            } else {
+                const size_t x = tb + xo;
                 C[x] = (int64_t)c;
                 if (WIT) {
-                    const WitOut o = witness_entry((int64_t)c, we.s, we.t, we.relu, we.half, oor);
                     we.R[x] = o.r;
                     we.Rm[x] = (uint16_t)o.rm;
                     we.Y[x] = o.y;
                     we.Z[x] = o.z;
                     we.bits[x] = o.w;
-                    const uint64_t e = m61::lmul(we.E1[row], e2);
-                    el[i] = e & 0x7FFFFFFFull;
-                    eh[i] = e >> 31;
-                    vr[i] = o.r;
-                    vrm[i] = o.rm;
-                    vy[i] = o.y;
-                    vz[i] = o.z;
                 }
             }
         }
-        if (WIT) {
-            cacc[0] = m61::fold(cacc[0] + claim_terms<4>(el, eh, vr));
-            cacc[1] = m61::fold(cacc[1] + claim_terms<4>(el, eh, vrm));
-            cacc[2] = m61::fold(cacc[2] + claim_terms<4>(el, eh, vy));
-            cacc[3] = m61::fold(cacc[3] + claim_terms<4>(el, eh, vz));
-        }
     }
     if (WIT) {  // the stage area is free: every wave has passed the barrier above
-        const int any = __syncthreads_or(oor);
-        m61::block_sum<4>(cacc, (uint64_t *)&stage[0][0][0]);
-        if (tid == 0) {
+        uint64_t cacc[3];
 #pragma unroll
-            for (int q = 0; q < 4; q++) we.claim_part[4 * (size_t)blockIdx.x + q] = cacc[q];
+        for (int q = 0; q < 3; q++) {
+            const uint64_t v = m61::fold(m61::from_i64(cl3[q][0]) + m61::rotl(m61::from_i64(cl3[q][1]), 21) +
+                                         m61::rotl(m61::from_i64(cl3[q][2]), 42));
+            cacc[q] = m61::lmul(v, e2);
+        }
+        const int any = __syncthreads_or(oor);
+        m61::block_sum<3>(cacc, (uint64_t *)&stage[0][0][0]);
+        if (tid == 0) {
+            const uint64_t z = we.relu ? m61::rotl(m61::add(cacc[0], cacc[2]), 60) : cacc[0];  // 2^60 = 1/2
+#pragma unroll
+            for (int q = 0; q < 3; q++) we.claim_part[4 * (size_t)blockIdx.x + q] = cacc[q];
+            we.claim_part[4 * (size_t)blockIdx.x + 3] = z;
             we.flags[blockIdx.x] = (uint32_t)any;
         }
     }

@@ -257,16 +257,21 @@ __global__ __launch_bounds__(256) void k_split(const TA *__restrict__ A, uint32_
 constexpr int kFrontMaxLog = 16;   // largest log n, log k of the fused front (factor tables <= 256 words)
 
 // H (2^(v - v/2) words) and L (2^(v/2) words) for the point z (v <= 16);
-// folded values.  The caller synchronises.
-__device__ __forceinline__ void eq_factors(const uint64_t *__restrict__ z, int v, uint64_t *H, uint64_t *L)
+// folded values.  The point is staged in LDS first (zs, kFrontMaxLog words),
+// so the products wait on one load, not one per coordinate.  The caller
+// synchronises.
+__device__ __forceinline__ void eq_factors(const uint64_t *__restrict__ z, int v, uint64_t *H, uint64_t *L,
+                                           uint64_t *zs)
 {
+    if ((int)threadIdx.x < v) zs[threadIdx.x] = z[threadIdx.x];
+    __syncthreads();
     const int lb = v / 2, hb = v - lb, nh = 1 << hb;
     for (int i = threadIdx.x; i < nh + (1 << lb); i += blockDim.x) {
         const bool high = i < nh;
         const int idx = high ? i : i - nh, nv = high ? hb : lb, j0 = high ? 0 : hb;
         uint64_t acc = 1;
         for (int j = 0; j < nv; j++) {
-            const uint64_t zj = z[j0 + j];
+            const uint64_t zj = zs[j0 + j];
             acc = m61::lmul(acc, ((idx >> (nv - 1 - j)) & 1) ? zj : m61::lsub(1, zj));
         }
         (high ? H : L)[idx] = acc;
@@ -290,7 +295,7 @@ __device__ __forceinline__ void front_rowbind(const T *__restrict__ A, uint32_t 
     constexpr int NL = sizeof(T) == 2 ? 2 : 3, LB = sizeof(T) == 2 ? 31 : 21;
     constexpr uint64_t LMASK = (1ull << LB) - 1;
     uint64_t *H = tab, *Lt = tab + 256;
-    eq_factors(r1, ln, H, Lt);
+    eq_factors(r1, ln, H, Lt, tab + 512);
     __syncthreads();
     const uint32_t ncb = m / 64, cb = blk % ncb, ch = blk / ncb;
     const int tid = threadIdx.x, g = tid % G, slot = tid / G;
@@ -342,22 +347,22 @@ __device__ __forceinline__ void front_rowbind(const T *__restrict__ A, uint32_t 
     }
 }
 
-// Column binding of four rows per wave (16 per workgroup): lanes take 8
+// Column binding of RW rows per wave (4 RW per workgroup): lanes take 8
 // consecutive columns per step (one 16-byte load per row); eq(r2, c) =
 // e_hi 2^31 + e_lo is accumulated exactly per half in int64, one reduction
-// mod p per lane and row.
-constexpr int kFrontColRows = 16;
-
+// mod p per lane and row.  Four rows per wave share each eq value; one row
+// per wave gives small matrices four times the workgroups (more waves in
+// flight for a latency-bound role).
+template <int RW>
 __device__ __forceinline__ void front_colbind(const int16_t *__restrict__ B, uint32_t rows, uint32_t cols,
                                               const uint64_t *r2, int lk, uint32_t blk, uint64_t *out, uint64_t *tab)
 {
-    constexpr int RW = 4;
     uint64_t *H = tab, *Lt = tab + 256;
-    eq_factors(r2, lk, H, Lt);
+    eq_factors(r2, lk, H, Lt, tab + 512);
     __syncthreads();
     const int lb = lk / 2;
     const uint32_t lmask = (1u << lb) - 1;
-    const uint32_t r0 = blk * kFrontColRows + (threadIdx.x >> 6) * RW;  // wave-uniform
+    const uint32_t r0 = blk * 4 * RW + (threadIdx.x >> 6) * RW;  // wave-uniform
     const int lane = threadIdx.x & 63;
     if (r0 >= rows) return;
     int64_t lo[RW], hi[RW];
@@ -396,7 +401,7 @@ __device__ __forceinline__ void front_colbind(const int16_t *__restrict__ B, uin
 __device__ __forceinline__ void front_eq(const uint64_t *z, int v, uint64_t *out, uint32_t blk, uint64_t *tab)
 {
     uint64_t *H = tab, *Lt = tab + 256;
-    eq_factors(z, v, H, Lt);
+    eq_factors(z, v, H, Lt, tab + 512);
     __syncthreads();
     const int lb = v / 2;
     const uint32_t lmask = (1u << lb) - 1, nv = 1u << v;
@@ -425,10 +430,10 @@ struct FrontArgs {
     uint32_t n_rb, n_cb, n_sb, n_sa, n_e1;  // workgroups per role, in launch order (then E2)
 };
 
-template <typename TA, int LA>
+template <typename TA, int LA, int RW>
 __global__ __launch_bounds__(256) void k_front(FrontArgs f)
 {
-    __shared__ uint64_t tab[512];
+    __shared__ uint64_t tab[512 + kFrontMaxLog];  // eq factors H, L and the point
     __shared__ uint64_t red[(256 / (64 / (16 / (int)sizeof(TA)))) * 65];
     uint32_t b = blockIdx.x;
     if (b < f.n_rb) {
@@ -437,7 +442,7 @@ __global__ __launch_bounds__(256) void k_front(FrontArgs f)
     }
     b -= f.n_rb;
     if (b < f.n_cb) {
-        front_colbind(f.B, f.m, f.k, f.r2, f.lk, b, f.b, tab);
+        front_colbind<RW>(f.B, f.m, f.k, f.r2, f.lk, b, f.b, tab);
         return;
     }
     b -= f.n_cb;
@@ -787,17 +792,30 @@ void launch_front(const void *A, int a_is_i32, const int16_t *B, uint32_t n, uin
     f.b = b;
     f.E1 = E1;
     f.E2 = E2;
-    // about eight rows per lane and chunk: 256 rows (int16) or 128 (int32)
+    // Row binding: about eight rows per lane and chunk (256 rows for int16,
+    // 128 for int32), fewer (down to one per lane) while the role has under
+    // 256 workgroups, so that a small matrix still spreads over the CUs.
+    // Column binding: four rows per wave, one while that gives under 256
+    // workgroups.
+    constexpr uint32_t kFrontFill = 256;
+    const uint32_t rs = a_is_i32 ? 16 : 32;  // row slots of a row-binding workgroup
     f.rpc = a_is_i32 ? 128 : 256;
+    while (f.rpc > rs && (m / 64) * ((n + f.rpc - 1) / f.rpc) < kFrontFill) f.rpc >>= 1;
     f.n_rb = (m / 64) * ((n + f.rpc - 1) / f.rpc);
-    f.n_cb = (m + kFrontColRows - 1) / kFrontColRows;
+    const int rw = (m + 15) / 16 >= kFrontFill ? 4 : 1;
+    f.n_cb = (m + 4 * rw - 1) / (4 * rw);
     f.n_sb = (kp / 64) * (mp / 64);
     f.n_sa = (np + 3) / 4;
     f.n_e1 = (n + 1023) / 1024;
     const uint32_t n_e2 = (k + 1023) / 1024;
     const dim3 grid(f.n_rb + f.n_cb + f.n_sb + f.n_sa + f.n_e1 + n_e2);
-    if (a_is_i32) hipLaunchKernelGGL((k_front<int32_t, 4>), grid, dim3(256), 0, st, f);
-    else hipLaunchKernelGGL((k_front<int16_t, 2>), grid, dim3(256), 0, st, f);
+    if (a_is_i32) {
+        if (rw == 4) hipLaunchKernelGGL((k_front<int32_t, 4, 4>), grid, dim3(256), 0, st, f);
+        else hipLaunchKernelGGL((k_front<int32_t, 4, 1>), grid, dim3(256), 0, st, f);
+    } else {
+        if (rw == 4) hipLaunchKernelGGL((k_front<int16_t, 2, 4>), grid, dim3(256), 0, st, f);
+        else hipLaunchKernelGGL((k_front<int16_t, 2, 1>), grid, dim3(256), 0, st, f);
+    }
 }
 
 uint32_t gemm_tiles(uint32_t n, uint32_t k) { return (round_up64(k) / kTile) * (round_up64(n) / kTile); }

@@ -118,12 +118,14 @@ __global__ __launch_bounds__(kGramThreads) void k_plane_gram(
         if (tid < (1 << lP)) {
             if (eqs) {
                 a = eqs[tid];
-            } else {
+            } else {  // the point's coordinates loaded together, then the products
+                uint64_t zs[kMaxPlaneLog];
+#pragma unroll
+                for (int i = 0; i < kMaxPlaneLog; i++) zs[i] = i < lP ? sig[i] : 0;
                 a = 1;
-                for (int i = 0; i < lP; i++) {
-                    const uint64_t z = sig[i];
-                    a = m61::lmul(a, ((tid >> (lP - 1 - i)) & 1) ? z : m61::lsub(1, z));
-                }
+#pragma unroll
+                for (int i = 0; i < kMaxPlaneLog; i++)
+                    if (i < lP) a = m61::lmul(a, ((tid >> (lP - 1 - i)) & 1) ? zs[i] : m61::lsub(1, zs[i]));
             }
         }
         s_eqs[tid] = m61::canon(a);

@@ -323,3 +323,40 @@ def test_product_large_layer(ra, kind):
     L = dict(A=A, B=B, Z=g["Z"].cpu().numpy(), R=g["R"].cpu().numpy(), Rm=g["Rm"].cpu().numpy(),
              Y=g["Y"].cpu().numpy(), bits=g["bits"].cpu().numpy(), transcript=g["transcript"], chained=False)
     assert ra.ra_verify(seed, [L]) == (0, 0)
+
+
+def test_product_wide_rows_fused_witness(ra):
+    """A 2 x 16 x 2^23 layer: 64 rows of 8-byte outputs span 2^32 bytes, so the
+    product's epilogue stores through full 64-bit addresses instead of 32-bit
+    offsets from the tile's first entry.  The fused witness must equal numpy's
+    rescale and the separate witness pass (plan=False), with identical
+    transcripts."""
+    n, m, k, s = 2, 16, 1 << 23, 12
+    rng = np.random.default_rng(23)
+    A = rng.integers(-32768, 32768, size=(n, m)).astype(np.int16)
+    B = rng.integers(-32768, 32768, size=(m, k)).astype(np.int16)
+    B[:, -1] = 32767
+    A[0] = 32767
+    Cw = A.astype(np.int64) @ B.astype(np.int64)             # |C| <= 16 * 2^30
+    half = 1 << (s - 1)
+    R = (Cw + half) >> s
+    u = np.where(R >= 0, R, -R - 1).max()
+    t = max(0, int(u).bit_length() - 1)
+    assert s + 2 * (t + 2) <= 64 and t <= 29
+    Ad, Bd = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    seed = 0x5EED23
+    ctx = ra.Context(seed=seed, deferred=True)
+    g = ra.prove_layer(ctx, Ad, Bd, s, True, 0, t)
+    ctx.sync()
+    assert np.array_equal(g["C"].cpu().numpy(), Cw)
+    Rg = g["R"].cpu().numpy().astype(np.int64)
+    assert np.array_equal(Rg, R)
+    assert np.array_equal(g["Rm"].cpu().numpy().view(np.uint16).astype(np.int64), (Cw + half) & ((1 << s) - 1))
+    assert np.array_equal(g["Y"].cpu().numpy().astype(np.int64), np.abs(R))
+    assert np.array_equal(g["Z"].cpu().numpy().astype(np.int64), np.maximum(R, 0))
+    ctx2 = ra.Context(seed=seed, deferred=True)
+    g2 = ra.prove_layer(ctx2, Ad, Bd, s, True, 0, t, plan=False)
+    ctx2.sync()
+    for key in ("R", "Rm", "Y", "Z", "bits"):
+        assert torch.equal(g[key], g2[key]), key
+    assert g["transcript"] == g2["transcript"]

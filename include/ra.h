@@ -354,6 +354,20 @@ ra_status ra_commit_workspace_size(ra_dtype dtype, size_t *bytes);
  * Waits for its work. */
 ra_status ra_commit(ra_ctx *ctx, const void *d_values, ra_dtype dtype, uint64_t n, const void *d_gens, void *d_ws,
                     size_t ws_bytes, uint8_t *out);
+/* Commitments to several tables in one call, each as ra_commit (Sec. II-C,
+ * the Pedersen vector commitment g^a): table t has d_values[t] (device,
+ * caller-owned), dtypes[t] (RA_I16, RA_U16, RA_I32 or RA_U64) and ns[t]
+ * values, every table committed with the generators d_gens from generator 0
+ * (at least max ns[t] of them).  The tables' bucket passes run one after
+ * another; their bucket sums, bit sums and final doubling chains each run in
+ * one launch for all tables, so the short serial parts of the tables overlap.
+ * out: 64 host bytes per table, table t at out + 64 t, the same bytes
+ * ra_commit gives.  count in 1 .. 64 (RA_E_INVAL for 0, a null pointer or an
+ * unknown dtype; RA_E_NOT_IMPLEMENTED above 64).  Workspace:
+ * ra_commit_batch_workspace_size.  Waits for its work. */
+ra_status ra_commit_batch_workspace_size(const int32_t *dtypes, uint32_t count, size_t *bytes);
+ra_status ra_commit_batch(ra_ctx *ctx, const void *const *d_values, const int32_t *dtypes, const uint64_t *ns,
+                          uint32_t count, const void *d_gens, void *d_ws, size_t ws_bytes, uint8_t *out);
 /* Host opening check: *ok = 1 if commitment (64 bytes) is sum_i v_i G_i for
  * the host values and generators (layouts as above), else 0. */
 ra_status ra_commit_open(const void *h_values, ra_dtype dtype, uint64_t n, const void *h_gens,

@@ -1807,3 +1807,46 @@ extern "C" ra_status ra_commit(ra_ctx *c, const void *d_values, ra_dtype dtype, 
     c->stage_used = 0;
     return RA_OK;
 }
+
+extern "C" ra_status ra_commit_batch_workspace_size(const int32_t *dtypes, uint32_t count, size_t *bytes)
+{
+    if (!dtypes || !bytes || count == 0) return RA_E_INVAL;
+    if (count > (uint32_t)kCommitBatchMax) return RA_E_NOT_IMPLEMENTED;
+    int kinds[kCommitBatchMax];
+    for (uint32_t t = 0; t < count; t++)
+        if ((kinds[t] = commit_kind((ra_dtype)dtypes[t])) < 0) return RA_E_INVAL;
+    size_t offs[kCommitBatchMax];
+    *bytes = msm_batch_offsets(kinds, (int)count, offs) + 64 * (size_t)count + 256;
+    return RA_OK;
+}
+
+extern "C" ra_status ra_commit_batch(ra_ctx *c, const void *const *d_values, const int32_t *dtypes,
+                                     const uint64_t *ns, uint32_t count, const void *d_gens, void *d_ws,
+                                     size_t ws_bytes, uint8_t *out)
+{
+    if (!c || !d_values || !dtypes || !ns || !d_gens || !out || count == 0) return RA_E_INVAL;
+    if (count > (uint32_t)kCommitBatchMax) return RA_E_NOT_IMPLEMENTED;
+    int kinds[kCommitBatchMax];
+    for (uint32_t t = 0; t < count; t++) {
+        if ((kinds[t] = commit_kind((ra_dtype)dtypes[t])) < 0) return RA_E_INVAL;
+        if (ns[t] && !d_values[t]) return RA_E_INVAL;
+    }
+    ra_status st = drain(c);
+    if (st != RA_OK && c->deferred_err == RA_OK) c->deferred_err = st;
+    size_t offs[kCommitBatchMax];
+    const size_t tables = msm_batch_offsets(kinds, (int)count, offs);
+    const size_t need = tables + 64 * (size_t)count + 256;
+    char *ws = nullptr;
+    if ((st = call_ws(c, d_ws, ws_bytes, need, &ws)) != RA_OK) return st;
+    hipStream_t s = c->stream;
+    uint8_t *dout = (uint8_t *)(ws + tables);
+    launch_commit_batch(d_values, kinds, ns, (int)count, (const uint32_t *)d_gens, ws, dout, s);
+    RA_HIP(hipGetLastError());
+    size_t off = 0;
+    if ((st = stage_take(c, 8 * count, &off)) != RA_OK) return st;
+    RA_HIP(hipMemcpyAsync(c->h_stage + off, dout, 64 * (size_t)count, hipMemcpyDeviceToHost, s));
+    RA_HIP(hipStreamSynchronize(s));
+    std::memcpy(out, c->h_stage + off, 64 * (size_t)count);
+    c->stage_used = 0;
+    return RA_OK;
+}

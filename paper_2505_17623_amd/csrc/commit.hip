@@ -279,53 +279,94 @@ __device__ __forceinline__ void group64_tree(uint32_t (*p)[kJacWords])
     __syncthreads();
 }
 
-// S[w][b] = sum over the C chunks of in[w][c][b]: 64 threads per bucket, each
-// a strided share, then a tree.
-__global__ __launch_bounds__(256) void k_pip_bucket_sums(const uint32_t *__restrict__ in, int W, int C,
-                                                         uint32_t *__restrict__ S)
+// The tables of one batch: windows of table t are the global windows
+// wpre[t] .. wpre[t + 1] - 1; its workspace starts off[t] bytes into ws:
+// room for the chunks' bucket sums (W kMsmChunks 256 points, of which the
+// bucket pass fills W C 256, window-major), the bucket sums S (W 256),
+// their bit sums U (W 8).
+struct MsmBatch {
+    int count;
+    uint32_t wpre[kCommitBatchMax + 1];
+    uint32_t C[kCommitBatchMax];
+    uint64_t off[kCommitBatchMax];
+};
+__device__ __forceinline__ int batch_table(const MsmBatch &b, uint32_t gw)
+{
+    int t = 0;
+    while (t + 1 < b.count && gw >= b.wpre[t + 1]) t++;
+    return t;
+}
+__device__ __forceinline__ uint32_t *batch_chunks(char *ws, const MsmBatch &b, int t)
+{
+    return (uint32_t *)(ws + b.off[t]);
+}
+__device__ __forceinline__ uint32_t *batch_S(char *ws, const MsmBatch &b, int t)
+{
+    const uint32_t W = b.wpre[t + 1] - b.wpre[t];
+    return batch_chunks(ws, b, t) + (size_t)W * kMsmChunks * 256 * kJacWords;
+}
+__device__ __forceinline__ uint32_t *batch_U(char *ws, const MsmBatch &b, int t)
+{
+    const uint32_t W = b.wpre[t + 1] - b.wpre[t];
+    return batch_S(ws, b, t) + (size_t)W * 256 * kJacWords;
+}
+
+// S[w][b] = sum over the C chunks of the chunks' bucket b of window w: 64
+// threads per bucket, each a strided share, then a tree.  Four buckets of
+// one window per workgroup; the workgroups run over the batch's windows.
+__global__ __launch_bounds__(256) void k_pip_bucket_sums(char *ws, MsmBatch bt)
 {
     __shared__ uint32_t part[256][kJacWords];
     const int tid = threadIdx.x, g = tid >> 6, j = tid & 63;
-    const int wb = blockIdx.x * 4 + g, w = wb >> 8, b = wb & 255;  // (window, bucket)
+    const uint32_t wb = blockIdx.x * 4 + g, gw = wb >> 8, b = wb & 255;  // (global window, bucket)
+    const int t = batch_table(bt, gw);                                     // workgroup-uniform
+    const uint32_t w = gw - bt.wpre[t];
+    const int C = (int)bt.C[t];
+    const uint32_t *in = batch_chunks(ws, bt, t);
     Jac acc = secp::jac_inf();
-    if (w < W && b >= 1)
+    if (b >= 1)
         for (int c = j; c < C; c += 64) acc = secp::jac_add(acc, load_jac(in + (((size_t)w * C + c) * 256 + b) * kJacWords));
     store_jac(part[tid], acc);
     group64_tree(part);
-    if (j == 0 && w < W) store_jac(S + ((size_t)w * 256 + b) * kJacWords, load_jac(part[tid]));
+    if (j == 0) store_jac(batch_S(ws, bt, t) + ((size_t)w * 256 + b) * kJacWords, load_jac(part[tid]));
 }
 
 // U[w][k] = sum over the b with bit k of S[w][b] (128 buckets): 64 threads
 // per (w, k), two buckets each, then a tree.
-__global__ __launch_bounds__(256) void k_pip_bit_sums(const uint32_t *__restrict__ S, int W, uint32_t *__restrict__ U)
+__global__ __launch_bounds__(256) void k_pip_bit_sums(char *ws, MsmBatch bt)
 {
     __shared__ uint32_t part[256][kJacWords];
     const int tid = threadIdx.x, g = tid >> 6, j = tid & 63;
-    const int wk = blockIdx.x * 4 + g, w = wk >> 3, k = wk & 7;
+    const uint32_t wk = blockIdx.x * 4 + g, gw = wk >> 3, k = wk & 7;
+    const int t = batch_table(bt, gw);  // workgroup-uniform (four bits of one window)
+    const uint32_t w = gw - bt.wpre[t];
+    const uint32_t *S = batch_S(ws, bt, t);
     Jac acc = secp::jac_inf();
-    if (w < W)
-        for (int q = j; q < 128; q += 64) {  // the q-th b with bit k set
-            const int b = ((q >> k) << (k + 1)) | (1 << k) | (q & ((1 << k) - 1));
-            acc = secp::jac_add(acc, load_jac(S + ((size_t)w * 256 + b) * kJacWords));
-        }
+    for (int q = j; q < 128; q += 64) {  // the q-th b with bit k set
+        const int b = ((q >> k) << (k + 1)) | (1 << k) | (q & ((1 << k) - 1));
+        acc = secp::jac_add(acc, load_jac(S + ((size_t)w * 256 + b) * kJacWords));
+    }
     store_jac(part[tid], acc);
     group64_tree(part);
-    if (j == 0 && w < W) store_jac(U + ((size_t)w * 8 + k) * kJacWords, load_jac(part[tid]));
+    if (j == 0) store_jac(batch_U(ws, bt, t) + ((size_t)w * 8 + k) * kJacWords, load_jac(part[tid]));
 }
 
 // P = sum_w 2^(8w) T_w, T_w = sum_k 2^k U[w][k]: the windows' T_w by one
-// thread each, then Horner over the windows; affine bytes to out.
-__global__ __launch_bounds__(64) void k_pip_final(const uint32_t *__restrict__ U, int W, uint8_t *__restrict__ out)
+// thread each, then Horner over the windows; affine bytes to out + 64 t.
+// One workgroup per table.
+__global__ __launch_bounds__(64) void k_pip_final(char *ws, MsmBatch bt, uint8_t *__restrict__ out)
 {
     __shared__ uint32_t T[8][kJacWords];
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, t = blockIdx.x;
+    const int W = (int)(bt.wpre[t + 1] - bt.wpre[t]);
+    const uint32_t *U = batch_U(ws, bt, t);
     if (tid < W) {
-        Jac t = secp::jac_inf();
+        Jac acc = secp::jac_inf();
         for (int k = 7; k >= 0; k--) {
-            t = secp::jac_dbl(t);
-            t = secp::jac_add(t, load_jac(U + ((size_t)tid * 8 + k) * kJacWords));
+            acc = secp::jac_dbl(acc);
+            acc = secp::jac_add(acc, load_jac(U + ((size_t)tid * 8 + k) * kJacWords));
         }
-        store_jac(T[tid], t);
+        store_jac(T[tid], acc);
     }
     __syncthreads();
     if (tid == 0) {
@@ -336,23 +377,48 @@ __global__ __launch_bounds__(64) void k_pip_final(const uint32_t *__restrict__ U
         }
         uint8_t bytes[64];
         secp::jac_encode(p, bytes);
-        for (int i = 0; i < 64; i++) out[i] = bytes[i];
+        for (int i = 0; i < 64; i++) out[64 * (size_t)t + i] = bytes[i];
     }
+}
+
+size_t msm_batch_offsets(const int *kinds, int count, size_t *offs)
+{
+    size_t o = 0;
+    for (int t = 0; t < count; t++) {
+        offs[t] = o;
+        o += (msm_workspace_bytes(kinds[t]) + 255) & ~(size_t)255;
+    }
+    return o;
+}
+
+void launch_commit_batch(const void *const *vals, const int *kinds, const uint64_t *ns, int count,
+                         const uint32_t *gens, void *ws, uint8_t *out, hipStream_t st)
+{
+    MsmBatch bt{};
+    bt.count = count;
+    size_t offs[kCommitBatchMax];
+    msm_batch_offsets(kinds, count, offs);
+    for (int t = 0; t < count; t++) {
+        const int W = msm_windows(kinds[t]);
+        const uint64_t n = ns[t], subs = (n + kPipSub - 1) / kPipSub;
+        const int C = (int)(subs < (uint64_t)kMsmChunks ? (subs ? subs : 1) : kMsmChunks);
+        const uint64_t per = ((n + C - 1) / C + kPipSub - 1) / kPipSub * kPipSub;  // whole sorts per chunk but the last
+        bt.wpre[t + 1] = bt.wpre[t] + (uint32_t)W;
+        bt.C[t] = (uint32_t)C;
+        bt.off[t] = offs[t];
+        hipLaunchKernelGGL(k_pip_buckets, dim3(C, W), dim3(256), 0, st, vals[t], kinds[t], n, gens, per,
+                           (uint32_t *)((char *)ws + offs[t]));
+    }
+    const uint32_t nw = bt.wpre[count];
+    hipLaunchKernelGGL(k_pip_bucket_sums, dim3(nw * 64), dim3(256), 0, st, (char *)ws, bt);
+    hipLaunchKernelGGL(k_pip_bit_sums, dim3(nw * 2), dim3(256), 0, st, (char *)ws, bt);
+    hipLaunchKernelGGL(k_pip_final, dim3(count), dim3(64), 0, st, (char *)ws, bt, out);
 }
 
 void launch_commit(const void *vals, int kind, uint64_t n, const uint32_t *gens, void *ws, uint8_t *out,
                    hipStream_t st)
 {
-    const int W = msm_windows(kind);
-    const uint64_t subs = (n + kPipSub - 1) / kPipSub;
-    const int C = (int)(subs < (uint64_t)kMsmChunks ? (subs ? subs : 1) : kMsmChunks);
-    const uint64_t per = ((n + C - 1) / C + kPipSub - 1) / kPipSub * kPipSub;  // whole sorts per chunk but the last
-    uint32_t *chunk_sums = (uint32_t *)ws;
-    uint32_t *S = chunk_sums + (size_t)W * kMsmChunks * 256 * kJacWords, *U = S + (size_t)W * 256 * kJacWords;
-    hipLaunchKernelGGL(k_pip_buckets, dim3(C, W), dim3(256), 0, st, vals, kind, n, gens, per, chunk_sums);
-    hipLaunchKernelGGL(k_pip_bucket_sums, dim3(W * 64), dim3(256), 0, st, chunk_sums, W, C, S);
-    hipLaunchKernelGGL(k_pip_bit_sums, dim3(W * 2), dim3(256), 0, st, S, W, U);
-    hipLaunchKernelGGL(k_pip_final, dim3(1), dim3(64), 0, st, U, W, out);
+    launch_commit_batch(&vals, &kind, &n, 1, gens, ws, out, st);
 }
 
 }  // namespace ra

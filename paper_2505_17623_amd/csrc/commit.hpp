@@ -19,4 +19,14 @@ size_t msm_workspace_bytes(int kind);
 void launch_commit(const void *vals, int kind, uint64_t n, const uint32_t *gens, void *ws, uint8_t *out,
                    hipStream_t st);
 
+// Several tables at once: table t (values vals[t], kind kinds[t], ns[t]
+// values, generators from gens[0]) uses the workspace at ws + offset t of
+// msm_batch_offsets and writes its 64 bytes to out + 64 t.  The bucket passes
+// run table by table; the bucket sums, bit sums and final chains of all
+// tables each run in one launch.
+constexpr int kCommitBatchMax = 64;
+size_t msm_batch_offsets(const int *kinds, int count, size_t *offs);  // fills offs[count], returns the total
+void launch_commit_batch(const void *const *vals, const int *kinds, const uint64_t *ns, int count,
+                         const uint32_t *gens, void *ws, uint8_t *out, hipStream_t st);
+
 }  // namespace ra

@@ -30,7 +30,8 @@ EXPORTS = ["ra_ctx_create", "ra_ctx_create_stream", "ra_ctx_destroy", "ra_ctx_cu
            "ra_workspace_size_fp2", "ra_verify_fp2", "ra_link_prove", "ra_link_workspace_size",
            "ra_link_gather", "ra_verify_fs",
            "ra_ctx_create_fs", "ra_prove_layer_fs",
-           "ra_commit_generators", "ra_commit_workspace_size", "ra_commit", "ra_commit_open"]
+           "ra_commit_generators", "ra_commit_workspace_size", "ra_commit", "ra_commit_open",
+           "ra_commit_batch_workspace_size", "ra_commit_batch"]
 
 
 class RAError(RuntimeError):
@@ -150,6 +151,8 @@ def lib():
         L.ra_commit_workspace_size.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
         L.ra_commit.argtypes = [vp, vp, ctypes.c_int, u64, vp, vp, ctypes.c_size_t, ctypes.c_char_p]
         L.ra_commit_open.argtypes = [vp, ctypes.c_int, u64, vp, ctypes.c_char_p, ctypes.POINTER(ctypes.c_int32)]
+        L.ra_commit_batch_workspace_size.argtypes = [vp, ctypes.c_uint32, ctypes.POINTER(ctypes.c_size_t)]
+        L.ra_commit_batch.argtypes = [vp, vp, vp, vp, ctypes.c_uint32, vp, vp, ctypes.c_size_t, ctypes.c_char_p]
         L.ra_prove_layer_fs.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                         vp, vp, vp, vp, vp, vp, u64, ctypes.c_char_p, vp, ctypes.c_size_t,
                                         ctypes.POINTER(LayerProofFp2), ctypes.c_char_p]
@@ -163,7 +166,7 @@ def lib():
                   L.ra_prove_layer_fp2, L.ra_workspace_size_fp2, L.ra_verify_fp2, L.ra_link_prove,
                   L.ra_link_workspace_size, L.ra_link_gather, L.ra_verify_fs, L.ra_ctx_create_fs,
                   L.ra_prove_layer_fs, L.ra_commit_generators, L.ra_commit_workspace_size, L.ra_commit,
-                  L.ra_commit_open,
+                  L.ra_commit_open, L.ra_commit_batch_workspace_size, L.ra_commit_batch,
                   L.ra_ctx_destroy, L.ra_ctx_cursor, L.ra_ctx_set_profiling, L.ra_ctx_profile,
                   L.ra_ctx_set_deferred, L.ra_ctx_sync,
                   L.ra_mle_bind, L.ra_sumcheck_matmul_prove,
@@ -763,6 +766,25 @@ def commit(ctx: Context, values: torch.Tensor, gens: torch.Tensor, dtype: int | 
     out = ctypes.create_string_buffer(64)
     _check(lib().ra_commit(ctx.h, _dptr(values), d, values.numel(), _dptr(gens), *_ws(ws), out), "ra_commit")
     return out.raw
+
+
+def commit_batch(ctx: Context, tables, gens: torch.Tensor, ws: torch.Tensor | None = None) -> list:
+    """Commitments to several tables in one call (ra_commit_batch): tables is
+    a list of device tensors or (tensor, dtype) pairs as for commit; returns
+    one 64-byte commitment per table."""
+    vals, dts, ns = [], [], []
+    for tb in tables:
+        v, d = tb if isinstance(tb, tuple) else (tb, None)
+        vals.append(_dptr(v))
+        dts.append(d if d is not None else _CDT[v.dtype])
+        ns.append(v.numel())
+    cnt = len(vals)
+    pv = (ctypes.c_void_p * cnt)(*vals)
+    pd = (ctypes.c_int32 * cnt)(*dts)
+    pn = (ctypes.c_uint64 * cnt)(*ns)
+    out = ctypes.create_string_buffer(64 * cnt)
+    _check(lib().ra_commit_batch(ctx.h, pv, pd, pn, cnt, _dptr(gens), *_ws(ws), out), "ra_commit_batch")
+    return [out.raw[64 * t:64 * (t + 1)] for t in range(cnt)]
 
 
 def commit_open(values: np.ndarray, gens_limbs: np.ndarray, commitment: bytes) -> bool:

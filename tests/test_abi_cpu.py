@@ -40,6 +40,29 @@ def test_exports_every_declared_symbol(ra):
         assert hasattr(L, s), s
 
 
+def test_commit_batch_workspace_size(ra):
+    """ra_commit_batch_workspace_size: one table's region per table (each as
+    ra_commit's, rounded to 256 bytes) plus 64 output bytes per table; no
+    tables or an unknown type is RA_E_INVAL, more than 64 tables
+    RA_E_NOT_IMPLEMENTED."""
+    L = ra.lib()
+    types = [ra.RA_I16, ra.RA_U16, ra.RA_I32, ra.RA_U64]
+    single = []
+    for t in types:
+        sz = ctypes.c_size_t()
+        assert L.ra_commit_workspace_size(t, ctypes.byref(sz)) == 0
+        single.append(sz.value - 256)  # ra_commit's region: the tables' sums, then 256 bytes of output
+    dts = (ctypes.c_int32 * 4)(*types)
+    sz = ctypes.c_size_t()
+    assert L.ra_commit_batch_workspace_size(dts, 4, ctypes.byref(sz)) == 0
+    assert sz.value == sum((b + 255) // 256 * 256 for b in single) + 64 * 4 + 256
+    assert L.ra_commit_batch_workspace_size(dts, 0, ctypes.byref(sz)) == -1
+    many = (ctypes.c_int32 * 65)(*([ra.RA_I32] * 65))
+    assert L.ra_commit_batch_workspace_size(many, 65, ctypes.byref(sz)) == -9
+    bad = (ctypes.c_int32 * 2)(ra.RA_I32, ra.RA_I64)
+    assert L.ra_commit_batch_workspace_size(bad, 2, ctypes.byref(sz)) == -1
+
+
 def test_host_side_argument_errors(ra):
     L = ra.lib()
     h = ctypes.c_void_p()

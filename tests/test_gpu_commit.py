@@ -141,3 +141,37 @@ def test_commit_heavy_buckets(ra, ctx):
     assert ec.decode(ra.commit(ctx, v, dev_gens)) == ec.add(even, ec.mul(3 << 16, odd))
     u = torch.full((n,), 1 << 40, dtype=torch.int64, device="cuda")
     assert ec.decode(ra.commit(ctx, u, dev_gens, ra.RA_U64)) == ec.mul(1 << 40, total)
+
+
+def test_commit_batch_matches_single_calls(ra, ctx, gens_small):
+    """ra_commit_batch over tables of every value type and size (one value to
+    3001, an all-zero table, an empty one) in one call: each table's point
+    equals its own ra_commit and the oracle's sum.  Then the argument checks:
+    no tables, more than 64, an unknown type."""
+    dev_gens, gens = gens_small
+    rng = np.random.default_rng(77)
+    tables, want = [], []
+    for i, (n, (dt, code)) in enumerate([(3001, DTYPES[2]), (1, DTYPES[0]), (256, DTYPES[3]), (7, DTYPES[1]),
+                                         (3001, DTYPES[3]), (100, DTYPES[2]), (0, DTYPES[2]), (4096, DTYPES[0])]):
+        info = np.iinfo(dt)
+        v = rng.integers(info.min, info.max, size=n, dtype=dt, endpoint=True)
+        if i == 5:
+            v[:] = 0
+        elif n >= 3:
+            v[:3] = [info.min, info.max, 0]
+        t = torch.from_numpy(v.view(np.int16 if dt == np.uint16 else (np.int64 if dt == np.uint64 else dt))).cuda()
+        tables.append((t, getattr(ra, code) if code else None))
+        want.append(ec.encode(ec.commit([int(x) for x in v], gens[:n])))
+    got = ra.commit_batch(ctx, tables, dev_gens)
+    assert got == want
+    assert got == [ra.commit(ctx, t, dev_gens, d) for t, d in tables]
+    import ctypes
+    L = ra.lib()
+    one = (ctypes.c_void_p * 65)(*([tables[0][0].data_ptr()] * 65))
+    dts = (ctypes.c_int32 * 65)(*([ra.RA_I32] * 65))
+    ns = (ctypes.c_uint64 * 65)(*([8] * 65))
+    out = ctypes.create_string_buffer(64 * 65)
+    assert L.ra_commit_batch(ctx.h, one, dts, ns, 0, dev_gens.data_ptr(), None, 0, out) == -1  # RA_E_INVAL
+    assert L.ra_commit_batch(ctx.h, one, dts, ns, 65, dev_gens.data_ptr(), None, 0, out) == -9  # RA_E_NOT_IMPLEMENTED
+    dts[1] = ra.RA_I64
+    assert L.ra_commit_batch(ctx.h, one, dts, ns, 2, dev_gens.data_ptr(), None, 0, out) == -1  # RA_E_INVAL

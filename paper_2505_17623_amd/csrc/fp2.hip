@@ -463,8 +463,16 @@ __global__ __launch_bounds__(256) void k_f2_planes(F2PlaneArgs a)
         if (on) {
             const int pr = (r << sh) | qp;
             const uint64_t *gr = g_re + pr * GS + qp, *gi = g_im + pr * GS + qp;
-            f2 row = f2of(0);
-            for (int c = 0; c < nrows; c++) row = f2add(row, f2mul(coef(c), f2{gr[c << sh], gi[c << sh]}));
+            // four independent partial sums, so the products of four rows are
+            // in flight together (the sum is exact in any order)
+            f2 r4[4] = {f2of(0), f2of(0), f2of(0), f2of(0)};
+            int c = 0;
+            for (; c + 3 < nrows; c += 4)
+#pragma unroll
+                for (int u = 0; u < 4; u++)
+                    r4[u] = f2add(r4[u], f2mul(coef(c + u), f2{gr[(c + u) << sh], gi[(c + u) << sh]}));
+            for (; c < nrows; c++) r4[0] = f2add(r4[0], f2mul(coef(c), f2{gr[c << sh], gi[c << sh]}));
+            const f2 row = f2add(f2add(r4[0], r4[1]), f2add(r4[2], r4[3]));
             const f2 cr = coef(r);
             Q = f2mul(cr, row);
             L = f2mul(cr, f2{g_re[pr * GS + pr], g_im[pr * GS + pr]});

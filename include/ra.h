@@ -278,7 +278,10 @@ typedef struct {
  * with tau = (tau_p, r1, r2) and W(q) = lambda_group(q) 2^(bit of q), i.e.
  * booleanity of every bit and recomposition of every range-checked value;
  * then with ReLU the zero-check sum_x eq((r1, r2), x) (R(x)^2 - Y(x)^2) = 0
- * of Eq. (6).  Inputs are the buffers the witness call filled and its info.
+ * of Eq. (6).  Inputs are the buffers the witness call filled and its info;
+ * as that call leaves them, the bit words are zero above the planes it writes
+ * (s + t + 2, with ReLU s + 2t + 4), and the plane rounds rely on it (a
+ * table with bits set there gives a transcript that does not verify).
  * Limit of this GPU path: N = n k <= 2^31 (the plane rounds' exact int32
  * sums), else RA_E_NOT_IMPLEMENTED. */
 ra_status ra_range_prove(ra_ctx *ctx, const uint64_t *d_bits, const int32_t *d_R, const int32_t *d_Y, uint32_t n,

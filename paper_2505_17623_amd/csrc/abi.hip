@@ -976,7 +976,10 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
 
     const RangeLayout rl = range_layout(N, lP, relu);
     const int L = rl.L, nhs = rl.nhs, reg = rl.reg, Bp = rl.Bp;
-    const int gtiles = rl.gtiles, gblocks = rl.gblocks;
+    // planes the witness writes (the bit words are zero above them): the Gram
+    // pass skips a block of sixteen planes that holds none
+    const int pused = c->s + (c->t + 2) * (relu ? 2 : 1);
+    const int gtiles = plane_gram_tiles(lP, pused), gblocks = rl.gblocks;  // workspace sized for rl.gtiles >= gtiles
     // transcript: [evals 4R][(unused)][bits_claim][range_sum][relu evals 4 lN][(unused)][r_at][y_at]
     const size_t F_R = 4 * (size_t)R, RS = F_R + 2, Z0 = F_R + 3, FZ = Z0 + 4 * (size_t)lN, trw = FZ + 3;
     char *ws = nullptr;
@@ -1006,11 +1009,12 @@ ra_status ra_range_prove(ra_ctx *c, const uint64_t *d_bits, const int32_t *d_R, 
     const RangeRiders riders{gpart, gblocks, gtiles, gram_reduce_groups(gtiles), gsum, rc};
     {   // plane rounds: Gram matrix on the matrix cores, Bx per output
         Timed tm(c, G_RANGE_PLANE);
-        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, sigma, Bx, gpart, riding ? &xs : nullptr, s);
+        launch_plane_gram(lP, d_bits, N, lk, c->d_eq, c->d_eq + n, sigma, Bx, gpart, riding ? &xs : nullptr, s,
+                          nullptr, pused);
     }
     if (!riding) {  // the Gram matrix; further workgroups: the constant block and the x set-up
         Timed tm(c, G_RANGE_SETUP);
-        launch_gram_reduce(lP, N, gpart, gsum, rc, xs, s);
+        launch_gram_reduce(lP, N, gpart, gsum, rc, xs, s, pused);
     }
     // Each x launch's extra workgroups assemble the rounds of the launch
     // before it; the first one also evaluates the plane rounds (the second

@@ -429,10 +429,13 @@ void launch_link_gather(const int32_t *Z, uint64_t nz, const int32_t *src, uint6
 
 // ---- launchers (planes.hip) ----
 // The Gram pass works on 16 x 16 tiles of G on and above the diagonal: 3 for
-// up to 32 planes, 10 for 64; each block of the pass writes kGramTileWords
-// words per tile, and the reduction takes 16 entries per workgroup.
+// up to 32 planes, 6 when P = 64 but only the first 48 planes can hold set
+// bits (pused, the planes the witness writes: s + t + 2, with ReLU
+// s + 2t + 4; the bit words are zero above them), 10 for 64; each block of
+// the pass writes kGramTileWords words per tile, and the reduction takes 16
+// entries per workgroup.
 constexpr int kGramTileWords = 256;
-int plane_gram_tiles(int lP);                 // tiles of the Gram matrix (3 or 10)
+int plane_gram_tiles(int lP, int pused = 64);  // tiles of the Gram matrix (3, 6 or 10)
 int plane_gram_blocks(uint64_t N, int lP);    // blocks of the Gram pass (each writes tiles * kGramTileWords words)
 inline int gram_reduce_groups(int tiles) { return tiles * kGramTileWords / 16; }
 // threads of the Gram pass that can run the set-up of the rounds over x
@@ -444,10 +447,10 @@ int plane_gram_set_up_threads(uint64_t N, int lP);
 // eqs (optional): the P values eq(sigma_p, q) given instead of computed from sig.
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
                        const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st,
-                       const uint64_t *eqs = nullptr);
+                       const uint64_t *eqs = nullptr, int pused = 64);
 // the Gram matrix G (gsum: 64 x 64 words, both triangles) from the partial
 // tiles; further workgroups run the set-up of the range check (rc, xs)
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,
-                        const XSetupArgs &xs, hipStream_t st);
+                        const XSetupArgs &xs, hipStream_t st, int pused = 64);
 
 }  // namespace ra

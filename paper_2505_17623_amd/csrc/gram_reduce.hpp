@@ -27,7 +27,9 @@ __device__ __forceinline__ void tile_blocks(int t, int nb, int &I, int &J)
 
 // Workgroup blk (256 threads) of the reduction: 16 entries of G, sixteen
 // lanes per entry (lane group g sums the partial tiles of blocks g, g + 16,
-// ...), then LDS; G[q][q'] is written in both triangles.
+// ...), then LDS; G[q][q'] is written in both triangles.  With 6 tiles (48
+// of 64 planes) the workgroups also clear the rest of the 64 x 64 matrix
+// (96 workgroups, 240 spare threads each, for 1792 entries).
 constexpr int kGramReduceLdsWords = 16 * 17;
 __device__ __forceinline__ void gram_reduce_block(const uint64_t *__restrict__ gpart, int nblk, int tiles,
                                                   uint64_t *__restrict__ G, int blk, uint64_t *lds)
@@ -44,6 +46,14 @@ __device__ __forceinline__ void gram_reduce_block(const uint64_t *__restrict__ g
     }
     for (; b < nblk; b += 16) a = m61::fold(a + gpart[(size_t)b * entries + e]);
     red[g][el] = a;
+    if (tiles == 6 && tid >= 16) {  // 48 planes: G's rows and columns of planes 48 .. 63 are zero
+        const int z = blk * 240 + (tid - 16);  // 16 x 64 entries of the rows, then 48 x 16 of the columns
+        if (z < 16 * 64 + 48 * 16) {
+            const int q = z < 1024 ? 48 + (z >> 6) : (z - 1024) >> 4;
+            const int q2 = z < 1024 ? (z & 63) : 48 + ((z - 1024) & 15);
+            G[q * 64 + q2] = 0;
+        }
+    }
     __syncthreads();
     if (tid >= 16) return;
     uint64_t v = 0;
@@ -52,7 +62,7 @@ __device__ __forceinline__ void gram_reduce_block(const uint64_t *__restrict__ g
     v = m61::canon(v);
     const int t = e / kGramTileWords, r = (e % kGramTileWords) >> 6, l = e & 63;
     int I, J;
-    tile_blocks(t, tiles == 3 ? 2 : 4, I, J);  // 3 tiles: 32 planes; 10: 64
+    tile_blocks(t, tiles == 3 ? 2 : (tiles == 6 ? 3 : 4), I, J);  // 3 tiles: 32 planes; 6: 48; 10: 64
     const int q = 16 * I + frag_row(l, r), q2 = 16 * J + (l & 15);
     G[q * 64 + q2] = v;
     G[q2 * 64 + q] = v;  // symmetric (the same value when the tile is diagonal)

@@ -295,7 +295,11 @@ __global__ __launch_bounds__(256) void k_gram_reduce(const uint64_t *__restrict_
     gram_reduce_block(gpart, nblk, tiles, G, blockIdx.x, red);
 }
 
-int plane_gram_tiles(int lP) { return GramShape<32>::kTiles * (lP <= 5) + GramShape<64>::kTiles * (lP > 5); }
+int plane_gram_tiles(int lP, int pused)
+{
+    if (lP <= 5) return GramShape<32>::kTiles;
+    return pused <= 48 ? GramShape<48>::kTiles : GramShape<64>::kTiles;
+}
 
 int plane_gram_set_up_threads(uint64_t N, int lP) { return plane_gram_blocks(N, lP) * 64 * kConsumers; }
 
@@ -308,7 +312,7 @@ int plane_gram_blocks(uint64_t N, int lP)
 
 void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const uint64_t *E1, const uint64_t *E2,
                        const uint64_t *sig, uint64_t *Bx, uint64_t *gpart, const XSetupArgs *xs, hipStream_t st,
-                       const uint64_t *eqs)
+                       const uint64_t *eqs, int pused)
 {
     const int nb = plane_gram_blocks(N, lP);
     const XSetupArgs none{};
@@ -316,15 +320,18 @@ void launch_plane_gram(int lP, const uint64_t *bits, uint64_t N, int lk, const u
     if (lP <= 5)
         hipLaunchKernelGGL(k_plane_gram<32>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
                            gpart, xs ? 1 : 0, x, eqs);
+    else if (plane_gram_tiles(lP, pused) == GramShape<48>::kTiles)  // planes 48 .. 63 are zero
+        hipLaunchKernelGGL(k_plane_gram<48>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
+                           gpart, xs ? 1 : 0, x, eqs);
     else
         hipLaunchKernelGGL(k_plane_gram<64>, dim3(nb), dim3(kGramThreads), 0, st, bits, N, lk, E1, E2, sig, lP, Bx,
                            gpart, xs ? 1 : 0, x, eqs);
 }
 
 void launch_gram_reduce(int lP, uint64_t N, const uint64_t *gpart, uint64_t *gsum, const RangeConsts &rc,
-                        const XSetupArgs &xs, hipStream_t st)
+                        const XSetupArgs &xs, hipStream_t st, int pused)
 {
-    const int tiles = plane_gram_tiles(lP), nb = plane_gram_blocks(N, lP), nred = gram_reduce_groups(tiles);
+    const int tiles = plane_gram_tiles(lP, pused), nb = plane_gram_blocks(N, lP), nred = gram_reduce_groups(tiles);
     const int xb = (x_setup_count(xs) + 255) / 256;
     const int ncj = rc.cj.nblk > 0 ? 1 : 0;
     hipLaunchKernelGGL(k_gram_reduce, dim3(nred + 1 + ncj + xb), dim3(256), 0, st, gpart, nb, tiles, gsum, nred, rc,

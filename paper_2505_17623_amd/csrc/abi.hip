@@ -1218,11 +1218,12 @@ ra_status ra_prove_layer_fp2(ra_ctx *c, const void *d_A, ra_dtype a_dtype, const
     // the plane-bound table Bx with the two parts of eq(sigma_p, .)
     launch_f2_eq(sig, lP, SIG, s);
     launch_f2_eq(sig, 0, ONE, s);
-    const int gt = plane_gram_tiles(lP), gb = plane_gram_blocks(N, lP);
+    const int pused = (int)io->s + (t + 2) * (relu ? 2 : 1);  // planes the witness writes
+    const int gt = plane_gram_tiles(lP, pused), gb = plane_gram_blocks(N, lP);
     uint64_t *gp0 = (uint64_t *)(ws + L.o_gp0), *gp1 = (uint64_t *)(ws + L.o_gp1);
-    launch_plane_gram(lP, d_bits, N, 0, EQ.re, ONE.re, sig, Bx.re, gp0, nullptr, s, SIG.re);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.re, ONE.re, sig, Bx.re, gp0, nullptr, s, SIG.re, pused);
     launch_f2_gram_sum(gp0, gb, gt, Gre, s);
-    launch_plane_gram(lP, d_bits, N, 0, EQ.im, ONE.re, sig, Bx.im, gp1, nullptr, s, SIG.im);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.im, ONE.re, sig, Bx.im, gp1, nullptr, s, SIG.im, pused);
     launch_f2_gram_sum(gp1, gb, gt, Gim, s);
     {
         F2PlaneArgs pa{};
@@ -1506,11 +1507,12 @@ extern "C" ra_status ra_prove_layer_fs(ra_ctx *c, const void *d_A, ra_dtype a_dt
     // draw sigma_p as they go, then Bx with eq(sigma_p, .)
     launch_fill0(SIG.re, 64, s);
     launch_f2_eq(lam, 0, ONE, s);
-    const int gt = plane_gram_tiles(lP), gb = plane_gram_blocks(N, lP);
+    const int pused = (int)io->s + (t + 2) * (relu ? 2 : 1);  // planes the witness writes
+    const int gt = plane_gram_tiles(lP, pused), gb = plane_gram_blocks(N, lP);
     uint64_t *gp0 = (uint64_t *)(ws + L.o_gp0), *gp1 = (uint64_t *)(ws + L.o_gp1);
-    launch_plane_gram(lP, d_bits, N, 0, EQ.re, ONE.re, SIG.re, Bx.re, gp0, nullptr, s, SIG.re);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.re, ONE.re, SIG.re, Bx.re, gp0, nullptr, s, SIG.re, pused);
     launch_f2_gram_sum(gp0, gb, gt, Gre, s);
-    launch_plane_gram(lP, d_bits, N, 0, EQ.im, ONE.re, SIG.re, Bx.im, gp1, nullptr, s, SIG.re);
+    launch_plane_gram(lP, d_bits, N, 0, EQ.im, ONE.re, SIG.re, Bx.im, gp1, nullptr, s, SIG.re, pused);
     launch_f2_gram_sum(gp1, gb, gt, Gim, s);
     {
         F2PlaneArgs pa{};

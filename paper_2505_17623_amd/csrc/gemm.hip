@@ -427,7 +427,7 @@ struct FrontArgs {
     uint64_t *b;         // column binding (m words)
     uint64_t *E1, *E2;   // eq tables for the later calls
     uint32_t rpc;        // rows per row-binding chunk
-    uint32_t n_rb, n_cb, n_sb, n_sa, n_e1;  // workgroups per role, in launch order (then E2)
+    uint32_t n_rb, n_cb, n_sb, n_sa, n_e1;  // workgroups per role (the E2 table's follow E1's)
 };
 
 template <typename TA, int LA, int RW>
@@ -436,27 +436,55 @@ __global__ __launch_bounds__(256) void k_front(FrontArgs f)
     __shared__ uint64_t tab[512 + kFrontMaxLog];  // eq factors H, L and the point
     __shared__ uint64_t red[(256 / (64 / (16 / (int)sizeof(TA)))) * 65];
     uint32_t b = blockIdx.x;
-    if (b < f.n_rb) {
-        front_rowbind<TA>((const TA *)f.A, f.n, f.m, f.r1, f.ln, f.rpc, b, f.acc, tab, red);
-        return;
+    // The four heavy roles, then the eq tables.  Workgroups start in index
+    // order, so the roles whose workgroups run longest go first and the short
+    // tiles of the split of B fill in behind them: with four rows per
+    // column-binding wave (large m, RW = 4) that role has the longest loop,
+    // then the split of A (a whole row per wave); with one row per wave the
+    // row binding leads and the split of A trails.
+    if constexpr (RW == 4) {
+        if (b < f.n_cb) {
+            front_colbind<RW>(f.B, f.m, f.k, f.r2, f.lk, b, f.b, tab);
+            return;
+        }
+        b -= f.n_cb;
+        if (b < f.n_sa) {
+            split_a_block<TA, LA>((const TA *)f.A, f.n, f.m, f.np, f.mp, f.Al, f.rowsum, f.rowlimb, b);
+            return;
+        }
+        b -= f.n_sa;
+        if (b < f.n_rb) {
+            front_rowbind<TA>((const TA *)f.A, f.n, f.m, f.r1, f.ln, f.rpc, b, f.acc, tab, red);
+            return;
+        }
+        b -= f.n_rb;
+        if (b < f.n_sb) {
+            split_bt_block(f.B, f.m, f.k, f.mp, f.kp, f.Bt, f.colpart, b % (f.kp / 64), b / (f.kp / 64));
+            return;
+        }
+        b -= f.n_sb;
+    } else {
+        if (b < f.n_rb) {
+            front_rowbind<TA>((const TA *)f.A, f.n, f.m, f.r1, f.ln, f.rpc, b, f.acc, tab, red);
+            return;
+        }
+        b -= f.n_rb;
+        if (b < f.n_cb) {
+            front_colbind<RW>(f.B, f.m, f.k, f.r2, f.lk, b, f.b, tab);
+            return;
+        }
+        b -= f.n_cb;
+        if (b < f.n_sb) {
+            split_bt_block(f.B, f.m, f.k, f.mp, f.kp, f.Bt, f.colpart, b % (f.kp / 64), b / (f.kp / 64));
+            return;
+        }
+        b -= f.n_sb;
+        if (b < f.n_sa) {
+            split_a_block<TA, LA>((const TA *)f.A, f.n, f.m, f.np, f.mp, f.Al, f.rowsum, f.rowlimb, b);
+            return;
+        }
+        b -= f.n_sa;
     }
-    b -= f.n_rb;
-    if (b < f.n_cb) {
-        front_colbind<RW>(f.B, f.m, f.k, f.r2, f.lk, b, f.b, tab);
-        return;
-    }
-    b -= f.n_cb;
-    if (b < f.n_sb) {
-        const uint32_t tx = f.kp / 64;
-        split_bt_block(f.B, f.m, f.k, f.mp, f.kp, f.Bt, f.colpart, b % tx, b / tx);
-        return;
-    }
-    b -= f.n_sb;
-    if (b < f.n_sa) {
-        split_a_block<TA, LA>((const TA *)f.A, f.n, f.m, f.np, f.mp, f.Al, f.rowsum, f.rowlimb, b);
-        return;
-    }
-    b -= f.n_sa;
     if (b < f.n_e1) front_eq(f.r1, f.ln, f.E1, b, tab);
     else front_eq(f.r2, f.lk, f.E2, b - f.n_e1, tab);
 }

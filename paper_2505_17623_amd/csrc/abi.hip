@@ -1410,7 +1410,6 @@ extern "C" ra_status ra_prove_layer_fs(ra_ctx *c, const void *d_A, ra_dtype a_dt
     uint64_t *fsch = (uint64_t *)(ws + L.o_fsch);
     uint32_t *err = (uint32_t *)(ws + L.o_err);
     uint8_t *root = (uint8_t *)(ws + L.o_root);
-    const size_t pstride = (size_t)kF2MaxBlocks * 8;
 
     // the witness: the exact product, t and P, then R, Rm, Y, Z and the bit
     // table (the F_p claims that pass also forms are not used: its eq tables

@@ -86,7 +86,6 @@ void launch_commit_generators(const uint8_t *domain, uint64_t first, uint64_t co
 // The bucket method
 // ---------------------------------------------------------------------------
 constexpr int kPipSub = 4096;              // values a workgroup sorts at a time (two workgroups fit a CU)
-constexpr int kPipRun = kPipSub / 256;     // sorted positions per thread
 constexpr int kPipParts = 256 + 255;       // run partials of one sort, at most
 constexpr int kJacWords = 24;              // X, Y, Z: eight 32-bit limbs each
 

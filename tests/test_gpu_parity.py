@@ -102,6 +102,8 @@ SHAPES = [
     (64, 2048, 16, 10, False, 1, 3000), # fused front feeding a global round (m beyond the LDS tail)
     (4, 4096, 8, 8, True, 0, 3000),     # two global rounds reading the fused front's accumulators
     (2, 8192, 8, 9, False, 1, 3000),    # three global rounds
+    (16, 4096, 1024, 10, True, 0, 3000),  # fused front with four rows per column-binding wave (its longest-first
+                                          # role order) and two column steps per row
 ]
 
 
